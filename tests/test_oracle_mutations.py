@@ -1,0 +1,59 @@
+"""The oracle's pins must catch plausible mistakes.  Each case plants one error
+into a temporary copy of the oracle (on the CPU only) and runs the pin suite
+against that copy; the suite has to fail."""
+import os
+import shutil
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+# (name, original text, planted mistake)
+MUTATIONS = [
+    ("lut_sign", "e = q[m * dsub + j] - C[m, :, j]", "e = q[m * dsub + j] + C[m, :, j]"),
+    ("lut_drops_weight", "acc = acc + w[m * dsub + j] * (e * e)", "acc = acc + (e * e)"),
+    ("lut_wrong_subdim", "w[m * dsub + j] * (e * e)", "w[m * dsub] * (e * e)"),
+    ("delta_wrong_index", "delta = delta + alpha[m, t] * W[m, t]", "delta = delta + alpha[t % M, m % r] * W[m, t]"),
+    ("delta_dropped", "C[m] = C_pq[m] + delta", "C[m] = C_pq[m]"),
+    ("adc_transposed", "d = d + lut[m][codes[ids, m]].astype(dtype)", "d = d + lut[m][codes[m % codes.shape[0], ids % codes.shape[1]]].astype(dtype)"),
+    ("topk_tie_larger_id", "order = np.lexsort((ids, d))[:k]", "order = np.lexsort((-ids, d))[:k]"),
+    ("filter_closed_hi", "mask &= (a >= lo) & (a < hi)", "mask &= (a >= lo) & (a <= hi)"),
+    ("bitmap_msb_first", "(idx & 31).astype(np.uint32)", "(31 - (idx & 31)).astype(np.uint32)"),
+    ("softplus_plain_exp", "y[~big] = np.log1p(np.exp(x[~big]))", "y[~big] = np.exp(x[~big])"),
+    ("fnv_wrong_order", "h ^= byte\n        h = (h * _FNV_PRIME) & _MASK64", "h = (h * _FNV_PRIME) & _MASK64\n        h ^= byte"),
+    ("alpha_single_row", "for r_i in rows:", "for r_i in rows[:1]:"),
+    ("fingerprint_no_clauses", "out.append(struct.pack(\"<iqq\", int(col), int(lo), int(hi)))", "pass"),
+]
+
+
+def _run_pins_on_copy(tmp_path, old, new):
+    src = os.path.join(ROOT, "oracle", "ifvs_oracle.py")
+    text = open(src).read()
+    assert old in text, f"mutation text {old!r} no longer applies; update it"
+    dst = tmp_path / "oracle"
+    shutil.copytree(os.path.join(ROOT, "oracle"), dst,
+                    ignore=shutil.ignore_patterns("__pycache__"))
+    (dst / "ifvs_oracle.py").write_text(text.replace(old, new, 1))
+    tests = tmp_path / "tests"
+    tests.mkdir()
+    shutil.copy(os.path.join(ROOT, "tests", "test_oracle_pins.py"), tests)
+    shutil.copytree(os.path.join(ROOT, "tests", "golden"), tests / "golden")
+    env = dict(os.environ, PYTHONPATH=str(tmp_path), PYTHONDONTWRITEBYTECODE="1")
+    proc = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
+                           str(tests / "test_oracle_pins.py")],
+                          cwd=tmp_path, env=env, capture_output=True, text=True, timeout=300)
+    return proc
+
+
+def test_unmutated_copy_passes(tmp_path):
+    old = MUTATIONS[0][1]
+    proc = _run_pins_on_copy(tmp_path, old, old)
+    assert proc.returncode == 0, proc.stdout[-2000:]
+
+
+@pytest.mark.parametrize("name,old,new", MUTATIONS, ids=[m[0] for m in MUTATIONS])
+def test_pins_catch_planted_mistake(tmp_path, name, old, new):
+    proc = _run_pins_on_copy(tmp_path, old, new)
+    assert proc.returncode == 1, f"planted mistake {name} went unnoticed:\n{proc.stdout[-2000:]}"
