@@ -1,0 +1,217 @@
+/*
+ * ifvs.h -- C ABI of the iFVS filtered vector search hot path for AMD MI355X
+ * (gfx950).
+ *
+ * The method (iFVS, "Towards Instance-Optimized Filtered Vector Search",
+ * Section 2) answers a filtered query <q, f> over a fixed PQ-quantized dataset
+ * in three stages -- Filter, Rank, Select -- using a codebook conditioned on
+ * the query and its predicate:
+ *
+ *   alpha = sum of h memory-bank rows chosen by hashing <q, f>   (Section 2, opening paragraph)
+ *   w_f   = softplus(w_z),  Delta = alpha . W,  C_iFVS = C_PQ + Delta   (Section 2, first display)
+ *   Filter: evaluate f over each vector's attributes -> candidate pool P
+ *   Rank:   weighted distance of q to each candidate reconstructed from C_iFVS
+ *           (the score display of Section 2 equals sum w q^2 minus this distance)
+ *   Select: the k best candidates (Section 1 SQL listing: ORDER BY ... LIMIT K)
+ *
+ * Conventions shared by every call
+ *  - Every call returns an ifvs_status; nothing throws across the boundary.
+ *    On a non-OK status ifvs_last_error() describes the failure.
+ *  - Host-side validation runs before anything is enqueued: a call that fails
+ *    validation enqueues no work and writes no output.
+ *  - Per-call arrays are caller-owned DEVICE memory unless stated otherwise;
+ *    the library never frees caller memory.  Predicates are HOST arrays.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
+ *    the call returns; outputs are valid once the stream has synchronized.
+ *    One index handle serves one stream at a time: calls on one handle from
+ *    different streams or threads concurrently race on its workspace.
+ *  - Device faults surface as IFVS_E_HIP at a later synchronizing call.
+ *  - The hot calls (select_codebook, build_lut, filter, filtered_search)
+ *    allocate nothing: their scratch lives in the index's workspace, sized at
+ *    load by max_batch and max_k.
+ */
+#ifndef IFVS_H
+#define IFVS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t ifvs_status;
+#define IFVS_OK             0
+#define IFVS_E_INVALID     (-1)   /* bad argument (pointer, size, shape, k, column, ...) */
+#define IFVS_E_NOMEM       (-2)   /* device or pinned host allocation failed (load only)  */
+#define IFVS_E_HIP         (-3)   /* a HIP runtime call failed; see ifvs_last_error()     */
+#define IFVS_E_UNSUPPORTED (-4)   /* valid request this build cannot serve (e.g. LDS budget) */
+#define IFVS_E_STATE       (-5)   /* call on a NULL handle                                */
+
+#define IFVS_MEM_HOST   0
+#define IFVS_MEM_DEVICE 1
+
+#define IFVS_LUT_F32 0            /* distance table entries in fp32 (the exact mode)        */
+#define IFVS_LUT_F16 1            /* entries rounded to binary16 (nearest even), summed in fp32 */
+
+#define IFVS_KSUB        256      /* codewords per subspace: 8-bit PQ codes                 */
+#define IFVS_MAX_CLAUSES 4
+#define IFVS_MAX_K       1024
+#define IFVS_MAX_ATTR    16
+
+typedef struct ifvs_index ifvs_index;   /* opaque; library-owned device state */
+
+/* Everything ifvs_load_index needs.  All arrays live in the memory named by
+ * mem_kind (all host or all device).  Shapes follow Section 2: D = dim,
+ * M = m subspaces of d = dim/m dimensions, K = ksub = 256 codewords, r
+ * adjustment directions, a bank of B = bank_rows rows, h hash functions. */
+typedef struct {
+  int64_t n;                 /* number of base vectors, 1 <= n < 2^31                     */
+  int32_t dim;               /* D, 1 <= dim <= 4096                                        */
+  int32_t m;                 /* M, dim % m == 0, m <= 256                                  */
+  int32_t ksub;              /* must be 256                                                */
+  int32_t n_attr;            /* relational attribute columns, 0..IFVS_MAX_ATTR             */
+  const uint8_t* codes;      /* [n][m] row-major PQ codes                                  */
+  const float*   codebook;   /* C_PQ [m][256][dim/m]                                       */
+  const int32_t* attrs;      /* [n_attr][n] column-major attribute values (NULL if n_attr==0) */
+  int32_t bank_rows;         /* B; 0 = no memory bank (alpha = 0, the identity of Section 2) */
+  int32_t r;                 /* adjustment directions, 1..64 when bank_rows > 0             */
+  int32_t h;                 /* hash functions, 1..16 when bank_rows > 0                    */
+  int32_t mem_kind;          /* IFVS_MEM_HOST or IFVS_MEM_DEVICE                           */
+  uint64_t hash_seed;        /* seeds the h hash functions                                 */
+  const float* bank;         /* memory bank [bank_rows][m*r] (NULL if bank_rows == 0)      */
+  const float* W;            /* direction tensor [m][r][256][dim/m] (NULL if bank_rows == 0) */
+  int32_t max_batch;         /* largest nq of any later call (sizes the workspace), >= 1    */
+  int32_t max_k;             /* largest k of any later call, 1..IFVS_MAX_K                 */
+} ifvs_index_desc;
+
+/* One clause lo <= attr[col] < hi (half-open, int64 bounds so that any int32
+ * attribute value can be included or excluded).  lo >= hi is an empty clause
+ * (nothing passes), not an error.  =v is [v, v+1); >v is [v+1, INT64_MAX);
+ * <=v is [INT64_MIN, v+1). */
+typedef struct {
+  int32_t col;               /* attribute column, 0 <= col < n_attr */
+  int32_t reserved;          /* must be 0 */
+  int64_t lo;
+  int64_t hi;
+} ifvs_clause;
+
+/* A predicate f: the conjunction of n_clauses clauses (Section 1 SQL listing:
+ * WHERE col1 > v1 AND col2 = v2); n_clauses == 0 is TRUE. */
+typedef struct {
+  int32_t n_clauses;         /* 0..IFVS_MAX_CLAUSES */
+  int32_t reserved;          /* must be 0 */
+  ifvs_clause c[IFVS_MAX_CLAUSES];
+} ifvs_predicate;
+
+/* ifvs_load_index -- make a quantized dataset resident on the current device
+ * (Abstract and Section 2: "a fixed, quantized vector dataset").
+ *  desc: shapes and arrays, see ifvs_index_desc.  The arrays are deep-copied
+ *        into library-owned device memory (codes are re-laid out into 64-row
+ *        interleaved tiles for coalesced reads); the caller may free them
+ *        after return.  The index is immutable afterwards.
+ *  out:  receives the handle; free it with ifvs_free_index.
+ * Errors: IFVS_E_INVALID for shapes outside the ranges above or NULL arrays,
+ * IFVS_E_NOMEM if an allocation fails (nothing is leaked), IFVS_E_HIP. */
+ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out);
+
+/* Release every device and host resource of the handle (NULL is a no-op).
+ * Synchronizes the device first so no enqueued work still uses the index. */
+void ifvs_free_index(ifvs_index* idx);
+
+/* ifvs_select_codebook -- per-query conditioning (Section 2, opening
+ * paragraph and first display).  For each query i < nq:
+ *   key   = FNV-1a-64 over q_i's fp32 bytes, then preds[i].n_clauses (int32),
+ *           then each clause as (col int32, lo int64, hi int64), little-endian
+ *   row_j = SplitMix64(key XOR SplitMix64(hash_seed + j)) mod B,  j < h
+ *   alpha_i = bank[row_0] + bank[row_1] + ... (fp32, in j order, from +0)
+ *   w_f_i   = softplus(w_z_i) evaluated in fp64, rounded once to fp32
+ *  q:         device [nq][dim] fp32
+ *  preds:     HOST [nq] predicates (hashed exactly as given)
+ *  w_z:       device [nq][dim] fp32, or NULL: w_f = 1 exactly
+ *  alpha_out: device [nq][m*r] fp32; may be NULL only when bank_rows == 0
+ *             (then nothing is written for alpha)
+ *  wf_out:    device [nq][dim] fp32
+ * Errors: IFVS_E_INVALID (nq outside 1..max_batch, NULL q / wf_out, bad
+ * predicate), IFVS_E_STATE (NULL handle), IFVS_E_HIP. */
+ifvs_status ifvs_select_codebook(ifvs_index* idx, int32_t nq, const float* q,
+                                 const ifvs_predicate* preds, const float* w_z,
+                                 float* alpha_out, float* wf_out, void* stream);
+
+/* ifvs_build_lut -- each query's asymmetric distance table over its
+ * conditioned codebook (Section 2 first display and Rank stage):
+ *   C[m][c][j]  = C_PQ[m][c][j] + sum_{t<r} alpha[m*r+t] * W[m][t][c][j]
+ *   LUT[m][c]   = sum_{j<d} w_f[m*d+j] * (q[m*d+j] - C[m][c][j])^2
+ * in fp32 with every operation rounded (no fused multiply-add), t and j summed
+ * in index order from +0.
+ *  q:       device [nq][dim] fp32
+ *  alpha:   device [nq][m*r] fp32, or NULL: Delta = 0 (C_iFVS = C_PQ)
+ *  wf:      device [nq][dim] fp32, or NULL: w_f = 1
+ *  lut_dtype: IFVS_LUT_F32 or IFVS_LUT_F16 (entries rounded to nearest even
+ *           binary16; values beyond its range become +inf)
+ *  lut_out: device [nq][m][256] of fp32 or binary16
+ * Errors: IFVS_E_INVALID (nq, NULL q / lut_out, alpha given with no bank,
+ * unknown dtype), IFVS_E_STATE, IFVS_E_HIP. */
+ifvs_status ifvs_build_lut(ifvs_index* idx, int32_t nq, const float* q, const float* alpha,
+                           const float* wf, int32_t lut_dtype, void* lut_out, void* stream);
+
+/* ifvs_filter -- the Filter stage alone (Section 2, stage 1): selection
+ * bitmaps and pool sizes.
+ *  preds:      HOST [nq]
+ *  bitmap_out: device [nq][ceil(n/32)] uint32; vector i of query q is bit
+ *              (i mod 32) of word (i div 32), least significant bit first;
+ *              bits past n are 0
+ *  count_out:  device [nq] int64 pool sizes |P_q|, or NULL
+ * Errors: IFVS_E_INVALID (nq, NULL bitmap_out, column out of range,
+ * n_clauses > 4, nonzero reserved fields), IFVS_E_STATE, IFVS_E_HIP. */
+ifvs_status ifvs_filter(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
+                        uint32_t* bitmap_out, int64_t* count_out, void* stream);
+
+/* ifvs_filtered_search -- Filter, Rank and Select for a batch (Section 2,
+ * stages 1-3).  For each query q: the candidate pool P_q = vectors whose
+ * attributes satisfy preds[q]; dist(v) = sum_{m<M} LUT_q[m][code_v[m]]
+ * (fp32, m in index order from +0; an fp16 table is widened entry by entry);
+ * the k smallest (dist, id) pairs in ascending order, ties to the smaller id.
+ *  preds:      HOST [nq]
+ *  lut:        device [nq][m][256] in lut_dtype (from ifvs_build_lut)
+ *  k:          1..max_k
+ *  ids_out:    device [nq][k] int32; rows with |P_q| < k end in id -1
+ *  dist_out:   device [nq][k] fp32; +inf where the id is -1
+ *  bitmap_out: device [nq][ceil(n/32)] uint32 copy of the selection bitmaps
+ *              (layout as in ifvs_filter), or NULL
+ * Errors: IFVS_E_INVALID (nq, k, NULL lut / ids_out / dist_out, predicate
+ * errors as in ifvs_filter, unknown dtype), IFVS_E_UNSUPPORTED (one query's
+ * fp32 table plus its top-k pool exceeds the 160 KB LDS budget: use
+ * IFVS_LUT_F16), IFVS_E_STATE, IFVS_E_HIP. */
+ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
+                                 const void* lut, int32_t lut_dtype, int32_t k,
+                                 int32_t* ids_out, float* dist_out, uint32_t* bitmap_out,
+                                 void* stream);
+
+/* Tuning knobs, never needed for correctness.  IFVS_OPT_QTILE forces the
+ * number of queries whose tables share one LDS residency and one pass over
+ * the codes (0 = automatic); IFVS_OPT_SPLITS forces the number of code chunks
+ * a query tile is cut into (0 = automatic).
+ * Errors: IFVS_E_INVALID for an unknown option or a negative value. */
+#define IFVS_OPT_QTILE  1
+#define IFVS_OPT_SPLITS 2
+ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value);
+
+/* ifvs_get_plan -- the launch plan ifvs_filtered_search would use for a
+ * batch of nq queries with this k and lut_dtype, without doing any work:
+ * out4[0] queries per tile (tables sharing one LDS residency and one pass
+ * over the codes), out4[1] code chunks per query tile, out4[2] 64-row code
+ * tiles per chunk, out4[3] LDS bytes per workgroup.  For measurement and
+ * tests.  Errors: IFVS_E_INVALID (NULL out4, k), IFVS_E_UNSUPPORTED (as in
+ * ifvs_filtered_search), IFVS_E_STATE. */
+ifvs_status ifvs_get_plan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_dtype,
+                          int64_t* out4);
+
+/* Text of the last failure on the calling thread; valid until the next call
+ * on this thread.  Never NULL. */
+const char* ifvs_last_error(void);
+
+#ifdef __cplusplus
+}  /* extern "C" */
+#endif
+
+#endif /* IFVS_H */

@@ -1,0 +1,448 @@
+// Host runtime of libifvs: the C ABI declared in include/ifvs.h.
+//
+// Owns the device-resident index (codes re-laid out into 64-row tiles,
+// codebook, attribute columns, memory bank, direction tensor), a workspace
+// sized once at load (device copies of the predicates, selection bitmaps,
+// pool sizes, per-wavefront top-k partials, pinned staging for predicates),
+// argument validation, and the launch plan of each call.  The hot calls
+// allocate nothing.
+#include "ifvs.h"
+#include "ifvs_internal.h"
+
+#include <algorithm>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <limits>
+#include <string>
+
+using namespace ifvs;
+
+namespace {
+
+thread_local std::string g_error = "no error";
+
+ifvs_status fail(ifvs_status st, const std::string& msg) {
+  g_error = msg;
+  return st;
+}
+
+ifvs_status hip_fail(hipError_t e, const char* what) {
+  return fail(IFVS_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define IFVS_HIP(call, what)                      \
+  do {                                            \
+    const hipError_t e_ = (call);                 \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+// Test hook: IFVS_FAIL_ALLOC=n makes the n-th allocation of a process fail
+// (1-based), so out-of-memory paths can be exercised on purpose.
+int g_alloc_counter = 0;
+
+bool forced_alloc_failure() {
+  static const int fail_at = [] {
+    const char* s = std::getenv("IFVS_FAIL_ALLOC");
+    return s ? std::atoi(s) : 0;
+  }();
+  ++g_alloc_counter;
+  return fail_at > 0 && g_alloc_counter == fail_at;
+}
+
+constexpr int kStagingSlots = 4;
+
+}  // namespace
+
+struct ifvs_index {
+  int device = 0;
+  int64_t n = 0;
+  int dim = 0, m = 0, dsub = 0, n_attr = 0;
+  int bank_rows = 0, r = 0, h = 0;
+  uint64_t hash_seed = 0;
+  int mw = 0;
+  int64_t n_tiles = 0;
+  int max_batch = 0, max_k = 0;
+
+  uint32_t* codes_t = nullptr;   // [n_tiles][mw][64] code words
+  float* cpq = nullptr;          // [m][256][dsub]
+  int32_t* attrs = nullptr;      // [n_attr][n]
+  float* bank = nullptr;         // [bank_rows][m*r]
+  float* W = nullptr;            // [m][r][256][dsub]
+
+  DevPred* preds_dev = nullptr;  // [max_batch]
+  DevPred* staging[kStagingSlots] = {};
+  hipEvent_t staged[kStagingSlots] = {};
+  bool slot_busy[kStagingSlots] = {};
+  int next_slot = 0;
+
+  uint64_t* bitmap = nullptr;    // [max_batch][stride64]
+  int64_t stride64 = 0;
+  unsigned long long* counts = nullptr;  // [max_batch]
+  uint64_t* partials = nullptr;  // per-wavefront top-k keys
+  size_t partial_keys = 0;
+
+  int opt_qtile = 0, opt_splits = 0;
+
+  ~ifvs_index() {
+    hipSetDevice(device);
+    hipDeviceSynchronize();
+    for (void* p : {static_cast<void*>(codes_t), static_cast<void*>(cpq), static_cast<void*>(attrs),
+                    static_cast<void*>(bank), static_cast<void*>(W), static_cast<void*>(preds_dev),
+                    static_cast<void*>(bitmap), static_cast<void*>(counts),
+                    static_cast<void*>(partials)})
+      if (p) hipFree(p);
+    for (int i = 0; i < kStagingSlots; ++i) {
+      if (staging[i]) hipHostFree(staging[i]);
+      if (staged[i]) hipEventDestroy(staged[i]);
+    }
+  }
+};
+
+namespace {
+
+template <typename T>
+ifvs_status dev_alloc(T** p, size_t count, const char* what) {
+  *p = nullptr;
+  if (count == 0) count = 1;
+  if (forced_alloc_failure()) return fail(IFVS_E_NOMEM, std::string("forced allocation failure: ") + what);
+  const hipError_t e = hipMalloc(reinterpret_cast<void**>(p), count * sizeof(T));
+  if (e != hipSuccess) {
+    *p = nullptr;
+    (void)hipGetLastError();
+    return fail(IFVS_E_NOMEM, std::string("device allocation failed: ") + what);
+  }
+  return IFVS_OK;
+}
+
+ifvs_status check_index(const ifvs_index* idx) {
+  if (!idx) return fail(IFVS_E_STATE, "NULL index handle");
+  return IFVS_OK;
+}
+
+ifvs_status check_nq(const ifvs_index* idx, int32_t nq) {
+  if (nq < 0 || nq > idx->max_batch)
+    return fail(IFVS_E_INVALID, "nq = " + std::to_string(nq) + " outside 0.." +
+                                    std::to_string(idx->max_batch) + " (max_batch)");
+  return IFVS_OK;
+}
+
+// Validate the caller's predicates and turn them into DevPred records.
+ifvs_status normalize_predicates(const ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
+                                 DevPred* out) {
+  if (nq > 0 && !preds) return fail(IFVS_E_INVALID, "preds is NULL");
+  for (int32_t i = 0; i < nq; ++i) {
+    const ifvs_predicate& p = preds[i];
+    if (p.n_clauses < 0 || p.n_clauses > IFVS_MAX_CLAUSES)
+      return fail(IFVS_E_INVALID, "query " + std::to_string(i) + ": n_clauses = " +
+                                      std::to_string(p.n_clauses) + " outside 0..4");
+    if (p.reserved != 0) return fail(IFVS_E_INVALID, "query " + std::to_string(i) + ": reserved field not 0");
+    DevPred d{};
+    d.n_raw = p.n_clauses;
+    int n_eff = 0;
+    bool empty = false;
+    for (int c = 0; c < p.n_clauses; ++c) {
+      const ifvs_clause& cl = p.c[c];
+      if (cl.col < 0 || cl.col >= idx->n_attr)
+        return fail(IFVS_E_INVALID, "query " + std::to_string(i) + ": clause " + std::to_string(c) +
+                                        " column " + std::to_string(cl.col) + " outside 0.." +
+                                        std::to_string(idx->n_attr - 1));
+      if (cl.reserved != 0)
+        return fail(IFVS_E_INVALID, "query " + std::to_string(i) + ": clause reserved field not 0");
+      d.raw_col[c] = cl.col;
+      d.raw_lo[c] = cl.lo;
+      d.raw_hi[c] = cl.hi;
+      // Intersect [lo, hi) with the int32 range.
+      const int64_t lo = std::max<int64_t>(cl.lo, std::numeric_limits<int32_t>::min());
+      const int64_t hi = std::min<int64_t>(cl.hi, int64_t(std::numeric_limits<int32_t>::max()) + 1);
+      if (cl.lo >= cl.hi || lo >= hi) {
+        empty = true;
+        continue;
+      }
+      const uint64_t width = static_cast<uint64_t>(hi - lo);
+      if (width >= (1ull << 32)) continue;           // admits every int32 value
+      d.col[n_eff] = cl.col;
+      d.lo[n_eff] = static_cast<int32_t>(lo);
+      d.width[n_eff] = static_cast<uint32_t>(width);
+      ++n_eff;
+    }
+    d.n_eff = empty ? -1 : n_eff;
+    out[i] = d;
+  }
+  return IFVS_OK;
+}
+
+// Copy validated predicates to the device through a pinned staging slot.
+ifvs_status stage_predicates(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
+                             hipStream_t s) {
+  const int slot = idx->next_slot;
+  idx->next_slot = (slot + 1) % kStagingSlots;
+  if (idx->slot_busy[slot]) IFVS_HIP(hipEventSynchronize(idx->staged[slot]), "waiting for staging slot");
+  DevPred* host = idx->staging[slot];
+  const ifvs_status st = normalize_predicates(idx, nq, preds, host);
+  if (st != IFVS_OK) return st;
+  IFVS_HIP(hipMemcpyAsync(idx->preds_dev, host, sizeof(DevPred) * nq, hipMemcpyHostToDevice, s),
+           "copying predicates");
+  IFVS_HIP(hipEventRecord(idx->staged[slot], s), "recording staging event");
+  idx->slot_busy[slot] = true;
+  return IFVS_OK;
+}
+
+ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_dtype, ScanPlan* plan) {
+  const int lut_bytes = lut_dtype == IFVS_LUT_F16 ? 2 : 4;
+  const int qmax = scan_max_qtile(idx->m, lut_bytes, k);
+  if (qmax < 1)
+    return fail(IFVS_E_UNSUPPORTED, "one query's distance table (" + std::to_string(idx->m) +
+                                        " x 256 x " + std::to_string(lut_bytes) +
+                                        " B) plus its top-k pools exceeds the 160 KB LDS budget; use IFVS_LUT_F16");
+  int want = idx->opt_qtile > 0 ? idx->opt_qtile : 8;
+  want = std::min(want, std::max(1, nq));
+  want = std::min(want, qmax);
+  plan->qtile = std::max(1, scan_supported_qtile(want));
+  const int64_t gy = (std::max(1, nq) + plan->qtile - 1) / plan->qtile;
+  // Enough workgroups to fill 256 CUs several times, each with >= 16 tiles.
+  int64_t splits = idx->opt_splits > 0 ? idx->opt_splits : (2048 + gy - 1) / gy;
+  splits = std::min<int64_t>(splits, std::max<int64_t>(1, idx->n_tiles / 16));
+  const int64_t cap = static_cast<int64_t>(idx->partial_keys /
+                                           (static_cast<size_t>(std::max(1, nq)) * kScanWaves * k));
+  splits = std::max<int64_t>(1, std::min<int64_t>(splits, std::min<int64_t>(cap, 65535)));
+  plan->tiles_per_block = (idx->n_tiles + splits - 1) / splits;
+  plan->splits = static_cast<int>((idx->n_tiles + plan->tiles_per_block - 1) / plan->tiles_per_block);
+  plan->kpl = pool_kpl(k);
+  plan->pool_stride = 64 * plan->kpl;
+  plan->lds_bytes = static_cast<size_t>(idx->m) * plan->qtile * kKsub * lut_bytes +
+                    static_cast<size_t>(kScanWaves) * plan->qtile * plan->pool_stride * sizeof(uint64_t);
+  return IFVS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ifvs_last_error(void) { return g_error.c_str(); }
+
+ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
+  if (!desc || !out) return fail(IFVS_E_INVALID, "desc or out is NULL");
+  *out = nullptr;
+  const ifvs_index_desc& d = *desc;
+  if (d.n < 1 || d.n >= (int64_t(1) << 31)) return fail(IFVS_E_INVALID, "n must be in 1..2^31-1");
+  if (d.dim < 1 || d.dim > 4096) return fail(IFVS_E_INVALID, "dim must be in 1..4096");
+  if (d.m < 1 || d.m > 256 || d.dim % d.m != 0) return fail(IFVS_E_INVALID, "m must divide dim and be in 1..256");
+  if (d.ksub != IFVS_KSUB) return fail(IFVS_E_INVALID, "ksub must be 256 (8-bit codes)");
+  if (d.n_attr < 0 || d.n_attr > IFVS_MAX_ATTR) return fail(IFVS_E_INVALID, "n_attr must be in 0..16");
+  if (d.mem_kind != IFVS_MEM_HOST && d.mem_kind != IFVS_MEM_DEVICE) return fail(IFVS_E_INVALID, "unknown mem_kind");
+  if (!d.codes || !d.codebook) return fail(IFVS_E_INVALID, "codes or codebook is NULL");
+  if (d.n_attr > 0 && !d.attrs) return fail(IFVS_E_INVALID, "attrs is NULL but n_attr > 0");
+  if (d.bank_rows < 0) return fail(IFVS_E_INVALID, "bank_rows must be >= 0");
+  if (d.bank_rows > 0) {
+    if (d.r < 1 || d.r > 64) return fail(IFVS_E_INVALID, "r must be in 1..64");
+    if (d.h < 1 || d.h > 16) return fail(IFVS_E_INVALID, "h must be in 1..16");
+    if (!d.bank || !d.W) return fail(IFVS_E_INVALID, "bank or W is NULL but bank_rows > 0");
+  }
+  if (d.max_batch < 1 || d.max_batch > 65535 * 8) return fail(IFVS_E_INVALID, "max_batch must be in 1..524280");
+  if (d.max_k < 1 || d.max_k > IFVS_MAX_K) return fail(IFVS_E_INVALID, "max_k must be in 1..1024");
+
+  ifvs_index* idx = new ifvs_index();
+  auto bail = [&](ifvs_status st) {
+    delete idx;
+    return st;
+  };
+  if (hipError_t e = hipGetDevice(&idx->device); e != hipSuccess) return bail(hip_fail(e, "hipGetDevice"));
+  idx->n = d.n;
+  idx->dim = d.dim;
+  idx->m = d.m;
+  idx->dsub = d.dim / d.m;
+  idx->n_attr = d.n_attr;
+  idx->bank_rows = d.bank_rows;
+  idx->r = d.bank_rows > 0 ? d.r : 0;
+  idx->h = d.bank_rows > 0 ? d.h : 0;
+  idx->hash_seed = d.hash_seed;
+  idx->mw = (d.m + 3) / 4;
+  idx->n_tiles = (d.n + kTileRows - 1) / kTileRows;
+  idx->max_batch = d.max_batch;
+  idx->max_k = d.max_k;
+  const hipMemcpyKind kind = d.mem_kind == IFVS_MEM_DEVICE ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
+
+  ifvs_status st;
+  // codes -> 64-row tiles
+  {
+    uint8_t* tmp = nullptr;
+    if ((st = dev_alloc(&tmp, static_cast<size_t>(d.n) * d.m, "codes staging")) != IFVS_OK) return bail(st);
+    if ((st = dev_alloc(&idx->codes_t, static_cast<size_t>(idx->n_tiles) * idx->mw * 64, "codes")) != IFVS_OK) {
+      hipFree(tmp);
+      return bail(st);
+    }
+    hipError_t e = hipMemcpy(tmp, d.codes, static_cast<size_t>(d.n) * d.m, kind);
+    if (e == hipSuccess) e = launch_relayout_codes(tmp, d.n, d.m, idx->mw, idx->codes_t, idx->n_tiles, nullptr);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    hipFree(tmp);
+    if (e != hipSuccess) return bail(hip_fail(e, "loading codes"));
+  }
+  const size_t cb = static_cast<size_t>(d.m) * kKsub * idx->dsub;
+  if ((st = dev_alloc(&idx->cpq, cb, "codebook")) != IFVS_OK) return bail(st);
+  if (hipError_t e = hipMemcpy(idx->cpq, d.codebook, cb * sizeof(float), kind); e != hipSuccess)
+    return bail(hip_fail(e, "loading codebook"));
+  if (d.n_attr > 0) {
+    const size_t na = static_cast<size_t>(d.n_attr) * d.n;
+    if ((st = dev_alloc(&idx->attrs, na, "attributes")) != IFVS_OK) return bail(st);
+    if (hipError_t e = hipMemcpy(idx->attrs, d.attrs, na * sizeof(int32_t), kind); e != hipSuccess)
+      return bail(hip_fail(e, "loading attributes"));
+  }
+  if (d.bank_rows > 0) {
+    const size_t nb = static_cast<size_t>(d.bank_rows) * d.m * d.r;
+    const size_t nw = static_cast<size_t>(d.m) * d.r * kKsub * idx->dsub;
+    if ((st = dev_alloc(&idx->bank, nb, "memory bank")) != IFVS_OK) return bail(st);
+    if ((st = dev_alloc(&idx->W, nw, "direction tensor W")) != IFVS_OK) return bail(st);
+    if (hipError_t e = hipMemcpy(idx->bank, d.bank, nb * sizeof(float), kind); e != hipSuccess)
+      return bail(hip_fail(e, "loading memory bank"));
+    if (hipError_t e = hipMemcpy(idx->W, d.W, nw * sizeof(float), kind); e != hipSuccess)
+      return bail(hip_fail(e, "loading W"));
+  }
+
+  // Workspace.
+  if ((st = dev_alloc(&idx->preds_dev, d.max_batch, "predicates")) != IFVS_OK) return bail(st);
+  for (int i = 0; i < kStagingSlots; ++i) {
+    if (forced_alloc_failure() ||
+        hipHostMalloc(reinterpret_cast<void**>(&idx->staging[i]), sizeof(DevPred) * d.max_batch,
+                      hipHostMallocDefault) != hipSuccess) {
+      idx->staging[i] = nullptr;
+      (void)hipGetLastError();
+      return bail(fail(IFVS_E_NOMEM, "pinned staging allocation failed"));
+    }
+    if (hipError_t e = hipEventCreateWithFlags(&idx->staged[i], hipEventDisableTiming); e != hipSuccess)
+      return bail(hip_fail(e, "creating staging event"));
+  }
+  idx->stride64 = idx->n_tiles;
+  if ((st = dev_alloc(&idx->bitmap, static_cast<size_t>(d.max_batch) * idx->stride64, "selection bitmaps")) != IFVS_OK)
+    return bail(st);
+  if ((st = dev_alloc(&idx->counts, d.max_batch, "pool sizes")) != IFVS_OK) return bail(st);
+  // Partials: room for at least 64 chunks per query, capped near 512 MB.
+  {
+    const size_t per_chunk = static_cast<size_t>(d.max_batch) * kScanWaves * d.max_k;
+    const size_t chunks = std::max<size_t>(16, std::min<size_t>(256, (size_t(512) << 20) / 8 / per_chunk));
+    idx->partial_keys = per_chunk * chunks;
+    if ((st = dev_alloc(&idx->partials, idx->partial_keys, "top-k partials")) != IFVS_OK) return bail(st);
+  }
+  if (hipError_t e = hipDeviceSynchronize(); e != hipSuccess) return bail(hip_fail(e, "finishing load"));
+  *out = idx;
+  return IFVS_OK;
+}
+
+void ifvs_free_index(ifvs_index* idx) { delete idx; }
+
+ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (value < 0 || value > (1 << 20)) return fail(IFVS_E_INVALID, "option value out of range");
+  switch (option) {
+    case IFVS_OPT_QTILE: idx->opt_qtile = static_cast<int>(value); return IFVS_OK;
+    case IFVS_OPT_SPLITS: idx->opt_splits = static_cast<int>(value); return IFVS_OK;
+    default: return fail(IFVS_E_INVALID, "unknown option " + std::to_string(option));
+  }
+}
+
+ifvs_status ifvs_select_codebook(ifvs_index* idx, int32_t nq, const float* q,
+                                 const ifvs_predicate* preds, const float* w_z, float* alpha_out,
+                                 float* wf_out, void* stream) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
+  if (nq == 0) return IFVS_OK;
+  if (!q || !wf_out) return fail(IFVS_E_INVALID, "q or wf_out is NULL");
+  if (idx->bank_rows > 0 && !alpha_out) return fail(IFVS_E_INVALID, "alpha_out is NULL but the index has a memory bank");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  if (ifvs_status st = stage_predicates(idx, nq, preds, s); st != IFVS_OK) return st;
+  IFVS_HIP(launch_condition(q, idx->dim, idx->preds_dev, nq, idx->bank, idx->bank_rows,
+                            idx->m * idx->r, idx->h, idx->hash_seed, w_z,
+                            idx->bank_rows > 0 ? alpha_out : nullptr, wf_out, s),
+           "launching condition kernel");
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_build_lut(ifvs_index* idx, int32_t nq, const float* q, const float* alpha,
+                           const float* wf, int32_t lut_dtype, void* lut_out, void* stream) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
+  if (lut_dtype != IFVS_LUT_F32 && lut_dtype != IFVS_LUT_F16) return fail(IFVS_E_INVALID, "unknown lut_dtype");
+  if (nq == 0) return IFVS_OK;
+  if (!q || !lut_out) return fail(IFVS_E_INVALID, "q or lut_out is NULL");
+  if (alpha && idx->bank_rows == 0) return fail(IFVS_E_INVALID, "alpha given but the index has no memory bank");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  IFVS_HIP(launch_build_lut(q, idx->dim, idx->m, idx->dsub, idx->r, idx->cpq, idx->W, alpha, wf, nq,
+                            lut_dtype, lut_out, s),
+           "launching LUT kernel");
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_filter(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
+                        uint32_t* bitmap_out, int64_t* count_out, void* stream) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
+  if (nq == 0) return IFVS_OK;
+  if (!bitmap_out) return fail(IFVS_E_INVALID, "bitmap_out is NULL");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  if (ifvs_status st = stage_predicates(idx, nq, preds, s); st != IFVS_OK) return st;
+  IFVS_HIP(launch_filter(idx->attrs, idx->n, idx->n_attr, idx->preds_dev, nq, idx->bitmap,
+                         idx->stride64, idx->counts, s),
+           "launching filter kernel");
+  const size_t words = static_cast<size_t>((idx->n + 31) / 32);
+  IFVS_HIP(hipMemcpy2DAsync(bitmap_out, words * 4, idx->bitmap, idx->stride64 * 8, words * 4, nq,
+                            hipMemcpyDeviceToDevice, s),
+           "copying bitmaps");
+  if (count_out)
+    IFVS_HIP(hipMemcpyAsync(count_out, idx->counts, sizeof(int64_t) * nq, hipMemcpyDeviceToDevice, s),
+             "copying pool sizes");
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
+                                 const void* lut, int32_t lut_dtype, int32_t k, int32_t* ids_out,
+                                 float* dist_out, uint32_t* bitmap_out, void* stream) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
+  if (lut_dtype != IFVS_LUT_F32 && lut_dtype != IFVS_LUT_F16) return fail(IFVS_E_INVALID, "unknown lut_dtype");
+  if (k < 1 || k > idx->max_k)
+    return fail(IFVS_E_INVALID, "k = " + std::to_string(k) + " outside 1.." + std::to_string(idx->max_k) + " (max_k)");
+  if (nq == 0) return IFVS_OK;
+  if (!lut || !ids_out || !dist_out) return fail(IFVS_E_INVALID, "lut, ids_out or dist_out is NULL");
+  if (reinterpret_cast<uintptr_t>(lut) % 16 != 0) return fail(IFVS_E_INVALID, "lut must be 16-byte aligned");
+  ScanPlan plan{};
+  if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, &plan); st != IFVS_OK) return st;
+  // Predicates are validated before anything is enqueued.
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  if (ifvs_status st = stage_predicates(idx, nq, preds, s); st != IFVS_OK) return st;
+  IFVS_HIP(launch_filter(idx->attrs, idx->n, idx->n_attr, idx->preds_dev, nq, idx->bitmap,
+                         idx->stride64, nullptr, s),
+           "launching filter kernel");
+  if (bitmap_out) {
+    const size_t words = static_cast<size_t>((idx->n + 31) / 32);
+    IFVS_HIP(hipMemcpy2DAsync(bitmap_out, words * 4, idx->bitmap, idx->stride64 * 8, words * 4, nq,
+                              hipMemcpyDeviceToDevice, s),
+             "copying bitmaps");
+  }
+  IFVS_HIP(launch_scan_dense(idx->codes_t, idx->n_tiles, idx->m, idx->mw, lut, lut_dtype, nq,
+                             idx->bitmap, idx->stride64, k, plan, idx->partials, s),
+           "launching scan kernel");
+  const int64_t per_query = static_cast<int64_t>(plan.splits) * kScanWaves * k;
+  IFVS_HIP(launch_topk_merge(idx->partials, nq, per_query, k, ids_out, dist_out, s),
+           "launching top-k merge kernel");
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_get_plan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_dtype,
+                          int64_t* out4) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (!out4) return fail(IFVS_E_INVALID, "out is NULL");
+  if (k < 1 || k > idx->max_k) return fail(IFVS_E_INVALID, "k outside 1..max_k");
+  ScanPlan plan{};
+  if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, &plan); st != IFVS_OK) return st;
+  out4[0] = plan.qtile;
+  out4[1] = plan.splits;
+  out4[2] = plan.tiles_per_block;
+  out4[3] = static_cast<int64_t>(plan.lds_bytes);
+  return IFVS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,153 @@
+// Distance-table build (Section 2, first display and Rank stage): for each
+// query and subspace m, the conditioned codeword
+//     C[c][j] = C_PQ[m][c][j] + sum_{t<r} alpha[m*r+t] * W[m][t][c][j]
+// and the table entry
+//     LUT[m][c] = sum_{j<d} w_f[m*d+j] * (q[m*d+j] - C[c][j])^2 .
+// Every product and sum is a separately rounded fp32 operation (explicit
+// round-to-nearest intrinsics, so no fused multiply-add), t and j summed in
+// index order from +0: the table is bit-identical to the plain definition.
+//
+// Layout: one workgroup per (subspace, chunk of queries), one thread per
+// centroid c.  A thread keeps its codeword C_PQ[m][c] and its r x d slice of
+// W in registers for the whole query chunk, so W and C_PQ are read once per
+// chunk; the query's q, w_f and alpha values are the same for the whole
+// workgroup (scalar loads).  The 256 entries of one (query, m) row are one
+// coalesced 1 KB (fp32) or 512 B (binary16) store.  The contraction over r is
+// 8 deep and d is 2..8, far too shallow for matrix cores; the kernel is
+// store-bound in the identity mode and a few microseconds per batch otherwise.
+#include "ifvs_internal.h"
+
+namespace ifvs {
+
+namespace {
+
+constexpr int kQueriesPerBlock = 16;
+
+__device__ __forceinline__ void store_entry(float* out, int64_t i, float v) { out[i] = v; }
+__device__ __forceinline__ void store_entry(__half* out, int64_t i, float v) {
+  out[i] = __float2half_rn(v);
+}
+
+// d and r known at compile time (R == 0: no alpha, C_iFVS = C_PQ).
+template <int DSUB, int R, typename OutT>
+__global__ __launch_bounds__(256) void lut_fixed_kernel(
+    const float* __restrict__ q, int dim, int M, const float* __restrict__ cpq,
+    const float* __restrict__ W, const float* __restrict__ alpha, const float* __restrict__ wf,
+    int nq, OutT* __restrict__ out) {
+  const int m = blockIdx.x;
+  const int c = threadIdx.x;
+  float creg[DSUB];
+#pragma unroll
+  for (int j = 0; j < DSUB; ++j) creg[j] = cpq[(static_cast<int64_t>(m) * kKsub + c) * DSUB + j];
+  float wreg[R > 0 ? R : 1][DSUB];
+  if constexpr (R > 0) {
+#pragma unroll
+    for (int t = 0; t < R; ++t)
+#pragma unroll
+      for (int j = 0; j < DSUB; ++j)
+        wreg[t][j] = W[((static_cast<int64_t>(m) * R + t) * kKsub + c) * DSUB + j];
+  }
+  const int q_begin = blockIdx.y * kQueriesPerBlock;
+  const int q_end = min(nq, q_begin + kQueriesPerBlock);
+  for (int qi = q_begin; qi < q_end; ++qi) {
+    const float* qv = q + static_cast<int64_t>(qi) * dim + m * DSUB;
+    const float* wv = wf ? wf + static_cast<int64_t>(qi) * dim + m * DSUB : nullptr;
+    float areg[R > 0 ? R : 1];
+    if constexpr (R > 0) {
+#pragma unroll
+      for (int t = 0; t < R; ++t) areg[t] = alpha[(static_cast<int64_t>(qi) * M + m) * R + t];
+    }
+    float acc = 0.0f;
+#pragma unroll
+    for (int j = 0; j < DSUB; ++j) {
+      float C = creg[j];
+      if constexpr (R > 0) {
+        float delta = 0.0f;
+#pragma unroll
+        for (int t = 0; t < R; ++t) delta = __fadd_rn(delta, __fmul_rn(areg[t], wreg[t][j]));
+        C = __fadd_rn(C, delta);
+      }
+      const float e = __fsub_rn(qv[j], C);
+      const float w = wv ? wv[j] : 1.0f;
+      acc = __fadd_rn(acc, __fmul_rn(w, __fmul_rn(e, e)));
+    }
+    store_entry(out, (static_cast<int64_t>(qi) * M + m) * kKsub + c, acc);
+  }
+}
+
+// Any d and r: the same arithmetic with operands read from memory.
+template <typename OutT>
+__global__ __launch_bounds__(256) void lut_generic_kernel(
+    const float* __restrict__ q, int dim, int M, int dsub, int r, const float* __restrict__ cpq,
+    const float* __restrict__ W, const float* __restrict__ alpha, const float* __restrict__ wf,
+    int nq, OutT* __restrict__ out) {
+  const int m = blockIdx.x;
+  const int c = threadIdx.x;
+  const int q_begin = blockIdx.y * kQueriesPerBlock;
+  const int q_end = min(nq, q_begin + kQueriesPerBlock);
+  for (int qi = q_begin; qi < q_end; ++qi) {
+    const float* qv = q + static_cast<int64_t>(qi) * dim + static_cast<int64_t>(m) * dsub;
+    const float* wv = wf ? wf + static_cast<int64_t>(qi) * dim + static_cast<int64_t>(m) * dsub : nullptr;
+    float acc = 0.0f;
+    for (int j = 0; j < dsub; ++j) {
+      float C = cpq[(static_cast<int64_t>(m) * kKsub + c) * dsub + j];
+      if (alpha) {
+        float delta = 0.0f;
+        for (int t = 0; t < r; ++t)
+          delta = __fadd_rn(delta, __fmul_rn(alpha[(static_cast<int64_t>(qi) * M + m) * r + t],
+                                             W[((static_cast<int64_t>(m) * r + t) * kKsub + c) * dsub + j]));
+        C = __fadd_rn(C, delta);
+      }
+      const float e = __fsub_rn(qv[j], C);
+      const float w = wv ? wv[j] : 1.0f;
+      acc = __fadd_rn(acc, __fmul_rn(w, __fmul_rn(e, e)));
+    }
+    store_entry(out, (static_cast<int64_t>(qi) * M + m) * kKsub + c, acc);
+  }
+}
+
+template <int DSUB, typename OutT>
+bool launch_fixed_r(int r, bool has_alpha, dim3 g, hipStream_t s, const float* q, int dim, int M,
+                    const float* cpq, const float* W, const float* alpha, const float* wf, int nq,
+                    OutT* out) {
+  if (!has_alpha) {
+    lut_fixed_kernel<DSUB, 0, OutT><<<g, dim3(256), 0, s>>>(q, dim, M, cpq, W, nullptr, wf, nq, out);
+    return true;
+  }
+  if (r == 8) {
+    lut_fixed_kernel<DSUB, 8, OutT><<<g, dim3(256), 0, s>>>(q, dim, M, cpq, W, alpha, wf, nq, out);
+    return true;
+  }
+  return false;
+}
+
+template <typename OutT>
+void launch_typed(const float* q, int dim, int M, int dsub, int r, const float* cpq,
+                  const float* W, const float* alpha, const float* wf, int nq, OutT* out,
+                  hipStream_t s) {
+  const dim3 g(M, (nq + kQueriesPerBlock - 1) / kQueriesPerBlock);
+  const bool has_alpha = alpha != nullptr;
+  bool done = false;
+  switch (dsub) {
+    case 2: done = launch_fixed_r<2>(r, has_alpha, g, s, q, dim, M, cpq, W, alpha, wf, nq, out); break;
+    case 4: done = launch_fixed_r<4>(r, has_alpha, g, s, q, dim, M, cpq, W, alpha, wf, nq, out); break;
+    case 8: done = launch_fixed_r<8>(r, has_alpha, g, s, q, dim, M, cpq, W, alpha, wf, nq, out); break;
+    default: break;
+  }
+  if (!done)
+    lut_generic_kernel<OutT><<<g, dim3(256), 0, s>>>(q, dim, M, dsub, r, cpq, W, alpha, wf, nq, out);
+}
+
+}  // namespace
+
+hipError_t launch_build_lut(const float* q, int dim, int m, int dsub, int r, const float* cpq,
+                            const float* W, const float* alpha, const float* wf, int nq,
+                            int lut_dtype, void* lut_out, hipStream_t s) {
+  if (lut_dtype == 1)
+    launch_typed(q, dim, m, dsub, r, cpq, W, alpha, wf, nq, static_cast<__half*>(lut_out), s);
+  else
+    launch_typed(q, dim, m, dsub, r, cpq, W, alpha, wf, nq, static_cast<float*>(lut_out), s);
+  return hipGetLastError();
+}
+
+}  // namespace ifvs

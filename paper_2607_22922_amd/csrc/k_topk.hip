@@ -1,0 +1,55 @@
+// Select stage (Section 2, stage 3): reduce the per-wavefront candidate
+// lists written by the scan to each query's k best (distance, id) pairs in
+// ascending order, ties to the smaller id, padding with (-1, +inf) when the
+// candidate pool holds fewer than k vectors.
+//
+// One wavefront per query streams its partial keys through the same
+// threshold-filtered pool used by the scan; the partial lists are each sorted,
+// so after the first few lists almost every key is rejected by one compare.
+#include "ifvs_internal.h"
+#include "topk_device.h"
+
+namespace ifvs {
+
+namespace {
+
+__global__ __launch_bounds__(64) void topk_merge_kernel(const uint64_t* __restrict__ partials,
+                                                        int64_t per_query, int k, int kpl,
+                                                        int32_t* __restrict__ ids_out,
+                                                        float* __restrict__ dist_out) {
+  extern __shared__ uint64_t pool[];
+  const int q = blockIdx.x;
+  const int lane = threadIdx.x;
+  int cnt = 0;
+  uint64_t thr = kNoKey;
+  const uint64_t* src = partials + static_cast<size_t>(q) * per_query;
+  for (int64_t b = 0; b < per_query; b += 64) {
+    const int64_t i = b + lane;
+    const uint64_t key = i < per_query ? src[i] : kNoKey;
+    pool_push(pool, cnt, thr, key, key < thr, k, kpl);
+  }
+  pool_compact(pool, cnt, thr, k, kpl);
+  for (int e = lane; e < k; e += 64) {
+    const uint64_t key = pool[e];
+    const size_t o = static_cast<size_t>(q) * k + e;
+    if (key == kNoKey) {
+      ids_out[o] = -1;
+      dist_out[o] = __builtin_inff();
+    } else {
+      ids_out[o] = static_cast<int32_t>(static_cast<uint32_t>(key));
+      dist_out[o] = from_ordered_bits(static_cast<uint32_t>(key >> 32));
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_topk_merge(const uint64_t* partials, int nq, int64_t per_query, int k,
+                             int32_t* ids_out, float* dist_out, hipStream_t s) {
+  const int kpl = pool_kpl(k);
+  const size_t lds = static_cast<size_t>(64 * kpl) * sizeof(uint64_t);
+  topk_merge_kernel<<<dim3(nq), dim3(64), lds, s>>>(partials, per_query, k, kpl, ids_out, dist_out);
+  return hipGetLastError();
+}
+
+}  // namespace ifvs

@@ -1,0 +1,264 @@
+"""Python binding of libifvs (include/ifvs.h): argument marshalling only.
+
+Every step of the search runs in the HIP kernels of libifvs.so; this module
+turns torch tensors into device pointers, predicates into the C struct
+layout, and status codes into exceptions.  PyTorch provides device memory and
+the current HIP stream, nothing else.  There is no fallback: without the
+built library (``python -m paper_2607_22922_amd.build``) importing this module
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libifvs.so")
+
+OK, E_INVALID, E_NOMEM, E_HIP, E_UNSUPPORTED, E_STATE = 0, -1, -2, -3, -4, -5
+MEM_HOST, MEM_DEVICE = 0, 1
+LUT_F32, LUT_F16 = 0, 1
+KSUB = 256
+MAX_CLAUSES = 4
+MAX_K = 1024
+OPT_QTILE, OPT_SPLITS = 1, 2
+
+EXPORTED = ("ifvs_load_index", "ifvs_free_index", "ifvs_select_codebook", "ifvs_build_lut",
+            "ifvs_filter", "ifvs_filtered_search", "ifvs_set_option", "ifvs_get_plan",
+            "ifvs_last_error")
+
+
+class IfvsError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"ifvs status {status}: {message}")
+        self.status = status
+
+
+class IndexDesc(ctypes.Structure):
+    _fields_ = [
+        ("n", ctypes.c_int64),
+        ("dim", ctypes.c_int32),
+        ("m", ctypes.c_int32),
+        ("ksub", ctypes.c_int32),
+        ("n_attr", ctypes.c_int32),
+        ("codes", ctypes.c_void_p),
+        ("codebook", ctypes.c_void_p),
+        ("attrs", ctypes.c_void_p),
+        ("bank_rows", ctypes.c_int32),
+        ("r", ctypes.c_int32),
+        ("h", ctypes.c_int32),
+        ("mem_kind", ctypes.c_int32),
+        ("hash_seed", ctypes.c_uint64),
+        ("bank", ctypes.c_void_p),
+        ("W", ctypes.c_void_p),
+        ("max_batch", ctypes.c_int32),
+        ("max_k", ctypes.c_int32),
+    ]
+
+
+class Clause(ctypes.Structure):
+    _fields_ = [("col", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("lo", ctypes.c_int64), ("hi", ctypes.c_int64)]
+
+
+class Predicate(ctypes.Structure):
+    _fields_ = [("n_clauses", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("c", Clause * MAX_CLAUSES)]
+
+
+def _load_library() -> ctypes.CDLL:
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is missing: build it with "
+                          "`python -m paper_2607_22922_amd.build` (there is no fallback path)")
+    lib = ctypes.CDLL(_LIB_PATH)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    sig = {
+        "ifvs_load_index": ([ctypes.POINTER(IndexDesc), ctypes.POINTER(vp)], i32),
+        "ifvs_free_index": ([vp], None),
+        "ifvs_select_codebook": ([vp, i32, vp, vp, vp, vp, vp, vp], i32),
+        "ifvs_build_lut": ([vp, i32, vp, vp, vp, i32, vp, vp], i32),
+        "ifvs_filter": ([vp, i32, vp, vp, vp, vp], i32),
+        "ifvs_filtered_search": ([vp, i32, vp, vp, i32, i32, vp, vp, vp, vp], i32),
+        "ifvs_set_option": ([vp, i32, i64], i32),
+        "ifvs_get_plan": ([vp, i32, i32, i32, ctypes.POINTER(ctypes.c_int64)], i32),
+        "ifvs_last_error": ([], ctypes.c_char_p),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+_lib = _load_library()
+
+
+def lib() -> ctypes.CDLL:
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != OK:
+        raise IfvsError(status, _lib.ifvs_last_error().decode(errors="replace"))
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def pack_predicates(preds) -> ctypes.Array:
+    """List of clause lists [(col, lo, hi), ...] -> C array of ifvs_predicate."""
+    arr = (Predicate * max(1, len(preds)))()
+    for i, clauses in enumerate(preds):
+        if len(clauses) > MAX_CLAUSES:
+            arr[i].n_clauses = len(clauses)      # rejected by the library
+            continue
+        arr[i].n_clauses = len(clauses)
+        for j, (col, lo, hi) in enumerate(clauses):
+            arr[i].c[j].col = int(col)
+            arr[i].c[j].lo = int(lo)
+            arr[i].c[j].hi = int(hi)
+    return arr
+
+
+def _dev_f32(t, device):
+    return t.to(device=device, dtype=torch.float32).contiguous()
+
+
+class Index:
+    """A PQ-quantized dataset resident on one GPU (ifvs_load_index)."""
+
+    def __init__(self, codes, C_pq, attrs=None, bank=None, W=None, r=0, h=0, hash_seed=0,
+                 max_batch=256, max_k=100):
+        codes = codes.contiguous()
+        device = codes.device
+        self.mem_kind = MEM_DEVICE if device.type == "cuda" else MEM_HOST
+        n, m = codes.shape
+        M, ksub, dsub = C_pq.shape
+        assert M == m and ksub == KSUB, "C_pq must be [m][256][dsub]"
+        self._keep = []                                  # host/device arrays alive during load
+        cb = C_pq.to(device=device, dtype=torch.float32).contiguous()
+        at = None if attrs is None else attrs.to(device=device, dtype=torch.int32).contiguous()
+        bk = None if bank is None else bank.to(device=device, dtype=torch.float32).contiguous()
+        Wt = None if W is None else W.to(device=device, dtype=torch.float32).contiguous()
+        self._keep += [codes, cb, at, bk, Wt]
+        d = IndexDesc()
+        d.n, d.dim, d.m, d.ksub = n, m * dsub, m, KSUB
+        d.n_attr = 0 if at is None else at.shape[0]
+        d.codes, d.codebook, d.attrs = codes.data_ptr(), cb.data_ptr(), _ptr(at)
+        d.bank_rows = 0 if bk is None else bk.shape[0]
+        d.r, d.h, d.hash_seed = (int(r), int(h), int(hash_seed)) if bk is not None else (0, 0, 0)
+        d.mem_kind = self.mem_kind
+        d.bank, d.W = _ptr(bk), _ptr(Wt)
+        d.max_batch, d.max_k = int(max_batch), int(max_k)
+        handle = ctypes.c_void_p()
+        _check(_lib.ifvs_load_index(ctypes.byref(d), ctypes.byref(handle)))
+        self._keep = None
+        self.handle = handle
+        self.n, self.m, self.dsub, self.dim = n, m, dsub, m * dsub
+        self.n_attr = d.n_attr
+        self.bank_rows, self.r = d.bank_rows, d.r
+        self.max_batch, self.max_k = int(max_batch), int(max_k)
+        self.device = torch.device("cuda", torch.cuda.current_device())
+
+    @classmethod
+    def from_workload(cls, w, max_batch=256, max_k=None, conditioned=True):
+        return cls(w.codes, w.C_pq, w.attrs, w.bank if conditioned else None,
+                   w.W if conditioned else None, w.r, w.h, w.hash_seed,
+                   max_batch=max_batch, max_k=max_k or w.k)
+
+    def close(self):
+        if getattr(self, "handle", None) is not None and self.handle.value:
+            _lib.ifvs_free_index(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # ---------------------------------------------------------- raw calls
+    def set_option(self, option: int, value: int) -> None:
+        _check(_lib.ifvs_set_option(self.handle, option, int(value)))
+
+    def plan(self, nq: int, k: int, lut_dtype: int = LUT_F32) -> dict:
+        out = (ctypes.c_int64 * 4)()
+        _check(_lib.ifvs_get_plan(self.handle, nq, k, lut_dtype, out))
+        return dict(qtile=out[0], splits=out[1], tiles_per_block=out[2], lds_bytes=out[3])
+
+    def select_codebook_into(self, q, preds_c, w_z, alpha_out, wf_out, stream=None):
+        _check(_lib.ifvs_select_codebook(self.handle, q.shape[0], q.data_ptr(), preds_c,
+                                         _ptr(w_z), _ptr(alpha_out), wf_out.data_ptr(),
+                                         _stream(stream)))
+
+    def build_lut_into(self, q, alpha, wf, lut_dtype, lut_out, stream=None):
+        _check(_lib.ifvs_build_lut(self.handle, q.shape[0], q.data_ptr(), _ptr(alpha), _ptr(wf),
+                                   lut_dtype, lut_out.data_ptr(), _stream(stream)))
+
+    def filter_into(self, nq, preds_c, bitmap_out, count_out=None, stream=None):
+        _check(_lib.ifvs_filter(self.handle, nq, preds_c, bitmap_out.data_ptr(), _ptr(count_out),
+                                _stream(stream)))
+
+    def search_into(self, nq, preds_c, lut, lut_dtype, k, ids_out, dist_out, bitmap_out=None,
+                    stream=None):
+        _check(_lib.ifvs_filtered_search(self.handle, nq, preds_c, lut.data_ptr(), lut_dtype, k,
+                                         ids_out.data_ptr(), dist_out.data_ptr(), _ptr(bitmap_out),
+                                         _stream(stream)))
+
+    # ------------------------------------------------ allocating helpers
+    def words(self) -> int:
+        return (self.n + 31) // 32
+
+    def select_codebook(self, q, preds, w_z=None):
+        nq = q.shape[0]
+        q = _dev_f32(q, self.device)
+        w_z = None if w_z is None else _dev_f32(w_z, self.device)
+        alpha = (torch.empty(nq, self.m * self.r, device=self.device)
+                 if self.bank_rows > 0 else None)
+        wf = torch.empty(nq, self.dim, device=self.device)
+        self.select_codebook_into(q, pack_predicates(preds), w_z, alpha, wf)
+        return alpha, wf
+
+    def build_lut(self, q, alpha=None, wf=None, lut_dtype=LUT_F32):
+        nq = q.shape[0]
+        q = _dev_f32(q, self.device)
+        dt = torch.float16 if lut_dtype == LUT_F16 else torch.float32
+        lut = torch.empty(nq, self.m, KSUB, device=self.device, dtype=dt)
+        self.build_lut_into(q, alpha, wf, lut_dtype, lut)
+        return lut
+
+    def filter(self, preds):
+        nq = len(preds)
+        bm = torch.empty(nq, self.words(), device=self.device, dtype=torch.int32)
+        cnt = torch.empty(nq, device=self.device, dtype=torch.int64)
+        self.filter_into(nq, pack_predicates(preds), bm, cnt)
+        return bm, cnt
+
+    def search(self, preds, lut, k, lut_dtype=LUT_F32, want_bitmap=False):
+        nq = len(preds)
+        ids = torch.empty(nq, k, device=self.device, dtype=torch.int32)
+        dist = torch.empty(nq, k, device=self.device, dtype=torch.float32)
+        bm = (torch.empty(nq, self.words(), device=self.device, dtype=torch.int32)
+              if want_bitmap else None)
+        self.search_into(nq, pack_predicates(preds), lut, lut_dtype, k, ids, dist, bm)
+        return (ids, dist, bm) if want_bitmap else (ids, dist)
+
+    def query(self, q, preds, k, w_z=None, lut_dtype=LUT_F32, conditioned=True):
+        """All four steps for one batch: condition, table, filter+scan+select."""
+        alpha, wf = self.select_codebook(q, preds, w_z)
+        lut = self.build_lut(q, alpha if conditioned else None, wf, lut_dtype)
+        return self.search(preds, lut, k, lut_dtype)
+
+
+def bitmap_words_to_numpy(bm: torch.Tensor) -> np.ndarray:
+    """Device int32 words -> host uint32 words (same bits)."""
+    return bm.cpu().numpy().view(np.uint32)

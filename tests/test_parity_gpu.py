@@ -1,0 +1,225 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Stage by stage, each kernel is fed the same inputs as the oracle stage:
+bitmaps and pool sizes, alpha and w_f, distance tables and the scan + top-k
+must be bit-exact.  End to end from raw inputs: ids bit-exact, distances
+bit-exact to the fp32 oracle and within 1e-4 relative of the fp64
+definition."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from workload import make_workload, random_index
+from tests._gpu_util import (assert_bitexact, check_search_row, oracle_from_workload,
+                             oracle_index, say)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_2607_22922_amd import ifvs
+    return ifvs
+
+
+@pytest.fixture(scope="module")
+def c1(B):
+    say("[c1] generating workload on cuda")
+    w = make_workload("c1", device="cuda")
+    idx = B.Index.from_workload(w, max_batch=128, max_k=128)
+    return w, idx, oracle_from_workload(w)
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+# ------------------------------------------------------------------ stages
+def test_filter_bitmaps_and_counts_bitexact(B, c1):
+    w, idx, ox = c1
+    preds = w.preds[0.1]
+    bm, cnt = idx.filter(preds)
+    torch.cuda.synchronize()
+    bm, cnt = _np(bm).view(np.uint32), _np(cnt)
+    for i, p in enumerate(preds):
+        mask = O.predicate_mask(ox["attrs"], p)
+        assert np.array_equal(bm[i], O.selection_bitmap(mask)), i
+        assert cnt[i] == mask.sum()
+
+
+def test_condition_alpha_and_wf_bitexact(B, c1):
+    w, idx, ox = c1
+    s = 0.1
+    alpha, wf = idx.select_codebook(w.queries, w.preds[s], w.w_z[s])
+    torch.cuda.synchronize()
+    alpha, wf = _np(alpha), _np(wf)
+    for i in range(w.queries.shape[0]):
+        a_o, wf_o = O.select_codebook(_np(w.queries[i]), w.preds[s][i], ox["bank"], ox["h"],
+                                      ox["hash_seed"], _np(w.w_z[s][i]))
+        assert_bitexact(alpha[i], a_o, f"alpha q{i}")
+        assert_bitexact(wf[i], wf_o, f"w_f q{i}")
+    # no w_z: w_f is exactly 1
+    _, wf1 = idx.select_codebook(w.queries[:4], w.preds[s][:4], None)
+    assert torch.all(wf1 == 1.0)
+
+
+@pytest.mark.parametrize("conditioned", [True, False])
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+def test_lut_bitexact(B, c1, conditioned, dtype):
+    w, idx, ox = c1
+    s = 0.1
+    lut_dt = B.LUT_F16 if dtype == "f16" else B.LUT_F32
+    alpha, wf = idx.select_codebook(w.queries, w.preds[s], w.w_z[s])
+    lut = idx.build_lut(w.queries, alpha if conditioned else None, wf, lut_dt)
+    torch.cuda.synchronize()
+    lut, alpha_h, wf_h = _np(lut), _np(alpha), _np(wf)
+    for i in range(0, w.queries.shape[0], 7):
+        ref = O.build_lut(_np(w.queries[i]), alpha_h[i] if conditioned else None, wf_h[i],
+                          ox["C_pq"], ox["W"], w.M, w.r, lut_dtype=dtype)
+        assert_bitexact(lut[i], ref, f"LUT {dtype} q{i}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+def test_scan_and_select_on_gpu_tables_bitexact(B, c1, dtype):
+    """Rank + Select fed the GPU's own tables: ids and distances bit-exact."""
+    w, idx, ox = c1
+    s = 0.1
+    lut_dt = B.LUT_F16 if dtype == "f16" else B.LUT_F32
+    alpha, wf = idx.select_codebook(w.queries, w.preds[s], w.w_z[s])
+    lut = idx.build_lut(w.queries, alpha, wf, lut_dt)
+    ids, dist = idx.search(w.preds[s], lut, w.k, lut_dt)
+    torch.cuda.synchronize()
+    lut_h, ids, dist = _np(lut), _np(ids), _np(dist)
+    for i, p in enumerate(w.preds[s]):
+        cand = O.passing_ids(O.predicate_mask(ox["attrs"], p))
+        d = O.adc_distances(lut_h[i], ox["codes"], cand)
+        ids_o, dist_o = O.select_topk(d, cand, w.k)
+        check_search_row(ids[i], dist[i], ids_o, dist_o, f"{dtype} q{i}")
+
+
+@pytest.mark.parametrize("conditioned", [True, False])
+def test_end_to_end_c1_from_raw_inputs(B, c1, conditioned):
+    w, idx, ox = c1
+    s = 0.1
+    alpha, wf = idx.select_codebook(w.queries, w.preds[s], w.w_z[s])
+    lut = idx.build_lut(w.queries, alpha if conditioned else None, wf)
+    ids, dist, bm = idx.search(w.preds[s], lut, w.k, want_bitmap=True)
+    torch.cuda.synchronize()
+    ids, dist, bm = _np(ids), _np(dist), _np(bm).view(np.uint32)
+    for i, p in enumerate(w.preds[s]):
+        q, wz = _np(w.queries[i]), _np(w.w_z[s][i])
+        res = O.filtered_search(ox, q, p, w.k, w_z=wz, conditioned=conditioned)
+        res64 = O.filtered_search(ox, q, p, w.k, w_z=wz, conditioned=conditioned, dtype=np.float64)
+        assert np.array_equal(bm[i], O.selection_bitmap(res["mask"]))
+        check_search_row(ids[i], dist[i], res["ids"], res["dist"], f"q{i}",
+                         dist64=res64["dist"][: w.k])
+        # every returned id passes the predicate
+        good = ids[i][ids[i] >= 0]
+        assert res["mask"][good].all()
+
+
+# -------------------------------------------------------------- edge cases
+def _edge_index(B, N, M, dsub, n_attr=2, domain=50, seed=0, conditioned=True, max_k=128,
+                max_batch=64):
+    ix = random_index(N, M, dsub, n_attr, domain, seed, device="cuda")
+    idx = B.Index(ix["codes"], ix["C_pq"], ix["attrs"], ix["bank"] if conditioned else None,
+                  ix["W"] if conditioned else None, ix["r"], ix["h"], ix["hash_seed"],
+                  max_batch=max_batch, max_k=max_k)
+    ox = oracle_index(ix["codes"], ix["C_pq"], ix["attrs"], ix["bank"] if conditioned else None,
+                      ix["W"] if conditioned else None, ix["r"], ix["h"], ix["hash_seed"])
+    return idx, ox
+
+
+def _run_and_check(B, idx, ox, preds, k, dsub, M, lut_dtype="f32", conditioned=True, seed=1):
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    nq = len(preds)
+    q = torch.randn(nq, M * dsub, device="cuda", generator=g)
+    wz = 0.5413 + 0.3 * torch.randn(nq, M * dsub, device="cuda", generator=g)
+    dt = B.LUT_F16 if lut_dtype == "f16" else B.LUT_F32
+    alpha, wf = idx.select_codebook(q, preds, wz)
+    lut = idx.build_lut(q, alpha if conditioned else None, wf, dt)
+    ids, dist = idx.search(preds, lut, k, dt)
+    torch.cuda.synchronize()
+    ids, dist = _np(ids), _np(dist)
+    for i, p in enumerate(preds):
+        res = O.filtered_search(ox, _np(q[i]), p, k, w_z=_np(wz[i]), lut_dtype=lut_dtype,
+                                conditioned=conditioned)
+        check_search_row(ids[i], dist[i], res["ids"], res["dist"], f"q{i} {p}")
+    return ids
+
+
+@pytest.mark.parametrize("N,M,dsub", [(1, 16, 8), (63, 16, 8), (65, 48, 2), (4097, 120, 8),
+                                      (3000, 4, 3), (777, 7, 2), (20_001, 16, 8)])
+def test_ragged_sizes_and_generic_m(B, N, M, dsub):
+    say(f"[edge] N={N} M={M} dsub={dsub}")
+    idx, ox = _edge_index(B, N, M, dsub, seed=N + M)
+    preds = [[(0, 5, 40)], [(0, 0, 50), (1, 10, 30)], [], [(1, 7, 8)], [(0, 30, 10)]] * 3
+    _run_and_check(B, idx, ox, preds, k=10, dsub=dsub, M=M)
+
+
+@pytest.mark.parametrize("k", [1, 10, 64, 100, 300])
+def test_k_range_including_pool_sorted_in_lds(B, k):
+    say(f"[edge] k={k}")
+    idx, ox = _edge_index(B, 30_000, 16, 8, seed=k, max_k=300)
+    preds = [[(0, 0, 25)], [(0, 10, 11)], [(1, 0, 50)], [(0, 3, 4), (1, 3, 4)]] * 2
+    _run_and_check(B, idx, ox, preds, k=k, dsub=8, M=16)
+
+
+def test_pool_smaller_than_k_and_empty_pool(B):
+    idx, ox = _edge_index(B, 5000, 16, 8, domain=1000, seed=3)
+    preds = [[(0, 7, 8)], [(0, 7, 7)], [(0, 9, 3)], [(0, -(1 << 62), 1 << 62), (1, 999, 1000)]]
+    ids = _run_and_check(B, idx, ox, preds, k=20, dsub=8, M=16)
+    assert np.all(ids[1] == -1) and np.all(ids[2] == -1)
+
+
+def test_identity_index_and_fp16_tables(B):
+    idx, ox = _edge_index(B, 12_345, 48, 2, conditioned=False, seed=5)
+    preds = [[(0, 0, 20)], [(1, 5, 45)], []] * 5
+    _run_and_check(B, idx, ox, preds, k=10, dsub=2, M=48, conditioned=False)
+    _run_and_check(B, idx, ox, preds, k=10, dsub=2, M=48, conditioned=False, lut_dtype="f16")
+
+
+def test_ties_broken_by_smaller_id(B):
+    ix = random_index(4000, 16, 8, 1, 10, 11, device="cuda")
+    ix["codes"][1000:1200] = ix["codes"][17]          # 201 identical rows
+    idx = B.Index(ix["codes"], ix["C_pq"], ix["attrs"], max_batch=8, max_k=64)
+    ox = oracle_index(ix["codes"], ix["C_pq"], ix["attrs"])
+    rec = ix["C_pq"][torch.arange(16, device="cuda"), ix["codes"][17].long()].reshape(-1)
+    q = rec[None].repeat(2, 1).contiguous()
+    lut = idx.build_lut(q)
+    ids, dist = idx.search([[], [(0, 0, 5)]], lut, 50)
+    torch.cuda.synchronize()
+    for i, p in enumerate([[], [(0, 0, 5)]]):
+        res = O.filtered_search(ox, _np(q[i]), p, 50, conditioned=False)
+        check_search_row(_np(ids[i]), _np(dist[i]), res["ids"], res["dist"], f"ties q{i}")
+    assert _np(dist[0])[0] == 0.0 and list(_np(ids[0])[:3]) == [17, 1000, 1001]
+
+
+def test_many_attribute_columns(B):
+    idx, ox = _edge_index(B, 9000, 16, 8, n_attr=4, domain=20, seed=9)
+    preds = [[(3, 2, 9)], [(2, 0, 10), (3, 5, 20), (0, 1, 19), (1, 0, 15)], [(2, 4, 5)]] * 3
+    _run_and_check(B, idx, ox, preds, k=10, dsub=8, M=16)
+
+
+@pytest.mark.parametrize("qtile,splits", [(1, 1), (2, 3), (3, 7), (8, 0), (6, 40)])
+def test_forced_tiles_and_splits_same_answer(B, qtile, splits):
+    idx, ox = _edge_index(B, 50_000, 16, 8, seed=21)
+    idx.set_option(B.OPT_QTILE, qtile)
+    idx.set_option(B.OPT_SPLITS, splits)
+    preds = [[(0, 0, 25)], [(1, 3, 9)], [(0, 10, 12)]] * 5
+    _run_and_check(B, idx, ox, preds, k=10, dsub=8, M=16)
+
+
+def test_repeat_calls_are_deterministic(B, c1):
+    w, idx, _ = c1
+    s = 0.1
+    outs = []
+    for _ in range(3):
+        alpha, wf = idx.select_codebook(w.queries, w.preds[s], w.w_z[s])
+        lut = idx.build_lut(w.queries, alpha, wf)
+        ids, dist = idx.search(w.preds[s], lut, w.k)
+        torch.cuda.synchronize()
+        outs.append((_np(ids), _np(dist).view(np.uint32)))
+    for o in outs[1:]:
+        assert np.array_equal(o[0], outs[0][0]) and np.array_equal(o[1], outs[0][1])
