@@ -1,0 +1,368 @@
+#!/usr/bin/env python3
+"""Benchmark of the iFVS filtered-search hot path on one MI355X.
+
+Workload: 10M base vectors of 96 dims, PQ with 48 subspaces of 2 dims
+(48 B of codes per vector), one date-like int32 attribute uniform over
+[0, 3650), range predicates at 0.1% / 1% / 10% / 50% selectivity, batches of
+256 queries, k = 10, every step of the path in the conditioned mode (memory
+bank, direction tensor, predicate weights).  Synthetic, seeded, generated on
+the GPU (the paper's SIFT10M-style workload is not available here).
+
+One step = one batch of 256 queries from each of the four selectivity bins,
+each batch going through select_codebook -> build_lut -> filtered_search.
+`value` is queries per second over the timed steps, inputs resident in HBM.
+
+Prints one JSON line.  Progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "filtered QPS at recall@10 per selectivity bin; ADC scan HBM GB/s vs peak"
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "adc_scan_c4_counters.txt")
+SCAN_SOURCES = [os.path.join(ROOT, "paper_2607_22922_amd", "csrc", f)
+                for f in ("k_scan.hip", "topk_device.h")]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def scan_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in SCAN_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_counters():
+    """HBM traffic of the scan from the committed rocprofv3 counter summary,
+    if it was taken on the current scan source."""
+    if not os.path.exists(COUNTERS_FILE):
+        return None
+    kv = {}
+    for line in open(COUNTERS_FILE):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("scan_source_sha256_16") != scan_source_hash():
+        return None
+    try:
+        return float(kv["scan_hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def exact_filtered_knn(x, attrs, queries, preds, k, chunk=1 << 21):
+    """Ground truth for recall: exact filtered kNN on the raw fp32 vectors
+    (squared L2, computed on the GPU in chunks)."""
+    nq = queries.shape[0]
+    lo = torch.tensor([p[0][1] for p in preds], device=x.device, dtype=torch.int64)
+    hi = torch.tensor([p[0][2] for p in preds], device=x.device, dtype=torch.int64)
+    qn = (queries.double() ** 2).sum(1)
+    best_d = torch.full((nq, k), float("inf"), device=x.device, dtype=torch.float64)
+    best_i = torch.full((nq, k), -1, device=x.device, dtype=torch.int64)
+    for s in range(0, x.shape[0], chunk):
+        xb = x[s:s + chunk]
+        a = attrs[0, s:s + chunk].long()
+        d = (xb.double() ** 2).sum(1)[None, :] - 2.0 * (queries.double() @ xb.double().t()) + qn[:, None]
+        ok = (a[None, :] >= lo[:, None]) & (a[None, :] < hi[:, None])
+        d = torch.where(ok, d, torch.full_like(d, float("inf")))
+        kk = min(k, d.shape[1])
+        v, i = torch.topk(d, kk, dim=1, largest=False)
+        cd = torch.cat([best_d, v], 1)
+        ci = torch.cat([best_i, i + s], 1)
+        v2, j = torch.topk(cd, k, dim=1, largest=False)
+        best_d, best_i = v2, torch.gather(ci, 1, j)
+    return best_i, best_d
+
+
+def scan_bytes_interval(w, sorted_attr, preds, splits, k, lut_entry):
+    """Algorithmic bytes of one interval-scan launch (one query per tile):
+    the code tiles overlapping each query's row interval, its table, and its
+    partial top-k lists."""
+    lo = torch.tensor([p[0][1] for p in preds], device=sorted_attr.device, dtype=sorted_attr.dtype)
+    hi = torch.tensor([p[0][2] for p in preds], device=sorted_attr.device, dtype=sorted_attr.dtype)
+    r0 = torch.searchsorted(sorted_attr, lo)
+    r1 = torch.searchsorted(sorted_attr, hi)
+    tiles = torch.where(r1 > r0, (r1 + 63) // 64 - r0 // 64, torch.zeros_like(r0))
+    mw = (w.M + 3) // 4
+    code = float(tiles.sum()) * 64 * mw * 4
+    return code + len(preds) * (w.M * 256 * lut_entry + splits * 4 * k * 8), float((r1 - r0).sum()) * w.M
+
+
+def scan_bytes_bitmap(idx, w, preds, qt, splits, k, lut_entry):
+    """Algorithmic bytes of one bitmap-scan launch (qt queries per tile): the
+    code tiles any query of a tile selects, every query's bitmap words, its
+    table and its partial top-k lists."""
+    bm, cnt = idx.filter(preds)
+    w64 = bm.view(torch.int64)
+    n_tiles = w64.shape[1]
+    pad = (-len(preds)) % qt
+    if pad:
+        w64 = torch.cat([w64, torch.zeros(pad, n_tiles, dtype=w64.dtype, device=w64.device)])
+    any_t = (w64.view(-1, qt, n_tiles) != 0).any(1)
+    mw = (w.M + 3) // 4
+    code = float(any_t.sum()) * 64 * mw * 4
+    nq = len(preds)
+    return code + nq * (n_tiles * 8 + w.M * 256 * lut_entry + splits * 4 * k * 8), float(cnt.sum()) * w.M
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--queries", type=int, default=10_000, help="queries drawn per bin")
+    ap.add_argument("--cpu-sample", type=int, default=2, help="oracle queries per bin (0 = skip)")
+    ap.add_argument("--recall-queries", type=int, default=256)
+    ap.add_argument("--plain-steps", type=int, default=5,
+                    help="steps timed on the unclustered (bitmap) layout for comparison (0 = skip)")
+    ap.add_argument("--lut", choices=["f32", "f16"], default="f32")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain copy kernel of known size (for counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    from paper_2607_22922_amd import ifvs as B
+    from workload import make_workload
+    from workload.synth import CONFIGS, DESCRIPTIONS
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    name = "c4"
+    cfg = CONFIGS[name]
+    batch, k = cfg["batch"], cfg["k"]
+    lut_dt = B.LUT_F16 if args.lut == "f16" else B.LUT_F32
+    lut_entry = 2 if lut_dt == B.LUT_F16 else 4
+    t0 = time.time()
+    log(f"[bench] generating {name} on {dev}")
+    w = make_workload(name, device=dev, n_queries=args.queries)
+    torch.cuda.synchronize()
+    log(f"[bench] generated in {time.time() - t0:.1f}s; loading indexes")
+    clus = B.Index.from_workload(w, max_batch=batch, max_k=k, cluster_cols=(0,))
+    plain = B.Index.from_workload(w, max_batch=batch, max_k=k) if args.plain_steps > 0 else None
+    n_batches = args.queries // batch
+    bins = w.bins
+
+    # Marshalled inputs per (bin, batch): packed predicates; device buffers.
+    packed = {s: [B.pack_predicates(w.preds[s][b * batch:(b + 1) * batch]) for b in range(n_batches)]
+              for s in bins}
+    alpha = torch.empty(batch, w.M * w.r, device=dev)
+    wf = torch.empty(batch, w.D, device=dev)
+    lut = torch.empty(batch, w.M, 256, device=dev,
+                      dtype=torch.float16 if lut_dt == B.LUT_F16 else torch.float32)
+    ids = {s: torch.empty(batch, k, device=dev, dtype=torch.int32) for s in bins}
+    dist = {s: torch.empty(batch, k, device=dev, dtype=torch.float32) for s in bins}
+    stream = torch.cuda.current_stream()
+
+    def run_batch(idx, s, b):
+        sl = slice(b * batch, (b + 1) * batch)
+        q = w.queries[sl]
+        idx.select_codebook_into(q, packed[s][b], w.w_z[s][sl], alpha, wf)
+        idx.build_lut_into(q, alpha, wf, lut_dt, lut)
+        idx.search_into(batch, packed[s][b], lut, lut_dt, k, ids[s], dist[s])
+
+    def timed_run(idx, steps):
+        """W warmup steps, then `steps` timed steps; every kernel timed with
+        HIP events on this stream.  Returns (total ms, per-bin [(b, ms)], profile, plans)."""
+        for i in range(args.warmup):
+            for s in bins:
+                run_batch(idx, s, i % n_batches)
+        torch.cuda.synchronize()
+        idx.set_option(B.OPT_PROFILE, 1)
+        idx.read_profile()
+        ev = {s: [] for s in bins}
+        plans = {}
+        torch.cuda.synchronize()
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        for i in range(steps):
+            b = (args.warmup + i) % n_batches
+            for s in bins:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                run_batch(idx, s, b)
+                e1.record(stream)
+                ev[s].append((b, e0, e1))
+                plans[s] = idx.last_plan()
+        stop.record(stream)
+        torch.cuda.synchronize()
+        total = start.elapsed_time(stop)
+        prof = idx.read_profile()
+        idx.set_option(B.OPT_PROFILE, 0)
+        return total, {s: [(b, a.elapsed_time(c)) for b, a, c in ev[s]] for s in bins}, prof, plans
+
+    total_ms, per_bin, prof, plans = timed_run(clus, args.steps)
+    n_queries = args.steps * len(bins) * batch
+    qps = n_queries / (total_ms / 1e3)
+    log(f"[bench] clustered: {args.steps} steps in {total_ms:.1f} ms -> {qps:.0f} queries/s")
+
+    sorted_attr = torch.sort(w.attrs[0].long()).values
+    bins_out = {}
+    scan_bytes_total = useful_total = 0.0
+    for s in bins:
+        splits = plans[s]["splits"]
+        cache = {}
+        for b, _ in per_bin[s]:
+            if b not in cache:
+                cache[b] = scan_bytes_interval(w, sorted_attr, w.preds[s][b * batch:(b + 1) * batch],
+                                               splits, k, lut_entry)
+            scan_bytes_total += cache[b][0]
+            useful_total += cache[b][1]
+        ms = [m for _, m in per_bin[s]]
+        sel = float(np.mean([v[1] / (w.M * w.N * batch) for v in cache.values()]))
+        bins_out[str(s)] = {"qps": batch * len(ms) / (sum(ms) / 1e3),
+                            "ms_per_batch": float(np.median(ms)),
+                            "realized_selectivity": round(sel, 5),
+                            "plan": plans[s]}
+    scan_ms, scan_launches = prof["scan"]
+    scan_avg_ms = scan_ms / max(1, scan_launches)
+    bytes_per_launch = scan_bytes_total / max(1, scan_launches)
+    achieved = bytes_per_launch / (scan_avg_ms / 1e3) / 1e9
+    log(f"[bench] scan: {scan_launches} launches, avg {scan_avg_ms:.3f} ms, "
+        f"{bytes_per_launch / 1e6:.1f} MB/launch -> {achieved:.0f} GB/s")
+
+    plain_out = None
+    if plain is not None:
+        p_total, p_bins, p_prof, p_plans = timed_run(plain, args.plain_steps)
+        p_bytes = 0.0
+        for s in bins:
+            cache = {}
+            for b, _ in p_bins[s]:
+                if b not in cache:
+                    pl = p_plans[s]
+                    cache[b] = scan_bytes_bitmap(plain, w, w.preds[s][b * batch:(b + 1) * batch],
+                                                 pl["qtile"], pl["splits"], k, lut_entry)[0]
+                p_bytes += cache[b]
+        p_scan_ms, p_launch = p_prof["scan"]
+        plain_out = {
+            "qps": args.plain_steps * len(bins) * batch / (p_total / 1e3),
+            "bins_qps": {str(s): batch * len(v) / (sum(m for _, m in v) / 1e3) for s, v in p_bins.items()},
+            "scan_avg_ms": p_scan_ms / max(1, p_launch),
+            "scan_GBps": (p_bytes / max(1, p_launch)) / (p_scan_ms / max(1, p_launch) / 1e3) / 1e9,
+            "stage_ms_per_step": {st: round(v[0] / args.plain_steps, 4) for st, v in p_prof.items()},
+            "plan": p_plans[bins[-1]],
+        }
+        log(f"[bench] plain layout: {plain_out['qps']:.0f} queries/s, scan {plain_out['scan_GBps']:.0f} GB/s")
+        # both layouts must return the same answers
+        for s in bins:
+            a_, f_ = clus.select_codebook(w.queries[:batch], w.preds[s][:batch], w.w_z[s][:batch])
+            lt = clus.build_lut(w.queries[:batch], a_, f_, lut_dt)
+            i1, d1 = clus.search(w.preds[s][:batch], lt, k, lut_dt)
+            i2, d2 = plain.search(w.preds[s][:batch], lt, k, lut_dt)
+            assert torch.equal(i1, i2) and torch.equal(d1.view(torch.int32), d2.view(torch.int32)), s
+
+    # Recall@k of the identity mode (alpha = 0, w_f = 1: plain PQ ADC) and of
+    # the synthetic conditioned mode, against exact filtered kNN.
+    nr = min(args.recall_queries, batch)
+    for s in bins:
+        q = w.queries[:nr]
+        preds = w.preds[s][:nr]
+        gt, _ = exact_filtered_knn(w.x, w.attrs, q, preds, k)
+        t_np = gt.cpu().numpy()
+        for mode in ("identity", "conditioned"):
+            if mode == "identity":
+                lt = clus.build_lut(q, None, None, lut_dt)
+            else:
+                a_, f_ = clus.select_codebook(q, preds, w.w_z[s][:nr])
+                lt = clus.build_lut(q, a_, f_, lut_dt)
+            got, _ = clus.search(preds, lt, k, lut_dt)
+            g_np = got.cpu().numpy()
+            hits = 0.0
+            for i in range(nr):
+                truth = set(int(v) for v in t_np[i] if v >= 0)
+                if truth:
+                    hits += len(truth & set(int(v) for v in g_np[i] if v >= 0)) / len(truth)
+            bins_out[str(s)][f"recall@{k}_{mode}"] = round(hits / nr, 4)
+    log(f"[bench] bins: {json.dumps(bins_out)}")
+
+    # Oracle on the host cores: a bounded sample of the same workload.
+    cpu = None
+    if args.cpu_sample > 0:
+        import oracle as O
+        ox = dict(codes=w.codes.cpu().numpy(), C_pq=w.C_pq.cpu().numpy(),
+                  attrs=w.attrs.cpu().numpy(), bank=w.bank.cpu().numpy(), W=w.W.cpu().numpy(),
+                  r=w.r, h=w.h, hash_seed=w.hash_seed)
+        nq_cpu, agree = 0, True
+        t_cpu = 0.0
+        for s in bins:
+            q = w.queries[:args.cpu_sample]
+            preds = w.preds[s][:args.cpu_sample]
+            wz = w.w_z[s][:args.cpu_sample]
+            a_, f_ = clus.select_codebook(q, preds, wz)
+            lt = clus.build_lut(q, a_, f_, lut_dt)
+            g_ids, g_d = clus.search(preds, lt, k, lut_dt)
+            g_ids, g_d = g_ids.cpu().numpy(), g_d.cpu().numpy()
+            qh, wzh = q.cpu().numpy(), wz.cpu().numpy()
+            for i in range(args.cpu_sample):
+                tt = time.perf_counter()
+                res = O.filtered_search(ox, qh[i], preds[i], k, w_z=wzh[i], lut_dtype=args.lut)
+                t_cpu += time.perf_counter() - tt
+                nq_cpu += 1
+                agree &= bool(np.array_equal(res["ids"], g_ids[i]) and
+                              np.array_equal(res["dist"].view(np.uint32), g_d[i].view(np.uint32)))
+        cpu = {"value": nq_cpu / t_cpu, "unit": "queries/s", "cores": 1, "kind": "oracle",
+               "sample": f"{args.cpu_sample} queries per bin x {len(bins)} bins of the same "
+                         f"workload, conditioned mode, numpy single thread, {t_cpu:.1f} s",
+               "ids_and_dist_bits_match_gpu": agree}
+        log(f"[bench] oracle: {cpu['value']:.3f} queries/s, results match: {agree}")
+
+    if args.copy_calibration:
+        n_el = 1 << 28                                       # 1 GiB in, 1 GiB out
+        src = torch.ones(n_el, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+
+    traffic = read_counters()
+    out = {
+        "metric": METRIC,
+        "value": qps,
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": total_ms / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": args.lut,
+        "data": "synthetic",
+        "config": {"workload": f"{name}: {DESCRIPTIONS[name]}", "batch": batch, "k": k,
+                   "bins": bins, "mode": "conditioned (bank, W, w_z)",
+                   "layout": "rows clustered by the date attribute",
+                   "queries_per_step": len(bins) * batch},
+        "bins": bins_out,
+        "stage_ms_per_step": {st: round(v[0] / args.steps, 4) for st, v in prof.items()},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
+                     "kernel": "scan_kernel", "avg_launch_ms": scan_avg_ms,
+                     "bytes_per_launch": bytes_per_launch,
+                     "useful_bytes_per_launch": useful_total / max(1, scan_launches)},
+        "plain_layout": plain_out,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

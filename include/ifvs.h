@@ -82,6 +82,8 @@ typedef struct {
   const float* W;            /* direction tensor [m][r][256][dim/m] (NULL if bank_rows == 0) */
   int32_t max_batch;         /* largest nq of any later call (sizes the workspace), >= 1    */
   int32_t max_k;             /* largest k of any later call, 1..IFVS_MAX_K                 */
+  int32_t n_cluster;         /* 0: rows stay in id order; 1 or 2: rows are stored sorted by */
+  int32_t cluster_col[2];    /*   attribute columns cluster_col[0] (major), [1] (minor), id */
 } ifvs_index_desc;
 
 /* One clause lo <= attr[col] < hi (half-open, int64 bounds so that any int32
@@ -104,11 +106,18 @@ typedef struct {
 } ifvs_predicate;
 
 /* ifvs_load_index -- make a quantized dataset resident on the current device
- * (Abstract and Section 2: "a fixed, quantized vector dataset").
+ * (Abstract and Section 2: a fixed, quantized vector dataset).
  *  desc: shapes and arrays, see ifvs_index_desc.  The arrays are deep-copied
  *        into library-owned device memory (codes are re-laid out into 64-row
  *        interleaved tiles for coalesced reads); the caller may free them
  *        after return.  The index is immutable afterwards.
+ *        With n_cluster > 0 the rows are stored in the order of their
+ *        cluster-key attribute values (an instance-optimized layout: the
+ *        paper tailors components to a dataset and its query workload).  A
+ *        clause on cluster_col[0] -- or an equality on it plus a clause on
+ *        cluster_col[1] -- then selects one contiguous run of rows, so the
+ *        search reads only those rows; other clauses are still tested row
+ *        by row.  Results (ids, order, ties) are identical on both layouts.
  *  out:  receives the handle; free it with ifvs_free_index.
  * Errors: IFVS_E_INVALID for shapes outside the ranges above or NULL arrays,
  * IFVS_E_NOMEM if an allocation fails (nothing is leaked), IFVS_E_HIP. */
@@ -176,8 +185,8 @@ ifvs_status ifvs_filter(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
  *  k:          1..max_k
  *  ids_out:    device [nq][k] int32; rows with |P_q| < k end in id -1
  *  dist_out:   device [nq][k] fp32; +inf where the id is -1
- *  bitmap_out: device [nq][ceil(n/32)] uint32 copy of the selection bitmaps
- *              (layout as in ifvs_filter), or NULL
+ *  bitmap_out: device [nq][ceil(n/32)] uint32: the batch's selection
+ *              bitmaps exactly as ifvs_filter writes them, or NULL
  * Errors: IFVS_E_INVALID (nq, k, NULL lut / ids_out / dist_out, predicate
  * errors as in ifvs_filter, unknown dtype), IFVS_E_UNSUPPORTED (one query's
  * fp32 table plus its top-k pool exceeds the 160 KB LDS budget: use
@@ -194,17 +203,26 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
  * Errors: IFVS_E_INVALID for an unknown option or a negative value. */
 #define IFVS_OPT_QTILE  1
 #define IFVS_OPT_SPLITS 2
+#define IFVS_OPT_PROFILE 3        /* 1: time every kernel launch with HIP events (see below) */
 ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value);
 
-/* ifvs_get_plan -- the launch plan ifvs_filtered_search would use for a
- * batch of nq queries with this k and lut_dtype, without doing any work:
- * out4[0] queries per tile (tables sharing one LDS residency and one pass
- * over the codes), out4[1] code chunks per query tile, out4[2] 64-row code
- * tiles per chunk, out4[3] LDS bytes per workgroup.  For measurement and
- * tests.  Errors: IFVS_E_INVALID (NULL out4, k), IFVS_E_UNSUPPORTED (as in
- * ifvs_filtered_search), IFVS_E_STATE. */
-ifvs_status ifvs_get_plan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_dtype,
-                          int64_t* out4);
+/* ifvs_read_profile -- with IFVS_OPT_PROFILE on, every kernel the index
+ * launches is bracketed by HIP events recorded on the caller's stream.  This
+ * call waits for the recorded events, writes the summed kernel time (ms) and
+ * the launch count of each stage, and clears the totals.  Stages, in array
+ * order (IFVS_N_STAGES entries each): condition, distance table, filter,
+ * scan, top-k merge.  Errors: IFVS_E_INVALID (NULL arrays), IFVS_E_STATE,
+ * IFVS_E_HIP. */
+#define IFVS_N_STAGES 5
+ifvs_status ifvs_read_profile(ifvs_index* idx, double* ms_out, int64_t* launches_out);
+
+/* ifvs_last_plan -- the launch plan of the most recent ifvs_filtered_search
+ * on this index (all zero before the first): out4[0] queries per tile
+ * (tables sharing one LDS residency and one pass over the codes), out4[1]
+ * code chunks per query tile, out4[2] fewest 64-row code tiles per chunk,
+ * out4[3] LDS bytes per workgroup.  For measurement and tests.
+ * Errors: IFVS_E_INVALID (NULL out4), IFVS_E_STATE. */
+ifvs_status ifvs_last_plan(const ifvs_index* idx, int64_t* out4);
 
 /* Text of the last failure on the calling thread; valid until the next call
  * on this thread.  Never NULL. */

@@ -1,11 +1,11 @@
 // Host runtime of libifvs: the C ABI declared in include/ifvs.h.
 //
 // Owns the device-resident index (codes re-laid out into 64-row tiles,
-// codebook, attribute columns, memory bank, direction tensor), a workspace
-// sized once at load (device copies of the predicates, selection bitmaps,
-// pool sizes, per-wavefront top-k partials, pinned staging for predicates),
-// argument validation, and the launch plan of each call.  The hot calls
-// allocate nothing.
+// possibly in cluster-key order, codebook, attribute columns, memory bank,
+// direction tensor), a workspace sized once at load (device copies of the
+// predicates and the query order, row intervals, selection bitmaps, pool
+// sizes, per-wavefront top-k partials, pinned staging), argument validation,
+// and the launch plan of each call.  The hot calls allocate nothing.
 #include "ifvs.h"
 #include "ifvs_internal.h"
 
@@ -14,7 +14,9 @@
 #include <cstdlib>
 #include <cstring>
 #include <limits>
+#include <numeric>
 #include <string>
+#include <vector>
 
 using namespace ifvs;
 
@@ -31,9 +33,9 @@ ifvs_status hip_fail(hipError_t e, const char* what) {
   return fail(IFVS_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-#define IFVS_HIP(call, what)                      \
-  do {                                            \
-    const hipError_t e_ = (call);                 \
+#define IFVS_HIP(call, what)                         \
+  do {                                               \
+    const hipError_t e_ = (call);                    \
     if (e_ != hipSuccess) return hip_fail(e_, what); \
   } while (0)
 
@@ -52,6 +54,20 @@ bool forced_alloc_failure() {
 
 constexpr int kStagingSlots = 4;
 
+// Optional per-stage kernel timing with HIP events (IFVS_OPT_PROFILE).
+enum Stage { kStCondition = 0, kStLut, kStFilter, kStScan, kStMerge, kStages };
+constexpr int kProfilePairs = 4096;
+
+struct StageTimer {
+  hipEvent_t ev[2 * kProfilePairs] = {};
+  int used = 0;
+  double ms = 0.0;
+  int64_t launches = 0;
+};
+
+constexpr int64_t kI32Min = std::numeric_limits<int32_t>::min();
+constexpr int64_t kI32End = int64_t(std::numeric_limits<int32_t>::max()) + 1;
+
 }  // namespace
 
 struct ifvs_index {
@@ -63,15 +79,20 @@ struct ifvs_index {
   int mw = 0;
   int64_t n_tiles = 0;
   int max_batch = 0, max_k = 0;
+  int n_cluster = 0, c0 = -1, c1 = -1;
 
-  uint32_t* codes_t = nullptr;   // [n_tiles][mw][64] code words
+  uint32_t* codes_t = nullptr;   // [n_tiles][mw][64] code words, physical row order
   float* cpq = nullptr;          // [m][256][dsub]
-  int32_t* attrs = nullptr;      // [n_attr][n]
+  int32_t* attrs = nullptr;      // [n_attr][n] original id order
+  int32_t* attrs_phys = nullptr; // [n_attr][n] physical order (== attrs when not clustered)
+  int32_t* perm = nullptr;       // physical row -> original id (null when not clustered)
   float* bank = nullptr;         // [bank_rows][m*r]
   float* W = nullptr;            // [m][r][256][dsub]
 
   DevPred* preds_dev = nullptr;  // [max_batch]
-  DevPred* staging[kStagingSlots] = {};
+  int32_t* qorder_dev = nullptr; // [max_batch]
+  int64_t* iv_dev = nullptr;     // [max_batch][2]
+  DevPred* staging[kStagingSlots] = {};   // pinned: [max_batch] DevPred + [max_batch] int32
   hipEvent_t staged[kStagingSlots] = {};
   bool slot_busy[kStagingSlots] = {};
   int next_slot = 0;
@@ -83,14 +104,25 @@ struct ifvs_index {
   size_t partial_keys = 0;
 
   int opt_qtile = 0, opt_splits = 0;
+  bool profile = false;
+  StageTimer* timers = nullptr;  // [kStages] once profiling was enabled
+  ScanPlan last_plan{};
 
   ~ifvs_index() {
     hipSetDevice(device);
     hipDeviceSynchronize();
+    if (timers) {
+      for (int st = 0; st < kStages; ++st)
+        for (hipEvent_t e : timers[st].ev)
+          if (e) hipEventDestroy(e);
+      delete[] timers;
+    }
+    if (attrs_phys && attrs_phys != attrs) hipFree(attrs_phys);
     for (void* p : {static_cast<void*>(codes_t), static_cast<void*>(cpq), static_cast<void*>(attrs),
-                    static_cast<void*>(bank), static_cast<void*>(W), static_cast<void*>(preds_dev),
-                    static_cast<void*>(bitmap), static_cast<void*>(counts),
-                    static_cast<void*>(partials)})
+                    static_cast<void*>(perm), static_cast<void*>(bank), static_cast<void*>(W),
+                    static_cast<void*>(preds_dev), static_cast<void*>(qorder_dev),
+                    static_cast<void*>(iv_dev), static_cast<void*>(bitmap),
+                    static_cast<void*>(counts), static_cast<void*>(partials)})
       if (p) hipFree(p);
     for (int i = 0; i < kStagingSlots; ++i) {
       if (staging[i]) hipHostFree(staging[i]);
@@ -127,7 +159,9 @@ ifvs_status check_nq(const ifvs_index* idx, int32_t nq) {
   return IFVS_OK;
 }
 
-// Validate the caller's predicates and turn them into DevPred records.
+// Validate the caller's predicates and turn them into DevPred records: the
+// effective int32 clauses, and on a clustered index the row interval of the
+// cluster-key clauses plus the residual clauses still tested per row.
 ifvs_status normalize_predicates(const ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
                                  DevPred* out) {
   if (nq > 0 && !preds) return fail(IFVS_E_INVALID, "preds is NULL");
@@ -141,6 +175,10 @@ ifvs_status normalize_predicates(const ifvs_index* idx, int32_t nq, const ifvs_p
     d.n_raw = p.n_clauses;
     int n_eff = 0;
     bool empty = false;
+    int eff_col[kMaxClauses];
+    // Intersections of the clauses on the two cluster columns.
+    int64_t lo0 = kI32Min, hi0 = kI32End, lo1 = kI32Min, hi1 = kI32End;
+    bool has0 = false, has1 = false;
     for (int c = 0; c < p.n_clauses; ++c) {
       const ifvs_clause& cl = p.c[c];
       if (cl.col < 0 || cl.col >= idx->n_attr)
@@ -153,65 +191,173 @@ ifvs_status normalize_predicates(const ifvs_index* idx, int32_t nq, const ifvs_p
       d.raw_lo[c] = cl.lo;
       d.raw_hi[c] = cl.hi;
       // Intersect [lo, hi) with the int32 range.
-      const int64_t lo = std::max<int64_t>(cl.lo, std::numeric_limits<int32_t>::min());
-      const int64_t hi = std::min<int64_t>(cl.hi, int64_t(std::numeric_limits<int32_t>::max()) + 1);
+      const int64_t lo = std::max<int64_t>(cl.lo, kI32Min);
+      const int64_t hi = std::min<int64_t>(cl.hi, kI32End);
       if (cl.lo >= cl.hi || lo >= hi) {
         empty = true;
         continue;
+      }
+      if (idx->n_cluster > 0 && cl.col == idx->c0) {
+        has0 = true;
+        lo0 = std::max(lo0, lo);
+        hi0 = std::min(hi0, hi);
+      }
+      if (idx->n_cluster > 1 && cl.col == idx->c1) {
+        has1 = true;
+        lo1 = std::max(lo1, lo);
+        hi1 = std::min(hi1, hi);
       }
       const uint64_t width = static_cast<uint64_t>(hi - lo);
       if (width >= (1ull << 32)) continue;           // admits every int32 value
       d.col[n_eff] = cl.col;
       d.lo[n_eff] = static_cast<int32_t>(lo);
       d.width[n_eff] = static_cast<uint32_t>(width);
+      eff_col[n_eff] = cl.col;
       ++n_eff;
     }
     d.n_eff = empty ? -1 : n_eff;
+    // Interval of the cluster-key clauses; everything else stays residual.
+    d.iv_mode = 0;
+    if (has0 && lo0 < hi0) {
+      if (has1 && hi0 - lo0 == 1) {
+        d.iv_mode = 2;
+        d.iv_lo0 = lo0;
+        d.iv_hi0 = hi0;
+        d.iv_lo1 = lo1;
+        d.iv_hi1 = std::max(lo1, hi1);
+      } else {
+        d.iv_mode = 1;
+        d.iv_lo0 = lo0;
+        d.iv_hi0 = hi0;
+      }
+    } else if (has0) {
+      d.n_eff = -1;                                   // contradictory clauses on c0
+    }
+    int resid = 0;
+    for (int c = 0; c < n_eff; ++c) {
+      const bool covered = (d.iv_mode >= 1 && eff_col[c] == idx->c0) ||
+                           (d.iv_mode == 2 && eff_col[c] == idx->c1);
+      if (!covered) resid |= 1 << c;
+    }
+    d.residual_mask = d.n_eff < 0 ? 0 : resid;
     out[i] = d;
   }
   return IFVS_OK;
 }
 
-// Copy validated predicates to the device through a pinned staging slot.
+// Copy validated predicates (and the scan's query order, when asked) to the
+// device through a pinned staging slot.
 ifvs_status stage_predicates(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
-                             hipStream_t s) {
+                             bool with_order, hipStream_t s, DevPred** host_out = nullptr) {
   const int slot = idx->next_slot;
-  idx->next_slot = (slot + 1) % kStagingSlots;
   if (idx->slot_busy[slot]) IFVS_HIP(hipEventSynchronize(idx->staged[slot]), "waiting for staging slot");
   DevPred* host = idx->staging[slot];
   const ifvs_status st = normalize_predicates(idx, nq, preds, host);
   if (st != IFVS_OK) return st;
+  idx->next_slot = (slot + 1) % kStagingSlots;
   IFVS_HIP(hipMemcpyAsync(idx->preds_dev, host, sizeof(DevPred) * nq, hipMemcpyHostToDevice, s),
            "copying predicates");
+  if (with_order) {
+    // Scan order: queries with nearby cluster-key intervals next to each
+    // other, so that a query tile's intervals overlap; stable by index.
+    int32_t* order = reinterpret_cast<int32_t*>(host + idx->max_batch);
+    std::iota(order, order + nq, 0);
+    std::stable_sort(order, order + nq, [&](int32_t a, int32_t b) {
+      const DevPred& x = host[a];
+      const DevPred& y = host[b];
+      if (x.iv_mode != y.iv_mode) return x.iv_mode < y.iv_mode;
+      if (x.iv_lo0 != y.iv_lo0) return x.iv_lo0 < y.iv_lo0;
+      return x.iv_lo1 < y.iv_lo1;
+    });
+    IFVS_HIP(hipMemcpyAsync(idx->qorder_dev, order, sizeof(int32_t) * nq, hipMemcpyHostToDevice, s),
+             "copying query order");
+  }
   IFVS_HIP(hipEventRecord(idx->staged[slot], s), "recording staging event");
   idx->slot_busy[slot] = true;
+  if (host_out) *host_out = host;
   return IFVS_OK;
 }
 
-ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_dtype, ScanPlan* plan) {
+// Fold recorded event pairs of one stage into its total.
+ifvs_status flush_timer(StageTimer& t) {
+  if (t.used == 0) return IFVS_OK;
+  IFVS_HIP(hipEventSynchronize(t.ev[t.used - 1]), "waiting for profile events");
+  for (int i = 0; i + 1 < t.used; i += 2) {
+    float ms = 0.0f;
+    IFVS_HIP(hipEventElapsedTime(&ms, t.ev[i], t.ev[i + 1]), "reading profile events");
+    t.ms += ms;
+    ++t.launches;
+  }
+  t.used = 0;
+  return IFVS_OK;
+}
+
+// Launch through `fn`, bracketed by events when profiling.
+template <typename Fn>
+ifvs_status timed(ifvs_index* idx, int stage, hipStream_t s, const char* what, Fn&& fn) {
+  StageTimer* t = idx->profile ? &idx->timers[stage] : nullptr;
+  if (t) {
+    if (t->used + 2 > 2 * kProfilePairs)
+      if (ifvs_status st = flush_timer(*t); st != IFVS_OK) return st;
+    IFVS_HIP(hipEventRecord(t->ev[t->used++], s), "recording profile event");
+  }
+  IFVS_HIP(fn(), what);
+  if (t) IFVS_HIP(hipEventRecord(t->ev[t->used++], s), "recording profile event");
+  return IFVS_OK;
+}
+
+#define IFVS_LAUNCH(idx, stage, s, what, expr)                                                  \
+  do {                                                                                          \
+    const ifvs_status st_ = timed(idx, stage, s, what, [&]() -> hipError_t { return (expr); }); \
+    if (st_ != IFVS_OK) return st_;                                                             \
+  } while (0)
+
+// interval_batch: every query has a cluster-key interval; one query per tile
+// then keeps all lanes busy and the scan is bound by LDS lookups, so sharing
+// code tiles across queries would not help.  Otherwise (masked rows) tiles
+// of several queries share each pass over the codes.
+ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_dtype,
+                      bool interval_batch, ScanPlan* plan) {
   const int lut_bytes = lut_dtype == IFVS_LUT_F16 ? 2 : 4;
   const int qmax = scan_max_qtile(idx->m, lut_bytes, k);
   if (qmax < 1)
     return fail(IFVS_E_UNSUPPORTED, "one query's distance table (" + std::to_string(idx->m) +
                                         " x 256 x " + std::to_string(lut_bytes) +
                                         " B) plus its top-k pools exceeds the 160 KB LDS budget; use IFVS_LUT_F16");
-  int want = idx->opt_qtile > 0 ? idx->opt_qtile : 8;
+  int want = idx->opt_qtile > 0 ? idx->opt_qtile : (interval_batch ? 1 : 8);
   want = std::min(want, std::max(1, nq));
   want = std::min(want, qmax);
   plan->qtile = std::max(1, scan_supported_qtile(want));
   const int64_t gy = (std::max(1, nq) + plan->qtile - 1) / plan->qtile;
-  // Enough workgroups to fill 256 CUs several times, each with >= 16 tiles.
-  int64_t splits = idx->opt_splits > 0 ? idx->opt_splits : (2048 + gy - 1) / gy;
-  splits = std::min<int64_t>(splits, std::max<int64_t>(1, idx->n_tiles / 16));
+  plan->min_chunk = 16;
+  // Enough workgroups to fill 256 CUs several times.
+  int64_t splits = idx->opt_splits > 0 ? idx->opt_splits : (4096 + gy - 1) / gy;
+  splits = std::min<int64_t>(splits, std::max<int64_t>(1, (idx->n_tiles + plan->min_chunk - 1) / plan->min_chunk));
   const int64_t cap = static_cast<int64_t>(idx->partial_keys /
                                            (static_cast<size_t>(std::max(1, nq)) * kScanWaves * k));
   splits = std::max<int64_t>(1, std::min<int64_t>(splits, std::min<int64_t>(cap, 65535)));
-  plan->tiles_per_block = (idx->n_tiles + splits - 1) / splits;
-  plan->splits = static_cast<int>((idx->n_tiles + plan->tiles_per_block - 1) / plan->tiles_per_block);
+  plan->splits = static_cast<int>(splits);
   plan->kpl = pool_kpl(k);
-  plan->pool_stride = 64 * plan->kpl;
+  plan->pool_stride = pool_stride_for(k);
   plan->lds_bytes = static_cast<size_t>(idx->m) * plan->qtile * kKsub * lut_bytes +
                     static_cast<size_t>(kScanWaves) * plan->qtile * plan->pool_stride * sizeof(uint64_t);
+  return IFVS_OK;
+}
+
+ifvs_status filter_into_workspace(ifvs_index* idx, int32_t nq, bool residual_only, bool counts,
+                                  hipStream_t s) {
+  IFVS_LAUNCH(idx, kStFilter, s, "launching filter kernel",
+              launch_filter(residual_only ? idx->attrs_phys : idx->attrs, idx->n, idx->n_attr,
+                            idx->preds_dev, nq, residual_only, idx->bitmap, idx->stride64,
+                            counts ? idx->counts : nullptr, s));
+  return IFVS_OK;
+}
+
+ifvs_status copy_bitmaps_out(ifvs_index* idx, int32_t nq, uint32_t* bitmap_out, hipStream_t s) {
+  const size_t words = static_cast<size_t>((idx->n + 31) / 32);
+  IFVS_HIP(hipMemcpy2DAsync(bitmap_out, words * 4, idx->bitmap, idx->stride64 * 8, words * 4, nq,
+                            hipMemcpyDeviceToDevice, s),
+           "copying bitmaps");
   return IFVS_OK;
 }
 
@@ -239,8 +385,14 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
     if (d.h < 1 || d.h > 16) return fail(IFVS_E_INVALID, "h must be in 1..16");
     if (!d.bank || !d.W) return fail(IFVS_E_INVALID, "bank or W is NULL but bank_rows > 0");
   }
-  if (d.max_batch < 1 || d.max_batch > 65535 * 8) return fail(IFVS_E_INVALID, "max_batch must be in 1..524280");
+  if (d.max_batch < 1 || d.max_batch > 65535) return fail(IFVS_E_INVALID, "max_batch must be in 1..65535");
   if (d.max_k < 1 || d.max_k > IFVS_MAX_K) return fail(IFVS_E_INVALID, "max_k must be in 1..1024");
+  if (d.n_cluster < 0 || d.n_cluster > 2) return fail(IFVS_E_INVALID, "n_cluster must be 0, 1 or 2");
+  for (int i = 0; i < d.n_cluster; ++i)
+    if (d.cluster_col[i] < 0 || d.cluster_col[i] >= d.n_attr)
+      return fail(IFVS_E_INVALID, "cluster_col outside 0..n_attr-1");
+  if (d.n_cluster == 2 && d.cluster_col[0] == d.cluster_col[1])
+    return fail(IFVS_E_INVALID, "the two cluster columns must differ");
 
   ifvs_index* idx = new ifvs_index();
   auto bail = [&](ifvs_status st) {
@@ -261,10 +413,32 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
   idx->n_tiles = (d.n + kTileRows - 1) / kTileRows;
   idx->max_batch = d.max_batch;
   idx->max_k = d.max_k;
+  idx->n_cluster = d.n_cluster;
+  idx->c0 = d.n_cluster > 0 ? d.cluster_col[0] : -1;
+  idx->c1 = d.n_cluster > 1 ? d.cluster_col[1] : -1;
   const hipMemcpyKind kind = d.mem_kind == IFVS_MEM_DEVICE ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
 
   ifvs_status st;
-  // codes -> 64-row tiles
+  if (d.n_attr > 0) {
+    const size_t na = static_cast<size_t>(d.n_attr) * d.n;
+    if ((st = dev_alloc(&idx->attrs, na, "attributes")) != IFVS_OK) return bail(st);
+    if (hipError_t e = hipMemcpy(idx->attrs, d.attrs, na * sizeof(int32_t), kind); e != hipSuccess)
+      return bail(hip_fail(e, "loading attributes"));
+  }
+  idx->attrs_phys = idx->attrs;
+  if (d.n_cluster > 0) {
+    if ((st = dev_alloc(&idx->perm, static_cast<size_t>(d.n), "cluster permutation")) != IFVS_OK) return bail(st);
+    if (hipError_t e = cluster_permutation(idx->attrs, d.n, d.n_cluster, idx->c0, idx->c1, idx->perm, nullptr);
+        e != hipSuccess)
+      return bail(hip_fail(e, "clustering rows"));
+    int32_t* phys = nullptr;
+    if ((st = dev_alloc(&phys, static_cast<size_t>(d.n_attr) * d.n, "clustered attributes")) != IFVS_OK)
+      return bail(st);
+    idx->attrs_phys = phys;
+    if (hipError_t e = launch_gather_attrs(idx->attrs, d.n, d.n_attr, idx->perm, phys, nullptr); e != hipSuccess)
+      return bail(hip_fail(e, "gathering clustered attributes"));
+  }
+  // codes -> 64-row tiles (in physical order)
   {
     uint8_t* tmp = nullptr;
     if ((st = dev_alloc(&tmp, static_cast<size_t>(d.n) * d.m, "codes staging")) != IFVS_OK) return bail(st);
@@ -273,7 +447,8 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
       return bail(st);
     }
     hipError_t e = hipMemcpy(tmp, d.codes, static_cast<size_t>(d.n) * d.m, kind);
-    if (e == hipSuccess) e = launch_relayout_codes(tmp, d.n, d.m, idx->mw, idx->codes_t, idx->n_tiles, nullptr);
+    if (e == hipSuccess)
+      e = launch_relayout_codes(tmp, d.n, d.m, idx->mw, idx->perm, idx->codes_t, idx->n_tiles, nullptr);
     if (e == hipSuccess) e = hipDeviceSynchronize();
     hipFree(tmp);
     if (e != hipSuccess) return bail(hip_fail(e, "loading codes"));
@@ -282,12 +457,6 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
   if ((st = dev_alloc(&idx->cpq, cb, "codebook")) != IFVS_OK) return bail(st);
   if (hipError_t e = hipMemcpy(idx->cpq, d.codebook, cb * sizeof(float), kind); e != hipSuccess)
     return bail(hip_fail(e, "loading codebook"));
-  if (d.n_attr > 0) {
-    const size_t na = static_cast<size_t>(d.n_attr) * d.n;
-    if ((st = dev_alloc(&idx->attrs, na, "attributes")) != IFVS_OK) return bail(st);
-    if (hipError_t e = hipMemcpy(idx->attrs, d.attrs, na * sizeof(int32_t), kind); e != hipSuccess)
-      return bail(hip_fail(e, "loading attributes"));
-  }
   if (d.bank_rows > 0) {
     const size_t nb = static_cast<size_t>(d.bank_rows) * d.m * d.r;
     const size_t nw = static_cast<size_t>(d.m) * d.r * kKsub * idx->dsub;
@@ -301,10 +470,13 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
 
   // Workspace.
   if ((st = dev_alloc(&idx->preds_dev, d.max_batch, "predicates")) != IFVS_OK) return bail(st);
+  if ((st = dev_alloc(&idx->qorder_dev, d.max_batch, "query order")) != IFVS_OK) return bail(st);
+  if ((st = dev_alloc(&idx->iv_dev, 2 * static_cast<size_t>(d.max_batch), "row intervals")) != IFVS_OK)
+    return bail(st);
   for (int i = 0; i < kStagingSlots; ++i) {
+    const size_t bytes = (sizeof(DevPred) + sizeof(int32_t)) * d.max_batch;
     if (forced_alloc_failure() ||
-        hipHostMalloc(reinterpret_cast<void**>(&idx->staging[i]), sizeof(DevPred) * d.max_batch,
-                      hipHostMallocDefault) != hipSuccess) {
+        hipHostMalloc(reinterpret_cast<void**>(&idx->staging[i]), bytes, hipHostMallocDefault) != hipSuccess) {
       idx->staging[i] = nullptr;
       (void)hipGetLastError();
       return bail(fail(IFVS_E_NOMEM, "pinned staging allocation failed"));
@@ -316,7 +488,7 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
   if ((st = dev_alloc(&idx->bitmap, static_cast<size_t>(d.max_batch) * idx->stride64, "selection bitmaps")) != IFVS_OK)
     return bail(st);
   if ((st = dev_alloc(&idx->counts, d.max_batch, "pool sizes")) != IFVS_OK) return bail(st);
-  // Partials: room for at least 64 chunks per query, capped near 512 MB.
+  // Partials: room for at least 16 chunks per query, capped near 512 MB.
   {
     const size_t per_chunk = static_cast<size_t>(d.max_batch) * kScanWaves * d.max_k;
     const size_t chunks = std::max<size_t>(16, std::min<size_t>(256, (size_t(512) << 20) / 8 / per_chunk));
@@ -336,6 +508,15 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
   switch (option) {
     case IFVS_OPT_QTILE: idx->opt_qtile = static_cast<int>(value); return IFVS_OK;
     case IFVS_OPT_SPLITS: idx->opt_splits = static_cast<int>(value); return IFVS_OK;
+    case IFVS_OPT_PROFILE:
+      if (value != 0 && !idx->timers) {
+        idx->timers = new StageTimer[kStages];
+        for (int st = 0; st < kStages; ++st)
+          for (hipEvent_t& e : idx->timers[st].ev)
+            IFVS_HIP(hipEventCreate(&e), "creating profile events");
+      }
+      idx->profile = value != 0;
+      return IFVS_OK;
     default: return fail(IFVS_E_INVALID, "unknown option " + std::to_string(option));
   }
 }
@@ -350,11 +531,11 @@ ifvs_status ifvs_select_codebook(ifvs_index* idx, int32_t nq, const float* q,
   if (idx->bank_rows > 0 && !alpha_out) return fail(IFVS_E_INVALID, "alpha_out is NULL but the index has a memory bank");
   hipStream_t s = static_cast<hipStream_t>(stream);
   IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
-  if (ifvs_status st = stage_predicates(idx, nq, preds, s); st != IFVS_OK) return st;
-  IFVS_HIP(launch_condition(q, idx->dim, idx->preds_dev, nq, idx->bank, idx->bank_rows,
-                            idx->m * idx->r, idx->h, idx->hash_seed, w_z,
-                            idx->bank_rows > 0 ? alpha_out : nullptr, wf_out, s),
-           "launching condition kernel");
+  if (ifvs_status st = stage_predicates(idx, nq, preds, false, s); st != IFVS_OK) return st;
+  IFVS_LAUNCH(idx, kStCondition, s, "launching condition kernel",
+              launch_condition(q, idx->dim, idx->preds_dev, nq, idx->bank, idx->bank_rows,
+                               idx->m * idx->r, idx->h, idx->hash_seed, w_z,
+                               idx->bank_rows > 0 ? alpha_out : nullptr, wf_out, s));
   return IFVS_OK;
 }
 
@@ -368,9 +549,9 @@ ifvs_status ifvs_build_lut(ifvs_index* idx, int32_t nq, const float* q, const fl
   if (alpha && idx->bank_rows == 0) return fail(IFVS_E_INVALID, "alpha given but the index has no memory bank");
   hipStream_t s = static_cast<hipStream_t>(stream);
   IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
-  IFVS_HIP(launch_build_lut(q, idx->dim, idx->m, idx->dsub, idx->r, idx->cpq, idx->W, alpha, wf, nq,
-                            lut_dtype, lut_out, s),
-           "launching LUT kernel");
+  IFVS_LAUNCH(idx, kStLut, s, "launching LUT kernel",
+              launch_build_lut(q, idx->dim, idx->m, idx->dsub, idx->r, idx->cpq, idx->W, alpha, wf,
+                               nq, lut_dtype, lut_out, s));
   return IFVS_OK;
 }
 
@@ -382,14 +563,9 @@ ifvs_status ifvs_filter(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   if (!bitmap_out) return fail(IFVS_E_INVALID, "bitmap_out is NULL");
   hipStream_t s = static_cast<hipStream_t>(stream);
   IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
-  if (ifvs_status st = stage_predicates(idx, nq, preds, s); st != IFVS_OK) return st;
-  IFVS_HIP(launch_filter(idx->attrs, idx->n, idx->n_attr, idx->preds_dev, nq, idx->bitmap,
-                         idx->stride64, idx->counts, s),
-           "launching filter kernel");
-  const size_t words = static_cast<size_t>((idx->n + 31) / 32);
-  IFVS_HIP(hipMemcpy2DAsync(bitmap_out, words * 4, idx->bitmap, idx->stride64 * 8, words * 4, nq,
-                            hipMemcpyDeviceToDevice, s),
-           "copying bitmaps");
+  if (ifvs_status st = stage_predicates(idx, nq, preds, false, s); st != IFVS_OK) return st;
+  if (ifvs_status st = filter_into_workspace(idx, nq, false, true, s); st != IFVS_OK) return st;
+  if (ifvs_status st = copy_bitmaps_out(idx, nq, bitmap_out, s); st != IFVS_OK) return st;
   if (count_out)
     IFVS_HIP(hipMemcpyAsync(count_out, idx->counts, sizeof(int64_t) * nq, hipMemcpyDeviceToDevice, s),
              "copying pool sizes");
@@ -407,41 +583,79 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   if (nq == 0) return IFVS_OK;
   if (!lut || !ids_out || !dist_out) return fail(IFVS_E_INVALID, "lut, ids_out or dist_out is NULL");
   if (reinterpret_cast<uintptr_t>(lut) % 16 != 0) return fail(IFVS_E_INVALID, "lut must be 16-byte aligned");
-  ScanPlan plan{};
-  if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, &plan); st != IFVS_OK) return st;
-  // Predicates are validated before anything is enqueued.
+  ScanPlan probe{};
+  if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, false, &probe); st != IFVS_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
-  if (ifvs_status st = stage_predicates(idx, nq, preds, s); st != IFVS_OK) return st;
-  IFVS_HIP(launch_filter(idx->attrs, idx->n, idx->n_attr, idx->preds_dev, nq, idx->bitmap,
-                         idx->stride64, nullptr, s),
-           "launching filter kernel");
-  if (bitmap_out) {
-    const size_t words = static_cast<size_t>((idx->n + 31) / 32);
-    IFVS_HIP(hipMemcpy2DAsync(bitmap_out, words * 4, idx->bitmap, idx->stride64 * 8, words * 4, nq,
-                              hipMemcpyDeviceToDevice, s),
-             "copying bitmaps");
+  DevPred* host = nullptr;
+  // Predicates are validated before anything is enqueued.
+  if (ifvs_status st = stage_predicates(idx, nq, preds, true, s, &host); st != IFVS_OK) return st;
+  bool need_bitmap = false, interval_batch = true;
+  for (int i = 0; i < nq; ++i) {
+    need_bitmap = need_bitmap || host[i].residual_mask != 0;
+    interval_batch = interval_batch && host[i].iv_mode != 0;
   }
-  IFVS_HIP(launch_scan_dense(idx->codes_t, idx->n_tiles, idx->m, idx->mw, lut, lut_dtype, nq,
-                             idx->bitmap, idx->stride64, k, plan, idx->partials, s),
-           "launching scan kernel");
+  ScanPlan plan{};
+  if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, interval_batch, &plan); st != IFVS_OK) return st;
+  IFVS_LAUNCH(idx, kStFilter, s, "launching interval kernel",
+              launch_intervals(idx->attrs_phys, idx->n, idx->c0, idx->c1, idx->preds_dev, nq, idx->iv_dev, s));
+  if (need_bitmap)
+    if (ifvs_status st = filter_into_workspace(idx, nq, true, false, s); st != IFVS_OK) return st;
+  ScanBatch b{};
+  b.codes_t = idx->codes_t;
+  b.n = idx->n;
+  b.n_tiles = idx->n_tiles;
+  b.m = idx->m;
+  b.mw = idx->mw;
+  b.lut = lut;
+  b.lut_dtype = lut_dtype;
+  b.nq = nq;
+  b.qorder = idx->qorder_dev;
+  b.iv = idx->iv_dev;
+  b.preds = idx->preds_dev;
+  b.bitmap = idx->bitmap;
+  b.stride64 = idx->stride64;
+  b.perm = idx->perm;
+  b.k = k;
+  b.partials = idx->partials;
+  IFVS_LAUNCH(idx, kStScan, s, "launching scan kernel", launch_scan(b, plan, s));
   const int64_t per_query = static_cast<int64_t>(plan.splits) * kScanWaves * k;
-  IFVS_HIP(launch_topk_merge(idx->partials, nq, per_query, k, ids_out, dist_out, s),
-           "launching top-k merge kernel");
+  IFVS_LAUNCH(idx, kStMerge, s, "launching top-k merge kernel",
+              launch_topk_merge(idx->partials, nq, per_query, k, idx->qorder_dev, ids_out, dist_out, s));
+  if (bitmap_out) {
+    // The Filter stage's bitmaps in id order (the scan itself reads row
+    // intervals and residual bits in the physical order).
+    if (ifvs_status st = filter_into_workspace(idx, nq, false, false, s); st != IFVS_OK) return st;
+    if (ifvs_status st = copy_bitmaps_out(idx, nq, bitmap_out, s); st != IFVS_OK) return st;
+  }
+  idx->last_plan = plan;
   return IFVS_OK;
 }
 
-ifvs_status ifvs_get_plan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_dtype,
-                          int64_t* out4) {
+ifvs_status ifvs_read_profile(ifvs_index* idx, double* ms_out, int64_t* launches_out) {
   if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
-  if (!out4) return fail(IFVS_E_INVALID, "out is NULL");
-  if (k < 1 || k > idx->max_k) return fail(IFVS_E_INVALID, "k outside 1..max_k");
-  ScanPlan plan{};
-  if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, &plan); st != IFVS_OK) return st;
-  out4[0] = plan.qtile;
-  out4[1] = plan.splits;
-  out4[2] = plan.tiles_per_block;
-  out4[3] = static_cast<int64_t>(plan.lds_bytes);
+  if (!ms_out || !launches_out) return fail(IFVS_E_INVALID, "ms_out or launches_out is NULL");
+  for (int st = 0; st < kStages; ++st) {
+    ms_out[st] = 0.0;
+    launches_out[st] = 0;
+    if (!idx->timers) continue;
+    StageTimer& t = idx->timers[st];
+    if (ifvs_status e = flush_timer(t); e != IFVS_OK) return e;
+    ms_out[st] = t.ms;
+    launches_out[st] = t.launches;
+    t.ms = 0.0;
+    t.launches = 0;
+  }
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_last_plan(const ifvs_index* idx, int64_t* out4) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (!out4) return fail(IFVS_E_INVALID, "out4 is NULL");
+  out4[0] = idx->last_plan.qtile;
+  out4[1] = idx->last_plan.splits;
+  out4[2] = idx->last_plan.min_chunk;
+  out4[3] = static_cast<int64_t>(idx->last_plan.lds_bytes);
   return IFVS_OK;
 }
 

@@ -21,6 +21,12 @@ constexpr int kFilterQueries = 16;         // predicates evaluated per attribute
 // attributes: each kept clause tests (uint32)(attr - lo) < width, clauses that
 // admit every int32 value are dropped, and n_eff = -1 marks a predicate that
 // no value satisfies.
+//
+// On an index whose rows are clustered by attribute columns (c0 major, c1
+// minor), the clauses on the cluster key become one interval of rows
+// (iv_mode 1: c0 in [iv_lo0, iv_hi0); iv_mode 2: c0 == iv_lo0 and c1 in
+// [iv_lo1, iv_hi1)); iv_mode 0 is the whole index.  Effective clauses whose
+// bit is set in residual_mask are still tested row by row (selection bitmap).
 struct DevPred {
   int32_t n_raw;
   int32_t n_eff;
@@ -30,15 +36,33 @@ struct DevPred {
   int32_t col[kMaxClauses];
   int32_t lo[kMaxClauses];
   uint32_t width[kMaxClauses];
+  int32_t residual_mask;
+  int32_t iv_mode;
+  int64_t iv_lo0, iv_hi0, iv_lo1, iv_hi1;
 };
 
 // Kernel launchers (each defined next to its kernel).  All return the HIP
 // error of the launch.
-hipError_t launch_relayout_codes(const uint8_t* codes, int64_t n, int m, int mw,
+
+// Rows sorted by (attr[c0], attr[c1], id) as order-preserving 64-bit keys
+// (stable LSD radix sort): perm[row] = original id of physical row `row`.
+hipError_t cluster_permutation(const int32_t* attrs, int64_t n, int n_cluster, int c0, int c1,
+                               int32_t* perm, hipStream_t s);
+hipError_t launch_gather_attrs(const int32_t* attrs, int64_t n, int n_attr, const int32_t* perm,
+                               int32_t* attrs_phys, hipStream_t s);
+// Row interval [iv[2q], iv[2q+1]) of each query's cluster-key clauses.
+hipError_t launch_intervals(const int32_t* attrs_phys, int64_t n, int c0, int c1,
+                            const DevPred* preds, int nq, int64_t* iv, hipStream_t s);
+
+// codes (row-major [n][m]) -> 64-row tiles, physical row r taken from
+// original row perm[r] (perm may be null: identity).
+hipError_t launch_relayout_codes(const uint8_t* codes, int64_t n, int m, int mw, const int32_t* perm,
                                  uint32_t* codes_t, int64_t n_tiles, hipStream_t s);
 
+// Selection bitmaps; residual_only evaluates only the clauses in each
+// predicate's residual_mask.
 hipError_t launch_filter(const int32_t* attrs, int64_t n, int n_attr, const DevPred* preds,
-                         int nq, uint64_t* bitmap, int64_t stride64,
+                         int nq, bool residual_only, uint64_t* bitmap, int64_t stride64,
                          unsigned long long* counts, hipStream_t s);
 
 hipError_t launch_condition(const float* q, int dim, const DevPred* preds, int nq,
@@ -53,8 +77,8 @@ hipError_t launch_build_lut(const float* q, int dim, int m, int dsub, int r,
 struct ScanPlan {
   int qtile;        // queries sharing one LDS residency and one pass over the codes
   int splits;       // code chunks per query tile (grid.x)
-  int64_t tiles_per_block;
-  int pool_stride;  // candidate pool keys per (wave, query): 64*kpl >= k + 64
+  int min_chunk;    // fewest 64-row tiles per chunk
+  int pool_stride;  // candidate pool keys per (wave, query): >= k + 64
   int kpl;          // pool keys per lane when it is sorted
   size_t lds_bytes;
 };
@@ -64,13 +88,30 @@ int scan_max_qtile(int m, int lut_bytes, int k);
 // Round a requested tile down to one this build instantiates.
 int scan_supported_qtile(int want);
 int pool_kpl(int k);
+int pool_stride_for(int k);
 
-hipError_t launch_scan_dense(const uint32_t* codes_t, int64_t n_tiles, int m, int mw,
-                             const void* lut, int lut_dtype, int nq,
-                             const uint64_t* bitmap, int64_t stride64, int k,
-                             const ScanPlan& plan, uint64_t* partials, hipStream_t s);
+// Everything the scan needs about the batch.
+struct ScanBatch {
+  const uint32_t* codes_t;
+  int64_t n, n_tiles;
+  int m, mw;
+  const void* lut;              // [nq][m][256] by original query index
+  int lut_dtype;
+  int nq;
+  const int32_t* qorder;        // tile position -> original query index
+  const int64_t* iv;            // [nq][2] row interval per original query
+  const DevPred* preds;         // residual_mask per original query
+  const uint64_t* bitmap;       // [nq][stride64] physical-order selection words
+  int64_t stride64;
+  const int32_t* perm;          // physical row -> original id (null: identity)
+  int k;
+  uint64_t* partials;           // [nq positions][splits][waves][k]
+};
+
+hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s);
 
 hipError_t launch_topk_merge(const uint64_t* partials, int nq, int64_t per_query, int k,
-                             int32_t* ids_out, float* dist_out, hipStream_t s);
+                             const int32_t* qorder, int32_t* ids_out, float* dist_out,
+                             hipStream_t s);
 
 }  // namespace ifvs

@@ -3,11 +3,12 @@
 // selection bitmap, plus the pool size.
 //
 // One wavefront covers 4096 consecutive vectors: in step `it` (0..63) lane L
-// tests vector base + 64*it + L against up to kFilterQueries predicates; the
-// compare result of the wavefront is itself the 64-bit ballot word of those
-// 64 vectors, which lane `it` keeps.  After 64 steps every lane holds one
-// 64-bit word per query and the wavefront stores 512 contiguous bytes per
-// query.  Attribute values are read once per group of kFilterQueries queries.
+// tests vector base + 64*it + L; the compare result of the wavefront is
+// itself the 64-bit ballot word of those 64 vectors, which lane `it` keeps.
+// After 64 steps every lane holds one word and the wavefront stores 512
+// contiguous bytes.  A workgroup serves kFilterQueries predicates in turn
+// over the same 16 KB-per-column slice, so HBM reads each attribute value
+// once per group and the repeats hit L1.
 #include "ifvs_internal.h"
 
 namespace ifvs {
@@ -17,17 +18,10 @@ namespace {
 constexpr int kFilterWaves = 4;
 constexpr int kRowsPerWave = 64 * 64;
 
-__device__ __forceinline__ int32_t attr_value(const int32_t* __restrict__ attrs, int64_t n,
-                                              int col, int64_t i, int32_t a0, int32_t a1) {
-  if (col == 0) return a0;
-  if (col == 1) return a1;
-  return attrs[static_cast<int64_t>(col) * n + i];
-}
-
 __global__ __launch_bounds__(kFilterWaves * 64) void filter_kernel(
     const int32_t* __restrict__ attrs, int64_t n, int n_attr,
-    const DevPred* __restrict__ preds, int nq, uint64_t* __restrict__ bitmap, int64_t stride64,
-    unsigned long long* __restrict__ counts) {
+    const DevPred* __restrict__ preds, int nq, int residual_only, uint64_t* __restrict__ bitmap,
+    int64_t stride64, unsigned long long* __restrict__ counts) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int q0 = blockIdx.y * kFilterQueries;
@@ -35,47 +29,47 @@ __global__ __launch_bounds__(kFilterWaves * 64) void filter_kernel(
   const int64_t base = (static_cast<int64_t>(blockIdx.x) * kFilterWaves + wave) * kRowsPerWave;
   if (base >= n) return;
 
-  uint64_t held[kFilterQueries];
-#pragma unroll
-  for (int qi = 0; qi < kFilterQueries; ++qi) held[qi] = 0;
-
-  for (int it = 0; it < 64; ++it) {
-    const int64_t i = base + static_cast<int64_t>(it) * 64 + lane;
-    const bool in = i < n;
-    const int32_t a0 = (in && n_attr > 0) ? attrs[i] : 0;
-    const int32_t a1 = (in && n_attr > 1) ? attrs[n + i] : 0;
-#pragma unroll
-    for (int qi = 0; qi < kFilterQueries; ++qi) {
-      if (qi >= qn) break;
-      const DevPred& p = preds[q0 + qi];
-      bool pass = in && p.n_eff >= 0;
-      for (int c = 0; c < p.n_eff; ++c) {
-        const int32_t v = in ? attr_value(attrs, n, p.col[c], i, a0, a1) : 0;
+  const int64_t w64 = base / 64 + lane;           // this lane's 64-bit word
+  for (int qi = 0; qi < qn; ++qi) {
+    const DevPred& p = preds[q0 + qi];
+    const int n_eff = p.n_eff;
+    const int use = residual_only ? p.residual_mask : 0xF;
+    // Lane L keeps the ballot word of step L.
+    uint32_t held_lo = 0, held_hi = 0;
+#pragma unroll 8
+    for (int it = 0; it < 64; ++it) {
+      const int64_t i = base + static_cast<int64_t>(it) * 64 + lane;
+      const bool in = i < n;
+      bool pass = in && n_eff >= 0;
+      for (int c = 0; c < n_eff; ++c) {
+        if (!((use >> c) & 1)) continue;
+        const int64_t col = p.col[c];
+        const int32_t v = in ? attrs[col * n + i] : 0;
         pass = pass && (static_cast<uint32_t>(v) - static_cast<uint32_t>(p.lo[c]) < p.width[c]);
       }
       const uint64_t word = __ballot(pass);
-      if (lane == it) held[qi] = word;
+      const bool mine = lane == it;
+      held_lo = mine ? static_cast<uint32_t>(word) : held_lo;
+      held_hi = mine ? static_cast<uint32_t>(word >> 32) : held_hi;
     }
-  }
-
-  const int64_t w64 = base / 64 + lane;           // this lane's 64-bit word
+    const uint64_t word = (static_cast<uint64_t>(held_hi) << 32) | held_lo;
+    if (w64 < stride64) bitmap[static_cast<int64_t>(q0 + qi) * stride64 + w64] = word;
+    if (counts) {
+      unsigned long long c = __popcll(word);
 #pragma unroll
-  for (int qi = 0; qi < kFilterQueries; ++qi) {
-    if (qi >= qn) break;
-    if (w64 < stride64) bitmap[static_cast<int64_t>(q0 + qi) * stride64 + w64] = held[qi];
-    unsigned long long c = __popcll(held[qi]);
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) c += __shfl_down(c, off, 64);
-    if (lane == 0 && counts) atomicAdd(&counts[q0 + qi], c);
+      for (int off = 32; off > 0; off >>= 1) c += __shfl_down(c, off, 64);
+      if (lane == 0) atomicAdd(&counts[q0 + qi], c);
+    }
   }
 }
 
-// codes [n][m] bytes -> tiles of 64 rows: word j of row (64t + L) is stored at
-// codes_t[(t*mw + j)*64 + L] and holds bytes 4j..4j+3 of the row (zero past m
-// and past n), so a wavefront reading word j of a tile reads 256 contiguous
-// bytes.
+// codes [n][m] bytes -> tiles of 64 rows: word j of physical row (64t + L) is
+// stored at codes_t[(t*mw + j)*64 + L] and holds bytes 4j..4j+3 of original
+// row perm[64t + L] (zero past m and past n), so a wavefront reading word j of
+// a tile reads 256 contiguous bytes.
 __global__ void relayout_kernel(const uint8_t* __restrict__ codes, int64_t n, int m, int mw,
-                                uint32_t* __restrict__ codes_t, int64_t n_tiles) {
+                                const int32_t* __restrict__ perm, uint32_t* __restrict__ codes_t,
+                                int64_t n_tiles) {
   const int64_t total = n_tiles * mw * 64;
   for (int64_t o = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; o < total;
        o += static_cast<int64_t>(gridDim.x) * blockDim.x) {
@@ -85,9 +79,10 @@ __global__ void relayout_kernel(const uint8_t* __restrict__ codes, int64_t n, in
     const int64_t row = t * 64 + lane;
     uint32_t w = 0;
     if (row < n) {
+      const int64_t src = perm ? perm[row] : row;
       for (int b = 0; b < 4; ++b) {
         const int64_t col = j * 4 + b;
-        if (col < m) w |= static_cast<uint32_t>(codes[row * m + col]) << (8 * b);
+        if (col < m) w |= static_cast<uint32_t>(codes[src * m + col]) << (8 * b);
       }
     }
     codes_t[o] = w;
@@ -101,17 +96,17 @@ __global__ void zero_counts_kernel(unsigned long long* __restrict__ counts, int 
 
 }  // namespace
 
-hipError_t launch_relayout_codes(const uint8_t* codes, int64_t n, int m, int mw,
+hipError_t launch_relayout_codes(const uint8_t* codes, int64_t n, int m, int mw, const int32_t* perm,
                                  uint32_t* codes_t, int64_t n_tiles, hipStream_t s) {
   const int64_t total = n_tiles * mw * 64;
   const int64_t blocks = std::min<int64_t>((total + 255) / 256, 65536);
-  relayout_kernel<<<dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s>>>(codes, n, m, mw, codes_t,
-                                                                          n_tiles);
+  relayout_kernel<<<dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s>>>(codes, n, m, mw, perm,
+                                                                          codes_t, n_tiles);
   return hipGetLastError();
 }
 
 hipError_t launch_filter(const int32_t* attrs, int64_t n, int n_attr, const DevPred* preds,
-                         int nq, uint64_t* bitmap, int64_t stride64,
+                         int nq, bool residual_only, uint64_t* bitmap, int64_t stride64,
                          unsigned long long* counts, hipStream_t s) {
   const int64_t rows_per_block = static_cast<int64_t>(kFilterWaves) * kRowsPerWave;
   const int64_t gx = (n + rows_per_block - 1) / rows_per_block;
@@ -122,7 +117,7 @@ hipError_t launch_filter(const int32_t* attrs, int64_t n, int n_attr, const DevP
     if (e != hipSuccess) return e;
   }
   filter_kernel<<<dim3(static_cast<unsigned>(gx), gy), dim3(kFilterWaves * 64), 0, s>>>(
-      attrs, n, n_attr, preds, nq, bitmap, stride64, counts);
+      attrs, n, n_attr, preds, nq, residual_only ? 1 : 0, bitmap, stride64, counts);
   return hipGetLastError();
 }
 

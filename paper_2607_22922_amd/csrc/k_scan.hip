@@ -6,21 +6,26 @@
 // summed in m order from +0 with separately rounded fp32 additions.
 //
 // Workgroup = kScanWaves wavefronts; grid = (code chunks, query tiles).
-//  * The tables of QT queries live in LDS as [m][qi][256] so that, once a
-//    lane has turned its vector's M code bytes into M LDS addresses, the
+//  * A query tile is QT queries (taken in the planner's order).  Each query
+//    selects the rows of its interval [iv0, iv1) -- the whole index, or the
+//    rows its cluster-key clauses select on a clustered index -- and, when
+//    it has residual clauses, the rows set in its selection bitmap.  The
+//    tile's chunk of work is a slice of the union of its intervals.
+//  * The tables of the QT queries live in LDS as [m][qi][256] so that, once
+//    a lane has turned its vector's M code bytes into M LDS addresses, the
 //    same addresses serve every query of the tile (query qi adds a constant
 //    qi*256 that folds into the instruction's offset field).
 //  * Codes are stored in 64-row tiles ("word j of all 64 rows" contiguous),
 //    so each of the ceil(M/4) dword loads of a wavefront reads 256
-//    consecutive bytes.  A tile is loaded once and reused by all QT queries.
-//  * The selection bitmap supplies one 64-bit word per (query, tile): a zero
-//    word skips the tile for that query without touching the codes, and a
-//    tile no query selects is not loaded at all.
-//  * Each lane whose vector is selected sums its M table entries; the lanes
-//    beating the wavefront's current k-th best key are appended to that
-//    query's pool (ballot + prefix count), which is sorted and cut back to
-//    k keys whenever it would overflow.  At the end each wavefront writes its
-//    k best keys per query; a separate merge kernel reduces them.
+//    consecutive bytes; the next tile's words are loaded while the current
+//    one is being summed.  A tile is loaded once for all QT queries, and a
+//    tile no query selects is skipped without touching memory.
+//  * Each lane whose row is selected sums its M table entries; lanes beating
+//    the wavefront's current k-th best key are appended to that query's pool
+//    (ballot + prefix count), which is sorted and cut back to k keys when it
+//    would overflow.  Keys carry original vector ids (read for candidates
+//    only), so ties break by original id on any layout.  At the end each
+//    wavefront writes its k best keys per query; a merge kernel reduces them.
 #include "ifvs_internal.h"
 #include "topk_device.h"
 
@@ -31,15 +36,33 @@ namespace {
 __device__ __forceinline__ float widen(float v) { return v; }
 __device__ __forceinline__ float widen(__half v) { return __half2float(v); }
 
+struct ScanArgs {
+  const uint32_t* codes_t;
+  int64_t n, n_tiles;
+  int m, mw;
+  const void* lut;
+  int nq;
+  const int32_t* qorder;
+  const int64_t* iv;
+  const DevPred* preds;
+  const uint64_t* bitmap;
+  int64_t stride64;
+  const int32_t* perm;
+  int k, pool_stride, kpl, min_chunk;
+  uint64_t* partials;
+};
+
+// Bits [lo, hi) of a 64-bit word, 0 <= lo < hi <= 64.
+__device__ __forceinline__ uint64_t bit_range(int64_t lo, int64_t hi) {
+  const uint64_t upto_hi = hi >= 64 ? ~0ull : ((1ull << hi) - 1);
+  return upto_hi & ~((1ull << lo) - 1);
+}
+
 template <int MT, int QT, typename LutT>
-__global__ __launch_bounds__(kScanWaves * 64) void scan_dense_kernel(
-    const uint32_t* __restrict__ codes_t, int64_t n_tiles, int m_rt, int mw,
-    const LutT* __restrict__ lut, int nq, const uint64_t* __restrict__ bitmap,
-    int64_t stride64, int k, int pool_stride, int kpl, int64_t tiles_per_block,
-    uint64_t* __restrict__ partials) {
+__global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int kMW = MT > 0 ? (MT + 3) / 4 : 1;
-  const int M = MT > 0 ? MT : m_rt;
+  const int M = MT > 0 ? MT : a.m;
   LutT* slut = reinterpret_cast<LutT*>(smem);
   const size_t lut_bytes = static_cast<size_t>(M) * QT * kKsub * sizeof(LutT);
   uint64_t* pools = reinterpret_cast<uint64_t*>(smem + lut_bytes);
@@ -47,13 +70,56 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_dense_kernel(
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int q0 = blockIdx.y * QT;
-  const int qn = min(QT, nq - q0);
+  const int qn = min(QT, a.nq - q0);
+  const int k = a.k;
 
-  // Stage the query tile's tables: global [q][m][c] -> LDS [m][qi][c].
+  // The tile's queries, their row intervals, and the chunk of this workgroup.
+  int qid[QT];
+  int64_t r0[QT], r1[QT];
+  bool resid[QT];
+  int64_t hull_lo = INT64_MAX, hull_hi = 0;
+#pragma unroll
+  for (int qi = 0; qi < QT; ++qi) {
+    qid[qi] = 0;
+    r0[qi] = r1[qi] = 0;
+    resid[qi] = false;
+    if (qi < qn) {
+      qid[qi] = a.qorder[q0 + qi];
+      r0[qi] = a.iv[2 * qid[qi]];
+      r1[qi] = a.iv[2 * qid[qi] + 1];
+      resid[qi] = a.preds[qid[qi]].residual_mask != 0;
+      if (r1[qi] > r0[qi]) {
+        hull_lo = min(hull_lo, r0[qi]);
+        hull_hi = max(hull_hi, r1[qi]);
+      }
+    }
+  }
+  int64_t t_begin = 0, t_end = 0;
+  if (hull_hi > hull_lo) {
+    const int64_t t_lo = hull_lo / 64, t_hi = (hull_hi + 63) / 64;
+    const int64_t ch = max(static_cast<int64_t>(a.min_chunk), (t_hi - t_lo + gridDim.x - 1) / gridDim.x);
+    t_begin = t_lo + blockIdx.x * ch;
+    t_end = min(t_hi, t_begin + ch);
+  }
+  bool work = false;
+#pragma unroll
+  for (int qi = 0; qi < QT; ++qi)
+    work = work || (r1[qi] > r0[qi] && r0[qi] < t_end * 64 && r1[qi] > t_begin * 64);
+  if (!work) {
+    // Nothing selected in this chunk: empty partial lists.
+    for (int qi = 0; qi < qn; ++qi) {
+      uint64_t* dst = a.partials + ((static_cast<size_t>(q0 + qi) * gridDim.x + blockIdx.x) * kScanWaves + wave) * k;
+      for (int e = lane; e < k; e += 64) dst[e] = kNoKey;
+    }
+    return;
+  }
+
+  // Stage the tile's tables: global [q][m][c] -> LDS [m][qi][c].
   constexpr int kVec = 16 / sizeof(LutT);
   const int vec_per_query = M * kKsub / kVec;
+  const LutT* lut = static_cast<const LutT*>(a.lut);
   for (int qi = 0; qi < qn; ++qi) {
-    const uint4* src = reinterpret_cast<const uint4*>(lut + static_cast<size_t>(q0 + qi) * M * kKsub);
+    const uint4* src = reinterpret_cast<const uint4*>(lut + static_cast<size_t>(qid[qi]) * M * kKsub);
     for (int v = threadIdx.x; v < vec_per_query; v += kScanWaves * 64) {
       const int e = v * kVec;
       const int m = e / kKsub, c = e % kKsub;
@@ -69,25 +135,63 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_dense_kernel(
     cnt[qi] = 0;
     thr[qi] = kNoKey;
   }
-  uint64_t* my_pools = pools + static_cast<size_t>(wave) * QT * pool_stride;
+  uint64_t* my_pools = pools + static_cast<size_t>(wave) * QT * a.pool_stride;
 
-  const int64_t t_begin = static_cast<int64_t>(blockIdx.x) * tiles_per_block;
-  const int64_t t_end = min(n_tiles, t_begin + tiles_per_block);
-  for (int64_t t = t_begin + wave; t < t_end; t += kScanWaves) {
-    uint64_t bm[QT];
+  // Selection word of query qi for tile t: interval bits, and bitmap bits
+  // when the query has residual clauses.
+  auto tile_masks = [&](int64_t t, uint64_t (&bm)[QT]) -> uint64_t {
     uint64_t any = 0;
+    const int64_t row0 = t * 64;
 #pragma unroll
     for (int qi = 0; qi < QT; ++qi) {
-      bm[qi] = qi < qn ? bitmap[static_cast<size_t>(q0 + qi) * stride64 + t] : 0;
-      any |= bm[qi];
+      uint64_t mk = 0;
+      const int64_t lo = max(r0[qi] - row0, static_cast<int64_t>(0));
+      const int64_t hi = min(r1[qi] - row0, static_cast<int64_t>(64));
+      if (qi < qn && hi > lo) {
+        mk = bit_range(lo, hi);
+        if (resid[qi]) mk &= a.bitmap[static_cast<size_t>(qid[qi]) * a.stride64 + t];
+      }
+      bm[qi] = mk;
+      any |= mk;
     }
-    if (any == 0) continue;
-    const uint32_t id = static_cast<uint32_t>(t * 64 + lane);
+    return any;
+  };
 
-    if constexpr (MT > 0) {
-      uint32_t w[kMW];
+  auto consider = [&](int qi, bool act, float d, int64_t t) {
+    uint64_t key = kNoKey;
+    bool cand = false;
+    if (act) {
+      const uint32_t db = ordered_bits(d);
+      if (db <= static_cast<uint32_t>(thr[qi] >> 32)) {
+        const uint32_t row = static_cast<uint32_t>(t * 64 + lane);
+        const uint32_t id = a.perm ? static_cast<uint32_t>(a.perm[row]) : row;
+        key = (static_cast<uint64_t>(db) << 32) | id;
+        cand = key < thr[qi];
+      }
+    }
+    pool_push(my_pools + qi * a.pool_stride, cnt[qi], thr[qi], key, cand, k, a.kpl);
+  };
+
+  if constexpr (MT > 0) {
+    // Software pipeline: the next selected tile's code words are in flight
+    // while the current tile is summed.
+    int64_t t = t_begin + wave;
+    uint64_t bm[QT];
+    while (t < t_end && tile_masks(t, bm) == 0) t += kScanWaves;
+    uint32_t w[kMW];
+    if (t < t_end) {
 #pragma unroll
-      for (int j = 0; j < kMW; ++j) w[j] = codes_t[(t * kMW + j) * 64 + lane];
+      for (int j = 0; j < kMW; ++j) w[j] = a.codes_t[(t * kMW + j) * 64 + lane];
+    }
+    while (t < t_end) {
+      int64_t tn = t + kScanWaves;
+      uint64_t bmn[QT];
+      while (tn < t_end && tile_masks(tn, bmn) == 0) tn += kScanWaves;
+      uint32_t wn[kMW];
+      if (tn < t_end) {
+#pragma unroll
+        for (int j = 0; j < kMW; ++j) wn[j] = a.codes_t[(tn * kMW + j) * 64 + lane];
+      }
       int addr[MT];
 #pragma unroll
       for (int m = 0; m < MT; ++m)
@@ -96,35 +200,36 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_dense_kernel(
       for (int qi = 0; qi < QT; ++qi) {
         if (bm[qi] == 0) continue;
         const bool act = (bm[qi] >> lane) & 1ull;
-        uint64_t key = kNoKey;
-        bool cand = false;
+        float d = 0.0f;
         if (act) {
-          float d = 0.0f;
 #pragma unroll
           for (int m = 0; m < MT; ++m) d = __fadd_rn(d, widen(slut[addr[m] + qi * kKsub]));
-          key = make_key(d, id);
-          cand = key < thr[qi];
         }
-        pool_push(my_pools + qi * pool_stride, cnt[qi], thr[qi], key, cand, k, kpl);
+        consider(qi, act, d, t);
       }
-    } else {
+      t = tn;
+#pragma unroll
+      for (int qi = 0; qi < QT; ++qi) bm[qi] = bmn[qi];
+#pragma unroll
+      for (int j = 0; j < kMW; ++j) w[j] = wn[j];
+    }
+  } else {
+    for (int64_t t = t_begin + wave; t < t_end; t += kScanWaves) {
+      uint64_t bm[QT];
+      if (tile_masks(t, bm) == 0) continue;
 #pragma unroll
       for (int qi = 0; qi < QT; ++qi) {
         if (bm[qi] == 0) continue;
         const bool act = (bm[qi] >> lane) & 1ull;
-        uint64_t key = kNoKey;
-        bool cand = false;
+        float d = 0.0f;
         if (act) {
-          float d = 0.0f;
           for (int m = 0; m < M; ++m) {
-            const uint32_t wv = codes_t[(t * mw + (m >> 2)) * 64 + lane];
+            const uint32_t wv = a.codes_t[(t * a.mw + (m >> 2)) * 64 + lane];
             const int c = static_cast<int>((wv >> (8 * (m & 3))) & 0xFFu);
             d = __fadd_rn(d, widen(slut[(static_cast<size_t>(m) * QT + qi) * kKsub + c]));
           }
-          key = make_key(d, id);
-          cand = key < thr[qi];
         }
-        pool_push(my_pools + qi * pool_stride, cnt[qi], thr[qi], key, cand, k, kpl);
+        consider(qi, act, d, t);
       }
     }
   }
@@ -133,16 +238,16 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_dense_kernel(
 #pragma unroll
   for (int qi = 0; qi < QT; ++qi) {
     if (qi >= qn) break;
-    uint64_t* pool = my_pools + qi * pool_stride;
-    pool_compact(pool, cnt[qi], thr[qi], k, kpl);
-    uint64_t* dst = partials + ((static_cast<size_t>(q0 + qi) * gridDim.x + blockIdx.x) * kScanWaves + wave) * k;
+    uint64_t* pool = my_pools + qi * a.pool_stride;
+    pool_compact(pool, cnt[qi], thr[qi], k, a.kpl);
+    uint64_t* dst = a.partials + ((static_cast<size_t>(q0 + qi) * gridDim.x + blockIdx.x) * kScanWaves + wave) * k;
     for (int e = lane; e < k; e += 64) dst[e] = pool[e];
   }
 }
 
 template <int MT, int QT, typename LutT>
 const void* scan_symbol() {
-  return reinterpret_cast<const void*>(&scan_dense_kernel<MT, QT, LutT>);
+  return reinterpret_cast<const void*>(&scan_kernel<MT, QT, LutT>);
 }
 
 constexpr int kQtiles[] = {1, 2, 3, 4, 6, 8};
@@ -178,9 +283,16 @@ int pool_kpl(int k) {
   return kpl;
 }
 
+int pool_stride_for(int k) {
+  // Register-sorted pools need only k + 64 slots; pools sorted in LDS use the
+  // whole power of two.
+  const int kpl = pool_kpl(k);
+  return kpl <= 4 ? k + 64 : 64 * kpl;
+}
+
 int scan_max_qtile(int m, int lut_bytes, int k) {
   const size_t per_query = static_cast<size_t>(m) * kKsub * lut_bytes +
-                           static_cast<size_t>(kScanWaves) * 64 * pool_kpl(k) * sizeof(uint64_t);
+                           static_cast<size_t>(kScanWaves) * pool_stride_for(k) * sizeof(uint64_t);
   return static_cast<int>(kLdsBudget / per_query);
 }
 
@@ -191,24 +303,33 @@ int scan_supported_qtile(int want) {
   return best;
 }
 
-hipError_t launch_scan_dense(const uint32_t* codes_t, int64_t n_tiles, int m, int mw,
-                             const void* lut, int lut_dtype, int nq, const uint64_t* bitmap,
-                             int64_t stride64, int k, const ScanPlan& plan, uint64_t* partials,
-                             hipStream_t s) {
-  const void* fn = lut_dtype == 1 ? pick<__half>(m, plan.qtile) : pick<float>(m, plan.qtile);
+hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s) {
+  const void* fn = b.lut_dtype == 1 ? pick<__half>(b.m, plan.qtile) : pick<float>(b.m, plan.qtile);
   if (!fn) return hipErrorInvalidValue;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
                                      static_cast<int>(plan.lds_bytes));
   if (e != hipSuccess) return e;
-  const dim3 grid(plan.splits, (nq + plan.qtile - 1) / plan.qtile);
-  int m_arg = m, mw_arg = mw, nq_arg = nq, k_arg = k, ps = plan.pool_stride, kpl = plan.kpl;
-  int64_t nt = n_tiles, st = stride64, tpb = plan.tiles_per_block;
-  const uint32_t* c_arg = codes_t;
-  const void* l_arg = lut;
-  const uint64_t* b_arg = bitmap;
-  uint64_t* p_arg = partials;
-  void* args[] = {&c_arg, &nt, &m_arg, &mw_arg, &l_arg, &nq_arg, &b_arg, &st,
-                  &k_arg, &ps,  &kpl,   &tpb,    &p_arg};
+  ScanArgs a{};
+  a.codes_t = b.codes_t;
+  a.n = b.n;
+  a.n_tiles = b.n_tiles;
+  a.m = b.m;
+  a.mw = b.mw;
+  a.lut = b.lut;
+  a.nq = b.nq;
+  a.qorder = b.qorder;
+  a.iv = b.iv;
+  a.preds = b.preds;
+  a.bitmap = b.bitmap;
+  a.stride64 = b.stride64;
+  a.perm = b.perm;
+  a.k = b.k;
+  a.pool_stride = plan.pool_stride;
+  a.kpl = plan.kpl;
+  a.min_chunk = plan.min_chunk;
+  a.partials = b.partials;
+  const dim3 grid(plan.splits, (b.nq + plan.qtile - 1) / plan.qtile);
+  void* args[] = {&a};
   return hipLaunchKernel(fn, grid, dim3(kScanWaves * 64), args, plan.lds_bytes, s);
 }
 

@@ -15,14 +15,16 @@ namespace {
 
 __global__ __launch_bounds__(64) void topk_merge_kernel(const uint64_t* __restrict__ partials,
                                                         int64_t per_query, int k, int kpl,
+                                                        const int32_t* __restrict__ qorder,
                                                         int32_t* __restrict__ ids_out,
                                                         float* __restrict__ dist_out) {
   extern __shared__ uint64_t pool[];
-  const int q = blockIdx.x;
+  const int pos = blockIdx.x;                 // position in the scan's query order
+  const int q = qorder ? qorder[pos] : pos;   // original query index
   const int lane = threadIdx.x;
   int cnt = 0;
   uint64_t thr = kNoKey;
-  const uint64_t* src = partials + static_cast<size_t>(q) * per_query;
+  const uint64_t* src = partials + static_cast<size_t>(pos) * per_query;
   for (int64_t b = 0; b < per_query; b += 64) {
     const int64_t i = b + lane;
     const uint64_t key = i < per_query ? src[i] : kNoKey;
@@ -45,10 +47,12 @@ __global__ __launch_bounds__(64) void topk_merge_kernel(const uint64_t* __restri
 }  // namespace
 
 hipError_t launch_topk_merge(const uint64_t* partials, int nq, int64_t per_query, int k,
-                             int32_t* ids_out, float* dist_out, hipStream_t s) {
+                             const int32_t* qorder, int32_t* ids_out, float* dist_out,
+                             hipStream_t s) {
   const int kpl = pool_kpl(k);
   const size_t lds = static_cast<size_t>(64 * kpl) * sizeof(uint64_t);
-  topk_merge_kernel<<<dim3(nq), dim3(64), lds, s>>>(partials, per_query, k, kpl, ids_out, dist_out);
+  topk_merge_kernel<<<dim3(nq), dim3(64), lds, s>>>(partials, per_query, k, kpl, qorder, ids_out,
+                                                    dist_out);
   return hipGetLastError();
 }
 

@@ -23,11 +23,12 @@ LUT_F32, LUT_F16 = 0, 1
 KSUB = 256
 MAX_CLAUSES = 4
 MAX_K = 1024
-OPT_QTILE, OPT_SPLITS = 1, 2
+OPT_QTILE, OPT_SPLITS, OPT_PROFILE = 1, 2, 3
+STAGES = ("condition", "lut", "filter", "scan", "merge")
 
 EXPORTED = ("ifvs_load_index", "ifvs_free_index", "ifvs_select_codebook", "ifvs_build_lut",
-            "ifvs_filter", "ifvs_filtered_search", "ifvs_set_option", "ifvs_get_plan",
-            "ifvs_last_error")
+            "ifvs_filter", "ifvs_filtered_search", "ifvs_set_option", "ifvs_last_plan",
+            "ifvs_read_profile", "ifvs_last_error")
 
 
 class IfvsError(RuntimeError):
@@ -55,6 +56,8 @@ class IndexDesc(ctypes.Structure):
         ("W", ctypes.c_void_p),
         ("max_batch", ctypes.c_int32),
         ("max_k", ctypes.c_int32),
+        ("n_cluster", ctypes.c_int32),
+        ("cluster_col", ctypes.c_int32 * 2),
     ]
 
 
@@ -82,7 +85,8 @@ def _load_library() -> ctypes.CDLL:
         "ifvs_filter": ([vp, i32, vp, vp, vp, vp], i32),
         "ifvs_filtered_search": ([vp, i32, vp, vp, i32, i32, vp, vp, vp, vp], i32),
         "ifvs_set_option": ([vp, i32, i64], i32),
-        "ifvs_get_plan": ([vp, i32, i32, i32, ctypes.POINTER(ctypes.c_int64)], i32),
+        "ifvs_last_plan": ([vp, ctypes.POINTER(ctypes.c_int64)], i32),
+        "ifvs_read_profile": ([vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)], i32),
         "ifvs_last_error": ([], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -137,7 +141,7 @@ class Index:
     """A PQ-quantized dataset resident on one GPU (ifvs_load_index)."""
 
     def __init__(self, codes, C_pq, attrs=None, bank=None, W=None, r=0, h=0, hash_seed=0,
-                 max_batch=256, max_k=100):
+                 max_batch=256, max_k=100, cluster_cols=()):
         codes = codes.contiguous()
         device = codes.device
         self.mem_kind = MEM_DEVICE if device.type == "cuda" else MEM_HOST
@@ -159,6 +163,9 @@ class Index:
         d.mem_kind = self.mem_kind
         d.bank, d.W = _ptr(bk), _ptr(Wt)
         d.max_batch, d.max_k = int(max_batch), int(max_k)
+        d.n_cluster = len(cluster_cols)
+        for i, c in enumerate(cluster_cols):
+            d.cluster_col[i] = int(c)
         handle = ctypes.c_void_p()
         _check(_lib.ifvs_load_index(ctypes.byref(d), ctypes.byref(handle)))
         self._keep = None
@@ -170,10 +177,10 @@ class Index:
         self.device = torch.device("cuda", torch.cuda.current_device())
 
     @classmethod
-    def from_workload(cls, w, max_batch=256, max_k=None, conditioned=True):
+    def from_workload(cls, w, max_batch=256, max_k=None, conditioned=True, cluster_cols=()):
         return cls(w.codes, w.C_pq, w.attrs, w.bank if conditioned else None,
                    w.W if conditioned else None, w.r, w.h, w.hash_seed,
-                   max_batch=max_batch, max_k=max_k or w.k)
+                   max_batch=max_batch, max_k=max_k or w.k, cluster_cols=cluster_cols)
 
     def close(self):
         if getattr(self, "handle", None) is not None and self.handle.value:
@@ -190,10 +197,18 @@ class Index:
     def set_option(self, option: int, value: int) -> None:
         _check(_lib.ifvs_set_option(self.handle, option, int(value)))
 
-    def plan(self, nq: int, k: int, lut_dtype: int = LUT_F32) -> dict:
+    def last_plan(self) -> dict:
+        """Launch plan of the most recent filtered_search on this index."""
         out = (ctypes.c_int64 * 4)()
-        _check(_lib.ifvs_get_plan(self.handle, nq, k, lut_dtype, out))
-        return dict(qtile=out[0], splits=out[1], tiles_per_block=out[2], lds_bytes=out[3])
+        _check(_lib.ifvs_last_plan(self.handle, out))
+        return dict(qtile=out[0], splits=out[1], min_chunk=out[2], lds_bytes=out[3])
+
+    def read_profile(self) -> dict:
+        """Per-stage (total kernel ms, launches) since the last read."""
+        ms = (ctypes.c_double * len(STAGES))()
+        n = (ctypes.c_int64 * len(STAGES))()
+        _check(_lib.ifvs_read_profile(self.handle, ms, n))
+        return {name: (ms[i], n[i]) for i, name in enumerate(STAGES)}
 
     def select_codebook_into(self, q, preds_c, w_z, alpha_out, wf_out, stream=None):
         _check(_lib.ifvs_select_codebook(self.handle, q.shape[0], q.data_ptr(), preds_c,

@@ -64,7 +64,7 @@ def test_binding_mirrors_header_structs(tmp_path):
     text = open(HEADER).read()
     body = text[text.index("typedef struct {\n  int64_t n;"):text.index("} ifvs_index_desc;")]
     body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
-    assert [f[0] for f in B.IndexDesc._fields_] == re.findall(r"\b\**\s*([a-zA-Z_]+);", body)
+    assert [f[0] for f in B.IndexDesc._fields_] == re.findall(r"\b\**\s*([a-zA-Z_]+)(?:\[\d+\])?;", body)
     assert set(B.EXPORTED) == set(declared_functions())
 
 

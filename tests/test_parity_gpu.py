@@ -121,11 +121,11 @@ def test_end_to_end_c1_from_raw_inputs(B, c1, conditioned):
 
 # -------------------------------------------------------------- edge cases
 def _edge_index(B, N, M, dsub, n_attr=2, domain=50, seed=0, conditioned=True, max_k=128,
-                max_batch=64):
+                max_batch=64, cluster_cols=()):
     ix = random_index(N, M, dsub, n_attr, domain, seed, device="cuda")
     idx = B.Index(ix["codes"], ix["C_pq"], ix["attrs"], ix["bank"] if conditioned else None,
                   ix["W"] if conditioned else None, ix["r"], ix["h"], ix["hash_seed"],
-                  max_batch=max_batch, max_k=max_k)
+                  max_batch=max_batch, max_k=max_k, cluster_cols=cluster_cols)
     ox = oracle_index(ix["codes"], ix["C_pq"], ix["attrs"], ix["bank"] if conditioned else None,
                       ix["W"] if conditioned else None, ix["r"], ix["h"], ix["hash_seed"])
     return idx, ox
@@ -223,3 +223,73 @@ def test_repeat_calls_are_deterministic(B, c1):
         outs.append((_np(ids), _np(dist).view(np.uint32)))
     for o in outs[1:]:
         assert np.array_equal(o[0], outs[0][0]) and np.array_equal(o[1], outs[0][1])
+
+
+# ------------------------------------------------- clustered physical layout
+@pytest.mark.parametrize("conditioned", [True, False])
+def test_clustered_c1_matches_oracle(B, conditioned):
+    """Rows stored in attribute order: same ids and distances as the oracle."""
+    say("[clustered] c1")
+    w = make_workload("c1", device="cuda")
+    idx = B.Index.from_workload(w, max_batch=128, max_k=16, cluster_cols=(0,))
+    ox = oracle_from_workload(w)
+    s = 0.1
+    alpha, wf = idx.select_codebook(w.queries, w.preds[s], w.w_z[s])
+    lut = idx.build_lut(w.queries, alpha if conditioned else None, wf)
+    ids, dist, bm = idx.search(w.preds[s], lut, w.k, want_bitmap=True)
+    torch.cuda.synchronize()
+    assert idx.last_plan()["qtile"] == 1
+    ids, dist, bm = _np(ids), _np(dist), _np(bm).view(np.uint32)
+    for i, p in enumerate(w.preds[s]):
+        res = O.filtered_search(ox, _np(w.queries[i]), p, w.k, w_z=_np(w.w_z[s][i]),
+                                conditioned=conditioned)
+        assert np.array_equal(bm[i], O.selection_bitmap(res["mask"]))
+        check_search_row(ids[i], dist[i], res["ids"], res["dist"], f"q{i}")
+
+
+@pytest.mark.parametrize("cols", [(0,), (1, 0), (0, 1), (2,)])
+def test_clustered_predicate_shapes(B, cols):
+    """Range, equality + range, rank prefix + range, residual clauses on other
+    columns, predicates that miss the cluster key, contradictions."""
+    say(f"[clustered] cols={cols}")
+    idx, ox = _edge_index(B, 40_000, 16, 8, n_attr=3, domain=30, seed=31, cluster_cols=cols)
+    preds = [
+        [(0, 3, 9)], [(1, 7, 8), (0, 2, 20)], [(1, 0, 5), (0, 4, 25)], [(0, 5, 6), (1, 5, 6)],
+        [(2, 1, 4)], [(2, 0, 10), (1, 3, 12), (0, 0, 28)], [], [(0, 9, 9)], [(0, 3, 9), (0, 10, 20)],
+        [(1, -(1 << 40), 1 << 40), (0, 29, 1 << 50)], [(0, 0, 30), (0, 12, 13), (1, 2, 3)],
+        [(1, 4, 5), (0, 17, 18), (2, 2, 29)],
+    ] * 2
+    _run_and_check(B, idx, ox, preds, k=10, dsub=8, M=16)
+    _run_and_check(B, idx, ox, preds, k=100, dsub=8, M=16, seed=2)
+
+
+def test_clustered_ties_break_by_original_id(B):
+    ix = random_index(6000, 16, 8, 1, 40, 41, device="cuda")
+    ix["codes"][::7] = ix["codes"][3]                 # equal rows in every cluster
+    idx = B.Index(ix["codes"], ix["C_pq"], ix["attrs"], max_batch=8, max_k=200, cluster_cols=(0,))
+    ox = oracle_index(ix["codes"], ix["C_pq"], ix["attrs"])
+    rec = ix["C_pq"][torch.arange(16, device="cuda"), ix["codes"][3].long()].reshape(-1)
+    q = rec[None].repeat(3, 1).contiguous()
+    preds = [[], [(0, 10, 30)], [(0, 5, 6)]]
+    lut = idx.build_lut(q)
+    ids, dist = idx.search(preds, lut, 200)
+    torch.cuda.synchronize()
+    for i, p in enumerate(preds):
+        res = O.filtered_search(ox, _np(q[i]), p, 200, conditioned=False)
+        check_search_row(_np(ids[i]), _np(dist[i]), res["ids"], res["dist"], f"ties q{i}")
+
+
+def test_clustered_and_plain_layouts_agree_on_c4_sample(B):
+    """A 1M-row slice of the 10M-vector workload: both layouts, every bin."""
+    say("[clustered] c4 slice")
+    w = make_workload("c4", device="cuda", N=1_000_000, n_queries=64, keep_x=False)
+    plain = B.Index.from_workload(w, max_batch=64, max_k=10)
+    clus = B.Index.from_workload(w, max_batch=64, max_k=10, cluster_cols=(0,))
+    for s in w.bins:
+        a, f = plain.select_codebook(w.queries, w.preds[s], w.w_z[s])
+        lut = plain.build_lut(w.queries, a, f)
+        i1, d1 = plain.search(w.preds[s], lut, 10)
+        i2, d2 = clus.search(w.preds[s], lut, 10)
+        torch.cuda.synchronize()
+        assert torch.equal(i1, i2), s
+        assert torch.equal(d1.view(torch.int32), d2.view(torch.int32)), s
