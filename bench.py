@@ -182,7 +182,10 @@ def main():
 
     def timed_run(idx, steps):
         """W warmup steps, then `steps` timed steps; every kernel timed with
-        HIP events on this stream.  Returns (total ms, per-bin [(b, ms)], profile, plans)."""
+        HIP events on this stream.  Within the timed region the bins run one
+        after another (each bin's `steps` batches together) so the kernel
+        profile can be read per bin.  Returns (total ms, per-bin [(b, ms)],
+        per-bin profile, whole profile, plans)."""
         for i in range(args.warmup):
             for s in bins:
                 run_batch(idx, s, i % n_batches)
@@ -190,27 +193,29 @@ def main():
         idx.set_option(B.OPT_PROFILE, 1)
         idx.read_profile()
         ev = {s: [] for s in bins}
-        plans = {}
+        prof_bin, plans = {}, {}
         torch.cuda.synchronize()
         start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         start.record(stream)
-        for i in range(steps):
-            b = (args.warmup + i) % n_batches
-            for s in bins:
+        for s in bins:
+            for i in range(steps):
+                b = (args.warmup + i) % n_batches
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 e0.record(stream)
                 run_batch(idx, s, b)
                 e1.record(stream)
                 ev[s].append((b, e0, e1))
-                plans[s] = idx.last_plan()
+            plans[s] = idx.last_plan()
+            prof_bin[s] = idx.read_profile()           # waits for this bin's kernels
         stop.record(stream)
         torch.cuda.synchronize()
         total = start.elapsed_time(stop)
-        prof = idx.read_profile()
         idx.set_option(B.OPT_PROFILE, 0)
-        return total, {s: [(b, a.elapsed_time(c)) for b, a, c in ev[s]] for s in bins}, prof, plans
+        prof = {st: (sum(prof_bin[s][st][0] for s in bins), sum(prof_bin[s][st][1] for s in bins))
+                for st in prof_bin[bins[0]]}
+        return total, {s: [(b, a.elapsed_time(c)) for b, a, c in ev[s]] for s in bins}, prof_bin, prof, plans
 
-    total_ms, per_bin, prof, plans = timed_run(clus, args.steps)
+    total_ms, per_bin, prof_bin, prof, plans = timed_run(clus, args.steps)
     n_queries = args.steps * len(bins) * batch
     qps = n_queries / (total_ms / 1e3)
     log(f"[bench] clustered: {args.steps} steps in {total_ms:.1f} ms -> {qps:.0f} queries/s")
@@ -229,9 +234,17 @@ def main():
             useful_total += cache[b][1]
         ms = [m for _, m in per_bin[s]]
         sel = float(np.mean([v[1] / (w.M * w.N * batch) for v in cache.values()]))
+        b_ms, b_n = prof_bin[s]["scan"]
+        b_bytes = sum(cache[b][0] for b, _ in per_bin[s]) / max(1, b_n)
+        b_gbps = b_bytes / (b_ms / max(1, b_n) / 1e3) / 1e9
         bins_out[str(s)] = {"qps": batch * len(ms) / (sum(ms) / 1e3),
                             "ms_per_batch": float(np.median(ms)),
                             "realized_selectivity": round(sel, 5),
+                            "scan_ms": round(b_ms / max(1, b_n), 4),
+                            "scan_GBps": round(b_gbps, 1),
+                            "scan_frac_of_hbm_peak": round(b_gbps / HBM_PEAK_GBPS, 4),
+                            "stage_ms_per_launch": {st: round(v[0] / max(1, v[1]), 4)
+                                                   for st, v in prof_bin[s].items()},
                             "plan": plans[s]}
     scan_ms, scan_launches = prof["scan"]
     scan_avg_ms = scan_ms / max(1, scan_launches)
@@ -242,7 +255,7 @@ def main():
 
     plain_out = None
     if plain is not None:
-        p_total, p_bins, p_prof, p_plans = timed_run(plain, args.plain_steps)
+        p_total, p_bins, _, p_prof, p_plans = timed_run(plain, args.plain_steps)
         p_bytes = 0.0
         for s in bins:
             cache = {}
@@ -273,7 +286,7 @@ def main():
     # Recall@k of the identity mode (alpha = 0, w_f = 1: plain PQ ADC) and of
     # the synthetic conditioned mode, against exact filtered kNN.
     nr = min(args.recall_queries, batch)
-    for s in bins:
+    for s in (bins if nr > 0 else []):
         q = w.queries[:nr]
         preds = w.preds[s][:nr]
         gt, _ = exact_filtered_knn(w.x, w.attrs, q, preds, k)

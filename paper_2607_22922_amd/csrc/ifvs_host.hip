@@ -65,6 +65,8 @@ struct StageTimer {
   int64_t launches = 0;
 };
 
+constexpr int kFences = 4096;
+
 constexpr int64_t kI32Min = std::numeric_limits<int32_t>::min();
 constexpr int64_t kI32End = int64_t(std::numeric_limits<int32_t>::max()) + 1;
 
@@ -103,7 +105,12 @@ struct ifvs_index {
   uint64_t* partials = nullptr;  // per-wavefront top-k keys
   size_t partial_keys = 0;
 
-  int opt_qtile = 0, opt_splits = 0;
+  // Every (n / kFences)-th clustered key, copied to the host at load: lets
+  // the planner estimate each query's interval length without touching the
+  // device.
+  std::vector<int32_t> fence0, fence1;
+
+  int opt_qtile = 0, opt_splits = 0, opt_min_chunk = 0;
   bool profile = false;
   StageTimer* timers = nullptr;  // [kStages] once profiling was enabled
   ScanPlan last_plan{};
@@ -245,6 +252,30 @@ ifvs_status normalize_predicates(const ifvs_index* idx, int32_t nq, const ifvs_p
   return IFVS_OK;
 }
 
+// Estimated 64-row tiles of a query's cluster-key interval, from the fences
+// (exact to within two fence gaps).
+int64_t estimate_interval_tiles(const ifvs_index* idx, const DevPred& d) {
+  const auto& f0 = idx->fence0;
+  const auto& f1 = idx->fence1;
+  const int64_t nf = static_cast<int64_t>(f0.size());
+  if (d.n_eff < 0 || nf == 0) return 0;
+  if (d.iv_mode == 0) return idx->n_tiles;
+  auto rank = [&](int64_t x0, int64_t x1) {      // fences below (x0, x1)
+    int64_t lo = 0, hi = nf;
+    while (lo < hi) {
+      const int64_t mid = (lo + hi) / 2;
+      const bool below = d.iv_mode == 2 && f0[mid] == x0 ? f1[mid] < x1 : f0[mid] < x0;
+      if (below) lo = mid + 1;
+      else hi = mid;
+    }
+    return lo;
+  };
+  const int64_t r0 = d.iv_mode == 2 ? rank(d.iv_lo0, d.iv_lo1) : rank(d.iv_lo0, 0);
+  const int64_t r1 = d.iv_mode == 2 ? rank(d.iv_lo0, d.iv_hi1) : rank(d.iv_hi0, 0);
+  const int64_t rows = (r1 - r0 + 1) * idx->n / (nf - 1);
+  return std::min<int64_t>(idx->n_tiles, rows / 64 + 1);
+}
+
 // Copy validated predicates (and the scan's query order, when asked) to the
 // device through a pinned staging slot.
 ifvs_status stage_predicates(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
@@ -317,7 +348,7 @@ ifvs_status timed(ifvs_index* idx, int stage, hipStream_t s, const char* what, F
 // code tiles across queries would not help.  Otherwise (masked rows) tiles
 // of several queries share each pass over the codes.
 ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_dtype,
-                      bool interval_batch, ScanPlan* plan) {
+                      bool interval_batch, int64_t span_tiles, ScanPlan* plan) {
   const int lut_bytes = lut_dtype == IFVS_LUT_F16 ? 2 : 4;
   const int qmax = scan_max_qtile(idx->m, lut_bytes, k);
   if (qmax < 1)
@@ -329,9 +360,17 @@ ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_
   want = std::min(want, qmax);
   plan->qtile = std::max(1, scan_supported_qtile(want));
   const int64_t gy = (std::max(1, nq) + plan->qtile - 1) / plan->qtile;
-  plan->min_chunk = 16;
-  // Enough workgroups to fill 256 CUs several times.
-  int64_t splits = idx->opt_splits > 0 ? idx->opt_splits : (4096 + gy - 1) / gy;
+  // Interval scans: at least 8 tiles per wavefront per chunk, so the table
+  // staged into LDS is amortized over >= 512 rows.
+  plan->min_chunk = idx->opt_min_chunk > 0 ? idx->opt_min_chunk : (interval_batch ? 8 * kScanWaves : 16);
+  // Masked scans: enough workgroups to fill 256 CUs several times.  Interval
+  // scans: chunks of about 4096 tiles (measured best between 1K and 5K
+  // tiles per 8-wavefront workgroup), at least ~512 workgroups, at most 16
+  // chunks per query tile.
+  int64_t splits = (4096 + gy - 1) / gy;
+  if (interval_batch)
+    splits = std::min<int64_t>(16, std::max<int64_t>((span_tiles + 4095) / 4096, (512 + gy - 1) / gy));
+  if (idx->opt_splits > 0) splits = idx->opt_splits;
   splits = std::min<int64_t>(splits, std::max<int64_t>(1, (idx->n_tiles + plan->min_chunk - 1) / plan->min_chunk));
   const int64_t cap = static_cast<int64_t>(idx->partial_keys /
                                            (static_cast<size_t>(std::max(1, nq)) * kScanWaves * k));
@@ -437,6 +476,17 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
     idx->attrs_phys = phys;
     if (hipError_t e = launch_gather_attrs(idx->attrs, d.n, d.n_attr, idx->perm, phys, nullptr); e != hipSuccess)
       return bail(hip_fail(e, "gathering clustered attributes"));
+    // Host copy of every (n / kFences)-th clustered key (planner statistics).
+    std::vector<int32_t> col(static_cast<size_t>(d.n));
+    for (int c = 0; c < d.n_cluster; ++c) {
+      if (hipError_t e = hipMemcpy(col.data(), phys + static_cast<int64_t>(d.cluster_col[c]) * d.n,
+                                   sizeof(int32_t) * d.n, hipMemcpyDeviceToHost);
+          e != hipSuccess)
+        return bail(hip_fail(e, "reading cluster keys"));
+      auto& f = c == 0 ? idx->fence0 : idx->fence1;
+      f.resize(kFences + 1);
+      for (int i = 0; i <= kFences; ++i) f[i] = col[std::min<int64_t>(d.n - 1, static_cast<int64_t>(i) * d.n / kFences)];
+    }
   }
   // codes -> 64-row tiles (in physical order)
   {
@@ -508,6 +558,7 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
   switch (option) {
     case IFVS_OPT_QTILE: idx->opt_qtile = static_cast<int>(value); return IFVS_OK;
     case IFVS_OPT_SPLITS: idx->opt_splits = static_cast<int>(value); return IFVS_OK;
+    case IFVS_OPT_MIN_CHUNK: idx->opt_min_chunk = static_cast<int>(value); return IFVS_OK;
     case IFVS_OPT_PROFILE:
       if (value != 0 && !idx->timers) {
         idx->timers = new StageTimer[kStages];
@@ -584,19 +635,21 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   if (!lut || !ids_out || !dist_out) return fail(IFVS_E_INVALID, "lut, ids_out or dist_out is NULL");
   if (reinterpret_cast<uintptr_t>(lut) % 16 != 0) return fail(IFVS_E_INVALID, "lut must be 16-byte aligned");
   ScanPlan probe{};
-  if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, false, &probe); st != IFVS_OK) return st;
+  if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, false, 0, &probe); st != IFVS_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
   DevPred* host = nullptr;
   // Predicates are validated before anything is enqueued.
   if (ifvs_status st = stage_predicates(idx, nq, preds, true, s, &host); st != IFVS_OK) return st;
   bool need_bitmap = false, interval_batch = true;
+  int64_t span = 0;
   for (int i = 0; i < nq; ++i) {
     need_bitmap = need_bitmap || host[i].residual_mask != 0;
     interval_batch = interval_batch && host[i].iv_mode != 0;
+    if (idx->n_cluster > 0) span = std::max(span, estimate_interval_tiles(idx, host[i]));
   }
   ScanPlan plan{};
-  if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, interval_batch, &plan); st != IFVS_OK) return st;
+  if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, interval_batch, span, &plan); st != IFVS_OK) return st;
   IFVS_LAUNCH(idx, kStFilter, s, "launching interval kernel",
               launch_intervals(idx->attrs_phys, idx->n, idx->c0, idx->c1, idx->preds_dev, nq, idx->iv_dev, s));
   if (need_bitmap)

@@ -12,7 +12,7 @@ constexpr int kKsub = 256;
 constexpr int kMaxClauses = 4;
 constexpr int kTileRows = 64;              // vectors per code tile = one wavefront
 constexpr int kLdsBudget = 160 * 1024;     // LDS bytes per workgroup on gfx950
-constexpr int kScanWaves = 4;              // wavefronts per scan workgroup
+constexpr int kScanWaves = 8;              // wavefronts per scan workgroup
 constexpr int kFilterQueries = 16;         // predicates evaluated per attribute read
 
 // A predicate as the device sees it.  The raw fields are the caller's clauses

@@ -39,42 +39,61 @@ __global__ void gather_attrs_kernel(const int32_t* __restrict__ attrs, int64_t n
   }
 }
 
-// First row whose (c0, c1) key is >= (x0, x1) (x1 ignored when c1 < 0).
-__device__ int64_t lower_bound_rows(const int32_t* __restrict__ a0, const int32_t* __restrict__ a1,
-                                    int64_t n, int64_t x0, int64_t x1) {
-  int64_t lo = 0, hi = n;
-  while (lo < hi) {
-    const int64_t mid = lo + ((hi - lo) >> 1);
-    const int64_t v0 = a0[mid];
-    bool less = v0 < x0;
-    if (a1 && v0 == x0) less = static_cast<int64_t>(a1[mid]) < x1;
-    if (less) lo = mid + 1;
-    else hi = mid;
-  }
-  return lo;
+// (c0, c1) key of row r is below (x0, x1)?  (x1 ignored when a1 is null.)
+__device__ __forceinline__ bool key_below(const int32_t* __restrict__ a0, const int32_t* __restrict__ a1,
+                                          int64_t r, int64_t x0, int64_t x1) {
+  const int64_t v0 = a0[r];
+  if (a1 && v0 == x0) return static_cast<int64_t>(a1[r]) < x1;
+  return v0 < x0;
 }
 
-__global__ void intervals_kernel(const int32_t* __restrict__ attrs_phys, int64_t n, int c0, int c1,
-                                 const DevPred* __restrict__ preds, int nq, int64_t* __restrict__ iv) {
-  const int q = blockIdx.x * blockDim.x + threadIdx.x;
+// First row whose key is >= (x0, x1): a 64-ary search by one wavefront.
+// Each step every lane probes one of 64 evenly spaced rows of the current
+// range [lo, hi); the ballot of "probe below x" narrows the range to the gap
+// after the last such probe, so 10^7 rows take four dependent loads.
+__device__ int64_t wave_lower_bound(const int32_t* __restrict__ a0, const int32_t* __restrict__ a1,
+                                    int64_t n, int64_t x0, int64_t x1) {
+  const int lane = threadIdx.x & 63;
+  int64_t lo = 0, hi = n;               // answer in [lo, hi]
+  while (hi - lo > 64) {
+    const int64_t step = (hi - lo + 63) / 64;
+    const int64_t r = lo + lane * step; // probes lo, lo+step, ... (< hi or past it)
+    const bool below = r < hi && key_below(a0, a1, r, x0, x1);
+    const uint64_t mask = __ballot(below);
+    if (mask == 0) {
+      hi = lo;                           // key(lo) >= x
+    } else {
+      const int last = 63 - __clzll(mask);
+      const int64_t r_last = lo + last * step;
+      lo = r_last + 1;
+      hi = min(hi, r_last + step);
+    }
+  }
+  // Final <= 64 rows: one probe per lane.
+  const int64_t r = lo + lane;
+  const bool below = r < hi && key_below(a0, a1, r, x0, x1);
+  return lo + __popcll(__ballot(below));
+}
+
+__global__ __launch_bounds__(64) void intervals_kernel(const int32_t* __restrict__ attrs_phys, int64_t n,
+                                                       int c0, int c1, const DevPred* __restrict__ preds,
+                                                       int nq, int64_t* __restrict__ iv) {
+  const int q = blockIdx.x >> 1;        // two wavefronts per query: lower and upper bound
+  const bool upper = blockIdx.x & 1;
   if (q >= nq) return;
   const DevPred& p = preds[q];
-  int64_t r0 = 0, r1 = n;
+  int64_t r = upper ? n : 0;
   if (p.n_eff < 0) {
-    r0 = r1 = 0;
+    r = 0;
   } else if (p.iv_mode == 1) {
     const int32_t* a0 = attrs_phys + static_cast<int64_t>(c0) * n;
-    r0 = lower_bound_rows(a0, nullptr, n, p.iv_lo0, 0);
-    r1 = lower_bound_rows(a0, nullptr, n, p.iv_hi0, 0);
+    r = wave_lower_bound(a0, nullptr, n, upper ? p.iv_hi0 : p.iv_lo0, 0);
   } else if (p.iv_mode == 2) {
     const int32_t* a0 = attrs_phys + static_cast<int64_t>(c0) * n;
     const int32_t* a1 = attrs_phys + static_cast<int64_t>(c1) * n;
-    r0 = lower_bound_rows(a0, a1, n, p.iv_lo0, p.iv_lo1);
-    r1 = lower_bound_rows(a0, a1, n, p.iv_lo0, p.iv_hi1);
+    r = wave_lower_bound(a0, a1, n, p.iv_lo0, upper ? p.iv_hi1 : p.iv_lo1);
   }
-  if (r1 < r0) r1 = r0;
-  iv[2 * q] = r0;
-  iv[2 * q + 1] = r1;
+  if (threadIdx.x == 0) iv[2 * q + (upper ? 1 : 0)] = r;
 }
 
 unsigned grid_for(int64_t work) { return static_cast<unsigned>(std::min<int64_t>((work + 255) / 256, 65536)); }
@@ -121,7 +140,7 @@ hipError_t launch_gather_attrs(const int32_t* attrs, int64_t n, int n_attr, cons
 
 hipError_t launch_intervals(const int32_t* attrs_phys, int64_t n, int c0, int c1,
                             const DevPred* preds, int nq, int64_t* iv, hipStream_t s) {
-  intervals_kernel<<<dim3((nq + 63) / 64), dim3(64), 0, s>>>(attrs_phys, n, c0, c1, preds, nq, iv);
+  intervals_kernel<<<dim3(2 * nq), dim3(64), 0, s>>>(attrs_phys, n, c0, c1, preds, nq, iv);
   return hipGetLastError();
 }
 

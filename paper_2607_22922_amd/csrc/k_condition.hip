@@ -32,10 +32,13 @@ __device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
   return z ^ (z >> 31);
 }
 
+constexpr int kMaxDim = 4096;
+
 __global__ __launch_bounds__(64) void condition_kernel(
     const float* __restrict__ q, int dim, const DevPred* __restrict__ preds,
     const float* __restrict__ bank, int bank_rows, int mr, int h, uint64_t seed,
     const float* __restrict__ w_z, float* __restrict__ alpha_out, float* __restrict__ wf_out) {
+  __shared__ uint32_t qbits[kMaxDim];
   const int qi = blockIdx.x;
   const int lane = threadIdx.x;
   const float* qrow = q + static_cast<int64_t>(qi) * dim;
@@ -52,11 +55,14 @@ __global__ __launch_bounds__(64) void condition_kernel(
   if (bank_rows <= 0 || alpha_out == nullptr) return;
 
   // Fingerprint: FNV-1a-64 over q's fp32 bytes, the clause count (int32) and
-  // every clause as (col int32, lo int64, hi int64), little-endian.
+  // every clause as (col int32, lo int64, hi int64), little-endian.  The
+  // row is staged in LDS by all lanes; the fold itself is serial.
+  for (int i = lane; i < dim; i += 64) qbits[i] = __float_as_uint(qrow[i]);
+  __syncthreads();
   uint64_t key = 0;
   if (lane == 0) {
     uint64_t hh = kFnvOffset;
-    for (int i = 0; i < dim; ++i) hh = fnv_bytes(hh, __float_as_uint(qrow[i]), 4);
+    for (int i = 0; i < dim; ++i) hh = fnv_bytes(hh, qbits[i], 4);
     const DevPred& p = preds[qi];
     hh = fnv_bytes(hh, static_cast<uint32_t>(p.n_raw), 4);
     for (int c = 0; c < p.n_raw; ++c) {

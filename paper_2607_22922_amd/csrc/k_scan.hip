@@ -42,6 +42,7 @@ struct ScanArgs {
   int m, mw;
   const void* lut;
   int nq;
+  int splits, n_qtiles;
   const int32_t* qorder;
   const int64_t* iv;
   const DevPred* preds;
@@ -69,7 +70,11 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int q0 = blockIdx.y * QT;
+  // Chunk-major grid: consecutive workgroups (which the dispatcher deals
+  // round-robin to the 8 XCDs) take the same chunk of different query tiles,
+  // so sparse work spreads over every XCD and empty chunks come last.
+  const int chunk = blockIdx.x / a.n_qtiles;
+  const int q0 = (blockIdx.x % a.n_qtiles) * QT;
   const int qn = min(QT, a.nq - q0);
   const int k = a.k;
 
@@ -97,8 +102,8 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
   int64_t t_begin = 0, t_end = 0;
   if (hull_hi > hull_lo) {
     const int64_t t_lo = hull_lo / 64, t_hi = (hull_hi + 63) / 64;
-    const int64_t ch = max(static_cast<int64_t>(a.min_chunk), (t_hi - t_lo + gridDim.x - 1) / gridDim.x);
-    t_begin = t_lo + blockIdx.x * ch;
+    const int64_t ch = max(static_cast<int64_t>(a.min_chunk), (t_hi - t_lo + a.splits - 1) / a.splits);
+    t_begin = t_lo + chunk * ch;
     t_end = min(t_hi, t_begin + ch);
   }
   bool work = false;
@@ -108,7 +113,7 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
   if (!work) {
     // Nothing selected in this chunk: empty partial lists.
     for (int qi = 0; qi < qn; ++qi) {
-      uint64_t* dst = a.partials + ((static_cast<size_t>(q0 + qi) * gridDim.x + blockIdx.x) * kScanWaves + wave) * k;
+      uint64_t* dst = a.partials + ((static_cast<size_t>(q0 + qi) * a.splits + chunk) * kScanWaves + wave) * k;
       for (int e = lane; e < k; e += 64) dst[e] = kNoKey;
     }
     return;
@@ -240,7 +245,7 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
     if (qi >= qn) break;
     uint64_t* pool = my_pools + qi * a.pool_stride;
     pool_compact(pool, cnt[qi], thr[qi], k, a.kpl);
-    uint64_t* dst = a.partials + ((static_cast<size_t>(q0 + qi) * gridDim.x + blockIdx.x) * kScanWaves + wave) * k;
+    uint64_t* dst = a.partials + ((static_cast<size_t>(q0 + qi) * a.splits + chunk) * kScanWaves + wave) * k;
     for (int e = lane; e < k; e += 64) dst[e] = pool[e];
   }
 }
@@ -328,7 +333,9 @@ hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s) 
   a.kpl = plan.kpl;
   a.min_chunk = plan.min_chunk;
   a.partials = b.partials;
-  const dim3 grid(plan.splits, (b.nq + plan.qtile - 1) / plan.qtile);
+  a.splits = plan.splits;
+  a.n_qtiles = (b.nq + plan.qtile - 1) / plan.qtile;
+  const dim3 grid(static_cast<unsigned>(a.splits) * static_cast<unsigned>(a.n_qtiles));
   void* args[] = {&a};
   return hipLaunchKernel(fn, grid, dim3(kScanWaves * 64), args, plan.lds_bytes, s);
 }

@@ -23,7 +23,7 @@ LUT_F32, LUT_F16 = 0, 1
 KSUB = 256
 MAX_CLAUSES = 4
 MAX_K = 1024
-OPT_QTILE, OPT_SPLITS, OPT_PROFILE = 1, 2, 3
+OPT_QTILE, OPT_SPLITS, OPT_PROFILE, OPT_MIN_CHUNK = 1, 2, 3, 4
 STAGES = ("condition", "lut", "filter", "scan", "merge")
 
 EXPORTED = ("ifvs_load_index", "ifvs_free_index", "ifvs_select_codebook", "ifvs_build_lut",
