@@ -94,6 +94,7 @@ struct ifvs_index {
   DevPred* preds_dev = nullptr;  // [max_batch]
   int32_t* qorder_dev = nullptr; // [max_batch]
   int64_t* iv_dev = nullptr;     // [max_batch][2]
+  uint64_t* gthr_dev = nullptr;  // [max_batch] shared scan thresholds
   DevPred* staging[kStagingSlots] = {};   // pinned: [max_batch] DevPred + [max_batch] int32
   hipEvent_t staged[kStagingSlots] = {};
   bool slot_busy[kStagingSlots] = {};
@@ -128,7 +129,7 @@ struct ifvs_index {
     for (void* p : {static_cast<void*>(codes_t), static_cast<void*>(cpq), static_cast<void*>(attrs),
                     static_cast<void*>(perm), static_cast<void*>(bank), static_cast<void*>(W),
                     static_cast<void*>(preds_dev), static_cast<void*>(qorder_dev),
-                    static_cast<void*>(iv_dev), static_cast<void*>(bitmap),
+                    static_cast<void*>(iv_dev), static_cast<void*>(gthr_dev), static_cast<void*>(bitmap),
                     static_cast<void*>(counts), static_cast<void*>(partials)})
       if (p) hipFree(p);
     for (int i = 0; i < kStagingSlots; ++i) {
@@ -523,6 +524,8 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
   if ((st = dev_alloc(&idx->qorder_dev, d.max_batch, "query order")) != IFVS_OK) return bail(st);
   if ((st = dev_alloc(&idx->iv_dev, 2 * static_cast<size_t>(d.max_batch), "row intervals")) != IFVS_OK)
     return bail(st);
+  if ((st = dev_alloc(&idx->gthr_dev, static_cast<size_t>(d.max_batch), "scan thresholds")) != IFVS_OK)
+    return bail(st);
   for (int i = 0; i < kStagingSlots; ++i) {
     const size_t bytes = (sizeof(DevPred) + sizeof(int32_t)) * d.max_batch;
     if (forced_alloc_failure() ||
@@ -651,7 +654,8 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   ScanPlan plan{};
   if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, interval_batch, span, &plan); st != IFVS_OK) return st;
   IFVS_LAUNCH(idx, kStFilter, s, "launching interval kernel",
-              launch_intervals(idx->attrs_phys, idx->n, idx->c0, idx->c1, idx->preds_dev, nq, idx->iv_dev, s));
+              launch_intervals(idx->attrs_phys, idx->n, idx->c0, idx->c1, idx->preds_dev, nq, idx->iv_dev,
+                               idx->gthr_dev, s));
   if (need_bitmap)
     if (ifvs_status st = filter_into_workspace(idx, nq, true, false, s); st != IFVS_OK) return st;
   ScanBatch b{};
@@ -671,6 +675,7 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   b.perm = idx->perm;
   b.k = k;
   b.partials = idx->partials;
+  b.gthr = idx->gthr_dev;
   IFVS_LAUNCH(idx, kStScan, s, "launching scan kernel", launch_scan(b, plan, s));
   const int64_t per_query = static_cast<int64_t>(plan.splits) * kScanWaves * k;
   IFVS_LAUNCH(idx, kStMerge, s, "launching top-k merge kernel",

@@ -51,8 +51,10 @@ hipError_t cluster_permutation(const int32_t* attrs, int64_t n, int n_cluster, i
 hipError_t launch_gather_attrs(const int32_t* attrs, int64_t n, int n_attr, const int32_t* perm,
                                int32_t* attrs_phys, hipStream_t s);
 // Row interval [iv[2q], iv[2q+1]) of each query's cluster-key clauses.
+// Also resets each query's shared scan threshold gthr[q] to all ones.
 hipError_t launch_intervals(const int32_t* attrs_phys, int64_t n, int c0, int c1,
-                            const DevPred* preds, int nq, int64_t* iv, hipStream_t s);
+                            const DevPred* preds, int nq, int64_t* iv, uint64_t* gthr,
+                            hipStream_t s);
 
 // codes (row-major [n][m]) -> 64-row tiles, physical row r taken from
 // original row perm[r] (perm may be null: identity).
@@ -106,6 +108,7 @@ struct ScanBatch {
   const int32_t* perm;          // physical row -> original id (null: identity)
   int k;
   uint64_t* partials;           // [nq positions][splits][waves][k]
+  uint64_t* gthr;               // [nq] shared thresholds, all-ones before the scan
 };
 
 hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s);

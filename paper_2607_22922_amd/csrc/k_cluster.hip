@@ -77,7 +77,8 @@ __device__ int64_t wave_lower_bound(const int32_t* __restrict__ a0, const int32_
 
 __global__ __launch_bounds__(64) void intervals_kernel(const int32_t* __restrict__ attrs_phys, int64_t n,
                                                        int c0, int c1, const DevPred* __restrict__ preds,
-                                                       int nq, int64_t* __restrict__ iv) {
+                                                       int nq, int64_t* __restrict__ iv,
+                                                       uint64_t* __restrict__ gthr) {
   const int q = blockIdx.x >> 1;        // two wavefronts per query: lower and upper bound
   const bool upper = blockIdx.x & 1;
   if (q >= nq) return;
@@ -93,7 +94,10 @@ __global__ __launch_bounds__(64) void intervals_kernel(const int32_t* __restrict
     const int32_t* a1 = attrs_phys + static_cast<int64_t>(c1) * n;
     r = wave_lower_bound(a0, a1, n, p.iv_lo0, upper ? p.iv_hi1 : p.iv_lo1);
   }
-  if (threadIdx.x == 0) iv[2 * q + (upper ? 1 : 0)] = r;
+  if (threadIdx.x == 0) {
+    iv[2 * q + (upper ? 1 : 0)] = r;
+    if (!upper) gthr[q] = ~0ull;
+  }
 }
 
 unsigned grid_for(int64_t work) { return static_cast<unsigned>(std::min<int64_t>((work + 255) / 256, 65536)); }
@@ -139,8 +143,9 @@ hipError_t launch_gather_attrs(const int32_t* attrs, int64_t n, int n_attr, cons
 }
 
 hipError_t launch_intervals(const int32_t* attrs_phys, int64_t n, int c0, int c1,
-                            const DevPred* preds, int nq, int64_t* iv, hipStream_t s) {
-  intervals_kernel<<<dim3(2 * nq), dim3(64), 0, s>>>(attrs_phys, n, c0, c1, preds, nq, iv);
+                            const DevPred* preds, int nq, int64_t* iv, uint64_t* gthr,
+                            hipStream_t s) {
+  intervals_kernel<<<dim3(2 * nq), dim3(64), 0, s>>>(attrs_phys, n, c0, c1, preds, nq, iv, gthr);
   return hipGetLastError();
 }
 

@@ -20,10 +20,13 @@
 //    consecutive bytes; the next tile's words are loaded while the current
 //    one is being summed.  A tile is loaded once for all QT queries, and a
 //    tile no query selects is skipped without touching memory.
-//  * Each lane whose row is selected sums its M table entries; lanes beating
-//    the wavefront's current k-th best key are appended to that query's pool
-//    (ballot + prefix count), which is sorted and cut back to k keys when it
-//    would overflow.  Keys carry original vector ids (read for candidates
+//  * Each lane whose row is selected sums its M table entries in groups and
+//    drops out as soon as its partial sum exceeds the wavefront's current
+//    k-th distance (all entries are squares times non-negative weights, so
+//    partial sums only grow; checked per query when its table is staged).
+//    Lanes beating the current k-th best key are appended to that query's
+//    pool (ballot + prefix count), which is sorted and cut back to k keys
+//    when it would overflow.  Keys carry original vector ids (read for candidates
 //    only), so ties break by original id on any layout.  At the end each
 //    wavefront writes its k best keys per query; a merge kernel reduces them.
 #include "ifvs_internal.h"
@@ -51,6 +54,7 @@ struct ScanArgs {
   const int32_t* perm;
   int k, pool_stride, kpl, min_chunk;
   uint64_t* partials;
+  uint64_t* gthr;   // [nq] per original query: smallest k-th key any wavefront has published
 };
 
 // Bits [lo, hi) of a 64-bit word, 0 <= lo < hi <= 64.
@@ -119,19 +123,39 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
     return;
   }
 
-  // Stage the tile's tables: global [q][m][c] -> LDS [m][qi][c].
+  // Stage the tile's tables: global [q][m][c] -> LDS [m][qi][c], noting any
+  // entry that is negative or NaN (then partial sums are no lower bound).
+  __shared__ uint32_t s_not_monotone[QT];
+  __shared__ unsigned long long s_thr[QT];   // smallest k-th key published in this workgroup
+  if (threadIdx.x < QT) {
+    s_not_monotone[threadIdx.x] = 0;
+    s_thr[threadIdx.x] = kNoKey;
+  }
+  __syncthreads();
   constexpr int kVec = 16 / sizeof(LutT);
   const int vec_per_query = M * kKsub / kVec;
   const LutT* lut = static_cast<const LutT*>(a.lut);
   for (int qi = 0; qi < qn; ++qi) {
     const uint4* src = reinterpret_cast<const uint4*>(lut + static_cast<size_t>(qid[qi]) * M * kKsub);
+    bool bad = false;
     for (int v = threadIdx.x; v < vec_per_query; v += kScanWaves * 64) {
       const int e = v * kVec;
       const int m = e / kKsub, c = e % kKsub;
-      *reinterpret_cast<uint4*>(slut + (static_cast<size_t>(m) * QT + qi) * kKsub + c) = src[v];
+      const uint4 x = src[v];
+      *reinterpret_cast<uint4*>(slut + (static_cast<size_t>(m) * QT + qi) * kKsub + c) = x;
+      const LutT* xe = reinterpret_cast<const LutT*>(&x);
+#pragma unroll
+      for (int u = 0; u < kVec; ++u) bad = bad || !(widen(xe[u]) >= 0.0f);
     }
+    if (bad) atomicOr(&s_not_monotone[qi], 1u);
   }
   __syncthreads();
+  // Early abandonment: every entry >= 0 and fp32 addition of non-negative
+  // terms never decreases, so a partial sum above the current k-th distance
+  // bounds the full sum from below and the row cannot enter the top k.
+  bool monotone[QT];
+#pragma unroll
+  for (int qi = 0; qi < QT; ++qi) monotone[qi] = qi < qn && s_not_monotone[qi] == 0;
 
   int cnt[QT];
   uint64_t thr[QT];
@@ -162,22 +186,52 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
     return any;
   };
 
+  // Thresholds.  thr[qi] is the k-th smallest key of this wavefront's own
+  // pool.  Any wavefront's k-th key also bounds the query's answer (k smaller
+  // keys exist), so each wavefront publishes its threshold to the workgroup
+  // (LDS) and to the query (global memory) and filters with the smallest
+  // one it knows: bound[qi] = min(own, workgroup, query).  A row whose key is
+  // not below the bound cannot be among the query's k best.
+  uint64_t published[QT], gview[QT], bound[QT];
+#pragma unroll
+  for (int qi = 0; qi < QT; ++qi) published[qi] = gview[qi] = bound[qi] = kNoKey;
+  int tiles_seen = 0;
+  auto refresh_bounds = [&]() {
+    const bool read_global = (tiles_seen++ & 7) == 0;
+#pragma unroll
+    for (int qi = 0; qi < QT; ++qi) {
+      if (qi >= qn) continue;
+      if (read_global) gview[qi] = __hip_atomic_load(a.gthr + qid[qi], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const uint64_t blk = s_thr[qi];
+      uint64_t b = thr[qi] < blk ? thr[qi] : blk;
+      bound[qi] = b < gview[qi] ? b : gview[qi];
+    }
+  };
+
   auto consider = [&](int qi, bool act, float d, int64_t t) {
     uint64_t key = kNoKey;
     bool cand = false;
     if (act) {
       const uint32_t db = ordered_bits(d);
-      if (db <= static_cast<uint32_t>(thr[qi] >> 32)) {
+      if (db <= static_cast<uint32_t>(bound[qi] >> 32)) {
         const uint32_t row = static_cast<uint32_t>(t * 64 + lane);
         const uint32_t id = a.perm ? static_cast<uint32_t>(a.perm[row]) : row;
         key = (static_cast<uint64_t>(db) << 32) | id;
-        cand = key < thr[qi];
+        cand = key < bound[qi];
       }
     }
     pool_push(my_pools + qi * a.pool_stride, cnt[qi], thr[qi], key, cand, k, a.kpl);
+    if (thr[qi] < published[qi]) {
+      published[qi] = thr[qi];
+      if (lane == 0) {
+        atomicMin(&s_thr[qi], static_cast<unsigned long long>(thr[qi]));
+        __hip_atomic_fetch_min(a.gthr + qid[qi], thr[qi], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
   };
 
   if constexpr (MT > 0) {
+    constexpr int kGroup = MT % 8 == 0 && MT > 16 ? 8 : (MT % 4 == 0 ? 4 : MT);
     // Software pipeline: the next selected tile's code words are in flight
     // while the current tile is summed.
     int64_t t = t_begin + wave;
@@ -197,6 +251,7 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
 #pragma unroll
         for (int j = 0; j < kMW; ++j) wn[j] = a.codes_t[(tn * kMW + j) * 64 + lane];
       }
+      refresh_bounds();
       int addr[MT];
 #pragma unroll
       for (int m = 0; m < MT; ++m)
@@ -204,13 +259,23 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
 #pragma unroll
       for (int qi = 0; qi < QT; ++qi) {
         if (bm[qi] == 0) continue;
-        const bool act = (bm[qi] >> lane) & 1ull;
+        // Subspaces are summed in groups; after each group a lane whose
+        // partial sum already exceeds the k-th distance drops out (NaN cut
+        // before k candidates exist: nothing drops).
+        const float cut = monotone[qi] ? from_ordered_bits(static_cast<uint32_t>(bound[qi] >> 32))
+                                       : __builtin_nanf("");
+        bool live = (bm[qi] >> lane) & 1ull;
         float d = 0.0f;
-        if (act) {
 #pragma unroll
-          for (int m = 0; m < MT; ++m) d = __fadd_rn(d, widen(slut[addr[m] + qi * kKsub]));
+        for (int g = 0; g < MT / kGroup; ++g) {
+          if (live) {
+#pragma unroll
+            for (int u = 0; u < kGroup; ++u)
+              d = __fadd_rn(d, widen(slut[addr[g * kGroup + u] + qi * kKsub]));
+          }
+          live = live && !(d > cut);
         }
-        consider(qi, act, d, t);
+        consider(qi, live, d, t);
       }
       t = tn;
 #pragma unroll
@@ -222,6 +287,7 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
     for (int64_t t = t_begin + wave; t < t_end; t += kScanWaves) {
       uint64_t bm[QT];
       if (tile_masks(t, bm) == 0) continue;
+      refresh_bounds();
 #pragma unroll
       for (int qi = 0; qi < QT; ++qi) {
         if (bm[qi] == 0) continue;
@@ -333,6 +399,7 @@ hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s) 
   a.kpl = plan.kpl;
   a.min_chunk = plan.min_chunk;
   a.partials = b.partials;
+  a.gthr = b.gthr;
   a.splits = plan.splits;
   a.n_qtiles = (b.nq + plan.qtile - 1) / plan.qtile;
   const dim3 grid(static_cast<unsigned>(a.splits) * static_cast<unsigned>(a.n_qtiles));

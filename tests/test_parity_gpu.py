@@ -293,3 +293,25 @@ def test_clustered_and_plain_layouts_agree_on_c4_sample(B):
         torch.cuda.synchronize()
         assert torch.equal(i1, i2), s
         assert torch.equal(d1.view(torch.int32), d2.view(torch.int32)), s
+
+
+@pytest.mark.parametrize("cluster_cols", [(), (0,)])
+def test_negative_weights_rank_exactly(B, cluster_cols):
+    """Caller-supplied weights may be negative: table entries and distances
+    go negative, partial sums stop being lower bounds, and the ranking must
+    still match the oracle bit for bit."""
+    idx, ox = _edge_index(B, 20_000, 48, 2, seed=77, cluster_cols=cluster_cols)
+    g = torch.Generator(device="cuda").manual_seed(5)
+    preds = [[(0, 0, 40)], [(0, 10, 20)], [(1, 5, 45)], []] * 2
+    q = torch.randn(len(preds), 96, device="cuda", generator=g)
+    wf = torch.randn(len(preds), 96, device="cuda", generator=g)          # mixed signs
+    alpha, _ = idx.select_codebook(q, preds, None)
+    lut = idx.build_lut(q, alpha, wf)
+    ids, dist = idx.search(preds, lut, 25)
+    torch.cuda.synchronize()
+    for i, p in enumerate(preds):
+        lut_o = O.build_lut(_np(q[i]), _np(alpha[i]), _np(wf[i]), ox["C_pq"], ox["W"], 48, ox["r"])
+        cand = O.passing_ids(O.predicate_mask(ox["attrs"], p))
+        ids_o, dist_o = O.select_topk(O.adc_distances(lut_o, ox["codes"], cand), cand, 25)
+        check_search_row(_np(ids[i]), _np(dist[i]), ids_o, dist_o, f"neg q{i}")
+    assert (dist < 0).any()
