@@ -365,12 +365,12 @@ ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_
   // staged into LDS is amortized over >= 512 rows.
   plan->min_chunk = idx->opt_min_chunk > 0 ? idx->opt_min_chunk : (interval_batch ? 8 * kScanWaves : 16);
   // Masked scans: enough workgroups to fill 256 CUs several times.  Interval
-  // scans: chunks of about 4096 tiles (measured best between 1K and 5K
+  // scans: chunks of about 8192 tiles (measured best between 2K and 8K
   // tiles per 8-wavefront workgroup), at least ~512 workgroups, at most 16
   // chunks per query tile.
   int64_t splits = (4096 + gy - 1) / gy;
   if (interval_batch)
-    splits = std::min<int64_t>(16, std::max<int64_t>((span_tiles + 4095) / 4096, (512 + gy - 1) / gy));
+    splits = std::min<int64_t>(16, std::max<int64_t>((span_tiles + 8191) / 8192, (512 + gy - 1) / gy));
   if (idx->opt_splits > 0) splits = idx->opt_splits;
   splits = std::min<int64_t>(splits, std::max<int64_t>(1, (idx->n_tiles + plan->min_chunk - 1) / plan->min_chunk));
   const int64_t cap = static_cast<int64_t>(idx->partial_keys /

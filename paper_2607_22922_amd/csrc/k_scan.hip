@@ -36,6 +36,8 @@ namespace ifvs {
 
 namespace {
 
+constexpr int kXcds = 8;   // accelerator complex dies of an MI355X
+
 __device__ __forceinline__ float widen(float v) { return v; }
 __device__ __forceinline__ float widen(__half v) { return __half2float(v); }
 
@@ -74,11 +76,19 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  // Chunk-major grid: consecutive workgroups (which the dispatcher deals
-  // round-robin to the 8 XCDs) take the same chunk of different query tiles,
-  // so sparse work spreads over every XCD and empty chunks come last.
-  const int chunk = blockIdx.x / a.n_qtiles;
-  const int q0 = (blockIdx.x % a.n_qtiles) * QT;
+  // XCD-aware grid.  The dispatcher deals workgroups round-robin to the 8
+  // XCDs (workgroup b runs on XCD b % 8).  Each XCD gets a contiguous run of
+  // query tiles -- the planner orders queries by interval, so neighbours
+  // read nearly the same rows and share that XCD's L2 -- and walks it chunk
+  // by chunk: chunk c of all its query tiles, then chunk c + 1, so every XCD
+  // has work and empty chunks come last.
+  const int xcd = blockIdx.x % kXcds;
+  const int slot = blockIdx.x / kXcds;
+  const int per_xcd = (a.n_qtiles + kXcds - 1) / kXcds;
+  const int chunk = slot / per_xcd;
+  const int qtile = xcd * per_xcd + slot % per_xcd;
+  if (qtile >= a.n_qtiles || chunk >= a.splits) return;   // grid padding
+  const int q0 = qtile * QT;
   const int qn = min(QT, a.nq - q0);
   const int k = a.k;
 
@@ -402,7 +412,8 @@ hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s) 
   a.gthr = b.gthr;
   a.splits = plan.splits;
   a.n_qtiles = (b.nq + plan.qtile - 1) / plan.qtile;
-  const dim3 grid(static_cast<unsigned>(a.splits) * static_cast<unsigned>(a.n_qtiles));
+  const unsigned per_xcd = static_cast<unsigned>((a.n_qtiles + kXcds - 1) / kXcds);
+  const dim3 grid(static_cast<unsigned>(kXcds) * per_xcd * static_cast<unsigned>(a.splits));
   void* args[] = {&a};
   return hipLaunchKernel(fn, grid, dim3(kScanWaves * 64), args, plan.lds_bytes, s);
 }
