@@ -248,6 +248,14 @@ ifvs_status normalize_predicates(const ifvs_index* idx, int32_t nq, const ifvs_p
       if (!covered) resid |= 1 << c;
     }
     d.residual_mask = d.n_eff < 0 ? 0 : resid;
+    d.n_res = 0;
+    for (int c = 0; c < n_eff; ++c) {
+      if (!((d.residual_mask >> c) & 1)) continue;
+      d.res_col[d.n_res] = d.col[c];
+      d.res_lo[d.n_res] = d.lo[c];
+      d.res_width[d.n_res] = d.width[c];
+      ++d.n_res;
+    }
     out[i] = d;
   }
   return IFVS_OK;

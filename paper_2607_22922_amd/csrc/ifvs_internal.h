@@ -39,6 +39,11 @@ struct DevPred {
   int32_t residual_mask;
   int32_t iv_mode;
   int64_t iv_lo0, iv_hi0, iv_lo1, iv_hi1;
+  // The residual clauses alone, packed (n_res of them), in the same form.
+  int32_t n_res;
+  int32_t res_col[kMaxClauses];
+  int32_t res_lo[kMaxClauses];
+  uint32_t res_width[kMaxClauses];
 };
 
 // Kernel launchers (each defined next to its kernel).  All return the HIP
