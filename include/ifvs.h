@@ -199,12 +199,18 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
 /* Tuning knobs, never needed for correctness.  IFVS_OPT_QTILE forces the
  * number of queries whose tables share one LDS residency and one pass over
  * the codes (0 = automatic); IFVS_OPT_SPLITS forces the number of code chunks
- * a query tile is cut into (0 = automatic).
+ * a query tile is cut into (0 = automatic).  IFVS_OPT_GRID_TILES forces the
+ * chunk grid of clustered-index scans (0 = automatic: a grid of about 5120
+ * tiles when the widest interval spans 8192 or more 64-row tiles, else none):
+ * chunk c of a query tile is then grid cell (first cell of its span) + c,
+ * and a span needing more cells than there are chunks is cut into equal
+ * chunks instead.  Results never depend on these knobs.
  * Errors: IFVS_E_INVALID for an unknown option or a negative value. */
 #define IFVS_OPT_QTILE  1
 #define IFVS_OPT_SPLITS 2
 #define IFVS_OPT_PROFILE 3        /* 1: time every kernel launch with HIP events (see below) */
 #define IFVS_OPT_MIN_CHUNK 4      /* fewest 64-row code tiles per chunk (0 = automatic)      */
+#define IFVS_OPT_GRID_TILES 5     /* chunk grid cell in 64-row tiles (0 = automatic)         */
 ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value);
 
 /* ifvs_read_profile -- with IFVS_OPT_PROFILE on, every kernel the index
@@ -218,12 +224,13 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value);
 ifvs_status ifvs_read_profile(ifvs_index* idx, double* ms_out, int64_t* launches_out);
 
 /* ifvs_last_plan -- the launch plan of the most recent ifvs_filtered_search
- * on this index (all zero before the first): out4[0] queries per tile
- * (tables sharing one LDS residency and one pass over the codes), out4[1]
- * code chunks per query tile, out4[2] fewest 64-row code tiles per chunk,
- * out4[3] LDS bytes per workgroup.  For measurement and tests.
- * Errors: IFVS_E_INVALID (NULL out4), IFVS_E_STATE. */
-ifvs_status ifvs_last_plan(const ifvs_index* idx, int64_t* out4);
+ * on this index (all zero before the first): out5[0] queries per tile
+ * (tables sharing one LDS residency and one pass over the codes), out5[1]
+ * code chunks per query tile, out5[2] fewest 64-row code tiles per chunk,
+ * out5[3] LDS bytes per workgroup, out5[4] chunk grid cell in tiles (0: no
+ * grid).  For measurement and tests.
+ * Errors: IFVS_E_INVALID (NULL out5), IFVS_E_STATE. */
+ifvs_status ifvs_last_plan(const ifvs_index* idx, int64_t* out5);
 
 /* Text of the last failure on the calling thread; valid until the next call
  * on this thread.  Never NULL. */

@@ -112,6 +112,7 @@ struct ifvs_index {
   std::vector<int32_t> fence0, fence1;
 
   int opt_qtile = 0, opt_splits = 0, opt_min_chunk = 0;
+  int64_t opt_grid_tiles = 0;
   bool profile = false;
   StageTimer* timers = nullptr;  // [kStages] once profiling was enabled
   ScanPlan last_plan{};
@@ -377,8 +378,24 @@ ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_
   // tiles per 8-wavefront workgroup), at least ~512 workgroups, at most 16
   // chunks per query tile.
   int64_t splits = (4096 + gy - 1) / gy;
-  if (interval_batch)
-    splits = std::min<int64_t>(16, std::max<int64_t>((span_tiles + 8191) / 8192, (512 + gy - 1) / gy));
+  plan->chunk_tiles = 0;
+  if (interval_batch) {
+    // Long spans (>= 8192 tiles) are cut on a chunk grid of cells of about
+    // 5K tiles (measured best between 4K and 5K on 10M x 48-byte codes), so
+    // queries with nearby spans read the same cells at the same time; a span
+    // not aligned to the grid touches one cell more.  Short spans are cut
+    // into equal chunks, at least ~512 workgroups per batch.
+    if (idx->opt_grid_tiles > 0) {
+      plan->chunk_tiles = idx->opt_grid_tiles;
+    } else if (span_tiles >= 8192) {
+      const int64_t cells = (span_tiles + 5119) / 5120;
+      plan->chunk_tiles = (span_tiles + cells - 1) / cells;
+    }
+    if (plan->chunk_tiles > 0)
+      splits = (span_tiles + plan->chunk_tiles - 1) / plan->chunk_tiles + 1;
+    else
+      splits = std::min<int64_t>(16, std::max<int64_t>((span_tiles + 8191) / 8192, (512 + gy - 1) / gy));
+  }
   if (idx->opt_splits > 0) splits = idx->opt_splits;
   splits = std::min<int64_t>(splits, std::max<int64_t>(1, (idx->n_tiles + plan->min_chunk - 1) / plan->min_chunk));
   const int64_t cap = static_cast<int64_t>(idx->partial_keys /
@@ -387,8 +404,7 @@ ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_
   plan->splits = static_cast<int>(splits);
   plan->kpl = pool_kpl(k);
   plan->pool_stride = pool_stride_for(k);
-  plan->lds_bytes = static_cast<size_t>(idx->m) * plan->qtile * kKsub * lut_bytes +
-                    static_cast<size_t>(kScanWaves) * plan->qtile * plan->pool_stride * sizeof(uint64_t);
+  plan->lds_bytes = scan_lds_bytes(idx->m, plan->qtile, lut_bytes, plan->pool_stride);
   return IFVS_OK;
 }
 
@@ -570,6 +586,7 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
     case IFVS_OPT_QTILE: idx->opt_qtile = static_cast<int>(value); return IFVS_OK;
     case IFVS_OPT_SPLITS: idx->opt_splits = static_cast<int>(value); return IFVS_OK;
     case IFVS_OPT_MIN_CHUNK: idx->opt_min_chunk = static_cast<int>(value); return IFVS_OK;
+    case IFVS_OPT_GRID_TILES: idx->opt_grid_tiles = value; return IFVS_OK;
     case IFVS_OPT_PROFILE:
       if (value != 0 && !idx->timers) {
         idx->timers = new StageTimer[kStages];
@@ -715,13 +732,14 @@ ifvs_status ifvs_read_profile(ifvs_index* idx, double* ms_out, int64_t* launches
   return IFVS_OK;
 }
 
-ifvs_status ifvs_last_plan(const ifvs_index* idx, int64_t* out4) {
+ifvs_status ifvs_last_plan(const ifvs_index* idx, int64_t* out5) {
   if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
-  if (!out4) return fail(IFVS_E_INVALID, "out4 is NULL");
-  out4[0] = idx->last_plan.qtile;
-  out4[1] = idx->last_plan.splits;
-  out4[2] = idx->last_plan.min_chunk;
-  out4[3] = static_cast<int64_t>(idx->last_plan.lds_bytes);
+  if (!out5) return fail(IFVS_E_INVALID, "out5 is NULL");
+  out5[0] = idx->last_plan.qtile;
+  out5[1] = idx->last_plan.splits;
+  out5[2] = idx->last_plan.min_chunk;
+  out5[3] = static_cast<int64_t>(idx->last_plan.lds_bytes);
+  out5[4] = idx->last_plan.chunk_tiles;
   return IFVS_OK;
 }
 

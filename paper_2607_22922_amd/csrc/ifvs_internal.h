@@ -88,10 +88,13 @@ struct ScanPlan {
   int pool_stride;  // candidate pool keys per (wave, query): >= k + 64
   int kpl;          // pool keys per lane when it is sorted
   size_t lds_bytes;
+  int64_t chunk_tiles;  // > 0: chunk grid cell in tiles (interval scans); 0: equal chunks
 };
 
 // Largest query tile whose tables and pools fit the LDS budget (0 if none).
 int scan_max_qtile(int m, int lut_bytes, int k);
+// Dynamic LDS of one scan workgroup.
+size_t scan_lds_bytes(int m, int qtile, int lut_bytes, int pool_stride);
 // Round a requested tile down to one this build instantiates.
 int scan_supported_qtile(int want);
 int pool_kpl(int k);

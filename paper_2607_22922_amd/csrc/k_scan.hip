@@ -55,6 +55,7 @@ struct ScanArgs {
   int64_t stride64;
   const int32_t* perm;
   int k, pool_stride, kpl, min_chunk;
+  int64_t chunk_tiles;   // > 0: chunks on a grid of this many tiles (see below)
   uint64_t* partials;
   uint64_t* gthr;   // [nq] per original query: smallest k-th key any wavefront has published
 };
@@ -70,9 +71,15 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int kMW = MT > 0 ? (MT + 3) / 4 : 1;
   const int M = MT > 0 ? MT : a.m;
+  // LDS: tables first (at address 0, so a table address is the code byte
+  // times the entry size plus a constant that folds into the instruction),
+  // then the pools, the workgroup thresholds and the monotonicity flags.
   LutT* slut = reinterpret_cast<LutT*>(smem);
   const size_t lut_bytes = static_cast<size_t>(M) * QT * kKsub * sizeof(LutT);
   uint64_t* pools = reinterpret_cast<uint64_t*>(smem + lut_bytes);
+  unsigned long long* s_thr = reinterpret_cast<unsigned long long*>(
+      pools + static_cast<size_t>(kScanWaves) * QT * a.pool_stride);   // smallest k-th key published in this workgroup
+  uint32_t* s_not_monotone = reinterpret_cast<uint32_t*>(s_thr + QT);
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -113,17 +120,29 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
       }
     }
   }
+  // Chunks: with a chunk grid, chunk c of the tile is grid cell
+  // (first cell of its span) + c cut to the span, so query tiles with nearby
+  // spans read the same cells and, scheduled together on one XCD, share its
+  // L2.  A span that needs more cells than there are chunks (the planner's
+  // estimate fell short) is cut into equal chunks instead.
   int64_t t_begin = 0, t_end = 0;
   if (hull_hi > hull_lo) {
     const int64_t t_lo = hull_lo / 64, t_hi = (hull_hi + 63) / 64;
-    const int64_t ch = max(static_cast<int64_t>(a.min_chunk), (t_hi - t_lo + a.splits - 1) / a.splits);
-    t_begin = t_lo + chunk * ch;
-    t_end = min(t_hi, t_begin + ch);
+    const int64_t g = a.chunk_tiles;
+    if (g > 0 && (t_hi - 1) / g - t_lo / g < a.splits) {
+      const int64_t cell = t_lo / g + chunk;
+      t_begin = max(t_lo, cell * g);
+      t_end = min(t_hi, (cell + 1) * g);
+    } else {
+      const int64_t ch = max(static_cast<int64_t>(a.min_chunk), (t_hi - t_lo + a.splits - 1) / a.splits);
+      t_begin = t_lo + chunk * ch;
+      t_end = min(t_hi, t_begin + ch);
+    }
   }
   bool work = false;
 #pragma unroll
   for (int qi = 0; qi < QT; ++qi)
-    work = work || (r1[qi] > r0[qi] && r0[qi] < t_end * 64 && r1[qi] > t_begin * 64);
+    work = work || (t_begin < t_end && r1[qi] > r0[qi] && r0[qi] < t_end * 64 && r1[qi] > t_begin * 64);
   if (!work) {
     // Nothing selected in this chunk: empty partial lists.
     for (int qi = 0; qi < qn; ++qi) {
@@ -135,8 +154,6 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
 
   // Stage the tile's tables: global [q][m][c] -> LDS [m][qi][c], noting any
   // entry that is negative or NaN (then partial sums are no lower bound).
-  __shared__ uint32_t s_not_monotone[QT];
-  __shared__ unsigned long long s_thr[QT];   // smallest k-th key published in this workgroup
   if (threadIdx.x < QT) {
     s_not_monotone[threadIdx.x] = 0;
     s_thr[threadIdx.x] = kNoKey;
@@ -202,16 +219,27 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
   // (LDS) and to the query (global memory) and filters with the smallest
   // one it knows: bound[qi] = min(own, workgroup, query).  A row whose key is
   // not below the bound cannot be among the query's k best.
-  uint64_t published[QT], gview[QT], bound[QT];
+  //
+  // The query's value is read once per two tiles: the load is issued before
+  // the next tile's code words and taken in after the tile after it is
+  // summed.  Every load of a step is issued on every path, so the compiler's
+  // wait counts never make the current tile wait for the next one's words.
+  uint64_t published[QT], gview[QT], gnext[QT], bound[QT];
 #pragma unroll
-  for (int qi = 0; qi < QT; ++qi) published[qi] = gview[qi] = bound[qi] = kNoKey;
-  int tiles_seen = 0;
+  for (int qi = 0; qi < QT; ++qi) published[qi] = gview[qi] = gnext[qi] = bound[qi] = kNoKey;
+  auto global_issue = [&]() {
+#pragma unroll
+    for (int qi = 0; qi < QT; ++qi)
+      gnext[qi] = __hip_atomic_load(a.gthr + qid[qi], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  };
+  auto global_finish = [&]() {
+#pragma unroll
+    for (int qi = 0; qi < QT; ++qi) gview[qi] = gnext[qi];
+  };
   auto refresh_bounds = [&]() {
-    const bool read_global = (tiles_seen++ & 7) == 0;
 #pragma unroll
     for (int qi = 0; qi < QT; ++qi) {
       if (qi >= qn) continue;
-      if (read_global) gview[qi] = __hip_atomic_load(a.gthr + qid[qi], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       const uint64_t blk = s_thr[qi];
       uint64_t b = thr[qi] < blk ? thr[qi] : blk;
       bound[qi] = b < gview[qi] ? b : gview[qi];
@@ -242,25 +270,20 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
 
   if constexpr (MT > 0) {
     constexpr int kGroup = MT % 8 == 0 && MT > 16 ? 8 : (MT % 4 == 0 ? 4 : MT);
-    // Software pipeline: the next selected tile's code words are in flight
-    // while the current tile is summed.
-    int64_t t = t_begin + wave;
-    uint64_t bm[QT];
-    while (t < t_end && tile_masks(t, bm) == 0) t += kScanWaves;
-    uint32_t w[kMW];
-    if (t < t_end) {
+    // Software pipeline over two register sets: while the tile in one set is
+    // summed, the next selected tile's code words load into the other (no
+    // register copy, so nothing waits for the loads in flight).
+    auto next_selected = [&](int64_t t, uint64_t (&bm)[QT]) -> int64_t {
+      while (t < t_end && tile_masks(t, bm) == 0) t += kScanWaves;
+      return t;
+    };
+    // Past the chunk's end the loads repeat its last tile (in bounds, unused).
+    auto load_tile = [&](int64_t t, uint32_t (&w)[kMW]) {
+      const int64_t tc = t < t_end ? t : t_end - 1;
 #pragma unroll
-      for (int j = 0; j < kMW; ++j) w[j] = a.codes_t[(t * kMW + j) * 64 + lane];
-    }
-    while (t < t_end) {
-      int64_t tn = t + kScanWaves;
-      uint64_t bmn[QT];
-      while (tn < t_end && tile_masks(tn, bmn) == 0) tn += kScanWaves;
-      uint32_t wn[kMW];
-      if (tn < t_end) {
-#pragma unroll
-        for (int j = 0; j < kMW; ++j) wn[j] = a.codes_t[(tn * kMW + j) * 64 + lane];
-      }
+      for (int j = 0; j < kMW; ++j) w[j] = a.codes_t[(tc * kMW + j) * 64 + lane];
+    };
+    auto sum_tile = [&](int64_t t, const uint64_t (&bm)[QT], const uint32_t (&w)[kMW]) {
       refresh_bounds();
       int addr[MT];
 #pragma unroll
@@ -287,16 +310,28 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
         }
         consider(qi, live, d, t);
       }
-      t = tn;
-#pragma unroll
-      for (int qi = 0; qi < QT; ++qi) bm[qi] = bmn[qi];
-#pragma unroll
-      for (int j = 0; j < kMW; ++j) w[j] = wn[j];
+    };
+    uint64_t bma[QT], bmb[QT];
+    uint32_t wa[kMW], wb[kMW];
+    int64_t ta = next_selected(t_begin + wave, bma);
+    load_tile(ta, wa);
+    while (ta < t_end) {
+      const int64_t tb = next_selected(ta + kScanWaves, bmb);
+      global_issue();
+      load_tile(tb, wb);
+      sum_tile(ta, bma, wa);
+      if (tb >= t_end) break;
+      ta = next_selected(tb + kScanWaves, bma);
+      load_tile(ta, wa);
+      sum_tile(tb, bmb, wb);
+      global_finish();
     }
   } else {
     for (int64_t t = t_begin + wave; t < t_end; t += kScanWaves) {
       uint64_t bm[QT];
       if (tile_masks(t, bm) == 0) continue;
+      global_issue();
+      global_finish();
       refresh_bounds();
 #pragma unroll
       for (int qi = 0; qi < QT; ++qi) {
@@ -371,10 +406,17 @@ int pool_stride_for(int k) {
   return kpl <= 4 ? k + 64 : 64 * kpl;
 }
 
+size_t scan_lds_bytes(int m, int qtile, int lut_bytes, int pool_stride) {
+  // tables, pools, workgroup thresholds (8 B) and monotonicity flags (4 B)
+  return static_cast<size_t>(qtile) *
+         (static_cast<size_t>(m) * kKsub * lut_bytes +
+          static_cast<size_t>(kScanWaves) * pool_stride * sizeof(uint64_t) + 12);
+}
+
 int scan_max_qtile(int m, int lut_bytes, int k) {
-  const size_t per_query = static_cast<size_t>(m) * kKsub * lut_bytes +
-                           static_cast<size_t>(kScanWaves) * pool_stride_for(k) * sizeof(uint64_t);
-  return static_cast<int>(kLdsBudget / per_query);
+  int q = 0;
+  while (scan_lds_bytes(m, q + 1, lut_bytes, pool_stride_for(k)) <= static_cast<size_t>(kLdsBudget)) ++q;
+  return q;
 }
 
 int scan_supported_qtile(int want) {
@@ -408,6 +450,7 @@ hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s) 
   a.pool_stride = plan.pool_stride;
   a.kpl = plan.kpl;
   a.min_chunk = plan.min_chunk;
+  a.chunk_tiles = plan.chunk_tiles;
   a.partials = b.partials;
   a.gthr = b.gthr;
   a.splits = plan.splits;

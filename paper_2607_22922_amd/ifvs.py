@@ -23,7 +23,7 @@ LUT_F32, LUT_F16 = 0, 1
 KSUB = 256
 MAX_CLAUSES = 4
 MAX_K = 1024
-OPT_QTILE, OPT_SPLITS, OPT_PROFILE, OPT_MIN_CHUNK = 1, 2, 3, 4
+OPT_QTILE, OPT_SPLITS, OPT_PROFILE, OPT_MIN_CHUNK, OPT_GRID_TILES = 1, 2, 3, 4, 5
 STAGES = ("condition", "lut", "filter", "scan", "merge")
 
 EXPORTED = ("ifvs_load_index", "ifvs_free_index", "ifvs_select_codebook", "ifvs_build_lut",
@@ -199,9 +199,9 @@ class Index:
 
     def last_plan(self) -> dict:
         """Launch plan of the most recent filtered_search on this index."""
-        out = (ctypes.c_int64 * 4)()
+        out = (ctypes.c_int64 * 5)()
         _check(_lib.ifvs_last_plan(self.handle, out))
-        return dict(qtile=out[0], splits=out[1], min_chunk=out[2], lds_bytes=out[3])
+        return dict(qtile=out[0], splits=out[1], min_chunk=out[2], lds_bytes=out[3], grid_tiles=out[4])
 
     def read_profile(self) -> dict:
         """Per-stage (total kernel ms, launches) since the last read."""

@@ -263,6 +263,41 @@ def test_clustered_predicate_shapes(B, cols):
     _run_and_check(B, idx, ox, preds, k=100, dsub=8, M=16, seed=2)
 
 
+@pytest.mark.parametrize("cols", [(0,), (1, 0)])
+def test_clustered_chunk_grid_and_fallback(B, cols):
+    """Chunks cut on a grid of cells (forced small here; long spans get one by
+    default), including spans that need more cells than there are chunks
+    (cut into equal chunks instead): results equal the default plan's, which
+    equal the oracle's."""
+    say(f"[clustered] chunk grid cols={cols}")
+    idx, ox = _edge_index(B, 40_000, 16, 8, n_attr=2, domain=30, seed=37, cluster_cols=cols)
+    a, b = cols[0], 1 - cols[0]          # a: the cluster key every predicate bounds
+    preds = [[(a, 3, 9)], [(a, 0, 30)], [(a, 7, 8), (b, 2, 20)], [(a, 11, 12)], [(a, 1, 27), (b, 0, 15)],
+             [(a, 29, 30), (b, 2, 9)], [(a, 1, 27)], [(a, -5, 100)]] * 3
+    g = torch.Generator(device="cuda").manual_seed(3)
+    q = torch.randn(len(preds), 128, device="cuda", generator=g)
+    alpha, wf = idx.select_codebook(q, preds, None)
+    lut = idx.build_lut(q, alpha, wf)
+    ids0, dist0 = idx.search(preds, lut, 20)
+    torch.cuda.synchronize()
+    assert idx.last_plan()["grid_tiles"] == 0          # spans too short for a grid by default
+    for i, p in enumerate(preds[:8]):
+        lut_o = O.build_lut(_np(q[i]), _np(alpha[i]), _np(wf[i]), ox["C_pq"], ox["W"], 16, ox["r"])
+        cand = O.passing_ids(O.predicate_mask(ox["attrs"], p))
+        ids_o, dist_o = O.select_topk(O.adc_distances(lut_o, ox["codes"], cand), cand, 20)
+        check_search_row(_np(ids0[i]), _np(dist0[i]), ids_o, dist_o, f"grid q{i}")
+    for grid, splits in ((1, 0), (7, 0), (64, 0), (7, 2), (1, 3), (64, 1)):
+        idx.set_option(B.OPT_GRID_TILES, grid)
+        idx.set_option(B.OPT_SPLITS, splits)
+        ids, dist = idx.search(preds, lut, 20)
+        torch.cuda.synchronize()
+        assert idx.last_plan()["grid_tiles"] == grid
+        assert torch.equal(ids, ids0), (grid, splits)
+        assert torch.equal(dist.view(torch.int32), dist0.view(torch.int32)), (grid, splits)
+    idx.set_option(B.OPT_GRID_TILES, 0)
+    idx.set_option(B.OPT_SPLITS, 0)
+
+
 def test_clustered_ties_break_by_original_id(B):
     ix = random_index(6000, 16, 8, 1, 40, 41, device="cuda")
     ix["codes"][::7] = ix["codes"][3]                 # equal rows in every cluster
