@@ -71,12 +71,22 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int kMW = MT > 0 ? (MT + 3) / 4 : 1;
   const int M = MT > 0 ? MT : a.m;
-  // LDS: tables first (at address 0, so a table address is the code byte
-  // times the entry size plus a constant that folds into the instruction),
-  // then the pools, the workgroup thresholds and the monotonicity flags.
-  LutT* slut = reinterpret_cast<LutT*>(smem);
+  // LDS: the tables, then (dynamic) the pools, the workgroup thresholds and
+  // the monotonicity flags.  With M fixed at compile time the tables are a
+  // static array at a known address: a table address is then the code byte
+  // times the entry size (one shift with a byte select) plus a constant that
+  // folds into the instruction's offset.
+  LutT* slut;
   const size_t lut_bytes = static_cast<size_t>(M) * QT * kKsub * sizeof(LutT);
-  uint64_t* pools = reinterpret_cast<uint64_t*>(smem + lut_bytes);
+  uint64_t* pools;
+  if constexpr (MT > 0) {
+    __shared__ __align__(16) unsigned char s_lut[static_cast<size_t>(MT > 0 ? MT : 1) * QT * kKsub * sizeof(LutT)];
+    slut = reinterpret_cast<LutT*>(s_lut);
+    pools = reinterpret_cast<uint64_t*>(smem);
+  } else {
+    slut = reinterpret_cast<LutT*>(smem);
+    pools = reinterpret_cast<uint64_t*>(smem + lut_bytes);
+  }
   unsigned long long* s_thr = reinterpret_cast<unsigned long long*>(
       pools + static_cast<size_t>(kScanWaves) * QT * a.pool_stride);   // smallest k-th key published in this workgroup
   uint32_t* s_not_monotone = reinterpret_cast<uint32_t*>(s_thr + QT);
@@ -220,10 +230,10 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
   // one it knows: bound[qi] = min(own, workgroup, query).  A row whose key is
   // not below the bound cannot be among the query's k best.
   //
-  // The query's value is read once per two tiles: the load is issued before
-  // the next tile's code words and taken in after the tile after it is
-  // summed.  Every load of a step is issued on every path, so the compiler's
-  // wait counts never make the current tile wait for the next one's words.
+  // The query's value is read once per two tiles and taken in one loop
+  // iteration (two tiles) later, by when the load has long landed.  Every
+  // load of a step is issued on every path, so the compiler's wait counts
+  // never make the current tile wait for the next one's words.
   uint64_t published[QT], gview[QT], gnext[QT], bound[QT];
 #pragma unroll
   for (int qi = 0; qi < QT; ++qi) published[qi] = gview[qi] = gnext[qi] = bound[qi] = kNoKey;
@@ -317,6 +327,7 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
     load_tile(ta, wa);
     while (ta < t_end) {
       const int64_t tb = next_selected(ta + kScanWaves, bmb);
+      global_finish();
       global_issue();
       load_tile(tb, wb);
       sum_tile(ta, bma, wa);
@@ -324,7 +335,6 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
       ta = next_selected(tb + kScanWaves, bma);
       load_tile(ta, wa);
       sum_tile(tb, bmb, wb);
-      global_finish();
     }
   } else {
     for (int64_t t = t_begin + wave; t < t_end; t += kScanWaves) {
@@ -368,15 +378,29 @@ const void* scan_symbol() {
 
 constexpr int kQtiles[] = {1, 2, 3, 4, 6, 8};
 
+// Instantiated only where the static tables and the smallest pools fit.
+template <int MT, int QT, typename LutT>
+constexpr bool scan_fits() {
+  return static_cast<size_t>(MT) * QT * kKsub * sizeof(LutT) +
+             static_cast<size_t>(QT) * (kScanWaves * 65 * sizeof(uint64_t) + 12) <=
+         static_cast<size_t>(kLdsBudget);
+}
+
+template <int MT, int QT, typename LutT>
+const void* scan_symbol_if_fits() {
+  if constexpr (scan_fits<MT, QT, LutT>()) return scan_symbol<MT, QT, LutT>();
+  else return nullptr;
+}
+
 template <typename LutT, int MT>
 const void* pick_q(int qt) {
   switch (qt) {
-    case 1: return scan_symbol<MT, 1, LutT>();
-    case 2: return scan_symbol<MT, 2, LutT>();
-    case 3: return scan_symbol<MT, 3, LutT>();
-    case 4: return scan_symbol<MT, 4, LutT>();
-    case 6: return scan_symbol<MT, 6, LutT>();
-    case 8: return scan_symbol<MT, 8, LutT>();
+    case 1: return scan_symbol_if_fits<MT, 1, LutT>();
+    case 2: return scan_symbol_if_fits<MT, 2, LutT>();
+    case 3: return scan_symbol_if_fits<MT, 3, LutT>();
+    case 4: return scan_symbol_if_fits<MT, 4, LutT>();
+    case 6: return scan_symbol_if_fits<MT, 6, LutT>();
+    case 8: return scan_symbol_if_fits<MT, 8, LutT>();
     default: return nullptr;
   }
 }
@@ -429,8 +453,11 @@ int scan_supported_qtile(int want) {
 hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s) {
   const void* fn = b.lut_dtype == 1 ? pick<__half>(b.m, plan.qtile) : pick<float>(b.m, plan.qtile);
   if (!fn) return hipErrorInvalidValue;
-  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     static_cast<int>(plan.lds_bytes));
+  // Fixed-M kernels hold their tables in static LDS; the rest is dynamic.
+  const bool fixed_m = b.m == 16 || b.m == 48 || b.m == 120;
+  const size_t table = static_cast<size_t>(b.m) * plan.qtile * kKsub * (b.lut_dtype == 1 ? 2 : 4);
+  const size_t dyn = fixed_m ? plan.lds_bytes - table : plan.lds_bytes;
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(dyn));
   if (e != hipSuccess) return e;
   ScanArgs a{};
   a.codes_t = b.codes_t;
@@ -458,7 +485,7 @@ hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s) 
   const unsigned per_xcd = static_cast<unsigned>((a.n_qtiles + kXcds - 1) / kXcds);
   const dim3 grid(static_cast<unsigned>(kXcds) * per_xcd * static_cast<unsigned>(a.splits));
   void* args[] = {&a};
-  return hipLaunchKernel(fn, grid, dim3(kScanWaves * 64), args, plan.lds_bytes, s);
+  return hipLaunchKernel(fn, grid, dim3(kScanWaves * 64), args, dyn, s);
 }
 
 }  // namespace ifvs
