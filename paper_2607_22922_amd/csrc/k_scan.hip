@@ -29,6 +29,8 @@
 //    when it would overflow.  Keys carry original vector ids (read for candidates
 //    only), so ties break by original id on any layout.  At the end each
 //    wavefront writes its k best keys per query; a merge kernel reduces them.
+#include <climits>
+
 #include "ifvs_internal.h"
 #include "topk_device.h"
 
@@ -153,6 +155,17 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
 #pragma unroll
   for (int qi = 0; qi < QT; ++qi)
     work = work || (t_begin < t_end && r1[qi] > r0[qi] && r0[qi] < t_end * 64 && r1[qi] > t_begin * 64);
+  // Tile indices fit 32 bits (n < 2^31 rows), so the loop's uniform
+  // arithmetic stays on the scalar unit.  ft/lt: first and last tile a
+  // query's interval touches (ft > lt when it is empty).
+  const int tb = static_cast<int>(t_begin), te = static_cast<int>(t_end);
+  int ft[QT], lt[QT];
+#pragma unroll
+  for (int qi = 0; qi < QT; ++qi) {
+    const bool any = qi < qn && r1[qi] > r0[qi];
+    ft[qi] = any ? static_cast<int>(r0[qi] >> 6) : INT_MAX;
+    lt[qi] = any ? static_cast<int>((r1[qi] - 1) >> 6) : -1;
+  }
   if (!work) {
     // Nothing selected in this chunk: empty partial lists.
     for (int qi = 0; qi < qn; ++qi) {
@@ -203,20 +216,21 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
   }
   uint64_t* my_pools = pools + static_cast<size_t>(wave) * QT * a.pool_stride;
 
-  // Selection word of query qi for tile t: interval bits, and bitmap bits
-  // when the query has residual clauses.
-  auto tile_masks = [&](int64_t t, uint64_t (&bm)[QT]) -> uint64_t {
+  // Selection word of query qi for tile t: interval bits (all ones inside
+  // the interval, computed only on its first and last tile), and bitmap
+  // bits when the query has residual clauses.
+  auto tile_masks = [&](int t, uint64_t (&bm)[QT]) -> uint64_t {
     uint64_t any = 0;
-    const int64_t row0 = t * 64;
 #pragma unroll
     for (int qi = 0; qi < QT; ++qi) {
       uint64_t mk = 0;
-      const int64_t lo = max(r0[qi] - row0, static_cast<int64_t>(0));
-      const int64_t hi = min(r1[qi] - row0, static_cast<int64_t>(64));
-      if (qi < qn && hi > lo) {
-        mk = bit_range(lo, hi);
-        if (resid[qi]) mk &= a.bitmap[static_cast<size_t>(qid[qi]) * a.stride64 + t];
+      if (t > ft[qi] && t < lt[qi]) {
+        mk = ~0ull;
+      } else if (t == ft[qi] || t == lt[qi]) {
+        const int64_t row0 = static_cast<int64_t>(t) * 64;
+        mk = bit_range(max(r0[qi] - row0, static_cast<int64_t>(0)), min(r1[qi] - row0, static_cast<int64_t>(64)));
       }
+      if (resid[qi] && mk != 0) mk &= a.bitmap[static_cast<size_t>(qid[qi]) * a.stride64 + t];
       bm[qi] = mk;
       any |= mk;
     }
@@ -256,7 +270,7 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
     }
   };
 
-  auto consider = [&](int qi, bool act, float d, int64_t t) {
+  auto consider = [&](int qi, bool act, float d, int t) {
     uint64_t key = kNoKey;
     bool cand = false;
     if (act) {
@@ -283,61 +297,79 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
     // Software pipeline over two register sets: while the tile in one set is
     // summed, the next selected tile's code words load into the other (no
     // register copy, so nothing waits for the loads in flight).
-    auto next_selected = [&](int64_t t, uint64_t (&bm)[QT]) -> int64_t {
-      while (t < t_end && tile_masks(t, bm) == 0) t += kScanWaves;
+    auto next_selected = [&](int t, uint64_t (&bm)[QT]) -> int {
+      while (t < te && tile_masks(t, bm) == 0) t += kScanWaves;
       return t;
     };
     // Past the chunk's end the loads repeat its last tile (in bounds, unused).
-    auto load_tile = [&](int64_t t, uint32_t (&w)[kMW]) {
-      const int64_t tc = t < t_end ? t : t_end - 1;
+    auto load_tile = [&](int t, uint32_t (&w)[kMW]) {
+      const int tc = t < te ? t : te - 1;
+      const uint32_t* __restrict__ tile = a.codes_t + static_cast<size_t>(tc) * (kMW * 64);
 #pragma unroll
-      for (int j = 0; j < kMW; ++j) w[j] = a.codes_t[(tc * kMW + j) * 64 + lane];
+      for (int j = 0; j < kMW; ++j) w[j] = tile[j * 64 + lane];
     };
-    auto sum_tile = [&](int64_t t, const uint64_t (&bm)[QT], const uint32_t (&w)[kMW]) {
+    auto sum_tile = [&](int t, const uint64_t (&bm)[QT], const uint32_t (&w)[kMW]) {
       refresh_bounds();
-      int addr[MT];
-#pragma unroll
-      for (int m = 0; m < MT; ++m)
-        addr[m] = m * QT * kKsub + static_cast<int>((w[m >> 2] >> (8 * (m & 3))) & 0xFFu);
+      // Subspaces are summed in groups, all of the tile's queries side by
+      // side: a group's table reads of every query are issued before its
+      // additions, so the reads of different queries overlap.  After each
+      // group a lane whose partial sum already exceeds its query's k-th
+      // distance drops out (NaN cut before k candidates exist: nothing drops).
+      float cut[QT], d[QT];
+      bool live[QT];
 #pragma unroll
       for (int qi = 0; qi < QT; ++qi) {
-        if (bm[qi] == 0) continue;
-        // Subspaces are summed in groups; after each group a lane whose
-        // partial sum already exceeds the k-th distance drops out (NaN cut
-        // before k candidates exist: nothing drops).
-        const float cut = monotone[qi] ? from_ordered_bits(static_cast<uint32_t>(bound[qi] >> 32))
-                                       : __builtin_nanf("");
-        bool live = (bm[qi] >> lane) & 1ull;
-        float d = 0.0f;
-#pragma unroll
-        for (int g = 0; g < MT / kGroup; ++g) {
-          if (live) {
-#pragma unroll
-            for (int u = 0; u < kGroup; ++u)
-              d = __fadd_rn(d, widen(slut[addr[g * kGroup + u] + qi * kKsub]));
-          }
-          live = live && !(d > cut);
-        }
-        consider(qi, live, d, t);
+        cut[qi] = monotone[qi] ? from_ordered_bits(static_cast<uint32_t>(bound[qi] >> 32)) : __builtin_nanf("");
+        live[qi] = __builtin_amdgcn_inverse_ballot_w64(bm[qi]);
+        d[qi] = 0.0f;
       }
+#pragma unroll
+      for (int g = 0; g < MT / kGroup; ++g) {
+        int addr[kGroup];
+#pragma unroll
+        for (int u = 0; u < kGroup; ++u) {
+          const int m = g * kGroup + u;
+          addr[u] = m * QT * kKsub + static_cast<int>((w[m >> 2] >> (8 * (m & 3))) & 0xFFu);
+        }
+        LutT v[QT][kGroup];
+#pragma unroll
+        for (int qi = 0; qi < QT; ++qi) {
+          if (live[qi]) {
+#pragma unroll
+            for (int u = 0; u < kGroup; ++u) v[qi][u] = slut[addr[u] + qi * kKsub];
+          }
+        }
+#pragma unroll
+        for (int qi = 0; qi < QT; ++qi) {
+          if (live[qi]) {
+#pragma unroll
+            for (int u = 0; u < kGroup; ++u) d[qi] = __fadd_rn(d[qi], widen(v[qi][u]));
+          }
+          live[qi] = live[qi] && !(d[qi] > cut[qi]);
+        }
+      }
+#pragma unroll
+      for (int qi = 0; qi < QT; ++qi)
+        // Usually every lane has dropped out: nothing to offer.
+        if (__ballot(live[qi]) != 0) consider(qi, live[qi], d[qi], t);
     };
     uint64_t bma[QT], bmb[QT];
     uint32_t wa[kMW], wb[kMW];
-    int64_t ta = next_selected(t_begin + wave, bma);
+    int ta = next_selected(tb + wave, bma);
     load_tile(ta, wa);
-    while (ta < t_end) {
-      const int64_t tb = next_selected(ta + kScanWaves, bmb);
+    while (ta < te) {
+      const int tn = next_selected(ta + kScanWaves, bmb);
       global_finish();
       global_issue();
-      load_tile(tb, wb);
+      load_tile(tn, wb);
       sum_tile(ta, bma, wa);
-      if (tb >= t_end) break;
-      ta = next_selected(tb + kScanWaves, bma);
+      if (tn >= te) break;
+      ta = next_selected(tn + kScanWaves, bma);
       load_tile(ta, wa);
-      sum_tile(tb, bmb, wb);
+      sum_tile(tn, bmb, wb);
     }
   } else {
-    for (int64_t t = t_begin + wave; t < t_end; t += kScanWaves) {
+    for (int t = tb + wave; t < te; t += kScanWaves) {
       uint64_t bm[QT];
       if (tile_masks(t, bm) == 0) continue;
       global_issue();
@@ -346,11 +378,11 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
 #pragma unroll
       for (int qi = 0; qi < QT; ++qi) {
         if (bm[qi] == 0) continue;
-        const bool act = (bm[qi] >> lane) & 1ull;
+        const bool act = __builtin_amdgcn_inverse_ballot_w64(bm[qi]);
         float d = 0.0f;
         if (act) {
           for (int m = 0; m < M; ++m) {
-            const uint32_t wv = a.codes_t[(t * a.mw + (m >> 2)) * 64 + lane];
+            const uint32_t wv = a.codes_t[(static_cast<size_t>(t) * a.mw + (m >> 2)) * 64 + lane];
             const int c = static_cast<int>((wv >> (8 * (m & 3))) & 0xFFu);
             d = __fadd_rn(d, widen(slut[(static_cast<size_t>(m) * QT + qi) * kKsub + c]));
           }
