@@ -208,7 +208,8 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
  * Errors: IFVS_E_INVALID for an unknown option or a negative value. */
 #define IFVS_OPT_QTILE  1
 #define IFVS_OPT_SPLITS 2
-#define IFVS_OPT_PROFILE 3        /* 1: time every kernel launch with HIP events (see below) */
+#define IFVS_OPT_PROFILE 3        /* 1: time every kernel launch with HIP events (see below);
+                                     2: time only the scan kernel's launches              */
 #define IFVS_OPT_MIN_CHUNK 4      /* fewest 64-row code tiles per chunk (0 = automatic)      */
 #define IFVS_OPT_GRID_TILES 5     /* chunk grid cell in 64-row tiles (0 = automatic)         */
 ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value);

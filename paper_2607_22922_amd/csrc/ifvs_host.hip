@@ -52,7 +52,7 @@ bool forced_alloc_failure() {
   return fail_at > 0 && g_alloc_counter == fail_at;
 }
 
-constexpr int kStagingSlots = 4;
+constexpr int kStagingSlots = 8;
 
 // Optional per-stage kernel timing with HIP events (IFVS_OPT_PROFILE).
 enum Stage { kStCondition = 0, kStLut, kStFilter, kStScan, kStMerge, kStages };
@@ -96,6 +96,7 @@ struct ifvs_index {
   int64_t* iv_dev = nullptr;     // [max_batch][2]
   uint64_t* gthr_dev = nullptr;  // [max_batch] shared scan thresholds
   DevPred* staging[kStagingSlots] = {};   // pinned: [max_batch] DevPred + [max_batch] int32
+  DevPred* staging_dev[kStagingSlots] = {};  // the same slots as the device addresses them
   hipEvent_t staged[kStagingSlots] = {};
   bool slot_busy[kStagingSlots] = {};
   int next_slot = 0;
@@ -113,7 +114,7 @@ struct ifvs_index {
 
   int opt_qtile = 0, opt_splits = 0, opt_min_chunk = 0;
   int64_t opt_grid_tiles = 0;
-  bool profile = false;
+  int profile_mask = 0;          // stages timed with HIP events (IFVS_OPT_PROFILE)
   StageTimer* timers = nullptr;  // [kStages] once profiling was enabled
   ScanPlan last_plan{};
 
@@ -286,18 +287,21 @@ int64_t estimate_interval_tiles(const ifvs_index* idx, const DevPred& d) {
   return std::min<int64_t>(idx->n_tiles, rows / 64 + 1);
 }
 
-// Copy validated predicates (and the scan's query order, when asked) to the
-// device through a pinned staging slot.
+// Validate and normalize predicates into the next pinned staging slot (and
+// the scan's query order, when asked).  With copy_to_device the slot is
+// copied to the device workspace and released at once; otherwise the
+// caller's kernels read the slot itself (one wavefront-wide load per
+// predicate) and the caller releases it after enqueuing the last of them.
 ifvs_status stage_predicates(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
-                             bool with_order, hipStream_t s, DevPred** host_out = nullptr) {
+                             bool with_order, bool copy_to_device, hipStream_t s, int* slot_out,
+                             DevPred** host_out = nullptr) {
   const int slot = idx->next_slot;
   if (idx->slot_busy[slot]) IFVS_HIP(hipEventSynchronize(idx->staged[slot]), "waiting for staging slot");
+  idx->slot_busy[slot] = false;
   DevPred* host = idx->staging[slot];
   const ifvs_status st = normalize_predicates(idx, nq, preds, host);
   if (st != IFVS_OK) return st;
   idx->next_slot = (slot + 1) % kStagingSlots;
-  IFVS_HIP(hipMemcpyAsync(idx->preds_dev, host, sizeof(DevPred) * nq, hipMemcpyHostToDevice, s),
-           "copying predicates");
   if (with_order) {
     // Scan order: queries with nearby cluster-key intervals next to each
     // other, so that a query tile's intervals overlap; stable by index.
@@ -310,12 +314,22 @@ ifvs_status stage_predicates(ifvs_index* idx, int32_t nq, const ifvs_predicate* 
       if (x.iv_lo0 != y.iv_lo0) return x.iv_lo0 < y.iv_lo0;
       return x.iv_lo1 < y.iv_lo1;
     });
-    IFVS_HIP(hipMemcpyAsync(idx->qorder_dev, order, sizeof(int32_t) * nq, hipMemcpyHostToDevice, s),
-             "copying query order");
   }
+  if (copy_to_device) {
+    IFVS_HIP(hipMemcpyAsync(idx->preds_dev, host, sizeof(DevPred) * nq, hipMemcpyHostToDevice, s),
+             "copying predicates");
+    IFVS_HIP(hipEventRecord(idx->staged[slot], s), "recording staging event");
+    idx->slot_busy[slot] = true;
+  }
+  *slot_out = slot;
+  if (host_out) *host_out = host;
+  return IFVS_OK;
+}
+
+// The slot's readers are enqueued on s: it may be reused once they ran.
+ifvs_status release_slot(ifvs_index* idx, int slot, hipStream_t s) {
   IFVS_HIP(hipEventRecord(idx->staged[slot], s), "recording staging event");
   idx->slot_busy[slot] = true;
-  if (host_out) *host_out = host;
   return IFVS_OK;
 }
 
@@ -336,7 +350,7 @@ ifvs_status flush_timer(StageTimer& t) {
 // Launch through `fn`, bracketed by events when profiling.
 template <typename Fn>
 ifvs_status timed(ifvs_index* idx, int stage, hipStream_t s, const char* what, Fn&& fn) {
-  StageTimer* t = idx->profile ? &idx->timers[stage] : nullptr;
+  StageTimer* t = (idx->profile_mask >> stage) & 1 ? &idx->timers[stage] : nullptr;
   if (t) {
     if (t->used + 2 > 2 * kProfilePairs)
       if (ifvs_status st = flush_timer(*t); st != IFVS_OK) return st;
@@ -558,6 +572,9 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
       (void)hipGetLastError();
       return bail(fail(IFVS_E_NOMEM, "pinned staging allocation failed"));
     }
+    if (hipError_t e = hipHostGetDevicePointer(reinterpret_cast<void**>(&idx->staging_dev[i]), idx->staging[i], 0);
+        e != hipSuccess)
+      return bail(hip_fail(e, "mapping the staging slot"));
     if (hipError_t e = hipEventCreateWithFlags(&idx->staged[i], hipEventDisableTiming); e != hipSuccess)
       return bail(hip_fail(e, "creating staging event"));
   }
@@ -594,7 +611,8 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
           for (hipEvent_t& e : idx->timers[st].ev)
             IFVS_HIP(hipEventCreate(&e), "creating profile events");
       }
-      idx->profile = value != 0;
+      if (value > 2) return fail(IFVS_E_INVALID, "IFVS_OPT_PROFILE takes 0, 1 or 2");
+      idx->profile_mask = value == 0 ? 0 : (value == 1 ? (1 << kStages) - 1 : 1 << kStScan);
       return IFVS_OK;
     default: return fail(IFVS_E_INVALID, "unknown option " + std::to_string(option));
   }
@@ -610,12 +628,13 @@ ifvs_status ifvs_select_codebook(ifvs_index* idx, int32_t nq, const float* q,
   if (idx->bank_rows > 0 && !alpha_out) return fail(IFVS_E_INVALID, "alpha_out is NULL but the index has a memory bank");
   hipStream_t s = static_cast<hipStream_t>(stream);
   IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
-  if (ifvs_status st = stage_predicates(idx, nq, preds, false, s); st != IFVS_OK) return st;
+  int slot = 0;
+  if (ifvs_status st = stage_predicates(idx, nq, preds, false, false, s, &slot); st != IFVS_OK) return st;
   IFVS_LAUNCH(idx, kStCondition, s, "launching condition kernel",
-              launch_condition(q, idx->dim, idx->preds_dev, nq, idx->bank, idx->bank_rows,
+              launch_condition(q, idx->dim, idx->staging_dev[slot], nq, idx->bank, idx->bank_rows,
                                idx->m * idx->r, idx->h, idx->hash_seed, w_z,
                                idx->bank_rows > 0 ? alpha_out : nullptr, wf_out, s));
-  return IFVS_OK;
+  return release_slot(idx, slot, s);
 }
 
 ifvs_status ifvs_build_lut(ifvs_index* idx, int32_t nq, const float* q, const float* alpha,
@@ -642,7 +661,8 @@ ifvs_status ifvs_filter(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   if (!bitmap_out) return fail(IFVS_E_INVALID, "bitmap_out is NULL");
   hipStream_t s = static_cast<hipStream_t>(stream);
   IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
-  if (ifvs_status st = stage_predicates(idx, nq, preds, false, s); st != IFVS_OK) return st;
+  int slot = 0;
+  if (ifvs_status st = stage_predicates(idx, nq, preds, false, true, s, &slot); st != IFVS_OK) return st;
   if (ifvs_status st = filter_into_workspace(idx, nq, false, true, s); st != IFVS_OK) return st;
   if (ifvs_status st = copy_bitmaps_out(idx, nq, bitmap_out, s); st != IFVS_OK) return st;
   if (count_out)
@@ -667,8 +687,9 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   hipStream_t s = static_cast<hipStream_t>(stream);
   IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
   DevPred* host = nullptr;
+  int slot = 0;
   // Predicates are validated before anything is enqueued.
-  if (ifvs_status st = stage_predicates(idx, nq, preds, true, s, &host); st != IFVS_OK) return st;
+  if (ifvs_status st = stage_predicates(idx, nq, preds, true, false, s, &slot, &host); st != IFVS_OK) return st;
   bool need_bitmap = false, interval_batch = true;
   int64_t span = 0;
   for (int i = 0; i < nq; ++i) {
@@ -679,8 +700,10 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   ScanPlan plan{};
   if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, interval_batch, span, &plan); st != IFVS_OK) return st;
   IFVS_LAUNCH(idx, kStFilter, s, "launching interval kernel",
-              launch_intervals(idx->attrs_phys, idx->n, idx->c0, idx->c1, idx->preds_dev, nq, idx->iv_dev,
-                               idx->gthr_dev, s));
+              launch_intervals(idx->attrs_phys, idx->n, idx->c0, idx->c1, idx->staging_dev[slot],
+                               reinterpret_cast<const int32_t*>(idx->staging_dev[slot] + idx->max_batch), nq,
+                               idx->preds_dev, idx->qorder_dev, idx->iv_dev, idx->gthr_dev, s));
+  if (ifvs_status st = release_slot(idx, slot, s); st != IFVS_OK) return st;
   if (need_bitmap)
     if (ifvs_status st = filter_into_workspace(idx, nq, true, false, s); st != IFVS_OK) return st;
   ScanBatch b{};

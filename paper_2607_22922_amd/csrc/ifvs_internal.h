@@ -46,6 +46,14 @@ struct DevPred {
   uint32_t res_width[kMaxClauses];
 };
 
+// Copy one predicate with a wavefront (lane i moves dword i): a single round
+// trip when the source is the pinned host staging slot.
+__device__ inline void copy_pred(const DevPred* __restrict__ src, DevPred* __restrict__ dst, int lane) {
+  constexpr int kWords = static_cast<int>(sizeof(DevPred) / 4);
+  static_assert(sizeof(DevPred) % 4 == 0 && sizeof(DevPred) / 4 <= 64, "one dword per lane");
+  if (lane < kWords) reinterpret_cast<uint32_t*>(dst)[lane] = reinterpret_cast<const uint32_t*>(src)[lane];
+}
+
 // Kernel launchers (each defined next to its kernel).  All return the HIP
 // error of the launch.
 
@@ -57,8 +65,14 @@ hipError_t launch_gather_attrs(const int32_t* attrs, int64_t n, int n_attr, cons
                                int32_t* attrs_phys, hipStream_t s);
 // Row interval [iv[2q], iv[2q+1]) of each query's cluster-key clauses.
 // Also resets each query's shared scan threshold gthr[q] to all ones.
+// Row interval of every query on the clustered layout (whole index for
+// predicates without a cluster-key interval).  Reads the predicates and the
+// scan order from the staging slot (pinned host memory) and leaves device
+// copies in preds_out / order_out for the kernels that follow; resets the
+// per-query global thresholds.
 hipError_t launch_intervals(const int32_t* attrs_phys, int64_t n, int c0, int c1,
-                            const DevPred* preds, int nq, int64_t* iv, uint64_t* gthr,
+                            const DevPred* staged_preds, const int32_t* staged_order, int nq,
+                            DevPred* preds_out, int32_t* order_out, int64_t* iv, uint64_t* gthr,
                             hipStream_t s);
 
 // codes (row-major [n][m]) -> 64-row tiles, physical row r taken from

@@ -76,13 +76,23 @@ __device__ int64_t wave_lower_bound(const int32_t* __restrict__ a0, const int32_
 }
 
 __global__ __launch_bounds__(64) void intervals_kernel(const int32_t* __restrict__ attrs_phys, int64_t n,
-                                                       int c0, int c1, const DevPred* __restrict__ preds,
-                                                       int nq, int64_t* __restrict__ iv,
+                                                       int c0, int c1, const DevPred* __restrict__ staged_preds,
+                                                       const int32_t* __restrict__ staged_order, int nq,
+                                                       DevPred* __restrict__ preds_out,
+                                                       int32_t* __restrict__ order_out,
+                                                       int64_t* __restrict__ iv,
                                                        uint64_t* __restrict__ gthr) {
   const int q = blockIdx.x >> 1;        // two wavefronts per query: lower and upper bound
   const bool upper = blockIdx.x & 1;
   if (q >= nq) return;
-  const DevPred& p = preds[q];
+  __shared__ DevPred sp;
+  copy_pred(staged_preds + q, &sp, threadIdx.x);
+  __syncthreads();
+  if (!upper) {
+    copy_pred(&sp, preds_out + q, threadIdx.x);
+    if (threadIdx.x == 0) order_out[q] = staged_order[q];
+  }
+  const DevPred& p = sp;
   int64_t r = upper ? n : 0;
   if (p.n_eff < 0) {
     r = 0;
@@ -143,9 +153,11 @@ hipError_t launch_gather_attrs(const int32_t* attrs, int64_t n, int n_attr, cons
 }
 
 hipError_t launch_intervals(const int32_t* attrs_phys, int64_t n, int c0, int c1,
-                            const DevPred* preds, int nq, int64_t* iv, uint64_t* gthr,
+                            const DevPred* staged_preds, const int32_t* staged_order, int nq,
+                            DevPred* preds_out, int32_t* order_out, int64_t* iv, uint64_t* gthr,
                             hipStream_t s) {
-  intervals_kernel<<<dim3(2 * nq), dim3(64), 0, s>>>(attrs_phys, n, c0, c1, preds, nq, iv, gthr);
+  intervals_kernel<<<dim3(2 * nq), dim3(64), 0, s>>>(attrs_phys, n, c0, c1, staged_preds, staged_order, nq,
+                                                     preds_out, order_out, iv, gthr);
   return hipGetLastError();
 }
 

@@ -57,13 +57,17 @@ __global__ __launch_bounds__(64) void condition_kernel(
   // Fingerprint: FNV-1a-64 over q's fp32 bytes, the clause count (int32) and
   // every clause as (col int32, lo int64, hi int64), little-endian.  The
   // row is staged in LDS by all lanes; the fold itself is serial.
+  // The predicate comes from the staging slot (pinned host memory): one
+  // wavefront-wide copy into LDS, then the serial fold reads LDS.
+  __shared__ DevPred sp;
   for (int i = lane; i < dim; i += 64) qbits[i] = __float_as_uint(qrow[i]);
+  copy_pred(preds + qi, &sp, lane);
   __syncthreads();
   uint64_t key = 0;
   if (lane == 0) {
     uint64_t hh = kFnvOffset;
     for (int i = 0; i < dim; ++i) hh = fnv_bytes(hh, qbits[i], 4);
-    const DevPred& p = preds[qi];
+    const DevPred& p = sp;
     hh = fnv_bytes(hh, static_cast<uint32_t>(p.n_raw), 4);
     for (int c = 0; c < p.n_raw; ++c) {
       hh = fnv_bytes(hh, static_cast<uint32_t>(p.raw_col[c]), 4);
