@@ -212,6 +212,10 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
                                      2: time only the scan kernel's launches              */
 #define IFVS_OPT_MIN_CHUNK 4      /* fewest 64-row code tiles per chunk (0 = automatic)      */
 #define IFVS_OPT_GRID_TILES 5     /* chunk grid cell in 64-row tiles (0 = automatic)         */
+#define IFVS_OPT_GATHER 6         /* masked batches: 0 automatic (queries selecting up to 30% of
+                                     the rows, within the row-list capacity, are scored from
+                                     their compacted row list), 1 every query whose list fits,
+                                     2 never (every query takes the tiled scan)               */
 ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value);
 
 /* ifvs_read_profile -- with IFVS_OPT_PROFILE on, every kernel the index

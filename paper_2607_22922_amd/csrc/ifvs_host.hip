@@ -106,6 +106,13 @@ struct ifvs_index {
   unsigned long long* counts = nullptr;  // [max_batch]
   uint64_t* partials = nullptr;  // per-wavefront top-k keys
   size_t partial_keys = 0;
+  // Gather scan of masked batches (null when M has no gather kernel).
+  uint32_t* codes_rm = nullptr;  // [n][rw] row-major code words, physical order
+  int rw = 0;
+  int32_t* lists = nullptr;      // [max_batch][list_cap] selected physical rows
+  int32_t* list_n = nullptr;     // [max_batch]
+  int32_t* qmode = nullptr;      // [max_batch] 1: gather scan
+  int64_t list_cap = 0;
 
   // Every (n / kFences)-th clustered key, copied to the host at load: lets
   // the planner estimate each query's interval length without touching the
@@ -114,6 +121,8 @@ struct ifvs_index {
 
   int opt_qtile = 0, opt_splits = 0, opt_min_chunk = 0;
   int64_t opt_grid_tiles = 0;
+  int opt_gather = 0;   // 0 automatic, 1 every query whose list fits, 2 never
+  int opt_gather_auto_pct = 30;   // automatic mode: pools up to this % of the rows
   int profile_mask = 0;          // stages timed with HIP events (IFVS_OPT_PROFILE)
   StageTimer* timers = nullptr;  // [kStages] once profiling was enabled
   ScanPlan last_plan{};
@@ -132,7 +141,8 @@ struct ifvs_index {
                     static_cast<void*>(perm), static_cast<void*>(bank), static_cast<void*>(W),
                     static_cast<void*>(preds_dev), static_cast<void*>(qorder_dev),
                     static_cast<void*>(iv_dev), static_cast<void*>(gthr_dev), static_cast<void*>(bitmap),
-                    static_cast<void*>(counts), static_cast<void*>(partials)})
+                    static_cast<void*>(counts), static_cast<void*>(partials), static_cast<void*>(codes_rm),
+                    static_cast<void*>(lists), static_cast<void*>(list_n), static_cast<void*>(qmode)})
       if (p) hipFree(p);
     for (int i = 0; i < kStagingSlots; ++i) {
       if (staging[i]) hipHostFree(staging[i]);
@@ -367,6 +377,9 @@ ifvs_status timed(ifvs_index* idx, int stage, hipStream_t s, const char* what, F
     if (st_ != IFVS_OK) return st_;                                                             \
   } while (0)
 
+// Largest pool (rows) the automatic mode scores from a row list.
+int64_t gather_auto_rows(const ifvs_index* idx) { return idx->n * idx->opt_gather_auto_pct / 100; }
+
 // interval_batch: every query has a cluster-key interval; one query per tile
 // then keeps all lanes busy and the scan is bound by LDS lookups, so sharing
 // code tiles across queries would not help.  Otherwise (masked rows) tiles
@@ -542,6 +555,25 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
     hipFree(tmp);
     if (e != hipSuccess) return bail(hip_fail(e, "loading codes"));
   }
+  // Row-major copy of the codes and the row lists for the gather scan.
+  if (gather_supported(d.m, IFVS_LUT_F16)) {
+    idx->rw = gather_row_words(d.m);
+    if ((st = dev_alloc(&idx->codes_rm, static_cast<size_t>(d.n) * idx->rw, "row-major codes")) != IFVS_OK)
+      return bail(st);
+    if (hipError_t e = launch_rowmajor_codes(idx->codes_t, d.n, idx->mw, idx->rw, idx->codes_rm, nullptr);
+        e != hipSuccess)
+      return bail(hip_fail(e, "building row-major codes"));
+    // Lists hold up to 30% of the rows, capped at 2 GiB for the whole batch.
+    const int64_t by_rows = (3 * d.n + 9) / 10;
+    const int64_t by_bytes = std::max<int64_t>(4096, (int64_t(2) << 30) / (4 * static_cast<int64_t>(d.max_batch)));
+    idx->list_cap = std::min<int64_t>(d.n, std::min(by_rows, by_bytes));
+    if ((st = dev_alloc(&idx->lists, static_cast<size_t>(d.max_batch) * idx->list_cap, "row lists")) != IFVS_OK)
+      return bail(st);
+    if ((st = dev_alloc(&idx->list_n, static_cast<size_t>(d.max_batch), "row list sizes")) != IFVS_OK)
+      return bail(st);
+    if ((st = dev_alloc(&idx->qmode, static_cast<size_t>(d.max_batch), "scan modes")) != IFVS_OK)
+      return bail(st);
+  }
   const size_t cb = static_cast<size_t>(d.m) * kKsub * idx->dsub;
   if ((st = dev_alloc(&idx->cpq, cb, "codebook")) != IFVS_OK) return bail(st);
   if (hipError_t e = hipMemcpy(idx->cpq, d.codebook, cb * sizeof(float), kind); e != hipSuccess)
@@ -604,6 +636,10 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
     case IFVS_OPT_SPLITS: idx->opt_splits = static_cast<int>(value); return IFVS_OK;
     case IFVS_OPT_MIN_CHUNK: idx->opt_min_chunk = static_cast<int>(value); return IFVS_OK;
     case IFVS_OPT_GRID_TILES: idx->opt_grid_tiles = value; return IFVS_OK;
+    case IFVS_OPT_GATHER:
+      if (value > 2) return fail(IFVS_E_INVALID, "IFVS_OPT_GATHER takes 0, 1 or 2");
+      idx->opt_gather = static_cast<int>(value);
+      return IFVS_OK;
     case IFVS_OPT_PROFILE:
       if (value != 0 && !idx->timers) {
         idx->timers = new StageTimer[kStages];
@@ -704,8 +740,26 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
                                reinterpret_cast<const int32_t*>(idx->staging_dev[slot] + idx->max_batch), nq,
                                idx->preds_dev, idx->qorder_dev, idx->iv_dev, idx->gthr_dev, s));
   if (ifvs_status st = release_slot(idx, slot, s); st != IFVS_OK) return st;
-  if (need_bitmap)
+  // Masked batches: a query whose pool is small is scored from its compacted
+  // row list (decided on the device from the pool size); the rest take the
+  // tiled scan.  The full selection bitmap (physical order) and the pool
+  // sizes come from the Filter stage.
+  const int gather_lut = lut_dtype == IFVS_LUT_F16 ? 2 : 4;
+  const bool gather = !interval_batch && idx->codes_rm && idx->opt_gather != 2 &&
+                      gather_supported(idx->m, lut_dtype) &&
+                      static_cast<size_t>(idx->m) * kKsub * gather_lut + gather_lds_bytes(plan.pool_stride) <=
+                          static_cast<size_t>(kLdsBudget);
+  if (gather) {
+    IFVS_LAUNCH(idx, kStFilter, s, "launching filter kernel",
+                launch_filter(idx->attrs_phys, idx->n, idx->n_attr, idx->preds_dev, nq, false, idx->bitmap,
+                              idx->stride64, idx->counts, s));
+    const int64_t max_rows = idx->opt_gather == 1 ? idx->list_cap : std::min(idx->list_cap, gather_auto_rows(idx));
+    IFVS_LAUNCH(idx, kStFilter, s, "launching compaction kernel",
+                launch_compact(idx->bitmap, idx->stride64, idx->counts, nq, max_rows, idx->list_cap, idx->lists,
+                               idx->list_n, idx->qmode, s));
+  } else if (need_bitmap) {
     if (ifvs_status st = filter_into_workspace(idx, nq, true, false, s); st != IFVS_OK) return st;
+  }
   ScanBatch b{};
   b.codes_t = idx->codes_t;
   b.n = idx->n;
@@ -724,7 +778,31 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   b.k = k;
   b.partials = idx->partials;
   b.gthr = idx->gthr_dev;
+  b.mode = gather ? idx->qmode : nullptr;
   IFVS_LAUNCH(idx, kStScan, s, "launching scan kernel", launch_scan(b, plan, s));
+  if (gather) {
+    GatherBatch g{};
+    g.codes_rm = idx->codes_rm;
+    g.rw = idx->rw;
+    g.m = idx->m;
+    g.lut = lut;
+    g.lut_dtype = lut_dtype;
+    g.nq = nq;
+    g.qorder = idx->qorder_dev;
+    g.mode = idx->qmode;
+    g.lists = idx->lists;
+    g.list_n = idx->list_n;
+    g.list_cap = idx->list_cap;
+    g.splits = plan.splits;
+    g.gblocks = gather_blocks_per_query(idx->list_cap, plan.splits);
+    g.perm = idx->perm;
+    g.k = k;
+    g.pool_stride = plan.pool_stride;
+    g.kpl = plan.kpl;
+    g.partials = idx->partials;
+    g.gthr = idx->gthr_dev;
+    IFVS_LAUNCH(idx, kStScan, s, "launching gather scan kernel", launch_gather_scan(g, s));
+  }
   const int64_t per_query = static_cast<int64_t>(plan.splits) * kScanWaves * k;
   IFVS_LAUNCH(idx, kStMerge, s, "launching top-k merge kernel",
               launch_topk_merge(idx->partials, nq, per_query, k, idx->qorder_dev, ids_out, dist_out, s));

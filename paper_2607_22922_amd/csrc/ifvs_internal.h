@@ -131,7 +131,41 @@ struct ScanBatch {
   int k;
   uint64_t* partials;           // [nq positions][splits][waves][k]
   uint64_t* gthr;               // [nq] shared thresholds, all-ones before the scan
+  const int32_t* mode;          // [nq] 1: the query is scored by the gather scan (null: none is)
 };
+
+// Gather scan of compacted row lists (masked batches, few selected rows).
+struct GatherBatch {
+  const uint32_t* codes_rm;     // [n][rw] row-major code words, physical order
+  int rw;                       // words per row (16-byte multiple)
+  int m;
+  const void* lut;
+  int lut_dtype;
+  int nq;
+  const int32_t* qorder;
+  const int32_t* mode;
+  const int32_t* lists;         // [nq][list_cap] ascending physical rows
+  const int32_t* list_n;
+  int64_t list_cap;
+  int gblocks;                  // workgroups per query position (<= splits)
+  int splits;
+  const int32_t* perm;
+  int k, pool_stride, kpl;
+  uint64_t* partials;
+  uint64_t* gthr;
+};
+bool gather_supported(int m, int lut_dtype);
+int gather_row_words(int m);
+size_t gather_lds_bytes(int pool_stride);
+int gather_blocks_per_query(int64_t list_cap, int splits);
+hipError_t launch_rowmajor_codes(const uint32_t* codes_t, int64_t n, int mw, int rw, uint32_t* codes_rm,
+                                 hipStream_t s);
+// Per query: mode (1 when its pool holds at most max_rows rows; max_rows < 0:
+// never) and, for those, the ascending list of selected physical rows.
+hipError_t launch_compact(const uint64_t* bitmap, int64_t stride64, const unsigned long long* counts, int nq,
+                          int64_t max_rows, int64_t list_cap, int32_t* lists, int32_t* list_n, int32_t* mode,
+                          hipStream_t s);
+hipError_t launch_gather_scan(const GatherBatch& b, hipStream_t s);
 
 hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s);
 

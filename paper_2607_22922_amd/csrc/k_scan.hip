@@ -60,6 +60,7 @@ struct ScanArgs {
   int64_t chunk_tiles;   // > 0: chunks on a grid of this many tiles (see below)
   uint64_t* partials;
   uint64_t* gthr;   // [nq] per original query: smallest k-th key any wavefront has published
+  const int32_t* mode;   // [nq] 1: scored by the gather scan instead (null: none)
 };
 
 // Bits [lo, hi) of a 64-bit word, 0 <= lo < hi <= 64.
@@ -125,6 +126,7 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
       qid[qi] = a.qorder[q0 + qi];
       r0[qi] = a.iv[2 * qid[qi]];
       r1[qi] = a.iv[2 * qid[qi] + 1];
+      if (a.mode && a.mode[qid[qi]] == 1) r1[qi] = r0[qi];   // the gather scan scores it
       resid[qi] = a.preds[qid[qi]].residual_mask != 0;
       if (r1[qi] > r0[qi]) {
         hull_lo = min(hull_lo, r0[qi]);
@@ -510,6 +512,7 @@ hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s) 
   a.kpl = plan.kpl;
   a.min_chunk = plan.min_chunk;
   a.chunk_tiles = plan.chunk_tiles;
+  a.mode = b.mode;
   a.partials = b.partials;
   a.gthr = b.gthr;
   a.splits = plan.splits;

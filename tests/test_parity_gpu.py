@@ -298,6 +298,40 @@ def test_clustered_chunk_grid_and_fallback(B, cols):
     idx.set_option(B.OPT_SPLITS, 0)
 
 
+@pytest.mark.parametrize("cluster_cols,M,dsub,k,lut_dtype", [((), 16, 8, 10, "f32"), ((), 48, 2, 100, "f32"),
+                                                         ((), 16, 8, 37, "f16"), ((1,), 48, 2, 10, "f32")])
+def test_gather_scan_matches_oracle(B, cluster_cols, M, dsub, k, lut_dtype):
+    """Masked batches: queries scored from their compacted row lists (forced
+    on, automatic, forced off) give the oracle's ids and distance bits, with
+    pools from empty to the whole index."""
+    say(f"[gather] cols={cluster_cols} M={M} k={k} {lut_dtype}")
+    idx, ox = _edge_index(B, 30_000, M, dsub, n_attr=2, domain=40, seed=53, cluster_cols=cluster_cols)
+    preds = [[(0, 3, 4)], [(0, 0, 40)], [(1, 5, 7), (0, 2, 30)], [], [(0, 9, 9)], [(1, 0, 1), (0, 39, 40)],
+             [(0, 10, 30)], [(1, 17, 18)], [(0, 5, 6), (1, 5, 6)], [(1, 0, 20)]] * 2
+    g = torch.Generator(device="cuda").manual_seed(7)
+    q = torch.randn(len(preds), M * dsub, device="cuda", generator=g)
+    dt = B.LUT_F16 if lut_dtype == "f16" else B.LUT_F32
+    alpha, wf = idx.select_codebook(q, preds, None)
+    lut = idx.build_lut(q, alpha, wf, dt)
+    outs = {}
+    for mode in (1, 0, 2):
+        idx.set_option(B.OPT_GATHER, mode)
+        ids, dist = idx.search(preds, lut, k, dt)
+        torch.cuda.synchronize()
+        outs[mode] = (_np(ids), _np(dist))
+    idx.set_option(B.OPT_GATHER, 0)
+    for i, p in enumerate(preds[:10]):
+        lut_o = O.build_lut(_np(q[i]), _np(alpha[i]), _np(wf[i]), ox["C_pq"], ox["W"], M, ox["r"],
+                            lut_dtype=lut_dtype)
+        cand = O.passing_ids(O.predicate_mask(ox["attrs"], p))
+        ids_o, dist_o = O.select_topk(O.adc_distances(lut_o.astype(np.float32), ox["codes"], cand), cand, k)
+        for mode, (ids, dist) in outs.items():
+            check_search_row(ids[i], dist[i], ids_o, dist_o, f"gather={mode} q{i} {p}")
+    for mode in (0, 2):
+        assert np.array_equal(outs[mode][0], outs[1][0])
+        assert np.array_equal(outs[mode][1].view(np.uint32), outs[1][1].view(np.uint32))
+
+
 def test_clustered_ties_break_by_original_id(B):
     ix = random_index(6000, 16, 8, 1, 40, 41, device="cuda")
     ix["codes"][::7] = ix["codes"][3]                 # equal rows in every cluster
