@@ -91,11 +91,33 @@ def test_other_calls_validate(B, small):
     assert st == B.E_INVALID
     st, _ = _status(B, lib.ifvs_set_option, idx.handle, B.OPT_QTILE, -1)
     assert st == B.E_INVALID
+    for opt, bad in ((B.OPT_PROFILE, 3), (B.OPT_GATHER, 3), (B.OPT_GRID_TILES, -5)):
+        st, msg = _status(B, lib.ifvs_set_option, idx.handle, opt, bad)
+        assert st == B.E_INVALID, (opt, bad, msg)
+    for opt, good in ((B.OPT_GATHER, 2), (B.OPT_GATHER, 0), (B.OPT_GRID_TILES, 0)):
+        assert lib.ifvs_set_option(idx.handle, opt, good) == B.OK
     for fn, args in ((lib.ifvs_filtered_search, (None, 1, None, None, 0, 1, None, None, None, None)),
                      (lib.ifvs_build_lut, (None, 1, None, None, None, 0, None, None))):
         assert fn(*args) == B.E_STATE
     # nq = 0 is a no-op
     assert lib.ifvs_filtered_search(idx.handle, 0, None, None, 0, 10, None, None, None, None) == B.OK
+
+
+def test_profile_modes(B, small):
+    """IFVS_OPT_PROFILE 1 times every kernel launch, 2 only the scan's."""
+    idx, q, lut = small
+    preds = [[(0, 0, 10)]] * 4
+    for mode, timed in ((1, {"condition", "lut", "filter", "scan", "merge"}), (2, {"scan"})):
+        idx.set_option(B.OPT_PROFILE, mode)
+        idx.read_profile()
+        a, f = idx.select_codebook(q, preds, None)
+        lt = idx.build_lut(q, a, f)
+        idx.search(preds, lt, 10)
+        prof = idx.read_profile()
+        got = {st for st, (ms, n) in prof.items() if n > 0}
+        assert got == timed, (mode, prof)
+        assert all(ms >= 0.0 for ms, _ in prof.values())
+    idx.set_option(B.OPT_PROFILE, 0)
 
 
 def test_load_validation(B):
