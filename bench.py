@@ -247,6 +247,8 @@ def main():
         b_gbps = b_bytes / (b_ms / max(1, b_n) / 1e3) / 1e9
         bins_out[str(s)] = {"qps": batch * len(ms) / (sum(ms) / 1e3),
                             "ms_per_batch": float(np.median(ms)),
+                            "ms_per_batch_p10_p90": [round(float(np.percentile(ms, 10)), 4),
+                                                     round(float(np.percentile(ms, 90)), 4)],
                             "realized_selectivity": round(sel, 5),
                             "scan_ms": round(b_ms / max(1, b_n), 4),
                             "scan_GBps": round(b_gbps, 1),
@@ -376,6 +378,8 @@ def main():
         "stage_ms_per_step": {st: round(v[0] / stage_steps, 4) for st, v in stage_prof.items()},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
+                     "traffic_over_algorithmic": (round(traffic / bytes_per_launch, 4)
+                                                  if traffic is not None else None),
                      "kernel": "scan_kernel", "avg_launch_ms": scan_avg_ms,
                      "bytes_per_launch": bytes_per_launch,
                      "useful_bytes_per_launch": useful_total / max(1, scan_launches)},
