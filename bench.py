@@ -93,18 +93,30 @@ def exact_filtered_knn(x, attrs, queries, preds, k, chunk=1 << 21):
     return best_i, best_d
 
 
-def scan_bytes_interval(w, sorted_attr, preds, splits, k, lut_entry):
+SCAN_WAVES = 8   # wavefronts per scan workgroup, each writing k partial keys per chunk
+
+
+def scan_bytes_interval(w, sorted_attr, preds, plan, k, lut_entry):
     """Algorithmic bytes of one interval-scan launch (one query per tile):
     the code tiles overlapping each query's row interval, its table, and its
-    partial top-k lists."""
+    partial top-k lists (one per wavefront for every chunk written: with an
+    absolute chunk grid only the cells the interval touches)."""
     lo = torch.tensor([p[0][1] for p in preds], device=sorted_attr.device, dtype=sorted_attr.dtype)
     hi = torch.tensor([p[0][2] for p in preds], device=sorted_attr.device, dtype=sorted_attr.dtype)
     r0 = torch.searchsorted(sorted_attr, lo)
     r1 = torch.searchsorted(sorted_attr, hi)
-    tiles = torch.where(r1 > r0, (r1 + 63) // 64 - r0 // 64, torch.zeros_like(r0))
+    nonempty = r1 > r0
+    tiles = torch.where(nonempty, (r1 + 63) // 64 - r0 // 64, torch.zeros_like(r0))
     mw = (w.M + 3) // 4
     code = float(tiles.sum()) * 64 * mw * 4
-    return code + len(preds) * (w.M * 256 * lut_entry + splits * 4 * k * 8), float((r1 - r0).sum()) * w.M
+    g = plan.get("grid_tiles", 0)
+    if g and plan["splits"] * g >= (w.N + 63) // 64:   # absolute cells: one chunk per cell of the index
+        cells = torch.where(nonempty, ((r1 + 63) // 64 - 1) // g - (r0 // 64) // g + 1, torch.zeros_like(r0))
+        chunks = float(cells.sum())
+    else:
+        chunks = float(len(preds) * plan["splits"])
+    return (code + len(preds) * w.M * 256 * lut_entry + chunks * SCAN_WAVES * k * 8,
+            float((r1 - r0).sum()) * w.M)
 
 
 def scan_bytes_bitmap(idx, w, preds, qt, splits, k, lut_entry):
@@ -121,7 +133,7 @@ def scan_bytes_bitmap(idx, w, preds, qt, splits, k, lut_entry):
     mw = (w.M + 3) // 4
     code = float(any_t.sum()) * 64 * mw * 4
     nq = len(preds)
-    return code + nq * (n_tiles * 8 + w.M * 256 * lut_entry + splits * 4 * k * 8), float(cnt.sum()) * w.M
+    return code + nq * (n_tiles * 8 + w.M * 256 * lut_entry + splits * SCAN_WAVES * k * 8), float(cnt.sum()) * w.M
 
 
 def main():
@@ -232,12 +244,11 @@ def main():
     bins_out = {}
     scan_bytes_total = useful_total = 0.0
     for s in bins:
-        splits = plans[s]["splits"]
         cache = {}
         for b, _ in per_bin[s]:
             if b not in cache:
                 cache[b] = scan_bytes_interval(w, sorted_attr, w.preds[s][b * batch:(b + 1) * batch],
-                                               splits, k, lut_entry)
+                                               plans[s], k, lut_entry)
             scan_bytes_total += cache[b][0]
             useful_total += cache[b][1]
         ms = [m for _, m in per_bin[s]]

@@ -202,9 +202,10 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
  * a query tile is cut into (0 = automatic).  IFVS_OPT_GRID_TILES forces the
  * chunk grid of clustered-index scans (0 = automatic: a grid of about 5120
  * tiles when the widest interval spans 8192 or more 64-row tiles, else none):
- * chunk c of a query tile is then grid cell (first cell of its span) + c,
- * and a span needing more cells than there are chunks is cut into equal
- * chunks instead.  Results never depend on these knobs.
+ * chunk c of a query tile is then absolute grid cell c (every XCD walks the
+ * same cells), or with IFVS_OPT_GRID_RELATIVE grid cell (first cell of its
+ * span) + c; a span needing more cells than there are chunks is cut into
+ * equal chunks instead.  Results never depend on these knobs.
  * Errors: IFVS_E_INVALID for an unknown option or a negative value. */
 #define IFVS_OPT_QTILE  1
 #define IFVS_OPT_SPLITS 2
@@ -212,6 +213,8 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
                                      2: time only the scan kernel's launches              */
 #define IFVS_OPT_MIN_CHUNK 4      /* fewest 64-row code tiles per chunk (0 = automatic)      */
 #define IFVS_OPT_GRID_TILES 5     /* chunk grid cell in 64-row tiles (0 = automatic)         */
+#define IFVS_OPT_GRID_RELATIVE 7  /* 1: chunk c of a query tile is cell (its first cell) + c
+                                     instead of absolute cell c of the grid                 */
 #define IFVS_OPT_GATHER 6         /* masked batches: 0 automatic (queries selecting up to 30% of
                                      the rows, within the row-list capacity, are scored from
                                      their compacted row list), 1 every query whose list fits,

@@ -122,6 +122,7 @@ struct ifvs_index {
   int opt_qtile = 0, opt_splits = 0, opt_min_chunk = 0;
   int64_t opt_grid_tiles = 0;
   int opt_gather = 0;   // 0 automatic, 1 every query whose list fits, 2 never
+  int opt_grid_relative = 0;   // 1: grid chunks relative to each query tile's first cell
   int opt_gather_auto_pct = 30;   // automatic mode: pools up to this % of the rows
   int profile_mask = 0;          // stages timed with HIP events (IFVS_OPT_PROFILE)
   StageTimer* timers = nullptr;  // [kStages] once profiling was enabled
@@ -406,6 +407,7 @@ ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_
   // chunks per query tile.
   int64_t splits = (4096 + gy - 1) / gy;
   plan->chunk_tiles = 0;
+  plan->abs_cells = false;
   if (interval_batch) {
     // Long spans (>= 8192 tiles) are cut on a chunk grid of cells of about
     // 5K tiles (measured best between 4K and 5K on 10M x 48-byte codes), so
@@ -418,7 +420,14 @@ ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_
       const int64_t cells = (span_tiles + 5119) / 5120;
       plan->chunk_tiles = (span_tiles + cells - 1) / cells;
     }
-    if (plan->chunk_tiles > 0)
+    // Chunk c is absolute cell c of the grid: every XCD walks the same cells
+    // at the same time, so one HBM read of a cell can serve the other XCDs
+    // from the Infinity Cache.  Cells a query's interval misses cost one
+    // empty workgroup each.
+    plan->abs_cells = plan->chunk_tiles > 0 && idx->opt_grid_relative == 0;
+    if (plan->abs_cells)
+      splits = (idx->n_tiles + plan->chunk_tiles - 1) / plan->chunk_tiles;
+    else if (plan->chunk_tiles > 0)
       splits = (span_tiles + plan->chunk_tiles - 1) / plan->chunk_tiles + 1;
     else
       splits = std::min<int64_t>(16, std::max<int64_t>((span_tiles + 8191) / 8192, (512 + gy - 1) / gy));
@@ -428,6 +437,12 @@ ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_
   const int64_t cap = static_cast<int64_t>(idx->partial_keys /
                                            (static_cast<size_t>(std::max(1, nq)) * kScanWaves * k));
   splits = std::max<int64_t>(1, std::min<int64_t>(splits, std::min<int64_t>(cap, 65535)));
+  if (plan->abs_cells && splits != (idx->n_tiles + plan->chunk_tiles - 1) / plan->chunk_tiles) {
+    // Absolute cells need exactly one chunk per cell (a forced chunk count
+    // or too little partial-list room): chunks relative to each query tile,
+    // which handle any count.
+    plan->abs_cells = false;
+  }
   plan->splits = static_cast<int>(splits);
   plan->kpl = pool_kpl(k);
   plan->pool_stride = pool_stride_for(k);
@@ -636,6 +651,10 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
     case IFVS_OPT_SPLITS: idx->opt_splits = static_cast<int>(value); return IFVS_OK;
     case IFVS_OPT_MIN_CHUNK: idx->opt_min_chunk = static_cast<int>(value); return IFVS_OK;
     case IFVS_OPT_GRID_TILES: idx->opt_grid_tiles = value; return IFVS_OK;
+    case IFVS_OPT_GRID_RELATIVE:
+      if (value > 1) return fail(IFVS_E_INVALID, "IFVS_OPT_GRID_RELATIVE takes 0 or 1");
+      idx->opt_grid_relative = static_cast<int>(value);
+      return IFVS_OK;
     case IFVS_OPT_GATHER:
       if (value > 2) return fail(IFVS_E_INVALID, "IFVS_OPT_GATHER takes 0, 1 or 2");
       idx->opt_gather = static_cast<int>(value);
@@ -805,7 +824,9 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   }
   const int64_t per_query = static_cast<int64_t>(plan.splits) * kScanWaves * k;
   IFVS_LAUNCH(idx, kStMerge, s, "launching top-k merge kernel",
-              launch_topk_merge(idx->partials, nq, per_query, k, idx->qorder_dev, ids_out, dist_out, s));
+              launch_topk_merge(idx->partials, nq, per_query, k, idx->iv_dev,
+                                plan.abs_cells ? plan.chunk_tiles : 0, static_cast<int64_t>(kScanWaves) * k,
+                                idx->qorder_dev, ids_out, dist_out, s));
   if (bitmap_out) {
     // The Filter stage's bitmaps in id order (the scan itself reads row
     // intervals and residual bits in the physical order).

@@ -103,6 +103,7 @@ struct ScanPlan {
   int kpl;          // pool keys per lane when it is sorted
   size_t lds_bytes;
   int64_t chunk_tiles;  // > 0: chunk grid cell in tiles (interval scans); 0: equal chunks
+  bool abs_cells;       // chunk c is absolute grid cell c (splits = cells of the whole index)
 };
 
 // Largest query tile whose tables and pools fit the LDS budget (0 if none).
@@ -170,6 +171,7 @@ hipError_t launch_gather_scan(const GatherBatch& b, hipStream_t s);
 hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s);
 
 hipError_t launch_topk_merge(const uint64_t* partials, int nq, int64_t per_query, int k,
+                             const int64_t* iv, int64_t cell_tiles, int64_t slot_keys,
                              const int32_t* qorder, int32_t* ids_out, float* dist_out,
                              hipStream_t s);
 

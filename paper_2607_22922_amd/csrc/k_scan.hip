@@ -58,6 +58,7 @@ struct ScanArgs {
   const int32_t* perm;
   int k, pool_stride, kpl, min_chunk;
   int64_t chunk_tiles;   // > 0: chunks on a grid of this many tiles (see below)
+  int abs_cells;         // 1: chunk c is absolute grid cell c (all XCDs walk the same cells)
   uint64_t* partials;
   uint64_t* gthr;   // [nq] per original query: smallest k-th key any wavefront has published
   const int32_t* mode;   // [nq] 1: scored by the gather scan instead (null: none)
@@ -143,7 +144,10 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
   if (hull_hi > hull_lo) {
     const int64_t t_lo = hull_lo / 64, t_hi = (hull_hi + 63) / 64;
     const int64_t g = a.chunk_tiles;
-    if (g > 0 && (t_hi - 1) / g - t_lo / g < a.splits) {
+    if (g > 0 && a.abs_cells) {
+      t_begin = max(t_lo, chunk * g);
+      t_end = min(t_hi, (chunk + 1) * g);
+    } else if (g > 0 && (t_hi - 1) / g - t_lo / g < a.splits) {
       const int64_t cell = t_lo / g + chunk;
       t_begin = max(t_lo, cell * g);
       t_end = min(t_hi, (cell + 1) * g);
@@ -169,7 +173,10 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
     lt[qi] = any ? static_cast<int>((r1[qi] - 1) >> 6) : -1;
   }
   if (!work) {
-    // Nothing selected in this chunk: empty partial lists.
+    // Nothing selected in this chunk: empty partial lists (with absolute
+    // cells the merge reads only the cells a query's interval touches, so
+    // there is nothing to write).
+    if (a.abs_cells) return;
     for (int qi = 0; qi < qn; ++qi) {
       uint64_t* dst = a.partials + ((static_cast<size_t>(q0 + qi) * a.splits + chunk) * kScanWaves + wave) * k;
       for (int e = lane; e < k; e += 64) dst[e] = kNoKey;
@@ -512,6 +519,7 @@ hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s) 
   a.kpl = plan.kpl;
   a.min_chunk = plan.min_chunk;
   a.chunk_tiles = plan.chunk_tiles;
+  a.abs_cells = plan.abs_cells ? 1 : 0;
   a.mode = b.mode;
   a.partials = b.partials;
   a.gthr = b.gthr;

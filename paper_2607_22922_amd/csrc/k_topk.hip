@@ -6,6 +6,9 @@
 // One wavefront per query streams its partial keys through the same
 // threshold-filtered pool used by the scan; the partial lists are each sorted,
 // so after the first few lists almost every key is rejected by one compare.
+// When the scan's chunks are absolute cells of a grid, only the slots of the
+// cells the query's row interval touches are read (the scan leaves the others
+// unwritten).
 #include "ifvs_internal.h"
 #include "topk_device.h"
 
@@ -15,6 +18,8 @@ namespace {
 
 __global__ __launch_bounds__(64) void topk_merge_kernel(const uint64_t* __restrict__ partials,
                                                         int64_t per_query, int k, int kpl,
+                                                        const int64_t* __restrict__ iv,
+                                                        int64_t cell_tiles, int64_t slot_keys,
                                                         const int32_t* __restrict__ qorder,
                                                         int32_t* __restrict__ ids_out,
                                                         float* __restrict__ dist_out) {
@@ -25,9 +30,18 @@ __global__ __launch_bounds__(64) void topk_merge_kernel(const uint64_t* __restri
   int cnt = 0;
   uint64_t thr = kNoKey;
   const uint64_t* src = partials + static_cast<size_t>(pos) * per_query;
-  for (int64_t b = 0; b < per_query; b += 64) {
+  int64_t first = 0, end = per_query;
+  if (cell_tiles > 0) {
+    const int64_t r0 = iv[2 * q], r1 = iv[2 * q + 1];
+    first = end = 0;
+    if (r1 > r0) {
+      first = min(per_query, (r0 / 64) / cell_tiles * slot_keys);
+      end = min(per_query, ((r1 + 63) / 64 - 1) / cell_tiles * slot_keys + slot_keys);
+    }
+  }
+  for (int64_t b = first; b < end; b += 64) {
     const int64_t i = b + lane;
-    const uint64_t key = i < per_query ? src[i] : kNoKey;
+    const uint64_t key = i < end ? src[i] : kNoKey;
     pool_push(pool, cnt, thr, key, key < thr, k, kpl);
   }
   pool_compact(pool, cnt, thr, k, kpl);
@@ -47,12 +61,13 @@ __global__ __launch_bounds__(64) void topk_merge_kernel(const uint64_t* __restri
 }  // namespace
 
 hipError_t launch_topk_merge(const uint64_t* partials, int nq, int64_t per_query, int k,
+                             const int64_t* iv, int64_t cell_tiles, int64_t slot_keys,
                              const int32_t* qorder, int32_t* ids_out, float* dist_out,
                              hipStream_t s) {
   const int kpl = pool_kpl(k);
   const size_t lds = static_cast<size_t>(64 * kpl) * sizeof(uint64_t);
-  topk_merge_kernel<<<dim3(nq), dim3(64), lds, s>>>(partials, per_query, k, kpl, qorder, ids_out,
-                                                    dist_out);
+  topk_merge_kernel<<<dim3(nq), dim3(64), lds, s>>>(partials, per_query, k, kpl, iv, cell_tiles,
+                                                    slot_keys, qorder, ids_out, dist_out);
   return hipGetLastError();
 }
 
