@@ -10,9 +10,10 @@
 // Layout: one workgroup per (subspace, chunk of queries), one thread per
 // centroid c.  A thread keeps its codeword C_PQ[m][c] and its r x d slice of
 // W in registers for the whole query chunk, so W and C_PQ are read once per
-// chunk; the query's q, w_f and alpha values are the same for the whole
-// workgroup (scalar loads).  The 256 entries of one (query, m) row are one
-// coalesced 1 KB (fp32) or 512 B (binary16) store.  The contraction over r is
+// chunk.  The chunk's q, w_f and alpha values (the same for every thread)
+// are loaded once, all in flight together, into LDS and read back as
+// broadcasts.  The 256 entries of one (query, m) row are one coalesced 1 KB
+// (fp32) or 512 B (binary16) store.  The contraction over r is
 // 8 deep and d is 2..8, far too shallow for matrix cores; the kernel is
 // store-bound in the identity mode and a few microseconds per batch otherwise.
 #include "ifvs_internal.h"
@@ -47,16 +48,26 @@ __global__ __launch_bounds__(256) void lut_fixed_kernel(
       for (int j = 0; j < DSUB; ++j)
         wreg[t][j] = W[((static_cast<int64_t>(m) * R + t) * kKsub + c) * DSUB + j];
   }
+  // Per-query operands of the chunk: q and w_f (DSUB each) and alpha (R).
+  constexpr int kPer = 2 * DSUB + R;
+  __shared__ float s_op[kQueriesPerBlock][kPer];
   const int q_begin = blockIdx.y * kQueriesPerBlock;
   const int q_end = min(nq, q_begin + kQueriesPerBlock);
-  for (int qi = q_begin; qi < q_end; ++qi) {
-    const float* qv = q + static_cast<int64_t>(qi) * dim + m * DSUB;
-    const float* wv = wf ? wf + static_cast<int64_t>(qi) * dim + m * DSUB : nullptr;
-    float areg[R > 0 ? R : 1];
-    if constexpr (R > 0) {
 #pragma unroll
-      for (int t = 0; t < R; ++t) areg[t] = alpha[(static_cast<int64_t>(qi) * M + m) * R + t];
+  for (int idx = c; idx < kQueriesPerBlock * kPer; idx += 256) {
+    const int k = idx / kPer, o = idx % kPer;
+    const int qi = q_begin + k;
+    if (qi < q_end) {
+      float v;
+      if (o < DSUB) v = q[static_cast<int64_t>(qi) * dim + m * DSUB + o];
+      else if (o < 2 * DSUB) v = wf ? wf[static_cast<int64_t>(qi) * dim + m * DSUB + (o - DSUB)] : 1.0f;
+      else v = alpha[(static_cast<int64_t>(qi) * M + m) * R + (o - 2 * DSUB)];
+      s_op[k][o] = v;
     }
+  }
+  __syncthreads();
+  for (int qi = q_begin; qi < q_end; ++qi) {
+    const float* op = s_op[qi - q_begin];
     float acc = 0.0f;
 #pragma unroll
     for (int j = 0; j < DSUB; ++j) {
@@ -64,12 +75,11 @@ __global__ __launch_bounds__(256) void lut_fixed_kernel(
       if constexpr (R > 0) {
         float delta = 0.0f;
 #pragma unroll
-        for (int t = 0; t < R; ++t) delta = __fadd_rn(delta, __fmul_rn(areg[t], wreg[t][j]));
+        for (int t = 0; t < R; ++t) delta = __fadd_rn(delta, __fmul_rn(op[2 * DSUB + t], wreg[t][j]));
         C = __fadd_rn(C, delta);
       }
-      const float e = __fsub_rn(qv[j], C);
-      const float w = wv ? wv[j] : 1.0f;
-      acc = __fadd_rn(acc, __fmul_rn(w, __fmul_rn(e, e)));
+      const float e = __fsub_rn(op[j], C);
+      acc = __fadd_rn(acc, __fmul_rn(op[DSUB + j], __fmul_rn(e, e)));
     }
     store_entry(out, (static_cast<int64_t>(qi) * M + m) * kKsub + c, acc);
   }
