@@ -93,7 +93,7 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
   }
   unsigned long long* s_thr = reinterpret_cast<unsigned long long*>(
       pools + static_cast<size_t>(kScanWaves) * QT * a.pool_stride);   // smallest k-th key published in this workgroup
-  uint32_t* s_not_monotone = reinterpret_cast<uint32_t*>(s_thr + QT);
+  uint32_t* s_bad = reinterpret_cast<uint32_t*>(s_thr + QT);   // [wave][qi]: the wave saw a negative or NaN entry
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -113,18 +113,43 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
   const int qn = min(QT, a.nq - q0);
   const int k = a.k;
 
-  // The tile's queries, their row intervals, and the chunk of this workgroup.
+  // The tile's queries.
   int qid[QT];
+#pragma unroll
+  for (int qi = 0; qi < QT; ++qi) qid[qi] = qi < qn ? a.qorder[q0 + qi] : 0;
+
+  // Their tables (global [q][m][c]).  With M fixed at compile time every
+  // load of the staging is issued here, so the tables, the intervals below
+  // and the first code tile are all in flight together; the words land in
+  // LDS further down.
+  constexpr int kThreads = kScanWaves * 64;
+  constexpr int kVec = 16 / sizeof(LutT);
+  constexpr int kVecQ = (MT > 0 ? MT : 1) * kKsub / kVec;   // 16-byte vectors per table
+  constexpr int kLutPer = MT > 0 ? (kVecQ + kThreads - 1) / kThreads : 1;
+  const LutT* lut = static_cast<const LutT*>(a.lut);
+  uint4 lx[QT][kLutPer];
+  if constexpr (MT > 0) {
+#pragma unroll
+    for (int qi = 0; qi < QT; ++qi) {
+      if (qi >= qn) break;
+      const uint4* src = reinterpret_cast<const uint4*>(lut + static_cast<size_t>(qid[qi]) * M * kKsub);
+#pragma unroll
+      for (int u = 0; u < kLutPer; ++u) {
+        const int v = threadIdx.x + u * kThreads;
+        if (kVecQ % kThreads == 0 || v < kVecQ) lx[qi][u] = src[v];
+      }
+    }
+  }
+
+  // Their row intervals, and the chunk of this workgroup.
   int64_t r0[QT], r1[QT];
   bool resid[QT];
   int64_t hull_lo = INT64_MAX, hull_hi = 0;
 #pragma unroll
   for (int qi = 0; qi < QT; ++qi) {
-    qid[qi] = 0;
     r0[qi] = r1[qi] = 0;
     resid[qi] = false;
     if (qi < qn) {
-      qid[qi] = a.qorder[q0 + qi];
       r0[qi] = a.iv[2 * qid[qi]];
       r1[qi] = a.iv[2 * qid[qi] + 1];
       if (a.mode && a.mode[qid[qi]] == 1) r1[qi] = r0[qi];   // the gather scan scores it
@@ -184,47 +209,6 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
     return;
   }
 
-  // Stage the tile's tables: global [q][m][c] -> LDS [m][qi][c], noting any
-  // entry that is negative or NaN (then partial sums are no lower bound).
-  if (threadIdx.x < QT) {
-    s_not_monotone[threadIdx.x] = 0;
-    s_thr[threadIdx.x] = kNoKey;
-  }
-  __syncthreads();
-  constexpr int kVec = 16 / sizeof(LutT);
-  const int vec_per_query = M * kKsub / kVec;
-  const LutT* lut = static_cast<const LutT*>(a.lut);
-  for (int qi = 0; qi < qn; ++qi) {
-    const uint4* src = reinterpret_cast<const uint4*>(lut + static_cast<size_t>(qid[qi]) * M * kKsub);
-    bool bad = false;
-    for (int v = threadIdx.x; v < vec_per_query; v += kScanWaves * 64) {
-      const int e = v * kVec;
-      const int m = e / kKsub, c = e % kKsub;
-      const uint4 x = src[v];
-      *reinterpret_cast<uint4*>(slut + (static_cast<size_t>(m) * QT + qi) * kKsub + c) = x;
-      const LutT* xe = reinterpret_cast<const LutT*>(&x);
-#pragma unroll
-      for (int u = 0; u < kVec; ++u) bad = bad || !(widen(xe[u]) >= 0.0f);
-    }
-    if (bad) atomicOr(&s_not_monotone[qi], 1u);
-  }
-  __syncthreads();
-  // Early abandonment: every entry >= 0 and fp32 addition of non-negative
-  // terms never decreases, so a partial sum above the current k-th distance
-  // bounds the full sum from below and the row cannot enter the top k.
-  bool monotone[QT];
-#pragma unroll
-  for (int qi = 0; qi < QT; ++qi) monotone[qi] = qi < qn && s_not_monotone[qi] == 0;
-
-  int cnt[QT];
-  uint64_t thr[QT];
-#pragma unroll
-  for (int qi = 0; qi < QT; ++qi) {
-    cnt[qi] = 0;
-    thr[qi] = kNoKey;
-  }
-  uint64_t* my_pools = pools + static_cast<size_t>(wave) * QT * a.pool_stride;
-
   // Selection word of query qi for tile t: interval bits (all ones inside
   // the interval, computed only on its first and last tile), and bitmap
   // bits when the query has residual clauses.
@@ -245,6 +229,93 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
     }
     return any;
   };
+
+  // Software pipeline over two register sets (fixed M): while the tile in
+  // one set is summed, the next selected tile's code words load into the
+  // other (no register copy, so nothing waits for the loads in flight).
+  auto next_selected = [&](int t, uint64_t (&bm)[QT]) -> int {
+    while (t < te && tile_masks(t, bm) == 0) t += kScanWaves;
+    return t;
+  };
+  // Past the chunk's end the loads repeat its last tile (in bounds, unused).
+  auto load_tile = [&](int t, uint32_t (&w)[kMW]) {
+    const int tc = t < te ? t : te - 1;
+    const uint32_t* __restrict__ tile = a.codes_t + static_cast<size_t>(tc) * (kMW * 64);
+#pragma unroll
+    for (int j = 0; j < kMW; ++j) w[j] = tile[j * 64 + lane];
+  };
+  uint64_t bma[QT], bmb[QT];
+  uint32_t wa[kMW], wb[kMW];
+  int ta = 0;
+  if constexpr (MT > 0) {
+    ta = next_selected(tb + wave, bma);
+    load_tile(ta, wa);
+  }
+
+  // Tables into LDS as [m][qi][c], noting any entry that is negative or NaN
+  // (then partial sums are no lower bound).
+  bool bad[QT];
+#pragma unroll
+  for (int qi = 0; qi < QT; ++qi) bad[qi] = false;
+  if constexpr (MT > 0) {
+#pragma unroll
+    for (int qi = 0; qi < QT; ++qi) {
+      if (qi >= qn) break;
+#pragma unroll
+      for (int u = 0; u < kLutPer; ++u) {
+        const int v = threadIdx.x + u * kThreads;
+        if (kVecQ % kThreads == 0 || v < kVecQ) {
+          const int e = v * kVec;
+          const int m = e / kKsub, c = e % kKsub;
+          *reinterpret_cast<uint4*>(slut + (static_cast<size_t>(m) * QT + qi) * kKsub + c) = lx[qi][u];
+          const LutT* xe = reinterpret_cast<const LutT*>(&lx[qi][u]);
+#pragma unroll
+          for (int w = 0; w < kVec; ++w) bad[qi] = bad[qi] || !(widen(xe[w]) >= 0.0f);
+        }
+      }
+    }
+  } else {
+    const int vec_per_query = M * kKsub / kVec;
+    for (int qi = 0; qi < qn; ++qi) {
+      const uint4* src = reinterpret_cast<const uint4*>(lut + static_cast<size_t>(qid[qi]) * M * kKsub);
+      for (int v = threadIdx.x; v < vec_per_query; v += kThreads) {
+        const int e = v * kVec;
+        const int m = e / kKsub, c = e % kKsub;
+        const uint4 x = src[v];
+        *reinterpret_cast<uint4*>(slut + (static_cast<size_t>(m) * QT + qi) * kKsub + c) = x;
+        const LutT* xe = reinterpret_cast<const LutT*>(&x);
+#pragma unroll
+        for (int w = 0; w < kVec; ++w) bad[qi] = bad[qi] || !(widen(xe[w]) >= 0.0f);
+      }
+    }
+  }
+#pragma unroll
+  for (int qi = 0; qi < QT; ++qi) {
+    const bool wave_bad = __ballot(bad[qi]) != 0;
+    if (lane == 0) s_bad[wave * QT + qi] = wave_bad ? 1u : 0u;
+  }
+  if (threadIdx.x < QT) s_thr[threadIdx.x] = kNoKey;
+  __syncthreads();
+  // Early abandonment: every entry >= 0 and fp32 addition of non-negative
+  // terms never decreases, so a partial sum above the current k-th distance
+  // bounds the full sum from below and the row cannot enter the top k.
+  bool monotone[QT];
+#pragma unroll
+  for (int qi = 0; qi < QT; ++qi) {
+    bool mono = qi < qn;
+#pragma unroll
+    for (int w = 0; w < kScanWaves; ++w) mono = mono && s_bad[w * QT + qi] == 0;
+    monotone[qi] = mono;
+  }
+
+  int cnt[QT];
+  uint64_t thr[QT];
+#pragma unroll
+  for (int qi = 0; qi < QT; ++qi) {
+    cnt[qi] = 0;
+    thr[qi] = kNoKey;
+  }
+  uint64_t* my_pools = pools + static_cast<size_t>(wave) * QT * a.pool_stride;
 
   // Thresholds.  thr[qi] is the k-th smallest key of this wavefront's own
   // pool.  Any wavefront's k-th key also bounds the query's answer (k smaller
@@ -303,20 +374,6 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
 
   if constexpr (MT > 0) {
     constexpr int kGroup = MT % 8 == 0 && MT > 16 ? 8 : (MT % 4 == 0 ? 4 : MT);
-    // Software pipeline over two register sets: while the tile in one set is
-    // summed, the next selected tile's code words load into the other (no
-    // register copy, so nothing waits for the loads in flight).
-    auto next_selected = [&](int t, uint64_t (&bm)[QT]) -> int {
-      while (t < te && tile_masks(t, bm) == 0) t += kScanWaves;
-      return t;
-    };
-    // Past the chunk's end the loads repeat its last tile (in bounds, unused).
-    auto load_tile = [&](int t, uint32_t (&w)[kMW]) {
-      const int tc = t < te ? t : te - 1;
-      const uint32_t* __restrict__ tile = a.codes_t + static_cast<size_t>(tc) * (kMW * 64);
-#pragma unroll
-      for (int j = 0; j < kMW; ++j) w[j] = tile[j * 64 + lane];
-    };
     auto sum_tile = [&](int t, const uint64_t (&bm)[QT], const uint32_t (&w)[kMW]) {
       refresh_bounds();
       // Subspaces are summed in groups, all of the tile's queries side by
@@ -362,10 +419,6 @@ __global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a)
         // Usually every lane has dropped out: nothing to offer.
         if (__ballot(live[qi]) != 0) consider(qi, live[qi], d[qi], t);
     };
-    uint64_t bma[QT], bmb[QT];
-    uint32_t wa[kMW], wb[kMW];
-    int ta = next_selected(tb + wave, bma);
-    load_tile(ta, wa);
     while (ta < te) {
       const int tn = next_selected(ta + kScanWaves, bmb);
       global_finish();
@@ -423,7 +476,7 @@ constexpr int kQtiles[] = {1, 2, 3, 4, 6, 8};
 template <int MT, int QT, typename LutT>
 constexpr bool scan_fits() {
   return static_cast<size_t>(MT) * QT * kKsub * sizeof(LutT) +
-             static_cast<size_t>(QT) * (kScanWaves * 65 * sizeof(uint64_t) + 12) <=
+             static_cast<size_t>(QT) * (kScanWaves * 65 * sizeof(uint64_t) + 8 + 4 * kScanWaves) <=
          static_cast<size_t>(kLdsBudget);
 }
 
@@ -472,10 +525,11 @@ int pool_stride_for(int k) {
 }
 
 size_t scan_lds_bytes(int m, int qtile, int lut_bytes, int pool_stride) {
-  // tables, pools, workgroup thresholds (8 B) and monotonicity flags (4 B)
+  // tables, pools, workgroup thresholds (8 B) and per-wave monotonicity
+  // flags (4 B each)
   return static_cast<size_t>(qtile) *
          (static_cast<size_t>(m) * kKsub * lut_bytes +
-          static_cast<size_t>(kScanWaves) * pool_stride * sizeof(uint64_t) + 12);
+          static_cast<size_t>(kScanWaves) * pool_stride * sizeof(uint64_t) + 8 + 4 * kScanWaves);
 }
 
 int scan_max_qtile(int m, int lut_bytes, int k) {
