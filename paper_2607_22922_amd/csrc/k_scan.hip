@@ -70,8 +70,12 @@ __device__ __forceinline__ uint64_t bit_range(int64_t lo, int64_t hi) {
   return upto_hi & ~((1ull << lo) - 1);
 }
 
+// One-query tiles ask the compiler for six waves per SIMD (at most 80
+// VGPRs); the schedule it then picks measured about 3% faster on the dense
+// bins than its default.  Multi-query tiles keep the default.
 template <int MT, int QT, typename LutT>
-__global__ __launch_bounds__(kScanWaves * 64) void scan_kernel(const ScanArgs a) {
+__global__ __launch_bounds__(kScanWaves * 64) __attribute__((amdgpu_waves_per_eu(QT == 1 ? 6 : 1)))
+void scan_kernel(const ScanArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int kMW = MT > 0 ? (MT + 3) / 4 : 1;
   const int M = MT > 0 ? MT : a.m;
