@@ -104,6 +104,7 @@ struct ifvs_index {
   uint64_t* bitmap = nullptr;    // [max_batch][stride64]
   int64_t stride64 = 0;
   unsigned long long* counts = nullptr;  // [max_batch]
+  uint32_t* count_parts = nullptr;       // [max_batch][filter_count_parts(n)] per-workgroup pool sizes
   uint64_t* partials = nullptr;  // per-wavefront top-k keys
   size_t partial_keys = 0;
   // Gather scan of masked batches (null when M has no gather kernel).
@@ -142,7 +143,8 @@ struct ifvs_index {
                     static_cast<void*>(perm), static_cast<void*>(bank), static_cast<void*>(W),
                     static_cast<void*>(preds_dev), static_cast<void*>(qorder_dev),
                     static_cast<void*>(iv_dev), static_cast<void*>(gthr_dev), static_cast<void*>(bitmap),
-                    static_cast<void*>(counts), static_cast<void*>(partials), static_cast<void*>(codes_rm),
+                    static_cast<void*>(counts), static_cast<void*>(count_parts),
+                    static_cast<void*>(partials), static_cast<void*>(codes_rm),
                     static_cast<void*>(lists), static_cast<void*>(list_n), static_cast<void*>(qmode)})
       if (p) hipFree(p);
     for (int i = 0; i < kStagingSlots; ++i) {
@@ -455,7 +457,7 @@ ifvs_status filter_into_workspace(ifvs_index* idx, int32_t nq, bool residual_onl
   IFVS_LAUNCH(idx, kStFilter, s, "launching filter kernel",
               launch_filter(residual_only ? idx->attrs_phys : idx->attrs, idx->n, idx->n_attr,
                             idx->preds_dev, nq, residual_only, idx->bitmap, idx->stride64,
-                            counts ? idx->counts : nullptr, s));
+                            counts ? idx->counts : nullptr, idx->count_parts, s));
   return IFVS_OK;
 }
 
@@ -629,6 +631,9 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
   if ((st = dev_alloc(&idx->bitmap, static_cast<size_t>(d.max_batch) * idx->stride64, "selection bitmaps")) != IFVS_OK)
     return bail(st);
   if ((st = dev_alloc(&idx->counts, d.max_batch, "pool sizes")) != IFVS_OK) return bail(st);
+  if ((st = dev_alloc(&idx->count_parts, static_cast<size_t>(d.max_batch) * filter_count_parts(idx->n),
+                      "pool size partials")) != IFVS_OK)
+    return bail(st);
   // Partials: room for at least 16 chunks per query, capped near 512 MB.
   {
     const size_t per_chunk = static_cast<size_t>(d.max_batch) * kScanWaves * d.max_k;
@@ -771,7 +776,7 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   if (gather) {
     IFVS_LAUNCH(idx, kStFilter, s, "launching filter kernel",
                 launch_filter(idx->attrs_phys, idx->n, idx->n_attr, idx->preds_dev, nq, false, idx->bitmap,
-                              idx->stride64, idx->counts, s));
+                              idx->stride64, idx->counts, idx->count_parts, s));
     const int64_t max_rows = idx->opt_gather == 1 ? idx->list_cap : std::min(idx->list_cap, gather_auto_rows(idx));
     IFVS_LAUNCH(idx, kStFilter, s, "launching compaction kernel",
                 launch_compact(idx->bitmap, idx->stride64, idx->counts, nq, max_rows, idx->list_cap, idx->lists,

@@ -82,9 +82,12 @@ hipError_t launch_relayout_codes(const uint8_t* codes, int64_t n, int m, int mw,
 
 // Selection bitmaps; residual_only evaluates only the clauses in each
 // predicate's residual_mask.
+// Selection bitmaps (physical row order) and, when counts is not null, pool
+// sizes; count_parts is scratch of filter_count_parts(n) * nq words.
+int64_t filter_count_parts(int64_t n);
 hipError_t launch_filter(const int32_t* attrs, int64_t n, int n_attr, const DevPred* preds,
                          int nq, bool residual_only, uint64_t* bitmap, int64_t stride64,
-                         unsigned long long* counts, hipStream_t s);
+                         unsigned long long* counts, uint32_t* count_parts, hipStream_t s);
 
 hipError_t launch_condition(const float* q, int dim, const DevPred* preds, int nq,
                             const float* bank, int bank_rows, int mr, int h, uint64_t seed,

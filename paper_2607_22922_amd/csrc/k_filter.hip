@@ -2,14 +2,24 @@
 // predicate over the attribute columns and emit the candidate pool P as a
 // selection bitmap, plus the pool size.
 //
-// One wavefront covers 4096 consecutive vectors: in step `it` (0..63) lane L
-// loads the attributes of vector base + 64*it + L once and tests them against
-// the predicates of all kFilterQueries queries of its workgroup; the compare
-// result of the wavefront is itself the 64-bit ballot word of those 64
-// vectors, which lane `it` keeps (one word per query).  After 64 steps every
-// lane holds one word per query and the wavefront stores 512 contiguous bytes
-// per query.  Clause lists live in LDS; each attribute value is read once per
-// group of kFilterQueries queries.
+// One wavefront covers 4096 consecutive vectors and tests each attribute
+// value it reads against the predicates of all kFilterQueries queries of its
+// workgroup.  Clause lists live in LDS.
+//  * Single-column groups (every query one range clause on the same column,
+//    the common case): the wavefront stages 2048 values at a time in LDS with
+//    coalesced loads, then lane L walks rows 32L + 31 .. 32L of the block
+//    (padded LDS layout, no bank conflicts) and shifts each query's compare
+//    bit into its own 32-bit word: word = 2 * word + (v - lo < width).  Each
+//    lane then holds bitmap word L of the block per query (bit r = row
+//    32L + r), so the stores are coalesced and no cross-lane move is needed:
+//    three VALU operations per 64 (row, query) pairs.
+//  * Other groups: in step `it` (0..63) lane L loads the attributes of vector
+//    base + 64*it + L; the compare result of the wavefront is the 64-bit
+//    ballot word of those 64 vectors, which lane `it` keeps (one word per
+//    query), and the wavefront stores 512 contiguous bytes per query.
+// Pool sizes: each workgroup sums its waves' popcounts in LDS and writes one
+// partial count per query (no atomics: device-wide atomics on the same few
+// counters serialised the whole kernel); a small kernel adds the partials.
 #include "ifvs_internal.h"
 
 namespace ifvs {
@@ -18,6 +28,8 @@ namespace {
 
 constexpr int kFilterWaves = 4;
 constexpr int kRowsPerWave = 64 * 64;
+constexpr int kBlockRows = 2048;                        // rows staged per wavefront at a time
+constexpr int kBlockPad = kBlockRows + kBlockRows / 32; // one pad word per 32 rows
 
 // A predicate's clause list for one pass, as the kernel reads it from LDS.
 struct PassClauses {
@@ -35,8 +47,10 @@ __device__ __forceinline__ int32_t column_value(const int32_t* __restrict__ attr
 __global__ __launch_bounds__(kFilterWaves * 64) void filter_kernel(
     const int32_t* __restrict__ attrs, int64_t n, int n_attr,
     const DevPred* __restrict__ preds, int nq, int residual_only, uint64_t* __restrict__ bitmap,
-    int64_t stride64, unsigned long long* __restrict__ counts) {
+    int64_t stride64, uint32_t* __restrict__ count_parts) {
   __shared__ PassClauses sc[kFilterQueries];
+  __shared__ uint32_t s_vals[kFilterWaves * kBlockPad];
+  __shared__ uint32_t s_cnt[kFilterWaves][kFilterQueries];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int q0 = blockIdx.y * kFilterQueries;
@@ -60,20 +74,20 @@ __global__ __launch_bounds__(kFilterWaves * 64) void filter_kernel(
   }
   __syncthreads();
   const int64_t base = (static_cast<int64_t>(blockIdx.x) * kFilterWaves + wave) * kRowsPerWave;
-  if (base >= n) return;
+  // A wavefront past the last row does nothing but still joins the count
+  // reduction's barrier.
+  const bool active = base < n;
   // Common case: every query of the group tests one clause on the same
-  // column.  Then each step is one load and, per query, a subtract, a
-  // compare whose lane mask is the ballot word, and two selects.
+  // column (the transposed path below).
   int single_col = qn > 0 && sc[0].nc == 1 ? sc[0].col[0] : -1;
   for (int qi = 1; qi < qn; ++qi)
     if (sc[qi].nc != 1 || sc[qi].col[0] != single_col) single_col = -1;
 
-  // held_{lo,hi}[qi] of lane L: the ballot word of step L for query qi.
-  uint32_t held_lo[kFilterQueries], held_hi[kFilterQueries];
+  uint32_t cnt[kFilterQueries];   // this lane's selected rows per query
 #pragma unroll
-  for (int qi = 0; qi < kFilterQueries; ++qi) held_lo[qi] = held_hi[qi] = 0;
+  for (int qi = 0; qi < kFilterQueries; ++qi) cnt[qi] = 0;
 
-  if (single_col >= 0) {
+  if (active && single_col >= 0) {
     const int32_t* __restrict__ col = attrs + static_cast<int64_t>(single_col) * n;
     uint32_t lo[kFilterQueries], width[kFilterQueries];
 #pragma unroll
@@ -81,20 +95,56 @@ __global__ __launch_bounds__(kFilterWaves * 64) void filter_kernel(
       lo[qi] = qi < qn ? sc[qi].lo[0] : 0;
       width[qi] = qi < qn ? sc[qi].width[0] : 0;   // width 0: nothing passes
     }
+    uint32_t* vals = s_vals + wave * kBlockPad;
+    uint32_t* bitmap32 = reinterpret_cast<uint32_t*>(bitmap);
+    for (int blk = 0; blk < kRowsPerWave / kBlockRows; ++blk) {
+      const int64_t bb = base + static_cast<int64_t>(blk) * kBlockRows;
+      // Stage the block: local row r at vals[r + r / 32] (rows past n repeat
+      // the last row and are masked below).
+#pragma unroll 8
+      for (int j = 0; j < kBlockRows / 64; ++j) {
+        const int r = 64 * j + lane;
+        const int64_t i = bb + r;
+        vals[r + (r >> 5)] = static_cast<uint32_t>(col[i < n ? i : n - 1]);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      // Lane L: rows 32L + 31 down to 32L, so row 32L + r lands in bit r.
+      uint32_t word[kFilterQueries];
+#pragma unroll
+      for (int qi = 0; qi < kFilterQueries; ++qi) word[qi] = 0;
+      const uint32_t* mine = vals + 33 * lane;
 #pragma unroll 4
-    for (int it = 0; it < 64; ++it) {
-      const int64_t i = base + static_cast<int64_t>(it) * 64 + lane;
-      const bool in = i < n;
-      const uint32_t v = static_cast<uint32_t>(col[in ? i : n - 1]);
-      const bool mine = lane == it;
+      for (int r = 31; r >= 0; --r) {
+        const uint32_t v = mine[r];
+#pragma unroll
+        for (int qi = 0; qi < kFilterQueries; ++qi)
+          word[qi] = word[qi] + word[qi] + (v - lo[qi] < width[qi] ? 1u : 0u);
+      }
+      const int64_t row0 = bb + 32 * lane;
+      uint32_t valid = ~0u;
+      if (row0 + 32 > n) valid = row0 >= n ? 0u : ((1u << static_cast<int>(n - row0)) - 1u);
+      const int64_t w32 = bb / 32 + lane;
 #pragma unroll
       for (int qi = 0; qi < kFilterQueries; ++qi) {
-        const uint64_t word = __ballot(in && v - lo[qi] < width[qi]);
-        held_lo[qi] = mine ? static_cast<uint32_t>(word) : held_lo[qi];
-        held_hi[qi] = mine ? static_cast<uint32_t>(word >> 32) : held_hi[qi];
+        if (qi < qn) {
+          const uint32_t wd = word[qi] & valid;
+          if (w32 < 2 * stride64) bitmap32[static_cast<int64_t>(q0 + qi) * 2 * stride64 + w32] = wd;
+          cnt[qi] += static_cast<uint32_t>(__popc(wd));
+        }
       }
+      // The next block overwrites vals only after every lane has read it.
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
-  } else {
+  } else if (active) {
+  // held_{lo,hi}[qi] of lane L: the ballot word of step L for query qi.
+  uint32_t held_lo[kFilterQueries], held_hi[kFilterQueries];
+#pragma unroll
+  for (int qi = 0; qi < kFilterQueries; ++qi) held_lo[qi] = held_hi[qi] = 0;
+
   for (int it = 0; it < 64; ++it) {
     const int64_t i = base + static_cast<int64_t>(it) * 64 + lane;
     const bool in = i < n;
@@ -117,7 +167,6 @@ __global__ __launch_bounds__(kFilterWaves * 64) void filter_kernel(
       }
     }
   }
-  }
 
   const int64_t w64 = base / 64 + lane;           // this lane's 64-bit word
 #pragma unroll
@@ -125,14 +174,42 @@ __global__ __launch_bounds__(kFilterWaves * 64) void filter_kernel(
     if (qi < qn) {
       const uint64_t word = (static_cast<uint64_t>(held_hi[qi]) << 32) | held_lo[qi];
       if (w64 < stride64) bitmap[static_cast<int64_t>(q0 + qi) * stride64 + w64] = word;
-      if (counts) {
-        unsigned long long c = __popcll(word);
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) c += __shfl_down(c, off, 64);
-        if (lane == 0) atomicAdd(&counts[q0 + qi], c);
-      }
+      cnt[qi] = static_cast<uint32_t>(__popcll(word));
     }
   }
+  }
+
+  // Pool sizes: wavefront sums, then one partial per (workgroup, query).
+  if (count_parts) {
+#pragma unroll
+    for (int qi = 0; qi < kFilterQueries; ++qi) {
+      unsigned c = cnt[qi];
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) c += __shfl_down(c, off, 64);
+      if (lane == 0) s_cnt[wave][qi] = c;
+    }
+    __syncthreads();
+    if (threadIdx.x < qn) {
+      uint32_t sum = 0;
+#pragma unroll
+      for (int w = 0; w < kFilterWaves; ++w) sum += s_cnt[w][threadIdx.x];
+      count_parts[static_cast<int64_t>(q0 + threadIdx.x) * gridDim.x + blockIdx.x] = sum;
+    }
+  }
+}
+
+// counts[q] = sum of the q-th row of count_parts ([nq][parts]); one
+// wavefront per query.
+__global__ __launch_bounds__(64) void reduce_counts_kernel(const uint32_t* __restrict__ count_parts,
+                                                           int parts, int nq,
+                                                           unsigned long long* __restrict__ counts) {
+  const int q = blockIdx.x;
+  if (q >= nq) return;
+  unsigned long long c = 0;
+  for (int i = threadIdx.x; i < parts; i += 64) c += count_parts[static_cast<int64_t>(q) * parts + i];
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) c += __shfl_down(c, off, 64);
+  if (threadIdx.x == 0) counts[q] = c;
 }
 
 // codes [n][m] bytes -> tiles of 64 rows: word j of physical row (64t + L) is
@@ -161,11 +238,6 @@ __global__ void relayout_kernel(const uint8_t* __restrict__ codes, int64_t n, in
   }
 }
 
-__global__ void zero_counts_kernel(unsigned long long* __restrict__ counts, int nq) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < nq) counts[i] = 0;
-}
-
 }  // namespace
 
 hipError_t launch_relayout_codes(const uint8_t* codes, int64_t n, int m, int mw, const int32_t* perm,
@@ -177,19 +249,21 @@ hipError_t launch_relayout_codes(const uint8_t* codes, int64_t n, int m, int mw,
   return hipGetLastError();
 }
 
+int64_t filter_count_parts(int64_t n) {
+  const int64_t rows_per_block = static_cast<int64_t>(kFilterWaves) * kRowsPerWave;
+  return (n + rows_per_block - 1) / rows_per_block;
+}
+
 hipError_t launch_filter(const int32_t* attrs, int64_t n, int n_attr, const DevPred* preds,
                          int nq, bool residual_only, uint64_t* bitmap, int64_t stride64,
-                         unsigned long long* counts, hipStream_t s) {
-  const int64_t rows_per_block = static_cast<int64_t>(kFilterWaves) * kRowsPerWave;
-  const int64_t gx = (n + rows_per_block - 1) / rows_per_block;
+                         unsigned long long* counts, uint32_t* count_parts, hipStream_t s) {
+  const int64_t gx = filter_count_parts(n);
   const int gy = (nq + kFilterQueries - 1) / kFilterQueries;
-  if (counts) {
-    zero_counts_kernel<<<dim3((nq + 255) / 256), dim3(256), 0, s>>>(counts, nq);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
   filter_kernel<<<dim3(static_cast<unsigned>(gx), gy), dim3(kFilterWaves * 64), 0, s>>>(
-      attrs, n, n_attr, preds, nq, residual_only ? 1 : 0, bitmap, stride64, counts);
+      attrs, n, n_attr, preds, nq, residual_only ? 1 : 0, bitmap, stride64, counts ? count_parts : nullptr);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !counts) return e;
+  reduce_counts_kernel<<<dim3(nq), dim3(64), 0, s>>>(count_parts, static_cast<int>(gx), nq, counts);
   return hipGetLastError();
 }
 
