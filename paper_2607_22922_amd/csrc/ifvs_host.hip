@@ -779,7 +779,8 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
                               idx->stride64, idx->counts, idx->count_parts, s));
     const int64_t max_rows = idx->opt_gather == 1 ? idx->list_cap : std::min(idx->list_cap, gather_auto_rows(idx));
     IFVS_LAUNCH(idx, kStFilter, s, "launching compaction kernel",
-                launch_compact(idx->bitmap, idx->stride64, idx->counts, nq, max_rows, idx->list_cap, idx->lists,
+                launch_compact(idx->bitmap, idx->stride64, idx->counts, idx->count_parts,
+                               filter_count_parts(idx->n), nq, max_rows, idx->list_cap, idx->lists,
                                idx->list_n, idx->qmode, s));
   } else if (need_bitmap) {
     if (ifvs_status st = filter_into_workspace(idx, nq, true, false, s); st != IFVS_OK) return st;

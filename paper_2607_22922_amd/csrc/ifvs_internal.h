@@ -83,7 +83,10 @@ hipError_t launch_relayout_codes(const uint8_t* codes, int64_t n, int m, int mw,
 // Selection bitmaps; residual_only evaluates only the clauses in each
 // predicate's residual_mask.
 // Selection bitmaps (physical row order) and, when counts is not null, pool
-// sizes; count_parts is scratch of filter_count_parts(n) * nq words.
+// sizes; count_parts ([nq][filter_count_parts(n)] words) then holds, per
+// query, the exclusive prefix sums of the selected rows of consecutive
+// kFilterPartRows-row parts.
+constexpr int64_t kFilterPartRows = 4 * 64 * 64;
 int64_t filter_count_parts(int64_t n);
 hipError_t launch_filter(const int32_t* attrs, int64_t n, int n_attr, const DevPred* preds,
                          int nq, bool residual_only, uint64_t* bitmap, int64_t stride64,
@@ -166,9 +169,9 @@ hipError_t launch_rowmajor_codes(const uint32_t* codes_t, int64_t n, int mw, int
                                  hipStream_t s);
 // Per query: mode (1 when its pool holds at most max_rows rows; max_rows < 0:
 // never) and, for those, the ascending list of selected physical rows.
-hipError_t launch_compact(const uint64_t* bitmap, int64_t stride64, const unsigned long long* counts, int nq,
-                          int64_t max_rows, int64_t list_cap, int32_t* lists, int32_t* list_n, int32_t* mode,
-                          hipStream_t s);
+hipError_t launch_compact(const uint64_t* bitmap, int64_t stride64, const unsigned long long* counts,
+                          const uint32_t* count_prefix, int64_t parts, int nq, int64_t max_rows,
+                          int64_t list_cap, int32_t* lists, int32_t* list_n, int32_t* mode, hipStream_t s);
 hipError_t launch_gather_scan(const GatherBatch& b, hipStream_t s);
 
 hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s);

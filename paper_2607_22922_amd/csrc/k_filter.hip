@@ -19,7 +19,8 @@
 //    query), and the wavefront stores 512 contiguous bytes per query.
 // Pool sizes: each workgroup sums its waves' popcounts in LDS and writes one
 // partial count per query (no atomics: device-wide atomics on the same few
-// counters serialised the whole kernel); a small kernel adds the partials.
+// counters serialised the whole kernel); a small kernel adds the partials
+// and leaves their exclusive prefix sums for the row-list compaction.
 #include "ifvs_internal.h"
 
 namespace ifvs {
@@ -28,6 +29,7 @@ namespace {
 
 constexpr int kFilterWaves = 4;
 constexpr int kRowsPerWave = 64 * 64;
+static_assert(kFilterWaves * kRowsPerWave == kFilterPartRows, "one count partial per workgroup");
 constexpr int kBlockRows = 2048;                        // rows staged per wavefront at a time
 constexpr int kBlockPad = kBlockRows + kBlockRows / 32; // one pad word per 32 rows
 
@@ -198,18 +200,30 @@ __global__ __launch_bounds__(kFilterWaves * 64) void filter_kernel(
   }
 }
 
-// counts[q] = sum of the q-th row of count_parts ([nq][parts]); one
-// wavefront per query.
-__global__ __launch_bounds__(64) void reduce_counts_kernel(const uint32_t* __restrict__ count_parts,
-                                                           int parts, int nq,
-                                                           unsigned long long* __restrict__ counts) {
+// counts[q] = sum of the q-th row of count_parts ([nq][parts]), and the
+// row is turned into its exclusive prefix sums in place (the compaction
+// kernel's output offsets; every count is below 2^31).  One wavefront per
+// query.
+__global__ __launch_bounds__(64) void reduce_counts_kernel(uint32_t* __restrict__ count_parts, int parts,
+                                                           int nq, unsigned long long* __restrict__ counts) {
   const int q = blockIdx.x;
   if (q >= nq) return;
-  unsigned long long c = 0;
-  for (int i = threadIdx.x; i < parts; i += 64) c += count_parts[static_cast<int64_t>(q) * parts + i];
+  const int lane = threadIdx.x;
+  uint32_t* row = count_parts + static_cast<int64_t>(q) * parts;
+  uint32_t carry = 0;
+  for (int i0 = 0; i0 < parts; i0 += 64) {
+    const int i = i0 + lane;
+    const uint32_t v = i < parts ? row[i] : 0u;
+    uint32_t incl = v;
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) c += __shfl_down(c, off, 64);
-  if (threadIdx.x == 0) counts[q] = c;
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint32_t y = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += y;
+    }
+    if (i < parts) row[i] = carry + incl - v;
+    carry += __shfl(incl, 63, 64);
+  }
+  if (lane == 0) counts[q] = carry;
 }
 
 // codes [n][m] bytes -> tiles of 64 rows: word j of physical row (64t + L) is

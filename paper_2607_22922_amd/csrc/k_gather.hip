@@ -22,6 +22,10 @@ namespace {
 
 constexpr int kCompactThreads = 256;
 constexpr int kCompactWordsPerThread = 4;
+constexpr int64_t kWordsPerPart = kFilterPartRows / 64;   // bitmap words per filter count partial
+constexpr int kCompactParts = kCompactThreads * kCompactWordsPerThread / kWordsPerPart;
+static_assert(kCompactParts * kWordsPerPart == kCompactThreads * kCompactWordsPerThread, "whole parts");
+constexpr int kCompactStage = 8192;   // rows a compaction workgroup stages in LDS (32 KB)
 // Rows a gather workgroup scores at most (8 wavefronts x 64 lanes x 16).
 constexpr int64_t kGatherRowsPerBlock = static_cast<int64_t>(kScanWaves) * 64 * 16;
 
@@ -40,17 +44,21 @@ __global__ void rowmajor_kernel(const uint32_t* __restrict__ codes_t, int64_t n,
   }
 }
 
-// One workgroup per query: mode[q] = 1 (gather) when the pool holds at most
-// max_rows rows, and then the ascending list of its selected physical rows.
+// mode[q] = 1 (gather) when the pool holds at most max_rows rows, and then
+// the ascending list of its selected physical rows.  Workgroup (g, q) covers
+// kCompactParts consecutive filter parts of query q (thread t: 4 consecutive
+// bitmap words); its rows start at the Filter stage's prefix count of its
+// first part, and a workgroup prefix sum orders them within.
 __global__ __launch_bounds__(kCompactThreads) void compact_kernel(
     const uint64_t* __restrict__ bitmap, int64_t stride64, const unsigned long long* __restrict__ counts,
-    int nq, int64_t max_rows, int64_t list_cap, int32_t* __restrict__ lists, int32_t* __restrict__ list_n,
-    int32_t* __restrict__ mode) {
-  const int q = blockIdx.x;
-  if (q >= nq) return;
+    const uint32_t* __restrict__ count_prefix, int64_t parts, int nq, int64_t max_rows, int64_t list_cap,
+    int32_t* __restrict__ lists, int32_t* __restrict__ list_n, int32_t* __restrict__ mode) {
+  const int q = blockIdx.y;
+  const int64_t part0 = static_cast<int64_t>(blockIdx.x) * kCompactParts;
+  if (q >= nq || part0 >= parts) return;
   const unsigned long long cnt = counts[q];
   const bool gather = max_rows >= 0 && cnt <= static_cast<unsigned long long>(max_rows);
-  if (threadIdx.x == 0) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
     mode[q] = gather ? 1 : 0;
     list_n[q] = gather ? static_cast<int32_t>(cnt) : 0;
   }
@@ -60,46 +68,61 @@ __global__ __launch_bounds__(kCompactThreads) void compact_kernel(
   const int wave = threadIdx.x >> 6;
   const uint64_t* words = bitmap + static_cast<size_t>(q) * stride64;
   int32_t* out = lists + static_cast<size_t>(q) * list_cap;
-  int64_t base = 0;
-  constexpr int kChunk = kCompactThreads * kCompactWordsPerThread;
-  for (int64_t w0 = 0; w0 < stride64; w0 += kChunk) {
-    const int64_t first = w0 + static_cast<int64_t>(threadIdx.x) * kCompactWordsPerThread;
-    uint64_t wv[kCompactWordsPerThread];
-    int c = 0;
+  const int64_t first = part0 * kWordsPerPart + static_cast<int64_t>(threadIdx.x) * kCompactWordsPerThread;
+  uint64_t wv[kCompactWordsPerThread];
+  int c = 0;
 #pragma unroll
-    for (int u = 0; u < kCompactWordsPerThread; ++u) {
-      wv[u] = first + u < stride64 ? words[first + u] : 0ull;
-      c += __popcll(wv[u]);
-    }
-    // Exclusive prefix of c over the workgroup (threads in word order).
-    int incl = c;
+  for (int u = 0; u < kCompactWordsPerThread; ++u) {
+    wv[u] = first + u < stride64 ? words[first + u] : 0ull;
+    c += __popcll(wv[u]);
+  }
+  // Exclusive prefix of c over the workgroup (threads in word order).
+  int incl = c;
 #pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int y = __shfl_up(incl, off, 64);
-      if (lane >= off) incl += y;
-    }
-    if (lane == 63) s_wave_sum[wave] = incl;
-    __syncthreads();
-    int before = 0, total = 0;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += y;
+  }
+  if (lane == 63) s_wave_sum[wave] = incl;
+  __syncthreads();
+  int before = 0, total = 0;
 #pragma unroll
-    for (int i = 0; i < kCompactThreads / 64; ++i) {
-      const int sw = s_wave_sum[i];
-      before += i < wave ? sw : 0;
-      total += sw;
-    }
-    int64_t pos = base + before + incl - c;
+  for (int i = 0; i < kCompactThreads / 64; ++i) {
+    const int sw = s_wave_sum[i];
+    before += i < wave ? sw : 0;
+    total += sw;
+  }
+  const int64_t base = static_cast<int64_t>(count_prefix[static_cast<int64_t>(q) * parts + part0]);
+  if (total <= kCompactStage) {
+    // Each thread's rows go to LDS at their rank, then the workgroup copies
+    // them out with coalesced stores (a thread's own run of rows would make
+    // every store instruction touch up to 64 cache lines).
+    __shared__ int32_t s_rows[kCompactStage];
+    int pos = before + incl - c;
 #pragma unroll
     for (int u = 0; u < kCompactWordsPerThread; ++u) {
       uint64_t x = wv[u];
       while (x) {
         const int b = __ffsll(static_cast<long long>(x)) - 1;
-        if (pos < list_cap) out[pos] = static_cast<int32_t>((first + u) * 64 + b);
-        ++pos;
+        s_rows[pos++] = static_cast<int32_t>((first + u) * 64 + b);
         x &= x - 1;
       }
     }
-    base += total;
-    __syncthreads();   // s_wave_sum is rewritten by the next chunk
+    __syncthreads();
+    for (int i = threadIdx.x; i < total; i += kCompactThreads)
+      if (base + i < list_cap) out[base + i] = s_rows[i];
+    return;
+  }
+  int64_t pos = base + before + incl - c;
+#pragma unroll
+  for (int u = 0; u < kCompactWordsPerThread; ++u) {
+    uint64_t x = wv[u];
+    while (x) {
+      const int b = __ffsll(static_cast<long long>(x)) - 1;
+      if (pos < list_cap) out[pos] = static_cast<int32_t>((first + u) * 64 + b);
+      ++pos;
+      x &= x - 1;
+    }
   }
 }
 
@@ -300,11 +323,12 @@ hipError_t launch_rowmajor_codes(const uint32_t* codes_t, int64_t n, int mw, int
   return hipGetLastError();
 }
 
-hipError_t launch_compact(const uint64_t* bitmap, int64_t stride64, const unsigned long long* counts, int nq,
-                          int64_t max_rows, int64_t list_cap, int32_t* lists, int32_t* list_n, int32_t* mode,
-                          hipStream_t s) {
-  compact_kernel<<<dim3(nq), dim3(kCompactThreads), 0, s>>>(bitmap, stride64, counts, nq, max_rows, list_cap,
-                                                            lists, list_n, mode);
+hipError_t launch_compact(const uint64_t* bitmap, int64_t stride64, const unsigned long long* counts,
+                          const uint32_t* count_prefix, int64_t parts, int nq, int64_t max_rows,
+                          int64_t list_cap, int32_t* lists, int32_t* list_n, int32_t* mode, hipStream_t s) {
+  const dim3 grid(static_cast<unsigned>((parts + kCompactParts - 1) / kCompactParts), static_cast<unsigned>(nq));
+  compact_kernel<<<grid, dim3(kCompactThreads), 0, s>>>(bitmap, stride64, counts, count_prefix, parts, nq,
+                                                         max_rows, list_cap, lists, list_n, mode);
   return hipGetLastError();
 }
 

@@ -337,6 +337,23 @@ def test_gather_scan_matches_oracle(B, cluster_cols, M, dsub, k, lut_dtype):
         assert np.array_equal(outs[mode][1].view(np.uint32), outs[1][1].view(np.uint32))
 
 
+def test_gather_compaction_sparse_and_dense_workgroups(B):
+    """Row lists of gather-mode queries over several compaction workgroups
+    (65536 rows each): pools that a workgroup stages in LDS (about 1% and 5%
+    of its rows) and pools too large for that (about 20%), which it writes
+    directly; the search gives the oracle's ids and distance bits either way
+    and matches the tiled scan."""
+    say("[gather] compaction paths N=150000")
+    idx, ox = _edge_index(B, 150_000, 16, 8, n_attr=1, domain=100, seed=61, max_k=16)
+    preds = [[(0, 50, 51)], [(0, 0, 5)], [(0, 10, 30)], [(0, 93, 100)], [(0, 7, 8)], [(0, 60, 80)]]
+    idx.set_option(B.OPT_GATHER, 1)
+    ids = _run_and_check(B, idx, ox, preds, k=16, dsub=8, M=16)
+    idx.set_option(B.OPT_GATHER, 2)
+    ids2 = _run_and_check(B, idx, ox, preds, k=16, dsub=8, M=16)
+    idx.set_option(B.OPT_GATHER, 0)
+    assert np.array_equal(ids, ids2)
+
+
 def test_clustered_ties_break_by_original_id(B):
     ix = random_index(6000, 16, 8, 1, 40, 41, device="cuda")
     ix["codes"][::7] = ix["codes"][3]                 # equal rows in every cluster
