@@ -66,6 +66,7 @@ struct StageTimer {
 };
 
 constexpr int kFences = 4096;
+constexpr int64_t kMaxValueTable = int64_t{1} << 22;   // entries (16 MB) of the cluster key table
 
 constexpr int64_t kI32Min = std::numeric_limits<int32_t>::min();
 constexpr int64_t kI32End = int64_t(std::numeric_limits<int32_t>::max()) + 1;
@@ -87,6 +88,11 @@ struct ifvs_index {
   float* cpq = nullptr;          // [m][256][dsub]
   int32_t* attrs = nullptr;      // [n_attr][n] original id order
   int32_t* attrs_phys = nullptr; // [n_attr][n] physical order (== attrs when not clustered)
+  // Leading cluster key value table: vstart[t] = first physical row whose key
+  // is >= vmin + t (t < vcount, last entry n); null when the key's value
+  // range is too wide.
+  int32_t* vstart = nullptr;
+  int64_t vmin = 0, vcount = 0;
   int32_t* perm = nullptr;       // physical row -> original id (null when not clustered)
   float* bank = nullptr;         // [bank_rows][m*r]
   float* W = nullptr;            // [m][r][256][dsub]
@@ -143,7 +149,7 @@ struct ifvs_index {
                     static_cast<void*>(perm), static_cast<void*>(bank), static_cast<void*>(W),
                     static_cast<void*>(preds_dev), static_cast<void*>(qorder_dev),
                     static_cast<void*>(iv_dev), static_cast<void*>(gthr_dev), static_cast<void*>(bitmap),
-                    static_cast<void*>(counts), static_cast<void*>(count_parts),
+                    static_cast<void*>(counts), static_cast<void*>(count_parts), static_cast<void*>(vstart),
                     static_cast<void*>(partials), static_cast<void*>(codes_rm),
                     static_cast<void*>(lists), static_cast<void*>(list_n), static_cast<void*>(qmode)})
       if (p) hipFree(p);
@@ -555,6 +561,26 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
       auto& f = c == 0 ? idx->fence0 : idx->fence1;
       f.resize(kFences + 1);
       for (int i = 0; i <= kFences; ++i) f[i] = col[std::min<int64_t>(d.n - 1, static_cast<int64_t>(i) * d.n / kFences)];
+      // The leading key is sorted: where its values span at most kMaxValueTable
+      // integers, a value -> first-row table turns each interval bound into
+      // one load instead of a 64-ary search.
+      if (c == 0 && static_cast<int64_t>(col[d.n - 1]) - col[0] + 2 <= kMaxValueTable) {
+        const int64_t vmin = col[0];
+        const int64_t vcount = static_cast<int64_t>(col[d.n - 1]) - vmin + 2;
+        std::vector<int32_t> table(static_cast<size_t>(vcount));
+        int64_t row = 0;
+        for (int64_t t = 0; t < vcount; ++t) {
+          while (row < d.n && col[row] < vmin + t) ++row;
+          table[t] = static_cast<int32_t>(row);
+        }
+        if ((st = dev_alloc(&idx->vstart, static_cast<size_t>(vcount), "cluster key value table")) != IFVS_OK)
+          return bail(st);
+        if (hipError_t e = hipMemcpy(idx->vstart, table.data(), sizeof(int32_t) * vcount, hipMemcpyHostToDevice);
+            e != hipSuccess)
+          return bail(hip_fail(e, "loading cluster key value table"));
+        idx->vmin = vmin;
+        idx->vcount = vcount;
+      }
     }
   }
   // codes -> 64-row tiles (in physical order)
@@ -760,7 +786,8 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   ScanPlan plan{};
   if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, interval_batch, span, &plan); st != IFVS_OK) return st;
   IFVS_LAUNCH(idx, kStFilter, s, "launching interval kernel",
-              launch_intervals(idx->attrs_phys, idx->n, idx->c0, idx->c1, idx->staging_dev[slot],
+              launch_intervals(idx->attrs_phys, idx->n, idx->c0, idx->c1, idx->vstart, idx->vmin, idx->vcount,
+                               idx->staging_dev[slot],
                                reinterpret_cast<const int32_t*>(idx->staging_dev[slot] + idx->max_batch), nq,
                                idx->preds_dev, idx->qorder_dev, idx->iv_dev, idx->gthr_dev, s));
   if (ifvs_status st = release_slot(idx, slot, s); st != IFVS_OK) return st;

@@ -70,10 +70,12 @@ hipError_t launch_gather_attrs(const int32_t* attrs, int64_t n, int n_attr, cons
 // scan order from the staging slot (pinned host memory) and leaves device
 // copies in preds_out / order_out for the kernels that follow; resets the
 // per-query global thresholds.
-hipError_t launch_intervals(const int32_t* attrs_phys, int64_t n, int c0, int c1,
-                            const DevPred* staged_preds, const int32_t* staged_order, int nq,
-                            DevPred* preds_out, int32_t* order_out, int64_t* iv, uint64_t* gthr,
-                            hipStream_t s);
+// vstart (may be null): vstart[t] = first physical row whose leading cluster
+// key is >= vmin + t, for t < vcount (the last entry is n).
+hipError_t launch_intervals(const int32_t* attrs_phys, int64_t n, int c0, int c1, const int32_t* vstart,
+                            int64_t vmin, int64_t vcount, const DevPred* staged_preds,
+                            const int32_t* staged_order, int nq, DevPred* preds_out, int32_t* order_out,
+                            int64_t* iv, uint64_t* gthr, hipStream_t s);
 
 // codes (row-major [n][m]) -> 64-row tiles, physical row r taken from
 // original row perm[r] (perm may be null: identity).

@@ -47,14 +47,14 @@ __device__ __forceinline__ bool key_below(const int32_t* __restrict__ a0, const 
   return v0 < x0;
 }
 
-// First row whose key is >= (x0, x1): a 64-ary search by one wavefront.
-// Each step every lane probes one of 64 evenly spaced rows of the current
-// range [lo, hi); the ballot of "probe below x" narrows the range to the gap
+// First row of [lo, hi) whose key is >= (x0, x1) (hi when there is none),
+// given that the rows before lo are below it: a 64-ary search by one
+// wavefront.  Each step every lane probes one of 64 evenly spaced rows of the
+// current range; the ballot of "probe below x" narrows the range to the gap
 // after the last such probe, so 10^7 rows take four dependent loads.
 __device__ int64_t wave_lower_bound(const int32_t* __restrict__ a0, const int32_t* __restrict__ a1,
-                                    int64_t n, int64_t x0, int64_t x1) {
+                                    int64_t lo, int64_t hi, int64_t x0, int64_t x1) {
   const int lane = threadIdx.x & 63;
-  int64_t lo = 0, hi = n;               // answer in [lo, hi]
   while (hi - lo > 64) {
     const int64_t step = (hi - lo + 63) / 64;
     const int64_t r = lo + lane * step; // probes lo, lo+step, ... (< hi or past it)
@@ -75,8 +75,19 @@ __device__ int64_t wave_lower_bound(const int32_t* __restrict__ a0, const int32_
   return lo + __popcll(__ballot(below));
 }
 
+// First row whose leading key is >= x, from the value table (vstart[t] =
+// first row with leading key >= vmin + t, t < vcount; the last entry is n).
+__device__ __forceinline__ int64_t table_lower_bound(const int32_t* __restrict__ vstart, int64_t vmin,
+                                                     int64_t vcount, int64_t n, int64_t x) {
+  if (x <= vmin) return 0;
+  if (x >= vmin + (vcount - 1)) return n;
+  return vstart[x - vmin];
+}
+
 __global__ __launch_bounds__(64) void intervals_kernel(const int32_t* __restrict__ attrs_phys, int64_t n,
-                                                       int c0, int c1, const DevPred* __restrict__ staged_preds,
+                                                       int c0, int c1, const int32_t* __restrict__ vstart,
+                                                       int64_t vmin, int64_t vcount,
+                                                       const DevPred* __restrict__ staged_preds,
                                                        const int32_t* __restrict__ staged_order, int nq,
                                                        DevPred* __restrict__ preds_out,
                                                        int32_t* __restrict__ order_out,
@@ -97,12 +108,25 @@ __global__ __launch_bounds__(64) void intervals_kernel(const int32_t* __restrict
   if (p.n_eff < 0) {
     r = 0;
   } else if (p.iv_mode == 1) {
-    const int32_t* a0 = attrs_phys + static_cast<int64_t>(c0) * n;
-    r = wave_lower_bound(a0, nullptr, n, upper ? p.iv_hi0 : p.iv_lo0, 0);
+    const int64_t x = upper ? p.iv_hi0 : p.iv_lo0;
+    if (vstart) {
+      r = table_lower_bound(vstart, vmin, vcount, n, x);
+    } else {
+      const int32_t* a0 = attrs_phys + static_cast<int64_t>(c0) * n;
+      r = wave_lower_bound(a0, nullptr, 0, n, x, 0);
+    }
   } else if (p.iv_mode == 2) {
+    // Leading key equal to iv_lo0, second key in [iv_lo1, iv_hi1): the value
+    // table (when present) gives the rows of that leading key, the search
+    // runs inside them.
     const int32_t* a0 = attrs_phys + static_cast<int64_t>(c0) * n;
     const int32_t* a1 = attrs_phys + static_cast<int64_t>(c1) * n;
-    r = wave_lower_bound(a0, a1, n, p.iv_lo0, upper ? p.iv_hi1 : p.iv_lo1);
+    int64_t lo = 0, hi = n;
+    if (vstart) {
+      lo = table_lower_bound(vstart, vmin, vcount, n, p.iv_lo0);
+      hi = table_lower_bound(vstart, vmin, vcount, n, p.iv_lo0 + 1);
+    }
+    r = wave_lower_bound(a0, a1, lo, hi, p.iv_lo0, upper ? p.iv_hi1 : p.iv_lo1);
   }
   if (threadIdx.x == 0) {
     iv[2 * q + (upper ? 1 : 0)] = r;
@@ -152,12 +176,12 @@ hipError_t launch_gather_attrs(const int32_t* attrs, int64_t n, int n_attr, cons
   return hipGetLastError();
 }
 
-hipError_t launch_intervals(const int32_t* attrs_phys, int64_t n, int c0, int c1,
-                            const DevPred* staged_preds, const int32_t* staged_order, int nq,
-                            DevPred* preds_out, int32_t* order_out, int64_t* iv, uint64_t* gthr,
-                            hipStream_t s) {
-  intervals_kernel<<<dim3(2 * nq), dim3(64), 0, s>>>(attrs_phys, n, c0, c1, staged_preds, staged_order, nq,
-                                                     preds_out, order_out, iv, gthr);
+hipError_t launch_intervals(const int32_t* attrs_phys, int64_t n, int c0, int c1, const int32_t* vstart,
+                            int64_t vmin, int64_t vcount, const DevPred* staged_preds,
+                            const int32_t* staged_order, int nq, DevPred* preds_out, int32_t* order_out,
+                            int64_t* iv, uint64_t* gthr, hipStream_t s) {
+  intervals_kernel<<<dim3(2 * nq), dim3(64), 0, s>>>(attrs_phys, n, c0, c1, vstart, vmin, vcount, staged_preds,
+                                                     staged_order, nq, preds_out, order_out, iv, gthr);
   return hipGetLastError();
 }
 

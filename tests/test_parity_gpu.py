@@ -263,6 +263,30 @@ def test_clustered_predicate_shapes(B, cols):
     _run_and_check(B, idx, ox, preds, k=100, dsub=8, M=16, seed=2)
 
 
+@pytest.mark.parametrize("cols", [(0,), (0, 1)])
+def test_clustered_wide_key_range(B, cols):
+    """A leading cluster key whose values span ~3e7 integers (too wide for the
+    value -> row table, so every interval bound comes from the 64-ary search)
+    and, for comparison, the same rows with a narrow key (table lookups):
+    both give the oracle's results."""
+    say(f"[clustered] wide key cols={cols}")
+    S, OFF = 1_000_003, -(1 << 30)
+    base = [[(0, 3, 9)], [(0, 7, 8), (1, 2, 20)], [(0, 0, 30)], [(0, 29, 30)], [(0, 12, 12)],
+            [(0, -5, 2)], [(0, 28, 1 << 20)], [(0, 5, 6), (1, 5, 6)], [(1, 3, 7)], []]
+    for wide in (True, False):
+        ix = random_index(20_000, 16, 8, 2, 30, 43, device="cuda")
+        preds = base
+        if wide:
+            ix["attrs"][0] = ix["attrs"][0] * S + OFF
+            preds = [[(c, lo * S + OFF, hi * S + OFF) if c == 0 else (c, lo, hi) for c, lo, hi in p]
+                     for p in base]
+        idx = B.Index(ix["codes"], ix["C_pq"], ix["attrs"], ix["bank"], ix["W"], ix["r"], ix["h"],
+                      ix["hash_seed"], max_batch=16, max_k=32, cluster_cols=cols)
+        ox = oracle_index(ix["codes"], ix["C_pq"], ix["attrs"], ix["bank"], ix["W"], ix["r"], ix["h"],
+                          ix["hash_seed"])
+        _run_and_check(B, idx, ox, preds, k=32, dsub=8, M=16)
+
+
 @pytest.mark.parametrize("cols", [(0,), (1, 0)])
 def test_clustered_chunk_grid_and_fallback(B, cols):
     """Chunks cut on a grid of cells (forced small here; long spans get one by
