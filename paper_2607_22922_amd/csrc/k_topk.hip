@@ -3,9 +3,10 @@
 // ascending order, ties to the smaller id, padding with (-1, +inf) when the
 // candidate pool holds fewer than k vectors.
 //
-// One wavefront per query streams its partial keys through the same
-// threshold-filtered pool used by the scan; the partial lists are each sorted,
-// so after the first few lists almost every key is rejected by one compare.
+// One wavefront per query streams its partial keys (512 at a time, loaded
+// together) through the same threshold-filtered pool used by the scan; the
+// partial lists are each sorted, so after the first few lists almost every
+// key is rejected by one compare.
 // When the scan's chunks are absolute cells of a grid, only the slots of the
 // cells the query's row interval touches are read (the scan leaves the others
 // unwritten).
@@ -15,6 +16,8 @@
 namespace ifvs {
 
 namespace {
+
+constexpr int kMergeBatch = 8;
 
 __global__ __launch_bounds__(64) void topk_merge_kernel(const uint64_t* __restrict__ partials,
                                                         int64_t per_query, int k, int kpl,
@@ -39,10 +42,19 @@ __global__ __launch_bounds__(64) void topk_merge_kernel(const uint64_t* __restri
       end = min(per_query, ((r1 + 63) / 64 - 1) / cell_tiles * slot_keys + slot_keys);
     }
   }
-  for (int64_t b = first; b < end; b += 64) {
-    const int64_t i = b + lane;
-    const uint64_t key = i < end ? src[i] : kNoKey;
-    pool_push(pool, cnt, thr, key, key < thr, k, kpl);
+  // kMergeBatch chunks of 64 keys are loaded together, then offered in order.
+  for (int64_t b = first; b < end; b += 64 * kMergeBatch) {
+    uint64_t keys[kMergeBatch];
+#pragma unroll
+    for (int u = 0; u < kMergeBatch; ++u) {
+      const int64_t i = b + 64 * u + lane;
+      keys[u] = i < end ? src[i] : kNoKey;
+    }
+#pragma unroll
+    for (int u = 0; u < kMergeBatch; ++u) {
+      if (b + 64 * u >= end) break;
+      pool_push(pool, cnt, thr, keys[u], keys[u] < thr, k, kpl);
+    }
   }
   pool_compact(pool, cnt, thr, k, kpl);
   for (int e = lane; e < k; e += 64) {
