@@ -219,6 +219,9 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
                                      the rows, within the row-list capacity, are scored from
                                      their compacted row list), 1 every query whose list fits,
                                      2 never (every query takes the tiled scan)               */
+#define IFVS_OPT_SLOT_ORDER 8     /* chunk-grid scans: 0 dispatch whole-cell slots first in cell
+                                     order, then the others by decreasing estimated work (the
+                                     last workgroups are short), 1 slots in index order       */
 ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value);
 
 /* ifvs_read_profile -- with IFVS_OPT_PROFILE on, every kernel the index

@@ -101,6 +101,8 @@ struct ifvs_index {
   int32_t* qorder_dev = nullptr; // [max_batch]
   int64_t* iv_dev = nullptr;     // [max_batch][2]
   uint64_t* gthr_dev = nullptr;  // [max_batch] shared scan thresholds
+  int32_t* slot_order_dev = nullptr;  // [slot_order_cap] chunk-grid scan dispatch order
+  int64_t slot_order_cap = 0;
   DevPred* staging[kStagingSlots] = {};   // pinned: [max_batch] DevPred + [max_batch] int32
   DevPred* staging_dev[kStagingSlots] = {};  // the same slots as the device addresses them
   hipEvent_t staged[kStagingSlots] = {};
@@ -130,6 +132,7 @@ struct ifvs_index {
   int64_t opt_grid_tiles = 0;
   int opt_gather = 0;   // 0 automatic, 1 every query whose list fits, 2 never
   int opt_grid_relative = 0;   // 1: grid chunks relative to each query tile's first cell
+  int opt_slot_order = 0;      // 0: chunk-grid slots in estimated-work order, 1: in index order
   int opt_gather_auto_pct = 30;   // automatic mode: pools up to this % of the rows
   int profile_mask = 0;          // stages timed with HIP events (IFVS_OPT_PROFILE)
   StageTimer* timers = nullptr;  // [kStages] once profiling was enabled
@@ -149,6 +152,7 @@ struct ifvs_index {
                     static_cast<void*>(perm), static_cast<void*>(bank), static_cast<void*>(W),
                     static_cast<void*>(preds_dev), static_cast<void*>(qorder_dev),
                     static_cast<void*>(iv_dev), static_cast<void*>(gthr_dev), static_cast<void*>(bitmap),
+                    static_cast<void*>(slot_order_dev),
                     static_cast<void*>(counts), static_cast<void*>(count_parts), static_cast<void*>(vstart),
                     static_cast<void*>(partials), static_cast<void*>(codes_rm),
                     static_cast<void*>(lists), static_cast<void*>(list_n), static_cast<void*>(qmode)})
@@ -282,14 +286,18 @@ ifvs_status normalize_predicates(const ifvs_index* idx, int32_t nq, const ifvs_p
   return IFVS_OK;
 }
 
-// Estimated 64-row tiles of a query's cluster-key interval, from the fences
-// (exact to within two fence gaps).
-int64_t estimate_interval_tiles(const ifvs_index* idx, const DevPred& d) {
+// Estimated 64-row tiles [*t_lo, *t_hi) of a query's cluster-key interval,
+// from the fences (widened by one fence gap on each side).
+void estimate_interval_range(const ifvs_index* idx, const DevPred& d, int64_t* t_lo, int64_t* t_hi) {
   const auto& f0 = idx->fence0;
   const auto& f1 = idx->fence1;
   const int64_t nf = static_cast<int64_t>(f0.size());
-  if (d.n_eff < 0 || nf == 0) return 0;
-  if (d.iv_mode == 0) return idx->n_tiles;
+  *t_lo = *t_hi = 0;
+  if (d.n_eff < 0 || nf == 0) return;
+  if (d.iv_mode == 0) {
+    *t_hi = idx->n_tiles;
+    return;
+  }
   auto rank = [&](int64_t x0, int64_t x1) {      // fences below (x0, x1)
     int64_t lo = 0, hi = nf;
     while (lo < hi) {
@@ -302,8 +310,72 @@ int64_t estimate_interval_tiles(const ifvs_index* idx, const DevPred& d) {
   };
   const int64_t r0 = d.iv_mode == 2 ? rank(d.iv_lo0, d.iv_lo1) : rank(d.iv_lo0, 0);
   const int64_t r1 = d.iv_mode == 2 ? rank(d.iv_lo0, d.iv_hi1) : rank(d.iv_hi0, 0);
-  const int64_t rows = (r1 - r0 + 1) * idx->n / (nf - 1);
-  return std::min<int64_t>(idx->n_tiles, rows / 64 + 1);
+  const int64_t row_lo = std::max<int64_t>(0, r0 - 1) * idx->n / (nf - 1);
+  const int64_t row_hi = std::min<int64_t>(idx->n, r1 * idx->n / (nf - 1));
+  *t_lo = std::min<int64_t>(idx->n_tiles, row_lo / 64);
+  *t_hi = std::min<int64_t>(idx->n_tiles, std::max<int64_t>(*t_lo, (row_hi + 63) / 64));
+}
+
+// Estimated 64-row tiles of a query's cluster-key interval.
+int64_t estimate_interval_tiles(const ifvs_index* idx, const DevPred& d) {
+  int64_t lo = 0, hi = 0;
+  estimate_interval_range(idx, d, &lo, &hi);
+  return hi - lo;
+}
+
+// Dispatch order of a chunk-grid scan's slots.  Slot (query tile t, cell c)
+// of XCD x is item c * per_xcd + (t - x * per_xcd); out[x * per_xcd * splits
+// + i] is XCD x's i-th item.  Every item of every XCD appears once.  Items
+// whose estimated work is a whole cell come first, in cell order (all XCDs
+// walk the same cells together), then the rest by decreasing estimated work
+// in steps of 1/16 cell, and the estimated-empty ones last: the workgroups
+// dispatched last are short, so fewer CUs idle at the end of the launch.
+void order_scan_slots(const ifvs_index* idx, const DevPred* host, const int32_t* qorder, int nq,
+                      const ScanPlan& plan, int32_t* out) {
+  const int n_qtiles = (nq + plan.qtile - 1) / plan.qtile;
+  const int per_xcd = (n_qtiles + 7) / 8;
+  const int64_t g = plan.chunk_tiles;
+  const int64_t step = std::max<int64_t>(1, g / 16);
+  std::vector<int64_t> hull_lo(n_qtiles, 0), hull_hi(n_qtiles, 0);
+  for (int t = 0; t < n_qtiles; ++t) {
+    int64_t lo = INT64_MAX, hi = 0;
+    for (int qi = 0; qi < plan.qtile && t * plan.qtile + qi < nq; ++qi) {
+      int64_t a = 0, b = 0;
+      estimate_interval_range(idx, host[qorder[t * plan.qtile + qi]], &a, &b);
+      if (b > a) {
+        lo = std::min(lo, a);
+        hi = std::max(hi, b);
+      }
+    }
+    if (hi > lo) {
+      hull_lo[t] = lo;
+      hull_hi[t] = hi;
+    }
+  }
+  constexpr int kBuckets = 18;   // 0: empty, 1..16: partial in 1/16-cell steps, 17: whole cell
+  const int64_t items = static_cast<int64_t>(per_xcd) * plan.splits;
+  std::vector<uint8_t> bucket(static_cast<size_t>(items));
+  for (int x = 0; x < 8; ++x) {
+    int64_t count[kBuckets] = {};
+    for (int c = 0; c < plan.splits; ++c) {
+      for (int ql = 0; ql < per_xcd; ++ql) {
+        const int t = x * per_xcd + ql;
+        int64_t work = 0;
+        if (t < n_qtiles) work = std::max<int64_t>(0, std::min(hull_hi[t], (c + 1) * g) - std::max(hull_lo[t], c * g));
+        const int b = work >= g ? kBuckets - 1 : (work == 0 ? 0 : 1 + static_cast<int>(std::min<int64_t>(15, work / step)));
+        bucket[static_cast<size_t>(c) * per_xcd + ql] = static_cast<uint8_t>(b);
+        ++count[b];
+      }
+    }
+    int64_t start[kBuckets];
+    int64_t pos = 0;
+    for (int b = kBuckets - 1; b >= 0; --b) {
+      start[b] = pos;
+      pos += count[b];
+    }
+    int32_t* o = out + x * items;
+    for (int64_t i = 0; i < items; ++i) o[start[bucket[i]]++] = static_cast<int32_t>(i);
+  }
 }
 
 // Validate and normalize predicates into the next pinned staging slot (and
@@ -639,8 +711,16 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
     return bail(st);
   if ((st = dev_alloc(&idx->gthr_dev, static_cast<size_t>(d.max_batch), "scan thresholds")) != IFVS_OK)
     return bail(st);
+  // Room for the dispatch order of a chunk-grid scan: 8 XCD runs of query
+  // tiles times cells of at least 2048 tiles (the automatic grid uses
+  // larger ones), between 2^16 and 2^20 items.
+  idx->slot_order_cap = std::min<int64_t>(
+      int64_t{1} << 20,
+      std::max<int64_t>(int64_t{1} << 16, 8 * ((d.max_batch + 7) / 8) * ((idx->n_tiles + 2047) / 2048)));
+  if ((st = dev_alloc(&idx->slot_order_dev, static_cast<size_t>(idx->slot_order_cap), "scan dispatch order")) != IFVS_OK)
+    return bail(st);
   for (int i = 0; i < kStagingSlots; ++i) {
-    const size_t bytes = (sizeof(DevPred) + sizeof(int32_t)) * d.max_batch;
+    const size_t bytes = (sizeof(DevPred) + sizeof(int32_t)) * d.max_batch + sizeof(int32_t) * idx->slot_order_cap;
     if (forced_alloc_failure() ||
         hipHostMalloc(reinterpret_cast<void**>(&idx->staging[i]), bytes, hipHostMallocDefault) != hipSuccess) {
       idx->staging[i] = nullptr;
@@ -689,6 +769,10 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
     case IFVS_OPT_GATHER:
       if (value > 2) return fail(IFVS_E_INVALID, "IFVS_OPT_GATHER takes 0, 1 or 2");
       idx->opt_gather = static_cast<int>(value);
+      return IFVS_OK;
+    case IFVS_OPT_SLOT_ORDER:
+      if (value > 1) return fail(IFVS_E_INVALID, "IFVS_OPT_SLOT_ORDER takes 0 or 1");
+      idx->opt_slot_order = static_cast<int>(value);
       return IFVS_OK;
     case IFVS_OPT_PROFILE:
       if (value != 0 && !idx->timers) {
@@ -785,11 +869,24 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   }
   ScanPlan plan{};
   if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, interval_batch, span, &plan); st != IFVS_OK) return st;
+  // Chunk-grid scans: the slot dispatch order goes into the staging slot and
+  // the interval kernel copies it to the device.
+  const int32_t* qorder_host = reinterpret_cast<const int32_t*>(host + idx->max_batch);
+  int32_t* order_host = reinterpret_cast<int32_t*>(host + idx->max_batch) + idx->max_batch;
+  const int64_t n_order = plan.abs_cells && idx->opt_slot_order == 0
+                              ? static_cast<int64_t>(8) * ((((nq + plan.qtile - 1) / plan.qtile) + 7) / 8) * plan.splits
+                              : 0;
+  const bool ordered = n_order > 0 && n_order <= idx->slot_order_cap;
+  if (ordered) order_scan_slots(idx, host, qorder_host, nq, plan, order_host);
   IFVS_LAUNCH(idx, kStFilter, s, "launching interval kernel",
               launch_intervals(idx->attrs_phys, idx->n, idx->c0, idx->c1, idx->vstart, idx->vmin, idx->vcount,
                                idx->staging_dev[slot],
                                reinterpret_cast<const int32_t*>(idx->staging_dev[slot] + idx->max_batch), nq,
-                               idx->preds_dev, idx->qorder_dev, idx->iv_dev, idx->gthr_dev, s));
+                               idx->preds_dev, idx->qorder_dev, idx->iv_dev, idx->gthr_dev,
+                               ordered ? reinterpret_cast<const int32_t*>(idx->staging_dev[slot] + idx->max_batch) +
+                                             idx->max_batch
+                                       : nullptr,
+                               idx->slot_order_dev, ordered ? n_order : 0, s));
   if (ifvs_status st = release_slot(idx, slot, s); st != IFVS_OK) return st;
   // Masked batches: a query whose pool is small is scored from its compacted
   // row list (decided on the device from the pool size); the rest take the
@@ -831,6 +928,7 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   b.partials = idx->partials;
   b.gthr = idx->gthr_dev;
   b.mode = gather ? idx->qmode : nullptr;
+  b.slot_order = ordered ? idx->slot_order_dev : nullptr;
   IFVS_LAUNCH(idx, kStScan, s, "launching scan kernel", launch_scan(b, plan, s));
   if (gather) {
     GatherBatch g{};

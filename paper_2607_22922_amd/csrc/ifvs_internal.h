@@ -72,10 +72,13 @@ hipError_t launch_gather_attrs(const int32_t* attrs, int64_t n, int n_attr, cons
 // per-query global thresholds.
 // vstart (may be null): vstart[t] = first physical row whose leading cluster
 // key is >= vmin + t, for t < vcount (the last entry is n).
+// It also copies n_slots words of the scan's dispatch order from the
+// staging slot (slots_src) to slots_dst.
 hipError_t launch_intervals(const int32_t* attrs_phys, int64_t n, int c0, int c1, const int32_t* vstart,
                             int64_t vmin, int64_t vcount, const DevPred* staged_preds,
                             const int32_t* staged_order, int nq, DevPred* preds_out, int32_t* order_out,
-                            int64_t* iv, uint64_t* gthr, hipStream_t s);
+                            int64_t* iv, uint64_t* gthr, const int32_t* slots_src, int32_t* slots_dst,
+                            int64_t n_slots, hipStream_t s);
 
 // codes (row-major [n][m]) -> 64-row tiles, physical row r taken from
 // original row perm[r] (perm may be null: identity).
@@ -141,6 +144,7 @@ struct ScanBatch {
   uint64_t* partials;           // [nq positions][splits][waves][k]
   uint64_t* gthr;               // [nq] shared thresholds, all-ones before the scan
   const int32_t* mode;          // [nq] 1: the query is scored by the gather scan (null: none is)
+  const int32_t* slot_order;    // chunk-grid dispatch order (null: slots in index order)
 };
 
 // Gather scan of compacted row lists (masked batches, few selected rows).

@@ -92,9 +92,14 @@ __global__ __launch_bounds__(64) void intervals_kernel(const int32_t* __restrict
                                                        DevPred* __restrict__ preds_out,
                                                        int32_t* __restrict__ order_out,
                                                        int64_t* __restrict__ iv,
-                                                       uint64_t* __restrict__ gthr) {
+                                                       uint64_t* __restrict__ gthr,
+                                                       const int32_t* __restrict__ slots_src,
+                                                       int32_t* __restrict__ slots_dst, int64_t n_slots) {
   const int q = blockIdx.x >> 1;        // two wavefronts per query: lower and upper bound
   const bool upper = blockIdx.x & 1;
+  // The scan's dispatch order, spread over all workgroups of this launch.
+  for (int64_t i = blockIdx.x * 64 + threadIdx.x; i < n_slots; i += static_cast<int64_t>(gridDim.x) * 64)
+    slots_dst[i] = slots_src[i];
   if (q >= nq) return;
   __shared__ DevPred sp;
   copy_pred(staged_preds + q, &sp, threadIdx.x);
@@ -179,9 +184,11 @@ hipError_t launch_gather_attrs(const int32_t* attrs, int64_t n, int n_attr, cons
 hipError_t launch_intervals(const int32_t* attrs_phys, int64_t n, int c0, int c1, const int32_t* vstart,
                             int64_t vmin, int64_t vcount, const DevPred* staged_preds,
                             const int32_t* staged_order, int nq, DevPred* preds_out, int32_t* order_out,
-                            int64_t* iv, uint64_t* gthr, hipStream_t s) {
+                            int64_t* iv, uint64_t* gthr, const int32_t* slots_src, int32_t* slots_dst,
+                            int64_t n_slots, hipStream_t s) {
   intervals_kernel<<<dim3(2 * nq), dim3(64), 0, s>>>(attrs_phys, n, c0, c1, vstart, vmin, vcount, staged_preds,
-                                                     staged_order, nq, preds_out, order_out, iv, gthr);
+                                                     staged_order, nq, preds_out, order_out, iv, gthr, slots_src,
+                                                     slots_dst, n_slots);
   return hipGetLastError();
 }
 

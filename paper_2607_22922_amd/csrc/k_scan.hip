@@ -62,6 +62,10 @@ struct ScanArgs {
   uint64_t* partials;
   uint64_t* gthr;   // [nq] per original query: smallest k-th key any wavefront has published
   const int32_t* mode;   // [nq] 1: scored by the gather scan instead (null: none)
+  // Dispatch order (null: index order): workgroup b scans item
+  // slot_order[(b % kXcds) * per_xcd * splits + b / kXcds] of its XCD, item
+  // c * per_xcd + t meaning chunk c of the XCD's t-th query tile.
+  const int32_t* slot_order;
 };
 
 // Bits [lo, hi) of a 64-bit word, 0 <= lo < hi <= 64.
@@ -108,8 +112,9 @@ void scan_kernel(const ScanArgs a) {
   // by chunk: chunk c of all its query tiles, then chunk c + 1, so every XCD
   // has work and empty chunks come last.
   const int xcd = blockIdx.x % kXcds;
-  const int slot = blockIdx.x / kXcds;
   const int per_xcd = (a.n_qtiles + kXcds - 1) / kXcds;
+  const int slot = a.slot_order ? a.slot_order[static_cast<int64_t>(xcd) * per_xcd * a.splits + blockIdx.x / kXcds]
+                                : static_cast<int>(blockIdx.x / kXcds);
   const int chunk = slot / per_xcd;
   const int qtile = xcd * per_xcd + slot % per_xcd;
   if (qtile >= a.n_qtiles || chunk >= a.splits) return;   // grid padding
@@ -579,6 +584,7 @@ hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s) 
   a.chunk_tiles = plan.chunk_tiles;
   a.abs_cells = plan.abs_cells ? 1 : 0;
   a.mode = b.mode;
+  a.slot_order = b.slot_order;
   a.partials = b.partials;
   a.gthr = b.gthr;
   a.splits = plan.splits;

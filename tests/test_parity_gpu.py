@@ -311,20 +311,24 @@ def test_clustered_chunk_grid_and_fallback(B, cols):
         ids_o, dist_o = O.select_topk(O.adc_distances(lut_o, ox["codes"], cand), cand, 20)
         check_search_row(_np(ids0[i]), _np(dist0[i]), ids_o, dist_o, f"grid q{i}")
     # absolute cells (64-tile grid: one chunk per cell fits), relative cells,
-    # and grids whose cells outnumber the chunks (equal-chunk fallback)
-    for grid, splits, relative in ((64, 0, 0), (64, 0, 1), (100, 0, 0), (1, 0, 0), (7, 0, 1), (7, 2, 0),
-                                   (1, 3, 1), (64, 1, 0)):
+    # and grids whose cells outnumber the chunks (equal-chunk fallback); for
+    # absolute cells both dispatch orders (estimated work, index order)
+    for grid, splits, relative, order in ((64, 0, 0, 0), (64, 0, 0, 1), (64, 0, 1, 0), (100, 0, 0, 0),
+                                          (1, 0, 0, 0), (1, 0, 0, 1), (7, 0, 1, 0), (7, 2, 0, 0),
+                                          (1, 3, 1, 0), (64, 1, 0, 0), (13, 0, 0, 0)):
         idx.set_option(B.OPT_GRID_TILES, grid)
         idx.set_option(B.OPT_SPLITS, splits)
         idx.set_option(B.OPT_GRID_RELATIVE, relative)
+        idx.set_option(B.OPT_SLOT_ORDER, order)
         ids, dist = idx.search(preds, lut, 20)
         torch.cuda.synchronize()
         assert idx.last_plan()["grid_tiles"] == grid
-        assert torch.equal(ids, ids0), (grid, splits, relative)
-        assert torch.equal(dist.view(torch.int32), dist0.view(torch.int32)), (grid, splits, relative)
+        assert torch.equal(ids, ids0), (grid, splits, relative, order)
+        assert torch.equal(dist.view(torch.int32), dist0.view(torch.int32)), (grid, splits, relative, order)
     idx.set_option(B.OPT_GRID_TILES, 0)
     idx.set_option(B.OPT_SPLITS, 0)
     idx.set_option(B.OPT_GRID_RELATIVE, 0)
+    idx.set_option(B.OPT_SLOT_ORDER, 0)
 
 
 @pytest.mark.parametrize("cluster_cols,M,dsub,k,lut_dtype", [((), 16, 8, 10, "f32"), ((), 48, 2, 100, "f32"),
