@@ -1,19 +1,23 @@
 #!/usr/bin/env python3
 """Benchmark of the iFVS filtered-search hot path on one MI355X.
 
-Workload: 10M base vectors of 96 dims, PQ with 48 subspaces of 2 dims
-(48 B of codes per vector), one date-like int32 attribute uniform over
+Default workload (c4): 10M base vectors of 96 dims, PQ with 48 subspaces of
+2 dims (48 B of codes per vector), one date-like int32 attribute uniform over
 [0, 3650), range predicates at 0.1% / 1% / 10% / 50% selectivity, batches of
 256 queries, k = 10, every step of the path in the conditioned mode (memory
 bank, direction tensor, predicate weights).  Synthetic, seeded, generated on
 the GPU (the paper's SIFT10M-style workload is not available here).
+`--config c1|c2|c3|c5` measures the other synthetic workloads the same way
+(1M x 128 with a range and a category clause, 1M x 960 with k = 100,
+100M x 128, and the 10K-vector toy); rows are clustered by the range
+attribute, or by (category, range attribute) where queries carry both.
 
-One step = one batch of 256 queries from each of the four selectivity bins,
-each batch going through select_codebook -> build_lut -> filtered_search.
-`value` is queries per second over the timed steps, inputs resident in HBM.
-In the timed region only the scan kernel (the roofline kernel) is bracketed
-by HIP events; the per-stage breakdown comes from a short pass of its own in
-which every kernel is bracketed.
+One step = one batch of queries from each selectivity bin, each batch going
+through select_codebook -> build_lut -> filtered_search.  `value` is queries
+per second over the timed steps, inputs resident in HBM.  In the timed
+region only the scan kernel (the roofline kernel) is bracketed by HIP
+events; the per-stage breakdown comes from a short pass of its own in which
+every kernel is bracketed.
 
 Prints one JSON line.  Progress goes to stderr.
 """
@@ -69,29 +73,54 @@ def read_counters():
         return None
 
 
-def exact_filtered_knn(x, attrs, queries, preds, k, chunk=1 << 21):
-    """Ground truth for recall: exact filtered kNN on the raw fp32 vectors
-    (squared L2, computed on the GPU in chunks)."""
-    nq = queries.shape[0]
-    lo = torch.tensor([p[0][1] for p in preds], device=x.device, dtype=torch.int64)
-    hi = torch.tensor([p[0][2] for p in preds], device=x.device, dtype=torch.int64)
-    qn = (queries.double() ** 2).sum(1)
-    best_d = torch.full((nq, k), float("inf"), device=x.device, dtype=torch.float64)
-    best_i = torch.full((nq, k), -1, device=x.device, dtype=torch.int64)
-    for s in range(0, x.shape[0], chunk):
-        xb = x[s:s + chunk]
-        a = attrs[0, s:s + chunk].long()
-        d = (xb.double() ** 2).sum(1)[None, :] - 2.0 * (queries.double() @ xb.double().t()) + qn[:, None]
-        ok = (a[None, :] >= lo[:, None]) & (a[None, :] < hi[:, None])
-        d = torch.where(ok, d, torch.full_like(d, float("inf")))
-        kk = min(k, d.shape[1])
-        v, i = torch.topk(d, kk, dim=1, largest=False)
-        cd = torch.cat([best_d, v], 1)
-        ci = torch.cat([best_i, i + s], 1)
-        v2, j = torch.topk(cd, k, dim=1, largest=False)
-        best_d, best_i = v2, torch.gather(ci, 1, j)
-    return best_i, best_d
+def clause_tensors(preds, device):
+    """Clause lists as padded [nq][C] tensors (col, lo, hi); padding admits
+    every value."""
+    C = max(1, max(len(p) for p in preds))
+    col = torch.zeros(len(preds), C, dtype=torch.int64)
+    lo = torch.full((len(preds), C), -(1 << 62), dtype=torch.int64)
+    hi = torch.full((len(preds), C), 1 << 62, dtype=torch.int64)
+    for i, p in enumerate(preds):
+        for j, (c, a, b) in enumerate(p):
+            col[i, j], lo[i, j], hi[i, j] = c, a, b
+    return col.to(device), lo.to(device), hi.to(device)
 
+
+def exact_filtered_knn(name, N, attrs, queries, preds_by_bin, k):
+    """Ground truth for recall: exact filtered kNN on the raw fp32 vectors
+    (squared L2 in fp64), streamed over the regenerated base vectors so that
+    no config needs its raw vectors kept.  Returns {bin: ids [nq][k]}."""
+    from workload import base_chunks
+    dev = queries.device
+    nq = queries.shape[0]
+    qd = queries.double()
+    qn = (qd ** 2).sum(1)
+    cl = {s: clause_tensors(p, dev) for s, p in preds_by_bin.items()}
+    best = {s: (torch.full((nq, k), float("inf"), device=dev, dtype=torch.float64),
+                torch.full((nq, k), -1, device=dev, dtype=torch.int64)) for s in preds_by_bin}
+    for s0, xb in base_chunks(name, dev, N):
+        rows = xb.shape[0]
+        xd = xb.double()
+        d = (xd ** 2).sum(1)[None, :] - 2.0 * (qd @ xd.t()) + qn[:, None]
+        vals = attrs[:, s0:s0 + rows].long()
+        for s, (col, lo, hi) in cl.items():
+            ok = torch.ones(nq, rows, dtype=torch.bool, device=dev)
+            for j in range(col.shape[1]):
+                v = vals[col[:, j]]                                   # [nq][rows]
+                ok &= (v >= lo[:, j, None]) & (v < hi[:, j, None])
+            dd = torch.where(ok, d, torch.full_like(d, float("inf")))
+            v_, i_ = torch.topk(dd, min(k, rows), dim=1, largest=False)
+            bd, bi = best[s]
+            cd = torch.cat([bd, v_], 1)
+            ci = torch.cat([bi, i_ + s0], 1)
+            v2, j2 = torch.topk(cd, k, dim=1, largest=False)
+            best[s] = (v2, torch.gather(ci, 1, j2))
+    return {s: torch.where(torch.isinf(v), torch.full_like(i, -1), i) for s, (v, i) in best.items()}
+
+
+# Clustering of each workload's rows: the range attribute, or (category,
+# range attribute) where the queries carry an equality on the category.
+CLUSTER_COLS = {"c1": (0,), "c2": (1, 0), "c3": (0,), "c4": (0,), "c5": (1, 0)}
 
 SCAN_WAVES = 8   # wavefronts per scan workgroup, each writing k partial keys per chunk
 
@@ -119,6 +148,16 @@ def scan_bytes_interval(w, sorted_attr, preds, plan, k, lut_entry):
             float((r1 - r0).sum()) * w.M)
 
 
+def scan_bytes_passing(idx, w, preds, lut_entry):
+    """Bytes a scan of this batch must read at the least: the codes of every
+    (query, passing row) pair and each query's table.  Used where clustered
+    intervals are composite (category, range) and the tile count of an
+    interval is not a one-column search."""
+    _, cnt = idx.filter(preds)
+    useful = float(cnt.sum()) * w.M
+    return useful + len(preds) * w.M * 256 * lut_entry, useful
+
+
 def scan_bytes_bitmap(idx, w, preds, qt, splits, k, lut_entry):
     """Algorithmic bytes of one bitmap-scan launch (qt queries per tile): the
     code tiles any query of a tile selects, every query's bitmap words, its
@@ -141,11 +180,16 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--queries", type=int, default=10_000, help="queries drawn per bin")
+    ap.add_argument("--config", choices=sorted(CLUSTER_COLS), default="c4",
+                    help="synthetic workload (c4, the 10M-vector one, is the headline)")
+    ap.add_argument("--queries", type=int, default=None,
+                    help="queries drawn per bin (default: the config's count, at most 10,000)")
     ap.add_argument("--cpu-sample", type=int, default=2, help="oracle queries per bin (0 = skip)")
-    ap.add_argument("--recall-queries", type=int, default=256)
-    ap.add_argument("--plain-steps", type=int, default=5,
-                    help="steps timed on the unclustered (bitmap) layout for comparison (0 = skip)")
+    ap.add_argument("--recall-queries", type=int, default=None,
+                    help="queries per bin checked against exact filtered kNN (default 256; 100 on c1 and c5)")
+    ap.add_argument("--plain-steps", type=int, default=None,
+                    help="steps timed on the unclustered (bitmap) layout for comparison "
+                         "(0 = skip; default 5 on c4, else 0)")
     ap.add_argument("--lut", choices=["f32", "f16"], default="f32")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain copy kernel of known size (for counter calibration)")
@@ -162,19 +206,26 @@ def main():
 
     torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
-    name = "c4"
+    name = args.config
     cfg = CONFIGS[name]
-    batch, k = cfg["batch"], cfg["k"]
+    n_q = args.queries if args.queries is not None else min(cfg["n_queries"], 10_000)
+    batch, k = min(cfg.get("batch", 256), n_q), cfg["k"]
+    if args.plain_steps is None:
+        args.plain_steps = 5 if name == "c4" else 0
+    if args.recall_queries is None:
+        args.recall_queries = 100 if name in ("c1", "c5") else 256
+    cols = CLUSTER_COLS[name]
+    tile_bytes = cols == (0,)      # one-column intervals: bytes counted per code tile
     lut_dt = B.LUT_F16 if args.lut == "f16" else B.LUT_F32
     lut_entry = 2 if lut_dt == B.LUT_F16 else 4
     t0 = time.time()
     log(f"[bench] generating {name} on {dev}")
-    w = make_workload(name, device=dev, n_queries=args.queries)
+    w = make_workload(name, device=dev, n_queries=n_q, keep_x=False)
     torch.cuda.synchronize()
     log(f"[bench] generated in {time.time() - t0:.1f}s; loading indexes")
-    clus = B.Index.from_workload(w, max_batch=batch, max_k=k, cluster_cols=(0,))
+    clus = B.Index.from_workload(w, max_batch=batch, max_k=k, cluster_cols=cols)
     plain = B.Index.from_workload(w, max_batch=batch, max_k=k) if args.plain_steps > 0 else None
-    n_batches = args.queries // batch
+    n_batches = n_q // batch
     bins = w.bins
 
     # Marshalled inputs per (bin, batch): packed predicates; device buffers.
@@ -240,15 +291,16 @@ def main():
     qps = n_queries / (total_ms / 1e3)
     log(f"[bench] clustered: {args.steps} steps in {total_ms:.1f} ms -> {qps:.0f} queries/s")
 
-    sorted_attr = torch.sort(w.attrs[0].long()).values
+    sorted_attr = torch.sort(w.attrs[0].long()).values if tile_bytes else None
     bins_out = {}
     scan_bytes_total = useful_total = 0.0
     for s in bins:
         cache = {}
         for b, _ in per_bin[s]:
             if b not in cache:
-                cache[b] = scan_bytes_interval(w, sorted_attr, w.preds[s][b * batch:(b + 1) * batch],
-                                               plans[s], k, lut_entry)
+                bp = w.preds[s][b * batch:(b + 1) * batch]
+                cache[b] = (scan_bytes_interval(w, sorted_attr, bp, plans[s], k, lut_entry) if tile_bytes
+                            else scan_bytes_passing(clus, w, bp, lut_entry))
             scan_bytes_total += cache[b][0]
             useful_total += cache[b][1]
         ms = [m for _, m in per_bin[s]]
@@ -307,11 +359,15 @@ def main():
     # Recall@k of the identity mode (alpha = 0, w_f = 1: plain PQ ADC) and of
     # the synthetic conditioned mode, against exact filtered kNN.
     nr = min(args.recall_queries, batch)
+    gt_all = {}
+    if nr > 0:
+        t_gt = time.time()
+        gt_all = exact_filtered_knn(name, w.N, w.attrs, w.queries[:nr], {s: w.preds[s][:nr] for s in bins}, k)
+        log(f"[bench] exact filtered kNN of {nr} queries x {len(bins)} bins in {time.time() - t_gt:.1f}s")
     for s in (bins if nr > 0 else []):
         q = w.queries[:nr]
         preds = w.preds[s][:nr]
-        gt, _ = exact_filtered_knn(w.x, w.attrs, q, preds, k)
-        t_np = gt.cpu().numpy()
+        t_np = gt_all[s].cpu().numpy()
         for mode in ("identity", "conditioned"):
             if mode == "identity":
                 lt = clus.build_lut(q, None, None, lut_dt)
@@ -367,7 +423,7 @@ def main():
             torch.neg(src, out=dst)
         torch.cuda.synchronize()
 
-    traffic = read_counters()
+    traffic = read_counters() if name == "c4" else None
     out = {
         "metric": METRIC,
         "value": qps,
@@ -383,8 +439,10 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{name}: {DESCRIPTIONS[name]}", "batch": batch, "k": k,
                    "bins": bins, "mode": "conditioned (bank, W, w_z)",
-                   "layout": "rows clustered by the date attribute",
-                   "queries_per_step": len(bins) * batch},
+                   "layout": ("rows clustered by the range attribute" if cols == (0,)
+                              else "rows clustered by (category, range attribute)"),
+                   "queries_per_step": len(bins) * batch,
+                   "recall_queries_per_bin": nr},
         "bins": bins_out,
         "stage_ms_per_step": {st: round(v[0] / stage_steps, 4) for st, v in stage_prof.items()},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
@@ -392,6 +450,8 @@ def main():
                      "traffic_over_algorithmic": (round(traffic / bytes_per_launch, 4)
                                                   if traffic is not None else None),
                      "kernel": "scan_kernel", "avg_launch_ms": scan_avg_ms,
+                     "bytes_definition": ("code tiles overlapping each query's row interval + table + partial lists"
+                                          if tile_bytes else "codes of every (query, passing row) pair + table"),
                      "bytes_per_launch": bytes_per_launch,
                      "useful_bytes_per_launch": useful_total / max(1, scan_launches)},
         "plain_layout": plain_out,

@@ -7,7 +7,7 @@ import pytest
 import torch
 
 import oracle as O
-from workload import make_workload
+from workload import base_chunks, make_workload
 from workload.synth import CONFIGS, make_attributes, make_predicates, zipf_probs
 
 
@@ -66,3 +66,12 @@ def test_zipf_frequencies_and_rank_prefix_reading():
     # rank prefix [0, c) whose mass first reaches 0.5 (c = 5)
     preds = make_predicates(CONFIGS["c2"], 0.5, 3, 99)
     assert all(pp[1][1:] == (0, 5) for pp in preds)
+
+
+def test_base_chunks_regenerate_the_workload_vectors():
+    """The chunk stream used for ground truth is the stream the codes were
+    encoded from, at any chunk size that make_workload used."""
+    w = make_workload("c1", n_queries=4, chunk_rows=3000)
+    parts = list(base_chunks("c1", chunk_rows=3000))
+    assert [p for p, _ in parts] == [0, 3000, 6000, 9000]
+    assert torch.equal(torch.cat([c for _, c in parts]), w.x)

@@ -215,6 +215,24 @@ def make_attributes(cfg: dict, N: int, device="cpu") -> torch.Tensor:
 
 
 # ----------------------------------------------------------------- build
+def base_chunks(name: str, device="cpu", N: int | None = None, chunk_rows: int = 1 << 20):
+    """The config's base vectors in generation order: yields (first row,
+    [rows][D] fp32) chunk by chunk, the same stream make_workload encodes, so
+    the raw vectors of a large config can be regenerated (for ground truth)
+    without being kept."""
+    cfg = CONFIGS[name]
+    Nn = int(N if N is not None else cfg["N"])
+    c = cfg["idx"]
+    device = torch.device(device)
+    means = mixture_means(cfg["comps"], cfg["D"], 1000 * c + 0, device)
+    g_base = _gen(1000 * c + 1, device)
+    pos = 0
+    while pos < Nn:
+        rows = min(chunk_rows, Nn - pos)
+        yield pos, mixture_draw(rows, means, g_base)
+        pos += rows
+
+
 def make_workload(name: str, device="cpu", n_queries: int | None = None, N: int | None = None,
                   keep_x: bool = True, chunk_rows: int = 1 << 20) -> Workload:
     """Draw a whole workload.  ``N`` / ``n_queries`` shrink a config for quick
@@ -230,10 +248,11 @@ def make_workload(name: str, device="cpu", n_queries: int | None = None, N: int 
     device = torch.device(device)
 
     means = mixture_means(cfg["comps"], D, 1000 * c + 0, device)
-    # PQ training sample: its own seeded draw from the same mixture
+    # PQ training sample: the first base vectors, topped up by a seeded draw
+    # of its own from the same mixture
     n_sample = min(Nn, KMEANS_SAMPLE)
-    g_base = _gen(1000 * c + 1, device)
-    first = mixture_draw(min(Nn, chunk_rows), means, g_base)
+    chunks = base_chunks(name, device, Nn, chunk_rows)
+    _, first = next(chunks)
     if n_sample <= first.shape[0]:
         sample = first[:n_sample]
     else:
@@ -243,17 +262,13 @@ def make_workload(name: str, device="cpu", n_queries: int | None = None, N: int 
 
     codes = torch.empty(Nn, M, dtype=torch.uint8, device=device)
     xs = [] if keep_x else None
-    pos = 0
-    chunk = first
-    while True:
+    pos, chunk = 0, first
+    while chunk is not None:
         rows = chunk.shape[0]
         codes[pos:pos + rows] = pq_encode(chunk, C_pq)
         if keep_x:
             xs.append(chunk)
-        pos += rows
-        if pos >= Nn:
-            break
-        chunk = mixture_draw(min(chunk_rows, Nn - pos), means, g_base)
+        pos, chunk = next(chunks, (None, None))
     x = torch.cat(xs) if keep_x else None
 
     attrs = make_attributes(cfg, Nn, device)
