@@ -222,6 +222,10 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
 #define IFVS_OPT_SLOT_ORDER 8     /* chunk-grid scans: 0 dispatch whole-cell slots first in cell
                                      order, then the others by decreasing estimated work (the
                                      last workgroups are short), 1 slots in index order       */
+#define IFVS_OPT_SHARED_BOUND 9   /* k <= 16: the wavefronts of a scan workgroup publish their
+                                     best keys and prune with the k-th smallest published key:
+                                     0 automatic (on for chunk-grid scans of long intervals),
+                                     1 never, 2 always                                         */
 ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value);
 
 /* ifvs_read_profile -- with IFVS_OPT_PROFILE on, every kernel the index

@@ -133,6 +133,7 @@ struct ifvs_index {
   int opt_gather = 0;   // 0 automatic, 1 every query whose list fits, 2 never
   int opt_grid_relative = 0;   // 1: grid chunks relative to each query tile's first cell
   int opt_slot_order = 0;      // 0: chunk-grid slots in estimated-work order, 1: in index order
+  int opt_shared_bound = 0;    // workgroup bound from the wavefronts' published best keys: 0 auto, 1 off, 2 on
   int opt_gather_auto_pct = 30;   // automatic mode: pools up to this % of the rows
   int profile_mask = 0;          // stages timed with HIP events (IFVS_OPT_PROFILE)
   StageTimer* timers = nullptr;  // [kStages] once profiling was enabled
@@ -526,6 +527,12 @@ ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_
   plan->splits = static_cast<int>(splits);
   plan->kpl = pool_kpl(k);
   plan->pool_stride = pool_stride_for(k);
+  // The workgroup bound pays on long intervals (chunk-grid cells, about 1%
+  // less scan time at 50% selectivity on 10M x 48-byte codes); on short ones
+  // its extra compactions cost more than the lookups it saves (+30% to +70%
+  // at 0.1% and 1%), since their k-th best row stays far from the answer
+  // until the scan ends.
+  plan->shared_bound = idx->opt_shared_bound == 2 || (idx->opt_shared_bound == 0 && plan->chunk_tiles > 0);
   plan->lds_bytes = scan_lds_bytes(idx->m, plan->qtile, lut_bytes, plan->pool_stride);
   return IFVS_OK;
 }
@@ -773,6 +780,10 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
     case IFVS_OPT_SLOT_ORDER:
       if (value > 1) return fail(IFVS_E_INVALID, "IFVS_OPT_SLOT_ORDER takes 0 or 1");
       idx->opt_slot_order = static_cast<int>(value);
+      return IFVS_OK;
+    case IFVS_OPT_SHARED_BOUND:
+      if (value > 2) return fail(IFVS_E_INVALID, "IFVS_OPT_SHARED_BOUND takes 0, 1 or 2");
+      idx->opt_shared_bound = static_cast<int>(value);
       return IFVS_OK;
     case IFVS_OPT_PROFILE:
       if (value != 0 && !idx->timers) {

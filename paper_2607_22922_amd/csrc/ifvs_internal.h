@@ -13,6 +13,7 @@ constexpr int kMaxClauses = 4;
 constexpr int kTileRows = 64;              // vectors per code tile = one wavefront
 constexpr int kLdsBudget = 160 * 1024;     // LDS bytes per workgroup on gfx950
 constexpr int kScanWaves = 8;              // wavefronts per scan workgroup
+constexpr int kScanPub = 2;                // best keys per (wavefront, query) published for the workgroup bound
 constexpr int kFilterQueries = 16;         // predicates evaluated per attribute read
 
 // A predicate as the device sees it.  The raw fields are the caller's clauses
@@ -115,6 +116,7 @@ struct ScanPlan {
   size_t lds_bytes;
   int64_t chunk_tiles;  // > 0: chunk grid cell in tiles (interval scans); 0: equal chunks
   bool abs_cells;       // chunk c is absolute grid cell c (splits = cells of the whole index)
+  bool shared_bound;    // wavefronts publish their best keys for a workgroup bound (k <= 16)
 };
 
 // Largest query tile whose tables and pools fit the LDS budget (0 if none).

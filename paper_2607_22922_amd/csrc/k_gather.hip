@@ -251,12 +251,16 @@ __global__ __launch_bounds__(kScanWaves * 64) void gather_scan_kernel(const Gath
     if (live) {
       const uint32_t db = ordered_bits(d);
       if (db <= static_cast<uint32_t>(bound >> 32)) {
-        const uint32_t id = a.perm ? static_cast<uint32_t>(a.perm[row]) : static_cast<uint32_t>(row);
-        key = (static_cast<uint64_t>(db) << 32) | id;
-        cand = key < bound;
+        if (a.perm) {
+          key = row_key(db, static_cast<uint32_t>(row));   // original id looked up when the pool is compacted
+          cand = true;
+        } else {
+          key = (static_cast<uint64_t>(db) << 32) | static_cast<uint32_t>(row);
+          cand = key < bound;
+        }
       }
     }
-    pool_push(pool, cnt_pool, thr, key, cand, k, a.kpl);
+    pool_push(pool, cnt_pool, thr, key, cand, k, a.kpl, a.perm);
     if (thr < published) {
       published = thr;
       if (lane == 0) {
@@ -283,7 +287,7 @@ __global__ __launch_bounds__(kScanWaves * 64) void gather_scan_kernel(const Gath
     load_rows(s0, wa, ra);
     score(wb, rb);
   }
-  pool_compact(pool, cnt_pool, thr, k, a.kpl);
+  pool_compact(pool, cnt_pool, thr, k, a.kpl, a.perm);
   for (int e = lane; e < k; e += 64) slot_out(c)[e] = pool[e];
 }
 

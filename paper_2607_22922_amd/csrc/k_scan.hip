@@ -26,8 +26,9 @@
 //    partial sums only grow; checked per query when its table is staged).
 //    Lanes beating the current k-th best key are appended to that query's
 //    pool (ballot + prefix count), which is sorted and cut back to k keys
-//    when it would overflow.  Keys carry original vector ids (read for candidates
-//    only), so ties break by original id on any layout.  At the end each
+//    when it would overflow.  Keys carry original vector ids (on a clustered
+//    layout looked up when a pool is compacted), so ties break by original id
+//    on any layout.  At the end each
 //    wavefront writes its k best keys per query; a merge kernel reduces them.
 #include <climits>
 
@@ -66,7 +67,23 @@ struct ScanArgs {
   // slot_order[(b % kXcds) * per_xcd * splits + b / kXcds] of its XCD, item
   // c * per_xcd + t meaning chunk c of the XCD's t-th query tile.
   const int32_t* slot_order;
+  int shared_bound;      // 1: wavefronts publish their best keys (union bound, k <= 16)
 };
+
+// Lower this wavefront's published best keys to the first kScanPub keys of
+// its freshly compacted pool, then return the k-th smallest published key of
+// the workgroup (all ones while fewer than k are published).  Not inlined:
+// it runs only when a wavefront's best keys improve.
+__device__ __noinline__ uint64_t publish_best(const uint64_t* pool, int cnt, unsigned long long* pub, int wave,
+                                              int k) {
+  const int lane = __lane_id();
+  if (lane < kScanPub && lane < cnt) atomicMin(&pub[wave * kScanPub + lane], static_cast<unsigned long long>(pool[lane]));
+  uint64_t v[1] = {lane < kScanWaves * kScanPub
+                       ? static_cast<uint64_t>(__hip_atomic_load(&pub[lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP))
+                       : kNoKey};
+  wave_bitonic_sort<1>(v);
+  return shfl_u64(v[0], k - 1);
+}
 
 // Bits [lo, hi) of a 64-bit word, 0 <= lo < hi <= 64.
 __device__ __forceinline__ uint64_t bit_range(int64_t lo, int64_t hi) {
@@ -74,11 +91,32 @@ __device__ __forceinline__ uint64_t bit_range(int64_t lo, int64_t hi) {
   return upto_hi & ~((1ull << lo) - 1);
 }
 
-// One-query tiles ask the compiler for six waves per SIMD (at most 80
-// VGPRs); the schedule it then picks measured about 3% faster on the dense
-// bins than its default.  Multi-query tiles keep the default.
+// Waves per SIMD that one-query workgroups can reach, set by their LDS
+// (tables + pools, two or more workgroups of eight waves per CU): the
+// register budget of a wave follows from it (512 / waves VGPRs), and the
+// code pipeline takes as many tiles in flight as that budget holds.  The
+// code stream is latency-bound otherwise: with one tile in flight per wave a
+// CU has 16 x 3 KB outstanding and waits about 1 us for each.
 template <int MT, int QT, typename LutT>
-__global__ __launch_bounds__(kScanWaves * 64) __attribute__((amdgpu_waves_per_eu(QT == 1 ? 6 : 1)))
+constexpr int scan_waves_per_eu() {
+  if constexpr (QT != 1) return 1;
+  else if constexpr (MT == 120 && sizeof(LutT) == 4) return 2;
+  else if constexpr ((MT == 48 && sizeof(LutT) == 4) || MT == 120) return 4;
+  else return 6;
+}
+
+// Register sets (tiles in flight + the one being summed) of the pipeline,
+// chosen so that the kernel fits the register budget above without spills.
+template <int MT, int QT, typename LutT>
+constexpr int scan_depth() {
+  if constexpr (QT != 1 || MT <= 0) return 2;
+  else if constexpr (MT <= 16) return 3;
+  else if constexpr (sizeof(LutT) == 4 && scan_waves_per_eu<MT, QT, LutT>() <= 4) return 4;
+  else return 2;
+}
+
+template <int MT, int QT, typename LutT>
+__global__ __launch_bounds__(kScanWaves * 64) __attribute__((amdgpu_waves_per_eu(scan_waves_per_eu<MT, QT, LutT>())))
 void scan_kernel(const ScanArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int kMW = MT > 0 ? (MT + 3) / 4 : 1;
@@ -102,6 +140,8 @@ void scan_kernel(const ScanArgs a) {
   unsigned long long* s_thr = reinterpret_cast<unsigned long long*>(
       pools + static_cast<size_t>(kScanWaves) * QT * a.pool_stride);   // smallest k-th key published in this workgroup
   uint32_t* s_bad = reinterpret_cast<uint32_t*>(s_thr + QT);   // [wave][qi]: the wave saw a negative or NaN entry
+  // [qi][wave][kScanPub]: each wavefront's best keys, only ever lowered
+  unsigned long long* s_pub = reinterpret_cast<unsigned long long*>(s_bad + kScanWaves * QT);
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -239,9 +279,10 @@ void scan_kernel(const ScanArgs a) {
     return any;
   };
 
-  // Software pipeline over two register sets (fixed M): while the tile in
-  // one set is summed, the next selected tile's code words load into the
-  // other (no register copy, so nothing waits for the loads in flight).
+  // Software pipeline over kDepth register sets (fixed M): while the tile in
+  // one set is summed, the next kDepth - 1 selected tiles' code words are in
+  // flight into the others (no register copy, so nothing waits for the loads
+  // in flight).
   auto next_selected = [&](int t, uint64_t (&bm)[QT]) -> int {
     while (t < te && tile_masks(t, bm) == 0) t += kScanWaves;
     return t;
@@ -253,12 +294,18 @@ void scan_kernel(const ScanArgs a) {
 #pragma unroll
     for (int j = 0; j < kMW; ++j) w[j] = tile[j * 64 + lane];
   };
-  uint64_t bma[QT], bmb[QT];
-  uint32_t wa[kMW], wb[kMW];
-  int ta = 0;
+  constexpr int kDepth = scan_depth<MT, QT, LutT>();
+  uint64_t bms[kDepth][QT];
+  uint32_t ws[kDepth][kMW];
+  int ts[kDepth];
+  int t_next = tb + wave;
   if constexpr (MT > 0) {
-    ta = next_selected(tb + wave, bma);
-    load_tile(ta, wa);
+#pragma unroll
+    for (int i = 0; i < kDepth - 1; ++i) {
+      ts[i] = next_selected(t_next, bms[i]);
+      load_tile(ts[i], ws[i]);
+      t_next = ts[i] + kScanWaves;
+    }
   }
 
   // Tables into LDS as [m][qi][c], noting any entry that is negative or NaN
@@ -304,6 +351,7 @@ void scan_kernel(const ScanArgs a) {
     if (lane == 0) s_bad[wave * QT + qi] = wave_bad ? 1u : 0u;
   }
   if (threadIdx.x < QT) s_thr[threadIdx.x] = kNoKey;
+  if (threadIdx.x < QT * kScanWaves * kScanPub) s_pub[threadIdx.x] = kNoKey;
   __syncthreads();
   // Early abandonment: every entry >= 0 and fp32 addition of non-negative
   // terms never decreases, so a partial sum above the current k-th distance
@@ -340,6 +388,20 @@ void scan_kernel(const ScanArgs a) {
   uint64_t published[QT], gview[QT], gnext[QT], bound[QT];
 #pragma unroll
   for (int qi = 0; qi < QT; ++qi) published[qi] = gview[qi] = gnext[qi] = bound[qi] = kNoKey;
+  // Union bound.  A wavefront's own k-th key reflects only the rows it
+  // scanned, and the workgroup's smallest such key is about the
+  // (waves * k)-th best row the workgroup has seen -- too loose to stop the
+  // summation early on short intervals.  So whenever a candidate could
+  // improve a wavefront's kScanPub best keys, the wavefront compacts its pool
+  // and lowers its entries of s_pub (atomic minimum).  Each entry stays at
+  // least that wavefront's true j-th best key, and wavefronts scan disjoint
+  // rows, so at least k distinct rows have keys at or below the k-th
+  // smallest entry: it bounds the query's answer and is published like a
+  // threshold.
+  const bool union_bound = a.shared_bound && k <= kScanWaves * kScanPub;
+  uint64_t my_pub[QT];   // this wavefront's kScanPub-th best key as last published
+#pragma unroll
+  for (int qi = 0; qi < QT; ++qi) my_pub[qi] = kNoKey;
   auto global_issue = [&]() {
 #pragma unroll
     for (int qi = 0; qi < QT; ++qi)
@@ -366,12 +428,30 @@ void scan_kernel(const ScanArgs a) {
       const uint32_t db = ordered_bits(d);
       if (db <= static_cast<uint32_t>(bound[qi] >> 32)) {
         const uint32_t row = static_cast<uint32_t>(t * 64 + lane);
-        const uint32_t id = a.perm ? static_cast<uint32_t>(a.perm[row]) : row;
-        key = (static_cast<uint64_t>(db) << 32) | id;
-        cand = key < bound[qi];
+        if (a.perm) {
+          key = row_key(db, row);   // original id looked up when the pool is compacted
+          cand = true;
+        } else {
+          key = (static_cast<uint64_t>(db) << 32) | row;
+          cand = key < bound[qi];
+        }
       }
     }
-    pool_push(my_pools + qi * a.pool_stride, cnt[qi], thr[qi], key, cand, k, a.kpl);
+    const bool improve = union_bound && __ballot(cand && (key >> 32) < (my_pub[qi] >> 32)) != 0;
+    uint64_t* pool = my_pools + qi * a.pool_stride;
+    pool_push(pool, cnt[qi], thr[qi], key, cand, k, a.kpl, a.perm);
+    if (improve) {
+      pool_compact(pool, cnt[qi], thr[qi], k, a.kpl, a.perm);
+      my_pub[qi] = cnt[qi] >= kScanPub ? pool[kScanPub - 1] : kNoKey;
+      const uint64_t ub = publish_best(pool, cnt[qi], s_pub + qi * kScanWaves * kScanPub, wave, k);
+      if (ub < published[qi]) {
+        published[qi] = ub;
+        if (lane == 0) {
+          atomicMin(&s_thr[qi], static_cast<unsigned long long>(ub));
+          __hip_atomic_fetch_min(a.gthr + qid[qi], ub, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+    }
     if (thr[qi] < published[qi]) {
       published[qi] = thr[qi];
       if (lane == 0) {
@@ -428,17 +508,25 @@ void scan_kernel(const ScanArgs a) {
         // Usually every lane has dropped out: nothing to offer.
         if (__ballot(live[qi]) != 0) consider(qi, live[qi], d[qi], t);
     };
-    while (ta < te) {
-      const int tn = next_selected(ta + kScanWaves, bmb);
+    // Step i sums set i and refills the set summed in the step before with
+    // the tile kDepth - 1 places ahead; tiles are visited in increasing
+    // order, so the first one past the chunk ends the loop.
+    for (;;) {
       global_finish();
       global_issue();
-      load_tile(tn, wb);
-      sum_tile(ta, bma, wa);
-      if (tn >= te) break;
-      ta = next_selected(tn + kScanWaves, bma);
-      load_tile(ta, wa);
-      sum_tile(tn, bmb, wb);
+#pragma unroll
+      for (int i = 0; i < kDepth; ++i) {
+        constexpr int unused = 0;
+        (void)unused;
+        const int j = (i + kDepth - 1) % kDepth;
+        ts[j] = next_selected(t_next, bms[j]);
+        load_tile(ts[j], ws[j]);
+        t_next = ts[j] + kScanWaves;
+        if (ts[i] >= te) goto scanned;
+        sum_tile(ts[i], bms[i], ws[i]);
+      }
     }
+  scanned:;
   } else {
     for (int t = tb + wave; t < te; t += kScanWaves) {
       uint64_t bm[QT];
@@ -468,7 +556,7 @@ void scan_kernel(const ScanArgs a) {
   for (int qi = 0; qi < QT; ++qi) {
     if (qi >= qn) break;
     uint64_t* pool = my_pools + qi * a.pool_stride;
-    pool_compact(pool, cnt[qi], thr[qi], k, a.kpl);
+    pool_compact(pool, cnt[qi], thr[qi], k, a.kpl, a.perm);
     uint64_t* dst = a.partials + ((static_cast<size_t>(q0 + qi) * a.splits + chunk) * kScanWaves + wave) * k;
     for (int e = lane; e < k; e += 64) dst[e] = pool[e];
   }
@@ -485,7 +573,8 @@ constexpr int kQtiles[] = {1, 2, 3, 4, 6, 8};
 template <int MT, int QT, typename LutT>
 constexpr bool scan_fits() {
   return static_cast<size_t>(MT) * QT * kKsub * sizeof(LutT) +
-             static_cast<size_t>(QT) * (kScanWaves * 65 * sizeof(uint64_t) + 8 + 4 * kScanWaves) <=
+             static_cast<size_t>(QT) * (kScanWaves * 65 * sizeof(uint64_t) + 8 + 4 * kScanWaves +
+                                        kScanWaves * kScanPub * sizeof(uint64_t)) <=
          static_cast<size_t>(kLdsBudget);
 }
 
@@ -534,11 +623,12 @@ int pool_stride_for(int k) {
 }
 
 size_t scan_lds_bytes(int m, int qtile, int lut_bytes, int pool_stride) {
-  // tables, pools, workgroup thresholds (8 B) and per-wave monotonicity
-  // flags (4 B each)
+  // tables, pools, workgroup thresholds (8 B), per-wave monotonicity flags
+  // (4 B each) and published best keys
   return static_cast<size_t>(qtile) *
          (static_cast<size_t>(m) * kKsub * lut_bytes +
-          static_cast<size_t>(kScanWaves) * pool_stride * sizeof(uint64_t) + 8 + 4 * kScanWaves);
+          static_cast<size_t>(kScanWaves) * pool_stride * sizeof(uint64_t) + 8 + 4 * kScanWaves +
+          static_cast<size_t>(kScanWaves) * kScanPub * sizeof(uint64_t));
 }
 
 int scan_max_qtile(int m, int lut_bytes, int k) {
@@ -585,6 +675,7 @@ hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s) 
   a.abs_cells = plan.abs_cells ? 1 : 0;
   a.mode = b.mode;
   a.slot_order = b.slot_order;
+  a.shared_bound = plan.shared_bound ? 1 : 0;
   a.partials = b.partials;
   a.gthr = b.gthr;
   a.splits = plan.splits;

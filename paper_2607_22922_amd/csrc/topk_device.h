@@ -13,6 +13,15 @@
 // and a prefix count; when an append would overflow, the pool is sorted with
 // a register bitonic sort across the wavefront and cut back to its k
 // smallest keys, which also tightens the threshold.
+//
+// On a clustered index rows are stored in a permuted order and a key must
+// carry the original id (ties break by it).  Looking the id up when a row
+// becomes a candidate would put a dependent global load on the scan's path,
+// so candidates enter the pool as row keys -- the physical row with
+// kRowFlag set in the id field -- and the ids are looked up in `perm` when
+// the pool is compacted, once for all of them.  A row key only knows its
+// distance, so it is offered whenever its distance does not exceed the
+// threshold's; compaction then decides ties by the real id.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -34,6 +43,27 @@ __device__ __forceinline__ float from_ordered_bits(uint32_t t) {
 
 __device__ __forceinline__ uint64_t make_key(float d, uint32_t id) {
   return (static_cast<uint64_t>(ordered_bits(d)) << 32) | id;
+}
+
+// Id field of a row key: a physical row (< 2^31) still to be mapped to its
+// original id through perm.
+constexpr uint32_t kRowFlag = 0x80000000u;
+
+__device__ __forceinline__ uint64_t row_key(uint32_t dist_bits, uint32_t row) {
+  return (static_cast<uint64_t>(dist_bits) << 32) | kRowFlag | row;
+}
+
+// The key with its id field resolved (keys that are not row keys unchanged).
+__device__ __forceinline__ uint64_t resolve_key(uint64_t key, const int32_t* __restrict__ perm) {
+  if (key == ~0ull || !(static_cast<uint32_t>(key) & kRowFlag)) return key;
+  const uint32_t row = static_cast<uint32_t>(key) & ~kRowFlag;
+  return (key & 0xFFFFFFFF00000000ull) | static_cast<uint32_t>(perm[row]);
+}
+
+// May `key` still belong below `thr`?  Exact for resolved keys; a row key
+// is compared by distance only.
+__device__ __forceinline__ bool may_beat(uint64_t key, uint64_t thr, bool row_keys) {
+  return row_keys ? (key >> 32) <= (thr >> 32) : key < thr;
 }
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
@@ -99,13 +129,18 @@ __device__ __forceinline__ void wave_bitonic_sort(uint64_t (&v)[KPL]) {
 // (padded with kNoKey), and set the threshold once k keys exist.  Pools of
 // up to 256 keys are sorted in registers (KPL keys per lane).
 template <int KPL>
-__device__ __forceinline__ uint64_t pool_compact_regs(uint64_t* pool, int cnt, uint64_t thr, int k) {
+__device__ __forceinline__ uint64_t pool_compact_regs(uint64_t* pool, int cnt, uint64_t thr, int k,
+                                                      const int32_t* perm) {
   const int lane = lane_id();
   uint64_t v[KPL];
 #pragma unroll
   for (int s = 0; s < KPL; ++s) {
     const int e = lane * KPL + s;
     v[s] = e < cnt ? pool[e] : kNoKey;
+  }
+  if (perm) {
+#pragma unroll
+    for (int s = 0; s < KPL; ++s) v[s] = resolve_key(v[s], perm);
   }
   wave_bitonic_sort<KPL>(v);
 #pragma unroll
@@ -132,9 +167,12 @@ __device__ __forceinline__ void wave_lds_fence() {
   __builtin_amdgcn_wave_barrier();
 }
 
-__device__ __forceinline__ uint64_t pool_compact_lds(uint64_t* pool, int cnt, uint64_t thr, int k, int kpl) {
+__device__ __forceinline__ uint64_t pool_compact_lds(uint64_t* pool, int cnt, uint64_t thr, int k, int kpl,
+                                                     const int32_t* perm) {
   const int lane = lane_id();
   const int n = 64 * kpl;
+  if (perm)
+    for (int e = lane; e < cnt; e += 64) pool[e] = resolve_key(pool[e], perm);
   for (int e = cnt + lane; e < n; e += 64) pool[e] = kNoKey;
   wave_lds_fence();
   for (int size = 2; size <= n; size <<= 1) {
@@ -161,28 +199,33 @@ __device__ __forceinline__ uint64_t pool_compact_lds(uint64_t* pool, int cnt, ui
 // Sort the pool, keep its k smallest keys first; returns the new threshold
 // (the pool then holds min(cnt, k) keys).  Not inlined: compaction is rare,
 // and one copy per kernel keeps the code small.
-__device__ __noinline__ uint64_t pool_compact_call(uint64_t* pool, int cnt, uint64_t thr, int k, int kpl) {
-  if (kpl == 2) return pool_compact_regs<2>(pool, cnt, thr, k);
-  if (kpl == 4) return pool_compact_regs<4>(pool, cnt, thr, k);
-  return pool_compact_lds(pool, cnt, thr, k, kpl);
+// Row keys (perm non-null) are resolved first.
+__device__ __noinline__ uint64_t pool_compact_call(uint64_t* pool, int cnt, uint64_t thr, int k, int kpl,
+                                                   const int32_t* perm) {
+  if (kpl == 2) return pool_compact_regs<2>(pool, cnt, thr, k, perm);
+  if (kpl == 4) return pool_compact_regs<4>(pool, cnt, thr, k, perm);
+  return pool_compact_lds(pool, cnt, thr, k, kpl, perm);
 }
 
-__device__ __forceinline__ void pool_compact(uint64_t* pool, int& cnt, uint64_t& thr, int k, int kpl) {
-  thr = pool_compact_call(pool, cnt, thr, k, kpl);
+__device__ __forceinline__ void pool_compact(uint64_t* pool, int& cnt, uint64_t& thr, int k, int kpl,
+                                             const int32_t* perm = nullptr) {
+  thr = pool_compact_call(pool, cnt, thr, k, kpl, perm);
   cnt = cnt < k ? cnt : k;
 }
 
 // Offer one key per lane (`cand` false = nothing to offer).  Must be called
 // by every lane of the wavefront with the same pool, cnt and thr.  The pool
-// holds 64*kpl >= k + 64 keys (a power of two).
+// holds 64*kpl >= k + 64 keys (a power of two).  perm non-null: the keys
+// offered are row keys.
 __device__ __forceinline__ void pool_push(uint64_t* pool, int& cnt, uint64_t& thr,
-                                          uint64_t key, bool cand, int k, int kpl) {
+                                          uint64_t key, bool cand, int k, int kpl,
+                                          const int32_t* perm = nullptr) {
   uint64_t mask = __ballot(cand);
   if (mask == 0) return;
   int n = __popcll(mask);
   if (cnt + n > k + 64) {
-    pool_compact(pool, cnt, thr, k, kpl);
-    cand = cand && key < thr;
+    pool_compact(pool, cnt, thr, k, kpl, perm);
+    cand = cand && may_beat(key, thr, perm != nullptr);
     mask = __ballot(cand);
     if (mask == 0) return;
     n = __popcll(mask);

@@ -25,6 +25,7 @@ MAX_CLAUSES = 4
 MAX_K = 1024
 OPT_QTILE, OPT_SPLITS, OPT_PROFILE, OPT_MIN_CHUNK, OPT_GRID_TILES, OPT_GATHER, OPT_GRID_RELATIVE = 1, 2, 3, 4, 5, 6, 7
 OPT_SLOT_ORDER = 8
+OPT_SHARED_BOUND = 9
 STAGES = ("condition", "lut", "filter", "scan", "merge")
 
 EXPORTED = ("ifvs_load_index", "ifvs_free_index", "ifvs_select_codebook", "ifvs_build_lut",

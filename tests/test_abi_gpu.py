@@ -92,11 +92,12 @@ def test_other_calls_validate(B, small):
     st, _ = _status(B, lib.ifvs_set_option, idx.handle, B.OPT_QTILE, -1)
     assert st == B.E_INVALID
     for opt, bad in ((B.OPT_PROFILE, 3), (B.OPT_GATHER, 3), (B.OPT_GRID_TILES, -5), (B.OPT_SLOT_ORDER, 2),
-                     (B.OPT_GRID_RELATIVE, 2)):
+                     (B.OPT_GRID_RELATIVE, 2), (B.OPT_SHARED_BOUND, 3)):
         st, msg = _status(B, lib.ifvs_set_option, idx.handle, opt, bad)
         assert st == B.E_INVALID, (opt, bad, msg)
     for opt, good in ((B.OPT_GATHER, 2), (B.OPT_GATHER, 0), (B.OPT_GRID_TILES, 0), (B.OPT_SLOT_ORDER, 1),
-                      (B.OPT_SLOT_ORDER, 0)):
+                      (B.OPT_SLOT_ORDER, 0), (B.OPT_SHARED_BOUND, 1), (B.OPT_SHARED_BOUND, 2),
+                      (B.OPT_SHARED_BOUND, 0)):
         assert lib.ifvs_set_option(idx.handle, opt, good) == B.OK
     for fn, args in ((lib.ifvs_filtered_search, (None, 1, None, None, 0, 1, None, None, None, None)),
                      (lib.ifvs_build_lut, (None, 1, None, None, None, 0, None, None))):

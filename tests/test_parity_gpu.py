@@ -180,6 +180,34 @@ def test_identity_index_and_fp16_tables(B):
     _run_and_check(B, idx, ox, preds, k=10, dsub=2, M=48, conditioned=False, lut_dtype="f16")
 
 
+@pytest.mark.parametrize("cluster_cols", [(), (0,)])
+def test_ties_at_the_kth_distance_across_workgroups(B, cluster_cols):
+    """Many rows share the k-th distance and sit in different wavefronts and
+    workgroups (forced small chunks); the answer keeps the smallest ids."""
+    ix = random_index(30_000, 48, 2, 1, 30, 43, device="cuda")
+    ix["codes"][5::37] = ix["codes"][2]               # 811 copies of row 2
+    ix["codes"][11::53] = ix["codes"][9]              # 566 copies of row 9
+    idx = B.Index(ix["codes"], ix["C_pq"], ix["attrs"], max_batch=8, max_k=16, cluster_cols=cluster_cols)
+    idx.set_option(B.OPT_SPLITS, 7)
+    ox = oracle_index(ix["codes"], ix["C_pq"], ix["attrs"])
+    C = ix["C_pq"]
+    r2 = C[torch.arange(48, device="cuda"), ix["codes"][2].long()].reshape(-1)
+    r9 = C[torch.arange(48, device="cuda"), ix["codes"][9].long()].reshape(-1)
+    q = torch.stack([r2, r9, 0.5 * (r2 + r9), r2 + 0.01]).contiguous()
+    preds = [[(0, 0, 30)], [(0, 3, 25)], [(0, 0, 30)], [(0, 10, 12)]]
+    lut = idx.build_lut(q)
+    for shared in (0, 1, 2):
+        idx.set_option(B.OPT_SHARED_BOUND, shared)
+        for k in (1, 10, 16):
+            ids, dist = idx.search(preds, lut, k)
+            torch.cuda.synchronize()
+            for i, p in enumerate(preds):
+                res = O.filtered_search(ox, _np(q[i]), p, k, conditioned=False)
+                check_search_row(_np(ids[i]), _np(dist[i]), res["ids"], res["dist"], f"ties k={k} q{i} s{shared}")
+    idx.set_option(B.OPT_SPLITS, 0)
+    idx.set_option(B.OPT_SHARED_BOUND, 0)
+
+
 def test_ties_broken_by_smaller_id(B):
     ix = random_index(4000, 16, 8, 1, 10, 11, device="cuda")
     ix["codes"][1000:1200] = ix["codes"][17]          # 201 identical rows
@@ -329,6 +357,19 @@ def test_clustered_chunk_grid_and_fallback(B, cols):
     idx.set_option(B.OPT_SPLITS, 0)
     idx.set_option(B.OPT_GRID_RELATIVE, 0)
     idx.set_option(B.OPT_SLOT_ORDER, 0)
+    # k = 10: grid scans turn on the workgroup bound (published best keys)
+    ids10, dist10 = idx.search(preds, lut, 10)
+    torch.cuda.synchronize()
+    assert torch.equal(ids10, ids0[:, :10]) and torch.equal(dist10.view(torch.int32), dist0[:, :10].view(torch.int32))
+    for grid, shared in ((64, 0), (1, 0), (13, 1), (0, 2)):
+        idx.set_option(B.OPT_GRID_TILES, grid)
+        idx.set_option(B.OPT_SHARED_BOUND, shared)
+        ids, dist = idx.search(preds, lut, 10)
+        torch.cuda.synchronize()
+        assert torch.equal(ids, ids10), (grid, shared)
+        assert torch.equal(dist.view(torch.int32), dist10.view(torch.int32)), (grid, shared)
+    idx.set_option(B.OPT_GRID_TILES, 0)
+    idx.set_option(B.OPT_SHARED_BOUND, 0)
 
 
 @pytest.mark.parametrize("cluster_cols,M,dsub,k,lut_dtype", [((), 16, 8, 10, "f32"), ((), 48, 2, 100, "f32"),
@@ -382,7 +423,11 @@ def test_gather_compaction_sparse_and_dense_workgroups(B):
     assert np.array_equal(ids, ids2)
 
 
-def test_clustered_ties_break_by_original_id(B):
+@pytest.mark.parametrize("k", [200, 16, 10])
+def test_clustered_ties_break_by_original_id(B, k):
+    """Equal rows everywhere: the k-th distance is shared by many rows of
+    every wavefront, so the workgroup bound (k <= 16) and the deferred id
+    lookup must still keep the smaller original ids."""
     ix = random_index(6000, 16, 8, 1, 40, 41, device="cuda")
     ix["codes"][::7] = ix["codes"][3]                 # equal rows in every cluster
     idx = B.Index(ix["codes"], ix["C_pq"], ix["attrs"], max_batch=8, max_k=200, cluster_cols=(0,))
@@ -391,10 +436,10 @@ def test_clustered_ties_break_by_original_id(B):
     q = rec[None].repeat(3, 1).contiguous()
     preds = [[], [(0, 10, 30)], [(0, 5, 6)]]
     lut = idx.build_lut(q)
-    ids, dist = idx.search(preds, lut, 200)
+    ids, dist = idx.search(preds, lut, k)
     torch.cuda.synchronize()
     for i, p in enumerate(preds):
-        res = O.filtered_search(ox, _np(q[i]), p, 200, conditioned=False)
+        res = O.filtered_search(ox, _np(q[i]), p, k, conditioned=False)
         check_search_row(_np(ids[i]), _np(dist[i]), res["ids"], res["dist"], f"ties q{i}")
 
 
