@@ -19,6 +19,9 @@ Aref; VLDB 2026 workshop) and cites the passage it follows:
 * Section 2, stage 3 (Select): the top-k candidates by score are returned.
 * Section 2, training paragraph: alpha = 0 and w_f = 1 reduce C_iFVS to C_PQ.
 * Section 1, SQL listing: WHERE conjunction ... ORDER BY distance ... LIMIT K.
+* Section 3.1 (workloads): the ground truth is the exact filtered top-k over
+  the predicate-passing vectors; Section 3.2, pre-filtering baseline (i):
+  exact L2 distances over the full-precision vectors of the candidate set.
 
 Readings taken where the paper is silent (all listed in the design notes):
 
@@ -72,6 +75,8 @@ __all__ = [
     "adc_distances",
     "select_topk",
     "filtered_search",
+    "exact_distances",
+    "exact_filtered_search",
 ]
 
 KSUB = 256                      # codewords per subspace: 8-bit PQ codes
@@ -300,3 +305,31 @@ def filtered_search(index: dict, q, clauses, k, w_z=None, lut_dtype="f32",
     top_ids, top_d = select_topk(d, ids, k)
     return {"alpha": alpha, "w_f": w_f, "lut": lut, "mask": mask, "ids": top_ids,
             "dist": top_d, "n_pass": int(ids.shape[0])}
+
+
+# --------------------------------------------------------------------------
+# Exact filtered kNN over the full-precision vectors (Section 3.1 ground
+# truth; Section 3.2, pre-filtering baseline (i))
+# --------------------------------------------------------------------------
+def exact_distances(x, q, ids, dtype=np.float32):
+    """Squared L2 distance from q to each candidate's full-precision vector:
+    d(v) = sum_{j<D} (x[v][j] - q[j])^2, summed in j order from +0 in
+    ``dtype``, the difference, its square and each addition rounded
+    separately."""
+    x = np.asarray(x)
+    q = np.asarray(q).astype(dtype)
+    ids = np.asarray(ids, dtype=np.int64)
+    d = np.zeros(ids.shape[0], dtype=dtype)
+    for j in range(x.shape[1]):
+        e = x[ids, j].astype(dtype) - q[j]
+        d = d + e * e
+    return d
+
+
+def exact_filtered_search(x, attrs, q, clauses, k, dtype=np.float32):
+    """Exact filtered kNN: the predicate-passing rows ranked by
+    exact_distances, ascending (distance, id), padded to k with (-1, +inf)."""
+    ids = passing_ids(predicate_mask(attrs, clauses))
+    d = exact_distances(x, q, ids, dtype)
+    top_ids, top_d = select_topk(d, ids, k)
+    return {"ids": top_ids, "dist": top_d, "n_pass": int(ids.shape[0])}

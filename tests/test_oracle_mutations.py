@@ -25,6 +25,9 @@ MUTATIONS = [
     ("fnv_wrong_order", "h ^= byte\n        h = (h * _FNV_PRIME) & _MASK64", "h = (h * _FNV_PRIME) & _MASK64\n        h ^= byte"),
     ("alpha_single_row", "for r_i in rows:", "for r_i in rows[:1]:"),
     ("fingerprint_no_clauses", "out.append(struct.pack(\"<iqq\", int(col), int(lo), int(hi)))", "pass"),
+    ("exact_abs_not_square", "        d = d + e * e\n", "        d = d + np.abs(e)\n"),
+    ("exact_drops_last_dim", "    for j in range(x.shape[1]):\n        e = x[ids, j]", "    for j in range(x.shape[1] - 1):\n        e = x[ids, j]"),
+    ("exact_query_index_shift", "        e = x[ids, j].astype(dtype) - q[j]", "        e = x[ids, j].astype(dtype) - q[(j + 1) % q.shape[0]]"),
 ]
 
 

@@ -321,3 +321,77 @@ def test_fp16_lut_is_nearest_binary16_and_widened_in_adc():
     assert d.dtype == np.float32
     ref = sum(l16[m][codes[:, m]].astype(np.float64) for m in range(ix["M"]))
     np.testing.assert_allclose(d, ref, rtol=ix["M"] * U32)
+
+
+# ------------------------------------------------------- exact filtered kNN
+def test_exact_distances_within_fp32_bound_of_library_fp64():
+    """fp32 sequential squared L2 against scipy's fp64 cdist: the forward
+    error of 2D + 1 roundings of non-negative terms and differences."""
+    rng = np.random.default_rng(31)
+    for D in (3, 96, 128, 960):
+        x = (rng.standard_normal((300, D)) + 0.5).astype(np.float32)
+        q = rng.standard_normal(D).astype(np.float32)
+        ids = rng.permutation(300)[:120]
+        d32 = O.exact_distances(x, q, ids)
+        d64 = cdist(q[None].astype(np.float64), x[ids].astype(np.float64), "sqeuclidean")[0]
+        assert d32.dtype == np.float32
+        assert np.all(np.abs(d32 - d64) <= (2 * D + 2) * U32 * d64)
+        # fp64 mode is the definition to rounding of fp64
+        d_hi = O.exact_distances(x, q, ids, dtype=np.float64)
+        assert np.allclose(d_hi, d64, rtol=1e-12, atol=0)
+
+
+def test_exact_distance_written_out_for_one_vector():
+    """Two dimensions by hand: (1.5 - 0.25)^2 + (-2 - 1)^2 = 1.5625 + 9."""
+    x = np.array([[1.5, -2.0]], dtype=np.float32)
+    q = np.array([0.25, 1.0], dtype=np.float32)
+    assert O.exact_distances(x, q, [0])[0] == np.float32(10.5625)
+
+
+def test_exact_filtered_search_is_brute_force_knn():
+    rng = np.random.default_rng(32)
+    N, D = 500, 24
+    x = rng.standard_normal((N, D)).astype(np.float32)
+    attrs = rng.integers(0, 30, (2, N), dtype=np.int32)
+    for t in range(15):
+        q = rng.standard_normal(D).astype(np.float32)
+        lo = int(rng.integers(0, 25))
+        clauses = [(0, lo, lo + 6), (1, 0, 20)] if t % 3 else [(1, lo, lo + 1)]
+        res = O.exact_filtered_search(x, attrs, q, clauses, 12)
+        keep = np.flatnonzero(np.all([(attrs[c] >= a) & (attrs[c] < b) for c, a, b in clauses], axis=0))
+        dd = cdist(q[None].astype(np.float64), x[keep].astype(np.float64), "sqeuclidean")[0]
+        exact = keep[np.argsort(dd, kind="stable")[:12]]
+        n = min(12, keep.size)
+        assert res["n_pass"] == keep.size
+        assert list(res["ids"][:n]) == list(exact[:n])
+        assert np.all(res["ids"][n:] == -1) and np.all(np.isinf(res["dist"][n:]))
+
+
+def test_exact_search_agrees_with_lossless_pq_adc_ranking():
+    """With every vector its own codeword, identity-mode ADC and the exact
+    search rank the same rows (both are the squared L2 distance, summed in
+    different orders)."""
+    rng = np.random.default_rng(33)
+    N, M, dsub = 220, 6, 4
+    x = rng.standard_normal((N, M * dsub)).astype(np.float32)
+    C_pq = np.zeros((M, 256, dsub), dtype=np.float32)
+    for m in range(M):
+        C_pq[m, :N] = x[:, m * dsub:(m + 1) * dsub]
+    codes = np.tile(np.arange(N, dtype=np.uint8)[:, None], (1, M))
+    attrs = rng.integers(0, 10, (1, N), dtype=np.int32)
+    index = dict(codes=codes, C_pq=C_pq, attrs=attrs)
+    for t in range(10):
+        q = rng.standard_normal(M * dsub).astype(np.float32)
+        clauses = [(0, t % 5, t % 5 + 4)]
+        a = O.filtered_search(index, q, clauses, 8, conditioned=False)
+        b = O.exact_filtered_search(x, attrs, q, clauses, 8)
+        assert list(a["ids"]) == list(b["ids"])
+        assert np.allclose(a["dist"], b["dist"], rtol=1e-5)
+
+
+def test_exact_search_ties_go_to_the_smaller_id():
+    x = np.zeros((6, 4), dtype=np.float32)
+    x[[1, 4, 5]] = 1.0
+    attrs = np.zeros((1, 6), dtype=np.int32)
+    res = O.exact_filtered_search(x, attrs, np.ones(4, dtype=np.float32), [], 4)
+    assert list(res["ids"]) == [1, 4, 5, 0]
