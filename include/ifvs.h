@@ -196,6 +196,44 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
                                  int32_t* ids_out, float* dist_out, uint32_t* bitmap_out,
                                  void* stream);
 
+/* ifvs_load_vectors -- attach the full-precision base vectors, for exact
+ * filtered kNN (ifvs_exact_search).  The paper takes the exact top-k over
+ * the predicate-passing vectors as its ground truth (Section 3.1), and its
+ * pre-filtering baseline (i) computes exact L2 distances over the
+ * full-precision vectors of the candidate set (Section 3.2).
+ *  x:        [n][dim] fp32, row i = vector id i, in the memory named by
+ *            mem_kind; deep-copied (stored in the index's row order as fp32
+ *            and as bf16 matrix-core fragments, with each row's squared
+ *            norm), so the caller may free it after return.  Costs
+ *            n * dim * 6 bytes of device memory plus a workspace sized by
+ *            max_batch and max_k (a few hundred MB at most).
+ * Errors: IFVS_E_INVALID (NULL x, unknown mem_kind, a NaN or infinite
+ * value: nothing is kept), IFVS_E_STATE (NULL handle, or vectors already
+ * attached), IFVS_E_NOMEM, IFVS_E_HIP. */
+ifvs_status ifvs_load_vectors(ifvs_index* idx, const float* x, int32_t mem_kind);
+
+/* ifvs_exact_search -- exact filtered kNN (Section 3.1 ground truth; Section
+ * 3.2 pre-filtering baseline (i)).  For each query q: the pool P_q of
+ * vectors whose attributes satisfy preds[q] (as in ifvs_filter), ranked by
+ *   d(v) = sum_{j<dim} (x_v[j] - q[j])^2
+ * summed in j order from +0 in fp32, the difference, its square and each
+ * addition rounded separately (no fused multiply-add); the k smallest
+ * (d, id) pairs ascending, ties to the smaller id.  Results equal that
+ * definition exactly: where many queries share rows, a bf16 matrix-core pass
+ * with a rigorous error bound only decides which rows need scoring, and
+ * every returned distance is computed as defined.
+ *  q:        device [nq][dim] fp32
+ *  preds:    HOST [nq]
+ *  k:        1..max_k
+ *  ids_out:  device [nq][k] int32; rows with |P_q| < k end in id -1
+ *  dist_out: device [nq][k] fp32; +inf where the id is -1
+ * Errors: IFVS_E_INVALID (nq, k, NULL q / ids_out / dist_out, predicate
+ * errors as in ifvs_filter), IFVS_E_STATE (NULL handle, no vectors
+ * attached), IFVS_E_HIP.  Non-finite query values give unspecified
+ * rankings. */
+ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const ifvs_predicate* preds,
+                              int32_t k, int32_t* ids_out, float* dist_out, void* stream);
+
 /* Tuning knobs, never needed for correctness.  IFVS_OPT_QTILE forces the
  * number of queries whose tables share one LDS residency and one pass over
  * the codes (0 = automatic); IFVS_OPT_SPLITS forces the number of code chunks
@@ -226,6 +264,9 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
                                      best keys and prune with the k-th smallest published key:
                                      0 automatic (on for chunk-grid scans of long intervals),
                                      1 never, 2 always                                         */
+#define IFVS_OPT_EXACT_PLAN 10    /* ifvs_exact_search: 0 automatic (matrix-core screening when
+                                     the batch's queries share rows), 1 score every selected row
+                                     exactly, 2 always screen first                           */
 ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value);
 
 /* ifvs_read_profile -- with IFVS_OPT_PROFILE on, every kernel the index

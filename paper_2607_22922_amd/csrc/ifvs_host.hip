@@ -123,6 +123,25 @@ struct ifvs_index {
   int32_t* qmode = nullptr;      // [max_batch] 1: gather scan
   int64_t list_cap = 0;
 
+  // Full-precision vectors (ifvs_load_vectors) and the exact search's
+  // workspace.
+  float* xt = nullptr;           // [ceil(n/64)][dim][64] fp32, physical order
+  uint4* xb = nullptr;           // [ceil(n/32)][ksteps][64] bf16 fragments
+  float* xn = nullptr;           // [ceil(n/32)*32] squared norms
+  unsigned* xmax = nullptr;      // largest row norm (fp32 bits)
+  unsigned long long* xbad = nullptr;
+  uint4* qb = nullptr;           // query fragments
+  float* qn_x = nullptr;         // [max_batch] |q|^2
+  float* eps_x = nullptr;        // [max_batch] screening error bounds
+  float* thr_x = nullptr;        // [max_batch] candidate bounds
+  float* bins_x = nullptr;       // [max_batch][exact_bins_per_query(exact_splits_max)]
+  int exact_splits_max = 0;
+  int32_t* cand_x = nullptr;     // [max_batch][cand_cap]
+  int32_t* cand_n_x = nullptr;   // [max_batch]
+  int64_t cand_cap = 0;
+  uint64_t* partials_x = nullptr;  // [max_batch][exact_chunks_max][max_k]
+  int exact_chunks_max = 0;
+
   // Every (n / kFences)-th clustered key, copied to the host at load: lets
   // the planner estimate each query's interval length without touching the
   // device.
@@ -133,11 +152,30 @@ struct ifvs_index {
   int opt_gather = 0;   // 0 automatic, 1 every query whose list fits, 2 never
   int opt_grid_relative = 0;   // 1: grid chunks relative to each query tile's first cell
   int opt_slot_order = 0;      // 0: chunk-grid slots in estimated-work order, 1: in index order
+  int opt_exact_plan = 0;      // ifvs_exact_search: 0 automatic, 1 direct, 2 screened
   int opt_shared_bound = 0;    // workgroup bound from the wavefronts' published best keys: 0 auto, 1 off, 2 on
   int opt_gather_auto_pct = 30;   // automatic mode: pools up to this % of the rows
   int profile_mask = 0;          // stages timed with HIP events (IFVS_OPT_PROFILE)
   StageTimer* timers = nullptr;  // [kStages] once profiling was enabled
   ScanPlan last_plan{};
+
+  void free_vectors() {
+    for (void* p : {static_cast<void*>(xt), static_cast<void*>(xb), static_cast<void*>(xn),
+                    static_cast<void*>(xmax), static_cast<void*>(xbad), static_cast<void*>(qb),
+                    static_cast<void*>(qn_x), static_cast<void*>(eps_x), static_cast<void*>(thr_x),
+                    static_cast<void*>(bins_x), static_cast<void*>(cand_x), static_cast<void*>(cand_n_x),
+                    static_cast<void*>(partials_x)})
+      if (p) hipFree(p);
+    xt = nullptr;
+    xb = nullptr;
+    xn = nullptr;
+    xmax = nullptr;
+    xbad = nullptr;
+    qb = nullptr;
+    qn_x = eps_x = thr_x = bins_x = nullptr;
+    cand_x = cand_n_x = nullptr;
+    partials_x = nullptr;
+  }
 
   ~ifvs_index() {
     hipSetDevice(device);
@@ -158,6 +196,7 @@ struct ifvs_index {
                     static_cast<void*>(partials), static_cast<void*>(codes_rm),
                     static_cast<void*>(lists), static_cast<void*>(list_n), static_cast<void*>(qmode)})
       if (p) hipFree(p);
+    free_vectors();
     for (int i = 0; i < kStagingSlots; ++i) {
       if (staging[i]) hipHostFree(staging[i]);
       if (staged[i]) hipEventDestroy(staged[i]);
@@ -781,6 +820,10 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
       if (value > 1) return fail(IFVS_E_INVALID, "IFVS_OPT_SLOT_ORDER takes 0 or 1");
       idx->opt_slot_order = static_cast<int>(value);
       return IFVS_OK;
+    case IFVS_OPT_EXACT_PLAN:
+      if (value > 2) return fail(IFVS_E_INVALID, "IFVS_OPT_EXACT_PLAN takes 0, 1 or 2");
+      idx->opt_exact_plan = static_cast<int>(value);
+      return IFVS_OK;
     case IFVS_OPT_SHARED_BOUND:
       if (value > 2) return fail(IFVS_E_INVALID, "IFVS_OPT_SHARED_BOUND takes 0, 1 or 2");
       idx->opt_shared_bound = static_cast<int>(value);
@@ -976,6 +1019,184 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
     if (ifvs_status st = copy_bitmaps_out(idx, nq, bitmap_out, s); st != IFVS_OK) return st;
   }
   idx->last_plan = plan;
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_load_vectors(ifvs_index* idx, const float* x, int32_t mem_kind) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (idx->xt) return fail(IFVS_E_STATE, "vectors are already attached to this index");
+  if (!x) return fail(IFVS_E_INVALID, "x is NULL");
+  if (mem_kind != IFVS_MEM_HOST && mem_kind != IFVS_MEM_DEVICE) return fail(IFVS_E_INVALID, "unknown mem_kind");
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  const int64_t n = idx->n, n32 = (n + 31) / 32 * 32, n64 = (n + 63) / 64;
+  const int dim = idx->dim, ks = exact_ksteps(dim);
+  auto bail = [&](ifvs_status st) {
+    idx->free_vectors();
+    return st;
+  };
+  ifvs_status st;
+  if ((st = dev_alloc(&idx->xt, static_cast<size_t>(n64) * dim * 64, "fp32 vectors")) != IFVS_OK) return bail(st);
+  if ((st = dev_alloc(&idx->xb, static_cast<size_t>(n32 / 32) * ks * 64, "bf16 vector fragments")) != IFVS_OK)
+    return bail(st);
+  if ((st = dev_alloc(&idx->xn, static_cast<size_t>(n32), "vector norms")) != IFVS_OK) return bail(st);
+  if ((st = dev_alloc(&idx->xmax, 1, "largest norm")) != IFVS_OK) return bail(st);
+  if ((st = dev_alloc(&idx->xbad, 1, "non-finite count")) != IFVS_OK) return bail(st);
+  // Workspace of the searches: chunks and bins per query are bounded so the
+  // buffers stay small; the planner never exceeds them.
+  const int max_batch = idx->max_batch;
+  idx->exact_splits_max = 2048;
+  idx->exact_chunks_max = 1024;
+  idx->cand_cap = 16384;
+  const int n_qtiles = (max_batch + 31) / 32;
+  if ((st = dev_alloc(&idx->qb, static_cast<size_t>(n_qtiles) * ks * 64, "query fragments")) != IFVS_OK)
+    return bail(st);
+  if ((st = dev_alloc(&idx->qn_x, max_batch, "query norms")) != IFVS_OK) return bail(st);
+  if ((st = dev_alloc(&idx->eps_x, max_batch, "error bounds")) != IFVS_OK) return bail(st);
+  if ((st = dev_alloc(&idx->thr_x, max_batch, "candidate bounds")) != IFVS_OK) return bail(st);
+  if ((st = dev_alloc(&idx->bins_x, static_cast<size_t>(max_batch) * exact_bins_per_query(idx->exact_splits_max),
+                      "screening minima")) != IFVS_OK)
+    return bail(st);
+  if ((st = dev_alloc(&idx->cand_x, static_cast<size_t>(max_batch) * idx->cand_cap, "candidate lists")) != IFVS_OK)
+    return bail(st);
+  if ((st = dev_alloc(&idx->cand_n_x, max_batch, "candidate counts")) != IFVS_OK) return bail(st);
+  if ((st = dev_alloc(&idx->partials_x, static_cast<size_t>(max_batch) * idx->exact_chunks_max * idx->max_k,
+                      "exact top-k partials")) != IFVS_OK)
+    return bail(st);
+  const float* src = x;
+  float* staged = nullptr;
+  if (mem_kind == IFVS_MEM_HOST) {
+    if ((st = dev_alloc(&staged, static_cast<size_t>(n) * dim, "vector staging")) != IFVS_OK) return bail(st);
+    if (hipError_t e = hipMemcpy(staged, x, sizeof(float) * n * dim, hipMemcpyHostToDevice); e != hipSuccess) {
+      hipFree(staged);
+      return bail(hip_fail(e, "copying vectors"));
+    }
+    src = staged;
+  }
+  hipError_t e = hipMemset(idx->xmax, 0, sizeof(unsigned));
+  if (e == hipSuccess) e = hipMemset(idx->xbad, 0, sizeof(unsigned long long));
+  if (e == hipSuccess) e = launch_exact_stage(src, n, dim, idx->perm, idx->xt, idx->xb, idx->xn, idx->xmax, idx->xbad, 0);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  unsigned long long bad = 0;
+  if (e == hipSuccess) e = hipMemcpy(&bad, idx->xbad, sizeof(bad), hipMemcpyDeviceToHost);
+  if (staged) hipFree(staged);
+  if (e != hipSuccess) return bail(hip_fail(e, "staging vectors"));
+  if (bad) return bail(fail(IFVS_E_INVALID, std::to_string(bad) + " vector values are NaN or infinite"));
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const ifvs_predicate* preds, int32_t k,
+                              int32_t* ids_out, float* dist_out, void* stream) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (!idx->xt) return fail(IFVS_E_STATE, "no vectors attached to this index (ifvs_load_vectors)");
+  if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
+  if (k < 1 || k > idx->max_k)
+    return fail(IFVS_E_INVALID, "k = " + std::to_string(k) + " outside 1.." + std::to_string(idx->max_k) + " (max_k)");
+  if (nq == 0) return IFVS_OK;
+  if (!q || !ids_out || !dist_out) return fail(IFVS_E_INVALID, "q, ids_out or dist_out is NULL");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  DevPred* host = nullptr;
+  int slot = 0;
+  if (ifvs_status st = stage_predicates(idx, nq, preds, true, false, s, &slot, &host); st != IFVS_OK) return st;
+  // Plan.  Screening reads every row of a 32-query tile's hull twice in bf16
+  // (2 x 2 bytes per dimension); scoring directly reads each query's own
+  // interval once in fp32 (4 bytes per dimension).  Screen when the hulls
+  // together are shorter than the intervals together -- queries sharing
+  // rows -- unless forced.
+  const int32_t* qorder_host = reinterpret_cast<const int32_t*>(host + idx->max_batch);
+  bool need_bitmap = false;
+  int64_t sum_iv = 0, sum_hull = 0, max_iv = 0;
+  for (int t = 0; t * 32 < nq; ++t) {
+    int64_t lo = INT64_MAX, hi = 0;
+    for (int i = t * 32; i < std::min(nq, t * 32 + 32); ++i) {
+      const DevPred& d = host[qorder_host[i]];
+      need_bitmap = need_bitmap || d.residual_mask != 0;
+      int64_t a = 0, b = idx->n_tiles;
+      if (idx->n_cluster > 0) estimate_interval_range(idx, d, &a, &b);
+      if (d.n_eff < 0) a = b = 0;
+      if (b > a) {
+        sum_iv += b - a;
+        max_iv = std::max(max_iv, b - a);
+        lo = std::min(lo, a);
+        hi = std::max(hi, b);
+      }
+    }
+    if (hi > lo) sum_hull += hi - lo;
+  }
+  const bool screened = idx->opt_exact_plan == 2 || (idx->opt_exact_plan == 0 && sum_hull < sum_iv);
+  IFVS_LAUNCH(idx, kStFilter, s, "launching interval kernel",
+              launch_intervals(idx->attrs_phys, idx->n, idx->c0, idx->c1, idx->vstart, idx->vmin, idx->vcount,
+                               idx->staging_dev[slot],
+                               reinterpret_cast<const int32_t*>(idx->staging_dev[slot] + idx->max_batch), nq,
+                               idx->preds_dev, idx->qorder_dev, idx->iv_dev, idx->gthr_dev, nullptr,
+                               idx->slot_order_dev, 0, s));
+  if (ifvs_status st = release_slot(idx, slot, s); st != IFVS_OK) return st;
+  if (need_bitmap)
+    if (ifvs_status st = filter_into_workspace(idx, nq, true, false, s); st != IFVS_OK) return st;
+  IFVS_LAUNCH(idx, kStCondition, s, "launching exact query kernel",
+              launch_exact_queries(q, idx->dim, nq, idx->qorder_dev, idx->xmax, idx->qb, idx->qn_x, idx->eps_x,
+                                   idx->cand_n_x, s));
+  ExactRerank r{};
+  r.xt = idx->xt;
+  r.dim = idx->dim;
+  r.q = q;
+  r.qorder = idx->qorder_dev;
+  r.iv = idx->iv_dev;
+  r.preds = idx->preds_dev;
+  r.bitmap = idx->bitmap;
+  r.stride64 = idx->stride64;
+  r.perm = idx->perm;
+  r.nq = nq;
+  r.k = k;
+  r.partials = idx->partials_x;
+  if (screened) {
+    // Chunks of the hull: enough workgroups to fill the GPU, every row of
+    // the largest possible hull (the whole index) covered.
+    const int64_t quantum = exact_chunk_quantum();
+    const int64_t n_qtiles = (nq + 31) / 32;
+    int64_t chunk_rows = (idx->n * n_qtiles + 2047) / 2048;
+    chunk_rows = std::min<int64_t>(65536, std::max<int64_t>(4 * quantum, (chunk_rows + quantum - 1) / quantum * quantum));
+    int64_t splits = (idx->n + chunk_rows - 1) / chunk_rows;
+    if (splits > idx->exact_splits_max) {
+      splits = idx->exact_splits_max;
+      chunk_rows = ((idx->n + splits - 1) / splits + quantum - 1) / quantum * quantum;
+    }
+    ExactScreen e{};
+    e.xb = idx->xb;
+    e.xn = idx->xn;
+    e.dim = idx->dim;
+    e.qb = idx->qb;
+    e.qn = idx->qn_x;
+    e.thr = idx->thr_x;
+    e.qorder = idx->qorder_dev;
+    e.iv = idx->iv_dev;
+    e.preds = idx->preds_dev;
+    e.bitmap = idx->bitmap;
+    e.stride64 = idx->stride64;
+    e.nq = nq;
+    e.chunk_rows = chunk_rows;
+    e.splits = static_cast<int>(splits);
+    e.bins = idx->bins_x;
+    e.cand = idx->cand_x;
+    e.cand_n = idx->cand_n_x;
+    e.cand_cap = idx->cand_cap;
+    IFVS_LAUNCH(idx, kStScan, s, "launching exact screening (pass 1)", launch_exact_screen(e, 1, s));
+    IFVS_LAUNCH(idx, kStScan, s, "launching exact threshold kernel",
+                launch_exact_threshold(idx->bins_x, exact_bins_per_query(e.splits), nq, k, idx->eps_x, idx->thr_x, s));
+    IFVS_LAUNCH(idx, kStScan, s, "launching exact screening (pass 2)", launch_exact_screen(e, 2, s));
+    r.cand = idx->cand_x;
+    r.cand_n = idx->cand_n_x;
+    r.cand_cap = idx->cand_cap;
+    r.chunks = 16;
+  } else {
+    // About 4096 rows per wavefront (the planner's interval estimates only
+    // size the grid; every chunk covers its share of the true interval).
+    r.chunks = static_cast<int>(std::min<int64_t>(idx->exact_chunks_max, std::max<int64_t>(1, (max_iv + 63) / 64)));
+  }
+  IFVS_LAUNCH(idx, kStScan, s, "launching exact scoring kernel", launch_exact_rerank(r, s));
+  IFVS_LAUNCH(idx, kStMerge, s, "launching top-k merge kernel",
+              launch_topk_merge(idx->partials_x, nq, static_cast<int64_t>(r.chunks) * k, k, idx->iv_dev, 0, k,
+                                idx->qorder_dev, ids_out, dist_out, s));
   return IFVS_OK;
 }
 

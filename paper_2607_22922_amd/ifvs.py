@@ -26,11 +26,12 @@ MAX_K = 1024
 OPT_QTILE, OPT_SPLITS, OPT_PROFILE, OPT_MIN_CHUNK, OPT_GRID_TILES, OPT_GATHER, OPT_GRID_RELATIVE = 1, 2, 3, 4, 5, 6, 7
 OPT_SLOT_ORDER = 8
 OPT_SHARED_BOUND = 9
+OPT_EXACT_PLAN = 10
 STAGES = ("condition", "lut", "filter", "scan", "merge")
 
 EXPORTED = ("ifvs_load_index", "ifvs_free_index", "ifvs_select_codebook", "ifvs_build_lut",
             "ifvs_filter", "ifvs_filtered_search", "ifvs_set_option", "ifvs_last_plan",
-            "ifvs_read_profile", "ifvs_last_error")
+            "ifvs_read_profile", "ifvs_last_error", "ifvs_load_vectors", "ifvs_exact_search")
 
 
 class IfvsError(RuntimeError):
@@ -90,6 +91,8 @@ def _load_library() -> ctypes.CDLL:
         "ifvs_last_plan": ([vp, ctypes.POINTER(ctypes.c_int64)], i32),
         "ifvs_read_profile": ([vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)], i32),
         "ifvs_last_error": ([], ctypes.c_char_p),
+        "ifvs_load_vectors": ([vp, vp, i32], i32),
+        "ifvs_exact_search": ([vp, i32, vp, vp, i32, vp, vp, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -231,6 +234,16 @@ class Index:
                                          ids_out.data_ptr(), dist_out.data_ptr(), _ptr(bitmap_out),
                                          _stream(stream)))
 
+    def load_vectors(self, x):
+        """Attach the full-precision vectors [n][dim] (ifvs_load_vectors)."""
+        x = x.to(dtype=torch.float32).contiguous()
+        _check(_lib.ifvs_load_vectors(self.handle, x.data_ptr(),
+                                      MEM_DEVICE if x.device.type == "cuda" else MEM_HOST))
+
+    def exact_search_into(self, q, preds_c, k, ids_out, dist_out, stream=None):
+        _check(_lib.ifvs_exact_search(self.handle, q.shape[0], q.data_ptr(), preds_c, k,
+                                      ids_out.data_ptr(), dist_out.data_ptr(), _stream(stream)))
+
     # ------------------------------------------------ allocating helpers
     def words(self) -> int:
         return (self.n + 31) // 32
@@ -268,6 +281,15 @@ class Index:
               if want_bitmap else None)
         self.search_into(nq, pack_predicates(preds), lut, lut_dtype, k, ids, dist, bm)
         return (ids, dist, bm) if want_bitmap else (ids, dist)
+
+    def exact_search(self, q, preds, k):
+        """Exact filtered kNN over the attached full-precision vectors."""
+        nq = len(preds)
+        q = _dev_f32(q, self.device)
+        ids = torch.empty(nq, k, device=self.device, dtype=torch.int32)
+        dist = torch.empty(nq, k, device=self.device, dtype=torch.float32)
+        self.exact_search_into(q, pack_predicates(preds), k, ids, dist)
+        return ids, dist
 
     def query(self, q, preds, k, w_z=None, lut_dtype=LUT_F32, conditioned=True):
         """All four steps for one batch: condition, table, filter+scan+select."""
