@@ -190,6 +190,9 @@ def main():
     ap.add_argument("--plain-steps", type=int, default=None,
                     help="steps timed on the unclustered (bitmap) layout for comparison "
                          "(0 = skip; default 5 on c4, else 0)")
+    ap.add_argument("--exact-steps", type=int, default=None,
+                    help="batches per bin timed for exact filtered kNN over the full-precision vectors "
+                         "(ifvs_exact_search; 0 = skip; default 4, 0 on c5)")
     ap.add_argument("--lut", choices=["f32", "f16"], default="f32")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain copy kernel of known size (for counter calibration)")
@@ -214,6 +217,8 @@ def main():
         args.plain_steps = 5 if name == "c4" else 0
     if args.recall_queries is None:
         args.recall_queries = 100 if name in ("c1", "c5") else 256
+    if args.exact_steps is None:
+        args.exact_steps = 0 if name == "c5" else 4
     cols = CLUSTER_COLS[name]
     tile_bytes = cols == (0,)      # one-column intervals: bytes counted per code tile
     lut_dt = B.LUT_F16 if args.lut == "f16" else B.LUT_F32
@@ -360,6 +365,7 @@ def main():
     # the synthetic conditioned mode, against exact filtered kNN.
     nr = min(args.recall_queries, batch)
     gt_all = {}
+    gt_all_ids = {}
     if nr > 0:
         t_gt = time.time()
         gt_all = exact_filtered_knn(name, w.N, w.attrs, w.queries[:nr], {s: w.preds[s][:nr] for s in bins}, k)
@@ -368,6 +374,7 @@ def main():
         q = w.queries[:nr]
         preds = w.preds[s][:nr]
         t_np = gt_all[s].cpu().numpy()
+        gt_all_ids[str(s)] = gt_all[s]
         for mode in ("identity", "conditioned"):
             if mode == "identity":
                 lt = clus.build_lut(q, None, None, lut_dt)
@@ -383,6 +390,46 @@ def main():
                     hits += len(truth & set(int(v) for v in g_np[i] if v >= 0)) / len(truth)
             bins_out[str(s)][f"recall@{k}_{mode}"] = round(hits / nr, 4)
     log(f"[bench] bins: {json.dumps(bins_out)}")
+
+    # Exact filtered kNN over the full-precision vectors (Section 3.2's
+    # pre-filtering baseline (i), the ground truth of Section 3.1): whole
+    # batches timed with events on the stream, every stage included.
+    exact_out = None
+    if args.exact_steps > 0:
+        from workload import base_chunks
+        x = torch.empty(w.N, w.D, device=dev)
+        for s0, xb in base_chunks(name, dev, w.N):
+            x[s0:s0 + xb.shape[0]] = xb
+        clus.load_vectors(x)
+        del x
+        torch.cuda.synchronize()
+        ex_ids = torch.empty(batch, k, device=dev, dtype=torch.int32)
+        ex_d = torch.empty(batch, k, device=dev)
+        ex_bins, ex_total = {}, 0.0
+        for s in bins:
+            clus.exact_search_into(w.queries[:batch], packed[s][0], k, ex_ids, ex_d)   # warmup
+            ms = []
+            for i in range(args.exact_steps):
+                b = i % n_batches
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                clus.exact_search_into(w.queries[b * batch:(b + 1) * batch], packed[s][b], k, ex_ids, ex_d)
+                e1.record(stream)
+                ms.append((e0, e1))
+            torch.cuda.synchronize()
+            ms = [a.elapsed_time(c) for a, c in ms]
+            ex_total += sum(ms)
+            ex_bins[str(s)] = {"qps": batch * len(ms) / (sum(ms) / 1e3), "ms_per_batch": float(np.median(ms))}
+            if str(s) in gt_all_ids:
+                nr_ = gt_all_ids[str(s)].shape[0]
+                clus.exact_search_into(w.queries[:batch], packed[s][0], k, ex_ids, ex_d)
+                same = (ex_ids[:nr_].long() == gt_all_ids[str(s)]).all(1).float().mean()
+                ex_bins[str(s)]["same_ids_as_fp64_ground_truth"] = round(float(same), 4)
+        exact_out = {"qps": args.exact_steps * len(bins) * batch / (ex_total / 1e3), "steps": args.exact_steps,
+                     "bins": ex_bins,
+                     "note": "exact fp32 squared L2 over the predicate-passing full-precision vectors; "
+                             "bf16 matrix-core screening with an error bound, exact scoring of survivors"}
+        log(f"[bench] exact search: {exact_out['qps']:.0f} queries/s; {json.dumps(ex_bins)}")
 
     # Oracle on the host cores: a bounded sample of the same workload.
     cpu = None
@@ -455,6 +502,7 @@ def main():
                      "bytes_per_launch": bytes_per_launch,
                      "useful_bytes_per_launch": useful_total / max(1, scan_launches)},
         "plain_layout": plain_out,
+        "exact_search": exact_out,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -134,7 +134,8 @@ struct ifvs_index {
   float* qn_x = nullptr;         // [max_batch] |q|^2
   float* eps_x = nullptr;        // [max_batch] screening error bounds
   float* thr_x = nullptr;        // [max_batch] candidate bounds
-  float* bins_x = nullptr;       // [max_batch][exact_bins_per_query(exact_splits_max)]
+  float* bins_x = nullptr;       // [max_batch][bins_cap]
+  int64_t bins_cap = 0;
   int exact_splits_max = 0;
   int32_t* cand_x = nullptr;     // [max_batch][cand_cap]
   int32_t* cand_n_x = nullptr;   // [max_batch]
@@ -1053,8 +1054,8 @@ ifvs_status ifvs_load_vectors(ifvs_index* idx, const float* x, int32_t mem_kind)
   if ((st = dev_alloc(&idx->qn_x, max_batch, "query norms")) != IFVS_OK) return bail(st);
   if ((st = dev_alloc(&idx->eps_x, max_batch, "error bounds")) != IFVS_OK) return bail(st);
   if ((st = dev_alloc(&idx->thr_x, max_batch, "candidate bounds")) != IFVS_OK) return bail(st);
-  if ((st = dev_alloc(&idx->bins_x, static_cast<size_t>(max_batch) * exact_bins_per_query(idx->exact_splits_max),
-                      "screening minima")) != IFVS_OK)
+  idx->bins_cap = 65536;
+  if ((st = dev_alloc(&idx->bins_x, static_cast<size_t>(max_batch) * idx->bins_cap, "screening minima")) != IFVS_OK)
     return bail(st);
   if ((st = dev_alloc(&idx->cand_x, static_cast<size_t>(max_batch) * idx->cand_cap, "candidate lists")) != IFVS_OK)
     return bail(st);
@@ -1105,7 +1106,7 @@ ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const
   // rows -- unless forced.
   const int32_t* qorder_host = reinterpret_cast<const int32_t*>(host + idx->max_batch);
   bool need_bitmap = false;
-  int64_t sum_iv = 0, sum_hull = 0, max_iv = 0;
+  int64_t sum_iv = 0, sum_hull = 0, max_iv = 0, min_iv = INT64_MAX;
   for (int t = 0; t * 32 < nq; ++t) {
     int64_t lo = INT64_MAX, hi = 0;
     for (int i = t * 32; i < std::min(nq, t * 32 + 32); ++i) {
@@ -1117,6 +1118,7 @@ ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const
       if (b > a) {
         sum_iv += b - a;
         max_iv = std::max(max_iv, b - a);
+        min_iv = std::min(min_iv, b - a);
         lo = std::min(lo, a);
         hi = std::max(hi, b);
       }
@@ -1161,7 +1163,15 @@ ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const
       splits = idx->exact_splits_max;
       chunk_rows = ((idx->n + splits - 1) / splits + quantum - 1) / quantum * quantum;
     }
+    // Bins: R lanes share one; R as large as leaves the shortest interval
+    // (estimated, in rows) at least 4k bins, within the bin budget.
+    const int64_t lane_rows = std::max<int64_t>(1, chunk_rows / (32 * 8));
+    const int64_t short_rows = min_iv == INT64_MAX ? 0 : min_iv * 64;
+    int bin_lanes = 32;
+    while (bin_lanes > 1 && short_rows / (lane_rows * bin_lanes) < 4 * static_cast<int64_t>(k)) bin_lanes /= 2;
+    while (exact_bins_per_query(static_cast<int>(splits), bin_lanes) > idx->bins_cap) bin_lanes *= 2;
     ExactScreen e{};
+    e.bin_lanes = bin_lanes;
     e.xb = idx->xb;
     e.xn = idx->xn;
     e.dim = idx->dim;
@@ -1182,7 +1192,8 @@ ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const
     e.cand_cap = idx->cand_cap;
     IFVS_LAUNCH(idx, kStScan, s, "launching exact screening (pass 1)", launch_exact_screen(e, 1, s));
     IFVS_LAUNCH(idx, kStScan, s, "launching exact threshold kernel",
-                launch_exact_threshold(idx->bins_x, exact_bins_per_query(e.splits), nq, k, idx->eps_x, idx->thr_x, s));
+                launch_exact_threshold(idx->bins_x, exact_bins_per_query(e.splits, e.bin_lanes), nq, k, idx->eps_x,
+                                       idx->thr_x, s));
     IFVS_LAUNCH(idx, kStScan, s, "launching exact screening (pass 2)", launch_exact_screen(e, 2, s));
     r.cand = idx->cand_x;
     r.cand_n = idx->cand_n_x;

@@ -191,7 +191,7 @@ hipError_t launch_topk_merge(const uint64_t* partials, int nq, int64_t per_query
 
 // Exact filtered kNN over the full-precision vectors (k_exact.hip).
 int exact_ksteps(int dim);                 // 16-dimension MFMA steps
-int64_t exact_bins_per_query(int splits);  // pass-1 values per query position
+int64_t exact_bins_per_query(int splits, int bin_lanes);  // pass-1 values per query position
 int64_t exact_chunk_quantum();             // screening chunks are multiples of this many rows
 // Per physical row r (original row perm[r]): fp32 copy in 64-row tiles
 // xt[(r / 64 * dim + j) * 64 + r % 64], bf16 MFMA fragments xb, |x|^2 xn
@@ -218,7 +218,8 @@ struct ExactScreen {
   int nq;
   int64_t chunk_rows;
   int splits;
-  float* bins;            // [positions][exact_bins_per_query(splits)]
+  int bin_lanes;          // lanes (power of two <= 32) whose row minima share a bin
+  float* bins;            // [positions][exact_bins_per_query(splits, bin_lanes)]
   int32_t* cand;          // [positions][cand_cap]
   int32_t* cand_n;
   int64_t cand_cap;

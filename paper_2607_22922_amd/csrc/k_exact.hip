@@ -14,10 +14,11 @@
 //    pass computes dd = |x|^2 + |q|^2 - 2 x.q for 32 queries x 32 rows per
 //    tile.  eps(q) bounds |dd - d| for every row (bf16 rounding of x and q,
 //    fp32 accumulation, and the fp32 rounding of d itself).  Pass 1 keeps,
-//    per (query, wavefront, chunk), the smallest dd of the rows it saw;
-//    these come from distinct rows, so the k-th smallest of them, v_k, has k
-//    rows with d <= v_k + eps, and every row of the exact top k has
-//    dd <= v_k + 2 eps.  Pass 2 lists the rows under that bound, and only
+//    per (query, wavefront, chunk, group of R lanes), the smallest dd of the
+//    rows it saw (R is chosen so that a query's interval spans several times
+//    k such bins); these come from distinct rows, so the k-th smallest of
+//    them, v_k, has k rows with d <= v_k + eps, and every row of the exact
+//    top k has dd <= v_k + 2 eps.  Pass 2 lists the rows under that bound, and only
 //    those are scored exactly.  Both plans end in the same exact scoring and
 //    merge, so results are identical.
 #include <hip/hip_runtime.h>
@@ -152,7 +153,8 @@ struct ScreenArgs {
   int nq, ks;
   int64_t chunk_rows;         // rows per workgroup chunk (multiple of 32 * kExWaves)
   int splits;                 // chunks per query tile
-  float* bins;                // pass 1: [positions][splits * kExWaves]
+  int bin_lanes;              // R: lanes whose minima share one bin (1, 2, ..., 32)
+  float* bins;                // pass 1: [positions][splits * kExWaves * 32 / R]
   int32_t* cand;              // pass 2: [positions][cand_cap]
   int32_t* cand_n;
   int64_t cand_cap;
@@ -260,20 +262,22 @@ __global__ __launch_bounds__(kExWaves * 64) void exact_screen_kernel(const Scree
     }
   }
   if (PASS == 1) {
-    // One value per (query, wavefront, chunk): the smallest over the 32 lanes
-    // holding the query's rows.
+    // One value per (query, wavefront, chunk, group of R lanes): the smallest
+    // over the R lanes' rows.
+    const int R = a.bin_lanes, per = 32 / R;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       float v = run_min[i];
-#pragma unroll
-      for (int o = 16; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o, 32));
+      for (int o = 1; o < R; o <<= 1) v = fminf(v, __shfl_xor(v, o, 32));
       run_min[i] = v;
     }
-    if ((lane & 31) == 0) {
+    if ((lane & (R - 1)) == 0) {
+      const size_t n_bins = static_cast<size_t>(a.splits) * kExWaves * per;
+      const size_t slot = static_cast<size_t>(chunk * kExWaves + wave) * per + (lane & 31) / R;
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int p = qt * 32 + 8 * (i >> 2) + 4 * half + (i & 3);
-        if (p < a.nq) a.bins[static_cast<size_t>(p) * a.splits * kExWaves + chunk * kExWaves + wave] = run_min[i];
+        if (p < a.nq) a.bins[static_cast<size_t>(p) * n_bins + slot] = run_min[i];
       }
     }
   }
@@ -352,8 +356,19 @@ __global__ __launch_bounds__(64) void exact_rerank_kernel(const RerankArgs a) {
     if (ok) {
       const float* xr = a.xt + static_cast<size_t>(row >> 6) * a.dim * 64 + (row & 63);
       float d = 0.0f;
-#pragma unroll 8
-      for (int j = 0; j < a.dim; ++j) {
+      // 16 values in flight, then added in j order
+      int j = 0;
+      for (; j + 16 <= a.dim; j += 16) {
+        float v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = xr[static_cast<size_t>(j + u) * 64];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const float e = __fsub_rn(v[u], s_q[j + u]);
+          d = __fadd_rn(d, __fmul_rn(e, e));
+        }
+      }
+      for (; j < a.dim; ++j) {
         const float e = __fsub_rn(xr[static_cast<size_t>(j) * 64], s_q[j]);
         d = __fadd_rn(d, __fmul_rn(e, e));
       }
@@ -430,6 +445,7 @@ hipError_t launch_exact_screen(const ExactScreen& e, int pass, hipStream_t s) {
   a.ks = exact_ksteps(e.dim);
   a.chunk_rows = e.chunk_rows;
   a.splits = e.splits;
+  a.bin_lanes = e.bin_lanes;
   a.bins = e.bins;
   a.cand = e.cand;
   a.cand_n = e.cand_n;
@@ -453,7 +469,9 @@ hipError_t launch_exact_threshold(const float* bins, int64_t n_bins, int nq, int
   return hipGetLastError();
 }
 
-int64_t exact_bins_per_query(int splits) { return static_cast<int64_t>(splits) * kExWaves; }
+int64_t exact_bins_per_query(int splits, int bin_lanes) {
+  return static_cast<int64_t>(splits) * kExWaves * (32 / bin_lanes);
+}
 int64_t exact_chunk_quantum() { return 32 * kExWaves; }
 
 hipError_t launch_exact_rerank(const ExactRerank& e, hipStream_t s) {
