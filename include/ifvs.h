@@ -203,9 +203,10 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
  * full-precision vectors of the candidate set (Section 3.2).
  *  x:        [n][dim] fp32, row i = vector id i, in the memory named by
  *            mem_kind; deep-copied (stored in the index's row order as fp32
- *            and as bf16 matrix-core fragments, with each row's squared
- *            norm), so the caller may free it after return.  Costs
- *            n * dim * 6 bytes of device memory plus a workspace sized by
+ *            twice, in 64-row tiles and row by row, and as bf16 matrix-core
+ *            fragments, with each row's squared norm), so the caller may
+ *            free it after return.  Costs n * dim * 10 bytes of device
+ *            memory plus a workspace sized by
  *            max_batch and max_k (a few hundred MB at most).
  * Errors: IFVS_E_INVALID (NULL x, unknown mem_kind, a NaN or infinite
  * value: nothing is kept), IFVS_E_STATE (NULL handle, or vectors already

@@ -126,6 +126,7 @@ struct ifvs_index {
   // Full-precision vectors (ifvs_load_vectors) and the exact search's
   // workspace.
   float* xt = nullptr;           // [ceil(n/64)][dim][64] fp32, physical order
+  float* xr = nullptr;           // [n][dim] fp32, physical order
   uint4* xb = nullptr;           // [ceil(n/32)][ksteps][64] bf16 fragments
   float* xn = nullptr;           // [ceil(n/32)*32] squared norms
   unsigned* xmax = nullptr;      // largest row norm (fp32 bits)
@@ -161,13 +162,14 @@ struct ifvs_index {
   ScanPlan last_plan{};
 
   void free_vectors() {
-    for (void* p : {static_cast<void*>(xt), static_cast<void*>(xb), static_cast<void*>(xn),
+    for (void* p : {static_cast<void*>(xt), static_cast<void*>(xr), static_cast<void*>(xb), static_cast<void*>(xn),
                     static_cast<void*>(xmax), static_cast<void*>(xbad), static_cast<void*>(qb),
                     static_cast<void*>(qn_x), static_cast<void*>(eps_x), static_cast<void*>(thr_x),
                     static_cast<void*>(bins_x), static_cast<void*>(cand_x), static_cast<void*>(cand_n_x),
                     static_cast<void*>(partials_x)})
       if (p) hipFree(p);
     xt = nullptr;
+    xr = nullptr;
     xb = nullptr;
     xn = nullptr;
     xmax = nullptr;
@@ -1025,18 +1027,20 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
 
 ifvs_status ifvs_load_vectors(ifvs_index* idx, const float* x, int32_t mem_kind) {
   if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
-  if (idx->xt) return fail(IFVS_E_STATE, "vectors are already attached to this index");
+  if (idx->xr) return fail(IFVS_E_STATE, "vectors are already attached to this index");
   if (!x) return fail(IFVS_E_INVALID, "x is NULL");
   if (mem_kind != IFVS_MEM_HOST && mem_kind != IFVS_MEM_DEVICE) return fail(IFVS_E_INVALID, "unknown mem_kind");
   IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
-  const int64_t n = idx->n, n32 = (n + 31) / 32 * 32, n64 = (n + 63) / 64;
+  const int64_t n = idx->n, n32 = (n + 31) / 32 * 32;
   const int dim = idx->dim, ks = exact_ksteps(dim);
   auto bail = [&](ifvs_status st) {
     idx->free_vectors();
     return st;
   };
   ifvs_status st;
-  if ((st = dev_alloc(&idx->xt, static_cast<size_t>(n64) * dim * 64, "fp32 vectors")) != IFVS_OK) return bail(st);
+  if ((st = dev_alloc(&idx->xt, static_cast<size_t>((n + 63) / 64) * dim * 64, "fp32 vector tiles")) != IFVS_OK)
+    return bail(st);
+  if ((st = dev_alloc(&idx->xr, static_cast<size_t>(n) * dim, "fp32 vectors")) != IFVS_OK) return bail(st);
   if ((st = dev_alloc(&idx->xb, static_cast<size_t>(n32 / 32) * ks * 64, "bf16 vector fragments")) != IFVS_OK)
     return bail(st);
   if ((st = dev_alloc(&idx->xn, static_cast<size_t>(n32), "vector norms")) != IFVS_OK) return bail(st);
@@ -1075,7 +1079,7 @@ ifvs_status ifvs_load_vectors(ifvs_index* idx, const float* x, int32_t mem_kind)
   }
   hipError_t e = hipMemset(idx->xmax, 0, sizeof(unsigned));
   if (e == hipSuccess) e = hipMemset(idx->xbad, 0, sizeof(unsigned long long));
-  if (e == hipSuccess) e = launch_exact_stage(src, n, dim, idx->perm, idx->xt, idx->xb, idx->xn, idx->xmax, idx->xbad, 0);
+  if (e == hipSuccess) e = launch_exact_stage(src, n, dim, idx->perm, idx->xt, idx->xr, idx->xb, idx->xn, idx->xmax, idx->xbad, 0);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   unsigned long long bad = 0;
   if (e == hipSuccess) e = hipMemcpy(&bad, idx->xbad, sizeof(bad), hipMemcpyDeviceToHost);
@@ -1088,7 +1092,7 @@ ifvs_status ifvs_load_vectors(ifvs_index* idx, const float* x, int32_t mem_kind)
 ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const ifvs_predicate* preds, int32_t k,
                               int32_t* ids_out, float* dist_out, void* stream) {
   if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
-  if (!idx->xt) return fail(IFVS_E_STATE, "no vectors attached to this index (ifvs_load_vectors)");
+  if (!idx->xr) return fail(IFVS_E_STATE, "no vectors attached to this index (ifvs_load_vectors)");
   if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
   if (k < 1 || k > idx->max_k)
     return fail(IFVS_E_INVALID, "k = " + std::to_string(k) + " outside 1.." + std::to_string(idx->max_k) + " (max_k)");
@@ -1140,6 +1144,7 @@ ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const
                                    idx->cand_n_x, s));
   ExactRerank r{};
   r.xt = idx->xt;
+  r.xr = idx->xr;
   r.dim = idx->dim;
   r.q = q;
   r.qorder = idx->qorder_dev;

@@ -193,13 +193,14 @@ hipError_t launch_topk_merge(const uint64_t* partials, int nq, int64_t per_query
 int exact_ksteps(int dim);                 // 16-dimension MFMA steps
 int64_t exact_bins_per_query(int splits, int bin_lanes);  // pass-1 values per query position
 int64_t exact_chunk_quantum();             // screening chunks are multiples of this many rows
-// Per physical row r (original row perm[r]): fp32 copy in 64-row tiles
-// xt[(r / 64 * dim + j) * 64 + r % 64], bf16 MFMA fragments xb, |x|^2 xn
+// Per physical row r (original row perm[r]): fp32 copies in 64-row tiles
+// xt[(r / 64 * dim + j) * 64 + r % 64] and row-major xr[r * dim + j], bf16
+// MFMA fragments xb, |x|^2 xn
 // ([ceil(n/32)*32], zero past n); the largest row norm as fp32 bits
 // (*max_norm_bits must start at 0) and the count of non-finite values (*bad,
 // starts at 0).
-hipError_t launch_exact_stage(const float* x, int64_t n, int dim, const int32_t* perm, float* xt, uint4* xb,
-                              float* xn, unsigned* max_norm_bits, unsigned long long* bad, hipStream_t s);
+hipError_t launch_exact_stage(const float* x, int64_t n, int dim, const int32_t* perm, float* xt, float* xr,
+                              uint4* xb, float* xn, unsigned* max_norm_bits, unsigned long long* bad, hipStream_t s);
 // Query fragments (ceil(nq/32) tiles), |q|^2, error bounds; clears cand_n.
 hipError_t launch_exact_queries(const float* q, int dim, int nq, const int32_t* qorder, const unsigned* max_norm_bits,
                                 uint4* qb, float* qn, float* eps, int32_t* cand_n, hipStream_t s);
@@ -228,7 +229,8 @@ hipError_t launch_exact_screen(const ExactScreen& e, int pass, hipStream_t s);
 hipError_t launch_exact_threshold(const float* bins, int64_t n_bins, int nq, int k, const float* eps, float* thr,
                                   hipStream_t s);
 struct ExactRerank {
-  const float* xt;
+  const float* xt;        // [ceil(n/64)][dim][64] fp32, physical order
+  const float* xr;        // [n][dim] fp32, physical order
   int dim;
   const float* q;         // [nq original][dim]
   const int32_t* qorder;

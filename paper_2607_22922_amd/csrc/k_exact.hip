@@ -59,15 +59,18 @@ __device__ __forceinline__ uint4 pack_fragment(const float* __restrict__ row, in
 }
 
 // ---------------------------------------------------------------- staging
-// One thread per physical row: the fp32 copy in 64-row tiles
-// (xt[(tile * dim + j) * 64 + lane]), |x|^2 (fp32, summed in j order) and the
+// One thread per physical row: the fp32 copies (64-row tiles,
+// xt[(r / 64 * dim + j) * 64 + r % 64], for scans of consecutive rows, and
+// row-major, xr[r * dim + j], for scattered rows), |x|^2 (fp32, summed in j
+// order) and the
 // bf16 fragments of its 32-row tile (xb[(tile32 * ks + s) * 64 + lane]: lane
 // l holds row l % 32, dims s * 16 + (l / 32) * 8 .. + 8).  Also the largest
 // norm (as fp32 bits; norms are non-negative) and a count of non-finite
 // values.
 __global__ __launch_bounds__(256) void exact_stage_kernel(const float* __restrict__ x, int64_t n, int dim,
                                                           int ks, const int32_t* __restrict__ perm,
-                                                          float* __restrict__ xt, uint4* __restrict__ xb,
+                                                          float* __restrict__ xt, float* __restrict__ xr,
+                                                          uint4* __restrict__ xb,
                                                           float* __restrict__ xn, unsigned* __restrict__ max_norm_bits,
                                                           unsigned long long* __restrict__ bad) {
   const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -81,6 +84,7 @@ __global__ __launch_bounds__(256) void exact_stage_kernel(const float* __restric
     for (int j = 0; j < dim; ++j) {
       const float v = src[j];
       xt[(static_cast<size_t>(r >> 6) * dim + j) * 64 + (r & 63)] = v;
+      xr[static_cast<size_t>(r) * dim + j] = v;
       acc = __fadd_rn(acc, __fmul_rn(v, v));
       nonfinite += isfinite(v) ? 0u : 1u;
     }
@@ -316,8 +320,11 @@ __global__ __launch_bounds__(64) void exact_threshold_kernel(const float* __rest
 }
 
 // ------------------------------------------------------------------ rerank
+constexpr int kStageDims = 64;     // dimensions of 64 rows staged in LDS per step
+
 struct RerankArgs {
-  const float* xt;            // fp32 rows, 64-row tiles
+  const float* xt;            // fp32 rows in 64-row tiles, physical order
+  const float* xr;            // fp32 rows, row-major, physical order
   int dim;
   const float* q;             // [nq original][dim]
   const int32_t* qorder;
@@ -334,44 +341,35 @@ struct RerankArgs {
 };
 
 // grid = (chunks, positions), one wavefront each: chunk c of the query's
-// work -- its candidate list (screened plan, list not overflowed) or its
-// row interval (direct plan, or a list that overflowed) -- scored exactly,
-// the k best keys written to partials.
+// work -- its candidate list (LISTED: screened plan, list not overflowed) or
+// its row interval (direct plan, or a list that overflowed) -- scored
+// exactly, the k best keys written to partials.
+//  * Consecutive rows (an interval): each lane reads its own row from the
+//    64-row tiles, one coalesced 256-byte load per dimension for the wave.
+//  * Scattered rows (a candidate list): the 64 lanes' rows are staged in
+//    LDS 64 dimensions at a time from the row-major copy, one coalesced
+//    256-byte load per row, then each lane reads its own row.
+// Either way each lane adds its row's terms in j order.
+template <bool LISTED>
 __global__ __launch_bounds__(64) void exact_rerank_kernel(const RerankArgs a) {
   extern __shared__ uint64_t smem_r[];
   uint64_t* pool = smem_r;
+  const int dim_pad = (a.dim + kStageDims - 1) / kStageDims * kStageDims;
   float* s_q = reinterpret_cast<float*>(smem_r + 64 * a.kpl);
+  float* s_x = s_q + dim_pad;                     // LISTED: [64 rows][kStageDims + 1]
   const int c = blockIdx.x, p = blockIdx.y;
   const int lane = threadIdx.x;
   const int o = a.qorder[p];
-  for (int j = lane; j < a.dim; j += 64) s_q[j] = a.q[static_cast<size_t>(o) * a.dim + j];
+  for (int j = lane; j < dim_pad; j += 64) s_q[j] = j < a.dim ? a.q[static_cast<size_t>(o) * a.dim + j] : 0.0f;
   __syncthreads();
   const int64_t iv0 = a.iv[2 * o], iv1 = a.iv[2 * o + 1];
   const bool resid = a.preds[o].residual_mask != 0;
-  const bool listed = a.cand_n && a.cand_n[p] <= a.cand_cap;
+  const bool listed = LISTED && a.cand_n[p] <= a.cand_cap;
   int cnt = 0;
   uint64_t thr = kNoKey;
-  auto score = [&](int64_t row, bool ok) {
+  auto offer = [&](int64_t row, bool ok, float d) {
     uint64_t key = kNoKey;
     if (ok) {
-      const float* xr = a.xt + static_cast<size_t>(row >> 6) * a.dim * 64 + (row & 63);
-      float d = 0.0f;
-      // 16 values in flight, then added in j order
-      int j = 0;
-      for (; j + 16 <= a.dim; j += 16) {
-        float v[16];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) v[u] = xr[static_cast<size_t>(j + u) * 64];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) {
-          const float e = __fsub_rn(v[u], s_q[j + u]);
-          d = __fadd_rn(d, __fmul_rn(e, e));
-        }
-      }
-      for (; j < a.dim; ++j) {
-        const float e = __fsub_rn(xr[static_cast<size_t>(j) * 64], s_q[j]);
-        d = __fadd_rn(d, __fmul_rn(e, e));
-      }
       const uint32_t id = a.perm ? static_cast<uint32_t>(a.perm[row]) : static_cast<uint32_t>(row);
       key = (static_cast<uint64_t>(ordered_bits(d)) << 32) | id;
     }
@@ -384,7 +382,35 @@ __global__ __launch_bounds__(64) void exact_rerank_kernel(const RerankArgs a) {
     const int32_t* list = a.cand + static_cast<size_t>(p) * a.cand_cap;
     for (int64_t b = i0; b < i1; b += 64) {
       const int64_t i = b + lane;
-      score(i < i1 ? list[i] : 0, i < i1);
+      const bool ok = i < i1;
+      const int32_t row = ok ? list[i] : 0;
+      const uint64_t okm = __ballot(ok);
+      float d = 0.0f;
+      for (int j0 = 0; j0 < a.dim; j0 += kStageDims) {
+        const int nj = min(kStageDims, a.dim - j0);
+#pragma unroll
+        for (int r0 = 0; r0 < 64; r0 += 16) {
+          float v[16];
+#pragma unroll
+          for (int u = 0; u < 16; ++u) {
+            const int ri = __builtin_amdgcn_readlane(row, r0 + u);
+            const bool live = ((okm >> (r0 + u)) & 1) && lane < nj;
+            v[u] = live ? a.xr[static_cast<size_t>(ri) * a.dim + j0 + lane] : 0.0f;
+          }
+#pragma unroll
+          for (int u = 0; u < 16; ++u) s_x[(r0 + u) * (kStageDims + 1) + lane] = v[u];
+        }
+        wave_lds_fence();
+        if (ok) {
+          const float* xrow = s_x + lane * (kStageDims + 1);
+          for (int j = 0; j < nj; ++j) {
+            const float e = __fsub_rn(xrow[j], s_q[j0 + j]);
+            d = __fadd_rn(d, __fmul_rn(e, e));
+          }
+        }
+        wave_lds_fence();
+      }
+      offer(row, ok, d);
     }
   } else if (iv1 > iv0) {
     // 64-row tiles of the interval, dealt out in contiguous runs
@@ -395,7 +421,27 @@ __global__ __launch_bounds__(64) void exact_rerank_kernel(const RerankArgs a) {
       const int64_t row = t * 64 + lane;
       bool ok = row >= iv0 && row < iv1;
       if (ok && resid) ok = (a.bitmap[static_cast<size_t>(o) * a.stride64 + t] >> lane) & 1ull;
-      score(row, ok);
+      float d = 0.0f;
+      if (ok) {
+        const float* xr = a.xt + static_cast<size_t>(t) * a.dim * 64 + lane;
+        // 16 values in flight, then added in j order
+        int j = 0;
+        for (; j + 16 <= a.dim; j += 16) {
+          float v[16];
+#pragma unroll
+          for (int u = 0; u < 16; ++u) v[u] = xr[static_cast<size_t>(j + u) * 64];
+#pragma unroll
+          for (int u = 0; u < 16; ++u) {
+            const float e = __fsub_rn(v[u], s_q[j + u]);
+            d = __fadd_rn(d, __fmul_rn(e, e));
+          }
+        }
+        for (; j < a.dim; ++j) {
+          const float e = __fsub_rn(xr[static_cast<size_t>(j) * 64], s_q[j]);
+          d = __fadd_rn(d, __fmul_rn(e, e));
+        }
+      }
+      offer(row, ok, d);
     }
   }
   pool_compact(pool, cnt, thr, a.k, a.kpl);
@@ -413,11 +459,12 @@ const void* screen_symbol(int pass) {
 
 int exact_ksteps(int dim) { return (dim + 15) / 16; }
 
-hipError_t launch_exact_stage(const float* x, int64_t n, int dim, const int32_t* perm, float* xt, uint4* xb,
-                              float* xn, unsigned* max_norm_bits, unsigned long long* bad, hipStream_t s) {
+hipError_t launch_exact_stage(const float* x, int64_t n, int dim, const int32_t* perm, float* xt, float* xr,
+                              uint4* xb, float* xn, unsigned* max_norm_bits, unsigned long long* bad, hipStream_t s) {
   const int64_t n32 = (n + 31) / 32 * 32;
   const unsigned blocks = static_cast<unsigned>((n32 + 255) / 256);
-  exact_stage_kernel<<<blocks, 256, 0, s>>>(x, n, dim, exact_ksteps(dim), perm, xt, xb, xn, max_norm_bits, bad);
+  exact_stage_kernel<<<blocks, 256, 0, s>>>(x, n, dim, exact_ksteps(dim), perm, xt, xr, xb, xn, max_norm_bits,
+                                            bad);
   return hipGetLastError();
 }
 
@@ -477,6 +524,7 @@ int64_t exact_chunk_quantum() { return 32 * kExWaves; }
 hipError_t launch_exact_rerank(const ExactRerank& e, hipStream_t s) {
   RerankArgs a{};
   a.xt = e.xt;
+  a.xr = e.xr;
   a.dim = e.dim;
   a.q = e.q;
   a.qorder = e.qorder;
@@ -492,14 +540,17 @@ hipError_t launch_exact_rerank(const ExactRerank& e, hipStream_t s) {
   a.kpl = pool_kpl(e.k);
   a.chunks = e.chunks;
   a.partials = e.partials;
-  const size_t lds = static_cast<size_t>(64 * a.kpl) * sizeof(uint64_t) + static_cast<size_t>(e.dim) * sizeof(float);
+  const bool listed = e.cand_n != nullptr;
+  const int dim_pad = (e.dim + kStageDims - 1) / kStageDims * kStageDims;
+  const size_t lds = static_cast<size_t>(64 * a.kpl) * sizeof(uint64_t) +
+                     (static_cast<size_t>(dim_pad) + (listed ? 64 * (kStageDims + 1) : 0)) * sizeof(float);
   if (lds > static_cast<size_t>(kLdsBudget)) return hipErrorInvalidValue;
-  hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&exact_rerank_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+  const void* fn = listed ? reinterpret_cast<const void*>(&exact_rerank_kernel<true>)
+                          : reinterpret_cast<const void*>(&exact_rerank_kernel<false>);
+  hipError_t err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
   if (err != hipSuccess) return err;
   void* args[] = {&a};
-  return hipLaunchKernel(reinterpret_cast<const void*>(&exact_rerank_kernel),
-                         dim3(static_cast<unsigned>(e.chunks), static_cast<unsigned>(e.nq)), dim3(64), args, lds, s);
+  return hipLaunchKernel(fn, dim3(static_cast<unsigned>(e.chunks), static_cast<unsigned>(e.nq)), dim3(64), args, lds, s);
 }
 
 }  // namespace ifvs
