@@ -148,6 +148,25 @@ def scan_bytes_interval(w, sorted_attr, preds, plan, k, lut_entry):
             float((r1 - r0).sum()) * w.M)
 
 
+def exact_screen_bytes(w, sorted_attr, preds):
+    """Bytes one screening pass of the exact search reads: every row of each
+    32-query tile's hull (queries ordered by interval start, as the library
+    orders them) as bf16 matrix-core fragments plus its squared norm."""
+    lo = torch.tensor([p[0][1] for p in preds], device=sorted_attr.device, dtype=sorted_attr.dtype)
+    hi = torch.tensor([p[0][2] for p in preds], device=sorted_attr.device, dtype=sorted_attr.dtype)
+    r0 = torch.searchsorted(sorted_attr, lo)
+    r1 = torch.searchsorted(sorted_attr, hi)
+    order = torch.argsort(lo, stable=True)
+    r0, r1 = r0[order], r1[order]
+    rows = 0
+    for t in range(0, len(preds), 32):
+        a, b = r0[t:t + 32], r1[t:t + 32]
+        keep = b > a
+        if bool(keep.any()):
+            rows += int(b[keep].max() - a[keep].min())
+    return rows * (((w.D + 15) // 16) * 32 + 4)
+
+
 def scan_bytes_passing(idx, w, preds, lut_entry):
     """Bytes a scan of this batch must read at the least: the codes of every
     (query, passing row) pair and each query's table.  Used where clustered
@@ -420,6 +439,10 @@ def main():
             ms = [a.elapsed_time(c) for a, c in ms]
             ex_total += sum(ms)
             ex_bins[str(s)] = {"qps": batch * len(ms) / (sum(ms) / 1e3), "ms_per_batch": float(np.median(ms))}
+            if tile_bytes:
+                ex_bins[str(s)]["screen_bytes_per_pass"] = int(np.mean(
+                    [exact_screen_bytes(w, sorted_attr, w.preds[s][(i % n_batches) * batch:(i % n_batches + 1) * batch])
+                     for i in range(args.exact_steps)]))
             if str(s) in gt_all_ids:
                 nr_ = gt_all_ids[str(s)].shape[0]
                 clus.exact_search_into(w.queries[:batch], packed[s][0], k, ex_ids, ex_d)
