@@ -22,6 +22,9 @@ Aref; VLDB 2026 workshop) and cites the passage it follows:
 * Section 3.1 (workloads): the ground truth is the exact filtered top-k over
   the predicate-passing vectors; Section 3.2, pre-filtering baseline (i):
   exact L2 distances over the full-precision vectors of the candidate set.
+* Section 3.2, pre-filtering baselines (iv) and (v): symmetric distance
+  computation (SDC) -- the query is quantized too, and a candidate's
+  distance sums codeword-to-codeword distances.
 
 Readings taken where the paper is silent (all listed in the design notes):
 
@@ -77,6 +80,10 @@ __all__ = [
     "filtered_search",
     "exact_distances",
     "exact_filtered_search",
+    "encode_query",
+    "sdc_table",
+    "sdc_lut",
+    "sdc_filtered_search",
 ]
 
 KSUB = 256                      # codewords per subspace: 8-bit PQ codes
@@ -333,3 +340,62 @@ def exact_filtered_search(x, attrs, q, clauses, k, dtype=np.float32):
     d = exact_distances(x, q, ids, dtype)
     top_ids, top_d = select_topk(d, ids, k)
     return {"ids": top_ids, "dist": top_d, "n_pass": int(ids.shape[0])}
+
+
+# --------------------------------------------------------------------------
+# Symmetric distance computation (Section 3.2, pre-filtering baselines (iv)
+# and (v)): both the query and the data are quantized
+# --------------------------------------------------------------------------
+def encode_query(q, C_pq, dtype=np.float32):
+    """The query's PQ code: per subspace m, the codeword nearest to its
+    sub-vector by squared L2 (summed in j order from +0 in ``dtype``), the
+    lowest index among equal distances."""
+    q = np.asarray(q).astype(dtype)
+    C = np.asarray(C_pq).astype(dtype)
+    M, K, dsub = C.shape
+    codes = np.empty(M, dtype=np.int64)
+    for m in range(M):
+        acc = np.zeros(K, dtype=dtype)
+        for j in range(dsub):
+            e = q[m * dsub + j] - C[m, :, j]
+            acc = acc + e * e
+        codes[m] = int(np.argmin(acc))          # first minimum
+    return codes
+
+
+def sdc_table(C_pq, dtype=np.float32):
+    """Codeword-to-codeword squared distances of every subspace:
+    T[m][a][b] = sum_{j<dsub} (C[m][a][j] - C[m][b][j])^2, j order from +0."""
+    C = np.asarray(C_pq).astype(dtype)
+    M, K, dsub = C.shape
+    T = np.empty((M, K, K), dtype=dtype)
+    for m in range(M):
+        acc = np.zeros((K, K), dtype=dtype)
+        for j in range(dsub):
+            e = C[m, :, j][:, None] - C[m, :, j][None, :]
+            acc = acc + e * e
+        T[m] = acc
+    return T
+
+
+def sdc_lut(q, C_pq, dtype=np.float32, lut_dtype="f32", table=None):
+    """The query's symmetric distance table: LUT[m][c] = T[m][enc(q)_m][c],
+    so that summing LUT[m][code_v[m]] over m (adc_distances) gives the SDC
+    distance of v.  lut_dtype "f16" rounds it to binary16 as build_lut does."""
+    T = sdc_table(C_pq, dtype) if table is None else table
+    codes = encode_query(q, C_pq, dtype)
+    lut = T[np.arange(T.shape[0]), codes]
+    if lut_dtype == "f16":
+        return lut.astype(np.float32).astype(np.float16)
+    return lut
+
+
+def sdc_filtered_search(index: dict, q, clauses, k, lut_dtype="f32", dtype=np.float32, table=None):
+    """Filter, then rank the pool by SDC distance (ascending, ties to the
+    smaller id), padded to k with (-1, +inf)."""
+    codes = np.asarray(index["codes"])
+    lut = sdc_lut(q, index["C_pq"], dtype, lut_dtype, table)
+    ids = passing_ids(predicate_mask(index["attrs"], clauses))
+    d = adc_distances(lut, codes, ids, dtype)
+    top_ids, top_d = select_topk(d, ids, k)
+    return {"lut": lut, "ids": top_ids, "dist": top_d, "n_pass": int(ids.shape[0])}

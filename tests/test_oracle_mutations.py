@@ -27,6 +27,9 @@ MUTATIONS = [
     ("fingerprint_no_clauses", "out.append(struct.pack(\"<iqq\", int(col), int(lo), int(hi)))", "pass"),
     ("exact_abs_not_square", "        d = d + e * e\n", "        d = d + np.abs(e)\n"),
     ("exact_drops_last_dim", "    for j in range(x.shape[1]):\n        e = x[ids, j]", "    for j in range(x.shape[1] - 1):\n        e = x[ids, j]"),
+    ("sdc_encode_last_minimum", "        codes[m] = int(np.argmin(acc))          # first minimum", "        codes[m] = int(K - 1 - np.argmin(acc[::-1]))"),
+    ("sdc_table_transposed_subspace", "            e = C[m, :, j][:, None] - C[m, :, j][None, :]", "            e = C[m, :, j][:, None] - C[(m + 1) % M, :, j][None, :]"),
+    ("sdc_lut_data_row", "    lut = T[np.arange(T.shape[0]), codes]", "    lut = T[np.arange(T.shape[0]), (codes + 1) % T.shape[1]]"),
     ("exact_query_index_shift", "        e = x[ids, j].astype(dtype) - q[j]", "        e = x[ids, j].astype(dtype) - q[(j + 1) % q.shape[0]]"),
 ]
 

@@ -395,3 +395,72 @@ def test_exact_search_ties_go_to_the_smaller_id():
     attrs = np.zeros((1, 6), dtype=np.int32)
     res = O.exact_filtered_search(x, attrs, np.ones(4, dtype=np.float32), [], 4)
     assert list(res["ids"]) == [1, 4, 5, 0]
+
+
+# ------------------------------------------------------------------- SDC
+def test_sdc_table_is_library_codeword_distances():
+    """Symmetric with a zero diagonal, and within the fp32 bound of scipy's
+    fp64 squared distances between codewords."""
+    rng = np.random.default_rng(41)
+    C = rng.standard_normal((3, 256, 5)).astype(np.float32)
+    T = O.sdc_table(C)
+    for m in range(3):
+        assert np.array_equal(T[m], T[m].T) and np.all(np.diag(T[m]) == 0)
+        ref = cdist(C[m].astype(np.float64), C[m].astype(np.float64), "sqeuclidean")
+        assert np.all(np.abs(T[m] - ref) <= (2 * 5 + 2) * U32 * ref)
+
+
+def test_encode_query_is_nearest_codeword():
+    rng = np.random.default_rng(42)
+    M, dsub = 4, 6
+    C = rng.standard_normal((M, 256, dsub)).astype(np.float32)
+    for t in range(20):
+        q = rng.standard_normal(M * dsub).astype(np.float32)
+        codes = O.encode_query(q, C)
+        for m in range(M):
+            d = cdist(q[None, m * dsub:(m + 1) * dsub].astype(np.float64), C[m].astype(np.float64), "sqeuclidean")[0]
+            assert codes[m] == int(np.argmin(d))
+    # equal distances: the lower index
+    C2 = np.zeros((1, 256, 2), dtype=np.float32)
+    C2[0, 7] = [1, 0]
+    C2[0, 3] = [0, 1]
+    C2[0, 1:] += 50
+    C2[0, 7] = [1, 0]
+    C2[0, 3] = [0, 1]
+    assert O.encode_query(np.zeros(2, dtype=np.float32), C2)[0] == 0       # codeword 0 is (0, 0)
+    C2[0, 0] = [9, 9]
+    assert O.encode_query(np.zeros(2, dtype=np.float32), C2)[0] == 3       # 3 and 7 tie at 1: lower index
+
+
+def test_sdc_at_a_reconstruction_is_identity_adc():
+    """A query equal to the reconstruction of codes c*: its code is c* and its
+    SDC table is the identity-mode ADC table, bit for bit."""
+    rng = np.random.default_rng(43)
+    M, dsub = 8, 4
+    C = rng.standard_normal((M, 256, dsub)).astype(np.float32)
+    cstar = rng.integers(0, 256, M)
+    q = np.concatenate([C[m, cstar[m]] for m in range(M)])
+    assert list(O.encode_query(q, C)) == list(cstar)
+    adc = O.build_lut(q, None, None, C, None, M, 0)
+    assert np.array_equal(O.sdc_lut(q, C).view(np.uint32), adc.view(np.uint32))
+
+
+def test_sdc_distance_is_distance_between_reconstructions():
+    rng = np.random.default_rng(44)
+    N, M, dsub = 300, 6, 3
+    C = rng.standard_normal((M, 256, dsub)).astype(np.float32)
+    codes = rng.integers(0, 256, (N, M)).astype(np.uint8)
+    attrs = rng.integers(0, 10, (1, N), dtype=np.int32)
+    index = dict(codes=codes, C_pq=C, attrs=attrs)
+    rec = lambda c: np.concatenate([C[m, c[m]] for m in range(M)]).astype(np.float64)
+    for t in range(6):
+        q = rng.standard_normal(M * dsub).astype(np.float32)
+        res = O.sdc_filtered_search(index, q, [(0, 2, 8)], 5)
+        qc = O.encode_query(q, C)
+        keep = np.flatnonzero((attrs[0] >= 2) & (attrs[0] < 8))
+        d64 = np.array([((rec(qc) - rec(codes[v])) ** 2).sum() for v in keep])
+        order = keep[np.lexsort((keep, d64))][:5]
+        assert list(res["ids"]) == list(order)
+        got = res["dist"].astype(np.float64)
+        ref = np.sort(d64)[:5]
+        assert np.all(np.abs(got - ref) <= 1e-5 * ref + 1e-6)
