@@ -212,6 +212,9 @@ def main():
     ap.add_argument("--exact-steps", type=int, default=None,
                     help="batches per bin timed for exact filtered kNN over the full-precision vectors "
                          "(ifvs_exact_search; 0 = skip; default 4, 0 on c5)")
+    ap.add_argument("--sdc-steps", type=int, default=4,
+                    help="batches per bin timed with symmetric distance tables (ifvs_build_sdc_lut + the "
+                         "same scan; 0 = skip)")
     ap.add_argument("--lut", choices=["f32", "f16"], default="f32")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain copy kernel of known size (for counter calibration)")
@@ -394,8 +397,10 @@ def main():
         preds = w.preds[s][:nr]
         t_np = gt_all[s].cpu().numpy()
         gt_all_ids[str(s)] = gt_all[s]
-        for mode in ("identity", "conditioned"):
-            if mode == "identity":
+        for mode in ("identity", "conditioned", "sdc"):
+            if mode == "sdc":
+                lt = clus.build_sdc_lut(q, lut_dt)
+            elif mode == "identity":
                 lt = clus.build_lut(q, None, None, lut_dt)
             else:
                 a_, f_ = clus.select_codebook(q, preds, w.w_z[s][:nr])
@@ -409,6 +414,34 @@ def main():
                     hits += len(truth & set(int(v) for v in g_np[i] if v >= 0)) / len(truth)
             bins_out[str(s)][f"recall@{k}_{mode}"] = round(hits / nr, 4)
     log(f"[bench] bins: {json.dumps(bins_out)}")
+
+    # Symmetric distance computation (Section 3.2, pre-filtering baselines
+    # (iv)/(v)): the query is quantized too; its codeword-distance table
+    # feeds the same scan.
+    sdc_out = None
+    if args.sdc_steps > 0:
+        sdc_bins, sdc_total = {}, 0.0
+        for s in bins:
+            clus.build_sdc_lut_into(w.queries[:batch], lut_dt, lut)
+            clus.search_into(batch, packed[s][0], lut, lut_dt, k, ids[s], dist[s])      # warmup
+            ev_ = []
+            for i in range(args.sdc_steps):
+                b = i % n_batches
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                clus.build_sdc_lut_into(w.queries[b * batch:(b + 1) * batch], lut_dt, lut)
+                clus.search_into(batch, packed[s][b], lut, lut_dt, k, ids[s], dist[s])
+                e1.record(stream)
+                ev_.append((e0, e1))
+            torch.cuda.synchronize()
+            ms = [a_.elapsed_time(c_) for a_, c_ in ev_]
+            sdc_total += sum(ms)
+            sdc_bins[str(s)] = {"qps": batch * len(ms) / (sum(ms) / 1e3), "ms_per_batch": float(np.median(ms))}
+            if f"recall@{k}_sdc" in bins_out[str(s)]:
+                sdc_bins[str(s)][f"recall@{k}"] = bins_out[str(s)][f"recall@{k}_sdc"]
+        sdc_out = {"qps": args.sdc_steps * len(bins) * batch / (sdc_total / 1e3), "steps": args.sdc_steps,
+                   "bins": sdc_bins}
+        log(f"[bench] SDC: {sdc_out['qps']:.0f} queries/s; {json.dumps(sdc_bins)}")
 
     # Exact filtered kNN over the full-precision vectors (Section 3.2's
     # pre-filtering baseline (i), the ground truth of Section 3.1): whole
@@ -526,6 +559,7 @@ def main():
                      "useful_bytes_per_launch": useful_total / max(1, scan_launches)},
         "plain_layout": plain_out,
         "exact_search": exact_out,
+        "sdc": sdc_out,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -163,6 +163,23 @@ ifvs_status ifvs_select_codebook(ifvs_index* idx, int32_t nq, const float* q,
 ifvs_status ifvs_build_lut(ifvs_index* idx, int32_t nq, const float* q, const float* alpha,
                            const float* wf, int32_t lut_dtype, void* lut_out, void* stream);
 
+/* ifvs_build_sdc_lut -- the symmetric distance table of each query, for the
+ * pre-filtering SDC baselines (iv) and (v) of Section 3.2: the query is
+ * quantized with the index's codebook C_PQ,
+ *   code[m]     = the c minimizing sum_{j<d} (q[m*d+j] - C_PQ[m][c][j])^2
+ *                 (fp32, j order from +0; the lowest c among equals),
+ * and LUT[m][c] = T[m][code[m]][c] with the codeword-to-codeword distances
+ *   T[m][a][b]  = sum_{j<d} (C_PQ[m][a][j] - C_PQ[m][b][j])^2
+ * (fp32, j order from +0; built once by ifvs_load_index).  Passed to
+ * ifvs_filtered_search it ranks the pool by SDC distance.
+ *  q:         device [nq][dim] fp32
+ *  lut_dtype: IFVS_LUT_F32 or IFVS_LUT_F16 (as ifvs_build_lut)
+ *  lut_out:   device [nq][m][256]
+ * Errors: IFVS_E_INVALID (nq, NULL q / lut_out, unknown dtype), IFVS_E_STATE,
+ * IFVS_E_HIP. */
+ifvs_status ifvs_build_sdc_lut(ifvs_index* idx, int32_t nq, const float* q, int32_t lut_dtype, void* lut_out,
+                               void* stream);
+
 /* ifvs_filter -- the Filter stage alone (Section 2, stage 1): selection
  * bitmaps and pool sizes.
  *  preds:      HOST [nq]

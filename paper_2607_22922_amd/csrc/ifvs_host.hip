@@ -86,6 +86,7 @@ struct ifvs_index {
 
   uint32_t* codes_t = nullptr;   // [n_tiles][mw][64] code words, physical row order
   float* cpq = nullptr;          // [m][256][dsub]
+  float* sdc = nullptr;          // [m][256][256] codeword-to-codeword squared distances
   int32_t* attrs = nullptr;      // [n_attr][n] original id order
   int32_t* attrs_phys = nullptr; // [n_attr][n] physical order (== attrs when not clustered)
   // Leading cluster key value table: vstart[t] = first physical row whose key
@@ -190,7 +191,8 @@ struct ifvs_index {
       delete[] timers;
     }
     if (attrs_phys && attrs_phys != attrs) hipFree(attrs_phys);
-    for (void* p : {static_cast<void*>(codes_t), static_cast<void*>(cpq), static_cast<void*>(attrs),
+    for (void* p : {static_cast<void*>(codes_t), static_cast<void*>(cpq), static_cast<void*>(sdc),
+                    static_cast<void*>(attrs),
                     static_cast<void*>(perm), static_cast<void*>(bank), static_cast<void*>(W),
                     static_cast<void*>(preds_dev), static_cast<void*>(qorder_dev),
                     static_cast<void*>(iv_dev), static_cast<void*>(gthr_dev), static_cast<void*>(bitmap),
@@ -742,6 +744,10 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
   if ((st = dev_alloc(&idx->cpq, cb, "codebook")) != IFVS_OK) return bail(st);
   if (hipError_t e = hipMemcpy(idx->cpq, d.codebook, cb * sizeof(float), kind); e != hipSuccess)
     return bail(hip_fail(e, "loading codebook"));
+  if ((st = dev_alloc(&idx->sdc, static_cast<size_t>(d.m) * kKsub * kKsub, "codeword distance table")) != IFVS_OK)
+    return bail(st);
+  if (hipError_t e = launch_sdc_table(idx->cpq, d.m, idx->dsub, idx->sdc, 0); e != hipSuccess)
+    return bail(hip_fail(e, "building the codeword distance table"));
   if (d.bank_rows > 0) {
     const size_t nb = static_cast<size_t>(d.bank_rows) * d.m * d.r;
     const size_t nw = static_cast<size_t>(d.m) * d.r * kKsub * idx->dsub;
@@ -877,6 +883,20 @@ ifvs_status ifvs_build_lut(ifvs_index* idx, int32_t nq, const float* q, const fl
   IFVS_LAUNCH(idx, kStLut, s, "launching LUT kernel",
               launch_build_lut(q, idx->dim, idx->m, idx->dsub, idx->r, idx->cpq, idx->W, alpha, wf,
                                nq, lut_dtype, lut_out, s));
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_build_sdc_lut(ifvs_index* idx, int32_t nq, const float* q, int32_t lut_dtype, void* lut_out,
+                               void* stream) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
+  if (lut_dtype != IFVS_LUT_F32 && lut_dtype != IFVS_LUT_F16) return fail(IFVS_E_INVALID, "unknown lut_dtype");
+  if (nq == 0) return IFVS_OK;
+  if (!q || !lut_out) return fail(IFVS_E_INVALID, "q or lut_out is NULL");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  IFVS_LAUNCH(idx, kStLut, s, "launching SDC table kernel",
+              launch_sdc_lut(q, idx->dim, idx->m, idx->dsub, idx->cpq, idx->sdc, nq, lut_dtype, lut_out, s));
   return IFVS_OK;
 }
 

@@ -189,6 +189,13 @@ hipError_t launch_topk_merge(const uint64_t* partials, int nq, int64_t per_query
                              const int32_t* qorder, int32_t* ids_out, float* dist_out,
                              hipStream_t s);
 
+// Symmetric distance computation (k_sdc.hip): the codeword table
+// T[m][a][b] (at load) and a query's table, the rows T[m][enc(q)_m] laid
+// out as [nq][m][256] fp32 (lut_dtype 0) or binary16 (1).
+hipError_t launch_sdc_table(const float* cpq, int m, int dsub, float* T, hipStream_t s);
+hipError_t launch_sdc_lut(const float* q, int dim, int m, int dsub, const float* cpq, const float* T, int nq,
+                          int lut_dtype, void* lut_out, hipStream_t s);
+
 // Exact filtered kNN over the full-precision vectors (k_exact.hip).
 int exact_ksteps(int dim);                 // 16-dimension MFMA steps
 int64_t exact_bins_per_query(int splits, int bin_lanes);  // pass-1 values per query position

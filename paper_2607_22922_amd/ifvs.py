@@ -31,7 +31,8 @@ STAGES = ("condition", "lut", "filter", "scan", "merge")
 
 EXPORTED = ("ifvs_load_index", "ifvs_free_index", "ifvs_select_codebook", "ifvs_build_lut",
             "ifvs_filter", "ifvs_filtered_search", "ifvs_set_option", "ifvs_last_plan",
-            "ifvs_read_profile", "ifvs_last_error", "ifvs_load_vectors", "ifvs_exact_search")
+            "ifvs_read_profile", "ifvs_last_error", "ifvs_load_vectors", "ifvs_exact_search",
+            "ifvs_build_sdc_lut")
 
 
 class IfvsError(RuntimeError):
@@ -92,6 +93,7 @@ def _load_library() -> ctypes.CDLL:
         "ifvs_read_profile": ([vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)], i32),
         "ifvs_last_error": ([], ctypes.c_char_p),
         "ifvs_load_vectors": ([vp, vp, i32], i32),
+        "ifvs_build_sdc_lut": ([vp, i32, vp, i32, vp, vp], i32),
         "ifvs_exact_search": ([vp, i32, vp, vp, i32, vp, vp, vp], i32),
     }
     for name, (args, res) in sig.items():
@@ -224,6 +226,10 @@ class Index:
         _check(_lib.ifvs_build_lut(self.handle, q.shape[0], q.data_ptr(), _ptr(alpha), _ptr(wf),
                                    lut_dtype, lut_out.data_ptr(), _stream(stream)))
 
+    def build_sdc_lut_into(self, q, lut_dtype, lut_out, stream=None):
+        _check(_lib.ifvs_build_sdc_lut(self.handle, q.shape[0], q.data_ptr(), lut_dtype, lut_out.data_ptr(),
+                                       _stream(stream)))
+
     def filter_into(self, nq, preds_c, bitmap_out, count_out=None, stream=None):
         _check(_lib.ifvs_filter(self.handle, nq, preds_c, bitmap_out.data_ptr(), _ptr(count_out),
                                 _stream(stream)))
@@ -264,6 +270,15 @@ class Index:
         dt = torch.float16 if lut_dtype == LUT_F16 else torch.float32
         lut = torch.empty(nq, self.m, KSUB, device=self.device, dtype=dt)
         self.build_lut_into(q, alpha, wf, lut_dtype, lut)
+        return lut
+
+    def build_sdc_lut(self, q, lut_dtype=LUT_F32):
+        """Symmetric distance tables (query quantized with the codebook)."""
+        nq = q.shape[0]
+        q = _dev_f32(q, self.device)
+        dt = torch.float16 if lut_dtype == LUT_F16 else torch.float32
+        lut = torch.empty(nq, self.m, KSUB, device=self.device, dtype=dt)
+        self.build_sdc_lut_into(q, lut_dtype, lut)
         return lut
 
     def filter(self, preds):
