@@ -22,6 +22,9 @@ Aref; VLDB 2026 workshop) and cites the passage it follows:
 * Section 3.1 (workloads): the ground truth is the exact filtered top-k over
   the predicate-passing vectors; Section 3.2, pre-filtering baseline (i):
   exact L2 distances over the full-precision vectors of the candidate set.
+* Section 3.2, pre-filtering baseline (ii): vectors reconstructed from their
+  PQ codes, then exact L2 distances (exact filtered kNN over the
+  reconstructions).
 * Section 3.2, pre-filtering baselines (iv) and (v): symmetric distance
   computation (SDC) -- the query is quantized too, and a candidate's
   distance sums codeword-to-codeword distances.
@@ -80,6 +83,7 @@ __all__ = [
     "filtered_search",
     "exact_distances",
     "exact_filtered_search",
+    "reconstruct",
     "encode_query",
     "sdc_table",
     "sdc_lut",
@@ -340,6 +344,18 @@ def exact_filtered_search(x, attrs, q, clauses, k, dtype=np.float32):
     d = exact_distances(x, q, ids, dtype)
     top_ids, top_d = select_topk(d, ids, k)
     return {"ids": top_ids, "dist": top_d, "n_pass": int(ids.shape[0])}
+
+
+# --------------------------------------------------------------------------
+# Reconstruction from PQ codes (Section 3.2, pre-filtering baseline (ii):
+# reconstruct, then exact_filtered_search over the reconstructions)
+# --------------------------------------------------------------------------
+def reconstruct(codes, C_pq):
+    """x_hat[v] = concatenation over m of codeword C_pq[m][codes[v][m]]."""
+    codes = np.asarray(codes).astype(np.int64)
+    C = np.asarray(C_pq)
+    M = C.shape[0]
+    return np.concatenate([C[m][codes[:, m]] for m in range(M)], axis=1)
 
 
 # --------------------------------------------------------------------------

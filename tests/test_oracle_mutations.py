@@ -30,6 +30,7 @@ MUTATIONS = [
     ("sdc_encode_last_minimum", "        codes[m] = int(np.argmin(acc))          # first minimum", "        codes[m] = int(K - 1 - np.argmin(acc[::-1]))"),
     ("sdc_table_transposed_subspace", "            e = C[m, :, j][:, None] - C[m, :, j][None, :]", "            e = C[m, :, j][:, None] - C[(m + 1) % M, :, j][None, :]"),
     ("sdc_lut_data_row", "    lut = T[np.arange(T.shape[0]), codes]", "    lut = T[np.arange(T.shape[0]), (codes + 1) % T.shape[1]]"),
+    ("reconstruct_wrong_subspace", "    return np.concatenate([C[m][codes[:, m]] for m in range(M)], axis=1)", "    return np.concatenate([C[m][codes[:, (m + 1) % M]] for m in range(M)], axis=1)"),
     ("exact_query_index_shift", "        e = x[ids, j].astype(dtype) - q[j]", "        e = x[ids, j].astype(dtype) - q[(j + 1) % q.shape[0]]"),
 ]
 

@@ -464,3 +464,27 @@ def test_sdc_distance_is_distance_between_reconstructions():
         got = res["dist"].astype(np.float64)
         ref = np.sort(d64)[:5]
         assert np.all(np.abs(got - ref) <= 1e-5 * ref + 1e-6)
+
+
+# --------------------------------------------------- reconstruct-then-exact
+def test_reconstruction_written_out_and_exact_over_it():
+    """x_hat of one row by hand; exact search over reconstructions ranks like
+    identity-mode ADC (both are squared L2 to x_hat, summed in different
+    orders) and returns distance 0 for a query equal to a reconstruction."""
+    rng = np.random.default_rng(51)
+    M, dsub, N = 4, 3, 400
+    C = rng.standard_normal((M, 256, dsub)).astype(np.float32)
+    codes = rng.integers(0, 256, (N, M)).astype(np.uint8)
+    xh = O.reconstruct(codes, C)
+    v = 17
+    assert np.array_equal(xh[v], np.concatenate([C[0, codes[v, 0]], C[1, codes[v, 1]],
+                                                 C[2, codes[v, 2]], C[3, codes[v, 3]]]))
+    attrs = rng.integers(0, 8, (1, N), dtype=np.int32)
+    index = dict(codes=codes, C_pq=C, attrs=attrs)
+    for t in range(8):
+        q = rng.standard_normal(M * dsub).astype(np.float32)
+        a = O.filtered_search(index, q, [(0, 1, 6)], 7, conditioned=False)
+        b = O.exact_filtered_search(xh, attrs, q, [(0, 1, 6)], 7)
+        assert list(a["ids"]) == list(b["ids"])
+    res = O.exact_filtered_search(xh, attrs, xh[v], [], 1)
+    assert res["ids"][0] == v and res["dist"][0] == 0.0
