@@ -230,6 +230,16 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
  * attached), IFVS_E_NOMEM, IFVS_E_HIP. */
 ifvs_status ifvs_load_vectors(ifvs_index* idx, const float* x, int32_t mem_kind);
 
+/* ifvs_load_reconstructions -- attach, in place of full-precision vectors,
+ * the reconstructions of the index's own codes: row i becomes the
+ * concatenation over m of codeword C_PQ[m][code_i[m]].  ifvs_exact_search
+ * then ranks by exact L2 to the reconstructions -- the pre-filtering
+ * baseline (ii) of Section 3.2 (reconstruct from PQ codes, then exact L2).
+ * Same memory and workspace as ifvs_load_vectors.
+ * Errors: IFVS_E_STATE (NULL handle, or vectors already attached),
+ * IFVS_E_NOMEM, IFVS_E_HIP. */
+ifvs_status ifvs_load_reconstructions(ifvs_index* idx);
+
 /* ifvs_exact_search -- exact filtered kNN (Section 3.1 ground truth; Section
  * 3.2 pre-filtering baseline (i)).  For each query q: the pool P_q of
  * vectors whose attributes satisfy preds[q] (as in ifvs_filter), ranked by

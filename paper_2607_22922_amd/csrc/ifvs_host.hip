@@ -1045,12 +1045,14 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   return IFVS_OK;
 }
 
-ifvs_status ifvs_load_vectors(ifvs_index* idx, const float* x, int32_t mem_kind) {
-  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
-  if (idx->xr) return fail(IFVS_E_STATE, "vectors are already attached to this index");
-  if (!x) return fail(IFVS_E_INVALID, "x is NULL");
-  if (mem_kind != IFVS_MEM_HOST && mem_kind != IFVS_MEM_DEVICE) return fail(IFVS_E_INVALID, "unknown mem_kind");
-  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+}  // extern "C"
+
+namespace {
+
+// Attach vectors to the index for the exact search: src is device memory
+// [n][dim]; src_perm maps physical row r to its row of src (null: src is in
+// physical order already).  Allocates the copies and the workspace.
+ifvs_status attach_vectors(ifvs_index* idx, const float* src, const int32_t* src_perm) {
   const int64_t n = idx->n, n32 = (n + 31) / 32 * 32;
   const int dim = idx->dim, ks = exact_ksteps(dim);
   auto bail = [&](ifvs_status st) {
@@ -1087,26 +1089,60 @@ ifvs_status ifvs_load_vectors(ifvs_index* idx, const float* x, int32_t mem_kind)
   if ((st = dev_alloc(&idx->partials_x, static_cast<size_t>(max_batch) * idx->exact_chunks_max * idx->max_k,
                       "exact top-k partials")) != IFVS_OK)
     return bail(st);
-  const float* src = x;
-  float* staged = nullptr;
-  if (mem_kind == IFVS_MEM_HOST) {
-    if ((st = dev_alloc(&staged, static_cast<size_t>(n) * dim, "vector staging")) != IFVS_OK) return bail(st);
-    if (hipError_t e = hipMemcpy(staged, x, sizeof(float) * n * dim, hipMemcpyHostToDevice); e != hipSuccess) {
-      hipFree(staged);
-      return bail(hip_fail(e, "copying vectors"));
-    }
-    src = staged;
-  }
   hipError_t e = hipMemset(idx->xmax, 0, sizeof(unsigned));
   if (e == hipSuccess) e = hipMemset(idx->xbad, 0, sizeof(unsigned long long));
-  if (e == hipSuccess) e = launch_exact_stage(src, n, dim, idx->perm, idx->xt, idx->xr, idx->xb, idx->xn, idx->xmax, idx->xbad, 0);
+  if (e == hipSuccess)
+    e = launch_exact_stage(src, n, dim, src_perm, idx->xt, idx->xr, idx->xb, idx->xn, idx->xmax, idx->xbad, 0);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   unsigned long long bad = 0;
   if (e == hipSuccess) e = hipMemcpy(&bad, idx->xbad, sizeof(bad), hipMemcpyDeviceToHost);
-  if (staged) hipFree(staged);
   if (e != hipSuccess) return bail(hip_fail(e, "staging vectors"));
   if (bad) return bail(fail(IFVS_E_INVALID, std::to_string(bad) + " vector values are NaN or infinite"));
   return IFVS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ifvs_status ifvs_load_vectors(ifvs_index* idx, const float* x, int32_t mem_kind) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (idx->xr) return fail(IFVS_E_STATE, "vectors are already attached to this index");
+  if (!x) return fail(IFVS_E_INVALID, "x is NULL");
+  if (mem_kind != IFVS_MEM_HOST && mem_kind != IFVS_MEM_DEVICE) return fail(IFVS_E_INVALID, "unknown mem_kind");
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  const float* src = x;
+  float* staged = nullptr;
+  if (mem_kind == IFVS_MEM_HOST) {
+    if (ifvs_status st = dev_alloc(&staged, static_cast<size_t>(idx->n) * idx->dim, "vector staging"); st != IFVS_OK)
+      return st;
+    if (hipError_t e = hipMemcpy(staged, x, sizeof(float) * idx->n * idx->dim, hipMemcpyHostToDevice);
+        e != hipSuccess) {
+      hipFree(staged);
+      return hip_fail(e, "copying vectors");
+    }
+    src = staged;
+  }
+  const ifvs_status st = attach_vectors(idx, src, idx->perm);
+  if (staged) hipFree(staged);
+  return st;
+}
+
+ifvs_status ifvs_load_reconstructions(ifvs_index* idx) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (idx->xr) return fail(IFVS_E_STATE, "vectors are already attached to this index");
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  float* rec = nullptr;
+  if (ifvs_status st = dev_alloc(&rec, static_cast<size_t>(idx->n) * idx->dim, "reconstructions"); st != IFVS_OK)
+    return st;
+  if (hipError_t e = launch_decode(idx->codes_t, idx->n, idx->m, idx->mw, idx->dsub, idx->cpq, rec, 0);
+      e != hipSuccess) {
+    hipFree(rec);
+    return hip_fail(e, "decoding codes");
+  }
+  const ifvs_status st = attach_vectors(idx, rec, nullptr);   // already in physical order
+  hipFree(rec);
+  return st;
 }
 
 ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const ifvs_predicate* preds, int32_t k,

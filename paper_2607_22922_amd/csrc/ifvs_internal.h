@@ -208,6 +208,10 @@ int64_t exact_chunk_quantum();             // screening chunks are multiples of 
 // starts at 0).
 hipError_t launch_exact_stage(const float* x, int64_t n, int dim, const int32_t* perm, float* xt, float* xr,
                               uint4* xb, float* xn, unsigned* max_norm_bits, unsigned long long* bad, hipStream_t s);
+// Reconstructions x[r][m * dsub + j] = C_PQ[m][code of physical row r][j]
+// (physical row order) from the 64-row code tiles.
+hipError_t launch_decode(const uint32_t* codes_t, int64_t n, int m, int mw, int dsub, const float* cpq, float* x,
+                         hipStream_t s);
 // Query fragments (ceil(nq/32) tiles), |q|^2, error bounds; clears cand_n.
 hipError_t launch_exact_queries(const float* q, int dim, int nq, const int32_t* qorder, const unsigned* max_norm_bits,
                                 uint4* qb, float* qn, float* eps, int32_t* cand_n, hipStream_t s);

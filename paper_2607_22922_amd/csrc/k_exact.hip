@@ -455,7 +455,30 @@ const void* screen_symbol(int pass) {
                    : reinterpret_cast<const void*>(&exact_screen_kernel<2, KS>);
 }
 
+// Reconstruction from the codes (the reconstruct-then-exact baseline (ii) of
+// Section 3.2): physical row r, dimension m * dsub + j, is codeword
+// C_PQ[m][code_r[m]][j]; one thread per (row, subspace).
+__global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict__ codes_t, int64_t n, int M, int mw,
+                                                     int dsub, const float* __restrict__ cpq, float* __restrict__ x) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= n * M) return;
+  const int64_t r = i / M;
+  const int m = static_cast<int>(i % M);
+  const uint32_t word = codes_t[((r >> 6) * mw + (m >> 2)) * 64 + (r & 63)];
+  const int code = static_cast<int>((word >> (8 * (m & 3))) & 0xFFu);
+  const float* c = cpq + (static_cast<size_t>(m) * kKsub + code) * dsub;
+  float* dst = x + static_cast<size_t>(r) * M * dsub + static_cast<size_t>(m) * dsub;
+  for (int j = 0; j < dsub; ++j) dst[j] = c[j];
+}
+
 }  // namespace
+
+hipError_t launch_decode(const uint32_t* codes_t, int64_t n, int m, int mw, int dsub, const float* cpq, float* x,
+                         hipStream_t s) {
+  const int64_t total = n * m;
+  decode_kernel<<<static_cast<unsigned>((total + 255) / 256), 256, 0, s>>>(codes_t, n, m, mw, dsub, cpq, x);
+  return hipGetLastError();
+}
 
 int exact_ksteps(int dim) { return (dim + 15) / 16; }
 

@@ -32,7 +32,7 @@ STAGES = ("condition", "lut", "filter", "scan", "merge")
 EXPORTED = ("ifvs_load_index", "ifvs_free_index", "ifvs_select_codebook", "ifvs_build_lut",
             "ifvs_filter", "ifvs_filtered_search", "ifvs_set_option", "ifvs_last_plan",
             "ifvs_read_profile", "ifvs_last_error", "ifvs_load_vectors", "ifvs_exact_search",
-            "ifvs_build_sdc_lut")
+            "ifvs_build_sdc_lut", "ifvs_load_reconstructions")
 
 
 class IfvsError(RuntimeError):
@@ -94,6 +94,7 @@ def _load_library() -> ctypes.CDLL:
         "ifvs_last_error": ([], ctypes.c_char_p),
         "ifvs_load_vectors": ([vp, vp, i32], i32),
         "ifvs_build_sdc_lut": ([vp, i32, vp, i32, vp, vp], i32),
+        "ifvs_load_reconstructions": ([vp], i32),
         "ifvs_exact_search": ([vp, i32, vp, vp, i32, vp, vp, vp], i32),
     }
     for name, (args, res) in sig.items():
@@ -245,6 +246,10 @@ class Index:
         x = x.to(dtype=torch.float32).contiguous()
         _check(_lib.ifvs_load_vectors(self.handle, x.data_ptr(),
                                       MEM_DEVICE if x.device.type == "cuda" else MEM_HOST))
+
+    def load_reconstructions(self):
+        """Attach the reconstructions of the codes (ifvs_load_reconstructions)."""
+        _check(_lib.ifvs_load_reconstructions(self.handle))
 
     def exact_search_into(self, q, preds_c, k, ids_out, dist_out, stream=None):
         _check(_lib.ifvs_exact_search(self.handle, q.shape[0], q.data_ptr(), preds_c, k,

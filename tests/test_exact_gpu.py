@@ -2,7 +2,8 @@
 against the CPU oracle: ids and distance bits equal on every query, for both
 plans (direct exact scoring; matrix-core screening followed by exact
 scoring), both row layouts, residual clauses, empty pools, pools smaller
-than k, ties, ragged dimensions, and the 10M-vector workload by sampling."""
+than k, ties, ragged dimensions, the 10M-vector workload by sampling, and
+the same search over the reconstructions of the codes."""
 import numpy as np
 import pytest
 import torch
@@ -182,3 +183,26 @@ def test_exact_search_c4_10m_sampled(B):
         for i in (0, 131):
             res = O.exact_filtered_search(xh, ah, _np(w.queries[i]), w.preds[s][i], 10)
             check_search_row(ids[i], dist[i], res["ids"], res["dist"], f"c4 s={s} q{i}")
+
+
+@pytest.mark.parametrize("cluster_cols", [(), (0,)])
+@pytest.mark.parametrize("plan", [1, 2])
+def test_reconstruct_then_exact_matches_oracle(B, cluster_cols, plan):
+    """Exact search over the reconstructions of the codes (the
+    reconstruct-then-exact baseline) against the oracle's reconstruct +
+    exact_filtered_search."""
+    say(f"[exact] reconstructions cols={cluster_cols} plan={plan}")
+    w = make_workload("c1", device="cuda", n_queries=40)
+    idx = B.Index.from_workload(w, max_batch=40, max_k=w.k, cluster_cols=cluster_cols)
+    idx.load_reconstructions()
+    idx.set_option(B.OPT_EXACT_PLAN, plan)
+    xh = O.reconstruct(_np(w.codes), _np(w.C_pq))
+    preds = w.preds[w.bins[0]][:36] + [[], [(0, 3, 3)], [(0, 0, 1000)], [(0, 500, 501)]]
+    ids, dist = idx.exact_search(w.queries, preds, w.k)
+    torch.cuda.synchronize()
+    ids, dist = _np(ids), _np(dist)
+    for i, p in enumerate(preds):
+        res = O.exact_filtered_search(xh, _np(w.attrs), _np(w.queries[i]), p, w.k)
+        check_search_row(ids[i], dist[i], res["ids"], res["dist"], f"rec q{i} {p}")
+    st = B.lib().ifvs_load_reconstructions(idx.handle)
+    assert st == B.E_STATE
