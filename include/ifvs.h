@@ -292,6 +292,17 @@ ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const
                                      best keys and prune with the k-th smallest published key:
                                      0 automatic (on for chunk-grid scans of long intervals),
                                      1 never, 2 always                                         */
+#define IFVS_OPT_SEED_TILES 11   /* one-query scans of M = 16, 48 or 120 with k <= 64: before
+                                     scanning, each wavefront ranks the selected rows of its first
+                                     n selected tiles by their partial sums over the first
+                                     subspace group and computes the full distance of its 8 best;
+                                     the k-th smallest of the workgroup's candidate distances
+                                     bounds the query's answer from the first tile on.  On a
+                                     chunk grid the tiles are the wavefront's first n of its
+                                     cell, otherwise 8n tiles drawn evenly from the query's
+                                     whole interval (all of them if it has fewer).
+                                     0 automatic (n = 64 on chunk-grid cells, off otherwise),
+                                     1 never, n > 1 at most n tiles                           */
 #define IFVS_OPT_EXACT_PLAN 10    /* ifvs_exact_search: 0 automatic (matrix-core screening when
                                      the batch's queries share rows), 1 score every selected row
                                      exactly, 2 always screen first                           */

@@ -156,7 +156,8 @@ struct ifvs_index {
   int opt_grid_relative = 0;   // 1: grid chunks relative to each query tile's first cell
   int opt_slot_order = 0;      // 0: chunk-grid slots in estimated-work order, 1: in index order
   int opt_exact_plan = 0;      // ifvs_exact_search: 0 automatic, 1 direct, 2 screened
-  int opt_shared_bound = 0;    // workgroup bound from the wavefronts' published best keys: 0 auto, 1 off, 2 on
+  int opt_shared_bound = 0;
+  int opt_seed_tiles = 0;      // seeded bound: 0 auto, 1 off, n > 1 at most n tiles per wavefront    // workgroup bound from the wavefronts' published best keys: 0 auto, 1 off, 2 on
   int opt_gather_auto_pct = 30;   // automatic mode: pools up to this % of the rows
   int profile_mask = 0;          // stages timed with HIP events (IFVS_OPT_PROFILE)
   StageTimer* timers = nullptr;  // [kStages] once profiling was enabled
@@ -533,6 +534,7 @@ ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_
   int64_t splits = (4096 + gy - 1) / gy;
   plan->chunk_tiles = 0;
   plan->abs_cells = false;
+  plan->seed_tiles = 0;
   if (interval_batch) {
     // Long spans (>= 8192 tiles) are cut on a chunk grid of cells of about
     // 5K tiles (measured best between 4K and 5K on 10M x 48-byte codes), so
@@ -545,6 +547,19 @@ ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_
       const int64_t cells = (span_tiles + 5119) / 5120;
       plan->chunk_tiles = (span_tiles + cells - 1) / cells;
     }
+    // Seeded bound (one query per tile, tables of a fixed M).  Automatic on
+    // chunk-grid cells, each wavefront ranking its first 64 tiles of the
+    // cell (6-9% less scan time at 10% and 50% selectivity on 10M x 48-byte
+    // codes).  Short intervals end before a wavefront's own k-th key gets
+    // close, but the seed must then rank nearly every tile of the query to
+    // find its k nearest rows, and every workgroup of the query pays for it:
+    // measured 4-45% slower at 0.1% and 1%, so only on request there.
+    const bool seedable = plan->qtile == 1 && (idx->m == 16 || idx->m == 48 || idx->m == 120) &&
+                          k <= kScanWaves * kScanSeed;
+    if (seedable && idx->opt_seed_tiles > 1)
+      plan->seed_tiles = idx->opt_seed_tiles;
+    else if (seedable && idx->opt_seed_tiles == 0 && plan->chunk_tiles > 0)
+      plan->seed_tiles = 64;
     // Chunk c is absolute cell c of the grid: every XCD walks the same cells
     // at the same time, so one HBM read of a cell can serve the other XCDs
     // from the Infinity Cache.  Cells a query's interval misses cost one
@@ -833,6 +848,7 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
       if (value > 2) return fail(IFVS_E_INVALID, "IFVS_OPT_EXACT_PLAN takes 0, 1 or 2");
       idx->opt_exact_plan = static_cast<int>(value);
       return IFVS_OK;
+    case IFVS_OPT_SEED_TILES: idx->opt_seed_tiles = static_cast<int>(value); return IFVS_OK;
     case IFVS_OPT_SHARED_BOUND:
       if (value > 2) return fail(IFVS_E_INVALID, "IFVS_OPT_SHARED_BOUND takes 0, 1 or 2");
       idx->opt_shared_bound = static_cast<int>(value);

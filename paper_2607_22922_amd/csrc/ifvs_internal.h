@@ -14,6 +14,7 @@ constexpr int kTileRows = 64;              // vectors per code tile = one wavefr
 constexpr int kLdsBudget = 160 * 1024;     // LDS bytes per workgroup on gfx950
 constexpr int kScanWaves = 8;              // wavefronts per scan workgroup
 constexpr int kScanPub = 2;                // best keys per (wavefront, query) published for the workgroup bound
+constexpr int kScanSeed = 8;               // seed candidates per wavefront (kScanWaves * kScanSeed = 64 >= k)
 constexpr int kFilterQueries = 16;         // predicates evaluated per attribute read
 
 // A predicate as the device sees it.  The raw fields are the caller's clauses
@@ -117,6 +118,7 @@ struct ScanPlan {
   int64_t chunk_tiles;  // > 0: chunk grid cell in tiles (interval scans); 0: equal chunks
   bool abs_cells;       // chunk c is absolute grid cell c (splits = cells of the whole index)
   bool shared_bound;    // wavefronts publish their best keys for a workgroup bound (k <= 16)
+  int seed_tiles;       // > 0: seeded bound from up to this many tiles per wavefront
 };
 
 // Largest query tile whose tables and pools fit the LDS budget (0 if none).

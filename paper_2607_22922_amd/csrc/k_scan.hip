@@ -68,6 +68,7 @@ struct ScanArgs {
   // c * per_xcd + t meaning chunk c of the XCD's t-th query tile.
   const int32_t* slot_order;
   int shared_bound;      // 1: wavefronts publish their best keys (union bound, k <= 16)
+  int seed_tiles;        // > 0: seeded bound from up to this many tiles per wavefront (QT = 1, k <= 64)
 };
 
 // Lower this wavefront's published best keys to the first kScanPub keys of
@@ -120,6 +121,8 @@ __global__ __launch_bounds__(kScanWaves * 64) __attribute__((amdgpu_waves_per_eu
 void scan_kernel(const ScanArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int kMW = MT > 0 ? (MT + 3) / 4 : 1;
+  // Subspaces summed between two early-abandonment checks (fixed M).
+  constexpr int kGroup = MT % 8 == 0 && MT > 16 ? 8 : (MT % 4 == 0 ? 4 : MT);
   const int M = MT > 0 ? MT : a.m;
   // LDS: the tables, then (dynamic) the pools, the workgroup thresholds and
   // the monotonicity flags.  With M fixed at compile time the tables are a
@@ -142,6 +145,8 @@ void scan_kernel(const ScanArgs a) {
   uint32_t* s_bad = reinterpret_cast<uint32_t*>(s_thr + QT);   // [wave][qi]: the wave saw a negative or NaN entry
   // [qi][wave][kScanPub]: each wavefront's best keys, only ever lowered
   unsigned long long* s_pub = reinterpret_cast<unsigned long long*>(s_bad + kScanWaves * QT);
+  // [wave][kScanSeed]: distances (order-preserving bits) of the seed candidates
+  uint32_t* s_seed = reinterpret_cast<uint32_t*>(s_pub + QT * kScanWaves * kScanPub);
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -299,13 +304,58 @@ void scan_kernel(const ScanArgs a) {
   uint32_t ws[kDepth][kMW];
   int ts[kDepth];
   int t_next = tb + wave;
-  if constexpr (MT > 0) {
+  auto preload = [&]() {
 #pragma unroll
     for (int i = 0; i < kDepth - 1; ++i) {
       ts[i] = next_selected(t_next, bms[i]);
       load_tile(ts[i], ws[i]);
       t_next = ts[i] + kScanWaves;
     }
+  };
+
+  // Seed tiles (see the seeded bound below).  Slot i of this wavefront is
+  // tile tb + wave + 8i of the chunk on a chunk grid; on short intervals the
+  // seed is drawn from the query's whole interval, so every chunk of the
+  // query gets the same query-wide bound: all its tiles when there are at
+  // most 8 * seed_tiles of them, else that many evenly spaced ones.
+  constexpr int kSW = (kGroup + 3) / 4;   // code words holding the first group
+  constexpr int kSB = 24;                 // seed tiles per wavefront and round of loads
+  const bool seeding = MT > 0 && QT == 1 && a.seed_tiles > 0 && k <= kScanWaves * kScanSeed && te > tb;
+  const int64_t seed_span = static_cast<int64_t>(lt[0]) - ft[0] + 1;
+  const int64_t seed_slots = static_cast<int64_t>(kScanWaves) * a.seed_tiles;
+  auto seed_tile = [&](int i) -> int {
+    if (i >= a.seed_tiles) return -1;
+    if (a.chunk_tiles > 0) {
+      const int t = tb + wave + kScanWaves * i;
+      return t < te ? t : -1;
+    }
+    const int64_t sl = wave + static_cast<int64_t>(kScanWaves) * i;
+    if (seed_span <= seed_slots) return sl < seed_span ? static_cast<int>(ft[0] + sl) : -1;
+    return static_cast<int>(ft[0] + sl * seed_span / seed_slots);
+  };
+  // Selection word of seed slot i (0: no tile or nothing selected); the
+  // tile in *t.
+  auto seed_mask = [&](int i, int* t) -> uint64_t {
+    *t = seed_tile(i);
+    if (*t < 0) return 0;
+    uint64_t b1[QT];
+    return tile_masks(*t, b1) != 0 ? b1[0] : 0;
+  };
+  uint32_t sw[kSB][kSW];
+  auto seed_load = [&](int round) {
+#pragma unroll
+    for (int i = 0; i < kSB; ++i) {
+      int t;
+      if (seed_mask(round * kSB + i, &t) != 0) {
+        const uint32_t* __restrict__ tile = a.codes_t + static_cast<size_t>(t) * (kMW * 64);
+#pragma unroll
+        for (int j = 0; j < kSW; ++j) sw[i][j] = tile[j * 64 + lane];
+      }
+    }
+  };
+  if constexpr (MT > 0) {
+    if (seeding) seed_load(0);
+    else preload();
   }
 
   // Tables into LDS as [m][qi][c], noting any entry that is negative or NaN
@@ -365,6 +415,87 @@ void scan_kernel(const ScanArgs a) {
     monotone[qi] = mono;
   }
 
+  // Seeded bound (one query per tile).  A wavefront's own k-th key stays
+  // far above the query's answer until its pool holds rows near the query,
+  // which on a short interval is about when the scan ends, so before the
+  // scan proper each wavefront sums the first subspace group of every
+  // selected row of its first seed_tiles selected tiles, keeps each lane's
+  // smallest such partial sum, and computes the full distance of the
+  // kScanSeed rows with the smallest ones (rows close to the query in the
+  // first subspaces are likely close overall).  They are selected rows and
+  // their distances are summed exactly as below, so the k-th smallest
+  // distance among the workgroup's candidates bounds the query's k-th
+  // distance: rows above it are dropped from the first tile on.
+  uint64_t seed = kNoKey;
+  if constexpr (MT > 0 && QT == 1) {
+    if (seeding && monotone[0]) {
+      float best_p = __builtin_inff();
+      int best_t = -1;
+      for (int round = 0;; ++round) {
+#pragma unroll
+        for (int i = 0; i < kSB; ++i) {
+          int t;
+          const uint64_t mk = seed_mask(round * kSB + i, &t);
+          if (mk != 0) {
+            float p = 0.0f;
+#pragma unroll
+            for (int u = 0; u < kGroup; ++u)
+              p = __fadd_rn(p, widen(slut[u * kKsub + static_cast<int>((sw[i][u >> 2] >> (8 * (u & 3))) & 0xFFu)]));
+            if (((mk >> lane) & 1) && p < best_p) {
+              best_p = p;
+              best_t = t;
+            }
+          }
+        }
+        if ((round + 1) * kSB >= a.seed_tiles) break;
+        seed_load(round + 1);
+      }
+      // The kScanSeed lanes with the smallest partial sums (lane breaks ties).
+      uint64_t ck = best_t >= 0 ? (static_cast<uint64_t>(ordered_bits(best_p)) << 32) | static_cast<uint32_t>(lane)
+                                : kNoKey;
+      bool chosen = false;
+#pragma unroll
+      for (int j = 0; j < kScanSeed; ++j) {
+        uint64_t mn = ck;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const uint64_t x = shfl_xor_u64(mn, o);
+          mn = x < mn ? x : mn;
+        }
+        if (mn == kNoKey) break;
+        if (ck == mn) {
+          chosen = true;
+          ck = kNoKey;
+        }
+      }
+      // The scan's first tiles are loaded while the candidates' rows are.
+      preload();
+      float dfull = 0.0f;
+      if (chosen) {
+        const uint32_t* __restrict__ tile = a.codes_t + static_cast<size_t>(best_t) * (kMW * 64);
+        uint32_t w[kMW];
+#pragma unroll
+        for (int j = 0; j < kMW; ++j) w[j] = tile[j * 64 + lane];
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+          dfull = __fadd_rn(dfull, widen(slut[m * kKsub + static_cast<int>((w[m >> 2] >> (8 * (m & 3))) & 0xFFu)]));
+      }
+      const uint64_t cm = __ballot(chosen);
+      const int nc = __popcll(cm);
+      if (chosen) s_seed[wave * kScanSeed + lanes_below(cm)] = ordered_bits(dfull);
+      if (lane >= nc && lane < kScanSeed) s_seed[wave * kScanSeed + lane] = ~0u;
+      __syncthreads();
+      uint64_t v[1] = {lane < kScanWaves * kScanSeed ? (static_cast<uint64_t>(s_seed[lane]) << 32) | 0xFFFFFFFFull
+                                                     : kNoKey};
+      wave_bitonic_sort<1>(v);
+      seed = shfl_u64(v[0], k - 1);
+      if (threadIdx.x == 0 && seed != kNoKey)
+        __hip_atomic_fetch_min(a.gthr + qid[0], seed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else if (seeding) {
+      preload();
+    }
+  }
+
   int cnt[QT];
   uint64_t thr[QT];
 #pragma unroll
@@ -417,7 +548,8 @@ void scan_kernel(const ScanArgs a) {
       if (qi >= qn) continue;
       const uint64_t blk = s_thr[qi];
       uint64_t b = thr[qi] < blk ? thr[qi] : blk;
-      bound[qi] = b < gview[qi] ? b : gview[qi];
+      b = b < gview[qi] ? b : gview[qi];
+      bound[qi] = QT == 1 && seed < b ? seed : b;
     }
   };
 
@@ -462,7 +594,6 @@ void scan_kernel(const ScanArgs a) {
   };
 
   if constexpr (MT > 0) {
-    constexpr int kGroup = MT % 8 == 0 && MT > 16 ? 8 : (MT % 4 == 0 ? 4 : MT);
     auto sum_tile = [&](int t, const uint64_t (&bm)[QT], const uint32_t (&w)[kMW]) {
       refresh_bounds();
       // Subspaces are summed in groups, all of the tile's queries side by
@@ -574,7 +705,8 @@ template <int MT, int QT, typename LutT>
 constexpr bool scan_fits() {
   return static_cast<size_t>(MT) * QT * kKsub * sizeof(LutT) +
              static_cast<size_t>(QT) * (kScanWaves * 65 * sizeof(uint64_t) + 8 + 4 * kScanWaves +
-                                        kScanWaves * kScanPub * sizeof(uint64_t)) <=
+                                        kScanWaves * kScanPub * sizeof(uint64_t)) +
+             kScanWaves * kScanSeed * sizeof(uint32_t) <=
          static_cast<size_t>(kLdsBudget);
 }
 
@@ -624,11 +756,12 @@ int pool_stride_for(int k) {
 
 size_t scan_lds_bytes(int m, int qtile, int lut_bytes, int pool_stride) {
   // tables, pools, workgroup thresholds (8 B), per-wave monotonicity flags
-  // (4 B each) and published best keys
+  // (4 B each) and published best keys, then the seed candidates
   return static_cast<size_t>(qtile) *
-         (static_cast<size_t>(m) * kKsub * lut_bytes +
-          static_cast<size_t>(kScanWaves) * pool_stride * sizeof(uint64_t) + 8 + 4 * kScanWaves +
-          static_cast<size_t>(kScanWaves) * kScanPub * sizeof(uint64_t));
+             (static_cast<size_t>(m) * kKsub * lut_bytes +
+              static_cast<size_t>(kScanWaves) * pool_stride * sizeof(uint64_t) + 8 + 4 * kScanWaves +
+              static_cast<size_t>(kScanWaves) * kScanPub * sizeof(uint64_t)) +
+         static_cast<size_t>(kScanWaves) * kScanSeed * sizeof(uint32_t);
 }
 
 int scan_max_qtile(int m, int lut_bytes, int k) {
@@ -676,6 +809,7 @@ hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s) 
   a.mode = b.mode;
   a.slot_order = b.slot_order;
   a.shared_bound = plan.shared_bound ? 1 : 0;
+  a.seed_tiles = plan.seed_tiles;
   a.partials = b.partials;
   a.gthr = b.gthr;
   a.splits = plan.splits;

@@ -27,6 +27,7 @@ OPT_QTILE, OPT_SPLITS, OPT_PROFILE, OPT_MIN_CHUNK, OPT_GRID_TILES, OPT_GATHER, O
 OPT_SLOT_ORDER = 8
 OPT_SHARED_BOUND = 9
 OPT_EXACT_PLAN = 10
+OPT_SEED_TILES = 11
 STAGES = ("condition", "lut", "filter", "scan", "merge")
 
 EXPORTED = ("ifvs_load_index", "ifvs_free_index", "ifvs_select_codebook", "ifvs_build_lut",

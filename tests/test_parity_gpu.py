@@ -441,6 +441,16 @@ def test_clustered_ties_break_by_original_id(B, k):
     for i, p in enumerate(preds):
         res = O.filtered_search(ox, _np(q[i]), p, k, conditioned=False)
         check_search_row(_np(ids[i]), _np(dist[i]), res["ids"], res["dist"], f"ties q{i}")
+    # interval batches with a seeded bound: the seed's k-th distance is the
+    # shared one, and rows at it must still be decided by original id
+    iv_preds = preds[1:]
+    ids0, dist0 = idx.search(iv_preds, lut[1:], k)
+    for seed_tiles in (2, 24):
+        idx.set_option(B.OPT_SEED_TILES, seed_tiles)
+        ids1, dist1 = idx.search(iv_preds, lut[1:], k)
+        torch.cuda.synchronize()
+        assert torch.equal(ids1, ids0) and torch.equal(dist1.view(torch.int32), dist0.view(torch.int32)), seed_tiles
+    idx.set_option(B.OPT_SEED_TILES, 0)
 
 
 def test_clustered_and_plain_layouts_agree_on_c4_sample(B):
@@ -457,6 +467,14 @@ def test_clustered_and_plain_layouts_agree_on_c4_sample(B):
         torch.cuda.synchronize()
         assert torch.equal(i1, i2), s
         assert torch.equal(d1.view(torch.int32), d2.view(torch.int32)), s
+        # seeded bounds (mixture data: the seed is close to the answer)
+        for seed_tiles in (1, 2, 24, 48):
+            clus.set_option(B.OPT_SEED_TILES, seed_tiles)
+            i3, d3 = clus.search(w.preds[s], lut, 10)
+            torch.cuda.synchronize()
+            assert torch.equal(i1, i3), (s, seed_tiles)
+            assert torch.equal(d1.view(torch.int32), d3.view(torch.int32)), (s, seed_tiles)
+        clus.set_option(B.OPT_SEED_TILES, 0)
 
 
 @pytest.mark.parametrize("cluster_cols", [(), (0,)])
@@ -479,3 +497,50 @@ def test_negative_weights_rank_exactly(B, cluster_cols):
         ids_o, dist_o = O.select_topk(O.adc_distances(lut_o, ox["codes"], cand), cand, 25)
         check_search_row(_np(ids[i]), _np(dist[i]), ids_o, dist_o, f"neg q{i}")
     assert (dist < 0).any()
+    if cluster_cols:
+        # no seed where partial sums are no bound (the table has negative entries)
+        iv = [p for p in preds if p]
+        ids0, dist0 = idx.search(iv, lut[[i for i, p in enumerate(preds) if p]], 25)
+        idx.set_option(B.OPT_SEED_TILES, 24)
+        ids1, dist1 = idx.search(iv, lut[[i for i, p in enumerate(preds) if p]], 25)
+        torch.cuda.synchronize()
+        idx.set_option(B.OPT_SEED_TILES, 0)
+        assert torch.equal(ids1, ids0) and torch.equal(dist1.view(torch.int32), dist0.view(torch.int32))
+
+
+@pytest.mark.parametrize("cols,M,dsub", [((0,), 16, 8), ((1, 0), 16, 8), ((0,), 48, 2), ((0,), 120, 8)])
+def test_seeded_bound_same_answer(B, cols, M, dsub):
+    """The seeded bound (a k-th distance over candidate rows ranked by their
+    first subspace group) on short intervals (tiles drawn from the whole
+    interval: all of them, or evenly spaced ones) and on chunk-grid cells,
+    with residual clauses, empty intervals, k up to 64 (and 65, where no seed
+    is taken): every setting gives the unseeded answer, which is the
+    oracle's."""
+    say(f"[seed] cols={cols} M={M}")
+    idx, ox = _edge_index(B, 30_000, M, dsub, n_attr=2, domain=30, seed=53 + M, cluster_cols=cols)
+    a, b = cols[0], 1 - cols[0]
+    preds = [[(a, 3, 9)], [(a, 0, 30)], [(a, 7, 8), (b, 2, 20)], [(a, 11, 12)], [(a, 1, 27), (b, 0, 15)],
+             [(a, 29, 30)], [(a, 9, 9)], [(a, 4, 26)]] * 2
+    g = torch.Generator(device="cuda").manual_seed(M)
+    q = torch.randn(len(preds), M * dsub, device="cuda", generator=g)
+    alpha, wf = idx.select_codebook(q, preds, None)
+    lut = idx.build_lut(q, alpha, wf)
+    for k in (1, 10, 64, 65):
+        idx.set_option(B.OPT_SEED_TILES, 1)
+        ids0, dist0 = idx.search(preds, lut, k)
+        torch.cuda.synchronize()
+        if k == 10:
+            for i, p in enumerate(preds[:8]):
+                lut_o = O.build_lut(_np(q[i]), _np(alpha[i]), _np(wf[i]), ox["C_pq"], ox["W"], M, ox["r"])
+                cand = O.passing_ids(O.predicate_mask(ox["attrs"], p))
+                ids_o, dist_o = O.select_topk(O.adc_distances(lut_o, ox["codes"], cand), cand, k)
+                check_search_row(_np(ids0[i]), _np(dist0[i]), ids_o, dist_o, f"seed q{i} {p}")
+        for seed_tiles, grid in ((2, 0), (3, 0), (24, 0), (1000, 0), (0, 64), (2, 64), (24, 7), (0, 1)):
+            idx.set_option(B.OPT_SEED_TILES, seed_tiles)
+            idx.set_option(B.OPT_GRID_TILES, grid)
+            ids, dist = idx.search(preds, lut, k)
+            torch.cuda.synchronize()
+            assert torch.equal(ids, ids0), (k, seed_tiles, grid)
+            assert torch.equal(dist.view(torch.int32), dist0.view(torch.int32)), (k, seed_tiles, grid)
+    idx.set_option(B.OPT_SEED_TILES, 0)
+    idx.set_option(B.OPT_GRID_TILES, 0)
