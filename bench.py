@@ -215,6 +215,9 @@ def main():
     ap.add_argument("--sdc-steps", type=int, default=4,
                     help="batches per bin timed with symmetric distance tables (ifvs_build_sdc_lut + the "
                          "same scan; 0 = skip)")
+    ap.add_argument("--host-steps", type=int, default=4,
+                    help="batches per bin timed with queries and weights uploaded from pinned host memory "
+                         "and results downloaded inside each batch (the PCIe-inclusive rate; 0 = skip)")
     ap.add_argument("--lut", choices=["f32", "f16"], default="f32")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain copy kernel of known size (for counter calibration)")
@@ -415,6 +418,49 @@ def main():
             bins_out[str(s)][f"recall@{k}_{mode}"] = round(hits / nr, 4)
     log(f"[bench] bins: {json.dumps(bins_out)}")
 
+    # PCIe-inclusive rate: the same step with the batch's query vectors and
+    # predicate weights copied from pinned host memory at its start and the
+    # ids and distances copied back at its end, all on the stream.
+    host_out = None
+    if args.host_steps > 0:
+        hq = torch.empty(batch, w.D, pin_memory=True)
+        hwz = torch.empty(batch, w.D, pin_memory=True)
+        hid = torch.empty(batch, k, dtype=torch.int32, pin_memory=True)
+        hdi = torch.empty(batch, k, pin_memory=True)
+        q_dev = torch.empty(batch, w.D, device=dev)
+        wz_dev = torch.empty(batch, w.D, device=dev)
+        host_src = {s: [(w.queries[b * batch:(b + 1) * batch].cpu(), w.w_z[s][b * batch:(b + 1) * batch].cpu())
+                        for b in range(min(n_batches, args.host_steps))] for s in bins}
+
+        def run_host(s, b):
+            hq.copy_(host_src[s][b][0])
+            hwz.copy_(host_src[s][b][1])
+            q_dev.copy_(hq, non_blocking=True)
+            wz_dev.copy_(hwz, non_blocking=True)
+            clus.select_codebook_into(q_dev, packed[s][b], wz_dev, alpha, wf)
+            clus.build_lut_into(q_dev, alpha, wf, lut_dt, lut)
+            clus.search_into(batch, packed[s][b], lut, lut_dt, k, ids[s], dist[s])
+            hid.copy_(ids[s], non_blocking=True)
+            hdi.copy_(dist[s], non_blocking=True)
+            torch.cuda.current_stream().synchronize()     # the caller reads the results
+
+        host_bins, host_total = {}, 0.0
+        for s in bins:
+            run_host(s, 0)                                 # warmup
+            ms = []
+            for i in range(args.host_steps):
+                b = i % len(host_src[s])
+                t_ = time.perf_counter()
+                run_host(s, b)
+                ms.append((time.perf_counter() - t_) * 1e3)
+            host_total += sum(ms)
+            host_bins[str(s)] = {"qps": batch * len(ms) / (sum(ms) / 1e3), "ms_per_batch": float(np.median(ms))}
+        host_out = {"qps": args.host_steps * len(bins) * batch / (host_total / 1e3), "steps": args.host_steps,
+                    "bytes_to_device_per_batch": 2 * batch * w.D * 4, "bytes_to_host_per_batch": batch * k * 8,
+                    "timing": "host wall clock per batch, from the host-side copy into the pinned buffers to "
+                              "the results in pinned host memory", "bins": host_bins}
+        log(f"[bench] with host transfers: {host_out['qps']:.0f} queries/s; {json.dumps(host_bins)}")
+
     # Symmetric distance computation (Section 3.2, pre-filtering baselines
     # (iv)/(v)): the query is quantized too; its codeword-distance table
     # feeds the same scan.
@@ -560,6 +606,7 @@ def main():
         "plain_layout": plain_out,
         "exact_search": exact_out,
         "sdc": sdc_out,
+        "host_transfers": host_out,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
