@@ -525,9 +525,11 @@ def test_seeded_bound_same_answer(B, cols, M, dsub):
     q = torch.randn(len(preds), M * dsub, device="cuda", generator=g)
     alpha, wf = idx.select_codebook(q, preds, None)
     lut = idx.build_lut(q, alpha, wf)
+    lut16 = idx.build_lut(q, alpha, wf, B.LUT_F16)
     for k in (1, 10, 64, 65):
         idx.set_option(B.OPT_SEED_TILES, 1)
         ids0, dist0 = idx.search(preds, lut, k)
+        i16, d16 = idx.search(preds, lut16, k, B.LUT_F16)
         torch.cuda.synchronize()
         if k == 10:
             for i, p in enumerate(preds[:8]):
@@ -542,5 +544,9 @@ def test_seeded_bound_same_answer(B, cols, M, dsub):
             torch.cuda.synchronize()
             assert torch.equal(ids, ids0), (k, seed_tiles, grid)
             assert torch.equal(dist.view(torch.int32), dist0.view(torch.int32)), (k, seed_tiles, grid)
+            if seed_tiles in (2, 24):                    # binary16 tables
+                ids, dist = idx.search(preds, lut16, k, B.LUT_F16)
+                torch.cuda.synchronize()
+                assert torch.equal(ids, i16) and torch.equal(dist.view(torch.int32), d16.view(torch.int32))
     idx.set_option(B.OPT_SEED_TILES, 0)
     idx.set_option(B.OPT_GRID_TILES, 0)
