@@ -71,21 +71,6 @@ struct ScanArgs {
   int seed_tiles;        // > 0: seeded bound from up to this many tiles per wavefront (QT = 1, k <= 64)
 };
 
-// Lower this wavefront's published best keys to the first kScanPub keys of
-// its freshly compacted pool, then return the k-th smallest published key of
-// the workgroup (all ones while fewer than k are published).  Not inlined:
-// it runs only when a wavefront's best keys improve.
-__device__ __noinline__ uint64_t publish_best(const uint64_t* pool, int cnt, unsigned long long* pub, int wave,
-                                              int k) {
-  const int lane = __lane_id();
-  if (lane < kScanPub && lane < cnt) atomicMin(&pub[wave * kScanPub + lane], static_cast<unsigned long long>(pool[lane]));
-  uint64_t v[1] = {lane < kScanWaves * kScanPub
-                       ? static_cast<uint64_t>(__hip_atomic_load(&pub[lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP))
-                       : kNoKey};
-  wave_bitonic_sort<1>(v);
-  return shfl_u64(v[0], k - 1);
-}
-
 // Bits [lo, hi) of a 64-bit word, 0 <= lo < hi <= 64.
 __device__ __forceinline__ uint64_t bit_range(int64_t lo, int64_t hi) {
   const uint64_t upto_hi = hi >= 64 ? ~0ull : ((1ull << hi) - 1);
@@ -143,8 +128,10 @@ void scan_kernel(const ScanArgs a) {
   unsigned long long* s_thr = reinterpret_cast<unsigned long long*>(
       pools + static_cast<size_t>(kScanWaves) * QT * a.pool_stride);   // smallest k-th key published in this workgroup
   uint32_t* s_bad = reinterpret_cast<uint32_t*>(s_thr + QT);   // [wave][qi]: the wave saw a negative or NaN entry
-  // [qi][wave][kScanPub]: each wavefront's best keys, only ever lowered
+  // [qi][wave][kScanPub]: each wavefront's smallest distances (order-preserving
+  // bits), only ever lowered (the area holds 8-byte words; half is used)
   unsigned long long* s_pub = reinterpret_cast<unsigned long long*>(s_bad + kScanWaves * QT);
+  uint32_t* s_best = reinterpret_cast<uint32_t*>(s_pub);
   // [wave][kScanSeed]: distances (order-preserving bits) of the seed candidates
   uint32_t* s_seed = reinterpret_cast<uint32_t*>(s_pub + QT * kScanWaves * kScanPub);
 
@@ -522,17 +509,18 @@ void scan_kernel(const ScanArgs a) {
   // Union bound.  A wavefront's own k-th key reflects only the rows it
   // scanned, and the workgroup's smallest such key is about the
   // (waves * k)-th best row the workgroup has seen -- too loose to stop the
-  // summation early on short intervals.  So whenever a candidate could
-  // improve a wavefront's kScanPub best keys, the wavefront compacts its pool
-  // and lowers its entries of s_pub (atomic minimum).  Each entry stays at
-  // least that wavefront's true j-th best key, and wavefronts scan disjoint
-  // rows, so at least k distinct rows have keys at or below the k-th
-  // smallest entry: it bounds the query's answer and is published like a
-  // threshold.
+  // summation early on short intervals.  So each wavefront keeps the two
+  // smallest distances it has summed in full (two distinct rows; a wavefront
+  // reduction over the step's surviving lanes, no pool work) and, when they
+  // fall, stores them in its slots of s_best.  Wavefronts scan disjoint
+  // rows, so the k-th smallest of the workgroup's 16 slots is the distance of
+  // one of k distinct rows at or below it: a bound on the query's answer,
+  // published like a threshold (with the largest id, so rows at that
+  // distance stay eligible).
   const bool union_bound = a.shared_bound && k <= kScanWaves * kScanPub;
-  uint64_t my_pub[QT];   // this wavefront's kScanPub-th best key as last published
+  uint32_t best1[QT], best2[QT];   // this wavefront's two smallest full distances
 #pragma unroll
-  for (int qi = 0; qi < QT; ++qi) my_pub[qi] = kNoKey;
+  for (int qi = 0; qi < QT; ++qi) best1[qi] = best2[qi] = ~0u;
   auto global_issue = [&]() {
 #pragma unroll
     for (int qi = 0; qi < QT; ++qi)
@@ -569,21 +557,61 @@ void scan_kernel(const ScanArgs a) {
         }
       }
     }
-    const bool improve = union_bound && __ballot(cand && (key >> 32) < (my_pub[qi] >> 32)) != 0;
-    uint64_t* pool = my_pools + qi * a.pool_stride;
-    pool_push(pool, cnt[qi], thr[qi], key, cand, k, a.kpl, a.perm);
-    if (improve) {
-      pool_compact(pool, cnt[qi], thr[qi], k, a.kpl, a.perm);
-      my_pub[qi] = cnt[qi] >= kScanPub ? pool[kScanPub - 1] : kNoKey;
-      const uint64_t ub = publish_best(pool, cnt[qi], s_pub + qi * kScanWaves * kScanPub, wave, k);
-      if (ub < published[qi]) {
-        published[qi] = ub;
-        if (lane == 0) {
-          atomicMin(&s_thr[qi], static_cast<unsigned long long>(ub));
-          __hip_atomic_fetch_min(a.gthr + qid[qi], ub, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (union_bound) {
+      // The step's two smallest full distances (pairs merged across lanes),
+      // then the wavefront's two smallest so far.
+      uint32_t x1 = act ? ordered_bits(d) : ~0u, x2 = ~0u;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y1 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(x1), o, 64));
+        const uint32_t y2 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(x2), o, 64));
+        const uint32_t hi = x1 > y1 ? x1 : y1;
+        const uint32_t lo2 = x2 < y2 ? x2 : y2;
+        x1 = x1 < y1 ? x1 : y1;
+        x2 = hi < lo2 ? hi : lo2;
+      }
+      const uint32_t hi = best1[qi] > x1 ? best1[qi] : x1;
+      const uint32_t lo2 = best2[qi] < x2 ? best2[qi] : x2;
+      const uint32_t n1 = best1[qi] < x1 ? best1[qi] : x1;
+      const uint32_t n2 = hi < lo2 ? hi : lo2;
+      if (n1 < best1[qi] || n2 < best2[qi]) {
+        // The k-th smallest slot only falls when a slot drops from at or
+        // above it to below it; the other improvements are only stored.
+        const uint32_t kth = static_cast<uint32_t>(published[qi] >> 32);
+        const bool crossed = (n1 < kth && best1[qi] >= kth) || (n2 < kth && best2[qi] >= kth);
+        best1[qi] = n1;
+        best2[qi] = n2;
+        uint32_t* slots = s_best + qi * kScanWaves * kScanPub;
+        if (lane < kScanPub)
+          __hip_atomic_store(&slots[wave * kScanPub + lane], lane == 0 ? n1 : n2, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (crossed) {
+          // Rank of each of the 16 slots (ties by slot index); the slot of
+          // rank k - 1 is the k-th smallest.
+          const uint32_t v = lane < kScanWaves * kScanPub
+                                 ? __hip_atomic_load(&slots[lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)
+                                 : ~0u;
+          int rank = 0;
+#pragma unroll
+          for (int j = 0; j < kScanWaves * kScanPub; ++j) {
+            const uint32_t vj = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), j));
+            rank += (vj < v || (vj == v && j < lane)) ? 1 : 0;
+          }
+          const uint64_t at = __ballot(lane < kScanWaves * kScanPub && rank == k - 1);
+          const uint32_t kv = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), __builtin_ctzll(at)));
+          const uint64_t ub = (static_cast<uint64_t>(kv) << 32) | 0xFFFFFFFFull;
+          if (ub < published[qi]) {
+            published[qi] = ub;
+            if (lane == 0) {
+              atomicMin(&s_thr[qi], static_cast<unsigned long long>(ub));
+              __hip_atomic_fetch_min(a.gthr + qid[qi], ub, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+          }
         }
       }
     }
+    uint64_t* pool = my_pools + qi * a.pool_stride;
+    pool_push(pool, cnt[qi], thr[qi], key, cand, k, a.kpl, a.perm);
     if (thr[qi] < published[qi]) {
       published[qi] = thr[qi];
       if (lane == 0) {
