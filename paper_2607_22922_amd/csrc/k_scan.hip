@@ -26,7 +26,11 @@
 //    partial sums only grow; checked per query when its table is staged).
 //    Lanes beating the current k-th best key are appended to that query's
 //    pool (ballot + prefix count), which is sorted and cut back to k keys
-//    when it would overflow.  Keys carry original vector ids (on a clustered
+//    when it would overflow.  The "current k-th distance" is the smallest
+//    valid bound known: the wavefront's own, the workgroup's and the
+//    query's (shared through LDS and global atomics), the k-th smallest of
+//    the wavefronts' two best distances (union bound), and a seed computed
+//    before the scan from rows ranked by their first subspace group.  Keys carry original vector ids (on a clustered
 //    layout looked up when a pool is compacted), so ties break by original id
 //    on any layout.  At the end each
 //    wavefront writes its k best keys per query; a merge kernel reduces them.
