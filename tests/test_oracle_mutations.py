@@ -35,21 +35,35 @@ MUTATIONS = [
 ]
 
 
-def _run_pins_on_copy(tmp_path, old, new):
-    src = os.path.join(ROOT, "oracle", "ifvs_oracle.py")
+# Planted mistakes in the training oracle, caught by its own pins.
+TRAIN_MUTATIONS = [
+    ("train_anchor_factor", "(lam * 2.0 / (M * K * d) / nq)", "(lam / (M * K * d) / nq)"),
+    ("train_table_grad_sign", 'g_delta = g_lut[:, :, None] * (-2.0 * wm * f["e"])',
+     'g_delta = g_lut[:, :, None] * (2.0 * wm * f["e"])'),
+    ("train_positive_share", 'g_s = f["p"] - f["pos"] / f["n_pos"]', 'g_s = f["p"] - f["pos"]'),
+    ("train_alpha_wrong_direction", 'g_alpha = np.einsum("mcj,mtcj->mt", g_delta, W.astype(np.float64)).reshape(M * r)',
+     'g_alpha = np.einsum("mcj,mtcj->tm", g_delta, W.astype(np.float64)).reshape(M * r)'),
+    ("train_bank_first_row_only", 'for row in f["rows"]:', 'for row in f["rows"][:1]:'),
+    ("train_wz_no_softplus_slope", "g_wz[i] = g_w * _sigmoid(np.asarray(w_z, dtype=np.float64))", "g_wz[i] = g_w"),
+    ("train_temperature_dropped", "g_dist = -g_s / tau / nq", "g_dist = -g_s / nq"),
+]
+
+
+def _run_pins_on_copy(tmp_path, old, new, target="ifvs_oracle.py", pins="test_oracle_pins.py"):
+    src = os.path.join(ROOT, "oracle", target)
     text = open(src).read()
     assert old in text, f"mutation text {old!r} no longer applies; update it"
     dst = tmp_path / "oracle"
     shutil.copytree(os.path.join(ROOT, "oracle"), dst,
                     ignore=shutil.ignore_patterns("__pycache__"))
-    (dst / "ifvs_oracle.py").write_text(text.replace(old, new, 1))
+    (dst / target).write_text(text.replace(old, new, 1))
     tests = tmp_path / "tests"
     tests.mkdir()
-    shutil.copy(os.path.join(ROOT, "tests", "test_oracle_pins.py"), tests)
+    shutil.copy(os.path.join(ROOT, "tests", pins), tests)
     shutil.copytree(os.path.join(ROOT, "tests", "golden"), tests / "golden")
     env = dict(os.environ, PYTHONPATH=str(tmp_path), PYTHONDONTWRITEBYTECODE="1")
     proc = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
-                           str(tests / "test_oracle_pins.py")],
+                           str(tests / pins)],
                           cwd=tmp_path, env=env, capture_output=True, text=True, timeout=300)
     return proc
 
@@ -64,3 +78,15 @@ def test_unmutated_copy_passes(tmp_path):
 def test_pins_catch_planted_mistake(tmp_path, name, old, new):
     proc = _run_pins_on_copy(tmp_path, old, new)
     assert proc.returncode == 1, f"planted mistake {name} went unnoticed:\n{proc.stdout[-2000:]}"
+
+
+def test_unmutated_train_copy_passes(tmp_path):
+    old = TRAIN_MUTATIONS[0][1]
+    proc = _run_pins_on_copy(tmp_path, old, old, "ifvs_train_oracle.py", "test_oracle_train.py")
+    assert proc.returncode == 0, proc.stdout[-2000:]
+
+
+@pytest.mark.parametrize("name,old,new", TRAIN_MUTATIONS, ids=[m[0] for m in TRAIN_MUTATIONS])
+def test_train_pins_catch_planted_mistake(tmp_path, name, old, new):
+    proc = _run_pins_on_copy(tmp_path, old, new, "ifvs_train_oracle.py", "test_oracle_train.py")
+    assert proc.returncode == 1, f"the training pins did not catch {name}:\n{proc.stdout[-2000:]}"
