@@ -230,6 +230,49 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
  * attached), IFVS_E_NOMEM, IFVS_E_HIP. */
 ifvs_status ifvs_load_vectors(ifvs_index* idx, const float* x, int32_t mem_kind);
 
+/* ifvs_train_step -- one training step of the filter-aware conditioning
+ * (Section 2, training paragraph): the memory bank and W of the index are
+ * updated in place by plain SGD, so later calls use the trained values.
+ *
+ * For each of the nq training queries (q, preds, w_z as for
+ * ifvs_select_codebook), cand[i][0..n_cand) are original vector ids, the
+ * first n_pos the query's ground-truth positives and the rest its hard
+ * negatives (the caller mines them, e.g. with ifvs_filtered_search); an id
+ * outside 0..n-1 (such as -1) is an absent slot.  With d_v the weighted
+ * distance of candidate v under the current conditioned codebook
+ * (ifvs_build_lut's table, subspaces summed in order) and P the present
+ * positives, the query's loss is
+ *   L_i = (1/P) sum_{positives p} [ logsumexp_v(-d_v / tau) + d_p / tau ]
+ *         + lambda * mean over (m, c, j) of Delta_i[m][c][j]^2
+ * (cross-entropy 0 when P = 0) and the step descends the batch mean of L_i:
+ *   bank[row] -= lr * dL/dalpha_i for each of query i's h hashed rows,
+ *   W -= lr * dL/dW.
+ * C_PQ and the codes are not changed.  The arithmetic is fp32 with fp64
+ * softmax statistics; the bank update uses atomics, so the order of its
+ * additions (and the last bits of the result) may vary between runs.
+ *
+ * q: device [nq][dim]; preds: host [nq]; w_z: device [nq][dim] or NULL
+ * (w_f = 1); cand: device [nq][n_cand] int32; loss_out: device [nq], L_i;
+ * dwz_out: device [nq][dim] or NULL, dL/dw_z (the gradient a predicate
+ * encoder would receive; requires w_z).  Enqueued on `stream`.  The first
+ * call allocates a training workspace sized by max_batch
+ * (max_batch * (2 M r + dim + 256 M (1 + dsub)) floats + h ints, and n ints
+ * on a clustered index).
+ * Errors: IFVS_E_STATE (no memory bank), IFVS_E_INVALID (nq > max_batch,
+ * n_cand not in 1..4096, n_pos not in 0..n_cand, tau <= 0, lambda < 0,
+ * non-finite tau/lambda/lr, NULL q/cand/loss_out, dwz_out without w_z, bad
+ * predicate), IFVS_E_UNSUPPORTED (table + candidates + gradients of one
+ * query beyond 160 KB of LDS), IFVS_E_NOMEM, IFVS_E_HIP. */
+ifvs_status ifvs_train_step(ifvs_index* idx, int32_t nq, const float* q, const ifvs_predicate* preds,
+                            const float* w_z, const int32_t* cand, int32_t n_cand, int32_t n_pos, float tau,
+                            float lambda, float lr, float* loss_out, float* dwz_out, void* stream);
+
+/* ifvs_read_params -- copy the index's current memory bank ([bank_rows][m*r])
+ * and W ([m][r][256][dim/m]) into caller memory (host or device; either
+ * pointer may be NULL), enqueued on `stream`.
+ * Errors: IFVS_E_STATE (no memory bank), IFVS_E_HIP. */
+ifvs_status ifvs_read_params(const ifvs_index* idx, float* bank_out, float* W_out, void* stream);
+
 /* ifvs_load_reconstructions -- attach, in place of full-precision vectors,
  * the reconstructions of the index's own codes: row i becomes the
  * concatenation over m of codeword C_PQ[m][code_i[m]].  ifvs_exact_search

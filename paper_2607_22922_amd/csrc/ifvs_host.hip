@@ -10,6 +10,7 @@
 #include "ifvs_internal.h"
 
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -145,6 +146,15 @@ struct ifvs_index {
   uint64_t* partials_x = nullptr;  // [max_batch][exact_chunks_max][max_k]
   int exact_chunks_max = 0;
 
+  // Training workspace (ifvs_train_step), allocated on its first call.
+  float* tr_alpha = nullptr;     // [max_batch][m*r]
+  float* tr_wf = nullptr;        // [max_batch][dim]
+  float* tr_lut = nullptr;       // [max_batch][m][256]
+  float* tr_gdelta = nullptr;    // [max_batch][m][256][dsub]
+  float* tr_galpha = nullptr;    // [max_batch][m*r]
+  int32_t* tr_rows = nullptr;    // [max_batch][h]
+  int32_t* inv_perm = nullptr;   // original id -> physical row (clustered layouts)
+
   // Every (n / kFences)-th clustered key, copied to the host at load: lets
   // the planner estimate each query's interval length without touching the
   // device.
@@ -156,8 +166,8 @@ struct ifvs_index {
   int opt_grid_relative = 0;   // 1: grid chunks relative to each query tile's first cell
   int opt_slot_order = 0;      // 0: chunk-grid slots in estimated-work order, 1: in index order
   int opt_exact_plan = 0;      // ifvs_exact_search: 0 automatic, 1 direct, 2 screened
-  int opt_shared_bound = 0;
-  int opt_seed_tiles = 0;      // seeded bound: 0 auto, 1 off, n > 1 at most n tiles per wavefront    // workgroup bound from the wavefronts' published best keys: 0 auto, 1 off, 2 on
+  int opt_shared_bound = 0;    // workgroup bound from the wavefronts' best distances: 0 auto, 1 off, 2 on
+  int opt_seed_tiles = 0;      // seeded bound: 0 auto, 1 off, n > 1 at most n tiles per wavefront
   int opt_gather_auto_pct = 30;   // automatic mode: pools up to this % of the rows
   int profile_mask = 0;          // stages timed with HIP events (IFVS_OPT_PROFILE)
   StageTimer* timers = nullptr;  // [kStages] once profiling was enabled
@@ -203,6 +213,10 @@ struct ifvs_index {
                     static_cast<void*>(lists), static_cast<void*>(list_n), static_cast<void*>(qmode)})
       if (p) hipFree(p);
     free_vectors();
+    for (void* p : {static_cast<void*>(tr_alpha), static_cast<void*>(tr_wf), static_cast<void*>(tr_lut),
+                    static_cast<void*>(tr_gdelta), static_cast<void*>(tr_galpha), static_cast<void*>(tr_rows),
+                    static_cast<void*>(inv_perm)})
+      if (p) hipFree(p);
     for (int i = 0; i < kStagingSlots; ++i) {
       if (staging[i]) hipHostFree(staging[i]);
       if (staged[i]) hipEventDestroy(staged[i]);
@@ -1302,6 +1316,105 @@ ifvs_status ifvs_read_profile(ifvs_index* idx, double* ms_out, int64_t* launches
     t.ms = 0.0;
     t.launches = 0;
   }
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_train_step(ifvs_index* idx, int32_t nq, const float* q, const ifvs_predicate* preds,
+                            const float* w_z, const int32_t* cand, int32_t n_cand, int32_t n_pos, float tau,
+                            float lambda, float lr, float* loss_out, float* dwz_out, void* stream) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
+  if (idx->bank_rows == 0) return fail(IFVS_E_STATE, "the index has no memory bank and W to train");
+  if (n_cand < 1 || n_cand > 4096) return fail(IFVS_E_INVALID, "n_cand must be in 1..4096");
+  if (n_pos < 0 || n_pos > n_cand) return fail(IFVS_E_INVALID, "n_pos must be in 0..n_cand");
+  if (!(tau > 0.0f) || !std::isfinite(tau)) return fail(IFVS_E_INVALID, "tau must be positive and finite");
+  if (!(lambda >= 0.0f) || !std::isfinite(lambda)) return fail(IFVS_E_INVALID, "lambda must be >= 0 and finite");
+  if (!std::isfinite(lr)) return fail(IFVS_E_INVALID, "lr must be finite");
+  if (nq == 0) return IFVS_OK;
+  if (!q || !cand || !loss_out) return fail(IFVS_E_INVALID, "q, cand or loss_out is NULL");
+  if (dwz_out && !w_z) return fail(IFVS_E_INVALID, "dwz_out needs w_z");
+  const int mr = idx->m * idx->r;
+  if (train_query_lds_bytes(idx->m, idx->dim, n_cand, mr) > static_cast<size_t>(kLdsBudget))
+    return fail(IFVS_E_UNSUPPORTED, "one query's table, candidates and gradients exceed the 160 KB LDS budget");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  if (!idx->tr_alpha) {
+    const size_t b = static_cast<size_t>(idx->max_batch);
+    ifvs_status st = IFVS_OK;
+    if ((st = dev_alloc(&idx->tr_alpha, b * mr, "training alpha")) != IFVS_OK ||
+        (st = dev_alloc(&idx->tr_wf, b * idx->dim, "training w_f")) != IFVS_OK ||
+        (st = dev_alloc(&idx->tr_lut, b * idx->m * kKsub, "training tables")) != IFVS_OK ||
+        (st = dev_alloc(&idx->tr_gdelta, b * idx->m * kKsub * idx->dsub, "training Delta gradients")) != IFVS_OK ||
+        (st = dev_alloc(&idx->tr_galpha, b * mr, "training alpha gradients")) != IFVS_OK ||
+        (st = dev_alloc(&idx->tr_rows, b * idx->h, "training bank rows")) != IFVS_OK) {
+      for (void* p : {static_cast<void*>(idx->tr_alpha), static_cast<void*>(idx->tr_wf),
+                      static_cast<void*>(idx->tr_lut), static_cast<void*>(idx->tr_gdelta),
+                      static_cast<void*>(idx->tr_galpha), static_cast<void*>(idx->tr_rows)})
+        if (p) hipFree(p);
+      idx->tr_alpha = idx->tr_wf = idx->tr_lut = idx->tr_gdelta = idx->tr_galpha = nullptr;
+      idx->tr_rows = nullptr;
+      return st;
+    }
+    if (idx->perm) {
+      if ((st = dev_alloc(&idx->inv_perm, static_cast<size_t>(idx->n), "inverse permutation")) != IFVS_OK)
+        return st;
+      IFVS_HIP(launch_invert_perm(idx->perm, idx->n, idx->inv_perm, s), "launching permutation inverse");
+    }
+  }
+  int slot = 0;
+  if (ifvs_status st = stage_predicates(idx, nq, preds, false, false, s, &slot); st != IFVS_OK) return st;
+  IFVS_LAUNCH(idx, kStCondition, s, "launching condition kernel",
+              launch_condition(q, idx->dim, idx->staging_dev[slot], nq, idx->bank, idx->bank_rows, mr, idx->h,
+                               idx->hash_seed, w_z, idx->tr_alpha, idx->tr_wf, s, idx->tr_rows));
+  if (ifvs_status st = release_slot(idx, slot, s); st != IFVS_OK) return st;
+  IFVS_LAUNCH(idx, kStLut, s, "launching LUT kernel",
+              launch_build_lut(q, idx->dim, idx->m, idx->dsub, idx->r, idx->cpq, idx->W, idx->tr_alpha, idx->tr_wf,
+                               nq, IFVS_LUT_F32, idx->tr_lut, s));
+  TrainArgs a{};
+  a.codes_t = idx->codes_t;
+  a.inv_perm = idx->inv_perm;
+  a.n = idx->n;
+  a.m = idx->m;
+  a.mw = idx->mw;
+  a.dsub = idx->dsub;
+  a.r = idx->r;
+  a.dim = idx->dim;
+  a.q = q;
+  a.w_z = w_z;
+  a.wf = idx->tr_wf;
+  a.alpha = idx->tr_alpha;
+  a.lut = idx->tr_lut;
+  a.cpq = idx->cpq;
+  a.W = idx->W;
+  a.cand = cand;
+  a.nq = nq;
+  a.n_cand = n_cand;
+  a.n_pos = n_pos;
+  a.tau = tau;
+  a.lam = lambda;
+  a.loss = loss_out;
+  a.gdelta = idx->tr_gdelta;
+  a.galpha = idx->tr_galpha;
+  a.dwz = dwz_out;
+  IFVS_HIP(launch_train_query(a, s), "launching training gradient kernel");
+  IFVS_HIP(launch_train_update_w(idx->W, idx->tr_gdelta, idx->tr_alpha, nq, idx->m, idx->r, idx->dsub, lr, s),
+           "launching W update");
+  IFVS_HIP(launch_train_update_bank(idx->bank, mr, idx->tr_rows, idx->h, idx->tr_galpha, nq, lr, s),
+           "launching memory bank update");
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_read_params(const ifvs_index* idx, float* bank_out, float* W_out, void* stream) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (idx->bank_rows == 0) return fail(IFVS_E_STATE, "the index has no memory bank and W");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  if (bank_out)
+    IFVS_HIP(hipMemcpyAsync(bank_out, idx->bank, sizeof(float) * idx->bank_rows * idx->m * idx->r,
+                            hipMemcpyDefault, s), "copying the memory bank");
+  if (W_out)
+    IFVS_HIP(hipMemcpyAsync(W_out, idx->W, sizeof(float) * idx->m * idx->r * kKsub * idx->dsub,
+                            hipMemcpyDefault, s), "copying W");
   return IFVS_OK;
 }
 

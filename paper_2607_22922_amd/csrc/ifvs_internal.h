@@ -99,9 +99,43 @@ hipError_t launch_filter(const int32_t* attrs, int64_t n, int n_attr, const DevP
                          int nq, bool residual_only, uint64_t* bitmap, int64_t stride64,
                          unsigned long long* counts, uint32_t* count_parts, hipStream_t s);
 
+// rows_out (optional, [nq][h]): the hashed bank rows of each query.
 hipError_t launch_condition(const float* q, int dim, const DevPred* preds, int nq,
                             const float* bank, int bank_rows, int mr, int h, uint64_t seed,
-                            const float* w_z, float* alpha_out, float* wf_out, hipStream_t s);
+                            const float* w_z, float* alpha_out, float* wf_out, hipStream_t s,
+                            int32_t* rows_out = nullptr);
+
+// One training step of the conditioning (Section 2, training paragraph).
+struct TrainArgs {
+  const uint32_t* codes_t;   // [n_tiles][mw][64] code words, physical order
+  const int32_t* inv_perm;   // original id -> physical row (null: identity)
+  int64_t n;
+  int m, mw, dsub, r, dim;
+  const float* q;            // [nq][dim]
+  const float* w_z;          // [nq][dim] or null (w_f = 1)
+  const float* wf;           // [nq][dim]
+  const float* alpha;        // [nq][m*r]
+  const float* lut;          // [nq][m][256] fp32
+  const float* cpq;          // [m][256][dsub]
+  const float* W;            // [m][r][256][dsub]
+  const int32_t* cand;       // [nq][n_cand] original ids (-1: absent), the first n_pos positives
+  int nq, n_cand, n_pos;
+  float tau, lam;
+  float* loss;               // [nq]
+  float* gdelta;             // [nq][m][256][dsub]
+  float* galpha;             // [nq][m*r]
+  float* dwz;                // [nq][dim] or null
+};
+size_t train_query_lds_bytes(int m, int dim, int n_cand, int mr);
+hipError_t launch_train_query(const TrainArgs& a, hipStream_t s);
+// W -= lr * sum_q gdelta_q (x) alpha_q, one thread per W entry.
+hipError_t launch_train_update_w(float* W, const float* gdelta, const float* alpha, int nq, int m, int r,
+                                 int dsub, float lr, hipStream_t s);
+// bank[rows_q[i]] -= lr * galpha_q for every query and hash function.
+hipError_t launch_train_update_bank(float* bank, int mr, const int32_t* rows, int h, const float* galpha,
+                                    int nq, float lr, hipStream_t s);
+// inv[perm[r]] = r.
+hipError_t launch_invert_perm(const int32_t* perm, int64_t n, int32_t* inv, hipStream_t s);
 
 hipError_t launch_build_lut(const float* q, int dim, int m, int dsub, int r,
                             const float* cpq, const float* W, const float* alpha,

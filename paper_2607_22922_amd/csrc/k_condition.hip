@@ -62,7 +62,8 @@ template <int H>
 __global__ __launch_bounds__(64) void condition_kernel(
     const float* __restrict__ q, int dim, const DevPred* __restrict__ preds,
     const float* __restrict__ bank, int bank_rows, int mr, uint64_t seed,
-    const float* __restrict__ w_z, float* __restrict__ alpha_out, float* __restrict__ wf_out) {
+    const float* __restrict__ w_z, float* __restrict__ alpha_out, float* __restrict__ wf_out,
+    int32_t* __restrict__ rows_out) {
   const int qi = blockIdx.x;
   const int lane = threadIdx.x;
   const float* qrow = q + static_cast<int64_t>(qi) * dim;
@@ -134,6 +135,8 @@ __global__ __launch_bounds__(64) void condition_kernel(
         splitmix64(key ^ splitmix64(seed + static_cast<uint64_t>(lane))) %
         static_cast<uint64_t>(bank_rows));
 
+  if (rows_out && lane < H) rows_out[static_cast<int64_t>(qi) * H + lane] = static_cast<int32_t>(my_row);
+
   // alpha = bank[row_0] + bank[row_1] + ... in hash-function order from +0.
   // Each pass covers kAlphaUnroll elements per lane; all H * kAlphaUnroll
   // loads are issued before the first add.
@@ -166,14 +169,15 @@ __global__ __launch_bounds__(64) void condition_kernel(
 
 hipError_t launch_condition(const float* q, int dim, const DevPred* preds, int nq,
                             const float* bank, int bank_rows, int mr, int h, uint64_t seed,
-                            const float* w_z, float* alpha_out, float* wf_out, hipStream_t s) {
+                            const float* w_z, float* alpha_out, float* wf_out, hipStream_t s,
+                            int32_t* rows_out) {
   const int hh = (bank_rows > 0 && alpha_out != nullptr) ? h : 0;
   if (hh < 0 || hh > kMaxHashes) return hipErrorInvalidValue;
   const dim3 grid(nq), block(64);
 #define IFVS_CONDITION_CASE(H)                                                              \
   case H:                                                                                    \
     condition_kernel<H><<<grid, block, 0, s>>>(q, dim, preds, bank, bank_rows, mr, seed, w_z, \
-                                               alpha_out, wf_out);                           \
+                                               alpha_out, wf_out, rows_out);                 \
     break;
   switch (hh) {
     IFVS_CONDITION_CASE(0) IFVS_CONDITION_CASE(1) IFVS_CONDITION_CASE(2)

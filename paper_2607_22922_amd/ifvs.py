@@ -33,7 +33,7 @@ STAGES = ("condition", "lut", "filter", "scan", "merge")
 EXPORTED = ("ifvs_load_index", "ifvs_free_index", "ifvs_select_codebook", "ifvs_build_lut",
             "ifvs_filter", "ifvs_filtered_search", "ifvs_set_option", "ifvs_last_plan",
             "ifvs_read_profile", "ifvs_last_error", "ifvs_load_vectors", "ifvs_exact_search",
-            "ifvs_build_sdc_lut", "ifvs_load_reconstructions")
+            "ifvs_build_sdc_lut", "ifvs_load_reconstructions", "ifvs_train_step", "ifvs_read_params")
 
 
 class IfvsError(RuntimeError):
@@ -97,6 +97,9 @@ def _load_library() -> ctypes.CDLL:
         "ifvs_build_sdc_lut": ([vp, i32, vp, i32, vp, vp], i32),
         "ifvs_load_reconstructions": ([vp], i32),
         "ifvs_exact_search": ([vp, i32, vp, vp, i32, vp, vp, vp], i32),
+        "ifvs_train_step": ([vp, i32, vp, vp, vp, vp, i32, i32, ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                             vp, vp, vp], i32),
+        "ifvs_read_params": ([vp, vp, vp, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -247,6 +250,29 @@ class Index:
         x = x.to(dtype=torch.float32).contiguous()
         _check(_lib.ifvs_load_vectors(self.handle, x.data_ptr(),
                                       MEM_DEVICE if x.device.type == "cuda" else MEM_HOST))
+
+    def train_step_into(self, q, preds_c, w_z, cand, n_pos, tau, lam, lr, loss_out, dwz_out=None, stream=None):
+        """One SGD step of the memory bank and W (ifvs_train_step)."""
+        _check(_lib.ifvs_train_step(self.handle, q.shape[0], q.data_ptr(), preds_c, _ptr(w_z), cand.data_ptr(),
+                                    cand.shape[1], int(n_pos), float(tau), float(lam), float(lr),
+                                    loss_out.data_ptr(), _ptr(dwz_out), _stream(stream)))
+
+    def train_step(self, q, preds, w_z, cand, n_pos, tau, lam, lr, want_dwz=False):
+        """Marshalling wrapper: returns (per-query loss, dL/dw_z or None)."""
+        q = q.contiguous()
+        cand = cand.to(dtype=torch.int32).contiguous()
+        loss = torch.empty(q.shape[0], device=self.device)
+        dwz = torch.empty_like(q) if want_dwz else None
+        self.train_step_into(q, pack_predicates(preds), None if w_z is None else w_z.contiguous(), cand, n_pos,
+                             tau, lam, lr, loss, dwz)
+        return loss, dwz
+
+    def read_params(self):
+        """The current memory bank [bank_rows][m*r] and W [m][r][256][dsub] (ifvs_read_params)."""
+        bank = torch.empty(self.bank_rows, self.m * self.r, device=self.device)
+        W = torch.empty(self.m, self.r, 256, self.dsub, device=self.device)
+        _check(_lib.ifvs_read_params(self.handle, bank.data_ptr(), W.data_ptr(), _stream(None)))
+        return bank, W
 
     def load_reconstructions(self):
         """Attach the reconstructions of the codes (ifvs_load_reconstructions)."""
