@@ -140,3 +140,16 @@ def test_train_step_errors(B):
     assert st == B.E_INVALID and "w_z" in msg, msg
     st, msg = _status(B, lib.ifvs_read_params, plain.handle, None, None, None)
     assert st == B.E_STATE, msg
+
+
+def test_training_loop_runs_and_fits_its_queries(B):
+    """The training loop end to end on the 10K-vector workload: the
+    conditioned search equals plain PQ before training (alpha = 0), the loss
+    falls, and recall on the training queries does not drop."""
+    from paper_2607_22922_amd import train
+    out = train.main(["--config", "c1", "--bin", "0.1", "--train-queries", "64", "--test-queries", "32",
+                      "--batch", "32", "--epochs", "4", "--n-neg", "16"])
+    assert out["recall@10_conditioned_before"] == out["recall@10_identity"]
+    losses = out["loss_per_epoch"]
+    assert all(np.isfinite(losses)) and losses[-1] < losses[0], losses
+    assert out["recall@10_conditioned_after"]["train"] >= out["recall@10_conditioned_before"]["train"]
