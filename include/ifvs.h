@@ -332,8 +332,9 @@ ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const
                                      order, then the others by decreasing estimated work (the
                                      last workgroups are short), 1 slots in index order       */
 #define IFVS_OPT_SHARED_BOUND 9   /* k <= 16: the wavefronts of a scan workgroup publish their
-                                     best keys and prune with the k-th smallest published key:
-                                     0 automatic (on for chunk-grid scans of long intervals),
+                                     two smallest distances and prune with the k-th smallest
+                                     published one: 0 automatic (on for chunk-grid scans whose
+                                     widest interval spans 32768 or more 64-row tiles),
                                      1 never, 2 always                                         */
 #define IFVS_OPT_SEED_TILES 11   /* one-query scans of M = 16, 48 or 120 with k <= 64: before
                                      scanning, each wavefront ranks the selected rows of its first

@@ -600,12 +600,13 @@ ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_
   plan->splits = static_cast<int>(splits);
   plan->kpl = pool_kpl(k);
   plan->pool_stride = pool_stride_for(k);
-  // The workgroup bound pays on long intervals (chunk-grid cells, about 1%
-  // less scan time at 50% selectivity on 10M x 48-byte codes); on short ones
-  // its extra compactions cost more than the lookups it saves (+30% to +70%
-  // at 0.1% and 1%), since their k-th best row stays far from the answer
-  // until the scan ends.
-  plan->shared_bound = idx->opt_shared_bound == 2 || (idx->opt_shared_bound == 0 && plan->chunk_tiles > 0);
+  // The workgroup bound pays on the longest intervals (measured: 5% less
+  // scan time at 50% selectivity on 10M x 48-byte codes, 7% at 10% on 100M x
+  // 16-byte codes, both spans of 78K+ tiles) and costs 3-9% on spans of
+  // about 16K tiles (10% of 10M, 1% of 100M rows) and more on short ones:
+  // its k-th slot needs many wavefronts' best rows before it is tight.
+  plan->shared_bound = idx->opt_shared_bound == 2 ||
+                       (idx->opt_shared_bound == 0 && plan->chunk_tiles > 0 && span_tiles >= 32768);
   plan->lds_bytes = scan_lds_bytes(idx->m, plan->qtile, lut_bytes, plan->pool_stride);
   return IFVS_OK;
 }
