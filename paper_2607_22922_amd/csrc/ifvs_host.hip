@@ -1356,10 +1356,15 @@ ifvs_status ifvs_train_step(ifvs_index* idx, int32_t nq, const float* q, const i
       idx->tr_rows = nullptr;
       return st;
     }
-    if (idx->perm) {
-      if ((st = dev_alloc(&idx->inv_perm, static_cast<size_t>(idx->n), "inverse permutation")) != IFVS_OK)
-        return st;
-      IFVS_HIP(launch_invert_perm(idx->perm, idx->n, idx->inv_perm, s), "launching permutation inverse");
+  }
+  if (idx->perm && !idx->inv_perm) {
+    // Candidates are original ids; the codes are in physical order.
+    if (ifvs_status st = dev_alloc(&idx->inv_perm, static_cast<size_t>(idx->n), "inverse permutation"); st != IFVS_OK)
+      return st;
+    if (hipError_t e = launch_invert_perm(idx->perm, idx->n, idx->inv_perm, s); e != hipSuccess) {
+      hipFree(idx->inv_perm);
+      idx->inv_perm = nullptr;
+      return hip_fail(e, "launching permutation inverse");
     }
   }
   int slot = 0;
