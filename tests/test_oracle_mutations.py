@@ -31,6 +31,10 @@ MUTATIONS = [
     ("sdc_table_transposed_subspace", "            e = C[m, :, j][:, None] - C[m, :, j][None, :]", "            e = C[m, :, j][:, None] - C[(m + 1) % M, :, j][None, :]"),
     ("sdc_lut_data_row", "    lut = T[np.arange(T.shape[0]), codes]", "    lut = T[np.arange(T.shape[0]), (codes + 1) % T.shape[1]]"),
     ("reconstruct_wrong_subspace", "    return np.concatenate([C[m][codes[:, m]] for m in range(M)], axis=1)", "    return np.concatenate([C[m][codes[:, (m + 1) % M]] for m in range(M)], axis=1)"),
+    ("hash_mask_not_modulus", "rows.append(splitmix64(key ^ salt) % n_rows)",
+     "rows.append(splitmix64(key ^ salt) & (n_rows - 1))"),
+    ("hash_salt_seed_xor_index", "salt = splitmix64((hash_seed + i) & _MASK64)",
+     "salt = splitmix64((hash_seed ^ i) & _MASK64)"),
     ("exact_query_index_shift", "        e = x[ids, j].astype(dtype) - q[j]", "        e = x[ids, j].astype(dtype) - q[(j + 1) % q.shape[0]]"),
 ]
 

@@ -70,6 +70,62 @@ def test_hashed_rows_range_seed_and_spread():
     assert O.hashed_rows(k, 1, B, 7)[0] == O.splitmix64(k ^ O.splitmix64(7)) % B
 
 
+def test_hashed_row_from_published_splitmix64_outputs():
+    """A bank row fixed by the published SplitMix64 sequence alone.  With seed
+    s0 the generator's first two outputs are SM(s0) and SM(s0 + gamma).  Take
+    hash function i = 3 under seed s0 + gamma - 3: its salt is
+    SM(s0 + gamma), the second published output; for the key
+    (second output) XOR s0, key XOR salt = s0, whose hash is the first
+    published output.  So row_3 = (first output) mod B, an integer computed
+    here without the oracle.  B = 45,000 is a bank size of the paper's
+    Table 2 (not a power of two, so mod and a bit mask differ), 4,097 a
+    second non-power-of-two check."""
+    (row,) = _golden_lines("splitmix64.txt")
+    s0, out1, out2 = int(row[0]), int(row[1]), int(row[2])
+    gamma, mask = 0x9E3779B97F4A7C15, (1 << 64) - 1
+    seed = (s0 + gamma - 3) & mask
+    assert (seed ^ 3) != (seed + 3) & mask          # salting by seed XOR i would differ
+    key = out2 ^ s0
+    for B in (45000, 4097):
+        rows = O.hashed_rows(key, 4, B, seed)
+        assert rows[3] == out1 % B, (B, rows)
+        assert all(0 <= r < B for r in rows)
+
+
+def test_hashed_rows_seed_shift():
+    """Hash function i under seed s is hash function 0 under seed s + i (the h
+    functions are the members s, s + 1, ..., s + h - 1 of one family), for
+    seeds where adding i carries across bits."""
+    rng = np.random.default_rng(5)
+    for t in range(200):
+        key = int(rng.integers(0, 1 << 63)) * 2 + t % 2
+        seed = int(rng.integers(0, 1 << 62)) | 0x7             # low bits set: s + i carries
+        B = int(rng.integers(2, 100000))
+        rows = O.hashed_rows(key, 6, B, seed)
+        for i in range(6):
+            assert rows[i] == O.hashed_rows(key, 1, B, seed + i)[0], (t, i)
+
+
+@pytest.mark.parametrize("B", [45000, 4097])
+def test_hashed_rows_cover_non_power_of_two_bank(B):
+    """Rows reach every part of a bank whose size is not a power of two:
+    close to all rows are hit and the hits are uniform over 45 (or 17)
+    equal slices (a bit mask instead of the modulus reaches only the rows
+    whose bits lie inside B - 1)."""
+    n_keys = 4 * B
+    keys = [O.fnv1a64(struct.pack("<q", i)) for i in range(n_keys)]
+    rows = np.array([O.hashed_rows(k, 1, B, 0x5EED)[0] for k in keys])
+    assert rows.min() >= 0 and rows.max() < B
+    hit = np.unique(rows).size / B
+    assert hit > 0.97, hit                  # 1 - e^-4 = 0.982 expected
+    assert rows.max() >= B - 20
+    n_slices = 45 if B == 45000 else 17
+    counts = np.bincount(rows * n_slices // B, minlength=n_slices)
+    exp = n_keys / n_slices
+    chi2 = ((counts - exp) ** 2 / exp).sum()
+    assert chi2 < 3 * n_slices, chi2        # about n_slices - 1 expected
+
+
 # ---------------------------------------------------------------- softplus
 def test_softplus_closed_forms():
     x = np.array([0.0, math.log(math.e - 1.0), 25.0, 100.0, -30.0, 1000.0], dtype=np.float64)

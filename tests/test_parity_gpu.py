@@ -121,8 +121,10 @@ def test_end_to_end_c1_from_raw_inputs(B, c1, conditioned):
 
 # -------------------------------------------------------------- edge cases
 def _edge_index(B, N, M, dsub, n_attr=2, domain=50, seed=0, conditioned=True, max_k=128,
-                max_batch=64, cluster_cols=()):
-    ix = random_index(N, M, dsub, n_attr, domain, seed, device="cuda")
+                max_batch=64, cluster_cols=(), bank_rows=64, h=None):
+    ix = random_index(N, M, dsub, n_attr, domain, seed, device="cuda", bank_rows=bank_rows)
+    if h is not None:
+        ix["h"] = h
     idx = B.Index(ix["codes"], ix["C_pq"], ix["attrs"], ix["bank"] if conditioned else None,
                   ix["W"] if conditioned else None, ix["r"], ix["h"], ix["hash_seed"],
                   max_batch=max_batch, max_k=max_k, cluster_cols=cluster_cols)
@@ -171,6 +173,36 @@ def test_pool_smaller_than_k_and_empty_pool(B):
     preds = [[(0, 7, 8)], [(0, 7, 7)], [(0, 9, 3)], [(0, -(1 << 62), 1 << 62), (1, 999, 1000)]]
     ids = _run_and_check(B, idx, ox, preds, k=20, dsub=8, M=16)
     assert np.all(ids[1] == -1) and np.all(ids[2] == -1)
+
+
+@pytest.mark.parametrize("cluster_cols", [(), (0,)])
+def test_non_power_of_two_bank(B, cluster_cols):
+    """B = 45,000 bank rows (a bank size of the paper's Table 2) with h = 3
+    hash functions: alpha and w_f bit-exact, and the conditioned search from
+    raw inputs equal to the oracle's."""
+    say(f"[bank] B=45000 h=3 cluster={cluster_cols}")
+    idx, ox = _edge_index(B, 20_000, 16, 8, n_attr=2, domain=1000, seed=45, bank_rows=45000, h=3,
+                          cluster_cols=cluster_cols)
+    rng = np.random.default_rng(45)
+    preds = [[(0, int(lo), int(lo) + 100)] for lo in rng.integers(0, 900, 40)] + \
+            [[(0, 5, 500), (1, 0, 300)], [], [(1, 17, 18)]]
+    g = torch.Generator(device="cuda").manual_seed(46)
+    q = torch.randn(len(preds), 128, device="cuda", generator=g)
+    wz = 0.5413 + 0.1 * torch.randn(len(preds), 128, device="cuda", generator=g)
+    alpha, wf = idx.select_codebook(q, preds, wz)
+    torch.cuda.synchronize()
+    alpha_h, wf_h = _np(alpha), _np(wf)
+    masked_differs = 0
+    for i, p in enumerate(preds):
+        a_o, wf_o = O.select_codebook(_np(q[i]), p, ox["bank"], 3, ox["hash_seed"], _np(wz[i]))
+        assert_bitexact(alpha_h[i], a_o, f"alpha q{i}")
+        assert_bitexact(wf_h[i], wf_o, f"w_f q{i}")
+        key = O.fingerprint(_np(q[i]), p)
+        rows = O.hashed_rows(key, 3, 45000, ox["hash_seed"])
+        masked = [O.splitmix64(key ^ O.splitmix64(ox["hash_seed"] + j)) & 44999 for j in range(3)]
+        masked_differs += rows != masked
+    assert masked_differs >= len(preds) - 1     # the modulus, not a bit mask, decides the rows
+    _run_and_check(B, idx, ox, preds, k=10, dsub=8, M=16, seed=47)
 
 
 def test_identity_index_and_fp16_tables(B):
