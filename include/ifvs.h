@@ -213,6 +213,31 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
                                  int32_t* ids_out, float* dist_out, uint32_t* bitmap_out,
                                  void* stream);
 
+/* ifvs_filtered_search_noalloc -- ifvs_filtered_search for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation calls.  Same arguments and the same
+ * results, bit for bit; the call allocates nothing.  Its workspace is a
+ * static array of 64 MiB of device memory, one copy per GPU, placed with the
+ * library's code object and held until the process ends.
+ *  - Every call on one GPU uses that GPU's array: calls that overlap on one
+ *    GPU (other streams or threads, any index handle) race and corrupt each
+ *    other's results, so serialize them.  The array keeps the last call's
+ *    contents; nothing in it has to start at zero.
+ *  - A batch takes 256 + 28 bytes per query (predicates, order, intervals,
+ *    thresholds), 1 MiB of scan dispatch order, ceil(n/64) * 8 bytes of
+ *    selection words per query when a predicate has clauses the row order
+ *    does not resolve (or bitmap_out is given), and k * 64 bytes per query
+ *    and code chunk of top-k partials; the number of chunks adapts to the
+ *    room that is left.
+ *  - Masked batches score every query by the tiled scan (no row-list gather).
+ * Errors: as ifvs_filtered_search, plus IFVS_E_INVALID when the batch does not
+ * fit the 64 MiB with one code chunk per query (send fewer queries per call,
+ * or use ifvs_filtered_search). */
+ifvs_status ifvs_filtered_search_noalloc(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
+                                         const void* lut, int32_t lut_dtype, int32_t k,
+                                         int32_t* ids_out, float* dist_out, uint32_t* bitmap_out,
+                                         void* stream);
+
 /* ifvs_load_vectors -- attach the full-precision base vectors, for exact
  * filtered kNN (ifvs_exact_search).  The paper takes the exact top-k over
  * the predicate-passing vectors as its ground truth (Section 3.1), and its

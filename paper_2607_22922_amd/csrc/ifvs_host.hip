@@ -15,6 +15,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <limits>
+#include <mutex>
 #include <numeric>
 #include <string>
 #include <vector>
@@ -71,6 +72,45 @@ constexpr int64_t kMaxValueTable = int64_t{1} << 22;   // entries (16 MB) of the
 
 constexpr int64_t kI32Min = std::numeric_limits<int32_t>::min();
 constexpr int64_t kI32End = int64_t(std::numeric_limits<int32_t>::max()) + 1;
+
+}  // namespace
+
+// Workspace of ifvs_filtered_search_noalloc: a static array in device memory,
+// one copy on every GPU the library runs on, placed with the code object (no
+// allocation call at run time) and held until the process ends.  In host code
+// `scratch` names a host-side stand-in, never the device copy: kernels and
+// copies use the device address that static_scratch_bind() looks up once per
+// device (hipGetSymbolAddress with that device current).
+constexpr size_t kStaticScratchBytes = size_t{64} << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};   // device address of `scratch` per device (null: not looked up)
+
+// Look up this device's copy of the static scratch array (the current device
+// must be `device`); later calls for the same device return at once.
+ifvs_status static_scratch_bind(int device) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (device < 0 || device >= kMaxDevices)
+    return fail(IFVS_E_UNSUPPORTED, "device ordinal " + std::to_string(device) + " beyond the static scratch table");
+  if (g_scratch_dev[device]) return IFVS_OK;
+  void* p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess || p == nullptr) {
+    (void)hipGetLastError();
+    return fail(IFVS_E_HIP, std::string("locating the static scratch array: ") + hipGetErrorString(e));
+  }
+  g_scratch_dev[device] = p;
+  return IFVS_OK;
+}
+
+void* static_scratch_ptr(int device) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  return device >= 0 && device < kMaxDevices ? g_scratch_dev[device] : nullptr;
+}
 
 }  // namespace
 
@@ -237,6 +277,84 @@ ifvs_status dev_alloc(T** p, size_t count, const char* what) {
     (void)hipGetLastError();
     return fail(IFVS_E_NOMEM, std::string("device allocation failed: ") + what);
   }
+  return IFVS_OK;
+}
+
+// Device memory one filtered search works in: the index's workspace, or, for
+// ifvs_filtered_search_noalloc, pieces of the library's static scratch array.
+struct SearchWs {
+  DevPred* preds = nullptr;          // [nq] normalized predicates
+  int32_t* qorder = nullptr;         // [nq] scan order
+  int64_t* iv = nullptr;             // [nq][2] row intervals
+  uint64_t* gthr = nullptr;          // [nq] shared scan thresholds
+  int32_t* slot_order = nullptr;     // chunk-grid dispatch order
+  int64_t slot_order_cap = 0;
+  uint64_t* bitmap = nullptr;        // [nq][stride64] selection words (null: batch needs none)
+  int64_t stride64 = 0;
+  unsigned long long* counts = nullptr;  // pool sizes and their per-part prefix sums (gather scan)
+  uint32_t* count_parts = nullptr;
+  int32_t* lists = nullptr;          // [nq][list_cap] row lists (null: no gather scan)
+  int32_t* list_n = nullptr;
+  int32_t* qmode = nullptr;
+  int64_t list_cap = 0;
+  uint64_t* partials = nullptr;      // per-wavefront top-k keys
+  size_t partial_keys = 0;
+};
+
+SearchWs index_ws(const ifvs_index* idx) {
+  SearchWs w;
+  w.preds = idx->preds_dev;
+  w.qorder = idx->qorder_dev;
+  w.iv = idx->iv_dev;
+  w.gthr = idx->gthr_dev;
+  w.slot_order = idx->slot_order_dev;
+  w.slot_order_cap = idx->slot_order_cap;
+  w.bitmap = idx->bitmap;
+  w.stride64 = idx->stride64;
+  w.counts = idx->counts;
+  w.count_parts = idx->count_parts;
+  w.lists = idx->lists;
+  w.list_n = idx->list_n;
+  w.qmode = idx->qmode;
+  w.list_cap = idx->list_cap;
+  w.partials = idx->partials;
+  w.partial_keys = idx->partial_keys;
+  return w;
+}
+
+// The search's workspace carved from the device's static scratch array, in
+// 256-byte aligned pieces: predicates, scan order, intervals, thresholds,
+// selection bitmaps when the batch needs them, the dispatch order, and all
+// the rest for top-k partials (the planner keeps the chunk count within it).
+// Nothing in it needs to start at zero: the interval kernel resets the
+// thresholds, and every other piece is written before it is read.
+ifvs_status carve_static_ws(const ifvs_index* idx, int32_t nq, int32_t k, bool bitmaps, SearchWs* ws) {
+  char* base = static_cast<char*>(static_scratch_ptr(idx->device));
+  if (!base) return fail(IFVS_E_STATE, "the static scratch array of this device was not looked up");
+  size_t used = 0;
+  auto take = [&](size_t bytes) {
+    used = (used + 255) & ~size_t{255};
+    char* p = base + used;
+    used += bytes;
+    return p;
+  };
+  const size_t n = static_cast<size_t>(nq);
+  ws->preds = reinterpret_cast<DevPred*>(take(sizeof(DevPred) * n));
+  ws->qorder = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * n));
+  ws->iv = reinterpret_cast<int64_t*>(take(2 * sizeof(int64_t) * n));
+  ws->gthr = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * n));
+  ws->stride64 = idx->stride64;
+  ws->bitmap = bitmaps ? reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * n * idx->stride64)) : nullptr;
+  ws->slot_order_cap = std::min<int64_t>(idx->slot_order_cap, int64_t{1} << 18);
+  ws->slot_order = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * ws->slot_order_cap));
+  used = (used + 255) & ~size_t{255};
+  const size_t min_partials = n * kScanWaves * static_cast<size_t>(k) * sizeof(uint64_t);
+  if (used + min_partials > kStaticScratchBytes)
+    return fail(IFVS_E_INVALID, "this batch needs " + std::to_string(used + min_partials) +
+                                    " bytes of scratch, more than the " + std::to_string(kStaticScratchBytes) +
+                                    " bytes of the allocation-free search (fewer queries, or ifvs_filtered_search)");
+  ws->partials = reinterpret_cast<uint64_t*>(base + used);
+  ws->partial_keys = (kStaticScratchBytes - used) / sizeof(uint64_t);
   return IFVS_OK;
 }
 
@@ -526,7 +644,7 @@ int64_t gather_auto_rows(const ifvs_index* idx) { return idx->n * idx->opt_gathe
 // code tiles across queries would not help.  Otherwise (masked rows) tiles
 // of several queries share each pass over the codes.
 ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_dtype,
-                      bool interval_batch, int64_t span_tiles, ScanPlan* plan) {
+                      bool interval_batch, int64_t span_tiles, size_t partial_keys, ScanPlan* plan) {
   const int lut_bytes = lut_dtype == IFVS_LUT_F16 ? 2 : 4;
   const int qmax = scan_max_qtile(idx->m, lut_bytes, k);
   if (qmax < 1)
@@ -588,7 +706,7 @@ ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_
   }
   if (idx->opt_splits > 0) splits = idx->opt_splits;
   splits = std::min<int64_t>(splits, std::max<int64_t>(1, (idx->n_tiles + plan->min_chunk - 1) / plan->min_chunk));
-  const int64_t cap = static_cast<int64_t>(idx->partial_keys /
+  const int64_t cap = static_cast<int64_t>(partial_keys /
                                            (static_cast<size_t>(std::max(1, nq)) * kScanWaves * k));
   splits = std::max<int64_t>(1, std::min<int64_t>(splits, std::min<int64_t>(cap, 65535)));
   if (plan->abs_cells && splits != (idx->n_tiles + plan->chunk_tiles - 1) / plan->chunk_tiles) {
@@ -611,18 +729,19 @@ ifvs_status plan_scan(const ifvs_index* idx, int32_t nq, int32_t k, int32_t lut_
   return IFVS_OK;
 }
 
-ifvs_status filter_into_workspace(ifvs_index* idx, int32_t nq, bool residual_only, bool counts,
-                                  hipStream_t s) {
+ifvs_status filter_into_workspace(ifvs_index* idx, const SearchWs& ws, int32_t nq, bool residual_only,
+                                  bool counts, hipStream_t s) {
   IFVS_LAUNCH(idx, kStFilter, s, "launching filter kernel",
               launch_filter(residual_only ? idx->attrs_phys : idx->attrs, idx->n, idx->n_attr,
-                            idx->preds_dev, nq, residual_only, idx->bitmap, idx->stride64,
-                            counts ? idx->counts : nullptr, idx->count_parts, s));
+                            ws.preds, nq, residual_only, ws.bitmap, ws.stride64,
+                            counts ? ws.counts : nullptr, ws.count_parts, s));
   return IFVS_OK;
 }
 
-ifvs_status copy_bitmaps_out(ifvs_index* idx, int32_t nq, uint32_t* bitmap_out, hipStream_t s) {
+ifvs_status copy_bitmaps_out(ifvs_index* idx, const SearchWs& ws, int32_t nq, uint32_t* bitmap_out,
+                             hipStream_t s) {
   const size_t words = static_cast<size_t>((idx->n + 31) / 32);
-  IFVS_HIP(hipMemcpy2DAsync(bitmap_out, words * 4, idx->bitmap, idx->stride64 * 8, words * 4, nq,
+  IFVS_HIP(hipMemcpy2DAsync(bitmap_out, words * 4, ws.bitmap, ws.stride64 * 8, words * 4, nq,
                             hipMemcpyDeviceToDevice, s),
            "copying bitmaps");
   return IFVS_OK;
@@ -667,6 +786,7 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
     return st;
   };
   if (hipError_t e = hipGetDevice(&idx->device); e != hipSuccess) return bail(hip_fail(e, "hipGetDevice"));
+  if (ifvs_status st0 = static_scratch_bind(idx->device); st0 != IFVS_OK) return bail(st0);
   idx->n = d.n;
   idx->dim = d.dim;
   idx->m = d.m;
@@ -941,17 +1061,26 @@ ifvs_status ifvs_filter(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
   int slot = 0;
   if (ifvs_status st = stage_predicates(idx, nq, preds, false, true, s, &slot); st != IFVS_OK) return st;
-  if (ifvs_status st = filter_into_workspace(idx, nq, false, true, s); st != IFVS_OK) return st;
-  if (ifvs_status st = copy_bitmaps_out(idx, nq, bitmap_out, s); st != IFVS_OK) return st;
+  const SearchWs ws = index_ws(idx);
+  if (ifvs_status st = filter_into_workspace(idx, ws, nq, false, true, s); st != IFVS_OK) return st;
+  if (ifvs_status st = copy_bitmaps_out(idx, ws, nq, bitmap_out, s); st != IFVS_OK) return st;
   if (count_out)
     IFVS_HIP(hipMemcpyAsync(count_out, idx->counts, sizeof(int64_t) * nq, hipMemcpyDeviceToDevice, s),
              "copying pool sizes");
   return IFVS_OK;
 }
 
-ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
-                                 const void* lut, int32_t lut_dtype, int32_t k, int32_t* ids_out,
-                                 float* dist_out, uint32_t* bitmap_out, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Filter, Rank and Select for one batch.  With static_scratch the device
+// workspace is carved from the static array of the index's device instead of
+// the index's own workspace (no gather scan then: every query takes the tiled
+// scan, with the same results).
+ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds, const void* lut,
+                        int32_t lut_dtype, int32_t k, int32_t* ids_out, float* dist_out, uint32_t* bitmap_out,
+                        void* stream, bool static_scratch) {
   if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
   if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
   if (lut_dtype != IFVS_LUT_F32 && lut_dtype != IFVS_LUT_F16) return fail(IFVS_E_INVALID, "unknown lut_dtype");
@@ -961,7 +1090,7 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   if (!lut || !ids_out || !dist_out) return fail(IFVS_E_INVALID, "lut, ids_out or dist_out is NULL");
   if (reinterpret_cast<uintptr_t>(lut) % 16 != 0) return fail(IFVS_E_INVALID, "lut must be 16-byte aligned");
   ScanPlan probe{};
-  if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, false, 0, &probe); st != IFVS_OK) return st;
+  if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, false, 0, size_t{1} << 40, &probe); st != IFVS_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
   DevPred* host = nullptr;
@@ -975,8 +1104,16 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
     interval_batch = interval_batch && host[i].iv_mode != 0;
     if (idx->n_cluster > 0) span = std::max(span, estimate_interval_tiles(idx, host[i]));
   }
+  SearchWs ws;
+  if (!static_scratch) {
+    ws = index_ws(idx);
+  } else if (ifvs_status st = carve_static_ws(idx, nq, k, need_bitmap || bitmap_out != nullptr, &ws);
+             st != IFVS_OK) {
+    return st;
+  }
   ScanPlan plan{};
-  if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, interval_batch, span, &plan); st != IFVS_OK) return st;
+  if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, interval_batch, span, ws.partial_keys, &plan); st != IFVS_OK)
+    return st;
   // Chunk-grid scans: the slot dispatch order goes into the staging slot and
   // the interval kernel copies it to the device.
   const int32_t* qorder_host = reinterpret_cast<const int32_t*>(host + idx->max_batch);
@@ -984,38 +1121,38 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   const int64_t n_order = plan.abs_cells && idx->opt_slot_order == 0
                               ? static_cast<int64_t>(8) * ((((nq + plan.qtile - 1) / plan.qtile) + 7) / 8) * plan.splits
                               : 0;
-  const bool ordered = n_order > 0 && n_order <= idx->slot_order_cap;
+  const bool ordered = n_order > 0 && n_order <= ws.slot_order_cap;
   if (ordered) order_scan_slots(idx, host, qorder_host, nq, plan, order_host);
   IFVS_LAUNCH(idx, kStFilter, s, "launching interval kernel",
               launch_intervals(idx->attrs_phys, idx->n, idx->c0, idx->c1, idx->vstart, idx->vmin, idx->vcount,
                                idx->staging_dev[slot],
                                reinterpret_cast<const int32_t*>(idx->staging_dev[slot] + idx->max_batch), nq,
-                               idx->preds_dev, idx->qorder_dev, idx->iv_dev, idx->gthr_dev,
+                               ws.preds, ws.qorder, ws.iv, ws.gthr,
                                ordered ? reinterpret_cast<const int32_t*>(idx->staging_dev[slot] + idx->max_batch) +
                                              idx->max_batch
                                        : nullptr,
-                               idx->slot_order_dev, ordered ? n_order : 0, s));
+                               ws.slot_order, ordered ? n_order : 0, s));
   if (ifvs_status st = release_slot(idx, slot, s); st != IFVS_OK) return st;
   // Masked batches: a query whose pool is small is scored from its compacted
   // row list (decided on the device from the pool size); the rest take the
   // tiled scan.  The full selection bitmap (physical order) and the pool
   // sizes come from the Filter stage.
   const int gather_lut = lut_dtype == IFVS_LUT_F16 ? 2 : 4;
-  const bool gather = !interval_batch && idx->codes_rm && idx->opt_gather != 2 &&
+  const bool gather = !interval_batch && idx->codes_rm && ws.lists && idx->opt_gather != 2 &&
                       gather_supported(idx->m, lut_dtype) &&
                       static_cast<size_t>(idx->m) * kKsub * gather_lut + gather_lds_bytes(plan.pool_stride) <=
                           static_cast<size_t>(kLdsBudget);
   if (gather) {
     IFVS_LAUNCH(idx, kStFilter, s, "launching filter kernel",
-                launch_filter(idx->attrs_phys, idx->n, idx->n_attr, idx->preds_dev, nq, false, idx->bitmap,
-                              idx->stride64, idx->counts, idx->count_parts, s));
-    const int64_t max_rows = idx->opt_gather == 1 ? idx->list_cap : std::min(idx->list_cap, gather_auto_rows(idx));
+                launch_filter(idx->attrs_phys, idx->n, idx->n_attr, ws.preds, nq, false, ws.bitmap,
+                              ws.stride64, ws.counts, ws.count_parts, s));
+    const int64_t max_rows = idx->opt_gather == 1 ? ws.list_cap : std::min(ws.list_cap, gather_auto_rows(idx));
     IFVS_LAUNCH(idx, kStFilter, s, "launching compaction kernel",
-                launch_compact(idx->bitmap, idx->stride64, idx->counts, idx->count_parts,
-                               filter_count_parts(idx->n), nq, max_rows, idx->list_cap, idx->lists,
-                               idx->list_n, idx->qmode, s));
+                launch_compact(ws.bitmap, ws.stride64, ws.counts, ws.count_parts,
+                               filter_count_parts(idx->n), nq, max_rows, ws.list_cap, ws.lists,
+                               ws.list_n, ws.qmode, s));
   } else if (need_bitmap) {
-    if (ifvs_status st = filter_into_workspace(idx, nq, true, false, s); st != IFVS_OK) return st;
+    if (ifvs_status st = filter_into_workspace(idx, ws, nq, true, false, s); st != IFVS_OK) return st;
   }
   ScanBatch b{};
   b.codes_t = idx->codes_t;
@@ -1026,17 +1163,17 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
   b.lut = lut;
   b.lut_dtype = lut_dtype;
   b.nq = nq;
-  b.qorder = idx->qorder_dev;
-  b.iv = idx->iv_dev;
-  b.preds = idx->preds_dev;
-  b.bitmap = idx->bitmap;
-  b.stride64 = idx->stride64;
+  b.qorder = ws.qorder;
+  b.iv = ws.iv;
+  b.preds = ws.preds;
+  b.bitmap = ws.bitmap;
+  b.stride64 = ws.stride64;
   b.perm = idx->perm;
   b.k = k;
-  b.partials = idx->partials;
-  b.gthr = idx->gthr_dev;
-  b.mode = gather ? idx->qmode : nullptr;
-  b.slot_order = ordered ? idx->slot_order_dev : nullptr;
+  b.partials = ws.partials;
+  b.gthr = ws.gthr;
+  b.mode = gather ? ws.qmode : nullptr;
+  b.slot_order = ordered ? ws.slot_order : nullptr;
   IFVS_LAUNCH(idx, kStScan, s, "launching scan kernel", launch_scan(b, plan, s));
   if (gather) {
     GatherBatch g{};
@@ -1046,34 +1183,50 @@ ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predica
     g.lut = lut;
     g.lut_dtype = lut_dtype;
     g.nq = nq;
-    g.qorder = idx->qorder_dev;
-    g.mode = idx->qmode;
-    g.lists = idx->lists;
-    g.list_n = idx->list_n;
-    g.list_cap = idx->list_cap;
+    g.qorder = ws.qorder;
+    g.mode = ws.qmode;
+    g.lists = ws.lists;
+    g.list_n = ws.list_n;
+    g.list_cap = ws.list_cap;
     g.splits = plan.splits;
-    g.gblocks = gather_blocks_per_query(idx->list_cap, plan.splits);
+    g.gblocks = gather_blocks_per_query(ws.list_cap, plan.splits);
     g.perm = idx->perm;
     g.k = k;
     g.pool_stride = plan.pool_stride;
     g.kpl = plan.kpl;
-    g.partials = idx->partials;
-    g.gthr = idx->gthr_dev;
+    g.partials = ws.partials;
+    g.gthr = ws.gthr;
     IFVS_LAUNCH(idx, kStScan, s, "launching gather scan kernel", launch_gather_scan(g, s));
   }
   const int64_t per_query = static_cast<int64_t>(plan.splits) * kScanWaves * k;
   IFVS_LAUNCH(idx, kStMerge, s, "launching top-k merge kernel",
-              launch_topk_merge(idx->partials, nq, per_query, k, idx->iv_dev,
+              launch_topk_merge(ws.partials, nq, per_query, k, ws.iv,
                                 plan.abs_cells ? plan.chunk_tiles : 0, static_cast<int64_t>(kScanWaves) * k,
-                                idx->qorder_dev, ids_out, dist_out, s));
+                                ws.qorder, ids_out, dist_out, s));
   if (bitmap_out) {
     // The Filter stage's bitmaps in id order (the scan itself reads row
     // intervals and residual bits in the physical order).
-    if (ifvs_status st = filter_into_workspace(idx, nq, false, false, s); st != IFVS_OK) return st;
-    if (ifvs_status st = copy_bitmaps_out(idx, nq, bitmap_out, s); st != IFVS_OK) return st;
+    if (ifvs_status st = filter_into_workspace(idx, ws, nq, false, false, s); st != IFVS_OK) return st;
+    if (ifvs_status st = copy_bitmaps_out(idx, ws, nq, bitmap_out, s); st != IFVS_OK) return st;
   }
   idx->last_plan = plan;
   return IFVS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
+                                 const void* lut, int32_t lut_dtype, int32_t k, int32_t* ids_out,
+                                 float* dist_out, uint32_t* bitmap_out, void* stream) {
+  return search_impl(idx, nq, preds, lut, lut_dtype, k, ids_out, dist_out, bitmap_out, stream, false);
+}
+
+ifvs_status ifvs_filtered_search_noalloc(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
+                                         const void* lut, int32_t lut_dtype, int32_t k, int32_t* ids_out,
+                                         float* dist_out, uint32_t* bitmap_out, void* stream) {
+  return search_impl(idx, nq, preds, lut, lut_dtype, k, ids_out, dist_out, bitmap_out, stream, true);
 }
 
 }  // extern "C"
@@ -1225,7 +1378,7 @@ ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const
                                idx->slot_order_dev, 0, s));
   if (ifvs_status st = release_slot(idx, slot, s); st != IFVS_OK) return st;
   if (need_bitmap)
-    if (ifvs_status st = filter_into_workspace(idx, nq, true, false, s); st != IFVS_OK) return st;
+    if (ifvs_status st = filter_into_workspace(idx, index_ws(idx), nq, true, false, s); st != IFVS_OK) return st;
   IFVS_LAUNCH(idx, kStCondition, s, "launching exact query kernel",
               launch_exact_queries(q, idx->dim, nq, idx->qorder_dev, idx->xmax, idx->qb, idx->qn_x, idx->eps_x,
                                    idx->cand_n_x, s));

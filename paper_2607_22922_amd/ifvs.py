@@ -33,7 +33,8 @@ STAGES = ("condition", "lut", "filter", "scan", "merge")
 EXPORTED = ("ifvs_load_index", "ifvs_free_index", "ifvs_select_codebook", "ifvs_build_lut",
             "ifvs_filter", "ifvs_filtered_search", "ifvs_set_option", "ifvs_last_plan",
             "ifvs_read_profile", "ifvs_last_error", "ifvs_load_vectors", "ifvs_exact_search",
-            "ifvs_build_sdc_lut", "ifvs_load_reconstructions", "ifvs_train_step", "ifvs_read_params")
+            "ifvs_build_sdc_lut", "ifvs_load_reconstructions", "ifvs_train_step", "ifvs_read_params",
+            "ifvs_filtered_search_noalloc")
 
 
 class IfvsError(RuntimeError):
@@ -89,6 +90,7 @@ def _load_library() -> ctypes.CDLL:
         "ifvs_build_lut": ([vp, i32, vp, vp, vp, i32, vp, vp], i32),
         "ifvs_filter": ([vp, i32, vp, vp, vp, vp], i32),
         "ifvs_filtered_search": ([vp, i32, vp, vp, i32, i32, vp, vp, vp, vp], i32),
+        "ifvs_filtered_search_noalloc": ([vp, i32, vp, vp, i32, i32, vp, vp, vp, vp], i32),
         "ifvs_set_option": ([vp, i32, i64], i32),
         "ifvs_last_plan": ([vp, ctypes.POINTER(ctypes.c_int64)], i32),
         "ifvs_read_profile": ([vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)], i32),
@@ -244,6 +246,14 @@ class Index:
         _check(_lib.ifvs_filtered_search(self.handle, nq, preds_c, lut.data_ptr(), lut_dtype, k,
                                          ids_out.data_ptr(), dist_out.data_ptr(), _ptr(bitmap_out),
                                          _stream(stream)))
+
+    def search_noalloc_into(self, nq, preds_c, lut, lut_dtype, k, ids_out, dist_out, bitmap_out=None,
+                            stream=None):
+        """ifvs_filtered_search_noalloc: the same search with the library's
+        static workspace (no allocation in the call)."""
+        _check(_lib.ifvs_filtered_search_noalloc(self.handle, nq, preds_c, lut.data_ptr(), lut_dtype, k,
+                                                 ids_out.data_ptr(), dist_out.data_ptr(), _ptr(bitmap_out),
+                                                 _stream(stream)))
 
     def load_vectors(self, x):
         """Attach the full-precision vectors [n][dim] (ifvs_load_vectors)."""
