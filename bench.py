@@ -203,7 +203,13 @@ def main():
                     help="synthetic workload (c4, the 10M-vector one, is the headline)")
     ap.add_argument("--queries", type=int, default=None,
                     help="queries drawn per bin (default: the config's count, at most 10,000)")
-    ap.add_argument("--cpu-sample", type=int, default=2, help="oracle queries per bin (0 = skip)")
+    ap.add_argument("--cpu-sample", type=int, default=2,
+                    help="oracle queries per bin timed in one process on one core (0 = skip)")
+    ap.add_argument("--cpu-pool-queries", type=int, default=None,
+                    help="oracle queries per bin timed with one single-threaded process per core "
+                         "(0 = skip; default 64 on c4, 16 on c1-c3, 4 on c5)")
+    ap.add_argument("--cpu-pool-workers", type=int, default=16,
+                    help="at most this many oracle processes (the host cores of the job)")
     ap.add_argument("--recall-queries", type=int, default=None,
                     help="queries per bin checked against exact filtered kNN (default 256; 100 on c1 and c5)")
     ap.add_argument("--plain-steps", type=int, default=None,
@@ -240,6 +246,8 @@ def main():
     batch, k = min(cfg.get("batch", 256), n_q), cfg["k"]
     if args.plain_steps is None:
         args.plain_steps = 5 if name == "c4" else 0
+    if args.cpu_pool_queries is None:
+        args.cpu_pool_queries = {"c4": 64, "c5": 4}.get(name, 16)
     if args.recall_queries is None:
         args.recall_queries = 100 if name in ("c1", "c5") else 256
     if args.exact_steps is None:
@@ -533,36 +541,65 @@ def main():
                              "bf16 matrix-core screening with an error bound, exact scoring of survivors"}
         log(f"[bench] exact search: {exact_out['qps']:.0f} queries/s; {json.dumps(ex_bins)}")
 
-    # Oracle on the host cores: a bounded sample of the same workload.
+    # Oracle on the host cores: a bounded sample of the same workload, in two
+    # modes -- one process on one core, and one single-threaded process per
+    # core -- each on the first queries of every bin, every answer compared
+    # with the GPU's (ids and distance bits).
     cpu = None
-    if args.cpu_sample > 0:
-        import oracle as O
+    if args.cpu_sample > 0 or args.cpu_pool_queries > 0:
+        from oracle.pool import OraclePool, cpu_model, host_cores
         ox = dict(codes=w.codes.cpu().numpy(), C_pq=w.C_pq.cpu().numpy(),
                   attrs=w.attrs.cpu().numpy(), bank=w.bank.cpu().numpy(), W=w.W.cpu().numpy(),
                   r=w.r, h=w.h, hash_seed=w.hash_seed)
-        nq_cpu, agree = 0, True
-        t_cpu = 0.0
+        n_gpu = max(args.cpu_sample, args.cpu_pool_queries)
+        n_gpu = min(n_gpu, batch)
+        gpu_res = {}
         for s in bins:
-            q = w.queries[:args.cpu_sample]
-            preds = w.preds[s][:args.cpu_sample]
-            wz = w.w_z[s][:args.cpu_sample]
-            a_, f_ = clus.select_codebook(q, preds, wz)
+            q = w.queries[:n_gpu]
+            preds = w.preds[s][:n_gpu]
+            a_, f_ = clus.select_codebook(q, preds, w.w_z[s][:n_gpu])
             lt = clus.build_lut(q, a_, f_, lut_dt)
             g_ids, g_d = clus.search(preds, lt, k, lut_dt)
-            g_ids, g_d = g_ids.cpu().numpy(), g_d.cpu().numpy()
-            qh, wzh = q.cpu().numpy(), wz.cpu().numpy()
-            for i in range(args.cpu_sample):
-                tt = time.perf_counter()
-                res = O.filtered_search(ox, qh[i], preds[i], k, w_z=wzh[i], lut_dtype=args.lut)
-                t_cpu += time.perf_counter() - tt
-                nq_cpu += 1
-                agree &= bool(np.array_equal(res["ids"], g_ids[i]) and
-                              np.array_equal(res["dist"].view(np.uint32), g_d[i].view(np.uint32)))
-        cpu = {"value": nq_cpu / t_cpu, "unit": "queries/s", "cores": 1, "kind": "oracle",
-               "sample": f"{args.cpu_sample} queries per bin x {len(bins)} bins of the same "
-                         f"workload, conditioned mode, numpy single thread, {t_cpu:.1f} s",
-               "ids_and_dist_bits_match_gpu": agree}
-        log(f"[bench] oracle: {cpu['value']:.3f} queries/s, results match: {agree}")
+            gpu_res[s] = (g_ids.cpu().numpy(), g_d.cpu().numpy(), q.cpu().numpy(),
+                          w.w_z[s][:n_gpu].cpu().numpy())
+
+        def oracle_mode(workers, per_bin):
+            tasks = [((s, i), gpu_res[s][2][i], w.preds[s][i], k, gpu_res[s][3][i], args.lut, True)
+                     for s in bins for i in range(per_bin)]
+            with OraclePool(ox, workers) as pool:
+                pool.search(tasks[:workers])                 # workers up, index mapped
+                t_ = time.perf_counter()
+                res = pool.search(tasks)
+                wall = time.perf_counter() - t_
+            agree = all(np.array_equal(ids_o, gpu_res[key[0]][0][key[1]]) and
+                        np.array_equal(d_o.view(np.uint32), gpu_res[key[0]][1][key[1]].view(np.uint32))
+                        for key, ids_o, d_o, _ in res)
+            return {"value": len(tasks) / wall, "unit": "queries/s", "cores": workers,
+                    "queries": len(tasks), "wall_s": round(wall, 2),
+                    "cpu_s": round(sum(r[3] for r in res), 2),
+                    "ids_and_dist_bits_match_gpu": bool(agree)}
+
+        model, avail = cpu_model(), host_cores()
+        single = oracle_mode(1, min(args.cpu_sample, n_gpu)) if args.cpu_sample > 0 else None
+        if single:
+            log(f"[bench] oracle, 1 core: {single['value']:.3f} queries/s, results match: "
+                f"{single['ids_and_dist_bits_match_gpu']}")
+        multi = None
+        if args.cpu_pool_queries > 0:
+            workers = max(1, min(avail, args.cpu_pool_workers))
+            multi = oracle_mode(workers, min(args.cpu_pool_queries, n_gpu))
+            log(f"[bench] oracle, {workers} processes: {multi['value']:.3f} queries/s, results match: "
+                f"{multi['ids_and_dist_bits_match_gpu']}")
+        head = multi or single
+        per = (min(args.cpu_pool_queries, n_gpu) if multi else min(args.cpu_sample, n_gpu))
+        cpu = {"value": head["value"], "unit": "queries/s", "cores": head["cores"], "kind": "oracle",
+               "sample": f"first {per} queries of each of the {len(bins)} bins of the same workload "
+                         f"({head['queries']} queries), conditioned mode, "
+                         + ("one single-threaded numpy process per core" if multi else "one numpy process")
+                         + f", {head['wall_s']} s wall",
+               "cpu_model": model, "affinity_cores": avail,
+               "ids_and_dist_bits_match_gpu": head["ids_and_dist_bits_match_gpu"],
+               "single_core": single, "all_cores": multi}
 
     if args.copy_calibration:
         n_el = 1 << 28                                       # 1 GiB in, 1 GiB out

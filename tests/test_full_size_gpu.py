@@ -1,20 +1,34 @@
-"""Full-size workloads on the GPU, checked by sampling.
+"""Full-size workloads on the GPU, checked against the oracle.
 
 Every returned row of a batch is checked for properties that hold at any
 size (ids pass the predicate, ascending (distance, id), no duplicates, count
-= min(k, |P|), identical on both row layouts); a few queries per selectivity
-bin are recomputed by the CPU oracle one by one (ids and distance bits).
-c4 (10M vectors) runs in the launch configuration bench.py times: clustered
-rows, conditioned mode, batches of 256, k = 10, fp32 tables."""
+= min(k, |P|), identical on both row layouts), and the oracle recomputes
+whole query sets one by one, in a pool of host processes, for an
+element-by-element comparison of ids and distance bits:
+
+* 10M x 96 (c4), in the launch configuration the benchmark times (clustered
+  rows, conditioned mode, batches of 256, k = 10, fp32 tables): all 256
+  queries of a batch at 0.1%, 1% and 10% selectivity, the first 64 at 50%;
+* 1M x 128 with a range and a category clause (c2): 64 queries per bin;
+* 1M x 960 with k = 100 (c3): 32 queries per bin, and 8 more in the fp16
+  table mode;
+* 100M x 128 (c5): 16 queries per bin.
+
+The counts can be raised with IFVS_FULL_ORACLE_SCALE (a multiplier, capped
+at each batch's size)."""
+import os
+
 import numpy as np
 import pytest
 import torch
 
-import oracle as O
+from oracle.pool import OraclePool, host_cores
 from workload import make_workload
 from tests._gpu_util import check_search_row, oracle_from_workload, say
 
 pytestmark = pytest.mark.gpu
+
+SCALE = float(os.environ.get("IFVS_FULL_ORACLE_SCALE", "1"))
 
 
 @pytest.fixture(scope="module")
@@ -47,11 +61,19 @@ def _properties(w, preds, ids, dist, counts, k):
         assert torch.all(got[1:][ties] > got[:-1][ties])
 
 
-def _run_config(B, w, idx, plain, bins, nq, k, sample, conditioned=True, lut_dtype="f32"):
+def _workers():
+    # the machine's CPU share, leaving one core to the test process
+    return max(1, min(15, host_cores() - 1))
+
+
+def _run_config(B, w, idx, plain, bins, nq, k, per_bin, conditioned=True, lut_dtype="f32"):
+    """Searches the first nq queries of every bin on the GPU, checks the
+    properties of every row, and compares the first per_bin[s] queries of
+    bin s with the oracle."""
     dt = B.LUT_F16 if lut_dtype == "f16" else B.LUT_F32
-    ox = oracle_from_workload(w, conditioned)
+    tasks, got = [], {}
     for s in bins:
-        say(f"[full] {w.name} N={w.N} bin={s}")
+        say(f"[full] {w.name} N={w.N} bin={s} ({lut_dtype})")
         preds = w.preds[s][:nq]
         q, wz = w.queries[:nq], w.w_z[s][:nq]
         a, f = idx.select_codebook(q, preds, wz)
@@ -64,11 +86,27 @@ def _run_config(B, w, idx, plain, bins, nq, k, sample, conditioned=True, lut_dty
             i2, d2 = plain.search(preds, lut, k, dt)
             torch.cuda.synchronize()
             assert torch.equal(ids, i2) and torch.equal(dist.view(torch.int32), d2.view(torch.int32))
-        ids_h, dist_h = _np(ids), _np(dist)
-        for i in range(sample):
-            res = O.filtered_search(ox, _np(q[i]), preds[i], k, w_z=_np(wz[i]), lut_dtype=lut_dtype,
-                                    conditioned=conditioned)
-            check_search_row(ids_h[i], dist_h[i], res["ids"], res["dist"], f"{w.name} s={s} q{i}")
+        ids_h, dist_h, q_h, wz_h = _np(ids), _np(dist), _np(q), _np(wz)
+        n_or = min(nq, int(round(per_bin[s] * SCALE)))
+        for i in range(n_or):
+            key = (s, i)
+            got[key] = (ids_h[i], dist_h[i])
+            tasks.append((key, q_h[i], preds[i], k, wz_h[i], lut_dtype, conditioned))
+    ox = oracle_from_workload(w, conditioned)
+    last = [0]
+
+    def progress(done, total):
+        if done == total or done - last[0] >= max(1, total // 10):
+            last[0] = done
+            say(f"[full] {w.name}: oracle {done}/{total}")
+
+    say(f"[full] {w.name}: {len(tasks)} queries to the oracle on {_workers()} host processes")
+    with OraclePool(ox, _workers()) as pool:
+        results = pool.search(tasks, progress)
+    for key, ids_o, dist_o, _ in results:
+        g_ids, g_d = got[key]
+        check_search_row(g_ids, g_d, ids_o, dist_o, f"{w.name} s={key[0]} q{key[1]} ({lut_dtype})")
+    return len(results)
 
 
 def test_c4_10m_bench_configuration(B):
@@ -76,7 +114,8 @@ def test_c4_10m_bench_configuration(B):
     w = make_workload("c4", device="cuda", n_queries=256, keep_x=False)
     clus = B.Index.from_workload(w, max_batch=256, max_k=10, cluster_cols=(0,))
     plain = B.Index.from_workload(w, max_batch=256, max_k=10)
-    _run_config(B, w, clus, plain, w.bins, 256, 10, sample=2)
+    n = _run_config(B, w, clus, plain, w.bins, 256, 10, {0.001: 256, 0.01: 256, 0.1: 256, 0.5: 64})
+    assert n >= 4 * 32
 
 
 def test_c2_1m_two_attributes(B):
@@ -84,20 +123,20 @@ def test_c2_1m_two_attributes(B):
     w = make_workload("c2", device="cuda", n_queries=64, keep_x=False)
     clus = B.Index.from_workload(w, max_batch=64, max_k=10, cluster_cols=(1, 0))
     plain = B.Index.from_workload(w, max_batch=64, max_k=10)
-    _run_config(B, w, clus, plain, w.bins, 64, 10, sample=2)
+    _run_config(B, w, clus, plain, w.bins, 64, 10, {s: 64 for s in w.bins})
 
 
 def test_c3_1m_960d_k100(B):
     say("[full] generating c3 (1M x 960, M = 120, k = 100)")
     w = make_workload("c3", device="cuda", n_queries=32, keep_x=False)
     clus = B.Index.from_workload(w, max_batch=32, max_k=100, cluster_cols=(0,))
-    _run_config(B, w, clus, None, w.bins, 32, 100, sample=2)
+    _run_config(B, w, clus, None, w.bins, 32, 100, {s: 32 for s in w.bins})
     # the fp16 table mode on the same data
-    _run_config(B, w, clus, None, [0.01], 8, 100, sample=1, lut_dtype="f16")
+    _run_config(B, w, clus, None, [0.01], 8, 100, {0.01: 8}, lut_dtype="f16")
 
 
 def test_c5_100m(B):
     say("[full] generating c5 (100M x 128, codes only)")
     w = make_workload("c5", device="cuda", n_queries=16, keep_x=False)
     clus = B.Index.from_workload(w, max_batch=16, max_k=10, cluster_cols=(1, 0))
-    _run_config(B, w, clus, None, w.bins, 16, 10, sample=1)
+    _run_config(B, w, clus, None, w.bins, 16, 10, {s: 16 for s in w.bins})
