@@ -56,8 +56,9 @@ def scan_source_hash() -> str:
 
 
 def read_counters():
-    """HBM traffic of the scan from the committed rocprofv3 counter summary,
-    if it was taken on the current scan source."""
+    """Fabric-side bytes of the scan per launch, overall and per selectivity
+    bin, from the committed rocprofv3 counter summary, if it was taken on the
+    current scan source: {"mean": bytes, "by_bin": {bin: bytes}}."""
     if not os.path.exists(COUNTERS_FILE):
         return None
     kv = {}
@@ -68,9 +69,83 @@ def read_counters():
     if kv.get("scan_source_sha256_16") != scan_source_hash():
         return None
     try:
-        return float(kv["scan_hbm_bytes_per_launch"])
+        by_bin = {}
+        for item in kv["scan_fabric_bytes_per_launch_by_bin"].split(","):
+            b, v = item.split(":")
+            by_bin[b.strip()] = float(v)
+        return {"mean": float(kv["scan_fabric_bytes_per_launch"]), "by_bin": by_bin}
     except (KeyError, ValueError):
         return None
+
+
+SCAN_KERNEL_C4 = "scan_kernel<48, 1, float>"
+
+
+def is_timed_scan_c4(kernel_name):
+    """The timed scan kernel of the 10M-vector workload (not its read-counting build)."""
+    return "scan_kernel<48, 1, float" in kernel_name and "true>" not in kernel_name
+
+
+def summarize_counters(fetch_dir, write_dir, bins, steps, out_path, commands):
+    """Writes the counter summary bench.py reads (see read_counters) from two
+    rocprofv3 --pmc runs of `bench.py --steps S --warmup 0 ... --copy-calibration`
+    (FETCH_SIZE, then WRITE_SIZE): the first 2 * S * len(bins) dispatches of
+    the timed scan kernel are the timed pass and the stage pass, bins in
+    order, S launches each; the copy kernel (1 GiB read, 1 GiB written)
+    calibrates KiB to bytes."""
+    import csv
+    import glob
+
+    def per_dispatch(d, counter):
+        rows = []
+        for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(path) as f:
+                for r in csv.DictReader(f):
+                    if r.get("Counter_Name") == counter:
+                        rows.append((int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
+        agg = {}
+        for did, kname, v in rows:
+            a = agg.setdefault(did, [kname, 0.0])
+            a[1] += v
+        return [(did, agg[did][0], agg[did][1]) for did in sorted(agg)]
+
+    fetch = per_dispatch(fetch_dir, "FETCH_SIZE")
+    write = per_dispatch(write_dir, "WRITE_SIZE")
+    copy_f = [v for _, kn, v in fetch if "neg" in kn.lower()]
+    copy_w = [v for _, kn, v in write if "neg" in kn.lower()]
+    gib_kib = float(1 << 20)
+    f_fac = gib_kib / float(np.median(copy_f))
+    w_fac = gib_kib / float(np.median(copy_w))
+    n_timed = 2 * steps * len(bins)
+    sf = [v for _, kn, v in fetch if is_timed_scan_c4(kn)][:n_timed]
+    sw = [v for _, kn, v in write if is_timed_scan_c4(kn)][:n_timed]
+    if len(sf) < n_timed or len(sw) < n_timed:
+        raise RuntimeError(f"expected {n_timed} scan dispatches, found {len(sf)} / {len(sw)}")
+    by_bin = {}
+    for i, s in enumerate(bins):
+        sel = [j for j in range(n_timed) if (j % (steps * len(bins))) // steps == i]
+        by_bin[str(s)] = float(np.mean([(sf[j] * f_fac + sw[j] * w_fac) * 1024 for j in sel]))
+    mean = float(np.mean([(sf[j] * f_fac + sw[j] * w_fac) * 1024 for j in range(n_timed)]))
+    with open(out_path, "w") as f:
+        f.write("# Fabric-side traffic of the ADC scan kernel (%s) on the 10M-vector\n" % SCAN_KERNEL_C4)
+        f.write("# workload (10M x 96-d, PQ 48x2, clustered rows, batches of 256, k = 10), MI355X.\n")
+        f.write("# Two rocprofv3 counter passes over the benchmark's timed pass and its stage pass\n")
+        f.write("# (%d launches per bin each, bins %s), plus a copy kernel of known size (torch.neg\n"
+                % (steps, "/".join(str(b) for b in bins)))
+        f.write("# over 1 GiB fp32) for calibration.  Counters are KiB per dispatch.  FETCH_SIZE counts\n")
+        f.write("# bytes the L2s request from the fabric: Infinity Cache hits are included (no gfx950\n")
+        f.write("# counter separates them from HBM reads), so this is an upper bound on HBM traffic.\n")
+        for c in commands:
+            f.write("# command: %s\n" % c)
+        f.write("copy_fetch_kib_per_dispatch = %.1f\n" % float(np.median(copy_f)))
+        f.write("copy_write_kib_per_dispatch = %.1f\n" % float(np.median(copy_w)))
+        f.write("fetch_factor = %.5f\nwrite_factor = %.5f\n" % (f_fac, w_fac))
+        f.write("scan_fetch_kib_per_dispatch = %s\n" % ", ".join("%.0f" % v for v in sf))
+        f.write("scan_write_kib_per_dispatch = %s\n" % ", ".join("%.0f" % v for v in sw))
+        f.write("scan_fabric_bytes_per_launch_by_bin = %s\n"
+                % ", ".join("%s:%.0f" % (b, v) for b, v in by_bin.items()))
+        f.write("scan_fabric_bytes_per_launch = %.0f\n" % mean)
+        f.write("scan_source_sha256_16 = %s\n" % scan_source_hash())
 
 
 def clause_tensors(preds, device):
@@ -124,6 +199,11 @@ CLUSTER_COLS = {"c1": (0,), "c2": (1, 0), "c3": (0,), "c4": (0,), "c5": (1, 0)}
 
 SCAN_WAVES = 8   # wavefronts per scan workgroup, each writing k partial keys per chunk
 
+# The benchmark run the scan's counter passes profile: the timed pass and the
+# stage pass only (3 launches per bin each), plus the calibration copy.
+COUNTER_RUN = ("--steps 3 --warmup 0 --plain-steps 0 --cpu-sample 0 --cpu-pool-queries 0 --recall-queries 0 "
+               "--sdc-steps 0 --exact-steps 0 --host-steps 0 --no-lds-roof --copy-calibration")
+
 
 def scan_bytes_interval(w, sorted_attr, preds, plan, k, lut_entry):
     """Algorithmic bytes of one interval-scan launch (one query per tile):
@@ -146,6 +226,53 @@ def scan_bytes_interval(w, sorted_attr, preds, plan, k, lut_entry):
         chunks = float(len(preds) * plan["splits"])
     return (code + len(preds) * w.M * 256 * lut_entry + chunks * SCAN_WAVES * k * 8,
             float((r1 - r0).sum()) * w.M)
+
+
+def scan_union_bytes(w, sorted_attr, preds, plan, k, lut_entry, idx=None):
+    """Bytes one scan launch must move between HBM and the chip at the
+    least: every code tile that some query of the batch selects, read once
+    (one-column intervals; otherwise every row some query selects, at M
+    bytes), each query's table, and the partial top-k lists written."""
+    mw = (w.M + 3) // 4
+    if sorted_attr is not None:
+        lo = torch.tensor([p[0][1] for p in preds], device=sorted_attr.device, dtype=sorted_attr.dtype)
+        hi = torch.tensor([p[0][2] for p in preds], device=sorted_attr.device, dtype=sorted_attr.dtype)
+        r0 = torch.searchsorted(sorted_attr, lo).cpu().numpy()
+        r1 = torch.searchsorted(sorted_attr, hi).cpu().numpy()
+        keep = r1 > r0
+        t0, t1 = r0[keep] // 64, (r1[keep] + 63) // 64
+        order = np.argsort(t0, kind="stable")
+        tiles, end = 0, -1
+        for a, b in zip(t0[order], t1[order]):
+            a = max(a, end)
+            if b > a:
+                tiles += b - a
+                end = b
+        code = float(tiles) * 64 * mw * 4
+        g = plan.get("grid_tiles", 0)
+        if g and plan["splits"] * g >= (w.N + 63) // 64:
+            chunks = float(np.sum(((r1[keep] + 63) // 64 - 1) // g - (r0[keep] // 64) // g + 1))
+        else:
+            chunks = float(len(preds) * plan["splits"])
+    else:
+        bm, _ = idx.filter(preds)
+        any_row = bm.view(torch.int32)
+        acc = torch.zeros_like(any_row[0])
+        for i in range(any_row.shape[0]):
+            acc |= any_row[i]
+        rows = sum(bin(int(v) & 0xFFFFFFFF).count("1") for v in acc.cpu().tolist())
+        code = float(rows) * w.M
+        chunks = float(len(preds) * plan["splits"])
+    return code + len(preds) * w.M * 256 * lut_entry + chunks * SCAN_WAVES * k * 8
+
+
+def lds_roof(hist, rate):
+    """LDS time of a scan's table reads: hist[n] reads with n active lanes,
+    rate[n] such reads per second chip-wide (the probe).  Returns (lookups,
+    seconds)."""
+    lookups = sum(n * hist[n] for n in range(1, 65))
+    secs = sum(hist[n] / rate[n] for n in range(1, 65) if hist[n])
+    return lookups, secs
 
 
 def exact_screen_bytes(w, sorted_attr, preds):
@@ -207,7 +334,7 @@ def main():
                     help="oracle queries per bin timed in one process on one core (0 = skip)")
     ap.add_argument("--cpu-pool-queries", type=int, default=None,
                     help="oracle queries per bin timed with one single-threaded process per core "
-                         "(0 = skip; default 64 on c4, 16 on c1-c3, 4 on c5)")
+                         "(0 = skip; default 256 on c4, 16 on c1-c3, 4 on c5)")
     ap.add_argument("--cpu-pool-workers", type=int, default=16,
                     help="at most this many oracle processes (the host cores of the job)")
     ap.add_argument("--recall-queries", type=int, default=None,
@@ -225,9 +352,25 @@ def main():
                     help="batches per bin timed with queries and weights uploaded from pinned host memory "
                          "and results downloaded inside each batch (the PCIe-inclusive rate; 0 = skip)")
     ap.add_argument("--lut", choices=["f32", "f16"], default="f32")
+    ap.add_argument("--no-lds-roof", dest="lds_roof", action="store_false",
+                    help="skip the read-counting pass and the LDS probe")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain copy kernel of known size (for counter calibration)")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write the scan's counter summary (profiles/adc_scan_c4_counters.txt) from the "
+                         "output folders of the two rocprofv3 counter runs of COUNTER_RUN, then exit")
     args = ap.parse_args()
+
+    if args.summarize_counters:
+        from workload.synth import CONFIGS
+        cmds = [f"cd /tmp && export TMPDIR=/tmp; cd <repo>; rocprofv3 --pmc {c} --output-format csv -d "
+                f"{d} -o run -- python3 bench.py {COUNTER_RUN}"
+                for c, d in zip(("FETCH_SIZE", "WRITE_SIZE"), args.summarize_counters)]
+        cmds.append("python3 bench.py --steps %d --summarize-counters %s %s"
+                    % (args.steps, *args.summarize_counters))
+        summarize_counters(*args.summarize_counters, CONFIGS["c4"]["bins"], args.steps, COUNTERS_FILE, cmds)
+        print(open(COUNTERS_FILE).read())
+        return
 
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
@@ -247,7 +390,7 @@ def main():
     if args.plain_steps is None:
         args.plain_steps = 5 if name == "c4" else 0
     if args.cpu_pool_queries is None:
-        args.cpu_pool_queries = {"c4": 64, "c5": 4}.get(name, 16)
+        args.cpu_pool_queries = {"c4": 256, "c5": 4}.get(name, 16)
     if args.recall_queries is None:
         args.recall_queries = 100 if name in ("c1", "c5") else 256
     if args.exact_steps is None:
@@ -322,6 +465,21 @@ def main():
         return total, {s: [(b, a.elapsed_time(c)) for b, a, c in ev[s]] for s in bins}, prof_bin, prof, plans
 
     total_ms, per_bin, prof_bin, prof, plans = timed_run(clus, args.steps)
+    # The scan's table reads by active lanes, counted by the read-counting
+    # build of the scan over the same batches (untimed), and the LDS's rate
+    # for reads of each lane count, measured on this GPU.
+    read_hist = {}
+    if args.lds_roof:
+        clus.set_option(B.OPT_COUNT_READS, 1)
+        clus.read_scan_reads()
+        for s in bins:
+            for b, _ in per_bin[s]:
+                run_batch(clus, s, b)
+            read_hist[s] = clus.read_scan_reads()
+        clus.set_option(B.OPT_COUNT_READS, 0)
+        lds_rate = [0.0] + [B.probe_lds_gather(n) for n in range(1, 65)]
+        log(f"[bench] LDS random reads per second (chip): 64 lanes {lds_rate[64]:.3e}, "
+            f"32 {lds_rate[32]:.3e}, 8 {lds_rate[8]:.3e}, 1 {lds_rate[1]:.3e}")
     # Stage breakdown (every kernel bracketed by events) in a short pass of its own.
     _, _, stage_bin, stage_prof, _ = timed_run(clus, min(args.steps, 3), profile=1, warmup=0)
     stage_steps = min(args.steps, 3)
@@ -330,39 +488,79 @@ def main():
     log(f"[bench] clustered: {args.steps} steps in {total_ms:.1f} ms -> {qps:.0f} queries/s")
 
     sorted_attr = torch.sort(w.attrs[0].long()).values if tile_bytes else None
+    fabric = read_counters() if name == "c4" else None
     bins_out = {}
-    scan_bytes_total = useful_total = 0.0
+    scan_bytes_total = useful_total = union_total = 0.0
+    lds_lookups_total = lds_secs_total = 0.0
     for s in bins:
         cache = {}
         for b, _ in per_bin[s]:
             if b not in cache:
                 bp = w.preds[s][b * batch:(b + 1) * batch]
-                cache[b] = (scan_bytes_interval(w, sorted_attr, bp, plans[s], k, lut_entry) if tile_bytes
-                            else scan_bytes_passing(clus, w, bp, lut_entry))
+                cache[b] = ((scan_bytes_interval(w, sorted_attr, bp, plans[s], k, lut_entry) if tile_bytes
+                             else scan_bytes_passing(clus, w, bp, lut_entry))
+                            + (scan_union_bytes(w, sorted_attr, bp, plans[s], k, lut_entry, clus),))
             scan_bytes_total += cache[b][0]
             useful_total += cache[b][1]
+            union_total += cache[b][2]
         ms = [m for _, m in per_bin[s]]
         sel = float(np.mean([v[1] / (w.M * w.N * batch) for v in cache.values()]))
         b_ms, b_n = prof_bin[s]["scan"]
+        b_sec = b_ms / max(1, b_n) / 1e3
         b_bytes = sum(cache[b][0] for b, _ in per_bin[s]) / max(1, b_n)
-        b_gbps = b_bytes / (b_ms / max(1, b_n) / 1e3) / 1e9
+        b_gbps = b_bytes / b_sec / 1e9
+        b_union = sum(cache[b][2] for b, _ in per_bin[s]) / max(1, b_n)
+        roofs = {"hbm": {"achieved_GBps": round(b_union / b_sec / 1e9, 1), "peak_GBps": HBM_PEAK_GBPS,
+                         "frac": round(b_union / b_sec / 1e9 / HBM_PEAK_GBPS, 4),
+                         "bytes_per_launch": b_union}}
+        if fabric is not None and str(s) in fabric["by_bin"]:
+            fb = fabric["by_bin"][str(s)]
+            roofs["hbm"]["fabric_bytes_per_launch"] = fb
+            roofs["hbm"]["fabric_frac"] = round(fb / b_sec / 1e9 / HBM_PEAK_GBPS, 4)
+        if s in read_hist:
+            lk, lsec = lds_roof(read_hist[s], lds_rate)
+            lk, lsec = lk / max(1, b_n), lsec / max(1, b_n)
+            lds_lookups_total += lk * b_n
+            lds_secs_total += lsec * b_n
+            roofs["lds"] = {"lookups_per_launch": lk,
+                            "achieved_GBps": round(4 * lk / b_sec / 1e9, 1),
+                            "peak_GBps": round(4 * lk / lsec / 1e9, 1) if lsec > 0 else None,
+                            "frac": round(lsec / b_sec, 4),
+                            "reads_per_launch": sum(read_hist[s]) / max(1, b_n),
+                            "lanes_per_read": round(lk / max(1.0, sum(read_hist[s]) / max(1, b_n)), 2)}
+        bound = max(roofs, key=lambda r: roofs[r]["frac"])
+        roofs["bound"] = bound
+        roofs["frac"] = roofs[bound]["frac"]
         bins_out[str(s)] = {"qps": batch * len(ms) / (sum(ms) / 1e3),
                             "ms_per_batch": float(np.median(ms)),
                             "ms_per_batch_p10_p90": [round(float(np.percentile(ms, 10)), 4),
                                                      round(float(np.percentile(ms, 90)), 4)],
                             "realized_selectivity": round(sel, 5),
                             "scan_ms": round(b_ms / max(1, b_n), 4),
-                            "scan_GBps": round(b_gbps, 1),
-                            "scan_frac_of_hbm_peak": round(b_gbps / HBM_PEAK_GBPS, 4),
+                            "scan_effective_GBps": round(b_gbps, 1),
+                            "roofline": roofs,
                             "stage_ms_per_launch": {st: round(v[0] / max(1, v[1]), 4)
                                                    for st, v in stage_bin[s].items()},
                             "plan": plans[s]}
     scan_ms, scan_launches = prof["scan"]
     scan_avg_ms = scan_ms / max(1, scan_launches)
     bytes_per_launch = scan_bytes_total / max(1, scan_launches)
-    achieved = bytes_per_launch / (scan_avg_ms / 1e3) / 1e9
+    effective = bytes_per_launch / (scan_avg_ms / 1e3) / 1e9
+    union_per_launch = union_total / max(1, scan_launches)
+    hbm_achieved = union_per_launch / (scan_avg_ms / 1e3) / 1e9
+    if read_hist and lds_secs_total > 0:
+        lds_frac = lds_secs_total / (scan_ms / 1e3)
+        lds_achieved = 4 * lds_lookups_total / (scan_ms / 1e3) / 1e9
+        lds_peak = 4 * lds_lookups_total / lds_secs_total / 1e9
+    else:
+        lds_frac = lds_achieved = lds_peak = None
+    if lds_frac is not None and lds_frac > hbm_achieved / HBM_PEAK_GBPS:
+        roof_bound, achieved, peak = "lds", lds_achieved, lds_peak
+    else:
+        roof_bound, achieved, peak = "hbm", hbm_achieved, HBM_PEAK_GBPS
     log(f"[bench] scan: {scan_launches} launches, avg {scan_avg_ms:.3f} ms, "
-        f"{bytes_per_launch / 1e6:.1f} MB/launch -> {achieved:.0f} GB/s")
+        f"{union_per_launch / 1e6:.1f} MB/launch from HBM at least -> {hbm_achieved:.0f} GB/s; "
+        f"bound {roof_bound}: {achieved:.0f} of {peak:.0f} GB/s")
 
     plain_out = None
     if plain is not None:
@@ -609,7 +807,7 @@ def main():
             torch.neg(src, out=dst)
         torch.cuda.synchronize()
 
-    traffic = read_counters() if name == "c4" else None
+    traffic = fabric["mean"] if fabric is not None else None
     out = {
         "metric": METRIC,
         "value": qps,
@@ -631,14 +829,29 @@ def main():
                    "recall_queries_per_bin": nr},
         "bins": bins_out,
         "stage_ms_per_step": {st: round(v[0] / stage_steps, 4) for st, v in stage_prof.items()},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
-                     "traffic_over_algorithmic": (round(traffic / bytes_per_launch, 4)
-                                                  if traffic is not None else None),
+        "roofline": {"bound": roof_bound, "achieved": achieved, "peak": peak, "unit": "GB/s",
+                     "frac": achieved / peak, "traffic": traffic,
                      "kernel": "scan_kernel", "avg_launch_ms": scan_avg_ms,
-                     "bytes_definition": ("code tiles overlapping each query's row interval + table + partial lists"
-                                          if tile_bytes else "codes of every (query, passing row) pair + table"),
-                     "bytes_per_launch": bytes_per_launch,
+                     "hbm": {"achieved": hbm_achieved, "peak": HBM_PEAK_GBPS, "frac": hbm_achieved / HBM_PEAK_GBPS,
+                             "bytes_per_launch": union_per_launch,
+                             "bytes_definition": "code tiles some query of the batch selects, read once, + tables "
+                                                 "+ partial lists written (the least a launch moves to and from HBM)",
+                             "fabric_bytes_per_launch": traffic,
+                             "fabric_definition": "rocprofv3 FETCH_SIZE x 2 + WRITE_SIZE (copy-kernel calibrated): "
+                                                  "bytes the L2s request from the fabric, Infinity Cache hits "
+                                                  "included; no counter on gfx950 separates those from HBM reads"},
+                     "lds": ({"achieved": lds_achieved, "peak": lds_peak, "frac": lds_frac,
+                              "definition": "4 bytes per table entry the scan reads from LDS (reads counted by "
+                                            "active lanes in an untimed pass over the same batches) / scan time; "
+                                            "peak: the LDS's measured rate for random 4-byte reads with the same "
+                                            "mix of active lanes (ifvs_probe_lds_gather)"}
+                             if lds_frac is not None else None),
+                     "effective_GBps": effective,
+                     "effective_definition": ("code tiles overlapping each query's row interval + table + partial "
+                                              "lists, counted once per query (rows several queries share are "
+                                              "re-read, mostly from L2)" if tile_bytes else
+                                              "codes of every (query, passing row) pair + table"),
+                     "effective_bytes_per_launch": bytes_per_launch,
                      "useful_bytes_per_launch": useful_total / max(1, scan_launches)},
         "plain_layout": plain_out,
         "exact_search": exact_out,

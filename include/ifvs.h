@@ -375,6 +375,13 @@ ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const
 #define IFVS_OPT_EXACT_PLAN 10    /* ifvs_exact_search: 0 automatic (matrix-core screening when
                                      the batch's queries share rows), 1 score every selected row
                                      exactly, 2 always screen first                           */
+#define IFVS_OPT_COUNT_READS 12  /* measurement only: 1 = scans run a build of the scan kernel
+                                     that also counts its table reads (one per subspace and
+                                     wavefront instruction) by the number of active lanes, read
+                                     back with ifvs_read_scan_reads; needs one query per tile
+                                     and M of 16, 48 or 120 (else the search fails with
+                                     IFVS_E_UNSUPPORTED).  Results are unchanged; the counting
+                                     adds LDS atomics, so it is not the build to time.  0 = off */
 ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value);
 
 /* ifvs_read_profile -- with IFVS_OPT_PROFILE on, every kernel the index
@@ -386,6 +393,26 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value);
  * IFVS_E_HIP. */
 #define IFVS_N_STAGES 5
 ifvs_status ifvs_read_profile(ifvs_index* idx, double* ms_out, int64_t* launches_out);
+
+/* ifvs_read_scan_reads -- with IFVS_OPT_COUNT_READS on: hist_out[n] (65
+ * entries) = table reads the scans issued with n of a wavefront's 64 lanes
+ * active (a read is one LDS instruction of a wavefront; it fetches n table
+ * entries), summed over the scans since the last call, which it then clears.
+ * Waits for `stream`.  The LDS cost of the Rank stage's distance-table
+ * lookups (Section 2, stage 2) follows from it and ifvs_probe_lds_gather.
+ * All zero when counting was never on.
+ * Errors: IFVS_E_INVALID (NULL hist_out), IFVS_E_STATE, IFVS_E_HIP. */
+ifvs_status ifvs_read_scan_reads(ifvs_index* idx, int64_t* hist_out, void* stream);
+
+/* ifvs_probe_lds_gather -- a measurement of the current GPU, not a step of
+ * the method: the chip-wide rate (*wave_reads_per_s, wavefront instructions
+ * per second) of 4-byte LDS reads at random addresses of a 48 KB table, with
+ * active_lanes (1..64) lanes per instruction, the access the Rank stage's
+ * table lookups make (Section 2, stage 2).  Three workgroups of eight
+ * wavefronts per CU; enqueued on `stream`, waited for.  Allocates and frees
+ * 4 bytes of device memory.
+ * Errors: IFVS_E_INVALID (active_lanes out of range, NULL output), IFVS_E_HIP. */
+ifvs_status ifvs_probe_lds_gather(int32_t active_lanes, double* wave_reads_per_s, void* stream);
 
 /* ifvs_last_plan -- the launch plan of the most recent ifvs_filtered_search
  * on this index (all zero before the first): out5[0] queries per tile

@@ -210,6 +210,10 @@ struct ifvs_index {
   int opt_seed_tiles = 0;      // seeded bound: 0 auto, 1 off, n > 1 at most n tiles per wavefront
   int opt_gather_auto_pct = 30;   // automatic mode: pools up to this % of the rows
   int profile_mask = 0;          // stages timed with HIP events (IFVS_OPT_PROFILE)
+  // IFVS_OPT_COUNT_READS: scans run the read-counting build, which adds its
+  // table reads by active lanes into this device histogram ([65]).
+  int opt_count_reads = 0;
+  unsigned long long* read_hist = nullptr;
   StageTimer* timers = nullptr;  // [kStages] once profiling was enabled
   ScanPlan last_plan{};
 
@@ -250,7 +254,8 @@ struct ifvs_index {
                     static_cast<void*>(slot_order_dev),
                     static_cast<void*>(counts), static_cast<void*>(count_parts), static_cast<void*>(vstart),
                     static_cast<void*>(partials), static_cast<void*>(codes_rm),
-                    static_cast<void*>(lists), static_cast<void*>(list_n), static_cast<void*>(qmode)})
+                    static_cast<void*>(lists), static_cast<void*>(list_n), static_cast<void*>(qmode),
+                    static_cast<void*>(read_hist)})
       if (p) hipFree(p);
     free_vectors();
     for (void* p : {static_cast<void*>(tr_alpha), static_cast<void*>(tr_wf), static_cast<void*>(tr_lut),
@@ -988,6 +993,15 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
       if (value > 2) return fail(IFVS_E_INVALID, "IFVS_OPT_SHARED_BOUND takes 0, 1 or 2");
       idx->opt_shared_bound = static_cast<int>(value);
       return IFVS_OK;
+    case IFVS_OPT_COUNT_READS:
+      if (value > 1) return fail(IFVS_E_INVALID, "IFVS_OPT_COUNT_READS takes 0 or 1");
+      if (value == 1 && !idx->read_hist) {
+        IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+        if (ifvs_status st = dev_alloc(&idx->read_hist, 65, "read histogram"); st != IFVS_OK) return st;
+        IFVS_HIP(hipMemset(idx->read_hist, 0, 65 * sizeof(unsigned long long)), "clearing the read histogram");
+      }
+      idx->opt_count_reads = static_cast<int>(value);
+      return IFVS_OK;
     case IFVS_OPT_PROFILE:
       if (value != 0 && !idx->timers) {
         idx->timers = new StageTimer[kStages];
@@ -1101,7 +1115,9 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   int64_t span = 0;
   for (int i = 0; i < nq; ++i) {
     need_bitmap = need_bitmap || host[i].residual_mask != 0;
-    interval_batch = interval_batch && host[i].iv_mode != 0;
+    // A predicate no row can satisfy has the empty interval on a clustered
+    // index, so it does not take the batch off the interval plan.
+    interval_batch = interval_batch && (host[i].iv_mode != 0 || (idx->n_cluster > 0 && host[i].n_eff < 0));
     if (idx->n_cluster > 0) span = std::max(span, estimate_interval_tiles(idx, host[i]));
   }
   SearchWs ws;
@@ -1114,6 +1130,10 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   ScanPlan plan{};
   if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, interval_batch, span, ws.partial_keys, &plan); st != IFVS_OK)
     return st;
+  if (idx->opt_count_reads &&
+      (!scan_can_count(idx->m, plan.qtile, lut_dtype) || plan.lds_bytes + kLookupHistBytes > size_t{kLdsBudget}))
+    return fail(IFVS_E_UNSUPPORTED, "IFVS_OPT_COUNT_READS: no read-counting scan for this plan (it needs one query "
+                                    "per tile, M of 16, 48 or 120, and 272 bytes of LDS to spare)");
   // Chunk-grid scans: the slot dispatch order goes into the staging slot and
   // the interval kernel copies it to the device.
   const int32_t* qorder_host = reinterpret_cast<const int32_t*>(host + idx->max_batch);
@@ -1174,6 +1194,7 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   b.gthr = ws.gthr;
   b.mode = gather ? ws.qmode : nullptr;
   b.slot_order = ordered ? ws.slot_order : nullptr;
+  b.lookup_hist = idx->opt_count_reads ? idx->read_hist : nullptr;
   IFVS_LAUNCH(idx, kStScan, s, "launching scan kernel", launch_scan(b, plan, s));
   if (gather) {
     GatherBatch g{};
@@ -1470,6 +1491,32 @@ ifvs_status ifvs_read_profile(ifvs_index* idx, double* ms_out, int64_t* launches
     t.ms = 0.0;
     t.launches = 0;
   }
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_read_scan_reads(ifvs_index* idx, int64_t* hist_out, void* stream) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (!hist_out) return fail(IFVS_E_INVALID, "hist_out is NULL");
+  for (int i = 0; i < 65; ++i) hist_out[i] = 0;
+  if (!idx->read_hist) return IFVS_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  unsigned long long h[65];
+  IFVS_HIP(hipMemcpyAsync(h, idx->read_hist, sizeof(h), hipMemcpyDeviceToHost, s), "reading the read histogram");
+  IFVS_HIP(hipStreamSynchronize(s), "reading the read histogram");
+  IFVS_HIP(hipMemsetAsync(idx->read_hist, 0, sizeof(h), s), "clearing the read histogram");
+  IFVS_HIP(hipStreamSynchronize(s), "clearing the read histogram");
+  for (int i = 0; i < 65; ++i) hist_out[i] = static_cast<int64_t>(h[i]);
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_probe_lds_gather(int32_t active_lanes, double* wave_reads_per_s, void* stream) {
+  if (active_lanes < 1 || active_lanes > 64) return fail(IFVS_E_INVALID, "active_lanes outside 1..64");
+  if (!wave_reads_per_s) return fail(IFVS_E_INVALID, "wave_reads_per_s is NULL");
+  // Three eight-wavefront workgroups per CU (24 waves: as many 48 KB tables
+  // as the LDS holds), 1024 iterations of 32 reads each, 4 timed launches.
+  IFVS_HIP(lds_gather_probe(active_lanes, 1024, 3, 4, static_cast<hipStream_t>(stream), wave_reads_per_s),
+           "LDS gather probe");
   return IFVS_OK;
 }
 

@@ -16,6 +16,7 @@ constexpr int kScanWaves = 8;              // wavefronts per scan workgroup
 constexpr int kScanPub = 2;                // best keys per (wavefront, query) published for the workgroup bound
 constexpr int kScanSeed = 8;               // seed candidates per wavefront (kScanWaves * kScanSeed = 64 >= k)
 constexpr int kFilterQueries = 16;         // predicates evaluated per attribute read
+constexpr int kLookupHistBytes = 272;      // LDS of the scan's read-counting build: 65 counters, padded
 
 // A predicate as the device sees it.  The raw fields are the caller's clauses
 // exactly as given (they are hashed into the memory bank); the effective
@@ -183,6 +184,7 @@ struct ScanBatch {
   uint64_t* gthr;               // [nq] shared thresholds, all-ones before the scan
   const int32_t* mode;          // [nq] 1: the query is scored by the gather scan (null: none is)
   const int32_t* slot_order;    // chunk-grid dispatch order (null: slots in index order)
+  unsigned long long* lookup_hist;  // [65] non-null: run the read-counting build (see scan_can_count)
 };
 
 // Gather scan of compacted row lists (masked batches, few selected rows).
@@ -219,6 +221,14 @@ hipError_t launch_compact(const uint64_t* bitmap, int64_t stride64, const unsign
 hipError_t launch_gather_scan(const GatherBatch& b, hipStream_t s);
 
 hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s);
+// Whether a read-counting build of the scan exists for this plan (one query
+// per tile, M of 16, 48 or 120).
+bool scan_can_count(int m, int qtile, int lut_dtype);
+
+// LDS gather probe (k_probe.hip): wavefront-level 4-byte random LDS reads per
+// second, chip-wide, with `active` lanes (1..64) per read, measured over
+// `reps` launches of wg_per_cu eight-wavefront workgroups per CU.
+hipError_t lds_gather_probe(int active, int iters, int wg_per_cu, int reps, hipStream_t s, double* wave_reads_per_s);
 
 hipError_t launch_topk_merge(const uint64_t* partials, int nq, int64_t per_query, int k,
                              const int64_t* iv, int64_t cell_tiles, int64_t slot_keys,

@@ -73,6 +73,9 @@ struct ScanArgs {
   const int32_t* slot_order;
   int shared_bound;      // 1: wavefronts publish their best keys (union bound, k <= 16)
   int seed_tiles;        // > 0: seeded bound from up to this many tiles per wavefront (QT = 1, k <= 64)
+  // Counting instantiation only: lookup_hist[n] += the table reads (one
+  // per subspace and wavefront instruction) issued with n active lanes.
+  unsigned long long* lookup_hist;
 };
 
 // Bits [lo, hi) of a 64-bit word, 0 <= lo < hi <= 64.
@@ -105,7 +108,10 @@ constexpr int scan_depth() {
   else return 2;
 }
 
-template <int MT, int QT, typename LutT>
+// kCount: the same scan, also counting its table reads by active lanes in
+// an LDS histogram flushed to a.lookup_hist (a measurement build: the
+// counting adds LDS atomics, so it is never the timed kernel).
+template <int MT, int QT, typename LutT, bool kCount = false>
 __global__ __launch_bounds__(kScanWaves * 64) __attribute__((amdgpu_waves_per_eu(scan_waves_per_eu<MT, QT, LutT>())))
 void scan_kernel(const ScanArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
@@ -138,6 +144,13 @@ void scan_kernel(const ScanArgs a) {
   uint32_t* s_best = reinterpret_cast<uint32_t*>(s_pub);
   // [wave][kScanSeed]: distances (order-preserving bits) of the seed candidates
   uint32_t* s_seed = reinterpret_cast<uint32_t*>(s_pub + QT * kScanWaves * kScanPub);
+  // [65]: the counting build's histogram of table reads by active lanes
+  uint32_t* s_hist = s_seed + kScanWaves * kScanSeed;
+  auto count_reads = [&](uint64_t lanes, int reads) {
+    if constexpr (kCount) {
+      if (lanes != 0 && (threadIdx.x & 63) == 0) atomicAdd(&s_hist[__popcll(lanes)], static_cast<uint32_t>(reads));
+    }
+  };
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -393,6 +406,9 @@ void scan_kernel(const ScanArgs a) {
   }
   if (threadIdx.x < QT) s_thr[threadIdx.x] = kNoKey;
   if (threadIdx.x < QT * kScanWaves * kScanPub) s_pub[threadIdx.x] = kNoKey;
+  if constexpr (kCount) {
+    if (threadIdx.x < 65) s_hist[threadIdx.x] = 0;
+  }
   __syncthreads();
   // Early abandonment: every entry >= 0 and fp32 addition of non-negative
   // terms never decreases, so a partial sum above the current k-th distance
@@ -428,6 +444,7 @@ void scan_kernel(const ScanArgs a) {
           int t;
           const uint64_t mk = seed_mask(round * kSB + i, &t);
           if (mk != 0) {
+            count_reads(~0ull, kGroup);
             float p = 0.0f;
 #pragma unroll
             for (int u = 0; u < kGroup; ++u)
@@ -462,6 +479,7 @@ void scan_kernel(const ScanArgs a) {
       // The scan's first tiles are loaded while the candidates' rows are.
       preload();
       float dfull = 0.0f;
+      count_reads(__ballot(chosen), MT);
       if (chosen) {
         const uint32_t* __restrict__ tile = a.codes_t + static_cast<size_t>(best_t) * (kMW * 64);
         uint32_t w[kMW];
@@ -652,6 +670,7 @@ void scan_kernel(const ScanArgs a) {
         LutT v[QT][kGroup];
 #pragma unroll
         for (int qi = 0; qi < QT; ++qi) {
+          count_reads(__ballot(live[qi]), kGroup);
           if (live[qi]) {
 #pragma unroll
             for (int u = 0; u < kGroup; ++u) v[qi][u] = slut[addr[u] + qi * kKsub];
@@ -723,6 +742,11 @@ void scan_kernel(const ScanArgs a) {
     uint64_t* dst = a.partials + ((static_cast<size_t>(q0 + qi) * a.splits + chunk) * kScanWaves + wave) * k;
     for (int e = lane; e < k; e += 64) dst[e] = pool[e];
   }
+  if constexpr (kCount) {
+    __syncthreads();
+    if (threadIdx.x < 65 && s_hist[threadIdx.x] != 0)
+      atomicAdd(&a.lookup_hist[threadIdx.x], static_cast<unsigned long long>(s_hist[threadIdx.x]));
+  }
 }
 
 template <int MT, int QT, typename LutT>
@@ -757,6 +781,24 @@ const void* pick_q(int qt) {
     case 4: return scan_symbol_if_fits<MT, 4, LutT>();
     case 6: return scan_symbol_if_fits<MT, 6, LutT>();
     case 8: return scan_symbol_if_fits<MT, 8, LutT>();
+    default: return nullptr;
+  }
+}
+
+// The counting build exists for one-query tiles of a fixed M.
+template <typename LutT, int MT>
+const void* count_symbol_if_fits() {
+  if constexpr (scan_fits<MT, 1, LutT>()) return reinterpret_cast<const void*>(&scan_kernel<MT, 1, LutT, true>);
+  else return nullptr;
+}
+
+template <typename LutT>
+const void* pick_count(int m, int qt) {
+  if (qt != 1) return nullptr;
+  switch (m) {
+    case 16: return count_symbol_if_fits<LutT, 16>();
+    case 48: return count_symbol_if_fits<LutT, 48>();
+    case 120: return count_symbol_if_fits<LutT, 120>();
     default: return nullptr;
   }
 }
@@ -809,13 +851,19 @@ int scan_supported_qtile(int want) {
   return best;
 }
 
+bool scan_can_count(int m, int qtile, int lut_dtype) {
+  return (lut_dtype == 1 ? pick_count<__half>(m, qtile) : pick_count<float>(m, qtile)) != nullptr;
+}
+
 hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s) {
-  const void* fn = b.lut_dtype == 1 ? pick<__half>(b.m, plan.qtile) : pick<float>(b.m, plan.qtile);
+  const void* fn = b.lookup_hist ? (b.lut_dtype == 1 ? pick_count<__half>(b.m, plan.qtile)
+                                                     : pick_count<float>(b.m, plan.qtile))
+                                 : (b.lut_dtype == 1 ? pick<__half>(b.m, plan.qtile) : pick<float>(b.m, plan.qtile));
   if (!fn) return hipErrorInvalidValue;
   // Fixed-M kernels hold their tables in static LDS; the rest is dynamic.
   const bool fixed_m = b.m == 16 || b.m == 48 || b.m == 120;
   const size_t table = static_cast<size_t>(b.m) * plan.qtile * kKsub * (b.lut_dtype == 1 ? 2 : 4);
-  const size_t dyn = fixed_m ? plan.lds_bytes - table : plan.lds_bytes;
+  const size_t dyn = (fixed_m ? plan.lds_bytes - table : plan.lds_bytes) + (b.lookup_hist ? kLookupHistBytes : 0);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(dyn));
   if (e != hipSuccess) return e;
   ScanArgs a{};
@@ -844,6 +892,7 @@ hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s) 
   a.seed_tiles = plan.seed_tiles;
   a.partials = b.partials;
   a.gthr = b.gthr;
+  a.lookup_hist = b.lookup_hist;
   a.splits = plan.splits;
   a.n_qtiles = (b.nq + plan.qtile - 1) / plan.qtile;
   const unsigned per_xcd = static_cast<unsigned>((a.n_qtiles + kXcds - 1) / kXcds);

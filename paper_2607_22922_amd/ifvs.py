@@ -28,13 +28,14 @@ OPT_SLOT_ORDER = 8
 OPT_SHARED_BOUND = 9
 OPT_EXACT_PLAN = 10
 OPT_SEED_TILES = 11
+OPT_COUNT_READS = 12
 STAGES = ("condition", "lut", "filter", "scan", "merge")
 
 EXPORTED = ("ifvs_load_index", "ifvs_free_index", "ifvs_select_codebook", "ifvs_build_lut",
             "ifvs_filter", "ifvs_filtered_search", "ifvs_set_option", "ifvs_last_plan",
             "ifvs_read_profile", "ifvs_last_error", "ifvs_load_vectors", "ifvs_exact_search",
             "ifvs_build_sdc_lut", "ifvs_load_reconstructions", "ifvs_train_step", "ifvs_read_params",
-            "ifvs_filtered_search_noalloc")
+            "ifvs_filtered_search_noalloc", "ifvs_read_scan_reads", "ifvs_probe_lds_gather")
 
 
 class IfvsError(RuntimeError):
@@ -102,6 +103,8 @@ def _load_library() -> ctypes.CDLL:
         "ifvs_train_step": ([vp, i32, vp, vp, vp, vp, i32, i32, ctypes.c_float, ctypes.c_float, ctypes.c_float,
                              vp, vp, vp], i32),
         "ifvs_read_params": ([vp, vp, vp, vp], i32),
+        "ifvs_read_scan_reads": ([vp, ctypes.POINTER(ctypes.c_int64), vp], i32),
+        "ifvs_probe_lds_gather": ([i32, ctypes.POINTER(ctypes.c_double), vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -130,6 +133,14 @@ def _stream(stream) -> int:
     if stream is None:
         return torch.cuda.current_stream().cuda_stream
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def probe_lds_gather(active_lanes: int, stream=None) -> float:
+    """ifvs_probe_lds_gather: chip-wide wavefront reads per second of random
+    4-byte LDS reads with `active_lanes` lanes each (a GPU measurement)."""
+    out = ctypes.c_double()
+    _check(_lib.ifvs_probe_lds_gather(int(active_lanes), ctypes.byref(out), _stream(stream)))
+    return out.value
 
 
 def pack_predicates(preds) -> ctypes.Array:
@@ -223,6 +234,13 @@ class Index:
         n = (ctypes.c_int64 * len(STAGES))()
         _check(_lib.ifvs_read_profile(self.handle, ms, n))
         return {name: (ms[i], n[i]) for i, name in enumerate(STAGES)}
+
+    def read_scan_reads(self, stream=None) -> list:
+        """With OPT_COUNT_READS on: [65] table reads issued with n active
+        lanes (index n) since the last read."""
+        out = (ctypes.c_int64 * 65)()
+        _check(_lib.ifvs_read_scan_reads(self.handle, out, _stream(stream)))
+        return list(out)
 
     def select_codebook_into(self, q, preds_c, w_z, alpha_out, wf_out, stream=None):
         _check(_lib.ifvs_select_codebook(self.handle, q.shape[0], q.data_ptr(), preds_c,

@@ -40,3 +40,23 @@ def test_clause_tensors_padding_admits_everything():
     assert lo[0, 0] < -(1 << 40) and hi[0, 0] > (1 << 40)
     assert (col[1, 0], lo[1, 0], hi[1, 0]) == (1, 3, 4)
     assert (col[2, 1], lo[2, 1], hi[2, 1]) == (1, 0, 2)
+
+
+def test_union_bytes_count_each_selected_tile_once():
+    class W:
+        M, N = 48, 6400
+    sorted_attr = torch.arange(6400) // 10            # value v on rows [10v, 10v + 10)
+    preds = [[(0, 0, 10)], [(0, 5, 20)], [(0, 100, 101)], [(0, 3, 3)]]
+    # rows [0, 100), [50, 200), [1000, 1010), none: tiles [0, 2) + [0, 4) + [15, 16) -> 5 tiles
+    got = bench.scan_union_bytes(W, sorted_attr, preds, {"splits": 2, "grid_tiles": 0}, 10, 4)
+    assert got == 5 * 64 * 12 * 4 + 4 * 48 * 256 * 4 + 4 * 2 * bench.SCAN_WAVES * 10 * 8
+
+
+def test_lds_roof_weights_reads_by_their_rate():
+    hist = [0] * 65
+    hist[64], hist[8] = 10, 4
+    rate = [0.0] + [1e9] * 64
+    rate[8] = 4e9
+    lookups, secs = bench.lds_roof(hist, rate)
+    assert lookups == 64 * 10 + 8 * 4
+    assert abs(secs - (10 / 1e9 + 4 / 4e9)) < 1e-18

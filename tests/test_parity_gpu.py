@@ -582,3 +582,22 @@ def test_seeded_bound_same_answer(B, cols, M, dsub):
                 assert torch.equal(ids, i16) and torch.equal(dist.view(torch.int32), d16.view(torch.int32))
     idx.set_option(B.OPT_SEED_TILES, 0)
     idx.set_option(B.OPT_GRID_TILES, 0)
+
+
+@pytest.mark.parametrize("seed_tiles", [0, 8])
+def test_clustered_batch_with_unsatisfiable_predicates(B, seed_tiles):
+    """Predicates no row satisfies (lo >= hi, contradictory ranges) have the
+    empty interval on a clustered index: the batch keeps the one-query
+    interval plan and those rows come back as padding, the rest as the
+    oracle's."""
+    say(f"[edge] clustered batch with empty predicates seed={seed_tiles}")
+    idx, ox = _edge_index(B, 40_000, 48, 2, n_attr=1, domain=500, seed=71, cluster_cols=(0,))
+    idx.set_option(B.OPT_SEED_TILES, seed_tiles)
+    preds = [[(0, 10, 60)], [(0, 9, 9)], [(0, 100, 400)], [(0, 30, 20)], [(0, 5, 50), (0, 70, 90)],
+             [(0, 0, 500)], [(0, 499, 500)]] * 3
+    ids = _run_and_check(B, idx, ox, preds, k=10, dsub=2, M=48)
+    assert idx.last_plan()["qtile"] == 1
+    for i, p in enumerate(preds):
+        if i % 7 in (1, 3, 4):
+            assert np.all(ids[i] == -1), p
+    idx.set_option(B.OPT_SEED_TILES, 0)
