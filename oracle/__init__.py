@@ -7,3 +7,4 @@ imports it and shares no code with it.
 """
 from .ifvs_oracle import *  # noqa: F401,F403
 from .ifvs_oracle import __all__  # noqa: F401
+from .ifvs_encoder_oracle import encode_predicate  # noqa: F401

@@ -53,6 +53,23 @@ TRAIN_MUTATIONS = [
 ]
 
 
+# Planted mistakes in the predicate-encoder oracle, caught by its pins.
+ENCODER_MUTATIONS = [
+    ("enc_softmax_over_queries", "A = _softmax_rows((Q[:, sl] @ K[:, sl].T) / np.sqrt(dtype(dh)))",
+     "A = _softmax_rows((K[:, sl] @ Q[:, sl].T) / np.sqrt(dtype(dh))).T"),
+    ("enc_unscaled_scores", "A = _softmax_rows((Q[:, sl] @ K[:, sl].T) / np.sqrt(dtype(dh)))",
+     "A = _softmax_rows(Q[:, sl] @ K[:, sl].T)"),
+    ("enc_heads_share_values", "O[:, sl] = A @ V[:, sl]", "O[:, sl] = A @ V[:, :dh]"),
+    ("enc_attention_residual_dropped", 'X = X + O @ f("Wo") + f("bo")', 'X = O @ f("Wo") + f("bo")'),
+    ("enc_ffn_without_relu", 'Hd = np.maximum(Z @ f("W1") + f("b1"), dtype(0))', 'Hd = Z @ f("W1") + f("b1")'),
+    ("enc_layer_norm_without_eps", "np.sqrt(var + dtype(LN_EPS))", "np.sqrt(var)"),
+    ("enc_summary_token_last", 'z = layer_norm(X[0], enc["lnf_g"]', 'z = layer_norm(X[-1], enc["lnf_g"]'),
+    ("enc_bounds_swapped", "rows.append(ce[int(cl[0])] + a * fw[0] + b * fw[1] + fb)",
+     "rows.append(ce[int(cl[0])] + b * fw[0] + a * fw[1] + fb)"),
+    ("enc_bounds_unclipped", "a = min(max((float(lo) - off) * sc, -1.0), 2.0)", "a = (float(lo) - off) * sc"),
+]
+
+
 def _run_pins_on_copy(tmp_path, old, new, target="ifvs_oracle.py", pins="test_oracle_pins.py"):
     src = os.path.join(ROOT, "oracle", target)
     text = open(src).read()
@@ -65,7 +82,9 @@ def _run_pins_on_copy(tmp_path, old, new, target="ifvs_oracle.py", pins="test_or
     tests.mkdir()
     shutil.copy(os.path.join(ROOT, "tests", pins), tests)
     shutil.copytree(os.path.join(ROOT, "tests", "golden"), tests / "golden")
-    env = dict(os.environ, PYTHONPATH=str(tmp_path), PYTHONDONTWRITEBYTECODE="1")
+    # The copy comes first on the path; the seeded input generators come
+    # from the repository (they hold none of the oracle's arithmetic).
+    env = dict(os.environ, PYTHONPATH=os.pathsep.join([str(tmp_path), ROOT]), PYTHONDONTWRITEBYTECODE="1")
     proc = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
                            str(tests / pins)],
                           cwd=tmp_path, env=env, capture_output=True, text=True, timeout=300)
@@ -94,3 +113,15 @@ def test_unmutated_train_copy_passes(tmp_path):
 def test_train_pins_catch_planted_mistake(tmp_path, name, old, new):
     proc = _run_pins_on_copy(tmp_path, old, new, "ifvs_train_oracle.py", "test_oracle_train.py")
     assert proc.returncode == 1, f"the training pins did not catch {name}:\n{proc.stdout[-2000:]}"
+
+
+def test_unmutated_encoder_copy_passes(tmp_path):
+    old = ENCODER_MUTATIONS[0][1]
+    proc = _run_pins_on_copy(tmp_path, old, old, "ifvs_encoder_oracle.py", "test_oracle_encoder.py")
+    assert proc.returncode == 0, proc.stdout[-2000:]
+
+
+@pytest.mark.parametrize("name,old,new", ENCODER_MUTATIONS, ids=[m[0] for m in ENCODER_MUTATIONS])
+def test_encoder_pins_catch_planted_mistake(tmp_path, name, old, new):
+    proc = _run_pins_on_copy(tmp_path, old, new, "ifvs_encoder_oracle.py", "test_oracle_encoder.py")
+    assert proc.returncode == 1, f"the encoder pins did not catch {name}:\n{proc.stdout[-2000:]}"

@@ -58,6 +58,8 @@ PARAM_STD = 0.05                # std of synthetic bank and W entries
 WZ_CENTER = math.log(math.e - 1.0)   # softplus(WZ_CENTER) = 1
 WZ_STD = 0.1
 ZIPF_S = 1.1
+# Predicate encoder sizes (hidden width, heads, layers, feed-forward width).
+ENC_HIDDEN, ENC_HEADS, ENC_LAYERS, ENC_FFN = 64, 4, 2, 128
 
 
 def _gen(seed: int, device) -> torch.Generator:
@@ -87,6 +89,7 @@ class Workload:
     r: int = R_DIRS
     h: int = H_FUNCS
     hash_seed: int = 0
+    enc: dict | None = None        # predicate encoder weights (random_encoder)
     x: torch.Tensor | None = None  # raw base vectors (None when not kept)
     cat_probs: torch.Tensor | None = None
     extra: dict = field(default_factory=dict)
@@ -285,10 +288,44 @@ def make_workload(name: str, device="cpu", n_queries: int | None = None, N: int 
         w_z[s] = (WZ_CENTER + WZ_STD * torch.randn(nq, D, generator=g_c, device=device)).contiguous()
 
     cat_probs = zipf_probs(cfg["attrs"][1][1]) if len(cfg["attrs"]) > 1 else None
+    domains = [d for _, d in cfg["attrs"]]
+    enc = random_encoder(len(domains), D, domains, 1000 * c + 7, device)
     return Workload(name=name, N=Nn, D=D, M=M, dsub=dsub, k=cfg["k"], bins=list(cfg["bins"]),
-                    codes=codes, C_pq=C_pq, attrs=attrs, domains=[d for _, d in cfg["attrs"]],
+                    codes=codes, C_pq=C_pq, attrs=attrs, domains=domains,
                     queries=queries, preds=preds, w_z=w_z, bank=bank, W=W,
-                    hash_seed=0x5EED0000 + c, x=x, cat_probs=cat_probs)
+                    hash_seed=0x5EED0000 + c, x=x, cat_probs=cat_probs, enc=enc)
+
+
+def random_encoder(n_attr: int, D: int, domains, seed: int, device="cpu", hidden: int = ENC_HIDDEN,
+                   heads: int = ENC_HEADS, layers: int = ENC_LAYERS, ffn: int = ENC_FFN) -> dict:
+    """Seeded synthetic weights of the predicate encoder (the trained ones are
+    not published).  Matrices are drawn N(0, 1/fan_in), layer-norm gains
+    1 + N(0, 0.1^2), biases N(0, 0.1^2), embeddings N(0, 1); the output map
+    is scaled so that w_z = WZ_CENTER + N(0, WZ_STD^2)-sized variations, the
+    spread of the synthetic w_z above.  Bound normalization: offset 0 and
+    scale 1 / domain per column (a column's values map into [0, 1))."""
+    g = _gen(seed, device)
+    H, F = hidden, ffn
+
+    def rn(*shape, std=1.0):
+        return (torch.randn(*shape, generator=g, device=device) * std).contiguous()
+
+    def layer():
+        return dict(ln1_g=1.0 + rn(H, std=0.1), ln1_b=rn(H, std=0.1),
+                    Wq=rn(H, H, std=H ** -0.5), Wk=rn(H, H, std=H ** -0.5), Wv=rn(H, H, std=H ** -0.5),
+                    bq=rn(H, std=0.1), bk=rn(H, std=0.1), bv=rn(H, std=0.1),
+                    Wo=rn(H, H, std=H ** -0.5), bo=rn(H, std=0.1),
+                    ln2_g=1.0 + rn(H, std=0.1), ln2_b=rn(H, std=0.1),
+                    W1=rn(H, F, std=H ** -0.5), b1=rn(F, std=0.1), W2=rn(F, H, std=F ** -0.5), b2=rn(H, std=0.1))
+
+    enc = dict(heads=heads,
+               col_offset=torch.zeros(n_attr, dtype=torch.float64),
+               col_scale=torch.tensor([1.0 / float(d) for d in domains], dtype=torch.float64),
+               col_embed=rn(n_attr, H), feat_w=rn(2, H), feat_b=rn(H, std=0.1), cls=rn(H))
+    enc["layers"] = [layer() for _ in range(layers)]
+    enc.update(lnf_g=1.0 + rn(H, std=0.1), lnf_b=rn(H, std=0.1), out_w=rn(H, D, std=WZ_STD * H ** -0.5),
+               out_b=torch.full((D,), WZ_CENTER, device=device))
+    return enc
 
 
 def random_index(N: int, M: int, dsub: int, n_attr: int, domain: int, seed: int,
