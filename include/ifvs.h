@@ -330,6 +330,69 @@ ifvs_status ifvs_load_reconstructions(ifvs_index* idx);
 ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const ifvs_predicate* preds,
                               int32_t k, int32_t* ids_out, float* dist_out, void* stream);
 
+/* ---- Predicate encoder (Section 2, opening paragraph) ------------------
+ * The relational predicate f is encoded by a light-weight Transformer into
+ * the filter-aware weight vector w_z in R^D (then w_f = softplus(w_z),
+ * Section 2 first display).  The paper gives no architecture; this library
+ * implements the following one, with caller-supplied (trained) weights:
+ *   tokens: a summary token `cls`, then one token per clause (col, lo, hi)
+ *     in the predicate's order: col_embed[col] + a * feat_w[0] + b * feat_w[1]
+ *     + feat_b, where a = clip((lo - col_offset[col]) * col_scale[col], -1, 2)
+ *     and b likewise of hi, computed in double and rounded to float; no
+ *     positional encoding.
+ *   `layers` pre-norm encoder layers over all tokens:
+ *     Z = LN1(X); Q|K|V = Z Wqkv + bqkv; per head (width H / heads)
+ *     A = softmax over keys of Q K^T / sqrt(H / heads);
+ *     X += concat(A V) Wo + bo;  X += relu(LN2(X) W1 + b1) W2 + b2
+ *   w_z = LNf(X[summary]) Wout + bout.
+ *   LN(x) = (x - mean) / sqrt(biased variance + 1e-5) * g + b over H;
+ *   matrices map row vectors (y = x W + b) and are stored [in][out].
+ * `params` packs, as consecutive float arrays: col_embed [n_attr][H],
+ * feat_w [2][H], feat_b [H], cls [H]; per layer: ln1_g [H], ln1_b [H],
+ * Wqkv [H][3H] (columns: Q, then K, then V), bqkv [3H], Wo [H][H], bo [H],
+ * ln2_g [H], ln2_b [H], W1 [H][F], b1 [F], W2 [F][H], b2 [H]; then lnf_g [H],
+ * lnf_b [H], Wout [H][dim], bout [dim] -- n_params floats in all
+ * (ifvs_encoder_params gives the count).  Arithmetic is fp32 (the
+ * projections on matrix cores); results are within 1e-4 relative of the
+ * definition in exact arithmetic at the shapes the tests use. */
+typedef struct {
+  int32_t hidden;             /* H: 16..128, a multiple of 16                    */
+  int32_t heads;              /* divides H                                       */
+  int32_t layers;             /* 1..8                                            */
+  int32_t ffn;                /* F: 16..256, a multiple of 16                    */
+  int64_t n_params;           /* floats in params (must equal ifvs_encoder_params) */
+  const float* params;        /* packed weights, layout above                    */
+  const double* col_offset;   /* [n_attr] bound offset of each attribute column  */
+  const double* col_scale;    /* [n_attr] bound scale of each column (finite)    */
+  int32_t mem_kind;           /* IFVS_MEM_HOST | IFVS_MEM_DEVICE, all three arrays */
+  int32_t reserved;           /* must be 0 */
+} ifvs_encoder_desc;
+
+/* Floats in the packed parameters of an encoder of these sizes for an index
+ * of `n_attr` attribute columns and `dim` dimensions; -1 when a size is out
+ * of range. */
+int64_t ifvs_encoder_params(int32_t hidden, int32_t heads, int32_t layers, int32_t ffn, int32_t n_attr,
+                            int32_t dim);
+
+/* ifvs_load_encoder -- attaches an encoder to the index: deep-copies the
+ * desc's arrays into library-owned device memory (the caller may free its
+ * arrays after return), replacing any earlier encoder.  Synchronous.
+ * Errors: IFVS_E_INVALID (sizes out of range, n_params mismatch, NULL
+ * arrays, non-finite offset or scale, reserved != 0), IFVS_E_STATE (NULL
+ * handle), IFVS_E_NOMEM, IFVS_E_HIP.  On error the earlier encoder (if any)
+ * stays attached. */
+ifvs_status ifvs_load_encoder(ifvs_index* idx, const ifvs_encoder_desc* desc);
+
+/* ifvs_encode_predicates -- w_z of each predicate through the attached
+ * encoder (Section 2, opening paragraph), ready for ifvs_select_codebook.
+ *  preds:  HOST [nq], validated as in ifvs_filter (copied inside the call)
+ *  wz_out: device [nq][dim] fp32, caller-owned
+ * Enqueued on `stream`; nq = 0 writes nothing.
+ * Errors: IFVS_E_INVALID (nq outside 0..max_batch, NULL wz_out, predicate
+ * errors), IFVS_E_STATE (NULL handle, no encoder attached), IFVS_E_HIP. */
+ifvs_status ifvs_encode_predicates(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds, float* wz_out,
+                                   void* stream);
+
 /* Tuning knobs, never needed for correctness.  IFVS_OPT_QTILE forces the
  * number of queries whose tables share one LDS residency and one pass over
  * the codes (0 = automatic); IFVS_OPT_SPLITS forces the number of code chunks
@@ -389,9 +452,9 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value);
  * call waits for the recorded events, writes the summed kernel time (ms) and
  * the launch count of each stage, and clears the totals.  Stages, in array
  * order (IFVS_N_STAGES entries each): condition, distance table, filter,
- * scan, top-k merge.  Errors: IFVS_E_INVALID (NULL arrays), IFVS_E_STATE,
- * IFVS_E_HIP. */
-#define IFVS_N_STAGES 5
+ * scan, top-k merge, predicate encoder.  Errors: IFVS_E_INVALID (NULL
+ * arrays), IFVS_E_STATE, IFVS_E_HIP. */
+#define IFVS_N_STAGES 6
 ifvs_status ifvs_read_profile(ifvs_index* idx, double* ms_out, int64_t* launches_out);
 
 /* ifvs_read_scan_reads -- with IFVS_OPT_COUNT_READS on: hist_out[n] (65

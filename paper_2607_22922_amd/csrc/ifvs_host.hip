@@ -57,7 +57,7 @@ bool forced_alloc_failure() {
 constexpr int kStagingSlots = 8;
 
 // Optional per-stage kernel timing with HIP events (IFVS_OPT_PROFILE).
-enum Stage { kStCondition = 0, kStLut, kStFilter, kStScan, kStMerge, kStages };
+enum Stage { kStCondition = 0, kStLut, kStFilter, kStScan, kStMerge, kStEncode, kStages };
 constexpr int kProfilePairs = 4096;
 
 struct StageTimer {
@@ -214,6 +214,11 @@ struct ifvs_index {
   // table reads by active lanes into this device histogram ([65]).
   int opt_count_reads = 0;
   unsigned long long* read_hist = nullptr;
+  // Predicate encoder (ifvs_load_encoder); null params: none attached.
+  float* enc_params = nullptr;
+  double* enc_off = nullptr;     // [n_attr]
+  double* enc_scale = nullptr;   // [n_attr]
+  int enc_H = 0, enc_heads = 0, enc_layers = 0, enc_F = 0;
   StageTimer* timers = nullptr;  // [kStages] once profiling was enabled
   ScanPlan last_plan{};
 
@@ -255,7 +260,8 @@ struct ifvs_index {
                     static_cast<void*>(counts), static_cast<void*>(count_parts), static_cast<void*>(vstart),
                     static_cast<void*>(partials), static_cast<void*>(codes_rm),
                     static_cast<void*>(lists), static_cast<void*>(list_n), static_cast<void*>(qmode),
-                    static_cast<void*>(read_hist)})
+                    static_cast<void*>(read_hist), static_cast<void*>(enc_params),
+                    static_cast<void*>(enc_off), static_cast<void*>(enc_scale)})
       if (p) hipFree(p);
     free_vectors();
     for (void* p : {static_cast<void*>(tr_alpha), static_cast<void*>(tr_wf), static_cast<void*>(tr_lut),
@@ -1492,6 +1498,96 @@ ifvs_status ifvs_read_profile(ifvs_index* idx, double* ms_out, int64_t* launches
     t.launches = 0;
   }
   return IFVS_OK;
+}
+
+int64_t ifvs_encoder_params(int32_t hidden, int32_t heads, int32_t layers, int32_t ffn, int32_t n_attr,
+                            int32_t dim) {
+  if (hidden < 16 || hidden > 128 || hidden % 16 != 0) return -1;
+  if (heads < 1 || hidden % heads != 0) return -1;
+  if (layers < 1 || layers > 8) return -1;
+  if (ffn < 16 || ffn > 256 || ffn % 16 != 0) return -1;
+  if (n_attr < 1 || dim < 1) return -1;
+  const int64_t H = hidden, F = ffn;
+  const int64_t per_layer = 2 * H + H * 3 * H + 3 * H + H * H + H + 2 * H + H * F + F + F * H + H;
+  return int64_t{n_attr} * H + 2 * H + H + H + layers * per_layer + 2 * H + H * dim + dim;
+}
+
+ifvs_status ifvs_load_encoder(ifvs_index* idx, const ifvs_encoder_desc* desc) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (!desc) return fail(IFVS_E_INVALID, "desc is NULL");
+  const ifvs_encoder_desc& d = *desc;
+  if (d.reserved != 0) return fail(IFVS_E_INVALID, "encoder desc: reserved field not 0");
+  if (idx->n_attr < 1) return fail(IFVS_E_INVALID, "the index has no attribute columns to encode");
+  const int64_t want = ifvs_encoder_params(d.hidden, d.heads, d.layers, d.ffn, idx->n_attr, idx->dim);
+  if (want < 0)
+    return fail(IFVS_E_INVALID, "encoder sizes out of range (hidden 16..128 and ffn 16..256, multiples of 16; "
+                                "heads dividing hidden; layers 1..8)");
+  if (d.n_params != want)
+    return fail(IFVS_E_INVALID, "encoder n_params = " + std::to_string(d.n_params) + ", the sizes need " +
+                                    std::to_string(want));
+  if (!d.params || !d.col_offset || !d.col_scale) return fail(IFVS_E_INVALID, "encoder arrays must not be NULL");
+  if (d.mem_kind != IFVS_MEM_HOST && d.mem_kind != IFVS_MEM_DEVICE) return fail(IFVS_E_INVALID, "unknown mem_kind");
+  const hipMemcpyKind kind = d.mem_kind == IFVS_MEM_HOST ? hipMemcpyHostToDevice : hipMemcpyDeviceToDevice;
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  std::vector<double> off(idx->n_attr), sc(idx->n_attr);
+  IFVS_HIP(hipMemcpy(off.data(), d.col_offset, off.size() * sizeof(double),
+                     d.mem_kind == IFVS_MEM_HOST ? hipMemcpyHostToHost : hipMemcpyDeviceToHost),
+           "reading encoder offsets");
+  IFVS_HIP(hipMemcpy(sc.data(), d.col_scale, sc.size() * sizeof(double),
+                     d.mem_kind == IFVS_MEM_HOST ? hipMemcpyHostToHost : hipMemcpyDeviceToHost),
+           "reading encoder scales");
+  for (int c = 0; c < idx->n_attr; ++c)
+    if (!std::isfinite(off[c]) || !std::isfinite(sc[c]))
+      return fail(IFVS_E_INVALID, "encoder offset or scale of column " + std::to_string(c) + " is not finite");
+  float* p = nullptr;
+  double* o = nullptr;
+  double* k = nullptr;
+  auto undo = [&](ifvs_status st) {
+    for (void* x : {static_cast<void*>(p), static_cast<void*>(o), static_cast<void*>(k)})
+      if (x) (void)hipFree(x);
+    return st;
+  };
+  if (ifvs_status st = dev_alloc(&p, static_cast<size_t>(want), "encoder parameters"); st != IFVS_OK) return undo(st);
+  if (ifvs_status st = dev_alloc(&o, static_cast<size_t>(idx->n_attr), "encoder offsets"); st != IFVS_OK)
+    return undo(st);
+  if (ifvs_status st = dev_alloc(&k, static_cast<size_t>(idx->n_attr), "encoder scales"); st != IFVS_OK)
+    return undo(st);
+  if (hipError_t e = hipMemcpy(p, d.params, static_cast<size_t>(want) * sizeof(float), kind); e != hipSuccess)
+    return undo(hip_fail(e, "loading encoder parameters"));
+  if (hipError_t e = hipMemcpy(o, off.data(), off.size() * sizeof(double), hipMemcpyHostToDevice); e != hipSuccess)
+    return undo(hip_fail(e, "loading encoder offsets"));
+  if (hipError_t e = hipMemcpy(k, sc.data(), sc.size() * sizeof(double), hipMemcpyHostToDevice); e != hipSuccess)
+    return undo(hip_fail(e, "loading encoder scales"));
+  if (hipError_t e = hipDeviceSynchronize(); e != hipSuccess) return undo(hip_fail(e, "loading the encoder"));
+  for (void* x : {static_cast<void*>(idx->enc_params), static_cast<void*>(idx->enc_off),
+                  static_cast<void*>(idx->enc_scale)})
+    if (x) (void)hipFree(x);
+  idx->enc_params = p;
+  idx->enc_off = o;
+  idx->enc_scale = k;
+  idx->enc_H = d.hidden;
+  idx->enc_heads = d.heads;
+  idx->enc_layers = d.layers;
+  idx->enc_F = d.ffn;
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_encode_predicates(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds, float* wz_out,
+                                   void* stream) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
+  if (!idx->enc_params) return fail(IFVS_E_STATE, "no encoder attached (ifvs_load_encoder)");
+  if (nq == 0) return IFVS_OK;
+  if (!wz_out) return fail(IFVS_E_INVALID, "wz_out is NULL");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  int slot = 0;
+  if (ifvs_status st = stage_predicates(idx, nq, preds, false, false, s, &slot); st != IFVS_OK) return st;
+  IFVS_LAUNCH(idx, kStEncode, s, "launching encoder kernel",
+              launch_encoder(idx->enc_params, idx->enc_off, idx->enc_scale, idx->enc_H, idx->enc_heads,
+                             idx->enc_layers, idx->enc_F, idx->dim, idx->n_attr, idx->staging_dev[slot], nq,
+                             wz_out, s));
+  return release_slot(idx, slot, s);
 }
 
 ifvs_status ifvs_read_scan_reads(ifvs_index* idx, int64_t* hist_out, void* stream) {

@@ -221,6 +221,13 @@ hipError_t launch_compact(const uint64_t* bitmap, int64_t stride64, const unsign
 hipError_t launch_gather_scan(const GatherBatch& b, hipStream_t s);
 
 hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s);
+// Predicate encoder (k_encoder.hip): w_z [nq][D] of the predicates in
+// `preds` (device-readable DevPred records) through the packed parameters
+// (layout in ifvs.h), H <= 128 a multiple of 16, F <= 256 a multiple of 16.
+size_t encoder_lds_bytes(int H, int F);
+hipError_t launch_encoder(const float* params, const double* off, const double* scale, int H, int heads, int layers,
+                          int F, int D, int n_attr, const DevPred* preds, int nq, float* wz, hipStream_t s);
+
 // Whether a read-counting build of the scan exists for this plan (one query
 // per tile, M of 16, 48 or 120).
 bool scan_can_count(int m, int qtile, int lut_dtype);

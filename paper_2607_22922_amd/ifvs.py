@@ -29,13 +29,14 @@ OPT_SHARED_BOUND = 9
 OPT_EXACT_PLAN = 10
 OPT_SEED_TILES = 11
 OPT_COUNT_READS = 12
-STAGES = ("condition", "lut", "filter", "scan", "merge")
+STAGES = ("condition", "lut", "filter", "scan", "merge", "encode")
 
 EXPORTED = ("ifvs_load_index", "ifvs_free_index", "ifvs_select_codebook", "ifvs_build_lut",
             "ifvs_filter", "ifvs_filtered_search", "ifvs_set_option", "ifvs_last_plan",
             "ifvs_read_profile", "ifvs_last_error", "ifvs_load_vectors", "ifvs_exact_search",
             "ifvs_build_sdc_lut", "ifvs_load_reconstructions", "ifvs_train_step", "ifvs_read_params",
-            "ifvs_filtered_search_noalloc", "ifvs_read_scan_reads", "ifvs_probe_lds_gather")
+            "ifvs_filtered_search_noalloc", "ifvs_read_scan_reads", "ifvs_probe_lds_gather",
+            "ifvs_encoder_params", "ifvs_load_encoder", "ifvs_encode_predicates")
 
 
 class IfvsError(RuntimeError):
@@ -78,6 +79,21 @@ class Predicate(ctypes.Structure):
                 ("c", Clause * MAX_CLAUSES)]
 
 
+class EncoderDesc(ctypes.Structure):
+    _fields_ = [
+        ("hidden", ctypes.c_int32),
+        ("heads", ctypes.c_int32),
+        ("layers", ctypes.c_int32),
+        ("ffn", ctypes.c_int32),
+        ("n_params", ctypes.c_int64),
+        ("params", ctypes.c_void_p),
+        ("col_offset", ctypes.c_void_p),
+        ("col_scale", ctypes.c_void_p),
+        ("mem_kind", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+    ]
+
+
 def _load_library() -> ctypes.CDLL:
     if not os.path.exists(_LIB_PATH):
         raise ImportError(f"{_LIB_PATH} is missing: build it with "
@@ -105,6 +121,9 @@ def _load_library() -> ctypes.CDLL:
         "ifvs_read_params": ([vp, vp, vp, vp], i32),
         "ifvs_read_scan_reads": ([vp, ctypes.POINTER(ctypes.c_int64), vp], i32),
         "ifvs_probe_lds_gather": ([i32, ctypes.POINTER(ctypes.c_double), vp], i32),
+        "ifvs_encoder_params": ([i32, i32, i32, i32, i32, i32], i64),
+        "ifvs_load_encoder": ([vp, ctypes.POINTER(EncoderDesc)], i32),
+        "ifvs_encode_predicates": ([vp, i32, vp, vp, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -234,6 +253,40 @@ class Index:
         n = (ctypes.c_int64 * len(STAGES))()
         _check(_lib.ifvs_read_profile(self.handle, ms, n))
         return {name: (ms[i], n[i]) for i, name in enumerate(STAGES)}
+
+    def load_encoder(self, enc: dict) -> None:
+        """ifvs_load_encoder from a dict of weights (the names of the layout
+        in ifvs.h; per-layer weights under "layers", a list of dicts with
+        Wq, Wk, Wv, bq, bk, bv, Wo, bo, ln1_g, ln1_b, ln2_g, ln2_b, W1, b1,
+        W2, b2).  Packs them in the documented order (host memory)."""
+        H, F = int(enc["cls"].shape[0]), int(enc["layers"][0]["W1"].shape[1])
+        heads, layers = int(enc["heads"]), len(enc["layers"])
+        f = lambda t: torch.as_tensor(t).detach().to("cpu", torch.float32).reshape(-1)
+        parts = [f(enc["col_embed"]), f(enc["feat_w"]), f(enc["feat_b"]), f(enc["cls"])]
+        for p in enc["layers"]:
+            wqkv = torch.cat([torch.as_tensor(p[k]).detach().cpu().float() for k in ("Wq", "Wk", "Wv")], dim=1)
+            bqkv = torch.cat([torch.as_tensor(p[k]).detach().cpu().float() for k in ("bq", "bk", "bv")])
+            parts += [f(p["ln1_g"]), f(p["ln1_b"]), f(wqkv), f(bqkv), f(p["Wo"]), f(p["bo"]),
+                      f(p["ln2_g"]), f(p["ln2_b"]), f(p["W1"]), f(p["b1"]), f(p["W2"]), f(p["b2"])]
+        parts += [f(enc["lnf_g"]), f(enc["lnf_b"]), f(enc["out_w"]), f(enc["out_b"])]
+        packed = torch.cat(parts).contiguous()
+        off = torch.as_tensor(enc["col_offset"]).detach().to("cpu", torch.float64).contiguous()
+        sc = torch.as_tensor(enc["col_scale"]).detach().to("cpu", torch.float64).contiguous()
+        d = EncoderDesc()
+        d.hidden, d.heads, d.layers, d.ffn = H, heads, layers, F
+        d.n_params = packed.numel()
+        d.params, d.col_offset, d.col_scale = packed.data_ptr(), off.data_ptr(), sc.data_ptr()
+        d.mem_kind = MEM_HOST
+        _check(_lib.ifvs_load_encoder(self.handle, ctypes.byref(d)))
+
+    def encode_predicates_into(self, nq, preds_c, wz_out, stream=None):
+        _check(_lib.ifvs_encode_predicates(self.handle, nq, preds_c, wz_out.data_ptr(), _stream(stream)))
+
+    def encode_predicates(self, preds):
+        """w_z [nq][dim] of each predicate through the attached encoder."""
+        wz = torch.empty(len(preds), self.dim, device=self.device, dtype=torch.float32)
+        self.encode_predicates_into(len(preds), pack_predicates(preds), wz)
+        return wz
 
     def read_scan_reads(self, stream=None) -> list:
         """With OPT_COUNT_READS on: [65] table reads issued with n active

@@ -75,3 +75,18 @@ def test_null_handle_and_error_text_without_gpu():
     assert b"NULL" in lib.ifvs_last_error()
     assert lib.ifvs_load_index(None, None) == B.E_INVALID
     lib.ifvs_free_index(None)
+
+
+def test_encoder_parameter_count_matches_the_documented_layout():
+    """ifvs_encoder_params (a host-only function) counts the floats of the
+    layout include/ifvs.h documents; sizes out of range give -1."""
+    lib = ctypes.CDLL(LIB)
+    fn = lib.ifvs_encoder_params
+    fn.argtypes = [ctypes.c_int32] * 6
+    fn.restype = ctypes.c_int64
+    for H, heads, L, F, A, D in [(64, 4, 2, 128, 1, 96), (16, 16, 1, 16, 3, 7), (128, 8, 8, 256, 2, 960)]:
+        per_layer = 2 * H + 3 * H * H + 3 * H + H * H + H + 2 * H + H * F + F + F * H + H
+        assert fn(H, heads, L, F, A, D) == A * H + 2 * H + 2 * H + L * per_layer + 2 * H + H * D + D
+    for bad in [(8, 1, 1, 16, 1, 4), (48 + 1, 1, 1, 16, 1, 4), (64, 3, 1, 16, 1, 4), (64, 4, 0, 16, 1, 4),
+                (64, 4, 9, 16, 1, 4), (64, 4, 1, 272, 1, 4), (144, 4, 1, 16, 1, 4), (64, 4, 1, 16, 0, 4)]:
+        assert fn(*bad) == -1, bad
