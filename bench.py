@@ -406,6 +406,9 @@ def main():
     log(f"[bench] generated in {time.time() - t0:.1f}s; loading indexes")
     clus = B.Index.from_workload(w, max_batch=batch, max_k=k, cluster_cols=cols)
     plain = B.Index.from_workload(w, max_batch=batch, max_k=k) if args.plain_steps > 0 else None
+    for ix_ in (clus, plain):
+        if ix_ is not None:
+            ix_.load_encoder(w.enc)
     n_batches = n_q // batch
     bins = w.bins
 
@@ -413,6 +416,7 @@ def main():
     packed = {s: [B.pack_predicates(w.preds[s][b * batch:(b + 1) * batch]) for b in range(n_batches)]
               for s in bins}
     alpha = torch.empty(batch, w.M * w.r, device=dev)
+    wz = torch.empty(batch, w.D, device=dev)
     wf = torch.empty(batch, w.D, device=dev)
     lut = torch.empty(batch, w.M, 256, device=dev,
                       dtype=torch.float16 if lut_dt == B.LUT_F16 else torch.float32)
@@ -423,7 +427,8 @@ def main():
     def run_batch(idx, s, b):
         sl = slice(b * batch, (b + 1) * batch)
         q = w.queries[sl]
-        idx.select_codebook_into(q, packed[s][b], w.w_z[s][sl], alpha, wf)
+        idx.encode_predicates_into(batch, packed[s][b], wz)
+        idx.select_codebook_into(q, packed[s][b], wz, alpha, wf)
         idx.build_lut_into(q, alpha, wf, lut_dt, lut)
         idx.search_into(batch, packed[s][b], lut, lut_dt, k, ids[s], dist[s])
 
@@ -586,7 +591,8 @@ def main():
         log(f"[bench] plain layout: {plain_out['qps']:.0f} queries/s, scan {plain_out['scan_GBps']:.0f} GB/s")
         # both layouts must return the same answers
         for s in bins:
-            a_, f_ = clus.select_codebook(w.queries[:batch], w.preds[s][:batch], w.w_z[s][:batch])
+            a_, f_ = clus.select_codebook(w.queries[:batch], w.preds[s][:batch],
+                                          clus.encode_predicates(w.preds[s][:batch]))
             lt = clus.build_lut(w.queries[:batch], a_, f_, lut_dt)
             i1, d1 = clus.search(w.preds[s][:batch], lt, k, lut_dt)
             i2, d2 = plain.search(w.preds[s][:batch], lt, k, lut_dt)
@@ -612,7 +618,7 @@ def main():
             elif mode == "identity":
                 lt = clus.build_lut(q, None, None, lut_dt)
             else:
-                a_, f_ = clus.select_codebook(q, preds, w.w_z[s][:nr])
+                a_, f_ = clus.select_codebook(q, preds, clus.encode_predicates(preds))
                 lt = clus.build_lut(q, a_, f_, lut_dt)
             got, _ = clus.search(preds, lt, k, lut_dt)
             g_np = got.cpu().numpy()
@@ -624,26 +630,24 @@ def main():
             bins_out[str(s)][f"recall@{k}_{mode}"] = round(hits / nr, 4)
     log(f"[bench] bins: {json.dumps(bins_out)}")
 
-    # PCIe-inclusive rate: the same step with the batch's query vectors and
-    # predicate weights copied from pinned host memory at its start and the
-    # ids and distances copied back at its end, all on the stream.
+    # PCIe-inclusive rate: the same step with the batch's query vectors
+    # copied from pinned host memory at its start and the ids and distances
+    # copied back at its end, all on the stream (the predicate weights come
+    # from the encoder on the device, the predicates are host arrays already).
     host_out = None
     if args.host_steps > 0:
         hq = torch.empty(batch, w.D, pin_memory=True)
-        hwz = torch.empty(batch, w.D, pin_memory=True)
         hid = torch.empty(batch, k, dtype=torch.int32, pin_memory=True)
         hdi = torch.empty(batch, k, pin_memory=True)
         q_dev = torch.empty(batch, w.D, device=dev)
-        wz_dev = torch.empty(batch, w.D, device=dev)
-        host_src = {s: [(w.queries[b * batch:(b + 1) * batch].cpu(), w.w_z[s][b * batch:(b + 1) * batch].cpu())
+        host_src = {s: [w.queries[b * batch:(b + 1) * batch].cpu()
                         for b in range(min(n_batches, args.host_steps))] for s in bins}
 
         def run_host(s, b):
-            hq.copy_(host_src[s][b][0])
-            hwz.copy_(host_src[s][b][1])
+            hq.copy_(host_src[s][b])
             q_dev.copy_(hq, non_blocking=True)
-            wz_dev.copy_(hwz, non_blocking=True)
-            clus.select_codebook_into(q_dev, packed[s][b], wz_dev, alpha, wf)
+            clus.encode_predicates_into(batch, packed[s][b], wz)
+            clus.select_codebook_into(q_dev, packed[s][b], wz, alpha, wf)
             clus.build_lut_into(q_dev, alpha, wf, lut_dt, lut)
             clus.search_into(batch, packed[s][b], lut, lut_dt, k, ids[s], dist[s])
             hid.copy_(ids[s], non_blocking=True)
@@ -662,7 +666,7 @@ def main():
             host_total += sum(ms)
             host_bins[str(s)] = {"qps": batch * len(ms) / (sum(ms) / 1e3), "ms_per_batch": float(np.median(ms))}
         host_out = {"qps": args.host_steps * len(bins) * batch / (host_total / 1e3), "steps": args.host_steps,
-                    "bytes_to_device_per_batch": 2 * batch * w.D * 4, "bytes_to_host_per_batch": batch * k * 8,
+                    "bytes_to_device_per_batch": batch * w.D * 4, "bytes_to_host_per_batch": batch * k * 8,
                     "timing": "host wall clock per batch, from the host-side copy into the pinned buffers to "
                               "the results in pinned host memory", "bins": host_bins}
         log(f"[bench] with host transfers: {host_out['qps']:.0f} queries/s; {json.dumps(host_bins)}")
@@ -755,27 +759,31 @@ def main():
         for s in bins:
             q = w.queries[:n_gpu]
             preds = w.preds[s][:n_gpu]
-            a_, f_ = clus.select_codebook(q, preds, w.w_z[s][:n_gpu])
+            wz_g = clus.encode_predicates(preds)
+            a_, f_ = clus.select_codebook(q, preds, wz_g)
             lt = clus.build_lut(q, a_, f_, lut_dt)
             g_ids, g_d = clus.search(preds, lt, k, lut_dt)
-            gpu_res[s] = (g_ids.cpu().numpy(), g_d.cpu().numpy(), q.cpu().numpy(),
-                          w.w_z[s][:n_gpu].cpu().numpy())
+            gpu_res[s] = (g_ids.cpu().numpy(), g_d.cpu().numpy(), q.cpu().numpy(), wz_g.cpu().numpy())
 
         def oracle_mode(workers, per_bin):
-            tasks = [((s, i), gpu_res[s][2][i], w.preds[s][i], k, gpu_res[s][3][i], args.lut, True)
+            # each task: the oracle encodes the predicate (checked against the
+            # GPU's w_z), then answers the query from the GPU's w_z, so ids and
+            # distance bits can be compared exactly
+            tasks = [((s, i), gpu_res[s][2][i], w.preds[s][i], k, gpu_res[s][3][i], args.lut, True, True)
                      for s in bins for i in range(per_bin)]
-            with OraclePool(ox, workers) as pool:
+            with OraclePool(ox, workers, encoder=w.enc) as pool:
                 pool.search(tasks[:workers])                 # workers up, index mapped
                 t_ = time.perf_counter()
                 res = pool.search(tasks)
                 wall = time.perf_counter() - t_
             agree = all(np.array_equal(ids_o, gpu_res[key[0]][0][key[1]]) and
                         np.array_equal(d_o.view(np.uint32), gpu_res[key[0]][1][key[1]].view(np.uint32))
-                        for key, ids_o, d_o, _ in res)
+                        for key, ids_o, d_o, *_ in res)
             return {"value": len(tasks) / wall, "unit": "queries/s", "cores": workers,
                     "queries": len(tasks), "wall_s": round(wall, 2),
                     "cpu_s": round(sum(r[3] for r in res), 2),
-                    "ids_and_dist_bits_match_gpu": bool(agree)}
+                    "ids_and_dist_bits_match_gpu": bool(agree),
+                    "encoder_max_rel_err": max(r[4] for r in res)}
 
         model, avail = cpu_model(), host_cores()
         single = oracle_mode(1, min(args.cpu_sample, n_gpu)) if args.cpu_sample > 0 else None
@@ -797,6 +805,7 @@ def main():
                          + f", {head['wall_s']} s wall",
                "cpu_model": model, "affinity_cores": avail,
                "ids_and_dist_bits_match_gpu": head["ids_and_dist_bits_match_gpu"],
+               "encoder_max_rel_err_vs_gpu": head["encoder_max_rel_err"],
                "single_core": single, "all_cores": multi}
 
     if args.copy_calibration:
@@ -822,7 +831,7 @@ def main():
         "dtype": args.lut,
         "data": "synthetic",
         "config": {"workload": f"{name}: {DESCRIPTIONS[name]}", "batch": batch, "k": k,
-                   "bins": bins, "mode": "conditioned (bank, W, w_z)",
+                   "bins": bins, "mode": "conditioned (predicate encoder -> w_z, memory bank, W)",
                    "layout": ("rows clustered by the range attribute" if cols == (0,)
                               else "rows clustered by (category, range attribute)"),
                    "queries_per_step": len(bins) * batch,

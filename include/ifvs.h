@@ -357,7 +357,7 @@ ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const
  * definition in exact arithmetic at the shapes the tests use. */
 typedef struct {
   int32_t hidden;             /* H: 16..128, a multiple of 16                    */
-  int32_t heads;              /* divides H                                       */
+  int32_t heads;              /* 1..16, divides H                                */
   int32_t layers;             /* 1..8                                            */
   int32_t ffn;                /* F: 16..256, a multiple of 16                    */
   int64_t n_params;           /* floats in params (must equal ifvs_encoder_params) */

@@ -13,6 +13,12 @@ A worker that dies makes ``search`` raise.  The index arrays are written
 once to a temporary directory as ``.npy`` files and memory-mapped read-only
 by every worker, so a 1.6 GB code array is held once in the page cache, not
 once per worker.
+
+With an encoder (a dict of predicate-encoder weights), a task may also ask
+the worker to encode its predicate with ``encode_predicate`` before the
+search (the oracle then does every step of a conditioned query); the
+search itself uses the w_z the task carries, and the worker reports how far
+the oracle's own w_z is from it.
 """
 from __future__ import annotations
 
@@ -76,9 +82,12 @@ class OraclePool:
     the oracle over one index (a dict as ``filtered_search`` takes it).
     Use as a context manager; ``search`` returns results in task order."""
 
-    def __init__(self, index: dict, workers: int | None = None):
+    def __init__(self, index: dict, workers: int | None = None, encoder: dict | None = None):
         self.workers = max(1, int(workers if workers is not None else host_cores()))
         self._dir = tempfile.mkdtemp(prefix="oracle_pool_")
+        if encoder is not None:
+            with open(os.path.join(self._dir, "encoder.pkl"), "wb") as f:
+                pickle.dump(_to_numpy(encoder), f)
         for name in _ARRAYS:
             a = index.get(name)
             if a is not None:
@@ -95,8 +104,10 @@ class OraclePool:
 
     def search(self, tasks, progress=None):
         """tasks: iterable of (key, q [D], clauses, k, w_z [D] or None,
-        lut_dtype, conditioned).  Returns [(key, ids, dist, seconds)] in task
-        order; ``progress(done, total)`` is called as results arrive."""
+        lut_dtype, conditioned[, encode]).  Returns [(key, ids, dist, seconds,
+        enc_err)] in task order, enc_err = max over dimensions of
+        |w_z - oracle w_z| / (|oracle w_z| + 0.01) for tasks that encode, else
+        None; ``progress(done, total)`` is called as results arrive."""
         tasks = list(tasks)
         out = [None] * len(tasks)
         nxt = 0
@@ -152,10 +163,25 @@ class OraclePool:
         return False
 
 
+def _to_numpy(obj):
+    if isinstance(obj, dict):
+        return {k: _to_numpy(v) for k, v in obj.items()}
+    if isinstance(obj, (list, tuple)):
+        return [_to_numpy(v) for v in obj]
+    if hasattr(obj, "detach"):
+        return obj.detach().cpu().numpy()
+    return obj
+
+
 def _worker(root: str) -> None:
+    from oracle.ifvs_encoder_oracle import encode_predicate
     from oracle.ifvs_oracle import filtered_search
     with open(os.path.join(root, "scalars.pkl"), "rb") as f:
         index = pickle.load(f)
+    enc = None
+    if os.path.exists(os.path.join(root, "encoder.pkl")):
+        with open(os.path.join(root, "encoder.pkl"), "rb") as f:
+            enc = pickle.load(f)
     for name in _ARRAYS:
         path = os.path.join(root, name + ".npy")
         index[name] = np.load(path, mmap_mode="r") if os.path.exists(path) else None
@@ -164,10 +190,16 @@ def _worker(root: str) -> None:
         msg = _recv(fin)
         if msg is None:
             return
-        pos, (key, q, clauses, k, w_z, lut_dtype, conditioned) = msg
+        pos, task = msg
+        key, q, clauses, k, w_z, lut_dtype, conditioned = task[:7]
+        encode = len(task) > 7 and bool(task[7])
         t0 = time.perf_counter()
+        enc_err = None
+        if encode:
+            ref = encode_predicate(clauses, enc)
+            enc_err = float(np.max(np.abs(np.asarray(w_z, dtype=np.float64) - ref) / (np.abs(ref) + 0.01)))
         res = filtered_search(index, q, clauses, k, w_z=w_z, lut_dtype=lut_dtype, conditioned=conditioned)
-        _send(fout, (pos, (key, res["ids"], res["dist"], time.perf_counter() - t0)))
+        _send(fout, (pos, (key, res["ids"], res["dist"], time.perf_counter() - t0, enc_err)))
 
 
 if __name__ == "__main__":

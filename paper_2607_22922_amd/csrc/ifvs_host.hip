@@ -1503,7 +1503,7 @@ ifvs_status ifvs_read_profile(ifvs_index* idx, double* ms_out, int64_t* launches
 int64_t ifvs_encoder_params(int32_t hidden, int32_t heads, int32_t layers, int32_t ffn, int32_t n_attr,
                             int32_t dim) {
   if (hidden < 16 || hidden > 128 || hidden % 16 != 0) return -1;
-  if (heads < 1 || hidden % heads != 0) return -1;
+  if (heads < 1 || heads > 16 || hidden % heads != 0) return -1;
   if (layers < 1 || layers > 8) return -1;
   if (ffn < 16 || ffn > 256 || ffn % 16 != 0) return -1;
   if (n_attr < 1 || dim < 1) return -1;
@@ -1521,7 +1521,7 @@ ifvs_status ifvs_load_encoder(ifvs_index* idx, const ifvs_encoder_desc* desc) {
   const int64_t want = ifvs_encoder_params(d.hidden, d.heads, d.layers, d.ffn, idx->n_attr, idx->dim);
   if (want < 0)
     return fail(IFVS_E_INVALID, "encoder sizes out of range (hidden 16..128 and ffn 16..256, multiples of 16; "
-                                "heads dividing hidden; layers 1..8)");
+                                "heads 1..16 dividing hidden; layers 1..8)");
   if (d.n_params != want)
     return fail(IFVS_E_INVALID, "encoder n_params = " + std::to_string(d.n_params) + ", the sizes need " +
                                     std::to_string(want));

@@ -10,12 +10,15 @@
 // summary token mapped by an H x D matrix to w_z.
 //
 // One workgroup encodes kEncQ predicates: their tokens are the rows of a
-// 32 x H matrix in LDS (8 slots per predicate: summary + at most 4 clauses,
+// 16 x H matrix in LDS (8 slots per predicate: summary + at most 4 clauses,
 // the rest padding that attention never reads).  Every projection (Q/K/V,
-// output, both feed-forward matrices) is a dense 32 x K x N contraction done
-// with fp32 matrix-core instructions (v_mfma_f32_16x16x4_f32), the weights
-// read from global memory (they stay in L2 across the workgroups); layer
-// norms, the per-head softmax and the final H x D map run on the vector ALU.
+// output, both feed-forward matrices) is a dense 16 x K x N contraction done
+// with fp32 matrix-core instructions (v_mfma_f32_16x16x4_f32).  The weights
+// (the same for every workgroup, so L2-resident) are staged into LDS in
+// column chunks of up to 34 KB, every thread moving 16-byte words with eight
+// loads in flight, so a projection waits for memory once or twice rather
+// than once per 16-deep step; layer norms, the per-head softmax and the
+// final H x D map run on the vector ALU.
 #include <cmath>
 
 #include "ifvs_internal.h"
@@ -24,12 +27,15 @@ namespace ifvs {
 
 namespace {
 
-constexpr int kEncQ = 4;                       // predicates per workgroup
+constexpr int kEncQ = 2;                       // predicates per workgroup
 constexpr int kEncSlots = 8;                   // token slots per predicate
-constexpr int kEncRows = kEncQ * kEncSlots;    // token rows per workgroup (two 16-row MFMA blocks)
+constexpr int kEncRows = kEncQ * kEncSlots;    // token rows per workgroup (one 16-row MFMA block)
 constexpr int kEncThreads = 256;
 constexpr int kEncWaves = kEncThreads / 64;
 constexpr int kPad = 4;                        // LDS row padding (floats): spreads a 16 x 4 operand over the banks
+constexpr int kWbuf = 9216;                    // floats of the weight staging buffer: 8192 + padding (36 KB)
+constexpr int kEncMaxHeads = 16;
+constexpr int kEncVec = 9 * 128 + 256;          // a layer's gains and biases at the largest H and F
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
@@ -43,100 +49,219 @@ struct EncArgs {
   float* wz;               // [nq][D]
 };
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+// Weight chunks.  A matrix W [K][N] (row-major, rows 16-byte aligned) goes
+// through the LDS buffer in chunks of chunk_cols(K, N) columns, at most 8192
+// floats each, so one chunk is eight 16-byte words per thread.  The next
+// chunk is loaded into registers (Prefetch) while the current one is
+// multiplied, so a projection seldom waits for memory.
+struct Chunk {
+  const float* W;
+  int K, N, n0, cols;
+};
+
+// Columns of the chunk starting at n0: the largest power of two (>= 16) that
+// fits both 8192 / K and the columns left (N - n0, a multiple of 16), so a
+// word's row and column follow from shifts.
+__device__ __forceinline__ int chunk_cols(int K, int N, int n0) {
+  const int lim = min(8192 / K, N - n0);
+  int c = 16;
+  while (2 * c <= lim) c *= 2;
+  return c;
 }
 
-// Y = (accumulate ? Y : 0) + A W + bias (then ReLU if relu), for the 32 token
-// rows: A [32][K] in LDS (row stride lda), W [K][N] row-major in global
-// memory, bias [N]; K a multiple of 4, N of 16.  Wave w computes the 16-column
-// blocks w, w + 4, ...; for each, both 16-row blocks share the B operand.
+__device__ __forceinline__ Chunk first_chunk(const float* W, int K, int N) { return {W, K, N, 0, chunk_cols(K, N, 0)}; }
+
+struct Prefetch {
+  float4 v0, v1, v2, v3, v4, v5, v6, v7;   // eight named words: they stay in registers
+};
+
+__device__ __forceinline__ float4 chunk_word(const Chunk& c, int u) {
+  const int sh = __builtin_ctz(c.cols / 4), words = c.K << sh;   // words per row: a power of two
+  // past the end: load the last word again (in bounds; not stored)
+  const int e = min(u * kEncThreads + static_cast<int>(threadIdx.x), words - 1);
+  return *reinterpret_cast<const float4*>(c.W + static_cast<size_t>(e >> sh) * c.N + c.n0 +
+                                          4 * (e & ((1 << sh) - 1)));
+}
+
+__device__ __forceinline__ void prefetch(const Chunk& c, Prefetch& pf) {
+  if (!c.W) return;
+  pf.v0 = chunk_word(c, 0);
+  pf.v1 = chunk_word(c, 1);
+  pf.v2 = chunk_word(c, 2);
+  pf.v3 = chunk_word(c, 3);
+  pf.v4 = chunk_word(c, 4);
+  pf.v5 = chunk_word(c, 5);
+  pf.v6 = chunk_word(c, 6);
+  pf.v7 = chunk_word(c, 7);
+}
+
+// Words past the chunk's end go to the 16-byte sink after the buffer.
+__device__ __forceinline__ void commit_word(const Chunk& c, float* Wb, int ldw, int u, const float4& v) {
+  const int sh = __builtin_ctz(c.cols / 4), words = c.K << sh;
+  const int e = u * kEncThreads + static_cast<int>(threadIdx.x);
+  const int at = e < words ? (e >> sh) * ldw + 4 * (e & ((1 << sh) - 1)) : kWbuf;
+  *reinterpret_cast<float4*>(Wb + at) = v;
+}
+
+__device__ __forceinline__ void commit(const Chunk& c, const Prefetch& pf, float* Wb, int ldw) {
+  commit_word(c, Wb, ldw, 0, pf.v0);
+  commit_word(c, Wb, ldw, 1, pf.v1);
+  commit_word(c, Wb, ldw, 2, pf.v2);
+  commit_word(c, Wb, ldw, 3, pf.v3);
+  commit_word(c, Wb, ldw, 4, pf.v4);
+  commit_word(c, Wb, ldw, 5, pf.v5);
+  commit_word(c, Wb, ldw, 6, pf.v6);
+  commit_word(c, Wb, ldw, 7, pf.v7);
+}
+
+// Y = (accumulate ? Y : 0) + A W + bias (then ReLU if relu), for the 16
+// token rows: A [16][K] in LDS (row stride lda), W [K][N], bias [N] (LDS); K a
+// multiple of 4, N of 16.  On entry pf holds W's first chunk; on return it
+// holds the first chunk of `next` (the following projection's matrix).
+// Wave w computes the 16-column blocks w, w + 4, ... of each chunk.
 // Operand layout of v_mfma_f32_16x16x4_f32: lane l holds A[l % 16][l / 16]
 // and B[l / 16][l % 16]; result register i of lane l is D[4 (l / 16) + i][l % 16].
-__device__ void gemm_rows(const float* A, int lda, int K, const float* __restrict__ W,
-                          const float* __restrict__ bias, int N, float* Y, int ldy, bool accumulate, bool relu) {
+__device__ __forceinline__ void gemm_rows(const float* A, int lda, const Chunk& w0, const float* bias, float* Y,
+                          int ldy, bool accumulate, bool relu, float* Wb, Prefetch& pf, const Chunk& next) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kq = lane >> 4;
-  for (int cb = wave; cb < N / 16; cb += kEncWaves) {
-    const int col = cb * 16 + r16;
-    floatx4 acc0 = {0.0f, 0.0f, 0.0f, 0.0f};
-    floatx4 acc1 = {0.0f, 0.0f, 0.0f, 0.0f};
-    for (int k0 = 0; k0 < K; k0 += 16) {
-      float b[4], a0[4], a1[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int k = k0 + 4 * u + kq;
-        const bool in = k < K;
-        b[u] = in ? W[static_cast<size_t>(k) * N + col] : 0.0f;
-        a0[u] = in ? A[r16 * lda + k] : 0.0f;
-        a1[u] = in ? A[(16 + r16) * lda + k] : 0.0f;
+  const int K = w0.K, N = w0.N;
+  for (Chunk c = w0; c.n0 < N;) {
+    const int ldw = c.cols + kPad;
+    __syncthreads();                      // the buffer's readers are done, A is written
+    commit(c, pf, Wb, ldw);
+    __syncthreads();
+    Chunk nx = c;
+    nx.n0 = c.n0 + c.cols;
+    nx.cols = nx.n0 < N ? chunk_cols(K, N, nx.n0) : 16;
+    prefetch(nx.n0 < N ? nx : next, pf);
+    // Two column blocks per wave at a time (two independent accumulator
+    // chains); a wave with one block left multiplies it twice and keeps one.
+    const int nb = c.cols / 16;
+    for (int cb = wave; cb < nb; cb += 2 * kEncWaves) {
+      const bool two = cb + kEncWaves < nb;
+      const int cb1 = two ? cb + kEncWaves : cb;
+      floatx4 acc0 = {0.0f, 0.0f, 0.0f, 0.0f};
+      floatx4 acc1 = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll 4
+      for (int k0 = 0; k0 < K; k0 += 4) {
+        const float av = A[r16 * lda + k0 + kq];
+        const float b0 = Wb[(k0 + kq) * ldw + cb * 16 + r16];
+        const float b1 = Wb[(k0 + kq) * ldw + cb1 * 16 + r16];
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b0, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b1, acc1, 0, 0, 0);
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[u], b[u], acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[u], b[u], acc1, 0, 0, 0);
+      for (int h = 0; h < 2; ++h) {
+        if (h == 1 && !two) break;
+        const int col = c.n0 + (h == 0 ? cb : cb1) * 16 + r16;
+        const float bc = bias[col];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int r = 4 * kq + i;
+          float y = (h == 0 ? acc0[i] : acc1[i]) + bc;
+          if (relu) y = fmaxf(y, 0.0f);
+          if (accumulate) y = Y[r * ldy + col] + y;
+          Y[r * ldy + col] = y;
+        }
       }
     }
-    const float bc = bias[col];
+    c = nx;
+  }
+  __syncthreads();
+}
+
+// Z[r] = LN(X[r]) * g + b for `rows` rows (X row r at X + r * ldx), H a
+// multiple of 16 up to 128: a row per 16-lane group (lane j of the group
+// holds elements j, j + 16, ...), the four groups of a wavefront on four
+// rows at once, so the reductions' shuffles of four rows overlap.
+__device__ __forceinline__ void layer_norm_rows(const float* X, int ldx, float* Z, int ldz, const float* g,
+                                                const float* bt, int H, int rows) {
+  const int lane = threadIdx.x & 63;
+  const int grp = threadIdx.x >> 4;          // 16 groups in the workgroup
+  const int j = lane & 15;
+  const int nt = H >> 4;
+  for (int r = grp; r < rows; r += kEncThreads / 16) {
+    float v[8];
+    float sum = 0.0f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r0 = 4 * kq + i, r1 = 16 + 4 * kq + i;
-      float y0 = acc0[i] + bc, y1 = acc1[i] + bc;
-      if (relu) {
-        y0 = fmaxf(y0, 0.0f);
-        y1 = fmaxf(y1, 0.0f);
-      }
-      if (accumulate) {
-        y0 = Y[r0 * ldy + col] + y0;
-        y1 = Y[r1 * ldy + col] + y1;
-      }
-      Y[r0 * ldy + col] = y0;
-      Y[r1 * ldy + col] = y1;
+    for (int t = 0; t < 8; ++t) {
+      v[t] = t < nt ? X[r * ldx + j + 16 * t] : 0.0f;
+      sum += v[t];
     }
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1) sum += __shfl_xor(sum, o, 16);
+    const float mean = sum / static_cast<float>(H);
+    float sq = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      v[t] = t < nt ? v[t] - mean : 0.0f;
+      sq += v[t] * v[t];
+    }
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1) sq += __shfl_xor(sq, o, 16);
+    const float rstd = 1.0f / sqrtf(sq / static_cast<float>(H) + 1e-5f);
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+      if (t < nt) Z[r * ldz + j + 16 * t] = v[t] * rstd * g[j + 16 * t] + bt[j + 16 * t];
   }
 }
 
-// Z[r] = LN(X[r]) * g + b for `rows` rows (H <= 128: lane l holds elements
-// l and l + 64), one wavefront per row.
-__device__ void layer_norm_rows(const float* X, int ldx, float* Z, int ldz, const float* __restrict__ g,
-                                const float* __restrict__ bt, int H, int rows) {
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const bool h0 = lane < H, h1 = lane + 64 < H;
-  for (int r = wave; r < rows; r += kEncWaves) {
-    const float v0 = h0 ? X[r * ldx + lane] : 0.0f;
-    const float v1 = h1 ? X[r * ldx + lane + 64] : 0.0f;
-    const float mean = wave_sum(v0 + v1) / static_cast<float>(H);
-    const float d0 = h0 ? v0 - mean : 0.0f;
-    const float d1 = h1 ? v1 - mean : 0.0f;
-    const float var = wave_sum(d0 * d0 + d1 * d1) / static_cast<float>(H);
-    const float rstd = 1.0f / sqrtf(var + 1e-5f);
-    if (h0) Z[r * ldz + lane] = d0 * rstd * g[lane] + bt[lane];
-    if (h1) Z[r * ldz + lane + 64] = d1 * rstd * g[lane + 64] + bt[lane + 64];
-  }
+// One layer's parameters inside the packed array.
+struct LayerPtrs {
+  const float *ln1_g, *ln1_b, *Wqkv, *bqkv, *Wo, *bo, *ln2_g, *ln2_b, *W1, *b1, *W2, *b2;
+};
+
+__device__ __forceinline__ LayerPtrs layer_ptrs(const float* L, int H, int F) {
+  LayerPtrs p;
+  p.ln1_g = L;
+  p.ln1_b = p.ln1_g + H;
+  p.Wqkv = p.ln1_b + H;
+  p.bqkv = p.Wqkv + static_cast<size_t>(H) * 3 * H;
+  p.Wo = p.bqkv + 3 * H;
+  p.bo = p.Wo + static_cast<size_t>(H) * H;
+  p.ln2_g = p.bo + H;
+  p.ln2_b = p.ln2_g + H;
+  p.W1 = p.ln2_b + H;
+  p.b1 = p.W1 + static_cast<size_t>(H) * F;
+  p.W2 = p.b1 + F;
+  p.b2 = p.W2 + static_cast<size_t>(F) * H;
+  return p;
 }
 
 __global__ __launch_bounds__(kEncThreads) void encoder_kernel(const EncArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int H = a.H, F = a.F;
   const int ldh = H + kPad, ldq = 3 * H + kPad, ldf = F + kPad;
-  float* X = reinterpret_cast<float*>(smem);          // [32][ldh] token states
-  float* Z = X + kEncRows * ldh;                      // [32][ldh] normalized tokens / attention output
-  float* QKV = Z + kEncRows * ldh;                    // [32][ldq]
-  float* Hd = QKV + kEncRows * ldq;                   // [32][ldf] feed-forward hidden
-  DevPred* sp = reinterpret_cast<DevPred*>(Hd + kEncRows * ldf);   // [kEncQ]
-  float* fa = reinterpret_cast<float*>(sp + kEncQ);   // [32] normalized lower bound of the row's clause
-  float* fb = fa + kEncRows;                          // [32] normalized upper bound
-  int* kind = reinterpret_cast<int*>(fb + kEncRows);  // [32] 0 padding, 1 summary, 2 clause
-  int* col = kind + kEncRows;                         // [32] clause column
+  float* X = reinterpret_cast<float*>(smem);          // [16][ldh] token states
+  float* Z = X + kEncRows * ldh;                      // [16][ldh] normalized tokens / attention output
+  float* QKV = Z + kEncRows * ldh;                    // [16][ldq]
+  float* Hd = QKV + kEncRows * ldq;                   // [16][ldf] feed-forward hidden
+  float* Wb = Hd + kEncRows * ldf;                    // [kWbuf + 4] weight staging (+ a 16-byte sink)
+  float* Sc = Wb + kWbuf + 4;                         // [kEncQ][heads][8][8] attention scores
+  float* sv = Sc + kEncQ * kEncMaxHeads * kEncSlots * kEncSlots;   // [kEncVec] the layer's gains and biases
+  DevPred* sp = reinterpret_cast<DevPred*>(sv + kEncVec);   // [kEncQ]
+  float* fa = reinterpret_cast<float*>(sp + kEncQ);   // [16] normalized lower bound of the row's clause
+  float* fb = fa + kEncRows;                          // [16] normalized upper bound
+  int* kind = reinterpret_cast<int*>(fb + kEncRows);  // [16] 0 padding, 1 summary, 2 clause
+  int* col = kind + kEncRows;                         // [16] clause column
   int* seq = col + kEncRows;                          // [kEncQ] tokens of each predicate
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int q0 = blockIdx.x * kEncQ;
+  const float* col_embed = a.p;
+  const float* feat_w = col_embed + static_cast<size_t>(a.n_attr) * H;
+  const float* feat_b = feat_w + 2 * H;
+  const float* cls = feat_b + H;
+  const float* layer0 = cls + H;
+  const size_t layer_floats = static_cast<size_t>(2 * H) + 3 * H * H + 3 * H + H * H + H + 2 * H + H * F + F +
+                              F * H + H;
+  // The first projection's weights are on their way while the predicates
+  // come from host memory.
+  Prefetch pf;
+  prefetch(first_chunk(layer_ptrs(layer0, H, F).Wqkv, H, 3 * H), pf);
   if (wave < kEncQ && q0 + wave < a.nq) copy_pred(a.preds + q0 + wave, sp + wave, lane);
   __syncthreads();
 
@@ -167,11 +292,6 @@ __global__ __launch_bounds__(kEncThreads) void encoder_kernel(const EncArgs a) {
     if (i == 0) seq[qi] = q0 + qi < a.nq ? 1 + sp[qi].n_raw : 0;
   }
   __syncthreads();
-  const float* P = a.p;
-  const float* col_embed = P;
-  const float* feat_w = col_embed + static_cast<size_t>(a.n_attr) * H;
-  const float* feat_b = feat_w + 2 * H;
-  const float* cls = feat_b + H;
   for (int e = threadIdx.x; e < kEncRows * H; e += kEncThreads) {
     const int r = e / H, h = e % H;
     float v = 0.0f;
@@ -186,74 +306,91 @@ __global__ __launch_bounds__(kEncThreads) void encoder_kernel(const EncArgs a) {
   }
   __syncthreads();
 
-  const float* L = cls + H;
   const int dh = H / a.heads;
   const float inv_sqrt_dh = 1.0f / sqrtf(static_cast<float>(dh));
   for (int layer = 0; layer < a.layers; ++layer) {
-    const float* ln1_g = L;
-    const float* ln1_b = ln1_g + H;
-    const float* Wqkv = ln1_b + H;
-    const float* bqkv = Wqkv + static_cast<size_t>(H) * 3 * H;
-    const float* Wo = bqkv + 3 * H;
-    const float* bo = Wo + static_cast<size_t>(H) * H;
-    const float* ln2_g = bo + H;
-    const float* ln2_b = ln2_g + H;
-    const float* W1 = ln2_b + H;
-    const float* b1 = W1 + static_cast<size_t>(H) * F;
-    const float* W2 = b1 + F;
-    const float* b2 = W2 + static_cast<size_t>(F) * H;
-    L = b2 + H;
+    const LayerPtrs w = layer_ptrs(layer0 + layer * layer_floats, H, F);
+    const Chunk none{nullptr, 1, 1, 0, 16};
+    const Chunk after_ffn =
+        layer + 1 < a.layers ? first_chunk(layer_ptrs(layer0 + (layer + 1) * layer_floats, H, F).Wqkv, H, 3 * H)
+                             : none;
 
-    layer_norm_rows(X, ldh, Z, ldh, ln1_g, ln1_b, H, kEncRows);
-    __syncthreads();
-    gemm_rows(Z, ldh, H, Wqkv, bqkv, 3 * H, QKV, ldq, false, false);
-    __syncthreads();
-    // Attention of token i of predicate qi in head hd over the predicate's
-    // tokens; the output (head slices side by side) goes to Z.  Padding rows
-    // get zeros.
-    for (int t = threadIdx.x; t < kEncQ * a.heads * kEncSlots; t += kEncThreads) {
-      const int qi = t / (a.heads * kEncSlots);
-      const int hd = (t / kEncSlots) % a.heads;
-      const int i = t % kEncSlots;
+    // The layer's gains and biases into LDS, one round of loads: sv holds
+    // ln1_g, ln1_b | bqkv | bo, ln2_g, ln2_b | b1 | b2.
+    {
+      const int n = 9 * H + F;
+      float v[6];
+#pragma unroll
+      for (int u = 0; u < 6; ++u) {
+        const int i = static_cast<int>(threadIdx.x) + u * kEncThreads;
+        const float* src = i < 2 * H ? w.ln1_g + i
+                           : i < 5 * H ? w.bqkv + (i - 2 * H)
+                           : i < 8 * H ? w.bo + (i - 5 * H)
+                           : i < 8 * H + F ? w.b1 + (i - 8 * H)
+                                           : w.b2 + (i - 8 * H - F);
+        v[u] = i < n ? *src : 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < 6; ++u) {
+        const int i = static_cast<int>(threadIdx.x) + u * kEncThreads;
+        if (i < n) sv[i] = v[u];
+      }
+      __syncthreads();
+    }
+    const float* s_ln1_g = sv;
+    const float* s_ln1_b = sv + H;
+    const float* s_bqkv = sv + 2 * H;
+    const float* s_bo = sv + 5 * H;
+    const float* s_ln2_g = sv + 6 * H;
+    const float* s_ln2_b = sv + 7 * H;
+    const float* s_b1 = sv + 8 * H;
+    const float* s_b2 = sv + 8 * H + F;
+    layer_norm_rows(X, ldh, Z, ldh, s_ln1_g, s_ln1_b, H, kEncRows);
+    gemm_rows(Z, ldh, first_chunk(w.Wqkv, H, 3 * H), s_bqkv, QKV, ldq, false, false, Wb, pf,
+              first_chunk(w.Wo, H, H));
+    // Attention, in two passes over all threads.  Scores: one item per
+    // (predicate, head, query token i, key token j) of the predicate's
+    // tokens, into Sc.  Outputs: one item per (predicate, head, token i,
+    // dimension d) -- the softmax over the keys of row i, then the weighted
+    // sum of V -- into Z (head slices side by side); padding rows get zeros.
+    for (int t = threadIdx.x; t < kEncQ * a.heads * kEncSlots * kEncSlots; t += kEncThreads) {
+      const int j = t % kEncSlots, i = (t / kEncSlots) % kEncSlots;
+      const int hd = (t / (kEncSlots * kEncSlots)) % a.heads, qi = t / (kEncSlots * kEncSlots * a.heads);
       const int S = seq[qi];
-      const int ri = qi * kEncSlots + i;
-      float* o = Z + ri * ldh + hd * dh;
-      if (i >= S) {
-        for (int d = 0; d < dh; ++d) o[d] = 0.0f;
-        continue;
-      }
-      const float* qv = QKV + ri * ldq + hd * dh;
-      float s[kEncSlots];
-      float mx = -INFINITY;
-      for (int j = 0; j < S; ++j) {
-        const float* kv = QKV + (qi * kEncSlots + j) * ldq + H + hd * dh;
-        float acc = 0.0f;
-        for (int d = 0; d < dh; ++d) acc += qv[d] * kv[d];
-        s[j] = acc * inv_sqrt_dh;
-        mx = fmaxf(mx, s[j]);
-      }
-      float sum = 0.0f;
-      for (int j = 0; j < S; ++j) {
-        s[j] = expf(s[j] - mx);
-        sum += s[j];
-      }
-      const float inv = 1.0f / sum;
-      for (int d = 0; d < dh; ++d) {
-        float acc = 0.0f;
-        for (int j = 0; j < S; ++j) acc += s[j] * QKV[(qi * kEncSlots + j) * ldq + 2 * H + hd * dh + d];
-        o[d] = acc * inv;
-      }
+      if (i >= S || j >= S) continue;
+      const float* qv = QKV + (qi * kEncSlots + i) * ldq + hd * dh;
+      const float* kv = QKV + (qi * kEncSlots + j) * ldq + H + hd * dh;
+      float acc = 0.0f;
+#pragma unroll 4
+      for (int d = 0; d < dh; ++d) acc += qv[d] * kv[d];
+      Sc[t] = acc * inv_sqrt_dh;
     }
     __syncthreads();
-    gemm_rows(Z, ldh, H, Wo, bo, H, X, ldh, true, false);
-    __syncthreads();
-    layer_norm_rows(X, ldh, Z, ldh, ln2_g, ln2_b, H, kEncRows);
-    __syncthreads();
-    gemm_rows(Z, ldh, H, W1, b1, F, Hd, ldf, false, true);
-    __syncthreads();
-    gemm_rows(Hd, ldf, F, W2, b2, H, X, ldh, true, false);
-    __syncthreads();
+    for (int t = threadIdx.x; t < kEncRows * H; t += kEncThreads) {
+      const int d = t % dh, hd = (t / dh) % a.heads, r = t / H;   // r = qi * kEncSlots + i
+      const int qi = r / kEncSlots, i = r % kEncSlots;
+      const int S = seq[qi];
+      float out = 0.0f;
+      if (i < S) {
+        const float* sc = Sc + ((qi * a.heads + hd) * kEncSlots + i) * kEncSlots;
+        float mx = -INFINITY;
+        for (int j = 0; j < S; ++j) mx = fmaxf(mx, sc[j]);
+        float sum = 0.0f, acc = 0.0f;
+        for (int j = 0; j < S; ++j) {
+          const float e = expf(sc[j] - mx);
+          sum += e;
+          acc += e * QKV[(qi * kEncSlots + j) * ldq + 2 * H + hd * dh + d];
+        }
+        out = acc / sum;
+      }
+      Z[r * ldh + hd * dh + d] = out;
+    }
+    gemm_rows(Z, ldh, first_chunk(w.Wo, H, H), s_bo, X, ldh, true, false, Wb, pf, first_chunk(w.W1, H, F));
+    layer_norm_rows(X, ldh, Z, ldh, s_ln2_g, s_ln2_b, H, kEncRows);
+    gemm_rows(Z, ldh, first_chunk(w.W1, H, F), s_b1, Hd, ldf, false, true, Wb, pf, first_chunk(w.W2, F, H));
+    gemm_rows(Hd, ldf, first_chunk(w.W2, F, H), s_b2, X, ldh, true, false, Wb, pf, after_ffn);
   }
+  const float* L = layer0 + a.layers * layer_floats;
 
   // w_z = LN_f(summary token) W_out + b_out, the kEncQ predicates side by
   // side so every W_out row is read once per workgroup.
@@ -263,11 +400,14 @@ __global__ __launch_bounds__(kEncThreads) void encoder_kernel(const EncArgs a) {
   const float* out_b = out_w + static_cast<size_t>(H) * a.D;
   // (row r of the normalization is predicate r's summary token: input row
   // stride kEncSlots rows)
-  layer_norm_rows(X, kEncSlots * ldh, Z, ldh, lnf_g, lnf_b, H, kEncQ);
+  for (int i = threadIdx.x; i < 2 * H; i += kEncThreads) sv[i] = lnf_g[i];   // lnf_g, lnf_b are adjacent
+  __syncthreads();
+  layer_norm_rows(X, kEncSlots * ldh, Z, ldh, sv, sv + H, H, kEncQ);
   __syncthreads();
   const int nv = min(kEncQ, a.nq - q0);
   for (int d = threadIdx.x; d < a.D; d += kEncThreads) {
-    float acc[kEncQ] = {0.0f, 0.0f, 0.0f, 0.0f};
+    float acc[kEncQ] = {};
+#pragma unroll 16
     for (int h = 0; h < H; ++h) {
       const float w = out_w[static_cast<size_t>(h) * a.D + d];
 #pragma unroll
@@ -280,7 +420,8 @@ __global__ __launch_bounds__(kEncThreads) void encoder_kernel(const EncArgs a) {
 }  // namespace
 
 size_t encoder_lds_bytes(int H, int F) {
-  const size_t floats = static_cast<size_t>(kEncRows) * (2 * (H + kPad) + (3 * H + kPad) + (F + kPad));
+  const size_t floats = static_cast<size_t>(kEncRows) * (2 * (H + kPad) + (3 * H + kPad) + (F + kPad)) + kWbuf + 4 +
+                        kEncQ * kEncMaxHeads * kEncSlots * kEncSlots + kEncVec;
   return floats * sizeof(float) + kEncQ * sizeof(DevPred) + kEncRows * 2 * sizeof(float) +
          (2 * kEncRows + kEncQ) * sizeof(int);
 }

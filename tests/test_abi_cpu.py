@@ -88,5 +88,5 @@ def test_encoder_parameter_count_matches_the_documented_layout():
         per_layer = 2 * H + 3 * H * H + 3 * H + H * H + H + 2 * H + H * F + F + F * H + H
         assert fn(H, heads, L, F, A, D) == A * H + 2 * H + 2 * H + L * per_layer + 2 * H + H * D + D
     for bad in [(8, 1, 1, 16, 1, 4), (48 + 1, 1, 1, 16, 1, 4), (64, 3, 1, 16, 1, 4), (64, 4, 0, 16, 1, 4),
-                (64, 4, 9, 16, 1, 4), (64, 4, 1, 272, 1, 4), (144, 4, 1, 16, 1, 4), (64, 4, 1, 16, 0, 4)]:
+                (64, 4, 9, 16, 1, 4), (64, 32, 1, 16, 1, 4), (64, 4, 1, 272, 1, 4), (144, 4, 1, 16, 1, 4), (64, 4, 1, 16, 0, 4)]:
         assert fn(*bad) == -1, bad

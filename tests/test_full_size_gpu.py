@@ -103,7 +103,7 @@ def _run_config(B, w, idx, plain, bins, nq, k, per_bin, conditioned=True, lut_dt
     say(f"[full] {w.name}: {len(tasks)} queries to the oracle on {_workers()} host processes")
     with OraclePool(ox, _workers()) as pool:
         results = pool.search(tasks, progress)
-    for key, ids_o, dist_o, _ in results:
+    for key, ids_o, dist_o, *_ in results:
         g_ids, g_d = got[key]
         check_search_row(g_ids, g_d, ids_o, dist_o, f"{w.name} s={key[0]} q{key[1]} ({lut_dtype})")
     return len(results)

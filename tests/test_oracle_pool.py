@@ -28,7 +28,8 @@ def test_pool_matches_single_calls():
     with OraclePool(ox, 3) as pool:
         got = pool.search(tasks)
     assert [g[0] for g in got] == [t[0] for t in tasks]
-    for (key, q, cl, k, wz, lt, cond), (key2, ids, dist, sec) in zip(tasks, got):
+    for (key, q, cl, k, wz, lt, cond), (key2, ids, dist, sec, enc_err) in zip(tasks, got):
+        assert enc_err is None
         ref = O.filtered_search(ox, q, cl, k, w_z=wz, lut_dtype=lt, conditioned=cond)
         assert np.array_equal(ids, ref["ids"]), key
         assert np.array_equal(dist.view(np.uint32), ref["dist"].view(np.uint32)), key
@@ -48,3 +49,24 @@ def test_pool_reports_a_dead_worker():
 def test_host_description():
     assert host_cores() >= 1
     assert isinstance(cpu_model(), str) and cpu_model()
+
+
+def test_pool_encodes_when_asked():
+    from oracle.ifvs_encoder_oracle import encode_predicate
+    from workload import random_encoder
+    rng = np.random.default_rng(8)
+    ox = _index(rng)
+    enc = random_encoder(2, 64, [1000, 1000], seed=4, hidden=32, heads=2, layers=1, ffn=32)
+    enc_np = {k: (v.numpy() if hasattr(v, "numpy") else v) for k, v in enc.items() if k != "layers"}
+    enc_np["layers"] = [{k: v.numpy() for k, v in p.items()} for p in enc["layers"]]
+    preds = [[(0, 5, 300)], [], [(1, 0, 10), (0, 7, 700)]]
+    wz = [encode_predicate(p, enc_np).astype(np.float32) for p in preds]
+    wz[2] = wz[2] * np.float32(1.001)                          # one w_z 0.1% off
+    tasks = [(i, rng.standard_normal(64).astype(np.float32), p, 5, wz[i], "f32", True, True)
+             for i, p in enumerate(preds)]
+    with OraclePool(ox, 2, encoder=enc) as pool:
+        got = pool.search(tasks)
+    assert got[0][4] < 1e-6 and got[1][4] < 1e-6
+    assert 5e-4 < got[2][4] < 2e-3
+    ref = O.filtered_search(ox, tasks[2][1], preds[2], 5, w_z=wz[2])
+    assert np.array_equal(got[2][1], ref["ids"])
