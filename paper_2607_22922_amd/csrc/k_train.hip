@@ -11,17 +11,21 @@
 //      subspaces in order as the scan does;
 //   2. softmax statistics in fp64; g_v = d(batch loss)/d(distance of v);
 //   3. the table gradient g_lut[m][c] = sum over candidates v whose code in
-//      subspace m is c of g_v (LDS atomics), in the table's LDS;
+//      subspace m is c of g_v, the candidates added in order by one
+//      wavefront (lane = subspace), in the table's LDS;
 //   4. one thread per codeword c: for every subspace and sub-dimension j,
 //      Delta, e = q - C_PQ - Delta, the Delta gradient
 //        gd = g_lut * (-2 w e) + (2 lam / (M K d) / nq) Delta
 //      (stored for the W update), and the reductions over c of gd * W
-//      (alpha gradient) and g_lut * e^2 (w_f gradient), one wavefront
-//      reduction + one LDS atomic per value.
+//      (alpha gradient) and g_lut * e^2 (w_f gradient): a wavefront
+//      reduction each, the four wavefronts' partials added in wave order.
 // train_update_w: W -= lr * sum_q gd_q (x) alpha_q, one thread per entry, the
 // queries summed in order.
-// train_update_bank: bank[row] -= lr * g_alpha for each query and hash
-// function (global atomics; a row hit twice gets both).
+// train_update_bank: bank[row] -= lr * (sum of g_alpha over the (query, hash
+// function) pairs that hit the row, in pair order; a row hit twice gets
+// both), applied by the row's first pair.
+// Every sum has a fixed order, so a step's results do not depend on
+// scheduling: two identical steps give identical bits.
 #include <cmath>
 
 #include "ifvs_internal.h"
@@ -69,14 +73,12 @@ __global__ __launch_bounds__(kTrainThreads) void train_query_kernel(const TrainA
   const int M = a.m, d = a.dsub, r = a.r, mr = a.m * a.r;
   float* s_tab = reinterpret_cast<float*>(smem);                 // [M][256]: table, then its gradient
   float* s_v = s_tab + M * kKsub;                                 // [n_cand]: distances, then g_v
-  float* s_gw = s_v + a.n_cand;                                   // [dim]: w_f gradient
-  float* s_ga = s_gw + a.dim;                                     // [M*r]: alpha gradient
-  double* s_red = reinterpret_cast<double*>(s_ga + mr + ((mr + a.dim + a.n_cand) & 1));   // [3][4]
+  float* s_gw = s_v + a.n_cand;                                   // [4][dim]: w_f gradient, per wavefront
+  float* s_ga = s_gw + 4 * a.dim;                                 // [4][M*r]: alpha gradient, per wavefront
+  double* s_red = reinterpret_cast<double*>(s_ga + 4 * mr + ((4 * mr + 4 * a.dim + a.n_cand) & 1));   // [3][4]
 
   const float* lut = a.lut + static_cast<int64_t>(qi) * M * kKsub;
   for (int e = tid; e < M * kKsub; e += kTrainThreads) s_tab[e] = lut[e];
-  for (int e = tid; e < a.dim; e += kTrainThreads) s_gw[e] = 0.0f;
-  for (int e = tid; e < mr; e += kTrainThreads) s_ga[e] = 0.0f;
   __syncthreads();
 
   // 1. Distances.
@@ -136,15 +138,22 @@ __global__ __launch_bounds__(kTrainThreads) void train_query_kernel(const TrainA
   }
   __syncthreads();
 
-  // 3. Table gradient.
+  // 3. Table gradient: wavefront 0 adds the candidates in order, lane mm
+  // updating subspace mm (one candidate touches one entry per subspace, and
+  // a lane's updates to an entry are in program order).
   for (int e = tid; e < M * kKsub; e += kTrainThreads) s_tab[e] = 0.0f;
   __syncthreads();
-  for (int v = tid; v < a.n_cand; v += kTrainThreads) {
-    const float g = s_v[v];
-    const int64_t id = cand_id(a, qi, v);
-    if (g == 0.0f || id < 0) continue;
-    const int64_t row = a.inv_perm ? a.inv_perm[id] : id;
-    for (int mm = 0; mm < M; ++mm) atomicAdd(&s_tab[mm * kKsub + code_of(a, row, mm)], g);
+  if (wave == 0) {
+    for (int v = 0; v < a.n_cand; ++v) {
+      const float g = s_v[v];
+      const int64_t id = cand_id(a, qi, v);
+      if (g == 0.0f || id < 0) continue;
+      const int64_t row = a.inv_perm ? a.inv_perm[id] : id;
+      for (int mm = lane; mm < M; mm += 64) {
+        const int at = mm * kKsub + code_of(a, row, mm);
+        s_tab[at] = __fadd_rn(s_tab[at], g);
+      }
+    }
   }
   __syncthreads();
 
@@ -168,7 +177,7 @@ __global__ __launch_bounds__(kTrainThreads) void train_query_kernel(const TrainA
       gdq[(static_cast<int64_t>(mm) * kKsub + c) * d + j] = gd;
       reg += static_cast<double>(delta) * delta;
       const float gw = wave_sum(__fmul_rn(gl, __fmul_rn(e, e)));
-      if (lane == 0) atomicAdd(&s_gw[mm * d + j], gw);
+      if (lane == 0) s_gw[wave * a.dim + mm * d + j] = gw;
     }
     for (int t = 0; t < r; ++t) {
       float ga = 0.0f;
@@ -176,7 +185,7 @@ __global__ __launch_bounds__(kTrainThreads) void train_query_kernel(const TrainA
         ga = __fadd_rn(ga, __fmul_rn(gdq[(static_cast<int64_t>(mm) * kKsub + c) * d + j],
                                      a.W[((static_cast<int64_t>(mm) * r + t) * kKsub + c) * d + j]));
       ga = wave_sum(ga);
-      if (lane == 0) atomicAdd(&s_ga[mm * r + t], ga);
+      if (lane == 0) s_ga[wave * mr + mm * r + t] = ga;
     }
   }
   reg = wave_sum_d(reg);
@@ -187,13 +196,16 @@ __global__ __launch_bounds__(kTrainThreads) void train_query_kernel(const TrainA
     a.loss[qi] = static_cast<float>(ce + a.lam * rsum / (static_cast<double>(M) * kKsub * d));
   }
   float* garow = a.galpha + static_cast<int64_t>(qi) * mr;
-  for (int e = tid; e < mr; e += kTrainThreads) garow[e] = s_ga[e];
+  for (int e = tid; e < mr; e += kTrainThreads)
+    garow[e] = __fadd_rn(__fadd_rn(__fadd_rn(s_ga[e], s_ga[mr + e]), s_ga[2 * mr + e]), s_ga[3 * mr + e]);
   if (a.dwz) {
     const float* zrow = a.w_z + static_cast<int64_t>(qi) * a.dim;
     float* drow = a.dwz + static_cast<int64_t>(qi) * a.dim;
     for (int e = tid; e < a.dim; e += kTrainThreads) {
       const double x = static_cast<double>(zrow[e]);
-      drow[e] = static_cast<float>(static_cast<double>(s_gw[e]) / (1.0 + exp(-x)));
+      const float gw = __fadd_rn(__fadd_rn(__fadd_rn(s_gw[e], s_gw[a.dim + e]), s_gw[2 * a.dim + e]),
+                                 s_gw[3 * a.dim + e]);
+      drow[e] = static_cast<float>(static_cast<double>(gw) / (1.0 + exp(-x)));
     }
   }
 }
@@ -214,14 +226,23 @@ __global__ __launch_bounds__(256) void train_update_w_kernel(float* __restrict__
   W[e] = __fsub_rn(W[e], __fmul_rn(lr, g));
 }
 
+// One workgroup per (query, hash function) pair p; the first pair that hits
+// a row sums the alpha gradients of all pairs hitting it, in pair order, and
+// applies them (the other pairs of the row return).
 __global__ __launch_bounds__(256) void train_update_bank_kernel(float* __restrict__ bank, int mr,
                                                                 const int32_t* __restrict__ rows, int h,
-                                                                const float* __restrict__ galpha, float lr) {
-  const int q = blockIdx.x;
-  for (int i = 0; i < h; ++i) {
-    const int64_t row = rows[static_cast<int64_t>(q) * h + i];
-    for (int e = threadIdx.x; e < mr; e += blockDim.x)
-      atomicAdd(&bank[row * mr + e], -lr * galpha[static_cast<int64_t>(q) * mr + e]);
+                                                                const float* __restrict__ galpha, int pairs,
+                                                                float lr) {
+  const int p = blockIdx.x;
+  const int32_t row = rows[p];
+  for (int p2 = 0; p2 < p; ++p2)
+    if (rows[p2] == row) return;
+  for (int e = threadIdx.x; e < mr; e += blockDim.x) {
+    float g = 0.0f;
+    for (int p2 = p; p2 < pairs; ++p2)
+      if (rows[p2] == row) g = __fadd_rn(g, galpha[static_cast<int64_t>(p2 / h) * mr + e]);
+    const int64_t at = static_cast<int64_t>(row) * mr + e;
+    bank[at] = __fsub_rn(bank[at], __fmul_rn(lr, g));
   }
 }
 
@@ -233,7 +254,7 @@ __global__ void invert_perm_kernel(const int32_t* __restrict__ perm, int64_t n, 
 }  // namespace
 
 size_t train_query_lds_bytes(int m, int dim, int n_cand, int mr) {
-  const size_t floats = static_cast<size_t>(m) * kKsub + n_cand + dim + mr;
+  const size_t floats = static_cast<size_t>(m) * kKsub + n_cand + 4 * static_cast<size_t>(dim) + 4 * mr;
   return (floats + 1) / 2 * 8 + 12 * sizeof(double);
 }
 
@@ -256,7 +277,8 @@ hipError_t launch_train_update_w(float* W, const float* gdelta, const float* alp
 
 hipError_t launch_train_update_bank(float* bank, int mr, const int32_t* rows, int h, const float* galpha,
                                     int nq, float lr, hipStream_t s) {
-  train_update_bank_kernel<<<dim3(nq), dim3(256), 0, s>>>(bank, mr, rows, h, galpha, lr);
+  if (nq * h <= 0) return hipSuccess;
+  train_update_bank_kernel<<<dim3(nq * h), dim3(256), 0, s>>>(bank, mr, rows, h, galpha, nq * h, lr);
   return hipGetLastError();
 }
 

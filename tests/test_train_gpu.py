@@ -1,7 +1,7 @@
 """One training step of the conditioning on the GPU (ifvs_train_step)
 against the fp64 training oracle: per-query losses, the applied bank and W
-updates (lr = 1, so the change is the gradient), and dL/dw_z, within fp32
-tolerances, on plain and clustered layouts, with absent candidates,
+updates (the change divided by the learning rate is the gradient), and
+dL/dw_z, element by element within fp32 tolerances, on plain and clustered layouts, with absent candidates,
 duplicate hashed rows and queries without positives; then that the trained
 parameters are what the search uses."""
 import numpy as np
@@ -15,6 +15,11 @@ from tests._gpu_util import check_search_row, say
 
 pytestmark = pytest.mark.gpu
 
+# Learning rate of the parity steps: a power of two, so lr * g is exact, and
+# large enough that the read-back difference (old - new parameter) carries
+# the gradient's own fp32 precision rather than the parameters' last bits.
+LR = 1024.0
+
 
 @pytest.fixture(scope="module")
 def B():
@@ -27,9 +32,22 @@ def _np(t):
 
 
 def _close(got, want, what, rel=2e-4):
+    """Element by element: |gpu - oracle| <= rtol |oracle| + atol with
+    rtol = rel / 2 and atol = rel / 4 x the array's largest magnitude, and
+    the largest error within rel x that magnitude.  The floor covers fp32
+    cancellation: each entry sums up to a few thousand fp32 terms of both
+    signs (softmax weights of positives and negatives, Delta gradients over
+    queries), whose rounding errors reach n 2^-24 ~ 1e-4 of the terms'
+    magnitudes -- the same order as the largest entries (observed: at most
+    4e-5 of the largest magnitude, on entries that cancel to near zero)."""
     scale = max(float(np.abs(want).max()), 1e-30)
-    err = float(np.abs(got - want).max())
-    assert err <= rel * scale, f"{what}: max |gpu - oracle| = {err:.3e}, scale {scale:.3e}"
+    err = np.abs(got.astype(np.float64) - want)
+    bound = 0.5 * rel * np.abs(want) + 0.25 * rel * scale
+    bad = err > bound
+    assert not bad.any(), (f"{what}: {int(bad.sum())} of {bad.size} entries off; worst excess at "
+                           f"{int(np.argmax(err - bound))}: err {float(err.ravel()[np.argmax(err - bound)]):.3e}, "
+                           f"want {float(np.ravel(want)[np.argmax(err - bound)]):.3e}, scale {scale:.3e}")
+    assert float(err.max()) <= rel * scale, f"{what}: max |gpu - oracle| = {float(err.max()):.3e}, scale {scale:.3e}"
 
 
 def _problem(B, seed, M, dsub, cluster_cols, nq=12, n_cand=24, n_pos=4, bank_rows=32, with_wz=True, scale=20.0):
@@ -66,12 +84,12 @@ def test_train_step_matches_oracle(B, cluster_cols, M, dsub):
     tau, lam = 0.8, 0.05
     ref = _oracle(ix, q, w_z, cand, preds, n_pos, tau, lam)
     bank0, W0 = idx.read_params()
-    loss, dwz = idx.train_step(q, preds, w_z, cand, n_pos, tau, lam, 1.0, want_dwz=True)
+    loss, dwz = idx.train_step(q, preds, w_z, cand, n_pos, tau, lam, LR, want_dwz=True)
     bank1, W1 = idx.read_params()
     torch.cuda.synchronize()
     _close(_np(loss), ref["loss"], "loss", rel=1e-4)
-    _close(_np(bank0 - bank1), ref["bank"], "bank gradient")
-    _close(_np(W0 - W1), ref["W"], "W gradient")
+    _close(_np((bank0 - bank1) / LR), ref["bank"], "bank gradient")
+    _close(_np((W0 - W1) / LR), ref["W"], "W gradient")
     _close(_np(dwz), ref["w_z"], "w_z gradient")
     assert float(loss[2]) > 0 and abs(float(loss[2]) - ref["loss"][2]) <= 1e-4 * ref["loss"][2]
 
@@ -83,12 +101,12 @@ def test_train_step_without_w_z_and_duplicate_rows(B):
     tau, lam = 0.5, 0.2
     ref = _oracle(ix, q, None, cand, preds, n_pos, tau, lam)
     bank0, W0 = idx.read_params()
-    loss, _ = idx.train_step(q, preds, None, cand, n_pos, tau, lam, 1.0)
+    loss, _ = idx.train_step(q, preds, None, cand, n_pos, tau, lam, LR)
     bank1, W1 = idx.read_params()
     torch.cuda.synchronize()
     _close(_np(loss), ref["loss"], "loss", rel=1e-4)
-    _close(_np(bank0 - bank1), ref["bank"], "bank gradient")
-    _close(_np(W0 - W1), ref["W"], "W gradient")
+    _close(_np((bank0 - bank1) / LR), ref["bank"], "bank gradient")
+    _close(_np((W0 - W1) / LR), ref["W"], "W gradient")
 
 
 def test_trained_parameters_drive_the_search(B):
@@ -153,3 +171,18 @@ def test_training_loop_runs_and_fits_its_queries(B):
     losses = out["loss_per_epoch"]
     assert all(np.isfinite(losses)) and losses[-1] < losses[0], losses
     assert out["recall@10_conditioned_after"]["train"] >= out["recall@10_conditioned_before"]["train"]
+
+
+def test_train_step_is_deterministic(B):
+    """Two identical steps from identical states give identical bits (every
+    sum of the step has a fixed order): bank, W, losses and dL/dw_z, with
+    rows shared by several queries (a 3-row bank)."""
+    outs = []
+    for _ in range(2):
+        idx, ix, q, w_z, cand, preds, n_pos = _problem(B, 33, 16, 4, (0,), bank_rows=3)
+        loss, dwz = idx.train_step(q, preds, w_z, cand, n_pos, 0.8, 0.05, 1.0, want_dwz=True)
+        bank, W = idx.read_params()
+        torch.cuda.synchronize()
+        outs.append([_np(t).copy() for t in (loss, dwz, bank, W)])
+    for a, b, name in zip(outs[0], outs[1], ("loss", "dL/dw_z", "bank", "W")):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), name
