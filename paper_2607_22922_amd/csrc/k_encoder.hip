@@ -144,13 +144,25 @@ __device__ __forceinline__ void gemm_rows(const float* A, int lda, const Chunk& 
       const int cb1 = two ? cb + kEncWaves : cb;
       floatx4 acc0 = {0.0f, 0.0f, 0.0f, 0.0f};
       floatx4 acc1 = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll 4
-      for (int k0 = 0; k0 < K; k0 += 4) {
-        const float av = A[r16 * lda + k0 + kq];
-        const float b0 = Wb[(k0 + kq) * ldw + cb * 16 + r16];
-        const float b1 = Wb[(k0 + kq) * ldw + cb1 * 16 + r16];
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b0, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b1, acc1, 0, 0, 0);
+      // 64 of K at a time: all operands of 16 steps are read from LDS
+      // first (one wait), then the 32 matrix instructions run back to back;
+      // steps past K read row 0 and multiply by a zero A operand.
+      for (int kb = 0; kb < K; kb += 64) {
+        float av[16], b0[16], b1[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const int k = kb + 4 * u + kq;
+          const bool in = k < K;
+          const int kk = in ? k : 0;
+          av[u] = in ? A[r16 * lda + kk] : 0.0f;
+          b0[u] = Wb[kk * ldw + cb * 16 + r16];
+          b1[u] = Wb[kk * ldw + cb1 * 16 + r16];
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], b0[u], acc0, 0, 0, 0);
+          acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], b1[u], acc1, 0, 0, 0);
+        }
       }
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
