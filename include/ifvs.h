@@ -238,6 +238,79 @@ ifvs_status ifvs_filtered_search_noalloc(ifvs_index* idx, int32_t nq, const ifvs
                                          int32_t* ids_out, float* dist_out, uint32_t* bitmap_out,
                                          void* stream);
 
+/* ---- Coarse bound: exact pruning of the Rank stage ---------------------
+ * The Rank stage (Section 2, stage 2) sums M table entries per candidate.  A
+ * coarse quantizer of the index's reconstructions gives, per query, a lower
+ * bound on every candidate's distance from one table lookup, so candidates
+ * that cannot enter the top k are dropped before their sums.  With C_c the
+ * candidate's coarse centroid (itself a vector of PQ codes) and the
+ * triangle inequality in the weighted norm of w_f:
+ *   sqrt(dist(v)) >= sqrt(dist(C_c)) - sqrt(max_j w_f[j]) * (r_v + delta)
+ * where r_v = ||C_PQ(v) - C_PQ(C_c)|| (stored per row at build) and delta =
+ * sqrt(sum over m of (2 max_c ||Delta[m][c]||)^2) bounds what the
+ * conditioning Delta = alpha . W (Section 2, first display) adds between two
+ * code vectors.  Every term carries a rounding allowance, so a dropped
+ * candidate's computed distance exceeds the query's k-th: results are
+ * identical, bit for bit, to ifvs_filtered_search. */
+
+/* ifvs_build_coarse -- k-means over the reconstructions of evenly spaced
+ * rows (max(64 n_centroids, 65536) of them, at most n), starting from
+ * n_centroids evenly spaced rows and running `iters` iterations (sums in a
+ * fixed order: the build is deterministic); the centroids are then encoded
+ * with C_PQ and every row gets its nearest encoded centroid and its
+ * distance to it, rounded up to a bfloat16.  Synchronous; replaces any
+ * earlier coarse quantizer.  Costs n * 4 bytes, n_centroids * ceil(m/4) * 4
+ * and max_batch * (n_centroids + 8) * 4 bytes of device memory.
+ * Errors: IFVS_E_INVALID (n_centroids outside 1..4096 or above n, iters
+ * outside 0..1000), IFVS_E_UNSUPPORTED (dim > 128), IFVS_E_STATE,
+ * IFVS_E_NOMEM, IFVS_E_HIP. */
+ifvs_status ifvs_build_coarse(ifvs_index* idx, int32_t n_centroids, int32_t iters);
+
+/* ifvs_lut_bounds -- the two per-query factors of the coarse bound, for
+ * tables built by ifvs_build_lut with the same alpha and wf (NULL and NULL
+ * for ifvs_build_sdc_lut's tables):
+ *   bounds_out[2i]     >= sqrt(max_j wf_i[j]) (1 when wf is NULL; NaN, which
+ *                         disables the bound for that query, when a weight
+ *                         is negative or not finite)
+ *   bounds_out[2i + 1] >= delta_i, the conditioned codewords recomputed with
+ *                         the table build's own operations (0 when alpha is
+ *                         NULL)
+ *  alpha: device [nq][m*r] or NULL;  wf: device [nq][dim] or NULL
+ *  bounds_out: device [nq][2] fp32, caller-owned
+ * Enqueued on `stream`.  Errors: IFVS_E_INVALID (nq, NULL bounds_out, alpha
+ * given with no bank), IFVS_E_STATE, IFVS_E_HIP. */
+ifvs_status ifvs_lut_bounds(ifvs_index* idx, int32_t nq, const float* alpha, const float* wf, float* bounds_out,
+                            void* stream);
+
+/* ifvs_filtered_search_bounded -- ifvs_filtered_search with the coarse
+ * bound: lut_bounds (device [nq][2], from ifvs_lut_bounds for the same
+ * tables) lets the scan drop candidates by the bound above.  Same results as
+ * ifvs_filtered_search, bit for bit, whenever lut_bounds describes the
+ * tables; bounds computed for other tables can drop true neighbours.  The
+ * bound is used on one-query-per-tile scans of M = 16, 48 or 120 once
+ * ifvs_build_coarse has run (IFVS_OPT_COARSE: automatic on interval batches
+ * whose widest interval spans 1024 or more 64-row tiles); otherwise, or with
+ * lut_bounds NULL, the call is ifvs_filtered_search.  With the bound, the
+ * call adds one kernel that sums each query's table over the centroids'
+ * codes.  Errors: as ifvs_filtered_search. */
+ifvs_status ifvs_filtered_search_bounded(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
+                                         const void* lut, int32_t lut_dtype, const float* lut_bounds, int32_t k,
+                                         int32_t* ids_out, float* dist_out, uint32_t* bitmap_out, void* stream);
+
+/* ifvs_read_coarse -- the coarse quantizer, for inspection and tests
+ * (synchronous; every output may be NULL): *n_centroids_out; assign_out
+ * HOST [n] centroid of each vector id; radius_out HOST [n] its stored
+ * radius (an upper bound of ||C_PQ(v) - C_PQ(centroid)||); codes_out HOST
+ * [n_centroids][m] the centroids' PQ codes.
+ * Errors: IFVS_E_STATE (NULL handle or no coarse quantizer), IFVS_E_HIP. */
+ifvs_status ifvs_read_coarse(const ifvs_index* idx, int32_t* n_centroids_out, int32_t* assign_out,
+                             float* radius_out, uint8_t* codes_out);
+
+/* ifvs_last_coarse -- *used_out = 1 when the most recent filtered search on
+ * this index ran the scan with the coarse bound, else 0.
+ * Errors: IFVS_E_INVALID (NULL used_out), IFVS_E_STATE. */
+ifvs_status ifvs_last_coarse(const ifvs_index* idx, int32_t* used_out);
+
 /* ifvs_load_vectors -- attach the full-precision base vectors, for exact
  * filtered kNN (ifvs_exact_search).  The paper takes the exact top-k over
  * the predicate-passing vectors as its ground truth (Section 3.1), and its
@@ -438,9 +511,14 @@ ifvs_status ifvs_encode_predicates(ifvs_index* idx, int32_t nq, const ifvs_predi
 #define IFVS_OPT_EXACT_PLAN 10    /* ifvs_exact_search: 0 automatic (matrix-core screening when
                                      the batch's queries share rows), 1 score every selected row
                                      exactly, 2 always screen first                           */
+#define IFVS_OPT_COARSE 13       /* ifvs_filtered_search_bounded: 0 automatic (interval batches
+                                     whose widest interval spans 1024 or more 64-row tiles),
+                                     1 never, 2 whenever the plan has a coarse build (one query
+                                     per tile, M of 16, 48 or 120, LDS to spare)             */
 #define IFVS_OPT_COUNT_READS 12  /* measurement only: 1 = scans run a build of the scan kernel
                                      that also counts its table reads (one per subspace and
-                                     wavefront instruction) by the number of active lanes, read
+                                     wavefront instruction, and one per coarse-bound lookup)
+                                     by the number of active lanes, read
                                      back with ifvs_read_scan_reads; needs one query per tile
                                      and M of 16, 48 or 120 (else the search fails with
                                      IFVS_E_UNSUPPORTED).  Results are unchanged; the counting
@@ -452,9 +530,10 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value);
  * call waits for the recorded events, writes the summed kernel time (ms) and
  * the launch count of each stage, and clears the totals.  Stages, in array
  * order (IFVS_N_STAGES entries each): condition, distance table, filter,
- * scan, top-k merge, predicate encoder.  Errors: IFVS_E_INVALID (NULL
- * arrays), IFVS_E_STATE, IFVS_E_HIP. */
-#define IFVS_N_STAGES 6
+ * scan, top-k merge, predicate encoder, coarse bound (ifvs_lut_bounds and
+ * the centroid distances of a bounded search).  Errors: IFVS_E_INVALID
+ * (NULL arrays), IFVS_E_STATE, IFVS_E_HIP. */
+#define IFVS_N_STAGES 7
 ifvs_status ifvs_read_profile(ifvs_index* idx, double* ms_out, int64_t* launches_out);
 
 /* ifvs_read_scan_reads -- with IFVS_OPT_COUNT_READS on: hist_out[n] (65

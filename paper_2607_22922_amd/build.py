@@ -20,7 +20,8 @@ LIB = os.path.join(PKG, "libifvs.so")
 
 SOURCES = ["ifvs_host.hip", "k_cluster.hip", "k_filter.hip", "k_condition.hip", "k_lut.hip",
            "k_scan.hip", "k_gather.hip", "k_topk.hip", "k_exact.hip",
-           "k_sdc.hip", "k_train.hip", "k_probe.hip", "k_encoder.hip"]
+           "k_sdc.hip", "k_train.hip", "k_probe.hip", "k_encoder.hip", "k_coarse.hip",
+           "k_listscan.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -55,9 +55,14 @@ bool forced_alloc_failure() {
 }
 
 constexpr int kStagingSlots = 8;
+// Automatic coarse bound: interval batches whose widest interval spans at
+// least this many 64-row tiles.
+constexpr int64_t kCoarseAutoTiles = 1024;
+// Radius quantiles that split each coarse list into its kBands bands.
+constexpr float kBandQuantiles[kBands - 1] = {0.5f, 0.85f, 0.97f};
 
 // Optional per-stage kernel timing with HIP events (IFVS_OPT_PROFILE).
-enum Stage { kStCondition = 0, kStLut, kStFilter, kStScan, kStMerge, kStEncode, kStages };
+enum Stage { kStCondition = 0, kStLut, kStFilter, kStScan, kStMerge, kStEncode, kStCoarse, kStages };
 constexpr int kProfilePairs = 4096;
 
 struct StageTimer {
@@ -111,6 +116,43 @@ void* static_scratch_ptr(int device) {
   std::lock_guard<std::mutex> lock(g_scratch_mu);
   return device >= 0 && device < kMaxDevices ? g_scratch_dev[device] : nullptr;
 }
+
+// The coarse quantizer and the second copy of the codes in list order
+// (rows grouped by sub-list: centroid and radius band, each sub-list in
+// layout order), with the list plan's workspace.  Null words: none built.
+struct CoarseLists {
+  int C = 0;
+  int f_shift = 12;
+  uint32_t* words = nullptr;     // [n_tiles * 64] layout row: centroid id | radius (bfloat16, rounded up)
+  uint8_t* band = nullptr;       // [n] layout row: radius band within its list
+  uint32_t* cc_t = nullptr;      // [mw][C] centroid code words
+  int32_t* sub_off = nullptr;    // [C * kBands + 1] sub-list offsets in list order
+  float* rmax = nullptr;         // [C * kBands] largest radius of each sub-list
+  int32_t* cnt_f = nullptr;      // [(n >> f_shift) + 1][C * kBands]
+  uint32_t* codes_t = nullptr;   // [n_tiles][mw][64] list order
+  float* rad = nullptr;          // [n_tiles * 64] list order
+  int32_t* ids = nullptr;        // [n_tiles * 64] list position -> original id
+  int32_t* tmp_r0 = nullptr;     // [max_batch][C * kBands] list plan workspace
+  int32_t* tmp_r1 = nullptr;
+  int32_t* it_r0 = nullptr;      // [max_batch][C * kBands] list plan items
+  int32_t* it_r1 = nullptr;
+  int32_t* it_t = nullptr;
+  float* it_sdc = nullptr;
+  float* it_lb = nullptr;
+  float* hdr = nullptr;          // [max_batch][4]
+  uint32_t* slots = nullptr;     // [max_batch][kListSlots]
+
+  void release() {
+    for (void* p : {static_cast<void*>(words), static_cast<void*>(band), static_cast<void*>(cc_t),
+                    static_cast<void*>(sub_off), static_cast<void*>(rmax), static_cast<void*>(cnt_f),
+                    static_cast<void*>(codes_t), static_cast<void*>(rad), static_cast<void*>(ids),
+                    static_cast<void*>(tmp_r0), static_cast<void*>(tmp_r1), static_cast<void*>(it_r0),
+                    static_cast<void*>(it_r1), static_cast<void*>(it_t), static_cast<void*>(it_sdc),
+                    static_cast<void*>(it_lb), static_cast<void*>(hdr), static_cast<void*>(slots)})
+      if (p) (void)hipFree(p);
+    *this = CoarseLists{};
+  }
+};
 
 }  // namespace
 
@@ -219,8 +261,12 @@ struct ifvs_index {
   double* enc_off = nullptr;     // [n_attr]
   double* enc_scale = nullptr;   // [n_attr]
   int enc_H = 0, enc_heads = 0, enc_layers = 0, enc_F = 0;
+  // Coarse quantizer and the list order of the codes (ifvs_build_coarse).
+  CoarseLists coarse;
+  int opt_coarse = 0;                // 0 automatic, 1 never, 2 whenever the batch allows the list scan
   StageTimer* timers = nullptr;  // [kStages] once profiling was enabled
   ScanPlan last_plan{};
+  bool last_coarse = false;
 
   void free_vectors() {
     for (void* p : {static_cast<void*>(xt), static_cast<void*>(xr), static_cast<void*>(xb), static_cast<void*>(xn),
@@ -264,6 +310,7 @@ struct ifvs_index {
                     static_cast<void*>(enc_off), static_cast<void*>(enc_scale)})
       if (p) hipFree(p);
     free_vectors();
+    coarse.release();
     for (void* p : {static_cast<void*>(tr_alpha), static_cast<void*>(tr_wf), static_cast<void*>(tr_lut),
                     static_cast<void*>(tr_gdelta), static_cast<void*>(tr_galpha), static_cast<void*>(tr_rows),
                     static_cast<void*>(inv_perm)})
@@ -999,6 +1046,10 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
       if (value > 2) return fail(IFVS_E_INVALID, "IFVS_OPT_SHARED_BOUND takes 0, 1 or 2");
       idx->opt_shared_bound = static_cast<int>(value);
       return IFVS_OK;
+    case IFVS_OPT_COARSE:
+      if (value > 2) return fail(IFVS_E_INVALID, "IFVS_OPT_COARSE takes 0, 1 or 2");
+      idx->opt_coarse = static_cast<int>(value);
+      return IFVS_OK;
     case IFVS_OPT_COUNT_READS:
       if (value > 1) return fail(IFVS_E_INVALID, "IFVS_OPT_COUNT_READS takes 0 or 1");
       if (value == 1 && !idx->read_hist) {
@@ -1099,8 +1150,8 @@ namespace {
 // the index's own workspace (no gather scan then: every query takes the tiled
 // scan, with the same results).
 ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds, const void* lut,
-                        int32_t lut_dtype, int32_t k, int32_t* ids_out, float* dist_out, uint32_t* bitmap_out,
-                        void* stream, bool static_scratch) {
+                        int32_t lut_dtype, const float* lut_bounds, int32_t k, int32_t* ids_out, float* dist_out,
+                        uint32_t* bitmap_out, void* stream, bool static_scratch) {
   if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
   if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
   if (lut_dtype != IFVS_LUT_F32 && lut_dtype != IFVS_LUT_F16) return fail(IFVS_E_INVALID, "unknown lut_dtype");
@@ -1136,6 +1187,20 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   ScanPlan plan{};
   if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, interval_batch, span, ws.partial_keys, &plan); st != IFVS_OK)
     return st;
+  // List scan (coarse bound): when the caller passed the tables' bounds, a
+  // coarse build exists and every query's selection is its row interval
+  // (no residual clauses); automatic for batches whose widest interval spans
+  // at least kCoarseAutoTiles 64-row tiles.
+  const CoarseLists& cl = idx->coarse;
+  const int list_splits = std::min(kListSlots / (2 * kScanWaves),
+                                   idx->opt_splits > 0 ? idx->opt_splits : std::max(1, (1024 + nq - 1) / nq));
+  const bool list_mode =
+      lut_bounds && cl.words && idx->opt_coarse != 1 && !static_scratch && !need_bitmap &&
+      !idx->opt_count_reads && list_scan_supported(idx->m, lut_dtype) &&
+      list_plan_lds_bytes(idx->m, lut_dtype, cl.C) <= size_t{kLdsBudget} &&
+      list_scan_lds_bytes(idx->m, lut_dtype, pool_stride_for(k)) <= size_t{kLdsBudget} &&
+      static_cast<size_t>(nq) * list_splits * kScanWaves * k <= ws.partial_keys &&
+      (idx->opt_coarse == 2 || span >= kCoarseAutoTiles);
   if (idx->opt_count_reads &&
       (!scan_can_count(idx->m, plan.qtile, lut_dtype) || plan.lds_bytes + kLookupHistBytes > size_t{kLdsBudget}))
     return fail(IFVS_E_UNSUPPORTED, "IFVS_OPT_COUNT_READS: no read-counting scan for this plan (it needs one query "
@@ -1159,6 +1224,78 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
                                        : nullptr,
                                ws.slot_order, ordered ? n_order : 0, s));
   if (ifvs_status st = release_slot(idx, slot, s); st != IFVS_OK) return st;
+  if (list_mode) {
+    ListPlanArgs pa{};
+    pa.lut = lut;
+    pa.m = idx->m;
+    pa.nq = nq;
+    pa.cc_t = cl.cc_t;
+    pa.mw = idx->mw;
+    pa.C = cl.C;
+    pa.n_sub = cl.C * kBands;
+    pa.Sp = list_plan_width(cl.C);
+    pa.bounds = lut_bounds;
+    pa.iv = ws.iv;
+    pa.cnt_f = cl.cnt_f;
+    pa.f_shift = cl.f_shift;
+    pa.words = cl.words;
+    pa.band = cl.band;
+    pa.sub_off = cl.sub_off;
+    pa.rmax = cl.rmax;
+    pa.tmp_r0 = cl.tmp_r0;
+    pa.tmp_r1 = cl.tmp_r1;
+    pa.keep = coarse_keep(idx->m, idx->dsub, lut_dtype);
+    pa.abs_m = coarse_abs(idx->m, lut_dtype);
+    pa.it_r0 = cl.it_r0;
+    pa.it_r1 = cl.it_r1;
+    pa.it_t = cl.it_t;
+    pa.it_sdc = cl.it_sdc;
+    pa.it_lb = cl.it_lb;
+    pa.hdr = cl.hdr;
+    pa.slots = cl.slots;
+    IFVS_LAUNCH(idx, kStCoarse, s, "launching list plan kernel", launch_list_plan(pa, lut_dtype, s));
+    ListScanArgs sa{};
+    sa.codes_t = cl.codes_t;
+    sa.rad = cl.rad;
+    sa.ids = cl.ids;
+    sa.m = idx->m;
+    sa.mw = idx->mw;
+    sa.lut = lut;
+    sa.nq = nq;
+    sa.splits = list_splits;
+    sa.qorder = ws.qorder;
+    sa.it_r0 = cl.it_r0;
+    sa.it_r1 = cl.it_r1;
+    sa.it_t = cl.it_t;
+    sa.it_sdc = cl.it_sdc;
+    sa.it_lb = cl.it_lb;
+    sa.hdr = cl.hdr;
+    sa.C = cl.C * kBands;
+    sa.keep = pa.keep;
+    sa.abs_m = pa.abs_m;
+    sa.k = k;
+    sa.pool_stride = pool_stride_for(k);
+    sa.kpl = pool_kpl(k);
+    sa.partials = ws.partials;
+    sa.gthr = ws.gthr;
+    sa.slots = cl.slots;
+    IFVS_LAUNCH(idx, kStScan, s, "launching list scan kernel", launch_list_scan(sa, lut_dtype, s));
+    IFVS_LAUNCH(idx, kStMerge, s, "launching top-k merge kernel",
+                launch_topk_merge(ws.partials, nq, static_cast<int64_t>(list_splits) * kScanWaves * k, k, ws.iv, 0,
+                                  static_cast<int64_t>(kScanWaves) * k, ws.qorder, ids_out, dist_out, s));
+    if (bitmap_out) {
+      if (ifvs_status st = filter_into_workspace(idx, ws, nq, false, false, s); st != IFVS_OK) return st;
+      if (ifvs_status st = copy_bitmaps_out(idx, ws, nq, bitmap_out, s); st != IFVS_OK) return st;
+    }
+    ScanPlan lp{};
+    lp.qtile = 1;
+    lp.splits = list_splits;
+    lp.min_chunk = 0;
+    lp.lds_bytes = list_scan_lds_bytes(idx->m, lut_dtype, pool_stride_for(k));
+    idx->last_plan = lp;
+    idx->last_coarse = true;
+    return IFVS_OK;
+  }
   // Masked batches: a query whose pool is small is scored from its compacted
   // row list (decided on the device from the pool size); the rest take the
   // tiled scan.  The full selection bitmap (physical order) and the pool
@@ -1237,6 +1374,7 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     if (ifvs_status st = copy_bitmaps_out(idx, ws, nq, bitmap_out, s); st != IFVS_OK) return st;
   }
   idx->last_plan = plan;
+  idx->last_coarse = false;
   return IFVS_OK;
 }
 
@@ -1247,13 +1385,19 @@ extern "C" {
 ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
                                  const void* lut, int32_t lut_dtype, int32_t k, int32_t* ids_out,
                                  float* dist_out, uint32_t* bitmap_out, void* stream) {
-  return search_impl(idx, nq, preds, lut, lut_dtype, k, ids_out, dist_out, bitmap_out, stream, false);
+  return search_impl(idx, nq, preds, lut, lut_dtype, nullptr, k, ids_out, dist_out, bitmap_out, stream, false);
+}
+
+ifvs_status ifvs_filtered_search_bounded(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
+                                         const void* lut, int32_t lut_dtype, const float* lut_bounds, int32_t k,
+                                         int32_t* ids_out, float* dist_out, uint32_t* bitmap_out, void* stream) {
+  return search_impl(idx, nq, preds, lut, lut_dtype, lut_bounds, k, ids_out, dist_out, bitmap_out, stream, false);
 }
 
 ifvs_status ifvs_filtered_search_noalloc(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
                                          const void* lut, int32_t lut_dtype, int32_t k, int32_t* ids_out,
                                          float* dist_out, uint32_t* bitmap_out, void* stream) {
-  return search_impl(idx, nq, preds, lut, lut_dtype, k, ids_out, dist_out, bitmap_out, stream, true);
+  return search_impl(idx, nq, preds, lut, lut_dtype, nullptr, k, ids_out, dist_out, bitmap_out, stream, true);
 }
 
 }  // extern "C"
@@ -1728,6 +1872,248 @@ ifvs_status ifvs_last_plan(const ifvs_index* idx, int64_t* out5) {
   out5[2] = idx->last_plan.min_chunk;
   out5[3] = static_cast<int64_t>(idx->last_plan.lds_bytes);
   out5[4] = idx->last_plan.chunk_tiles;
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_last_coarse(const ifvs_index* idx, int32_t* used_out) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (!used_out) return fail(IFVS_E_INVALID, "used_out is NULL");
+  *used_out = idx->last_coarse ? 1 : 0;
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_build_coarse(ifvs_index* idx, int32_t n_centroids, int32_t iters) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (n_centroids < 1 || n_centroids > kCoarseMax || n_centroids > idx->n)
+    return fail(IFVS_E_INVALID, "n_centroids outside 1.." + std::to_string(kCoarseMax) + " (and at most n)");
+  if (iters < 0 || iters > 1000) return fail(IFVS_E_INVALID, "iters outside 0..1000");
+  if (idx->dim > kCoarseMaxDim)
+    return fail(IFVS_E_UNSUPPORTED, "a coarse quantizer needs dim <= " + std::to_string(kCoarseMaxDim));
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  const int C = n_centroids, D = idx->dim, mw = idx->mw;
+  const int64_t n = idx->n, n_pad = idx->n_tiles * kTileRows;
+  const int64_t S = coarse_samples(n, C);
+  float* X = nullptr;
+  float* cent = nullptr;
+  float* chat = nullptr;
+  int32_t* assign = nullptr;
+  uint32_t* cc = nullptr;
+  int32_t* lrow = nullptr;
+  CoarseLists nl;
+  nl.C = C;
+  auto cleanup = [&](ifvs_status st) {
+    for (void* p : {static_cast<void*>(X), static_cast<void*>(cent), static_cast<void*>(chat),
+                    static_cast<void*>(assign), static_cast<void*>(cc), static_cast<void*>(lrow)})
+      if (p) (void)hipFree(p);
+    nl.release();
+    return st;
+  };
+  auto alloc = [&](auto** p, size_t count, const char* what) { return dev_alloc(p, count, what); };
+  if (ifvs_status st = alloc(&X, static_cast<size_t>(S) * D, "coarse samples"); st != IFVS_OK) return cleanup(st);
+  if (ifvs_status st = alloc(&cent, static_cast<size_t>(C) * D, "coarse centroids"); st != IFVS_OK)
+    return cleanup(st);
+  if (ifvs_status st = alloc(&chat, static_cast<size_t>(C) * D, "encoded centroids"); st != IFVS_OK)
+    return cleanup(st);
+  if (ifvs_status st = alloc(&assign, static_cast<size_t>(S), "coarse assignment"); st != IFVS_OK) return cleanup(st);
+  if (ifvs_status st = alloc(&cc, static_cast<size_t>(C) * mw, "centroid codes"); st != IFVS_OK) return cleanup(st);
+  if (ifvs_status st = alloc(&nl.words, static_cast<size_t>(n_pad), "coarse row words"); st != IFVS_OK)
+    return cleanup(st);
+  hipStream_t s = nullptr;
+  auto step = [&](hipError_t e, const char* what) -> ifvs_status {
+    return e == hipSuccess ? IFVS_OK : hip_fail(e, what);
+  };
+  // Samples: evenly spaced rows; first centroids: C evenly spaced rows.
+  if (ifvs_status st = step(launch_coarse_sample(idx->codes_t, mw, idx->m, idx->dsub, idx->cpq, S, n / S, X, s),
+                            "launching coarse sample kernel");
+      st != IFVS_OK)
+    return cleanup(st);
+  if (ifvs_status st = step(launch_coarse_sample(idx->codes_t, mw, idx->m, idx->dsub, idx->cpq, C, n / C, cent, s),
+                            "launching coarse sample kernel");
+      st != IFVS_OK)
+    return cleanup(st);
+  for (int it = 0; it < iters; ++it)
+    if (ifvs_status st = step(launch_coarse_kmeans_step(X, S, D, cent, C, assign, s), "launching k-means kernels");
+        st != IFVS_OK)
+      return cleanup(st);
+  if (ifvs_status st = step(launch_coarse_encode(cent, C, idx->m, mw, idx->dsub, idx->cpq, cc, chat, s),
+                            "launching centroid encoding kernel");
+      st != IFVS_OK)
+    return cleanup(st);
+  if (ifvs_status st = step(launch_coarse_rows(idx->codes_t, n, n_pad, idx->m, mw, idx->dsub, idx->cpq, chat, C,
+                                               nl.words, s),
+                            "launching coarse assignment kernel");
+      st != IFVS_OK)
+    return cleanup(st);
+  if (ifvs_status st = step(hipDeviceSynchronize(), "building the coarse quantizer"); st != IFVS_OK)
+    return cleanup(st);
+
+  // Sub-lists (host).  Each row's radius band within its list: the list's
+  // radii at the quantiles kBandQuantiles split it into kBands bands (equal
+  // radii share a band).  Then a stable counting sort of the layout rows by
+  // sub-list s = c * kBands + b, the largest radius of each sub-list, and
+  // the rank table every 2^f_shift rows.
+  std::vector<uint32_t> hw(static_cast<size_t>(n));
+  std::vector<uint32_t> hcc(static_cast<size_t>(C) * mw);
+  if (ifvs_status st = step(hipMemcpy(hw.data(), nl.words, hw.size() * 4, hipMemcpyDeviceToHost), "reading row words");
+      st != IFVS_OK)
+    return cleanup(st);
+  if (ifvs_status st = step(hipMemcpy(hcc.data(), cc, hcc.size() * 4, hipMemcpyDeviceToHost), "reading centroids");
+      st != IFVS_OK)
+    return cleanup(st);
+  const int NS = C * kBands;
+  auto radius_of = [&](int64_t r) {
+    const uint32_t bits = hw[static_cast<size_t>(r)] & 0xFFFF0000u;
+    float rad;
+    std::memcpy(&rad, &bits, 4);
+    return rad;
+  };
+  std::vector<int32_t> coff(static_cast<size_t>(C) + 1, 0);
+  for (int64_t r = 0; r < n; ++r) ++coff[static_cast<size_t>(hw[static_cast<size_t>(r)] & 0xFFFFu) + 1];
+  for (int c = 0; c < C; ++c) coff[static_cast<size_t>(c) + 1] += coff[static_cast<size_t>(c)];
+  std::vector<float> radii(static_cast<size_t>(n));
+  {
+    std::vector<int32_t> pos(coff.begin(), coff.end() - 1);
+    for (int64_t r = 0; r < n; ++r)
+      radii[static_cast<size_t>(pos[hw[static_cast<size_t>(r)] & 0xFFFFu]++)] = radius_of(r);
+  }
+  std::vector<float> cut(static_cast<size_t>(C) * (kBands - 1));
+  for (int c = 0; c < C; ++c) {
+    auto b = radii.begin() + coff[static_cast<size_t>(c)], e = radii.begin() + coff[static_cast<size_t>(c) + 1];
+    std::sort(b, e);
+    const int64_t cnt = e - b;
+    for (int j = 0; j < kBands - 1; ++j)
+      cut[static_cast<size_t>(c) * (kBands - 1) + j] =
+          cnt > 0 ? *(b + std::min<int64_t>(cnt - 1, static_cast<int64_t>(kBandQuantiles[j] * cnt))) : 0.0f;
+  }
+  std::vector<uint8_t> hband(static_cast<size_t>(n));
+  std::vector<int32_t> off(static_cast<size_t>(NS) + 1, 0), hrow(static_cast<size_t>(n));
+  std::vector<float> rmax(static_cast<size_t>(NS), 0.0f);
+  for (int64_t r = 0; r < n; ++r) {
+    const int c = static_cast<int>(hw[static_cast<size_t>(r)] & 0xFFFFu);
+    const float rad = radius_of(r);
+    int b = 0;
+    while (b < kBands - 1 && rad > cut[static_cast<size_t>(c) * (kBands - 1) + b]) ++b;
+    hband[static_cast<size_t>(r)] = static_cast<uint8_t>(b);
+    const int sub = c * kBands + b;
+    ++off[static_cast<size_t>(sub) + 1];
+    rmax[static_cast<size_t>(sub)] = std::max(rmax[static_cast<size_t>(sub)], rad);
+  }
+  for (int sub = 0; sub < NS; ++sub) off[static_cast<size_t>(sub) + 1] += off[static_cast<size_t>(sub)];
+  nl.f_shift = 12;
+  while (((n >> nl.f_shift) + 1) * NS > (int64_t{1} << 24)) ++nl.f_shift;
+  const int64_t nb = (n >> nl.f_shift) + 1;
+  std::vector<int32_t> cnt_f(static_cast<size_t>(nb * NS));
+  {
+    std::vector<int32_t> run(static_cast<size_t>(NS), 0), pos(off.begin(), off.end() - 1);
+    const int64_t fmask = (int64_t{1} << nl.f_shift) - 1;
+    for (int64_t r = 0; r < n; ++r) {
+      if ((r & fmask) == 0) std::copy(run.begin(), run.end(), cnt_f.begin() + (r >> nl.f_shift) * NS);
+      const int sub = static_cast<int>(hw[static_cast<size_t>(r)] & 0xFFFFu) * kBands + hband[static_cast<size_t>(r)];
+      hrow[static_cast<size_t>(pos[static_cast<size_t>(sub)]++)] = static_cast<int32_t>(r);
+      ++run[static_cast<size_t>(sub)];
+    }
+    if ((n & fmask) == 0) std::copy(run.begin(), run.end(), cnt_f.begin() + (n >> nl.f_shift) * NS);
+  }
+  std::vector<uint32_t> cc_t(hcc.size());
+  for (int c = 0; c < C; ++c)
+    for (int w = 0; w < mw; ++w)
+      cc_t[static_cast<size_t>(w) * C + c] = hcc[static_cast<size_t>(c) * mw + w];
+
+  const size_t items = static_cast<size_t>(idx->max_batch) * NS;
+  if (ifvs_status st = alloc(&nl.cc_t, cc_t.size(), "centroid codes"); st != IFVS_OK) return cleanup(st);
+  if (ifvs_status st = alloc(&nl.sub_off, off.size(), "sub-list offsets"); st != IFVS_OK) return cleanup(st);
+  if (ifvs_status st = alloc(&nl.rmax, rmax.size(), "sub-list radii"); st != IFVS_OK) return cleanup(st);
+  if (ifvs_status st = alloc(&nl.cnt_f, cnt_f.size(), "sub-list rank table"); st != IFVS_OK) return cleanup(st);
+  if (ifvs_status st = alloc(&nl.band, hband.size(), "radius bands"); st != IFVS_OK) return cleanup(st);
+  if (ifvs_status st = alloc(&nl.codes_t, static_cast<size_t>(n_pad) * mw, "list-order codes"); st != IFVS_OK)
+    return cleanup(st);
+  if (ifvs_status st = alloc(&nl.rad, static_cast<size_t>(n_pad), "list-order radii"); st != IFVS_OK)
+    return cleanup(st);
+  if (ifvs_status st = alloc(&nl.ids, static_cast<size_t>(n_pad), "list-order ids"); st != IFVS_OK)
+    return cleanup(st);
+  if (ifvs_status st = alloc(&lrow, hrow.size(), "list rows"); st != IFVS_OK) return cleanup(st);
+  for (int32_t** a : {&nl.it_r0, &nl.it_r1, &nl.it_t, &nl.tmp_r0, &nl.tmp_r1})
+    if (ifvs_status st = alloc(a, items, "list plan"); st != IFVS_OK) return cleanup(st);
+  for (float** a : {&nl.it_sdc, &nl.it_lb})
+    if (ifvs_status st = alloc(a, items, "list plan"); st != IFVS_OK) return cleanup(st);
+  if (ifvs_status st = alloc(&nl.hdr, static_cast<size_t>(idx->max_batch) * 4, "list plan"); st != IFVS_OK)
+    return cleanup(st);
+  if (ifvs_status st = alloc(&nl.slots, static_cast<size_t>(idx->max_batch) * kListSlots, "list scan bound slots");
+      st != IFVS_OK)
+    return cleanup(st);
+  const struct {
+    void* dst;
+    const void* src;
+    size_t bytes;
+  } uploads[] = {{nl.cc_t, cc_t.data(), cc_t.size() * 4},   {nl.sub_off, off.data(), off.size() * 4},
+                 {nl.rmax, rmax.data(), rmax.size() * 4},    {nl.cnt_f, cnt_f.data(), cnt_f.size() * 4},
+                 {nl.band, hband.data(), hband.size()},      {lrow, hrow.data(), hrow.size() * 4}};
+  for (const auto& u : uploads)
+    if (ifvs_status st = step(hipMemcpy(u.dst, u.src, u.bytes, hipMemcpyHostToDevice), "uploading the lists");
+        st != IFVS_OK)
+      return cleanup(st);
+  if (ifvs_status st = step(launch_gather_list(idx->codes_t, mw, nl.words, idx->perm, lrow, n, idx->n_tiles,
+                                               nl.codes_t, nl.rad, nl.ids, s),
+                            "launching list gather kernels");
+      st != IFVS_OK)
+    return cleanup(st);
+  if (ifvs_status st = step(hipDeviceSynchronize(), "building the lists"); st != IFVS_OK) return cleanup(st);
+  idx->coarse.release();
+  idx->coarse = nl;
+  nl = CoarseLists{};
+  return cleanup(IFVS_OK);
+}
+
+ifvs_status ifvs_lut_bounds(ifvs_index* idx, int32_t nq, const float* alpha, const float* wf, float* bounds_out,
+                            void* stream) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
+  if (nq == 0) return IFVS_OK;
+  if (!bounds_out) return fail(IFVS_E_INVALID, "bounds_out is NULL");
+  if (alpha && idx->bank_rows == 0) return fail(IFVS_E_INVALID, "alpha given but the index has no memory bank");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  IFVS_LAUNCH(idx, kStCoarse, s, "launching table bounds kernel",
+              launch_lut_bounds(alpha, wf, idx->cpq, idx->W, nq, idx->m, idx->r, idx->dsub, bounds_out, s));
+  return IFVS_OK;
+}
+
+ifvs_status ifvs_read_coarse(const ifvs_index* idx, int32_t* n_centroids_out, int32_t* assign_out,
+                             float* radius_out, uint8_t* codes_out) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  const CoarseLists& cl = idx->coarse;
+  if (!cl.words) return fail(IFVS_E_STATE, "no coarse quantizer built (ifvs_build_coarse)");
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  IFVS_HIP(hipDeviceSynchronize(), "waiting for the device");
+  if (n_centroids_out) *n_centroids_out = cl.C;
+  if (assign_out || radius_out) {
+    std::vector<uint32_t> w(static_cast<size_t>(idx->n));
+    IFVS_HIP(hipMemcpy(w.data(), cl.words, w.size() * 4, hipMemcpyDeviceToHost), "reading coarse words");
+    std::vector<int32_t> perm;
+    if (idx->perm) {
+      perm.resize(static_cast<size_t>(idx->n));
+      IFVS_HIP(hipMemcpy(perm.data(), idx->perm, perm.size() * 4, hipMemcpyDeviceToHost), "reading the row order");
+    }
+    for (int64_t r = 0; r < idx->n; ++r) {
+      const int64_t id = idx->perm ? perm[static_cast<size_t>(r)] : r;
+      const uint32_t v = w[static_cast<size_t>(r)];
+      if (assign_out) assign_out[id] = static_cast<int32_t>(v & 0xFFFFu);
+      if (radius_out) {
+        const uint32_t bits = v & 0xFFFF0000u;
+        float f;
+        std::memcpy(&f, &bits, 4);
+        radius_out[id] = f;
+      }
+    }
+  }
+  if (codes_out) {
+    std::vector<uint32_t> cw(static_cast<size_t>(cl.C) * idx->mw);
+    IFVS_HIP(hipMemcpy(cw.data(), cl.cc_t, cw.size() * 4, hipMemcpyDeviceToHost), "reading centroid codes");
+    for (int c = 0; c < cl.C; ++c)
+      for (int m = 0; m < idx->m; ++m)
+        codes_out[static_cast<size_t>(c) * idx->m + m] =
+            static_cast<uint8_t>((cw[static_cast<size_t>(m / 4) * cl.C + c] >> (8 * (m % 4))) & 0xFFu);
+  }
   return IFVS_OK;
 }
 

@@ -17,6 +17,11 @@ constexpr int kScanPub = 2;                // best keys per (wavefront, query) p
 constexpr int kScanSeed = 8;               // seed candidates per wavefront (kScanWaves * kScanSeed = 64 >= k)
 constexpr int kFilterQueries = 16;         // predicates evaluated per attribute read
 constexpr int kLookupHistBytes = 272;      // LDS of the scan's read-counting build: 65 counters, padded
+constexpr int kCoarseMaxDim = 128;         // largest D with a coarse quantizer (a row held in registers)
+constexpr int kCoarseMax = 4096;           // most coarse centroids
+constexpr int kBands = 4;                  // radius bands per coarse list (sub-lists)
+constexpr int kMaxItems = kCoarseMax * kBands;   // sub-lists a list plan sorts in one workgroup
+constexpr int kItemMask = kMaxItems - 1;         // sub-list index bits of a plan's sort key
 
 // A predicate as the device sees it.  The raw fields are the caller's clauses
 // exactly as given (they are hashed into the memory bank); the effective
@@ -231,6 +236,89 @@ hipError_t launch_encoder(const float* params, const double* off, const double* 
 // Whether a read-counting build of the scan exists for this plan (one query
 // per tile, M of 16, 48 or 120).
 bool scan_can_count(int m, int qtile, int lut_dtype);
+// Coarse quantizer (k_coarse.hip).  Per layout row one word: centroid id in
+// the low 16 bits, the radius ||c0 - x0|| rounded up to a bfloat16 in the
+// high 16.
+int64_t coarse_samples(int64_t n, int C);
+float coarse_keep(int m, int dsub, int lut_dtype);   // 1 - eps on squared distances
+float coarse_abs(int m, int lut_dtype);              // absolute rounding allowance of a table sum
+hipError_t launch_coarse_sample(const uint32_t* codes_t, int mw, int m, int dsub, const float* cpq, int64_t S,
+                                int64_t stride, float* X, hipStream_t s);
+hipError_t launch_coarse_kmeans_step(const float* X, int64_t S, int D, float* cent, int C, int32_t* assign,
+                                     hipStream_t s);
+hipError_t launch_coarse_encode(const float* cent, int C, int m, int mw, int dsub, const float* cpq, uint32_t* cc,
+                                float* chat, hipStream_t s);
+hipError_t launch_coarse_rows(const uint32_t* codes_t, int64_t n, int64_t n_pad, int m, int mw, int dsub,
+                              const float* cpq, const float* chat, int C, uint32_t* words, hipStream_t s);
+hipError_t launch_lut_bounds(const float* alpha, const float* wf, const float* cpq, const float* W, int nq, int m,
+                             int r, int dsub, float* bounds, hipStream_t s);
+// List order: rows grouped by sub-list s = (centroid c, radius band b),
+// s = c * kBands + b, positions [sub_off[s], sub_off[s+1]), each sub-list in
+// layout order.  Code tiles, radii and original ids gathered through
+// src_rows[p] = layout row of position p.
+hipError_t launch_gather_list(const uint32_t* src_t, int mw, const uint32_t* words, const int32_t* perm,
+                              const int32_t* src_rows, int64_t n, int64_t n_tiles, uint32_t* dst_t, float* rad,
+                              int32_t* ids, hipStream_t s);
+
+// Per-query list plan (one workgroup per original query index).
+struct ListPlanArgs {
+  const void* lut;          // [nq][m][256] tables (fp32 or binary16)
+  int m, nq;
+  const uint32_t* cc_t;     // [mw][C] centroid code words
+  int mw, C, n_sub, Sp;     // n_sub = C * kBands sub-lists, Sp = list_plan_width(C)
+  const float* bounds;      // [nq][2]: sqrt(max w), delta (ifvs_lut_bounds)
+  const int64_t* iv;        // [nq][2] layout row interval of each query
+  const int32_t* cnt_f;     // [(n >> f_shift) + 1][n_sub]: rows of sub-list s among layout rows [0, b << f_shift)
+  int f_shift;
+  const uint32_t* words;    // [n] layout row words (centroid id in the low 16 bits)
+  const uint8_t* band;      // [n] layout row radius band
+  const int32_t* sub_off;   // [n_sub + 1]
+  const float* rmax;        // [n_sub] largest radius of each sub-list
+  float keep, abs_m;
+  int32_t* tmp_r0;          // [nq][n_sub] workspace
+  int32_t* tmp_r1;          // [nq][n_sub] workspace
+  // Outputs by original query: items [nq][n_sub] in increasing bound order,
+  // and a header [nq][4] = {items (int bits), tiles (int bits), sqrt(max w),
+  // delta}.
+  int32_t* it_r0;           // first list position of the item's rows
+  int32_t* it_r1;           // one past the last
+  int32_t* it_t;            // 64-row tiles the items before it touch
+  float* it_sdc;            // lower bound of the query's distance to the sub-list's centroid
+  float* it_lb;             // lower bound of the distance of every row of the sub-list (NaN: none)
+  float* hdr;
+  uint32_t* slots;          // [nq][kListSlots] the list scan's union-bound slots, reset here
+};
+int list_plan_width(int C);   // power of two >= C * kBands
+size_t list_plan_lds_bytes(int m, int lut_dtype, int C);
+hipError_t launch_list_plan(const ListPlanArgs& a, int lut_dtype, hipStream_t s);
+
+// List scan (k_listscan.hip): the Rank and Select stages over the items of
+// each query, nearest list first, skipping lists and rows by the bound.
+struct ListScanArgs {
+  const uint32_t* codes_t;  // [n_tiles][mw][64] list-order code words
+  const float* rad;         // [n_tiles * 64] list-order radii
+  const int32_t* ids;       // list position -> original id
+  int m, mw;
+  const void* lut;          // [nq][m][256] by original query
+  int nq, splits;           // workgroups per query position
+  const int32_t* qorder;    // position -> original query
+  const int32_t* it_r0;
+  const int32_t* it_r1;
+  const int32_t* it_t;
+  const float* it_sdc;
+  const float* it_lb;
+  const float* hdr;
+  int C;                    // item stride per query (sub-lists)
+  float keep, abs_m;
+  int k, pool_stride, kpl;
+  uint64_t* partials;       // [positions][splits][kScanWaves][k]
+  uint64_t* gthr;           // [nq] shared thresholds, all ones before the scan
+  uint32_t* slots;          // [nq][kListSlots] union-bound slots, all ones before the scan (list plan)
+};
+constexpr int kListSlots = 2 * kScanWaves * 16;   // two per wavefront of at most 16 workgroups per query
+bool list_scan_supported(int m, int lut_dtype);
+size_t list_scan_lds_bytes(int m, int lut_dtype, int pool_stride);
+hipError_t launch_list_scan(const ListScanArgs& a, int lut_dtype, hipStream_t s);
 
 // LDS gather probe (k_probe.hip): wavefront-level 4-byte random LDS reads per
 // second, chip-wide, with `active` lanes (1..64) per read, measured over

@@ -1,0 +1,363 @@
+// Rank and Select stages (Section 2, stages 2 and 3) in coarse-list order:
+// the same distances and the same top k as the interval scan, with rows that
+// cannot enter the top k skipped before their codes are read.
+//
+// The index keeps a second copy of its codes grouped by coarse centroid and
+// radius band (sub-lists; each in layout order, so the rows of a query's
+// layout interval are one run of positions per sub-list).  The list plan
+// gives each query its sub-lists that hold selected rows (items) in
+// increasing order of lb, a lower bound on the distance of every row of the
+// item, with sdc, a lower bound on the query's distance to the item's
+// centroid (a row's own bound is sdc - sqrt(max w) (r + delta), r its
+// radius).  A query is scanned by `splits` workgroups of kScanWaves
+// wavefronts; the G = splits * kScanWaves wavefronts share its tiles by
+// position in the concatenation of its items' tiles (wavefront g takes the
+// positions congruent to g mod G), so each row is scored by exactly one
+// wavefront whatever each one skips.  A wavefront stops at the first item
+// (or in the middle of one) whose lb^2 * keep - abs exceeds its current k-th
+// distance: every later item has a bound at least as large.  It also skips
+// a row when the row's own bound does.  lb^2 * keep - abs never exceeds a
+// row's computed distance (the rounding allowances of the bound), so a
+// skipped row is one whose distance exceeds the cut and the top k is
+// unchanged.
+//
+// Per tile the work is the interval scan's: sum of M table entries in
+// groups of subspaces with early abandonment, candidates into per-wavefront
+// pools of row keys resolved to original ids at compaction, thresholds
+// shared through LDS and a per-query global word.
+//
+// Query-wide union bound (k <= 2 G): a wavefront's own k-th key is loose
+// while it has seen only a tile or two of the nearest lists, so each
+// wavefront also keeps its two smallest full distances (two distinct rows)
+// in the query's 2 G global slots; the wavefronts scan disjoint rows, so the
+// k-th smallest slot is the distance of one of k distinct rows at or below
+// it, a bound on the query's k-th distance (published like a threshold, with
+// the largest id so rows at that distance stay eligible).
+#include <climits>
+
+#include "ifvs_internal.h"
+#include "topk_device.h"
+
+namespace ifvs {
+
+namespace {
+
+__device__ __forceinline__ float widen(float v) { return v; }
+__device__ __forceinline__ float widen(__half v) { return __half2float(v); }
+
+// Bits [lo, hi) of a 64-bit word, 0 <= lo < hi <= 64.
+__device__ __forceinline__ uint64_t bit_range(int lo, int hi) {
+  const uint64_t upto_hi = hi >= 64 ? ~0ull : ((1ull << hi) - 1);
+  return upto_hi & ~((1ull << lo) - 1);
+}
+
+// Two register sets of ceil(M/4) code words each, and a subspace group's
+// addresses and entries: M = 120 needs the register file of two waves per
+// SIMD.
+template <int MT, typename LutT>
+constexpr int list_waves_per_eu() {
+  return MT == 120 ? 2 : 4;
+}
+
+template <int MT, typename LutT>
+__global__ __launch_bounds__(kScanWaves * 64) __attribute__((amdgpu_waves_per_eu(list_waves_per_eu<MT, LutT>())))
+void list_scan_kernel(const ListScanArgs a) {
+  constexpr int kMW = (MT + 3) / 4;
+  constexpr int kGroup = MT % 8 == 0 && MT > 16 ? 8 : (MT % 4 == 0 ? 4 : MT);
+  constexpr int kThreads = kScanWaves * 64;
+  constexpr int kVec = 16 / sizeof(LutT);
+  constexpr int kVecQ = MT * kKsub / kVec;
+  __shared__ __align__(16) LutT s_lut[MT * kKsub];
+  extern __shared__ __align__(16) unsigned char smem[];
+  uint64_t* pools = reinterpret_cast<uint64_t*>(smem);
+  unsigned long long* s_thr = reinterpret_cast<unsigned long long*>(pools + kScanWaves * a.pool_stride);
+  uint32_t* s_bad = reinterpret_cast<uint32_t*>(s_thr + 1);
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int pos = blockIdx.x / a.splits, split = blockIdx.x % a.splits;
+  const int n_slots = 2 * kScanWaves * a.splits;
+  if (pos >= a.nq) return;
+  const int q = a.qorder[pos];
+  const int k = a.k;
+  const float* hdr = a.hdr + 4 * static_cast<size_t>(q);
+  const int n_items = __float_as_int(hdr[0]);
+  const float sw = hdr[2], delta = hdr[3];
+
+  // The query's table into LDS, noting negative or NaN entries (then partial
+  // sums bound nothing: no abandonment and no skipping).
+  const uint4* src = reinterpret_cast<const uint4*>(static_cast<const LutT*>(a.lut) + static_cast<size_t>(q) * MT * kKsub);
+  bool bad = false;
+  for (int v = threadIdx.x; v < kVecQ; v += kThreads) {
+    const uint4 x = src[v];
+    reinterpret_cast<uint4*>(s_lut)[v] = x;
+    const LutT* xe = reinterpret_cast<const LutT*>(&x);
+#pragma unroll
+    for (int e = 0; e < kVec; ++e) bad = bad || !(widen(xe[e]) >= 0.0f);
+  }
+  const bool wave_bad = __ballot(bad) != 0;
+  if (lane == 0) s_bad[wave] = wave_bad ? 1u : 0u;
+  if (threadIdx.x == 0) *s_thr = kNoKey;
+  __syncthreads();
+  bool monotone = true;
+#pragma unroll
+  for (int w = 0; w < kScanWaves; ++w) monotone = monotone && s_bad[w] == 0;
+
+  uint64_t* pool = pools + static_cast<size_t>(wave) * a.pool_stride;
+  int cnt = 0;
+  uint64_t thr = kNoKey, published = kNoKey, gview = kNoKey, gnext = kNoKey, bound = kNoKey;
+  float cut = __builtin_nanf("");
+  // bound = min(own k-th key, workgroup's, query's); cut its distance (NaN
+  // while there is none, or when the table is not monotone).
+  auto refresh = [&]() {
+    const uint64_t blk = __hip_atomic_load(s_thr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    uint64_t b = thr < blk ? thr : blk;
+    b = b < gview ? b : gview;
+    bound = b;
+    cut = monotone ? from_ordered_bits(static_cast<uint32_t>(bound >> 32)) : __builtin_nanf("");
+  };
+  auto pruned = [&](float lb) -> bool {
+    return lb > 0.0f && __fsub_rn(__fmul_rn(__fmul_rn(lb, lb), a.keep), a.abs_m) > cut;
+  };
+
+  // Tile generator over the query's items.
+  const int G = kScanWaves * a.splits, g = split * kScanWaves + wave;
+  const size_t ib = static_cast<size_t>(q) * a.C;
+  int batch = -64;
+  int stop_at = n_items;   // items from here on are prunable
+  uint64_t pend = 0;
+  int v_r0 = 0, v_r1 = 0, v_t = 0;
+  float v_sdc = 0.0f, v_lb = 0.0f;
+  bool in_item = false;
+  int i_r0 = 0, i_r1 = 0, i_t = 0, i_nt = 0, p = 0;
+  float i_sdc = 0.0f, i_lb = 0.0f;
+  auto next_tile = [&](int& t, uint64_t& mask, float& sdc) -> bool {
+    for (;;) {
+      if (in_item) {
+        if (pruned(i_lb)) {
+          // this item and every later one
+          stop_at = 0;
+          pend = 0;
+          in_item = false;
+          return false;
+        }
+        if (p < i_t + i_nt) {
+          t = (i_r0 >> 6) + (p - i_t);
+          p += G;
+          const int row0 = t * 64;
+          mask = bit_range(max(i_r0 - row0, 0), min(i_r1 - row0, 64));
+          sdc = i_sdc;
+          return true;
+        }
+        in_item = false;
+      }
+      if (pend == 0) {
+        batch += 64;
+        if (batch >= stop_at) return false;
+        const int it = batch + lane;
+        bool ok = false, gone = false;
+        if (it < stop_at) {
+          v_r0 = a.it_r0[ib + it];
+          v_r1 = a.it_r1[ib + it];
+          v_t = a.it_t[ib + it];
+          v_sdc = a.it_sdc[ib + it];
+          v_lb = a.it_lb[ib + it];
+          const int nt = ((v_r1 - 1) >> 6) - (v_r0 >> 6) + 1;
+          const int off = ((g - v_t) % G + G) % G;   // first position of the item this wavefront takes
+          gone = pruned(v_lb);
+          ok = off < nt && !gone;
+        }
+        const uint64_t gm = __ballot(gone);
+        if (gm != 0) {
+          // the first prunable item ends the query's list for this wavefront
+          const int j0 = __builtin_ctzll(gm);
+          stop_at = batch + j0;
+          ok = ok && lane < j0;
+        }
+        pend = __ballot(ok);
+        continue;
+      }
+      const int j = __builtin_ctzll(pend);
+      pend &= pend - 1;
+      i_r0 = __builtin_amdgcn_readlane(v_r0, j);
+      i_r1 = __builtin_amdgcn_readlane(v_r1, j);
+      i_t = __builtin_amdgcn_readlane(v_t, j);
+      i_sdc = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v_sdc), j));
+      i_lb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v_lb), j));
+      i_nt = ((i_r1 - 1) >> 6) - (i_r0 >> 6) + 1;
+      p = i_t + ((g - i_t) % G + G) % G;
+      in_item = true;
+    }
+  };
+  auto load = [&](int t, uint32_t (&w)[kMW], float& r) {
+    const uint32_t* __restrict__ tile = a.codes_t + static_cast<size_t>(t) * (kMW * 64);
+#pragma unroll
+    for (int j = 0; j < kMW; ++j) w[j] = tile[j * 64 + lane];
+    r = a.rad[static_cast<size_t>(t) * 64 + lane];
+  };
+  const bool union_bound = k <= n_slots;
+  uint32_t* slots = a.slots + static_cast<size_t>(q) * kListSlots;
+  uint32_t best1 = ~0u, best2 = ~0u;   // this wavefront's two smallest full distances
+  auto publish = [&](uint64_t key) {
+    if (key < published) {
+      published = key;
+      if (lane == 0) {
+        atomicMin(s_thr, static_cast<unsigned long long>(key));
+        __hip_atomic_fetch_min(a.gthr + q, key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  };
+  auto consider = [&](bool act, float d, int t) {
+    uint64_t key = kNoKey;
+    bool cand = false;
+    if (act) {
+      const uint32_t db = ordered_bits(d);
+      if (db <= static_cast<uint32_t>(bound >> 32)) {
+        key = row_key(db, static_cast<uint32_t>(t * 64 + lane));
+        cand = true;
+      }
+    }
+    if (union_bound) {
+      // The step's two smallest distances (pairs merged across lanes), then
+      // the wavefront's two smallest so far.
+      uint32_t x1 = act ? ordered_bits(d) : ~0u, x2 = ~0u;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y1 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(x1), o, 64));
+        const uint32_t y2 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(x2), o, 64));
+        const uint32_t hi = x1 > y1 ? x1 : y1;
+        const uint32_t lo2 = x2 < y2 ? x2 : y2;
+        x1 = x1 < y1 ? x1 : y1;
+        x2 = hi < lo2 ? hi : lo2;
+      }
+      const uint32_t hi = best1 > x1 ? best1 : x1;
+      const uint32_t lo2 = best2 < x2 ? best2 : x2;
+      const uint32_t n1 = best1 < x1 ? best1 : x1;
+      const uint32_t n2 = hi < lo2 ? hi : lo2;
+      if (n1 < best1 || n2 < best2) {
+        // The k-th smallest slot only falls when a slot drops from at or
+        // above the published value to below it.
+        const uint32_t kth = static_cast<uint32_t>(published >> 32);
+        const bool crossed = (n1 < kth && best1 >= kth) || (n2 < kth && best2 >= kth);
+        best1 = n1;
+        best2 = n2;
+        if (lane < 2)
+          __hip_atomic_store(&slots[2 * g + lane], lane == 0 ? n1 : n2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (crossed) {
+          uint64_t v[kListSlots / 64];
+#pragma unroll
+          for (int u = 0; u < kListSlots / 64; ++u) {
+            const int e = lane * (kListSlots / 64) + u;
+            const uint32_t sv =
+                e < n_slots ? __hip_atomic_load(&slots[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : ~0u;
+            v[u] = (static_cast<uint64_t>(sv) << 32) | 0xFFFFFFFFull;
+          }
+          wave_bitonic_sort<kListSlots / 64>(v);
+          const int e = k - 1;
+          uint64_t mine = v[0];
+#pragma unroll
+          for (int u = 1; u < kListSlots / 64; ++u)
+            if (u == e % (kListSlots / 64)) mine = v[u];
+          const uint64_t ub = shfl_u64(mine, e / (kListSlots / 64));
+          if ((ub >> 32) != 0xFFFFFFFFull) publish(ub);
+        }
+      }
+    }
+    pool_push(pool, cnt, thr, key, cand, k, a.kpl, a.ids);
+    publish(thr);
+  };
+  auto sum_tile = [&](int t, uint64_t mask, float sdc, const uint32_t (&w)[kMW], float rad) {
+    refresh();
+    bool live = __builtin_amdgcn_inverse_ballot_w64(mask);
+    if (monotone && live) {
+      const float lb = __fsub_rn(sdc, __fmul_rn(__fadd_rn(rad, delta), sw));
+      if (pruned(lb)) live = false;
+    }
+    float d = 0.0f;
+#pragma unroll
+    for (int gr = 0; gr < MT / kGroup; ++gr) {
+      int addr[kGroup];
+#pragma unroll
+      for (int u = 0; u < kGroup; ++u) {
+        const int m = gr * kGroup + u;
+        addr[u] = m * kKsub + static_cast<int>((w[m >> 2] >> (8 * (m & 3))) & 0xFFu);
+      }
+      if (live) {
+        LutT v[kGroup];
+#pragma unroll
+        for (int u = 0; u < kGroup; ++u) v[u] = s_lut[addr[u]];
+#pragma unroll
+        for (int u = 0; u < kGroup; ++u) d = __fadd_rn(d, widen(v[u]));
+      }
+      live = live && !(d > cut);
+    }
+    if (__ballot(live) != 0 || union_bound) consider(live, d, t);
+  };
+
+  // Two register sets: the next tile's words are loaded while the current
+  // one is summed.
+  uint32_t wa[kMW], wb[kMW];
+  float ra = 0.0f, rb = 0.0f, sa = 0.0f, sb = 0.0f;
+  int ta = 0, tb = 0;
+  uint64_t ma = 0, mb = 0;
+  bool ha = next_tile(ta, ma, sa);
+  if (ha) load(ta, wa, ra);
+  for (;;) {
+    gview = gnext;
+    gnext = __hip_atomic_load(a.gthr + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const bool hb = next_tile(tb, mb, sb);
+    if (hb) load(tb, wb, rb);
+    if (!ha) break;
+    sum_tile(ta, ma, sa, wa, ra);
+    ha = next_tile(ta, ma, sa);
+    if (ha) load(ta, wa, ra);
+    if (!hb) break;
+    sum_tile(tb, mb, sb, wb, rb);
+  }
+
+  pool_compact(pool, cnt, thr, k, a.kpl, a.ids);
+  uint64_t* dst = a.partials + ((static_cast<size_t>(pos) * a.splits + split) * kScanWaves + wave) * k;
+  for (int e = lane; e < k; e += 64) dst[e] = pool[e];
+}
+
+template <int MT>
+const void* pick_list_t(int lut_dtype) {
+  return lut_dtype == 1 ? reinterpret_cast<const void*>(&list_scan_kernel<MT, __half>)
+                        : reinterpret_cast<const void*>(&list_scan_kernel<MT, float>);
+}
+
+const void* pick_list(int m, int lut_dtype) {
+  switch (m) {
+    case 16: return pick_list_t<16>(lut_dtype);
+    case 48: return pick_list_t<48>(lut_dtype);
+    case 120: return pick_list_t<120>(lut_dtype);
+    default: return nullptr;
+  }
+}
+
+size_t list_dyn_bytes(int pool_stride) {
+  return static_cast<size_t>(kScanWaves) * pool_stride * sizeof(uint64_t) + 8 + 4 * kScanWaves;
+}
+
+}  // namespace
+
+bool list_scan_supported(int m, int lut_dtype) { return pick_list(m, lut_dtype) != nullptr; }
+
+size_t list_scan_lds_bytes(int m, int lut_dtype, int pool_stride) {
+  return static_cast<size_t>(m) * kKsub * (lut_dtype == 1 ? 2 : 4) + list_dyn_bytes(pool_stride);
+}
+
+hipError_t launch_list_scan(const ListScanArgs& a, int lut_dtype, hipStream_t s) {
+  const void* fn = pick_list(a.m, lut_dtype);
+  if (!fn || a.splits < 1) return hipErrorInvalidValue;
+  if (a.nq <= 0) return hipSuccess;
+  const size_t dyn = list_dyn_bytes(a.pool_stride);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(dyn));
+  if (e != hipSuccess) return e;
+  ListScanArgs args = a;
+  void* kargs[] = {&args};
+  return hipLaunchKernel(fn, dim3(static_cast<unsigned>(a.nq) * static_cast<unsigned>(a.splits)),
+                         dim3(kScanWaves * 64), kargs, dyn, s);
+}
+
+}  // namespace ifvs

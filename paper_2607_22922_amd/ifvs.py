@@ -29,14 +29,17 @@ OPT_SHARED_BOUND = 9
 OPT_EXACT_PLAN = 10
 OPT_SEED_TILES = 11
 OPT_COUNT_READS = 12
-STAGES = ("condition", "lut", "filter", "scan", "merge", "encode")
+OPT_COARSE = 13
+STAGES = ("condition", "lut", "filter", "scan", "merge", "encode", "coarse")
 
 EXPORTED = ("ifvs_load_index", "ifvs_free_index", "ifvs_select_codebook", "ifvs_build_lut",
             "ifvs_filter", "ifvs_filtered_search", "ifvs_set_option", "ifvs_last_plan",
             "ifvs_read_profile", "ifvs_last_error", "ifvs_load_vectors", "ifvs_exact_search",
             "ifvs_build_sdc_lut", "ifvs_load_reconstructions", "ifvs_train_step", "ifvs_read_params",
             "ifvs_filtered_search_noalloc", "ifvs_read_scan_reads", "ifvs_probe_lds_gather",
-            "ifvs_encoder_params", "ifvs_load_encoder", "ifvs_encode_predicates")
+            "ifvs_encoder_params", "ifvs_load_encoder", "ifvs_encode_predicates",
+            "ifvs_build_coarse", "ifvs_lut_bounds", "ifvs_filtered_search_bounded", "ifvs_read_coarse",
+            "ifvs_last_coarse")
 
 
 class IfvsError(RuntimeError):
@@ -124,6 +127,11 @@ def _load_library() -> ctypes.CDLL:
         "ifvs_encoder_params": ([i32, i32, i32, i32, i32, i32], i64),
         "ifvs_load_encoder": ([vp, ctypes.POINTER(EncoderDesc)], i32),
         "ifvs_encode_predicates": ([vp, i32, vp, vp, vp], i32),
+        "ifvs_build_coarse": ([vp, i32, i32], i32),
+        "ifvs_lut_bounds": ([vp, i32, vp, vp, vp, vp], i32),
+        "ifvs_filtered_search_bounded": ([vp, i32, vp, vp, i32, vp, i32, vp, vp, vp, vp], i32),
+        "ifvs_read_coarse": ([vp, ctypes.POINTER(i32), vp, vp, vp], i32),
+        "ifvs_last_coarse": ([vp, ctypes.POINTER(i32)], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -246,6 +254,51 @@ class Index:
         out = (ctypes.c_int64 * 5)()
         _check(_lib.ifvs_last_plan(self.handle, out))
         return dict(qtile=out[0], splits=out[1], min_chunk=out[2], lds_bytes=out[3], grid_tiles=out[4])
+
+    def last_coarse(self) -> bool:
+        """Whether the most recent filtered search ran the coarse bound."""
+        out = ctypes.c_int32()
+        _check(_lib.ifvs_last_coarse(self.handle, ctypes.byref(out)))
+        return bool(out.value)
+
+    def build_coarse(self, n_centroids: int, iters: int = 20) -> None:
+        """ifvs_build_coarse: the coarse quantizer of the exact pruning bound."""
+        _check(_lib.ifvs_build_coarse(self.handle, int(n_centroids), int(iters)))
+
+    def read_coarse(self):
+        """(assign [n] int32, radius [n] fp32, centroid codes [C][m] uint8),
+        host numpy arrays by vector id (ifvs_read_coarse)."""
+        c = ctypes.c_int32()
+        _check(_lib.ifvs_read_coarse(self.handle, ctypes.byref(c), None, None, None))
+        assign = np.empty(self.n, dtype=np.int32)
+        radius = np.empty(self.n, dtype=np.float32)
+        codes = np.empty((c.value, self.m), dtype=np.uint8)
+        _check(_lib.ifvs_read_coarse(self.handle, None, assign.ctypes.data, radius.ctypes.data,
+                                     codes.ctypes.data))
+        return assign, radius, codes
+
+    def lut_bounds_into(self, nq, alpha, wf, bounds_out, stream=None):
+        _check(_lib.ifvs_lut_bounds(self.handle, nq, _ptr(alpha), _ptr(wf), bounds_out.data_ptr(),
+                                    _stream(stream)))
+
+    def lut_bounds(self, nq, alpha=None, wf=None):
+        """[nq][2] factors of the coarse bound for tables built with alpha, wf."""
+        out = torch.empty(nq, 2, device=self.device, dtype=torch.float32)
+        self.lut_bounds_into(nq, alpha, wf, out)
+        return out
+
+    def search_bounded_into(self, nq, preds_c, lut, lut_dtype, lut_bounds, k, ids_out, dist_out, bitmap_out=None,
+                            stream=None):
+        _check(_lib.ifvs_filtered_search_bounded(self.handle, nq, preds_c, lut.data_ptr(), lut_dtype,
+                                                 _ptr(lut_bounds), k, ids_out.data_ptr(), dist_out.data_ptr(),
+                                                 _ptr(bitmap_out), _stream(stream)))
+
+    def search_bounded(self, preds, lut, lut_bounds, k, lut_dtype=LUT_F32):
+        nq = len(preds)
+        ids = torch.empty(nq, k, device=self.device, dtype=torch.int32)
+        dist = torch.empty(nq, k, device=self.device, dtype=torch.float32)
+        self.search_bounded_into(nq, pack_predicates(preds), lut, lut_dtype, lut_bounds, k, ids, dist)
+        return ids, dist
 
     def read_profile(self) -> dict:
         """Per-stage (total kernel ms, launches) since the last read."""
