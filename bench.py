@@ -13,7 +13,9 @@ the GPU (the paper's SIFT10M-style workload is not available here).
 attribute, or by (category, range attribute) where queries carry both.
 
 One step = one batch of queries from each selectivity bin, each batch going
-through select_codebook -> build_lut -> filtered_search.  `value` is queries
+through encode_predicates -> select_codebook -> build_lut ->
+filtered_search_bounded (the list scan with the coarse bound where the
+planner takes it: the 10% and 50% bins on c4; the interval scan elsewhere).  `value` is queries
 per second over the timed steps, inputs resident in HBM.  In the timed
 region only the scan kernel (the roofline kernel) is bracketed by HIP
 events; the per-stage breakdown comes from a short pass of its own in which
@@ -40,7 +42,7 @@ HBM_PEAK_GBPS = 8000.0
 METRIC = "filtered QPS at recall@10 per selectivity bin; ADC scan HBM GB/s vs peak"
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "adc_scan_c4_counters.txt")
 SCAN_SOURCES = [os.path.join(ROOT, "paper_2607_22922_amd", "csrc", f)
-                for f in ("k_scan.hip", "topk_device.h")]
+                for f in ("k_scan.hip", "k_listscan.hip", "k_coarse.hip", "topk_device.h")]
 
 
 def log(*a):
@@ -78,12 +80,14 @@ def read_counters():
         return None
 
 
-SCAN_KERNEL_C4 = "scan_kernel<48, 1, float>"
+SCAN_KERNEL_C4 = "scan_kernel<48, 1, float> and list_scan_kernel<48, float>"
 
 
 def is_timed_scan_c4(kernel_name):
-    """The timed scan kernel of the 10M-vector workload (not its read-counting build)."""
-    return "scan_kernel<48, 1, float" in kernel_name and "true>" not in kernel_name
+    """A timed scan kernel of the 10M-vector workload (the interval scan or
+    the list scan, not their read-counting builds)."""
+    return (("scan_kernel<48, 1, float" in kernel_name or "list_scan_kernel<48, float" in kernel_name)
+            and "true>" not in kernel_name)
 
 
 def summarize_counters(fetch_dir, write_dir, bins, steps, out_path, commands):
@@ -201,6 +205,7 @@ SCAN_WAVES = 8   # wavefronts per scan workgroup, each writing k partial keys pe
 
 # The benchmark run the scan's counter passes profile: the timed pass and the
 # stage pass only (3 launches per bin each), plus the calibration copy.
+COARSE_ITERS = 20
 COUNTER_RUN = ("--steps 3 --warmup 0 --plain-steps 0 --cpu-sample 0 --cpu-pool-queries 0 --recall-queries 0 "
                "--sdc-steps 0 --exact-steps 0 --host-steps 0 --no-lds-roof --copy-calibration")
 
@@ -352,6 +357,9 @@ def main():
                     help="batches per bin timed with queries and weights uploaded from pinned host memory "
                          "and results downloaded inside each batch (the PCIe-inclusive rate; 0 = skip)")
     ap.add_argument("--lut", choices=["f32", "f16"], default="f32")
+    ap.add_argument("--coarse", type=int, default=None,
+                    help="coarse centroids of the list scan (ifvs_build_coarse; 0 = plain interval scan only; "
+                         "default 2048 when D <= 128)")
     ap.add_argument("--no-recall-all", dest="recall_all", action="store_false",
                     help="skip recall over every query of every bin against ifvs_exact_search (needs the "
                          "exact-search leg)")
@@ -412,6 +420,16 @@ def main():
     for ix_ in (clus, plain):
         if ix_ is not None:
             ix_.load_encoder(w.enc)
+    if args.coarse is None:
+        args.coarse = 2048 if w.D <= 128 else 0
+    coarse_build_s = None
+    if args.coarse > 0:
+        torch.cuda.synchronize()
+        t_c = time.time()
+        clus.build_coarse(args.coarse, COARSE_ITERS)
+        coarse_build_s = time.time() - t_c
+        log(f"[bench] coarse quantizer ({args.coarse} centroids, {COARSE_ITERS} k-means iterations) and "
+            f"list order built in {coarse_build_s:.1f}s")
     n_batches = n_q // batch
     bins = w.bins
 
@@ -433,7 +451,12 @@ def main():
         idx.encode_predicates_into(batch, packed[s][b], wz)
         idx.select_codebook_into(q, packed[s][b], wz, alpha, wf)
         idx.build_lut_into(q, alpha, wf, lut_dt, lut)
-        idx.search_into(batch, packed[s][b], lut, lut_dt, k, ids[s], dist[s])
+        if idx is clus and args.coarse > 0:
+            # the tables' operands go with them: the search takes the list
+            # scan with the coarse bound where the planner picks it
+            idx.search_bounded_into(batch, packed[s][b], lut, lut_dt, alpha, wf, k, ids[s], dist[s])
+        else:
+            idx.search_into(batch, packed[s][b], lut, lut_dt, k, ids[s], dist[s])
 
     def timed_run(idx, steps, profile=2, warmup=None):
         """W warmup steps, then `steps` timed steps.  profile 2 brackets only
@@ -462,7 +485,7 @@ def main():
                 run_batch(idx, s, b)
                 e1.record(stream)
                 ev[s].append((b, e0, e1))
-            plans[s] = idx.last_plan()
+            plans[s] = dict(idx.last_plan(), list_scan=idx.last_coarse())
             prof_bin[s] = idx.read_profile()           # waits for this bin's kernels
         stop.record(stream)
         torch.cuda.synchronize()
@@ -498,8 +521,8 @@ def main():
     sorted_attr = torch.sort(w.attrs[0].long()).values if tile_bytes else None
     fabric = read_counters() if name == "c4" else None
     bins_out = {}
+    kind, bin_bytes, bin_lds = {}, {}, {}
     scan_bytes_total = useful_total = union_total = 0.0
-    lds_lookups_total = lds_secs_total = 0.0
     for s in bins:
         cache = {}
         for b, _ in per_bin[s]:
@@ -518,9 +541,22 @@ def main():
         b_bytes = sum(cache[b][0] for b, _ in per_bin[s]) / max(1, b_n)
         b_gbps = b_bytes / b_sec / 1e9
         b_union = sum(cache[b][2] for b, _ in per_bin[s]) / max(1, b_n)
+        is_list = bool(plans[s].get("list_scan"))
+        kind[s] = "list_scan_kernel" if is_list else "scan_kernel"
+        if is_list and s in read_hist:
+            # the list scan reads the code tiles and radii it sums (counted by
+            # its counting build), the tables and its item lists, and writes
+            # partial lists
+            tiles = read_hist[s][0] / max(1, b_n)
+            b_union = (tiles * ((w.M + 3) // 4 * 256 + 256) + batch * w.M * 256 * lut_entry
+                       + batch * plans[s]["splits"] * 8 * k * 8)
+            b_bytes = b_union
+        bin_bytes[s] = (b_union, b_bytes, b_n, b_ms)
         roofs = {"hbm": {"achieved_GBps": round(b_union / b_sec / 1e9, 1), "peak_GBps": HBM_PEAK_GBPS,
                          "frac": round(b_union / b_sec / 1e9 / HBM_PEAK_GBPS, 4),
                          "bytes_per_launch": b_union}}
+        if is_list and s in read_hist:
+            roofs["hbm"]["tiles_per_launch"] = read_hist[s][0] / max(1, b_n)
         if fabric is not None and str(s) in fabric["by_bin"]:
             fb = fabric["by_bin"][str(s)]
             roofs["hbm"]["fabric_bytes_per_launch"] = fb
@@ -528,8 +564,7 @@ def main():
         if s in read_hist:
             lk, lsec = lds_roof(read_hist[s], lds_rate)
             lk, lsec = lk / max(1, b_n), lsec / max(1, b_n)
-            lds_lookups_total += lk * b_n
-            lds_secs_total += lsec * b_n
+            bin_lds[s] = (lk * b_n, lsec * b_n)
             roofs["lds"] = {"lookups_per_launch": lk,
                             "achieved_GBps": round(4 * lk / b_sec / 1e9, 1),
                             "peak_GBps": round(4 * lk / lsec / 1e9, 1) if lsec > 0 else None,
@@ -545,17 +580,28 @@ def main():
                                                      round(float(np.percentile(ms, 90)), 4)],
                             "realized_selectivity": round(sel, 5),
                             "scan_ms": round(b_ms / max(1, b_n), 4),
+                            "scan_kernel": kind[s],
                             "scan_effective_GBps": round(b_gbps, 1),
                             "roofline": roofs,
                             "stage_ms_per_launch": {st: round(v[0] / max(1, v[1]), 4)
                                                    for st, v in stage_bin[s].items()},
                             "plan": plans[s]}
-    scan_ms, scan_launches = prof["scan"]
+    # The roofline of the dominant kernel: the scan kernel (interval or list)
+    # with the larger share of the scan time.
+    k_time = {}
+    for s in bins:
+        k_time[kind[s]] = k_time.get(kind[s], 0.0) + prof_bin[s]["scan"][0]
+    dom = max(k_time, key=k_time.get)
+    dom_bins = [s for s in bins if kind[s] == dom]
+    scan_ms = sum(prof_bin[s]["scan"][0] for s in dom_bins)
+    scan_launches = sum(prof_bin[s]["scan"][1] for s in dom_bins)
     scan_avg_ms = scan_ms / max(1, scan_launches)
-    bytes_per_launch = scan_bytes_total / max(1, scan_launches)
+    union_per_launch = sum(bin_bytes[s][0] * bin_bytes[s][2] for s in dom_bins) / max(1, scan_launches)
+    bytes_per_launch = sum(bin_bytes[s][1] * bin_bytes[s][2] for s in dom_bins) / max(1, scan_launches)
     effective = bytes_per_launch / (scan_avg_ms / 1e3) / 1e9
-    union_per_launch = union_total / max(1, scan_launches)
     hbm_achieved = union_per_launch / (scan_avg_ms / 1e3) / 1e9
+    lds_lookups_total = sum(bin_lds[s][0] for s in dom_bins if s in bin_lds)
+    lds_secs_total = sum(bin_lds[s][1] for s in dom_bins if s in bin_lds)
     if read_hist and lds_secs_total > 0:
         lds_frac = lds_secs_total / (scan_ms / 1e3)
         lds_achieved = 4 * lds_lookups_total / (scan_ms / 1e3) / 1e9
@@ -566,7 +612,7 @@ def main():
         roof_bound, achieved, peak = "lds", lds_achieved, lds_peak
     else:
         roof_bound, achieved, peak = "hbm", hbm_achieved, HBM_PEAK_GBPS
-    log(f"[bench] scan: {scan_launches} launches, avg {scan_avg_ms:.3f} ms, "
+    log(f"[bench] {dom} (bins {dom_bins}): {scan_launches} launches, avg {scan_avg_ms:.3f} ms, "
         f"{union_per_launch / 1e6:.1f} MB/launch from HBM at least -> {hbm_achieved:.0f} GB/s; "
         f"bound {roof_bound}: {achieved:.0f} of {peak:.0f} GB/s")
 
@@ -853,7 +899,9 @@ def main():
             torch.neg(src, out=dst)
         torch.cuda.synchronize()
 
-    traffic = fabric["mean"] if fabric is not None else None
+    traffic = None
+    if fabric is not None and all(str(s) in fabric["by_bin"] for s in dom_bins):
+        traffic = sum(fabric["by_bin"][str(s)] * prof_bin[s]["scan"][1] for s in dom_bins) / max(1, scan_launches)
     out = {
         "metric": METRIC,
         "value": qps,
@@ -868,6 +916,7 @@ def main():
         "dtype": args.lut,
         "data": "synthetic",
         "config": {"workload": f"{name}: {DESCRIPTIONS[name]}", "batch": batch, "k": k,
+                   "coarse_centroids": args.coarse, "coarse_build_s": coarse_build_s,
                    "bins": bins, "mode": "conditioned (predicate encoder -> w_z, memory bank, W)",
                    "layout": ("rows clustered by the range attribute" if cols == (0,)
                               else "rows clustered by (category, range attribute)"),
@@ -881,11 +930,16 @@ def main():
         "stage_ms_per_step": {st: round(v[0] / stage_steps, 4) for st, v in stage_prof.items()},
         "roofline": {"bound": roof_bound, "achieved": achieved, "peak": peak, "unit": "GB/s",
                      "frac": achieved / peak, "traffic": traffic,
-                     "kernel": "scan_kernel", "avg_launch_ms": scan_avg_ms,
+                     "kernel": dom, "bins": dom_bins, "avg_launch_ms": scan_avg_ms,
+                     "scan_ms_by_kernel": {kk: round(v / args.steps, 4) for kk, v in k_time.items()},
                      "hbm": {"achieved": hbm_achieved, "peak": HBM_PEAK_GBPS, "frac": hbm_achieved / HBM_PEAK_GBPS,
                              "bytes_per_launch": union_per_launch,
-                             "bytes_definition": "code tiles some query of the batch selects, read once, + tables "
-                                                 "+ partial lists written (the least a launch moves to and from HBM)",
+                             "bytes_definition": ("the code tiles and radii the list scan sums (its counting build "
+                                                  "counts them), + tables + partial lists written"
+                                                  if dom == "list_scan_kernel" else
+                                                  "code tiles some query of the batch selects, read once, + tables "
+                                                  "+ partial lists written (the least a launch moves to and from "
+                                                  "HBM)"),
                              "fabric_bytes_per_launch": traffic,
                              "fabric_definition": "rocprofv3 FETCH_SIZE x 2 + WRITE_SIZE (copy-kernel calibrated): "
                                                   "bytes the L2s request from the fabric, Infinity Cache hits "
@@ -897,7 +951,8 @@ def main():
                                             "mix of active lanes (ifvs_probe_lds_gather)"}
                              if lds_frac is not None else None),
                      "effective_GBps": effective,
-                     "effective_definition": ("code tiles overlapping each query's row interval + table + partial "
+                     "effective_definition": ("as bytes_per_launch" if dom == "list_scan_kernel" else
+                                              "code tiles overlapping each query's row interval + table + partial "
                                               "lists, counted once per query (rows several queries share are "
                                               "re-read, mostly from L2)" if tile_bytes else
                                               "codes of every (query, passing row) pair + table"),

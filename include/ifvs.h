@@ -241,34 +241,42 @@ ifvs_status ifvs_filtered_search_noalloc(ifvs_index* idx, int32_t nq, const ifvs
 /* ---- Coarse bound: exact pruning of the Rank stage ---------------------
  * The Rank stage (Section 2, stage 2) sums M table entries per candidate.  A
  * coarse quantizer of the index's reconstructions gives, per query, a lower
- * bound on every candidate's distance from one table lookup, so candidates
- * that cannot enter the top k are dropped before their sums.  With C_c the
- * candidate's coarse centroid (itself a vector of PQ codes) and the
- * triangle inequality in the weighted norm of w_f:
+ * bound on every candidate's distance, so candidates that cannot enter the
+ * top k are dropped without reading their codes.  With C_c the candidate's
+ * coarse centroid (itself a vector of PQ codes) and the triangle inequality
+ * in the weighted norm of w_f:
  *   sqrt(dist(v)) >= sqrt(dist(C_c)) - sqrt(max_j w_f[j]) * (r_v + delta)
  * where r_v = ||C_PQ(v) - C_PQ(C_c)|| (stored per row at build) and delta =
  * sqrt(sum over m of (2 max_c ||Delta[m][c]||)^2) bounds what the
  * conditioning Delta = alpha . W (Section 2, first display) adds between two
- * code vectors.  Every term carries a rounding allowance, so a dropped
- * candidate's computed distance exceeds the query's k-th: results are
- * identical, bit for bit, to ifvs_filtered_search. */
+ * code vectors.  The index keeps a second copy of its codes grouped by
+ * centroid and radius band (each centroid's rows split at its radius
+ * quantiles 0.5, 0.85 and 0.97), so a group's largest radius bounds all of
+ * its rows.  The list scan visits a query's groups in increasing order of
+ * that bound and stops at the first one whose bound exceeds the query's
+ * current k-th distance.  Every term carries a rounding allowance, so a
+ * dropped candidate's computed distance exceeds the query's k-th: results
+ * are identical, bit for bit, to ifvs_filtered_search. */
 
 /* ifvs_build_coarse -- k-means over the reconstructions of evenly spaced
  * rows (max(64 n_centroids, 65536) of them, at most n), starting from
  * n_centroids evenly spaced rows and running `iters` iterations (sums in a
  * fixed order: the build is deterministic); the centroids are then encoded
  * with C_PQ and every row gets its nearest encoded centroid and its
- * distance to it, rounded up to a bfloat16.  Synchronous; replaces any
- * earlier coarse quantizer.  Costs n * 4 bytes, n_centroids * ceil(m/4) * 4
- * and max_batch * (n_centroids + 8) * 4 bytes of device memory.
+ * distance to it, rounded up to a bfloat16; then the grouped copy of the
+ * codes.  Synchronous; replaces any earlier coarse quantizer.  Costs about
+ * n * (4 ceil(m/4) + 13) bytes of device memory (codes, radii, ids, row
+ * words and bands), a rank table of at most 64 MiB, and max_batch *
+ * n_centroids * 112 + max_batch * 1040 bytes of list-plan workspace.
  * Errors: IFVS_E_INVALID (n_centroids outside 1..4096 or above n, iters
  * outside 0..1000), IFVS_E_UNSUPPORTED (dim > 128), IFVS_E_STATE,
  * IFVS_E_NOMEM, IFVS_E_HIP. */
 ifvs_status ifvs_build_coarse(ifvs_index* idx, int32_t n_centroids, int32_t iters);
 
-/* ifvs_lut_bounds -- the two per-query factors of the coarse bound, for
- * tables built by ifvs_build_lut with the same alpha and wf (NULL and NULL
- * for ifvs_build_sdc_lut's tables):
+/* ifvs_lut_bounds -- the two per-query factors of the coarse bound (what
+ * ifvs_filtered_search_bounded computes inside), for tables built by
+ * ifvs_build_lut with the same alpha and wf (NULL and NULL for
+ * ifvs_build_sdc_lut's tables):
  *   bounds_out[2i]     >= sqrt(max_j wf_i[j]) (1 when wf is NULL; NaN, which
  *                         disables the bound for that query, when a weight
  *                         is negative or not finite)
@@ -283,19 +291,26 @@ ifvs_status ifvs_lut_bounds(ifvs_index* idx, int32_t nq, const float* alpha, con
                             void* stream);
 
 /* ifvs_filtered_search_bounded -- ifvs_filtered_search with the coarse
- * bound: lut_bounds (device [nq][2], from ifvs_lut_bounds for the same
- * tables) lets the scan drop candidates by the bound above.  Same results as
- * ifvs_filtered_search, bit for bit, whenever lut_bounds describes the
- * tables; bounds computed for other tables can drop true neighbours.  The
- * bound is used on one-query-per-tile scans of M = 16, 48 or 120 once
- * ifvs_build_coarse has run (IFVS_OPT_COARSE: automatic on interval batches
- * whose widest interval spans 1024 or more 64-row tiles); otherwise, or with
- * lut_bounds NULL, the call is ifvs_filtered_search.  With the bound, the
- * call adds one kernel that sums each query's table over the centroids'
- * codes.  Errors: as ifvs_filtered_search. */
+ * bound.  alpha and wf are the operands the tables were built with
+ * (ifvs_build_lut's; either may be NULL, and both are NULL for
+ * ifvs_build_sdc_lut's tables): when the list scan runs, the call computes
+ * the bound's factors from them as ifvs_lut_bounds does and drops
+ * candidates by the bound.  Same results as ifvs_filtered_search, bit for
+ * bit, whenever alpha and wf are the tables' operands; others can drop true
+ * neighbours.  The list scan runs once ifvs_build_coarse has run, when every
+ * query's selection is a run of rows of the index's layout (no clause
+ * tested row by row), M is 16, 48 or 120, and its workspace holds the batch
+ * (IFVS_OPT_COARSE: automatic for batches whose widest interval spans 8192
+ * or more 64-row tiles); otherwise the call is ifvs_filtered_search.  The
+ * list scan adds the bound kernels and one planning kernel per call (one
+ * workgroup per query sorts the query's groups by their bound).
+ * IFVS_OPT_SPLITS sets its workgroups per query (at most 16).
+ * Errors: as ifvs_filtered_search, plus IFVS_E_INVALID for alpha given on an
+ * index without a memory bank. */
 ifvs_status ifvs_filtered_search_bounded(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
-                                         const void* lut, int32_t lut_dtype, const float* lut_bounds, int32_t k,
-                                         int32_t* ids_out, float* dist_out, uint32_t* bitmap_out, void* stream);
+                                         const void* lut, int32_t lut_dtype, const float* alpha, const float* wf,
+                                         int32_t k, int32_t* ids_out, float* dist_out, uint32_t* bitmap_out,
+                                         void* stream);
 
 /* ifvs_read_coarse -- the coarse quantizer, for inspection and tests
  * (synchronous; every output may be NULL): *n_centroids_out; assign_out
@@ -511,17 +526,16 @@ ifvs_status ifvs_encode_predicates(ifvs_index* idx, int32_t nq, const ifvs_predi
 #define IFVS_OPT_EXACT_PLAN 10    /* ifvs_exact_search: 0 automatic (matrix-core screening when
                                      the batch's queries share rows), 1 score every selected row
                                      exactly, 2 always screen first                           */
-#define IFVS_OPT_COARSE 13       /* ifvs_filtered_search_bounded: 0 automatic (interval batches
-                                     whose widest interval spans 1024 or more 64-row tiles),
-                                     1 never, 2 whenever the plan has a coarse build (one query
-                                     per tile, M of 16, 48 or 120, LDS to spare)             */
+#define IFVS_OPT_COARSE 13       /* ifvs_filtered_search_bounded: 0 automatic (the list scan for
+                                     batches whose widest interval spans 8192 or more 64-row
+                                     tiles), 1 never, 2 whenever the batch allows it          */
 #define IFVS_OPT_COUNT_READS 12  /* measurement only: 1 = scans run a build of the scan kernel
                                      that also counts its table reads (one per subspace and
                                      wavefront instruction, and one per coarse-bound lookup)
-                                     by the number of active lanes, read
-                                     back with ifvs_read_scan_reads; needs one query per tile
-                                     and M of 16, 48 or 120 (else the search fails with
-                                     IFVS_E_UNSUPPORTED).  Results are unchanged; the counting
+                                     by the number of active lanes, and the code tiles it sums,
+                                     read back with ifvs_read_scan_reads; needs one query per
+                                     tile and M of 16, 48 or 120, or the list scan (else the
+                                     search fails with IFVS_E_UNSUPPORTED).  Results are unchanged; the counting
                                      adds LDS atomics, so it is not the build to time.  0 = off */
 ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value);
 
@@ -539,7 +553,9 @@ ifvs_status ifvs_read_profile(ifvs_index* idx, double* ms_out, int64_t* launches
 /* ifvs_read_scan_reads -- with IFVS_OPT_COUNT_READS on: hist_out[n] (65
  * entries) = table reads the scans issued with n of a wavefront's 64 lanes
  * active (a read is one LDS instruction of a wavefront; it fetches n table
- * entries), summed over the scans since the last call, which it then clears.
+ * entries), for n = 1..64, and hist_out[0] = the 64-row code tiles the
+ * scans summed, both summed over the scans since the last call, which it
+ * then clears.
  * Waits for `stream`.  The LDS cost of the Rank stage's distance-table
  * lookups (Section 2, stage 2) follows from it and ifvs_probe_lds_gather.
  * All zero when counting was never on.

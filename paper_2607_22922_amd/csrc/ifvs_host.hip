@@ -55,9 +55,11 @@ bool forced_alloc_failure() {
 }
 
 constexpr int kStagingSlots = 8;
-// Automatic coarse bound: interval batches whose widest interval spans at
-// least this many 64-row tiles.
-constexpr int64_t kCoarseAutoTiles = 1024;
+// Automatic list scan: batches whose widest interval spans at least this
+// many 64-row tiles (measured on 10M x 48-byte codes, 256 queries: at 10%
+// selectivity, 15.6K tiles, the list scan and its plan take 0.74 ms against
+// the interval scan's 1.16; at 1%, 1.6K tiles, 1.2 ms against 0.25).
+constexpr int64_t kCoarseAutoTiles = 8192;
 // Radius quantiles that split each coarse list into its kBands bands.
 constexpr float kBandQuantiles[kBands - 1] = {0.5f, 0.85f, 0.97f};
 
@@ -185,6 +187,8 @@ struct ifvs_index {
   int32_t* qorder_dev = nullptr; // [max_batch]
   int64_t* iv_dev = nullptr;     // [max_batch][2]
   uint64_t* gthr_dev = nullptr;  // [max_batch] shared scan thresholds
+  float* bound_parts = nullptr;  // [max_batch][2][m] coarse-bound partial maxima
+  float* bounds_ws = nullptr;    // [max_batch][2] coarse-bound factors of a bounded search
   int32_t* slot_order_dev = nullptr;  // [slot_order_cap] chunk-grid scan dispatch order
   int64_t slot_order_cap = 0;
   DevPred* staging[kStagingSlots] = {};   // pinned: [max_batch] DevPred + [max_batch] int32
@@ -302,6 +306,7 @@ struct ifvs_index {
                     static_cast<void*>(perm), static_cast<void*>(bank), static_cast<void*>(W),
                     static_cast<void*>(preds_dev), static_cast<void*>(qorder_dev),
                     static_cast<void*>(iv_dev), static_cast<void*>(gthr_dev), static_cast<void*>(bitmap),
+                    static_cast<void*>(bound_parts), static_cast<void*>(bounds_ws),
                     static_cast<void*>(slot_order_dev),
                     static_cast<void*>(counts), static_cast<void*>(count_parts), static_cast<void*>(vstart),
                     static_cast<void*>(partials), static_cast<void*>(codes_rm),
@@ -972,6 +977,10 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
   if ((st = dev_alloc(&idx->qorder_dev, d.max_batch, "query order")) != IFVS_OK) return bail(st);
   if ((st = dev_alloc(&idx->iv_dev, 2 * static_cast<size_t>(d.max_batch), "row intervals")) != IFVS_OK)
     return bail(st);
+  if ((st = dev_alloc(&idx->bound_parts, static_cast<size_t>(d.max_batch) * 2 * d.m, "bound workspace")) != IFVS_OK)
+    return bail(st);
+  if ((st = dev_alloc(&idx->bounds_ws, static_cast<size_t>(d.max_batch) * 2, "bound workspace")) != IFVS_OK)
+    return bail(st);
   if ((st = dev_alloc(&idx->gthr_dev, static_cast<size_t>(d.max_batch), "scan thresholds")) != IFVS_OK)
     return bail(st);
   // Room for the dispatch order of a chunk-grid scan: 8 XCD runs of query
@@ -1149,9 +1158,12 @@ namespace {
 // workspace is carved from the static array of the index's device instead of
 // the index's own workspace (no gather scan then: every query takes the tiled
 // scan, with the same results).
+// bounded: the caller gave the alpha and w_f its tables were built with
+// (either may be null), so the list scan may run with the coarse bound.
 ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds, const void* lut,
-                        int32_t lut_dtype, const float* lut_bounds, int32_t k, int32_t* ids_out, float* dist_out,
-                        uint32_t* bitmap_out, void* stream, bool static_scratch) {
+                        int32_t lut_dtype, bool bounded, const float* alpha, const float* wf, int32_t k,
+                        int32_t* ids_out, float* dist_out, uint32_t* bitmap_out, void* stream,
+                        bool static_scratch) {
   if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
   if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
   if (lut_dtype != IFVS_LUT_F32 && lut_dtype != IFVS_LUT_F16) return fail(IFVS_E_INVALID, "unknown lut_dtype");
@@ -1159,6 +1171,7 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     return fail(IFVS_E_INVALID, "k = " + std::to_string(k) + " outside 1.." + std::to_string(idx->max_k) + " (max_k)");
   if (nq == 0) return IFVS_OK;
   if (!lut || !ids_out || !dist_out) return fail(IFVS_E_INVALID, "lut, ids_out or dist_out is NULL");
+  if (alpha && idx->bank_rows == 0) return fail(IFVS_E_INVALID, "alpha given but the index has no memory bank");
   if (reinterpret_cast<uintptr_t>(lut) % 16 != 0) return fail(IFVS_E_INVALID, "lut must be 16-byte aligned");
   ScanPlan probe{};
   if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, false, 0, size_t{1} << 40, &probe); st != IFVS_OK) return st;
@@ -1187,7 +1200,7 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   ScanPlan plan{};
   if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, interval_batch, span, ws.partial_keys, &plan); st != IFVS_OK)
     return st;
-  // List scan (coarse bound): when the caller passed the tables' bounds, a
+  // List scan (coarse bound): when the caller passed the tables' operands, a
   // coarse build exists and every query's selection is its row interval
   // (no residual clauses); automatic for batches whose widest interval spans
   // at least kCoarseAutoTiles 64-row tiles.
@@ -1195,13 +1208,13 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   const int list_splits = std::min(kListSlots / (2 * kScanWaves),
                                    idx->opt_splits > 0 ? idx->opt_splits : std::max(1, (1024 + nq - 1) / nq));
   const bool list_mode =
-      lut_bounds && cl.words && idx->opt_coarse != 1 && !static_scratch && !need_bitmap &&
-      !idx->opt_count_reads && list_scan_supported(idx->m, lut_dtype) &&
+      bounded && cl.words && idx->opt_coarse != 1 && !static_scratch && !need_bitmap &&
+      list_scan_supported(idx->m, lut_dtype) &&
       list_plan_lds_bytes(idx->m, lut_dtype, cl.C) <= size_t{kLdsBudget} &&
       list_scan_lds_bytes(idx->m, lut_dtype, pool_stride_for(k)) <= size_t{kLdsBudget} &&
       static_cast<size_t>(nq) * list_splits * kScanWaves * k <= ws.partial_keys &&
       (idx->opt_coarse == 2 || span >= kCoarseAutoTiles);
-  if (idx->opt_count_reads &&
+  if (idx->opt_count_reads && !list_mode &&
       (!scan_can_count(idx->m, plan.qtile, lut_dtype) || plan.lds_bytes + kLookupHistBytes > size_t{kLdsBudget}))
     return fail(IFVS_E_UNSUPPORTED, "IFVS_OPT_COUNT_READS: no read-counting scan for this plan (it needs one query "
                                     "per tile, M of 16, 48 or 120, and 272 bytes of LDS to spare)");
@@ -1225,6 +1238,9 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
                                ws.slot_order, ordered ? n_order : 0, s));
   if (ifvs_status st = release_slot(idx, slot, s); st != IFVS_OK) return st;
   if (list_mode) {
+    IFVS_LAUNCH(idx, kStCoarse, s, "launching table bound kernels",
+                launch_lut_bounds(alpha, wf, idx->cpq, idx->W, nq, idx->m, idx->r, idx->dsub, idx->bound_parts,
+                                  idx->bounds_ws, s));
     ListPlanArgs pa{};
     pa.lut = lut;
     pa.m = idx->m;
@@ -1234,7 +1250,7 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     pa.C = cl.C;
     pa.n_sub = cl.C * kBands;
     pa.Sp = list_plan_width(cl.C);
-    pa.bounds = lut_bounds;
+    pa.bounds = idx->bounds_ws;
     pa.iv = ws.iv;
     pa.cnt_f = cl.cnt_f;
     pa.f_shift = cl.f_shift;
@@ -1279,6 +1295,7 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     sa.partials = ws.partials;
     sa.gthr = ws.gthr;
     sa.slots = cl.slots;
+    sa.lookup_hist = idx->opt_count_reads ? idx->read_hist : nullptr;
     IFVS_LAUNCH(idx, kStScan, s, "launching list scan kernel", launch_list_scan(sa, lut_dtype, s));
     IFVS_LAUNCH(idx, kStMerge, s, "launching top-k merge kernel",
                 launch_topk_merge(ws.partials, nq, static_cast<int64_t>(list_splits) * kScanWaves * k, k, ws.iv, 0,
@@ -1385,19 +1402,23 @@ extern "C" {
 ifvs_status ifvs_filtered_search(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
                                  const void* lut, int32_t lut_dtype, int32_t k, int32_t* ids_out,
                                  float* dist_out, uint32_t* bitmap_out, void* stream) {
-  return search_impl(idx, nq, preds, lut, lut_dtype, nullptr, k, ids_out, dist_out, bitmap_out, stream, false);
+  return search_impl(idx, nq, preds, lut, lut_dtype, false, nullptr, nullptr, k, ids_out, dist_out, bitmap_out,
+                     stream, false);
 }
 
 ifvs_status ifvs_filtered_search_bounded(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
-                                         const void* lut, int32_t lut_dtype, const float* lut_bounds, int32_t k,
-                                         int32_t* ids_out, float* dist_out, uint32_t* bitmap_out, void* stream) {
-  return search_impl(idx, nq, preds, lut, lut_dtype, lut_bounds, k, ids_out, dist_out, bitmap_out, stream, false);
+                                         const void* lut, int32_t lut_dtype, const float* alpha, const float* wf,
+                                         int32_t k, int32_t* ids_out, float* dist_out, uint32_t* bitmap_out,
+                                         void* stream) {
+  return search_impl(idx, nq, preds, lut, lut_dtype, true, alpha, wf, k, ids_out, dist_out, bitmap_out, stream,
+                     false);
 }
 
 ifvs_status ifvs_filtered_search_noalloc(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,
                                          const void* lut, int32_t lut_dtype, int32_t k, int32_t* ids_out,
                                          float* dist_out, uint32_t* bitmap_out, void* stream) {
-  return search_impl(idx, nq, preds, lut, lut_dtype, nullptr, k, ids_out, dist_out, bitmap_out, stream, true);
+  return search_impl(idx, nq, preds, lut, lut_dtype, false, nullptr, nullptr, k, ids_out, dist_out, bitmap_out,
+                     stream, true);
 }
 
 }  // extern "C"
@@ -2074,7 +2095,8 @@ ifvs_status ifvs_lut_bounds(ifvs_index* idx, int32_t nq, const float* alpha, con
   hipStream_t s = static_cast<hipStream_t>(stream);
   IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
   IFVS_LAUNCH(idx, kStCoarse, s, "launching table bounds kernel",
-              launch_lut_bounds(alpha, wf, idx->cpq, idx->W, nq, idx->m, idx->r, idx->dsub, bounds_out, s));
+              launch_lut_bounds(alpha, wf, idx->cpq, idx->W, nq, idx->m, idx->r, idx->dsub, idx->bound_parts,
+                                bounds_out, s));
   return IFVS_OK;
 }
 

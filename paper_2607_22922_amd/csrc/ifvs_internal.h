@@ -250,8 +250,11 @@ hipError_t launch_coarse_encode(const float* cent, int C, int m, int mw, int dsu
                                 float* chat, hipStream_t s);
 hipError_t launch_coarse_rows(const uint32_t* codes_t, int64_t n, int64_t n_pad, int m, int mw, int dsub,
                               const float* cpq, const float* chat, int C, uint32_t* words, hipStream_t s);
+// Per query: bounds [nq][2] = {sqrt(max w) widened, delta widened} of tables
+// built with alpha (null: no conditioning) and wf (null: w = 1); parts is a
+// [nq][2][m] workspace.
 hipError_t launch_lut_bounds(const float* alpha, const float* wf, const float* cpq, const float* W, int nq, int m,
-                             int r, int dsub, float* bounds, hipStream_t s);
+                             int r, int dsub, float* parts, float* bounds, hipStream_t s);
 // List order: rows grouped by sub-list s = (centroid c, radius band b),
 // s = c * kBands + b, positions [sub_off[s], sub_off[s+1]), each sub-list in
 // layout order.  Code tiles, radii and original ids gathered through
@@ -314,6 +317,7 @@ struct ListScanArgs {
   uint64_t* partials;       // [positions][splits][kScanWaves][k]
   uint64_t* gthr;           // [nq] shared thresholds, all ones before the scan
   uint32_t* slots;          // [nq][kListSlots] union-bound slots, all ones before the scan (list plan)
+  unsigned long long* lookup_hist;  // [65] non-null: the counting build (table reads by lanes, [0] tiles)
 };
 constexpr int kListSlots = 2 * kScanWaves * 16;   // two per wavefront of at most 16 workgroups per query
 bool list_scan_supported(int m, int lut_dtype);

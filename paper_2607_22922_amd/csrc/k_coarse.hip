@@ -48,16 +48,6 @@ __device__ __forceinline__ int code_at(const uint32_t* codes_t, int mw, int64_t 
 __device__ __forceinline__ float widen(float v) { return v; }
 __device__ __forceinline__ float widen(__half v) { return __half2float(v); }
 
-// Maximum over the wavefront; NaN in any lane gives NaN.
-__device__ __forceinline__ float wave_max_nan(float v) {
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const float u = __shfl_xor(v, o, 64);
-    v = (u != u || v != v) ? __builtin_nanf("") : fmaxf(v, u);
-  }
-  return v;
-}
-
 // X[i][j] = reconstruction of physical row i * stride, dimension j.
 __global__ __launch_bounds__(256) void coarse_sample_kernel(const uint32_t* __restrict__ codes_t, int mw, int dsub,
                                                             int D, const float* __restrict__ cpq, int64_t S,
@@ -211,66 +201,102 @@ __global__ __launch_bounds__(256) void coarse_rows_kernel(const uint32_t* __rest
   }
 }
 
-// Per query q: bounds[2q] = sqrt(max_j w_f[j]) widened by 2^-19 (NaN when a
-// weight is negative or not finite: no pruning for that query), bounds[2q+1]
-// = delta widened by `grow`.  The conditioned codewords are recomputed with
-// exactly the table kernel's operations (so Delta below is the shift the
-// tables saw); wavefront w takes subspaces w, w + 4, ..., a lane four
-// codewords.
-__global__ __launch_bounds__(256) void lut_bounds_kernel(const float* __restrict__ alpha, const float* __restrict__ wf,
-                                                         const float* __restrict__ cpq, const float* __restrict__ W,
-                                                         int M, int r, int dsub, int D, float grow,
-                                                         float* __restrict__ bounds) {
-  __shared__ float s_w[4], s_d[4];
-  const int q = blockIdx.x;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  float wmax = 1.0f;
-  bool ok = true;
-  if (wf) {
-    wmax = 0.0f;
-    for (int j = threadIdx.x; j < D; j += 256) {
-      const float v = wf[static_cast<size_t>(q) * D + j];
-      ok = ok && v >= 0.0f && v <= FLT_MAX;
-      wmax = fmaxf(wmax, v);
+// Bounds of the coarse bound, two kernels.  Partial (one workgroup per
+// subspace m and chunk of kBoundQueries queries, one thread per codeword c,
+// the operands of the table build in registers): per query,
+//   parts[q][0][m] = max_c ||C_iFVS[m][c] - C_PQ[m][c]||^2, the conditioned
+//                    codeword recomputed with exactly the table kernel's
+//                    operations (so this is the shift the tables saw);
+//   parts[q][1][m] = max_j w_f[m*d + j] (NaN when a weight of the subspace is
+//                    negative or not finite; 1 without weights).
+// Final (one thread per query): bounds[q] = {sqrt(max_m parts[q][1][m])
+// widened by 2^-19, sqrt(sum_m 4 parts[q][0][m]) * grow}.
+constexpr int kBoundQueries = 16;
+
+__device__ __forceinline__ float nan_max(float a, float b) {
+  return (a != a || b != b) ? __builtin_nanf("") : fmaxf(a, b);
+}
+
+template <int DSUB, int R>
+__global__ __launch_bounds__(256) void bound_parts_kernel(const float* __restrict__ alpha, const float* __restrict__ wf,
+                                                          const float* __restrict__ cpq, const float* __restrict__ W,
+                                                          int M, int dsub_rt, int r_rt, int nq,
+                                                          float* __restrict__ parts) {
+  constexpr bool kFixed = DSUB > 0;
+  const int dsub = kFixed ? DSUB : dsub_rt;
+  const int r = kFixed ? R : r_rt;
+  const int m = blockIdx.x;
+  const int c = threadIdx.x;
+  const int lane = c & 63, wave = c >> 6;
+  __shared__ float s_red[4];
+  float creg[kFixed ? DSUB : 1];
+  float wreg[kFixed ? R : 1][kFixed ? DSUB : 1];
+  if constexpr (kFixed) {
+#pragma unroll
+    for (int j = 0; j < DSUB; ++j) creg[j] = cpq[(static_cast<size_t>(m) * kKsub + c) * DSUB + j];
+    if (alpha) {
+#pragma unroll
+      for (int t = 0; t < R; ++t)
+#pragma unroll
+        for (int j = 0; j < DSUB; ++j) wreg[t][j] = W[((static_cast<size_t>(m) * R + t) * kKsub + c) * DSUB + j];
     }
   }
-  wmax = wave_max_nan(wmax);
-  const bool bad = __ballot(!ok) != 0;
-  float d2 = 0.0f;
-  if (alpha) {
-    for (int m = wave; m < M; m += 4) {
-      float mx = 0.0f;
-      for (int c = lane; c < kKsub; c += 64) {
-        float n2 = 0.0f;
-        for (int j = 0; j < dsub; ++j) {
-          float delta = 0.0f;
+  const int q_begin = blockIdx.y * kBoundQueries;
+  const int q_end = min(nq, q_begin + kBoundQueries);
+  for (int q = q_begin; q < q_end; ++q) {
+    float n2 = 0.0f;
+    if (alpha) {
+      const float* aq = alpha + (static_cast<size_t>(q) * M + m) * r;
+      for (int j = 0; j < dsub; ++j) {
+        float delta = 0.0f;
+        float base;
+        if constexpr (kFixed) {
+#pragma unroll
+          for (int t = 0; t < R; ++t) delta = __fadd_rn(delta, __fmul_rn(aq[t], wreg[t][j]));
+          base = creg[j];
+        } else {
           for (int t = 0; t < r; ++t)
-            delta = __fadd_rn(delta, __fmul_rn(alpha[(static_cast<size_t>(q) * M + m) * r + t],
-                                               W[((static_cast<size_t>(m) * r + t) * kKsub + c) * dsub + j]));
-          const float base = cpq[(static_cast<size_t>(m) * kKsub + c) * dsub + j];
-          const float e = __fsub_rn(__fadd_rn(base, delta), base);
-          n2 = __fadd_rn(n2, __fmul_rn(e, e));
+            delta = __fadd_rn(delta, __fmul_rn(aq[t], W[((static_cast<size_t>(m) * r + t) * kKsub + c) * dsub + j]));
+          base = cpq[(static_cast<size_t>(m) * kKsub + c) * dsub + j];
         }
-        mx = (n2 != n2 || mx != mx) ? __builtin_nanf("") : fmaxf(mx, n2);
+        const float e = __fsub_rn(__fadd_rn(base, delta), base);
+        n2 = __fadd_rn(n2, __fmul_rn(e, e));
       }
-      mx = wave_max_nan(mx);
-      d2 = __fadd_rn(d2, __fmul_rn(4.0f, mx));
     }
-  }
-  if (lane == 0) {
-    s_w[wave] = bad ? __builtin_nanf("") : wmax;
-    s_d[wave] = d2;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    float wm = s_w[0], dd = s_d[0];
-    for (int i = 1; i < 4; ++i) {
-      wm = (wm != wm || s_w[i] != s_w[i]) ? __builtin_nanf("") : fmaxf(wm, s_w[i]);
-      dd = __fadd_rn(dd, s_d[i]);
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) n2 = nan_max(n2, __shfl_xor(n2, o, 64));
+    if (lane == 0) s_red[wave] = n2;
+    __syncthreads();
+    if (c == 0) {
+      float mx = nan_max(nan_max(s_red[0], s_red[1]), nan_max(s_red[2], s_red[3]));
+      float wm = 1.0f;
+      if (wf) {
+        wm = 0.0f;
+        for (int j = 0; j < dsub; ++j) {
+          const float v = wf[static_cast<size_t>(q) * M * dsub + m * dsub + j];
+          wm = (v >= 0.0f && v <= FLT_MAX && wm == wm) ? fmaxf(wm, v) : __builtin_nanf("");
+        }
+      }
+      parts[(static_cast<size_t>(q) * 2) * M + m] = mx;
+      parts[(static_cast<size_t>(q) * 2 + 1) * M + m] = wm;
     }
-    bounds[2 * q] = __fmul_rn(sqrtf(wm), 1.0f + 0x1p-19f);
-    bounds[2 * q + 1] = __fmul_rn(sqrtf(dd), grow);
+    __syncthreads();
   }
+}
+
+__global__ __launch_bounds__(256) void bound_final_kernel(const float* __restrict__ parts, int M, int nq, float grow,
+                                                          float* __restrict__ bounds) {
+  const int q = blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= nq) return;
+  const float* pd = parts + static_cast<size_t>(q) * 2 * M;
+  const float* pw = pd + M;
+  float d2 = 0.0f, wm = 0.0f;
+  for (int m = 0; m < M; ++m) {
+    d2 = __fadd_rn(d2, __fmul_rn(4.0f, pd[m]));
+    wm = nan_max(wm, pw[m]);
+  }
+  bounds[2 * q] = __fmul_rn(sqrtf(wm), 1.0f + 0x1p-19f);
+  bounds[2 * q + 1] = __fmul_rn(sqrtf(d2), grow);
 }
 
 // List order (rows grouped by coarse centroid, each list in layout order):
@@ -514,10 +540,19 @@ hipError_t launch_coarse_rows(const uint32_t* codes_t, int64_t n, int64_t n_pad,
 }
 
 hipError_t launch_lut_bounds(const float* alpha, const float* wf, const float* cpq, const float* W, int nq, int m,
-                             int r, int dsub, float* bounds, hipStream_t s) {
+                             int r, int dsub, float* parts, float* bounds, hipStream_t s) {
   if (nq <= 0) return hipSuccess;
+  const dim3 g(static_cast<unsigned>(m), static_cast<unsigned>((nq + kBoundQueries - 1) / kBoundQueries));
+  if (dsub == 2 && r == 8)
+    bound_parts_kernel<2, 8><<<g, 256, 0, s>>>(alpha, wf, cpq, W, m, dsub, r, nq, parts);
+  else if (dsub == 8 && r == 8)
+    bound_parts_kernel<8, 8><<<g, 256, 0, s>>>(alpha, wf, cpq, W, m, dsub, r, nq, parts);
+  else
+    bound_parts_kernel<0, 0><<<g, 256, 0, s>>>(alpha, wf, cpq, W, m, dsub, r, nq, parts);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   const float grow = 1.0f + 2.0f * static_cast<float>(dsub + m + 8) * 0x1p-24f + 0x1p-20f;
-  lut_bounds_kernel<<<static_cast<unsigned>(nq), 256, 0, s>>>(alpha, wf, cpq, W, m, r, dsub, m * dsub, grow, bounds);
+  bound_final_kernel<<<static_cast<unsigned>((nq + 255) / 256), 256, 0, s>>>(parts, m, nq, grow, bounds);
   return hipGetLastError();
 }
 

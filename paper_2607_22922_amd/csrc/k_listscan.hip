@@ -59,7 +59,9 @@ constexpr int list_waves_per_eu() {
   return MT == 120 ? 2 : 4;
 }
 
-template <int MT, typename LutT>
+// kCount: a measurement build that also counts the table reads by active
+// lanes (entries 1..64 of a.lookup_hist) and the code tiles summed (entry 0).
+template <int MT, typename LutT, bool kCount = false>
 __global__ __launch_bounds__(kScanWaves * 64) __attribute__((amdgpu_waves_per_eu(list_waves_per_eu<MT, LutT>())))
 void list_scan_kernel(const ListScanArgs a) {
   constexpr int kMW = (MT + 3) / 4;
@@ -72,6 +74,7 @@ void list_scan_kernel(const ListScanArgs a) {
   uint64_t* pools = reinterpret_cast<uint64_t*>(smem);
   unsigned long long* s_thr = reinterpret_cast<unsigned long long*>(pools + kScanWaves * a.pool_stride);
   uint32_t* s_bad = reinterpret_cast<uint32_t*>(s_thr + 1);
+  uint32_t* s_hist = s_bad + kScanWaves;   // [65], counting build only
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -98,6 +101,9 @@ void list_scan_kernel(const ListScanArgs a) {
   const bool wave_bad = __ballot(bad) != 0;
   if (lane == 0) s_bad[wave] = wave_bad ? 1u : 0u;
   if (threadIdx.x == 0) *s_thr = kNoKey;
+  if constexpr (kCount) {
+    if (threadIdx.x < 65) s_hist[threadIdx.x] = 0;
+  }
   __syncthreads();
   bool monotone = true;
 #pragma unroll
@@ -268,6 +274,9 @@ void list_scan_kernel(const ListScanArgs a) {
   };
   auto sum_tile = [&](int t, uint64_t mask, float sdc, const uint32_t (&w)[kMW], float rad) {
     refresh();
+    if constexpr (kCount) {
+      if (lane == 0) atomicAdd(&s_hist[0], 1u);
+    }
     bool live = __builtin_amdgcn_inverse_ballot_w64(mask);
     if (monotone && live) {
       const float lb = __fsub_rn(sdc, __fmul_rn(__fadd_rn(rad, delta), sw));
@@ -281,6 +290,10 @@ void list_scan_kernel(const ListScanArgs a) {
       for (int u = 0; u < kGroup; ++u) {
         const int m = gr * kGroup + u;
         addr[u] = m * kKsub + static_cast<int>((w[m >> 2] >> (8 * (m & 3))) & 0xFFu);
+      }
+      if constexpr (kCount) {
+        const uint64_t lanes = __ballot(live);
+        if (lanes != 0 && lane == 0) atomicAdd(&s_hist[__popcll(lanes)], static_cast<uint32_t>(kGroup));
       }
       if (live) {
         LutT v[kGroup];
@@ -318,37 +331,47 @@ void list_scan_kernel(const ListScanArgs a) {
   pool_compact(pool, cnt, thr, k, a.kpl, a.ids);
   uint64_t* dst = a.partials + ((static_cast<size_t>(pos) * a.splits + split) * kScanWaves + wave) * k;
   for (int e = lane; e < k; e += 64) dst[e] = pool[e];
+  if constexpr (kCount) {
+    __syncthreads();
+    if (threadIdx.x < 65 && s_hist[threadIdx.x] != 0)
+      atomicAdd(&a.lookup_hist[threadIdx.x], static_cast<unsigned long long>(s_hist[threadIdx.x]));
+  }
 }
 
 template <int MT>
-const void* pick_list_t(int lut_dtype) {
+const void* pick_list_t(int lut_dtype, bool count) {
+  if (count)
+    return lut_dtype == 1 ? reinterpret_cast<const void*>(&list_scan_kernel<MT, __half, true>)
+                          : reinterpret_cast<const void*>(&list_scan_kernel<MT, float, true>);
   return lut_dtype == 1 ? reinterpret_cast<const void*>(&list_scan_kernel<MT, __half>)
                         : reinterpret_cast<const void*>(&list_scan_kernel<MT, float>);
 }
 
-const void* pick_list(int m, int lut_dtype) {
+const void* pick_list(int m, int lut_dtype, bool count) {
   switch (m) {
-    case 16: return pick_list_t<16>(lut_dtype);
-    case 48: return pick_list_t<48>(lut_dtype);
-    case 120: return pick_list_t<120>(lut_dtype);
+    case 16: return pick_list_t<16>(lut_dtype, count);
+    case 48: return pick_list_t<48>(lut_dtype, count);
+    case 120: return pick_list_t<120>(lut_dtype, count);
     default: return nullptr;
   }
 }
 
 size_t list_dyn_bytes(int pool_stride) {
-  return static_cast<size_t>(kScanWaves) * pool_stride * sizeof(uint64_t) + 8 + 4 * kScanWaves;
+  // pools, the workgroup threshold, monotonicity flags, the counting build's
+  // histogram
+  return static_cast<size_t>(kScanWaves) * pool_stride * sizeof(uint64_t) + 8 + 4 * kScanWaves + kLookupHistBytes;
 }
 
 }  // namespace
 
-bool list_scan_supported(int m, int lut_dtype) { return pick_list(m, lut_dtype) != nullptr; }
+bool list_scan_supported(int m, int lut_dtype) { return pick_list(m, lut_dtype, false) != nullptr; }
 
 size_t list_scan_lds_bytes(int m, int lut_dtype, int pool_stride) {
   return static_cast<size_t>(m) * kKsub * (lut_dtype == 1 ? 2 : 4) + list_dyn_bytes(pool_stride);
 }
 
 hipError_t launch_list_scan(const ListScanArgs& a, int lut_dtype, hipStream_t s) {
-  const void* fn = pick_list(a.m, lut_dtype);
+  const void* fn = pick_list(a.m, lut_dtype, a.lookup_hist != nullptr);
   if (!fn || a.splits < 1) return hipErrorInvalidValue;
   if (a.nq <= 0) return hipSuccess;
   const size_t dyn = list_dyn_bytes(a.pool_stride);

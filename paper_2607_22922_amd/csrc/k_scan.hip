@@ -109,8 +109,9 @@ constexpr int scan_depth() {
 }
 
 // kCount: the same scan, also counting its table reads by active lanes in
-// an LDS histogram flushed to a.lookup_hist (a measurement build: the
-// counting adds LDS atomics, so it is never the timed kernel).
+// an LDS histogram flushed to a.lookup_hist, and in entry 0 the code tiles
+// it sums (a measurement build: the counting adds LDS atomics, so it is
+// never the timed kernel).
 template <int MT, int QT, typename LutT, bool kCount = false>
 __global__ __launch_bounds__(kScanWaves * 64) __attribute__((amdgpu_waves_per_eu(scan_waves_per_eu<MT, QT, LutT>())))
 void scan_kernel(const ScanArgs a) {
@@ -646,6 +647,9 @@ void scan_kernel(const ScanArgs a) {
   if constexpr (MT > 0) {
     auto sum_tile = [&](int t, const uint64_t (&bm)[QT], const uint32_t (&w)[kMW]) {
       refresh_bounds();
+      if constexpr (kCount) {
+        if ((threadIdx.x & 63) == 0) atomicAdd(&s_hist[0], 1u);
+      }
       // Subspaces are summed in groups, all of the tile's queries side by
       // side: a group's table reads of every query are issued before its
       // additions, so the reads of different queries overlap.  After each

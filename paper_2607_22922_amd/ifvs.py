@@ -129,7 +129,7 @@ def _load_library() -> ctypes.CDLL:
         "ifvs_encode_predicates": ([vp, i32, vp, vp, vp], i32),
         "ifvs_build_coarse": ([vp, i32, i32], i32),
         "ifvs_lut_bounds": ([vp, i32, vp, vp, vp, vp], i32),
-        "ifvs_filtered_search_bounded": ([vp, i32, vp, vp, i32, vp, i32, vp, vp, vp, vp], i32),
+        "ifvs_filtered_search_bounded": ([vp, i32, vp, vp, i32, vp, vp, i32, vp, vp, vp, vp], i32),
         "ifvs_read_coarse": ([vp, ctypes.POINTER(i32), vp, vp, vp], i32),
         "ifvs_last_coarse": ([vp, ctypes.POINTER(i32)], i32),
     }
@@ -287,17 +287,19 @@ class Index:
         self.lut_bounds_into(nq, alpha, wf, out)
         return out
 
-    def search_bounded_into(self, nq, preds_c, lut, lut_dtype, lut_bounds, k, ids_out, dist_out, bitmap_out=None,
+    def search_bounded_into(self, nq, preds_c, lut, lut_dtype, alpha, wf, k, ids_out, dist_out, bitmap_out=None,
                             stream=None):
+        """ifvs_filtered_search_bounded: alpha and wf are the operands the
+        tables were built with (None for none)."""
         _check(_lib.ifvs_filtered_search_bounded(self.handle, nq, preds_c, lut.data_ptr(), lut_dtype,
-                                                 _ptr(lut_bounds), k, ids_out.data_ptr(), dist_out.data_ptr(),
+                                                 _ptr(alpha), _ptr(wf), k, ids_out.data_ptr(), dist_out.data_ptr(),
                                                  _ptr(bitmap_out), _stream(stream)))
 
-    def search_bounded(self, preds, lut, lut_bounds, k, lut_dtype=LUT_F32):
+    def search_bounded(self, preds, lut, alpha, wf, k, lut_dtype=LUT_F32):
         nq = len(preds)
         ids = torch.empty(nq, k, device=self.device, dtype=torch.int32)
         dist = torch.empty(nq, k, device=self.device, dtype=torch.float32)
-        self.search_bounded_into(nq, pack_predicates(preds), lut, lut_dtype, lut_bounds, k, ids, dist)
+        self.search_bounded_into(nq, pack_predicates(preds), lut, lut_dtype, alpha, wf, k, ids, dist)
         return ids, dist
 
     def read_profile(self) -> dict:

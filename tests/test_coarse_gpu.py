@@ -149,11 +149,11 @@ def test_bound_holds_for_every_row(B, c4s):
     assert pruned > 0
 
 
-def _search_pair(B, idx, preds, lut, bounds, k, dt):
+def _search_pair(B, idx, preds, lut, alpha, wf, k, dt):
     idx.set_option(B.OPT_COARSE, 1)
     ids0, d0 = idx.search(preds, lut, k, dt)
     idx.set_option(B.OPT_COARSE, 2)
-    ids1, d1 = idx.search_bounded(preds, lut, bounds, k, dt)
+    ids1, d1 = idx.search_bounded(preds, lut, alpha, wf, k, dt)
     torch.cuda.synchronize()
     used = idx.last_coarse()
     idx.set_option(B.OPT_COARSE, 0)
@@ -173,15 +173,14 @@ def test_bounded_search_equals_plain_and_oracle(B, c4s, lut_dtype, mode):
         wz = w.w_z[s][:nq]
         if mode == "sdc":
             lut = idx.build_sdc_lut(q, dt)
-            bounds = idx.lut_bounds(nq, None, None)
+            a = wf = None
         else:
             alpha, wf = idx.select_codebook(q, preds, wz)
             a = alpha if mode == "conditioned" else None
             lut = idx.build_lut(q, a, wf, dt)
-            bounds = idx.lut_bounds(nq, a, wf)
         for k in (1, 10, 100):
             say(f"[coarse] {mode} {lut_dtype} s={s} k={k}")
-            ids, dist, used = _search_pair(B, idx, preds, lut, bounds, k, dt)
+            ids, dist, used = _search_pair(B, idx, preds, lut, a, wf, k, dt)
             assert used
             if k == 10:
                 for i in range(0, nq, 3):
@@ -193,26 +192,31 @@ def test_bounded_search_equals_plain_and_oracle(B, c4s, lut_dtype, mode):
                     check_search_row(ids[i], dist[i], res["ids"], res["dist"], f"{mode} s={s} q{i}")
 
 
-def test_auto_mode_and_null_bounds(B, c4s):
-    w, idx, ox = c4s
+def test_auto_mode(B):
+    """Automatic mode: the list scan for a batch whose widest interval spans
+    8192 or more tiles, the interval scan for short intervals; the plain
+    search never takes it.  Answers identical throughout."""
+    say("[coarse] automatic mode, 640K rows")
+    w = make_workload("c4", device="cuda", N=640_000, n_queries=8, keep_x=False)
+    idx = B.Index.from_workload(w, max_batch=8, max_k=16, cluster_cols=(0,))
+    idx.build_coarse(512, 4)
     nq = 8
-    preds = [[(0, 0, 3650)]] * nq          # every row: a span of 1875 tiles
+    preds = [[(0, 0, 3650)]] * nq          # every row: a span of 10K tiles
     q = w.queries[:nq]
     alpha, wf = idx.select_codebook(q, preds, w.w_z[0.5][:nq])
     lut = idx.build_lut(q, alpha, wf)
-    bounds = idx.lut_bounds(nq, alpha, wf)
     ids0, d0 = idx.search(preds, lut, 10)
     assert not idx.last_coarse()
-    ids1, d1 = idx.search_bounded(preds, lut, bounds, 10)
+    ids1, d1 = idx.search_bounded(preds, lut, alpha, wf, 10)
     assert idx.last_coarse()
-    ids2, d2 = idx.search_bounded(preds, lut, None, 10)   # no bounds: the plain search
-    assert not idx.last_coarse()
     short = [[(0, 100, 110)]] * nq                          # 0.3% of the rows
-    idx.search_bounded(short, lut, bounds, 10)
+    ids2, d2 = idx.search_bounded(short, lut, alpha, wf, 10)
     assert not idx.last_coarse()
+    ids3, d3 = idx.search(short, lut, 10)
     torch.cuda.synchronize()
-    for ids, d in ((ids1, d1), (ids2, d2)):
-        assert torch.equal(ids, ids0) and torch.equal(d.view(torch.int32), d0.view(torch.int32))
+    assert torch.equal(ids1, ids0) and torch.equal(d1.view(torch.int32), d0.view(torch.int32))
+    assert torch.equal(ids2, ids3) and torch.equal(d2.view(torch.int32), d3.view(torch.int32))
+    idx.close()
 
 
 def test_negative_weights_unsatisfiable_predicates_and_residual_clauses(B):
@@ -238,8 +242,7 @@ def test_negative_weights_unsatisfiable_predicates_and_residual_clauses(B):
         wf = wf.clone()
         wf[1::5, 0] = -1.0
         lut = idx.build_lut(q, alpha, wf)
-        bounds = idx.lut_bounds(nq, alpha, wf)
-        ids, dist, used = _search_pair(B, idx, preds, lut, bounds, 10, B.LUT_F32)
+        ids, dist, used = _search_pair(B, idx, preds, lut, alpha, wf, 10, B.LUT_F32)
         assert used == listed
         alpha_n, wf_n = _np(alpha), _np(wf)
         for i in range(nq):
@@ -276,9 +279,8 @@ def test_ties_at_the_kth_distance(B, lut_dtype):
                                             0.01 * torch.randn(4, M * dsub, device="cuda", generator=g)])
     preds = [[(0, 0, 100)], [(0, 10, 90)], [(0, 0, 50)], [(0, 20, 100)]] * 2
     lut = idx.build_lut(q, None, None, dt)
-    bounds = idx.lut_bounds(8, None, None)
     for k in (5, 64, 128):
-        ids, dist, used = _search_pair(B, idx, preds, lut, bounds, k, dt)
+        ids, dist, used = _search_pair(B, idx, preds, lut, None, None, k, dt)
         assert used
         for i in range(8):
             res = O.filtered_search(ox, _np(q[i]), preds[i], k, lut_dtype=lut_dtype, conditioned=False)
@@ -299,7 +301,7 @@ def test_m16_index(B):
         q = w.queries[:16]
         alpha, wf = idx.select_codebook(q, preds, w.w_z[s][:16])
         lut = idx.build_lut(q, alpha, wf)
-        ids, dist, used = _search_pair(B, idx, preds, lut, idx.lut_bounds(16, alpha, wf), 10, B.LUT_F32)
+        ids, dist, used = _search_pair(B, idx, preds, lut, alpha, wf, 10, B.LUT_F32)
         assert used
         for i in range(0, 16, 4):
             res = O.filtered_search(ox, _np(q[i]), preds[i], 10, w_z=_np(w.w_z[s][i]))
