@@ -304,7 +304,8 @@ ifvs_status ifvs_lut_bounds(ifvs_index* idx, int32_t nq, const float* alpha, con
  * or more 64-row tiles); otherwise the call is ifvs_filtered_search.  The
  * list scan adds the bound kernels and one planning kernel per call (one
  * workgroup per query sorts the query's groups by their bound).
- * IFVS_OPT_SPLITS sets its workgroups per query (at most 16).
+ * IFVS_OPT_SPLITS sets its workgroups per query (rounded down to a power of
+ * two, at most 16; default about 2048 workgroups in all).
  * Errors: as ifvs_filtered_search, plus IFVS_E_INVALID for alpha given on an
  * index without a memory bank. */
 ifvs_status ifvs_filtered_search_bounded(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,

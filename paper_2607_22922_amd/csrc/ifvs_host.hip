@@ -1205,8 +1205,14 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   // (no residual clauses); automatic for batches whose widest interval spans
   // at least kCoarseAutoTiles 64-row tiles.
   const CoarseLists& cl = idx->coarse;
-  const int list_splits = std::min(kListSlots / (2 * kScanWaves),
-                                   idx->opt_splits > 0 ? idx->opt_splits : std::max(1, (1024 + nq - 1) / nq));
+  // Workgroups per query: a power of two, at most 16, about 2048 in all
+  // (measured on 10M x 48-byte codes, 256 queries: 8 per query 25% faster
+  // than 4 at 50% selectivity).
+  int list_splits = 1;
+  {
+    const int want = idx->opt_splits > 0 ? idx->opt_splits : std::max(1, (2048 + nq - 1) / nq);
+    while (list_splits * 2 <= std::min(want, kListSlots / (2 * kScanWaves))) list_splits *= 2;
+  }
   const bool list_mode =
       bounded && cl.words && idx->opt_coarse != 1 && !static_scratch && !need_bitmap &&
       list_scan_supported(idx->m, lut_dtype) &&

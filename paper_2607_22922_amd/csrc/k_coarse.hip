@@ -353,8 +353,11 @@ __global__ __launch_bounds__(256) void gather_list_rows_kernel(const uint32_t* _
 // sorted ascending by lb rounded down to 18 bits of its order-preserving
 // code (the item index fills the other 14); the items carry that rounded
 // lb, so a scan may stop at the first item it can prune: every later item
-// has a bound at least as large.  T = the 64-row tiles the items before it
-// touch.
+// has a bound at least as large.  Before them come, with no bound (NaN), the
+// sub-lists of the query's nearest centroid that has selected rows (its
+// rows hold the query's nearest rows as a rule, so the scan's k-th distance
+// is tight from its first tiles) and any sub-list whose bound is NaN.  T =
+// the 64-row tiles the items before it touch.
 template <typename LutT>
 __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
@@ -365,6 +368,7 @@ __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
   int32_t* s_cnt = reinterpret_cast<int32_t*>(scratch);                   // phase 2: [S]
   uint32_t* s_key = reinterpret_cast<uint32_t*>(s_cnt + S);               // phase 2: [Sp]
   __shared__ int s_count;
+  __shared__ unsigned long long s_near;   // (sdc bits, centroid) of the nearest selected centroid
   const int q = blockIdx.x;
   const int tid = threadIdx.x;
   const int64_t x0 = a.iv[2 * q], x1 = a.iv[2 * q + 1];
@@ -385,7 +389,10 @@ __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
   const int lut_vecs = a.m * kKsub * static_cast<int>(sizeof(LutT)) / 16;
   for (int v = tid; v < lut_vecs; v += 1024)
     reinterpret_cast<uint4*>(s_lut)[v] = reinterpret_cast<const uint4*>(lut)[v];
-  if (tid == 0) s_count = 0;
+  if (tid == 0) {
+    s_count = 0;
+    s_near = ~0ull;
+  }
   __syncthreads();
   for (int c = tid; c < C; c += 1024) {
     float d = 0.0f;
@@ -414,27 +421,41 @@ __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
     if (pass == 0) {
       for (int s = tid; s < S; s += 1024) a.tmp_r0[base + s] = a.sub_off[s] + s_cnt[s];
     } else {
-      int mine = 0;
-      for (int s = tid; s < Sp; s += 1024) {
-        uint32_t key = ~0u;
-        if (s < S) {
-          const int32_t r0 = a.tmp_r0[base + s];
-          const int32_t r1 = a.sub_off[s] + s_cnt[s];
-          if (r1 > r0) {
-            const float lb = __fsub_rn(s_sdc[s / kBands], __fmul_rn(__fadd_rn(a.rmax[s], delta), sw));
-            // NaN (no bound for this query) sorts first, never pruned
-            const uint32_t ob = lb == lb ? ordered_bits(lb) : 0u;
-            key = (ob & ~uint32_t{kItemMask}) | static_cast<uint32_t>(s);
-            a.tmp_r1[base + s] = r1;
-            ++mine;
-          }
+      for (int s = tid; s < S; s += 1024) {
+        const int32_t r0 = a.tmp_r0[base + s];
+        const int32_t r1 = a.sub_off[s] + s_cnt[s];
+        a.tmp_r1[base + s] = r1;
+        if (r1 > r0) {
+          const int c = s / kBands;
+          atomicMin(&s_near, (static_cast<unsigned long long>(ordered_bits(s_sdc[c])) << 32) |
+                                 static_cast<uint32_t>(c));
         }
-        s_key[s] = key;
       }
-      atomicAdd(&s_count, mine);
     }
     __syncthreads();
   }
+  {
+    const int near = s_near == ~0ull ? -1 : static_cast<int>(s_near & 0xFFFFFFFFu);
+    int mine = 0;
+    for (int s = tid; s < Sp; s += 1024) {
+      uint32_t key = ~0u;
+      if (s < S) {
+        const int32_t r0 = a.tmp_r0[base + s];
+        const int32_t r1 = a.tmp_r1[base + s];
+        if (r1 > r0) {
+          const float lb = __fsub_rn(s_sdc[s / kBands], __fmul_rn(__fadd_rn(a.rmax[s], delta), sw));
+          // the nearest centroid's sub-lists and NaN bounds sort first with
+          // the top bits 0, carried as NaN (never pruned)
+          const uint32_t ob = lb == lb && s / kBands != near ? ordered_bits(lb) : 0u;
+          key = (ob & ~uint32_t{kItemMask}) | static_cast<uint32_t>(s);
+          ++mine;
+        }
+      }
+      s_key[s] = key;
+    }
+    atomicAdd(&s_count, mine);
+  }
+  __syncthreads();
   // ascending bitonic sort of the Sp keys
   for (int size = 2; size <= Sp; size <<= 1) {
     for (int stride = size >> 1; stride > 0; stride >>= 1) {

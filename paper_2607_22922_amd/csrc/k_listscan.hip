@@ -61,7 +61,9 @@ constexpr int list_waves_per_eu() {
 
 // kCount: a measurement build that also counts the table reads by active
 // lanes (entries 1..64 of a.lookup_hist) and the code tiles summed (entry 0).
-template <int MT, typename LutT, bool kCount = false>
+// kDepth register sets: the tiles of kDepth - 1 of them are in flight while
+// one is summed.
+template <int MT, typename LutT, bool kCount = false, int kDepth = 2>
 __global__ __launch_bounds__(kScanWaves * 64) __attribute__((amdgpu_waves_per_eu(list_waves_per_eu<MT, LutT>())))
 void list_scan_kernel(const ListScanArgs a) {
   constexpr int kMW = (MT + 3) / 4;
@@ -127,7 +129,9 @@ void list_scan_kernel(const ListScanArgs a) {
   };
 
   // Tile generator over the query's items.
+  // G is a power of two (splits is), so positions reduce with a mask.
   const int G = kScanWaves * a.splits, g = split * kScanWaves + wave;
+  const int gmask = G - 1;
   const size_t ib = static_cast<size_t>(q) * a.C;
   int batch = -64;
   int stop_at = n_items;   // items from here on are prunable
@@ -169,7 +173,7 @@ void list_scan_kernel(const ListScanArgs a) {
           v_sdc = a.it_sdc[ib + it];
           v_lb = a.it_lb[ib + it];
           const int nt = ((v_r1 - 1) >> 6) - (v_r0 >> 6) + 1;
-          const int off = ((g - v_t) % G + G) % G;   // first position of the item this wavefront takes
+          const int off = (g - v_t) & gmask;   // first position of the item this wavefront takes
           gone = pruned(v_lb);
           ok = off < nt && !gone;
         }
@@ -191,7 +195,7 @@ void list_scan_kernel(const ListScanArgs a) {
       i_sdc = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v_sdc), j));
       i_lb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v_lb), j));
       i_nt = ((i_r1 - 1) >> 6) - (i_r0 >> 6) + 1;
-      p = i_t + ((g - i_t) % G + G) % G;
+      p = i_t + ((g - i_t) & gmask);
       in_item = true;
     }
   };
@@ -283,8 +287,11 @@ void list_scan_kernel(const ListScanArgs a) {
       if (pruned(lb)) live = false;
     }
     float d = 0.0f;
+    // (most tiles lose every row to the bound or to the first groups: the
+    // loop ends as soon as no lane is live)
 #pragma unroll
     for (int gr = 0; gr < MT / kGroup; ++gr) {
+      if (__ballot(live) == 0) break;
       int addr[kGroup];
 #pragma unroll
       for (int u = 0; u < kGroup; ++u) {
@@ -304,29 +311,42 @@ void list_scan_kernel(const ListScanArgs a) {
       }
       live = live && !(d > cut);
     }
-    if (__ballot(live) != 0 || union_bound) consider(live, d, t);
+    if (__ballot(live) != 0) consider(live, d, t);
   };
 
-  // Two register sets: the next tile's words are loaded while the current
-  // one is summed.
-  uint32_t wa[kMW], wb[kMW];
-  float ra = 0.0f, rb = 0.0f, sa = 0.0f, sb = 0.0f;
-  int ta = 0, tb = 0;
-  uint64_t ma = 0, mb = 0;
-  bool ha = next_tile(ta, ma, sa);
-  if (ha) load(ta, wa, ra);
+  // Register sets in a ring: step i refills the set summed in the step
+  // before with the next tile, then sums set i.  Tiles come in generation
+  // order, so the first set without one ends the scan.
+  uint32_t ws[kDepth][kMW];
+  float rs[kDepth], ss[kDepth];
+  int ts[kDepth];
+  uint64_t ms[kDepth];
+  bool hs[kDepth];
+#pragma unroll
+  for (int i = 0; i < kDepth; ++i) {
+    rs[i] = ss[i] = 0.0f;
+    ts[i] = 0;
+    ms[i] = 0;
+    hs[i] = false;
+  }
+#pragma unroll
+  for (int i = 0; i < kDepth - 1; ++i) {
+    hs[i] = next_tile(ts[i], ms[i], ss[i]);
+    if (hs[i]) load(ts[i], ws[i], rs[i]);
+  }
   for (;;) {
     gview = gnext;
     gnext = __hip_atomic_load(a.gthr + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const bool hb = next_tile(tb, mb, sb);
-    if (hb) load(tb, wb, rb);
-    if (!ha) break;
-    sum_tile(ta, ma, sa, wa, ra);
-    ha = next_tile(ta, ma, sa);
-    if (ha) load(ta, wa, ra);
-    if (!hb) break;
-    sum_tile(tb, mb, sb, wb, rb);
+#pragma unroll
+    for (int i = 0; i < kDepth; ++i) {
+      const int j = (i + kDepth - 1) % kDepth;
+      hs[j] = next_tile(ts[j], ms[j], ss[j]);
+      if (hs[j]) load(ts[j], ws[j], rs[j]);
+      if (!hs[i]) goto scanned;
+      sum_tile(ts[i], ms[i], ss[i], ws[i], rs[i]);
+    }
   }
+scanned:
 
   pool_compact(pool, cnt, thr, k, a.kpl, a.ids);
   uint64_t* dst = a.partials + ((static_cast<size_t>(pos) * a.splits + split) * kScanWaves + wave) * k;
@@ -372,7 +392,7 @@ size_t list_scan_lds_bytes(int m, int lut_dtype, int pool_stride) {
 
 hipError_t launch_list_scan(const ListScanArgs& a, int lut_dtype, hipStream_t s) {
   const void* fn = pick_list(a.m, lut_dtype, a.lookup_hist != nullptr);
-  if (!fn || a.splits < 1) return hipErrorInvalidValue;
+  if (!fn || a.splits < 1 || (a.splits & (a.splits - 1)) != 0) return hipErrorInvalidValue;
   if (a.nq <= 0) return hipSuccess;
   const size_t dyn = list_dyn_bytes(a.pool_stride);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(dyn));
