@@ -265,9 +265,9 @@ ifvs_status ifvs_filtered_search_noalloc(ifvs_index* idx, int32_t nq, const ifvs
  * with C_PQ and every row gets its nearest encoded centroid and its
  * distance to it, rounded up to a bfloat16; then the grouped copy of the
  * codes.  Synchronous; replaces any earlier coarse quantizer.  Costs about
- * n * (4 ceil(m/4) + 13) bytes of device memory (codes, radii, ids, row
- * words and bands), a rank table of at most 64 MiB, and max_batch *
- * n_centroids * 112 + max_batch * 1040 bytes of list-plan workspace.
+ * n * (4 ceil(m/4) + 13) bytes of device memory (codes, ids, row words,
+ * bands and list positions), a rank table of at most 64 MiB, and max_batch *
+ * n_centroids * 96 + max_batch * 1040 bytes of list-plan workspace.
  * Errors: IFVS_E_INVALID (n_centroids outside 1..4096 or above n, iters
  * outside 0..1000), IFVS_E_UNSUPPORTED (dim > 128), IFVS_E_STATE,
  * IFVS_E_NOMEM, IFVS_E_HIP. */
@@ -511,8 +511,9 @@ ifvs_status ifvs_encode_predicates(ifvs_index* idx, int32_t nq, const ifvs_predi
 #define IFVS_OPT_SHARED_BOUND 9   /* k <= 16: the wavefronts of a scan workgroup publish their
                                      two smallest distances and prune with the k-th smallest
                                      published one: 0 automatic (on for chunk-grid scans whose
-                                     widest interval spans 32768 or more 64-row tiles),
-                                     1 never, 2 always                                         */
+                                     widest interval spans 32768 or more 64-row tiles, and for
+                                     the list scan, where all wavefronts of the query share
+                                     them for k up to twice their number), 1 never, 2 always */
 #define IFVS_OPT_SEED_TILES 11   /* one-query scans of M = 16, 48 or 120 with k <= 64: before
                                      scanning, each wavefront ranks the selected rows of its first
                                      n selected tiles by their partial sums over the first

@@ -132,14 +132,13 @@ struct CoarseLists {
   float* rmax = nullptr;         // [C * kBands] largest radius of each sub-list
   int32_t* cnt_f = nullptr;      // [(n >> f_shift) + 1][C * kBands]
   uint32_t* codes_t = nullptr;   // [n_tiles][mw][64] list order
-  float* rad = nullptr;          // [n_tiles * 64] list order
   int32_t* ids = nullptr;        // [n_tiles * 64] list position -> original id
+  int32_t* lrow = nullptr;       // [n] list position -> layout row
   int32_t* tmp_r0 = nullptr;     // [max_batch][C * kBands] list plan workspace
   int32_t* tmp_r1 = nullptr;
   int32_t* it_r0 = nullptr;      // [max_batch][C * kBands] list plan items
   int32_t* it_r1 = nullptr;
   int32_t* it_t = nullptr;
-  float* it_sdc = nullptr;
   float* it_lb = nullptr;
   float* hdr = nullptr;          // [max_batch][4]
   uint32_t* slots = nullptr;     // [max_batch][kListSlots]
@@ -147,9 +146,10 @@ struct CoarseLists {
   void release() {
     for (void* p : {static_cast<void*>(words), static_cast<void*>(band), static_cast<void*>(cc_t),
                     static_cast<void*>(sub_off), static_cast<void*>(rmax), static_cast<void*>(cnt_f),
-                    static_cast<void*>(codes_t), static_cast<void*>(rad), static_cast<void*>(ids),
+                    static_cast<void*>(codes_t), static_cast<void*>(ids),
+                    static_cast<void*>(lrow),
                     static_cast<void*>(tmp_r0), static_cast<void*>(tmp_r1), static_cast<void*>(it_r0),
-                    static_cast<void*>(it_r1), static_cast<void*>(it_t), static_cast<void*>(it_sdc),
+                    static_cast<void*>(it_r1), static_cast<void*>(it_t),
                     static_cast<void*>(it_lb), static_cast<void*>(hdr), static_cast<void*>(slots)})
       if (p) (void)hipFree(p);
     *this = CoarseLists{};
@@ -1264,6 +1264,10 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     pa.band = cl.band;
     pa.sub_off = cl.sub_off;
     pa.rmax = cl.rmax;
+    pa.lrow = cl.lrow;
+    pa.codes_t = cl.codes_t;
+    pa.k = k;
+    pa.gthr = ws.gthr;
     pa.tmp_r0 = cl.tmp_r0;
     pa.tmp_r1 = cl.tmp_r1;
     pa.keep = coarse_keep(idx->m, idx->dsub, lut_dtype);
@@ -1271,14 +1275,12 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     pa.it_r0 = cl.it_r0;
     pa.it_r1 = cl.it_r1;
     pa.it_t = cl.it_t;
-    pa.it_sdc = cl.it_sdc;
     pa.it_lb = cl.it_lb;
     pa.hdr = cl.hdr;
     pa.slots = cl.slots;
     IFVS_LAUNCH(idx, kStCoarse, s, "launching list plan kernel", launch_list_plan(pa, lut_dtype, s));
     ListScanArgs sa{};
     sa.codes_t = cl.codes_t;
-    sa.rad = cl.rad;
     sa.ids = cl.ids;
     sa.m = idx->m;
     sa.mw = idx->mw;
@@ -1289,7 +1291,6 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     sa.it_r0 = cl.it_r0;
     sa.it_r1 = cl.it_r1;
     sa.it_t = cl.it_t;
-    sa.it_sdc = cl.it_sdc;
     sa.it_lb = cl.it_lb;
     sa.hdr = cl.hdr;
     sa.C = cl.C * kBands;
@@ -1302,6 +1303,7 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     sa.gthr = ws.gthr;
     sa.slots = cl.slots;
     sa.lookup_hist = idx->opt_count_reads ? idx->read_hist : nullptr;
+    sa.union_bound = idx->opt_shared_bound == 1 ? 0 : 1;
     IFVS_LAUNCH(idx, kStScan, s, "launching list scan kernel", launch_list_scan(sa, lut_dtype, s));
     IFVS_LAUNCH(idx, kStMerge, s, "launching top-k merge kernel",
                 launch_topk_merge(ws.partials, nq, static_cast<int64_t>(list_splits) * kScanWaves * k, k, ws.iv, 0,
@@ -1925,12 +1927,11 @@ ifvs_status ifvs_build_coarse(ifvs_index* idx, int32_t n_centroids, int32_t iter
   float* chat = nullptr;
   int32_t* assign = nullptr;
   uint32_t* cc = nullptr;
-  int32_t* lrow = nullptr;
   CoarseLists nl;
   nl.C = C;
   auto cleanup = [&](ifvs_status st) {
     for (void* p : {static_cast<void*>(X), static_cast<void*>(cent), static_cast<void*>(chat),
-                    static_cast<void*>(assign), static_cast<void*>(cc), static_cast<void*>(lrow)})
+                    static_cast<void*>(assign), static_cast<void*>(cc)})
       if (p) (void)hipFree(p);
     nl.release();
     return st;
@@ -2054,15 +2055,12 @@ ifvs_status ifvs_build_coarse(ifvs_index* idx, int32_t n_centroids, int32_t iter
   if (ifvs_status st = alloc(&nl.band, hband.size(), "radius bands"); st != IFVS_OK) return cleanup(st);
   if (ifvs_status st = alloc(&nl.codes_t, static_cast<size_t>(n_pad) * mw, "list-order codes"); st != IFVS_OK)
     return cleanup(st);
-  if (ifvs_status st = alloc(&nl.rad, static_cast<size_t>(n_pad), "list-order radii"); st != IFVS_OK)
-    return cleanup(st);
   if (ifvs_status st = alloc(&nl.ids, static_cast<size_t>(n_pad), "list-order ids"); st != IFVS_OK)
     return cleanup(st);
-  if (ifvs_status st = alloc(&lrow, hrow.size(), "list rows"); st != IFVS_OK) return cleanup(st);
+  if (ifvs_status st = alloc(&nl.lrow, hrow.size(), "list rows"); st != IFVS_OK) return cleanup(st);
   for (int32_t** a : {&nl.it_r0, &nl.it_r1, &nl.it_t, &nl.tmp_r0, &nl.tmp_r1})
     if (ifvs_status st = alloc(a, items, "list plan"); st != IFVS_OK) return cleanup(st);
-  for (float** a : {&nl.it_sdc, &nl.it_lb})
-    if (ifvs_status st = alloc(a, items, "list plan"); st != IFVS_OK) return cleanup(st);
+  if (ifvs_status st = alloc(&nl.it_lb, items, "list plan"); st != IFVS_OK) return cleanup(st);
   if (ifvs_status st = alloc(&nl.hdr, static_cast<size_t>(idx->max_batch) * 4, "list plan"); st != IFVS_OK)
     return cleanup(st);
   if (ifvs_status st = alloc(&nl.slots, static_cast<size_t>(idx->max_batch) * kListSlots, "list scan bound slots");
@@ -2074,13 +2072,13 @@ ifvs_status ifvs_build_coarse(ifvs_index* idx, int32_t n_centroids, int32_t iter
     size_t bytes;
   } uploads[] = {{nl.cc_t, cc_t.data(), cc_t.size() * 4},   {nl.sub_off, off.data(), off.size() * 4},
                  {nl.rmax, rmax.data(), rmax.size() * 4},    {nl.cnt_f, cnt_f.data(), cnt_f.size() * 4},
-                 {nl.band, hband.data(), hband.size()},      {lrow, hrow.data(), hrow.size() * 4}};
+                 {nl.band, hband.data(), hband.size()},      {nl.lrow, hrow.data(), hrow.size() * 4}};
   for (const auto& u : uploads)
     if (ifvs_status st = step(hipMemcpy(u.dst, u.src, u.bytes, hipMemcpyHostToDevice), "uploading the lists");
         st != IFVS_OK)
       return cleanup(st);
-  if (ifvs_status st = step(launch_gather_list(idx->codes_t, mw, nl.words, idx->perm, lrow, n, idx->n_tiles,
-                                               nl.codes_t, nl.rad, nl.ids, s),
+  if (ifvs_status st = step(launch_gather_list(idx->codes_t, mw, idx->perm, nl.lrow, n, idx->n_tiles, nl.codes_t,
+                                               nl.ids, s),
                             "launching list gather kernels");
       st != IFVS_OK)
     return cleanup(st);

@@ -22,6 +22,7 @@ constexpr int kCoarseMax = 4096;           // most coarse centroids
 constexpr int kBands = 4;                  // radius bands per coarse list (sub-lists)
 constexpr int kMaxItems = kCoarseMax * kBands;   // sub-lists a list plan sorts in one workgroup
 constexpr int kItemMask = kMaxItems - 1;         // sub-list index bits of a plan's sort key
+constexpr int kSeedRows = 4096;                  // rows of the nearest list a plan scores for its seed
 
 // A predicate as the device sees it.  The raw fields are the caller's clauses
 // exactly as given (they are hashed into the memory bank); the effective
@@ -257,11 +258,10 @@ hipError_t launch_lut_bounds(const float* alpha, const float* wf, const float* c
                              int r, int dsub, float* parts, float* bounds, hipStream_t s);
 // List order: rows grouped by sub-list s = (centroid c, radius band b),
 // s = c * kBands + b, positions [sub_off[s], sub_off[s+1]), each sub-list in
-// layout order.  Code tiles, radii and original ids gathered through
-// src_rows[p] = layout row of position p.
-hipError_t launch_gather_list(const uint32_t* src_t, int mw, const uint32_t* words, const int32_t* perm,
-                              const int32_t* src_rows, int64_t n, int64_t n_tiles, uint32_t* dst_t, float* rad,
-                              int32_t* ids, hipStream_t s);
+// layout order.  Code tiles and original ids gathered through src_rows[p] =
+// layout row of position p.
+hipError_t launch_gather_list(const uint32_t* src_t, int mw, const int32_t* perm, const int32_t* src_rows, int64_t n,
+                              int64_t n_tiles, uint32_t* dst_t, int32_t* ids, hipStream_t s);
 
 // Per-query list plan (one workgroup per original query index).
 struct ListPlanArgs {
@@ -277,6 +277,10 @@ struct ListPlanArgs {
   const uint8_t* band;      // [n] layout row radius band
   const int32_t* sub_off;   // [n_sub + 1]
   const float* rmax;        // [n_sub] largest radius of each sub-list
+  const int32_t* lrow;      // [n] list position -> layout row
+  const uint32_t* codes_t;  // list-order code tiles (the seed's rows)
+  int k;
+  uint64_t* gthr;           // [nq] the queries' shared thresholds (the seed lowers them)
   float keep, abs_m;
   int32_t* tmp_r0;          // [nq][n_sub] workspace
   int32_t* tmp_r1;          // [nq][n_sub] workspace
@@ -286,7 +290,6 @@ struct ListPlanArgs {
   int32_t* it_r0;           // first list position of the item's rows
   int32_t* it_r1;           // one past the last
   int32_t* it_t;            // 64-row tiles the items before it touch
-  float* it_sdc;            // lower bound of the query's distance to the sub-list's centroid
   float* it_lb;             // lower bound of the distance of every row of the sub-list (NaN: none)
   float* hdr;
   uint32_t* slots;          // [nq][kListSlots] the list scan's union-bound slots, reset here
@@ -299,7 +302,6 @@ hipError_t launch_list_plan(const ListPlanArgs& a, int lut_dtype, hipStream_t s)
 // each query, nearest list first, skipping lists and rows by the bound.
 struct ListScanArgs {
   const uint32_t* codes_t;  // [n_tiles][mw][64] list-order code words
-  const float* rad;         // [n_tiles * 64] list-order radii
   const int32_t* ids;       // list position -> original id
   int m, mw;
   const void* lut;          // [nq][m][256] by original query
@@ -308,7 +310,6 @@ struct ListScanArgs {
   const int32_t* it_r0;
   const int32_t* it_r1;
   const int32_t* it_t;
-  const float* it_sdc;
   const float* it_lb;
   const float* hdr;
   int C;                    // item stride per query (sub-lists)
@@ -318,6 +319,7 @@ struct ListScanArgs {
   uint64_t* gthr;           // [nq] shared thresholds, all ones before the scan
   uint32_t* slots;          // [nq][kListSlots] union-bound slots, all ones before the scan (list plan)
   unsigned long long* lookup_hist;  // [65] non-null: the counting build (table reads by lanes, [0] tiles)
+  int union_bound;          // 1: the query-wide union bound of the wavefronts' best distances
 };
 constexpr int kListSlots = 2 * kScanWaves * 16;   // two per wavefront of at most 16 workgroups per query
 bool list_scan_supported(int m, int lut_dtype);

@@ -318,23 +318,18 @@ __global__ __launch_bounds__(256) void gather_code_tiles_kernel(const uint32_t* 
   dst_t[e] = v;
 }
 
-// Per list position p < n_pad: the row's radius (from its layout word) and
-// its original id (perm null: the layout row is the id); 0 past n.
-__global__ __launch_bounds__(256) void gather_list_rows_kernel(const uint32_t* __restrict__ words,
-                                                               const int32_t* __restrict__ perm,
+// Per list position p < n_pad: the row's original id (perm null: the layout
+// row is the id); 0 past n.
+__global__ __launch_bounds__(256) void gather_list_rows_kernel(const int32_t* __restrict__ perm,
                                                                const int32_t* __restrict__ src_rows, int64_t n,
-                                                               int64_t n_pad, float* __restrict__ rad,
-                                                               int32_t* __restrict__ ids) {
+                                                               int64_t n_pad, int32_t* __restrict__ ids) {
   const int64_t p = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (p >= n_pad) return;
-  float rv = 0.0f;
   int32_t id = 0;
   if (p < n) {
     const int64_t r = src_rows[p];
-    rv = __uint_as_float(words[r] & 0xFFFF0000u);
     id = perm ? perm[r] : static_cast<int32_t>(r);
   }
-  rad[p] = rv;
   ids[p] = id;
 }
 
@@ -358,6 +353,13 @@ __global__ __launch_bounds__(256) void gather_list_rows_kernel(const uint32_t* _
 // rows hold the query's nearest rows as a rule, so the scan's k-th distance
 // is tight from its first tiles) and any sub-list whose bound is NaN.  T =
 // the 64-row tiles the items before it touch.
+//
+// Seed: the distances (summed exactly as the scan sums them) of the
+// selected rows among the first kSeedRows positions of the list of the
+// centroid with the smallest sdc; when there are k of them, the k-th
+// smallest bounds the query's k-th distance (k distinct selected rows lie
+// at or below it) and goes to the query's shared threshold, with the
+// largest id so rows at that distance stay eligible.
 template <typename LutT>
 __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
@@ -365,10 +367,12 @@ __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
   float* s_sdc = reinterpret_cast<float*>(smem);                          // [C]
   unsigned char* scratch = smem + ((static_cast<size_t>(C) * 4 + 15) & ~size_t{15});
   LutT* s_lut = reinterpret_cast<LutT*>(scratch);                         // phase 1
+  uint32_t* s_seed = reinterpret_cast<uint32_t*>(scratch + static_cast<size_t>(a.m) * kKsub * sizeof(LutT));
   int32_t* s_cnt = reinterpret_cast<int32_t*>(scratch);                   // phase 2: [S]
   uint32_t* s_key = reinterpret_cast<uint32_t*>(s_cnt + S);               // phase 2: [Sp]
   __shared__ int s_count;
   __shared__ unsigned long long s_near;   // (sdc bits, centroid) of the nearest selected centroid
+  __shared__ unsigned long long s_first;  // (sdc bits, centroid) of the nearest centroid
   const int q = blockIdx.x;
   const int tid = threadIdx.x;
   const int64_t x0 = a.iv[2 * q], x1 = a.iv[2 * q + 1];
@@ -392,6 +396,7 @@ __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
   if (tid == 0) {
     s_count = 0;
     s_near = ~0ull;
+    s_first = ~0ull;
   }
   __syncthreads();
   for (int c = tid; c < C; c += 1024) {
@@ -405,6 +410,52 @@ __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
     }
     const float lo = __fmul_rn(__fsub_rn(d, a.abs_m), a.keep);
     s_sdc[c] = lo > 0.0f && lo <= FLT_MAX ? __fmul_rn(sqrtf(lo), 1.0f - 0x1p-20f) : 0.0f;
+    atomicMin(&s_first, (static_cast<unsigned long long>(ordered_bits(s_sdc[c])) << 32) | static_cast<uint32_t>(c));
+  }
+  __syncthreads();
+  {
+    // The seed (see above), from the nearest centroid's list.
+    const int c0 = static_cast<int>(s_first & 0xFFFFFFFFu);
+    const int32_t p0 = a.sub_off[c0 * kBands], p1 = min(a.sub_off[c0 * kBands + kBands], p0 + kSeedRows);
+    for (int i = tid; i < kSeedRows; i += 1024) {
+      uint32_t key = ~0u;
+      const int32_t p = p0 + i;
+      if (p < p1) {
+        const int64_t r = a.lrow[p];
+        if (r >= x0 && r < x1) {
+          const uint32_t* tile = a.codes_t + static_cast<size_t>(p >> 6) * a.mw * 64 + (p & 63);
+          float d = 0.0f;
+          for (int w = 0; w < a.mw; ++w) {
+            const uint32_t word = tile[w * 64];
+            for (int b = 0; b < 4; ++b) {
+              const int m = 4 * w + b;
+              if (m < a.m) d = __fadd_rn(d, widen(s_lut[m * kKsub + static_cast<int>((word >> (8 * b)) & 0xFFu)]));
+            }
+          }
+          key = ordered_bits(d);
+        }
+      }
+      s_seed[i] = key;
+    }
+    __syncthreads();
+    for (int size = 2; size <= kSeedRows; size <<= 1) {
+      for (int stride = size >> 1; stride > 0; stride >>= 1) {
+        for (int p = tid; p < kSeedRows / 2; p += 1024) {
+          const int i = ((p & ~(stride - 1)) << 1) | (p & (stride - 1));
+          const int j = i | stride;
+          const uint32_t x = s_seed[i], y = s_seed[j];
+          const bool up = (i & size) == 0;
+          if (up ? (x > y) : (x < y)) {
+            s_seed[i] = y;
+            s_seed[j] = x;
+          }
+        }
+        __syncthreads();
+      }
+    }
+    if (tid == 0 && a.k <= kSeedRows && s_seed[a.k - 1] != ~0u)
+      atomicMin(reinterpret_cast<unsigned long long*>(a.gthr + q),
+                (static_cast<unsigned long long>(s_seed[a.k - 1]) << 32) | 0xFFFFFFFFull);
   }
   __syncthreads();
   // Phase 2: ranks at x0 (kept in tmp_r0), then at x1 with the items'
@@ -481,7 +532,6 @@ __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
     s_nt[i] = ((r1 - 1) >> 6) - (r0 >> 6) + 1;
     a.it_r0[base + i] = r0;
     a.it_r1[base + i] = r1;
-    a.it_sdc[base + i] = s_sdc[s / kBands];
     const uint32_t ob = key & ~uint32_t{kItemMask};
     a.it_lb[base + i] = ob == 0u ? __builtin_nanf("") : from_ordered_bits(ob);
   }
@@ -578,7 +628,7 @@ hipError_t launch_lut_bounds(const float* alpha, const float* wf, const float* c
 }
 
 size_t list_plan_lds_bytes(int m, int lut_dtype, int C) {
-  const size_t lut = static_cast<size_t>(m) * kKsub * (lut_dtype == 1 ? 2 : 4);
+  const size_t lut = static_cast<size_t>(m) * kKsub * (lut_dtype == 1 ? 2 : 4) + kSeedRows * 4;
   const size_t items = static_cast<size_t>(C) * kBands * 4 + static_cast<size_t>(list_plan_width(C)) * 4;
   return ((static_cast<size_t>(C) * 4 + 15) & ~size_t{15}) + std::max(lut, items);
 }
@@ -602,17 +652,15 @@ hipError_t launch_list_plan(const ListPlanArgs& a, int lut_dtype, hipStream_t s)
   return hipLaunchKernel(fn, dim3(static_cast<unsigned>(a.nq)), dim3(1024), kargs, lds, s);
 }
 
-hipError_t launch_gather_list(const uint32_t* src_t, int mw, const uint32_t* words, const int32_t* perm,
-                              const int32_t* src_rows, int64_t n, int64_t n_tiles, uint32_t* dst_t, float* rad,
-                              int32_t* ids, hipStream_t s) {
+hipError_t launch_gather_list(const uint32_t* src_t, int mw, const int32_t* perm, const int32_t* src_rows, int64_t n,
+                              int64_t n_tiles, uint32_t* dst_t, int32_t* ids, hipStream_t s) {
   const int64_t total = n_tiles * mw * 64;
   gather_code_tiles_kernel<<<static_cast<unsigned>((total + 255) / 256), 256, 0, s>>>(src_t, mw, src_rows, n, n_tiles,
                                                                                     dst_t);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t n_pad = n_tiles * 64;
-  gather_list_rows_kernel<<<static_cast<unsigned>((n_pad + 255) / 256), 256, 0, s>>>(words, perm, src_rows, n, n_pad,
-                                                                                    rad, ids);
+  gather_list_rows_kernel<<<static_cast<unsigned>((n_pad + 255) / 256), 256, 0, s>>>(perm, src_rows, n, n_pad, ids);
   return hipGetLastError();
 }
 

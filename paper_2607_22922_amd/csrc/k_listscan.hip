@@ -7,19 +7,18 @@
 // layout interval are one run of positions per sub-list).  The list plan
 // gives each query its sub-lists that hold selected rows (items) in
 // increasing order of lb, a lower bound on the distance of every row of the
-// item, with sdc, a lower bound on the query's distance to the item's
-// centroid (a row's own bound is sdc - sqrt(max w) (r + delta), r its
-// radius).  A query is scanned by `splits` workgroups of kScanWaves
+// item.  A query is scanned by `splits` workgroups of kScanWaves
 // wavefronts; the G = splits * kScanWaves wavefronts share its tiles by
 // position in the concatenation of its items' tiles (wavefront g takes the
 // positions congruent to g mod G), so each row is scored by exactly one
 // wavefront whatever each one skips.  A wavefront stops at the first item
 // (or in the middle of one) whose lb^2 * keep - abs exceeds its current k-th
-// distance: every later item has a bound at least as large.  It also skips
-// a row when the row's own bound does.  lb^2 * keep - abs never exceeds a
-// row's computed distance (the rounding allowances of the bound), so a
-// skipped row is one whose distance exceeds the cut and the top k is
-// unchanged.
+// distance: every later item has a bound at least as large.  lb^2 * keep -
+// abs never exceeds the computed distance of a row of the item (the
+// rounding allowances of the bound), so a skipped row is one whose distance
+// exceeds the cut and the top k is unchanged.  (A bound per row, from each
+// row's own radius, prunes about a quarter of the rows the items leave at
+// 50% selectivity on 10M x 48-byte codes, but costs more than it saves.)
 //
 // Per tile the work is the interval scan's: sum of M table entries in
 // groups of subspaces with early abandonment, candidates into per-wavefront
@@ -29,10 +28,12 @@
 // Query-wide union bound (k <= 2 G): a wavefront's own k-th key is loose
 // while it has seen only a tile or two of the nearest lists, so each
 // wavefront also keeps its two smallest full distances (two distinct rows)
-// in the query's 2 G global slots; the wavefronts scan disjoint rows, so the
-// k-th smallest slot is the distance of one of k distinct rows at or below
-// it, a bound on the query's k-th distance (published like a threshold, with
-// the largest id so rows at that distance stay eligible).
+// in the query's global slots, both in one 8-byte word stored whole (a
+// reader never sees one new and one old value, which could show one row
+// twice); the wavefronts scan disjoint rows, so the k-th smallest of the 2 G
+// values is the distance of one of k distinct rows at or below it, a bound
+// on the query's k-th distance (published like a threshold, with the
+// largest id so rows at that distance stay eligible).
 #include <climits>
 
 #include "ifvs_internal.h"
@@ -87,7 +88,6 @@ void list_scan_kernel(const ListScanArgs a) {
   const int k = a.k;
   const float* hdr = a.hdr + 4 * static_cast<size_t>(q);
   const int n_items = __float_as_int(hdr[0]);
-  const float sw = hdr[2], delta = hdr[3];
 
   // The query's table into LDS, noting negative or NaN entries (then partial
   // sums bound nothing: no abandonment and no skipping).
@@ -137,11 +137,11 @@ void list_scan_kernel(const ListScanArgs a) {
   int stop_at = n_items;   // items from here on are prunable
   uint64_t pend = 0;
   int v_r0 = 0, v_r1 = 0, v_t = 0;
-  float v_sdc = 0.0f, v_lb = 0.0f;
+  float v_lb = 0.0f;
   bool in_item = false;
   int i_r0 = 0, i_r1 = 0, i_t = 0, i_nt = 0, p = 0;
-  float i_sdc = 0.0f, i_lb = 0.0f;
-  auto next_tile = [&](int& t, uint64_t& mask, float& sdc) -> bool {
+  float i_lb = 0.0f;
+  auto next_tile = [&](int& t, uint64_t& mask) -> bool {
     for (;;) {
       if (in_item) {
         if (pruned(i_lb)) {
@@ -156,7 +156,6 @@ void list_scan_kernel(const ListScanArgs a) {
           p += G;
           const int row0 = t * 64;
           mask = bit_range(max(i_r0 - row0, 0), min(i_r1 - row0, 64));
-          sdc = i_sdc;
           return true;
         }
         in_item = false;
@@ -164,19 +163,20 @@ void list_scan_kernel(const ListScanArgs a) {
       if (pend == 0) {
         batch += 64;
         if (batch >= stop_at) return false;
+        // Every lane loads (lanes past the end reload the batch's first
+        // item) and every loaded value is used before the ballot, so the
+        // loads complete here and not at a later wait that would also hold
+        // the tile loads issued meanwhile.
         const int it = batch + lane;
-        bool ok = false, gone = false;
-        if (it < stop_at) {
-          v_r0 = a.it_r0[ib + it];
-          v_r1 = a.it_r1[ib + it];
-          v_t = a.it_t[ib + it];
-          v_sdc = a.it_sdc[ib + it];
-          v_lb = a.it_lb[ib + it];
-          const int nt = ((v_r1 - 1) >> 6) - (v_r0 >> 6) + 1;
-          const int off = (g - v_t) & gmask;   // first position of the item this wavefront takes
-          gone = pruned(v_lb);
-          ok = off < nt && !gone;
-        }
+        const int itc = it < stop_at ? it : batch;
+        v_r0 = a.it_r0[ib + itc];
+        v_r1 = a.it_r1[ib + itc];
+        v_t = a.it_t[ib + itc];
+        v_lb = a.it_lb[ib + itc];
+        const int nt = ((v_r1 - 1) >> 6) - (v_r0 >> 6) + 1;
+        const int off = (g - v_t) & gmask;   // first position of the item this wavefront takes
+        const bool gone = it < stop_at && pruned(v_lb);
+        bool ok = it < stop_at && off < nt && !gone;
         const uint64_t gm = __ballot(gone);
         if (gm != 0) {
           // the first prunable item ends the query's list for this wavefront
@@ -192,21 +192,19 @@ void list_scan_kernel(const ListScanArgs a) {
       i_r0 = __builtin_amdgcn_readlane(v_r0, j);
       i_r1 = __builtin_amdgcn_readlane(v_r1, j);
       i_t = __builtin_amdgcn_readlane(v_t, j);
-      i_sdc = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v_sdc), j));
       i_lb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v_lb), j));
       i_nt = ((i_r1 - 1) >> 6) - (i_r0 >> 6) + 1;
       p = i_t + ((g - i_t) & gmask);
       in_item = true;
     }
   };
-  auto load = [&](int t, uint32_t (&w)[kMW], float& r) {
+  auto load = [&](int t, uint32_t (&w)[kMW]) {
     const uint32_t* __restrict__ tile = a.codes_t + static_cast<size_t>(t) * (kMW * 64);
 #pragma unroll
     for (int j = 0; j < kMW; ++j) w[j] = tile[j * 64 + lane];
-    r = a.rad[static_cast<size_t>(t) * 64 + lane];
   };
-  const bool union_bound = k <= n_slots;
-  uint32_t* slots = a.slots + static_cast<size_t>(q) * kListSlots;
+  const bool union_bound = a.union_bound != 0 && k <= n_slots;
+  unsigned long long* pairs = reinterpret_cast<unsigned long long*>(a.slots + static_cast<size_t>(q) * kListSlots);
   uint32_t best1 = ~0u, best2 = ~0u;   // this wavefront's two smallest full distances
   auto publish = [&](uint64_t key) {
     if (key < published) {
@@ -251,24 +249,32 @@ void list_scan_kernel(const ListScanArgs a) {
         const bool crossed = (n1 < kth && best1 >= kth) || (n2 < kth && best2 >= kth);
         best1 = n1;
         best2 = n2;
-        if (lane < 2)
-          __hip_atomic_store(&slots[2 * g + lane], lane == 0 ? n1 : n2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (lane == 0)
+          __hip_atomic_store(&pairs[g], (static_cast<unsigned long long>(n2) << 32) | n1, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
         if (crossed) {
-          uint64_t v[kListSlots / 64];
+          // all kListSlots / 2 words are loaded (the unused ones hold all
+          // ones), together, with one wait; each lane reads its own words
+          constexpr int kW = kListSlots / 128;
+          unsigned long long pw[kW];
 #pragma unroll
-          for (int u = 0; u < kListSlots / 64; ++u) {
-            const int e = lane * (kListSlots / 64) + u;
-            const uint32_t sv =
-                e < n_slots ? __hip_atomic_load(&slots[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : ~0u;
-            v[u] = (static_cast<uint64_t>(sv) << 32) | 0xFFFFFFFFull;
+          for (int u = 0; u < kW; ++u)
+            pw[u] = __hip_atomic_load(&pairs[lane * kW + u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          uint64_t v[2 * kW];
+#pragma unroll
+          for (int u = 0; u < kW; ++u) {
+            const bool used = lane * kW + u < n_slots / 2;
+            v[2 * u] = (static_cast<uint64_t>(used ? static_cast<uint32_t>(pw[u]) : ~0u) << 32) | 0xFFFFFFFFull;
+            v[2 * u + 1] = (static_cast<uint64_t>(used ? static_cast<uint32_t>(pw[u] >> 32) : ~0u) << 32) |
+                           0xFFFFFFFFull;
           }
-          wave_bitonic_sort<kListSlots / 64>(v);
+          wave_bitonic_sort<2 * kW>(v);
           const int e = k - 1;
           uint64_t mine = v[0];
 #pragma unroll
-          for (int u = 1; u < kListSlots / 64; ++u)
-            if (u == e % (kListSlots / 64)) mine = v[u];
-          const uint64_t ub = shfl_u64(mine, e / (kListSlots / 64));
+          for (int u = 1; u < 2 * kW; ++u)
+            if (u == e % (2 * kW)) mine = v[u];
+          const uint64_t ub = shfl_u64(mine, e / (2 * kW));
           if ((ub >> 32) != 0xFFFFFFFFull) publish(ub);
         }
       }
@@ -276,16 +282,11 @@ void list_scan_kernel(const ListScanArgs a) {
     pool_push(pool, cnt, thr, key, cand, k, a.kpl, a.ids);
     publish(thr);
   };
-  auto sum_tile = [&](int t, uint64_t mask, float sdc, const uint32_t (&w)[kMW], float rad) {
-    refresh();
+  auto sum_tile = [&](int t, uint64_t mask, const uint32_t (&w)[kMW]) {
     if constexpr (kCount) {
       if (lane == 0) atomicAdd(&s_hist[0], 1u);
     }
     bool live = __builtin_amdgcn_inverse_ballot_w64(mask);
-    if (monotone && live) {
-      const float lb = __fsub_rn(sdc, __fmul_rn(__fadd_rn(rad, delta), sw));
-      if (pruned(lb)) live = false;
-    }
     float d = 0.0f;
     // (most tiles lose every row to the bound or to the first groups: the
     // loop ends as soon as no lane is live)
@@ -316,34 +317,38 @@ void list_scan_kernel(const ListScanArgs a) {
 
   // Register sets in a ring: step i refills the set summed in the step
   // before with the next tile, then sums set i.  Tiles come in generation
-  // order, so the first set without one ends the scan.
+  // order, so the first set without one ends the scan.  The loads are issued
+  // on every path (tile 0 stands in when there is no next tile, in bounds
+  // and unused), so the compiler's wait counts never make a sum wait for the
+  // tile loaded after it.
+  // The bound is refreshed once per round of kDepth tiles (a bound a few
+  // tiles old is looser, never wrong).
   uint32_t ws[kDepth][kMW];
-  float rs[kDepth], ss[kDepth];
   int ts[kDepth];
   uint64_t ms[kDepth];
   bool hs[kDepth];
 #pragma unroll
   for (int i = 0; i < kDepth; ++i) {
-    rs[i] = ss[i] = 0.0f;
     ts[i] = 0;
     ms[i] = 0;
     hs[i] = false;
   }
 #pragma unroll
   for (int i = 0; i < kDepth - 1; ++i) {
-    hs[i] = next_tile(ts[i], ms[i], ss[i]);
-    if (hs[i]) load(ts[i], ws[i], rs[i]);
+    hs[i] = next_tile(ts[i], ms[i]);
+    load(hs[i] ? ts[i] : 0, ws[i]);
   }
   for (;;) {
     gview = gnext;
     gnext = __hip_atomic_load(a.gthr + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    refresh();
 #pragma unroll
     for (int i = 0; i < kDepth; ++i) {
       const int j = (i + kDepth - 1) % kDepth;
-      hs[j] = next_tile(ts[j], ms[j], ss[j]);
-      if (hs[j]) load(ts[j], ws[j], rs[j]);
+      hs[j] = next_tile(ts[j], ms[j]);
+      load(hs[j] ? ts[j] : 0, ws[j]);
       if (!hs[i]) goto scanned;
-      sum_tile(ts[i], ms[i], ss[i], ws[i], rs[i]);
+      sum_tile(ts[i], ms[i], ws[i]);
     }
   }
 scanned:

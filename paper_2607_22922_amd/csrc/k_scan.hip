@@ -139,10 +139,11 @@ void scan_kernel(const ScanArgs a) {
   unsigned long long* s_thr = reinterpret_cast<unsigned long long*>(
       pools + static_cast<size_t>(kScanWaves) * QT * a.pool_stride);   // smallest k-th key published in this workgroup
   uint32_t* s_bad = reinterpret_cast<uint32_t*>(s_thr + QT);   // [wave][qi]: the wave saw a negative or NaN entry
-  // [qi][wave][kScanPub]: each wavefront's smallest distances (order-preserving
-  // bits), only ever lowered (the area holds 8-byte words; half is used)
+  // [qi][wave]: each wavefront's two smallest distances (order-preserving
+  // bits, the second in the high half) in one 8-byte word, stored whole so a
+  // reader never sees one new and one old value (the area holds kScanPub
+  // words per wavefront; the first is used)
   unsigned long long* s_pub = reinterpret_cast<unsigned long long*>(s_bad + kScanWaves * QT);
-  uint32_t* s_best = reinterpret_cast<uint32_t*>(s_pub);
   // [wave][kScanSeed]: distances (order-preserving bits) of the seed candidates
   uint32_t* s_seed = reinterpret_cast<uint32_t*>(s_pub + QT * kScanWaves * kScanPub);
   // [65]: the counting build's histogram of table reads by active lanes
@@ -604,16 +605,19 @@ void scan_kernel(const ScanArgs a) {
         const bool crossed = (n1 < kth && best1[qi] >= kth) || (n2 < kth && best2[qi] >= kth);
         best1[qi] = n1;
         best2[qi] = n2;
-        uint32_t* slots = s_best + qi * kScanWaves * kScanPub;
-        if (lane < kScanPub)
-          __hip_atomic_store(&slots[wave * kScanPub + lane], lane == 0 ? n1 : n2, __ATOMIC_RELAXED,
+        unsigned long long* pairs = s_pub + qi * kScanWaves;
+        if (lane == 0)
+          __hip_atomic_store(&pairs[wave], (static_cast<unsigned long long>(n2) << 32) | n1, __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_WORKGROUP);
         if (crossed) {
           // Rank of each of the 16 slots (ties by slot index); the slot of
-          // rank k - 1 is the k-th smallest.
-          const uint32_t v = lane < kScanWaves * kScanPub
-                                 ? __hip_atomic_load(&slots[lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)
-                                 : ~0u;
+          // rank k - 1 is the k-th smallest.  Lanes 2w and 2w + 1 read
+          // wavefront w's word in the same instruction, so they see one pair.
+          const unsigned long long pw =
+              lane < kScanWaves * kScanPub
+                  ? __hip_atomic_load(&pairs[lane >> 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)
+                  : ~0ull;
+          const uint32_t v = static_cast<uint32_t>((lane & 1) ? pw >> 32 : pw);
           int rank = 0;
 #pragma unroll
           for (int j = 0; j < kScanWaves * kScanPub; ++j) {

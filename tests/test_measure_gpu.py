@@ -32,6 +32,19 @@ def _case(B, N=20_037, M=48, nq=40):
     return ix, idx, q, preds, n_sel
 
 
+def _interval_tiles(ix, preds):
+    """64-row tiles of the clustered layout (rows sorted by the attribute)
+    that hold a row of each query's interval, summed over the queries."""
+    a = np.sort(ix["attrs"][0].cpu().numpy())
+    tiles = 0
+    for p in preds:
+        (_, lo, hi), = p
+        r0, r1 = int(np.searchsorted(a, lo)), int(np.searchsorted(a, hi))
+        if r1 > r0:
+            tiles += (r1 - 1) // 64 - r0 // 64 + 1
+    return tiles
+
+
 def _counted(B, idx, preds, lut):
     idx.set_option(B.OPT_COUNT_READS, 1)
     idx.read_scan_reads()
@@ -53,9 +66,9 @@ def test_counting_scan_same_results_and_every_read_counted(B):
     ids1, d1, hist = _counted(B, idx, preds, lut)
     torch.cuda.synchronize()
     assert torch.equal(ids0, ids1) and torch.equal(d0.view(torch.int32), d1.view(torch.int32))
-    assert hist[0] == 0
-    assert sum(n * hist[n] for n in range(65)) == M * n_sel
-    assert sum(hist) % 8 == 0          # reads come in groups of 8 subspaces at M = 48
+    assert hist[0] == _interval_tiles(ix, preds)    # entry 0: every tile of each interval, once
+    assert sum(n * hist[n] for n in range(1, 65)) == M * n_sel
+    assert sum(hist[1:]) % 8 == 0      # reads come in groups of 8 subspaces at M = 48
 
 
 def test_counting_scan_with_early_abandonment(B):
@@ -67,7 +80,8 @@ def test_counting_scan_with_early_abandonment(B):
     ids1, d1, hist = _counted(B, idx, preds, lut)
     torch.cuda.synchronize()
     assert torch.equal(ids0, ids1) and torch.equal(d0.view(torch.int32), d1.view(torch.int32))
-    lookups = sum(n * hist[n] for n in range(65))
+    lookups = sum(n * hist[n] for n in range(1, 65))
+    assert hist[0] == _interval_tiles(ix, preds)
     # the first group of 8 subspaces is read for every selected row, the rest
     # only while a row can still enter the top k
     assert 8 * n_sel <= lookups <= M * n_sel
