@@ -142,6 +142,9 @@ struct CoarseLists {
   float* it_lb = nullptr;
   float* hdr = nullptr;          // [max_batch][4]
   uint32_t* slots = nullptr;     // [max_batch][kListSlots]
+  int4* jobs = nullptr;          // [max_batch * kListJobs] list scan job table
+  int32_t* n_keys = nullptr;     // [max_batch] partial keys written per query position
+  int32_t* job_ctr = nullptr;    // [2] next job, job count
 
   void release() {
     for (void* p : {static_cast<void*>(words), static_cast<void*>(band), static_cast<void*>(cc_t),
@@ -150,7 +153,8 @@ struct CoarseLists {
                     static_cast<void*>(lrow),
                     static_cast<void*>(tmp_r0), static_cast<void*>(tmp_r1), static_cast<void*>(it_r0),
                     static_cast<void*>(it_r1), static_cast<void*>(it_t),
-                    static_cast<void*>(it_lb), static_cast<void*>(hdr), static_cast<void*>(slots)})
+                    static_cast<void*>(it_lb), static_cast<void*>(hdr), static_cast<void*>(slots),
+                    static_cast<void*>(jobs), static_cast<void*>(n_keys), static_cast<void*>(job_ctr)})
       if (p) (void)hipFree(p);
     *this = CoarseLists{};
   }
@@ -1205,14 +1209,11 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   // (no residual clauses); automatic for batches whose widest interval spans
   // at least kCoarseAutoTiles 64-row tiles.
   const CoarseLists& cl = idx->coarse;
-  // Workgroups per query: a power of two, at most 16, about 2048 in all
-  // (measured on 10M x 48-byte codes, 256 queries: 8 per query 25% faster
-  // than 4 at 50% selectivity).
-  int list_splits = 1;
-  {
-    const int want = idx->opt_splits > 0 ? idx->opt_splits : std::max(1, (2048 + nq - 1) / nq);
-    while (list_splits * 2 <= std::min(want, kListSlots / (2 * kScanWaves))) list_splits *= 2;
-  }
+  // Jobs per query: at most kListJobs (IFVS_OPT_SPLITS lowers the cap), as
+  // the partial lists have room.
+  int list_jobs = std::min(kListJobs, idx->opt_splits > 0 ? idx->opt_splits : kListJobs);
+  while (list_jobs > 1 && static_cast<size_t>(nq) * list_jobs * kScanWaves * k > ws.partial_keys) --list_jobs;
+  const int list_splits = list_jobs;
   const bool list_mode =
       bounded && cl.words && idx->opt_coarse != 1 && !static_scratch && !need_bitmap &&
       list_scan_supported(idx->m, lut_dtype) &&
@@ -1279,6 +1280,19 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     pa.hdr = cl.hdr;
     pa.slots = cl.slots;
     IFVS_LAUNCH(idx, kStCoarse, s, "launching list plan kernel", launch_list_plan(pa, lut_dtype, s));
+    ListJobArgs ja{};
+    ja.hdr = cl.hdr;
+    ja.qorder = ws.qorder;
+    ja.nq = nq;
+    ja.np2 = 1;
+    while (ja.np2 < nq) ja.np2 *= 2;
+    ja.k = k;
+    ja.max_jobs = list_jobs;
+    ja.jobs = cl.jobs;
+    ja.n_keys = cl.n_keys;
+    ja.job_next = cl.job_ctr;
+    ja.job_total = cl.job_ctr + 1;
+    IFVS_LAUNCH(idx, kStCoarse, s, "launching list job table kernel", launch_list_jobs(ja, s));
     ListScanArgs sa{};
     sa.codes_t = cl.codes_t;
     sa.ids = cl.ids;
@@ -1286,8 +1300,11 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     sa.mw = idx->mw;
     sa.lut = lut;
     sa.nq = nq;
-    sa.splits = list_splits;
+    sa.max_jobs = list_jobs;
     sa.qorder = ws.qorder;
+    sa.jobs = cl.jobs;
+    sa.job_next = cl.job_ctr;
+    sa.job_total = cl.job_ctr + 1;
     sa.it_r0 = cl.it_r0;
     sa.it_r1 = cl.it_r1;
     sa.it_t = cl.it_t;
@@ -1306,8 +1323,9 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     sa.union_bound = idx->opt_shared_bound == 1 ? 0 : 1;
     IFVS_LAUNCH(idx, kStScan, s, "launching list scan kernel", launch_list_scan(sa, lut_dtype, s));
     IFVS_LAUNCH(idx, kStMerge, s, "launching top-k merge kernel",
-                launch_topk_merge(ws.partials, nq, static_cast<int64_t>(list_splits) * kScanWaves * k, k, ws.iv, 0,
-                                  static_cast<int64_t>(kScanWaves) * k, ws.qorder, ids_out, dist_out, s));
+                launch_topk_merge(ws.partials, nq, static_cast<int64_t>(list_jobs) * kScanWaves * k, k, ws.iv, 0,
+                                  static_cast<int64_t>(kScanWaves) * k, ws.qorder, ids_out, dist_out, s,
+                                  cl.n_keys));
     if (bitmap_out) {
       if (ifvs_status st = filter_into_workspace(idx, ws, nq, false, false, s); st != IFVS_OK) return st;
       if (ifvs_status st = copy_bitmaps_out(idx, ws, nq, bitmap_out, s); st != IFVS_OK) return st;
@@ -2066,6 +2084,12 @@ ifvs_status ifvs_build_coarse(ifvs_index* idx, int32_t n_centroids, int32_t iter
   if (ifvs_status st = alloc(&nl.slots, static_cast<size_t>(idx->max_batch) * kListSlots, "list scan bound slots");
       st != IFVS_OK)
     return cleanup(st);
+  if (ifvs_status st = alloc(&nl.jobs, static_cast<size_t>(idx->max_batch) * kListJobs, "list scan jobs");
+      st != IFVS_OK)
+    return cleanup(st);
+  if (ifvs_status st = alloc(&nl.n_keys, static_cast<size_t>(idx->max_batch), "list scan jobs"); st != IFVS_OK)
+    return cleanup(st);
+  if (ifvs_status st = alloc(&nl.job_ctr, 2, "list scan jobs"); st != IFVS_OK) return cleanup(st);
   const struct {
     void* dst;
     const void* src;

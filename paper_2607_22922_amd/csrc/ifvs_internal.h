@@ -299,14 +299,31 @@ size_t list_plan_lds_bytes(int m, int lut_dtype, int C);
 hipError_t launch_list_plan(const ListPlanArgs& a, int lut_dtype, hipStream_t s);
 
 // List scan (k_listscan.hip): the Rank and Select stages over the items of
-// each query, nearest list first, skipping lists and rows by the bound.
+// each query in bound order, persistent workgroups taking jobs (chunks of a
+// query's tiles) from a table built after the plan.
+constexpr int kListJobs = 16;     // most jobs (and partial-list slots) per query
+constexpr int kJobTiles = 512;    // tiles per job before a query is split further
+struct ListJobArgs {
+  const float* hdr;         // [nq][4] list plan headers ([1]: tiles to scan, int bits)
+  const int32_t* qorder;
+  int nq, np2;              // np2: power of two >= nq
+  int k, max_jobs;          // max_jobs <= kListJobs
+  int4* jobs;               // [nq * kListJobs] (position, chunk, first tile position, end)
+  int32_t* n_keys;          // [positions] partial keys written per position
+  int* job_next;
+  int* job_total;
+};
+hipError_t launch_list_jobs(const ListJobArgs& a, hipStream_t s);
 struct ListScanArgs {
   const uint32_t* codes_t;  // [n_tiles][mw][64] list-order code words
   const int32_t* ids;       // list position -> original id
   int m, mw;
   const void* lut;          // [nq][m][256] by original query
-  int nq, splits;           // workgroups per query position
+  int nq, max_jobs;         // max_jobs: the partial-list slots per query (<= kListJobs)
   const int32_t* qorder;    // position -> original query
+  const int4* jobs;         // job table (launch_list_jobs)
+  int* job_next;            // job counter (0 before the scan)
+  const int* job_total;
   const int32_t* it_r0;
   const int32_t* it_r1;
   const int32_t* it_t;
@@ -315,13 +332,13 @@ struct ListScanArgs {
   int C;                    // item stride per query (sub-lists)
   float keep, abs_m;
   int k, pool_stride, kpl;
-  uint64_t* partials;       // [positions][splits][kScanWaves][k]
+  uint64_t* partials;       // [positions][max_jobs][kScanWaves][k]
   uint64_t* gthr;           // [nq] shared thresholds, all ones before the scan
   uint32_t* slots;          // [nq][kListSlots] union-bound slots, all ones before the scan (list plan)
   unsigned long long* lookup_hist;  // [65] non-null: the counting build (table reads by lanes, [0] tiles)
   int union_bound;          // 1: the query-wide union bound of the wavefronts' best distances
 };
-constexpr int kListSlots = 2 * kScanWaves * 16;   // two per wavefront of at most 16 workgroups per query
+constexpr int kListSlots = 2 * kScanWaves * kListJobs;   // two per wavefront of each job of a query
 bool list_scan_supported(int m, int lut_dtype);
 size_t list_scan_lds_bytes(int m, int lut_dtype, int pool_stride);
 hipError_t launch_list_scan(const ListScanArgs& a, int lut_dtype, hipStream_t s);
@@ -334,7 +351,7 @@ hipError_t lds_gather_probe(int active, int iters, int wg_per_cu, int reps, hipS
 hipError_t launch_topk_merge(const uint64_t* partials, int nq, int64_t per_query, int k,
                              const int64_t* iv, int64_t cell_tiles, int64_t slot_keys,
                              const int32_t* qorder, int32_t* ids_out, float* dist_out,
-                             hipStream_t s);
+                             hipStream_t s, const int32_t* n_keys = nullptr);   // n_keys: keys per position
 
 // Symmetric distance computation (k_sdc.hip): the codeword table
 // T[m][a][b] (at load) and a query's table, the rows T[m][enc(q)_m] laid

@@ -351,8 +351,10 @@ __global__ __launch_bounds__(256) void gather_list_rows_kernel(const int32_t* __
 // has a bound at least as large.  Before them come, with no bound (NaN), the
 // sub-lists of the query's nearest centroid that has selected rows (its
 // rows hold the query's nearest rows as a rule, so the scan's k-th distance
-// is tight from its first tiles) and any sub-list whose bound is NaN.  T =
-// the 64-row tiles the items before it touch.
+// is tight from its first tiles) and any sub-list whose bound is NaN.
+// Header: the item count; T, the 64-row tiles of the items before the first
+// one the seed's k-th distance prunes (of all items when there is no seed or
+// a table entry is negative or NaN); sqrt(max w); delta.
 //
 // Seed: the distances (summed exactly as the scan sums them) of the
 // selected rows among the first kSeedRows positions of the list of the
@@ -373,6 +375,9 @@ __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
   __shared__ int s_count;
   __shared__ unsigned long long s_near;   // (sdc bits, centroid) of the nearest selected centroid
   __shared__ unsigned long long s_first;  // (sdc bits, centroid) of the nearest centroid
+  __shared__ int s_lut_bad;               // a table entry is negative or NaN: no pruning
+  __shared__ int s_stop;                  // the first item the seed's bound prunes
+  __shared__ uint32_t s_seed_kth;         // the seed's k-th distance (order-preserving bits)
   const int q = blockIdx.x;
   const int tid = threadIdx.x;
   const int64_t x0 = a.iv[2 * q], x1 = a.iv[2 * q + 1];
@@ -391,12 +396,23 @@ __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
   // Phase 1: the table, then each centroid's bound.
   const LutT* lut = static_cast<const LutT*>(a.lut) + static_cast<size_t>(q) * a.m * kKsub;
   const int lut_vecs = a.m * kKsub * static_cast<int>(sizeof(LutT)) / 16;
-  for (int v = tid; v < lut_vecs; v += 1024)
-    reinterpret_cast<uint4*>(s_lut)[v] = reinterpret_cast<const uint4*>(lut)[v];
   if (tid == 0) {
     s_count = 0;
     s_near = ~0ull;
     s_first = ~0ull;
+    s_lut_bad = 0;
+    s_stop = 0x7FFFFFFF;
+  }
+  __syncthreads();
+  {
+    bool bad = false;
+    for (int v = tid; v < lut_vecs; v += 1024) {
+      const uint4 x = reinterpret_cast<const uint4*>(lut)[v];
+      reinterpret_cast<uint4*>(s_lut)[v] = x;
+      const LutT* xe = reinterpret_cast<const LutT*>(&x);
+      for (int e = 0; e < 16 / static_cast<int>(sizeof(LutT)); ++e) bad = bad || !(widen(xe[e]) >= 0.0f);
+    }
+    if (bad) s_lut_bad = 1;
   }
   __syncthreads();
   for (int c = tid; c < C; c += 1024) {
@@ -453,6 +469,7 @@ __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
         __syncthreads();
       }
     }
+    if (tid == 0) s_seed_kth = a.k <= kSeedRows ? s_seed[a.k - 1] : ~0u;
     if (tid == 0 && a.k <= kSeedRows && s_seed[a.k - 1] != ~0u)
       atomicMin(reinterpret_cast<unsigned long long*>(a.gthr + q),
                 (static_cast<unsigned long long>(s_seed[a.k - 1]) << 32) | 0xFFFFFFFFull);
@@ -553,9 +570,22 @@ __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
     __syncthreads();
   }
   for (int i = tid; i < n_items; i += 1024) a.it_t[base + i] = i == 0 ? 0 : s_nt[i - 1];
+  // T: the items' bounds rise in order, so the first item the seed's k-th
+  // distance prunes (the test the scan makes, whose bound is never looser)
+  // ends what any scan of the query visits.
+  if (s_lut_bad == 0 && s_seed_kth != ~0u) {
+    const float cut = from_ordered_bits(s_seed_kth);
+    for (int i = tid; i < n_items; i += 1024) {
+      const uint32_t ob = s_key[i] & ~uint32_t{kItemMask};
+      const float lb = ob == 0u ? __builtin_nanf("") : from_ordered_bits(ob);
+      if (lb > 0.0f && __fsub_rn(__fmul_rn(__fmul_rn(lb, lb), a.keep), a.abs_m) > cut) atomicMin(&s_stop, i);
+    }
+  }
+  __syncthreads();
   if (tid == 0) {
+    const int stop = min(s_stop, n_items);
     hdr[0] = __int_as_float(n_items);
-    hdr[1] = __int_as_float(n_items > 0 ? s_nt[n_items - 1] : 0);
+    hdr[1] = __int_as_float(stop > 0 ? s_nt[stop - 1] : 0);
     hdr[2] = sw;
     hdr[3] = delta;
   }

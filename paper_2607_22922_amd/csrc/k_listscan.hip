@@ -7,11 +7,14 @@
 // layout interval are one run of positions per sub-list).  The list plan
 // gives each query its sub-lists that hold selected rows (items) in
 // increasing order of lb, a lower bound on the distance of every row of the
-// item.  A query is scanned by `splits` workgroups of kScanWaves
-// wavefronts; the G = splits * kScanWaves wavefronts share its tiles by
-// position in the concatenation of its items' tiles (wavefront g takes the
-// positions congruent to g mod G), so each row is scored by exactly one
-// wavefront whatever each one skips.  A wavefront stops at the first item
+// item.  A query's work is the concatenation of its items' tiles up to the
+// first item that the plan's seed bound prunes; the job table splits it into
+// up to kListJobs chunks of about kJobTiles tiles or more (the queries with
+// the most tiles first) and a persistent grid of workgroups takes the jobs
+// from a counter, so a query with many tiles no longer holds the batch up.
+// In a job the kScanWaves wavefronts share the chunk by position (wavefront
+// w takes the positions congruent to w mod kScanWaves), so each row is scored
+// by exactly one wavefront whatever each one skips.  A wavefront stops at the first item
 // (or in the middle of one) whose lb^2 * keep - abs exceeds its current k-th
 // distance: every later item has a bound at least as large.  lb^2 * keep -
 // abs never exceeds the computed distance of a row of the item (the
@@ -25,16 +28,20 @@
 // pools of row keys resolved to original ids at compaction, thresholds
 // shared through LDS and a per-query global word.
 //
-// Query-wide union bound (k <= 2 G): a wavefront's own k-th key is loose
+// Query-wide union bound (k <= kListSlots): a wavefront's own k-th key is loose
 // while it has seen only a tile or two of the nearest lists, so each
 // wavefront also keeps its two smallest full distances (two distinct rows)
-// in the query's global slots, both in one 8-byte word stored whole (a
-// reader never sees one new and one old value, which could show one row
-// twice); the wavefronts scan disjoint rows, so the k-th smallest of the 2 G
-// values is the distance of one of k distinct rows at or below it, a bound
+// in the query's global slots (one per wavefront of each job), both in one
+// 8-byte word stored whole (a reader never sees one new and one old value,
+// which could show one row twice); the wavefronts scan disjoint rows, so the
+// k-th smallest of the kListSlots values is the distance of one of k distinct rows at or below it, a bound
 // on the query's k-th distance (published like a threshold, with the
 // largest id so rows at that distance stay eligible).
+#include <algorithm>
 #include <climits>
+#include <map>
+#include <mutex>
+#include <tuple>
 
 #include "ifvs_internal.h"
 #include "topk_device.h"
@@ -64,6 +71,13 @@ constexpr int list_waves_per_eu() {
 // lanes (entries 1..64 of a.lookup_hist) and the code tiles summed (entry 0).
 // kDepth register sets: the tiles of kDepth - 1 of them are in flight while
 // one is summed.
+//
+// Persistent: as many workgroups as the chip holds at once take jobs from a
+// global counter (the job table lists the heaviest queries first).  Job
+// (pos, c, p0, p1): chunk c of the query at position pos, the positions
+// [p0, p1) of its items' concatenated tiles; wavefront w takes the positions
+// congruent to w mod kScanWaves.  Each (job, wavefront) has its own partial
+// list ([pos][c][wave][k]) and union-bound word ([q][c * kScanWaves + wave]).
 template <int MT, typename LutT, bool kCount = false, int kDepth = 2>
 __global__ __launch_bounds__(kScanWaves * 64) __attribute__((amdgpu_waves_per_eu(list_waves_per_eu<MT, LutT>())))
 void list_scan_kernel(const ListScanArgs a) {
@@ -73,6 +87,7 @@ void list_scan_kernel(const ListScanArgs a) {
   constexpr int kVec = 16 / sizeof(LutT);
   constexpr int kVecQ = MT * kKsub / kVec;
   __shared__ __align__(16) LutT s_lut[MT * kKsub];
+  __shared__ int4 s_job;
   extern __shared__ __align__(16) unsigned char smem[];
   uint64_t* pools = reinterpret_cast<uint64_t*>(smem);
   unsigned long long* s_thr = reinterpret_cast<unsigned long long*>(pools + kScanWaves * a.pool_stride);
@@ -81,285 +96,393 @@ void list_scan_kernel(const ListScanArgs a) {
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int pos = blockIdx.x / a.splits, split = blockIdx.x % a.splits;
-  const int n_slots = 2 * kScanWaves * a.splits;
-  if (pos >= a.nq) return;
-  const int q = a.qorder[pos];
   const int k = a.k;
-  const float* hdr = a.hdr + 4 * static_cast<size_t>(q);
-  const int n_items = __float_as_int(hdr[0]);
-
-  // The query's table into LDS, noting negative or NaN entries (then partial
-  // sums bound nothing: no abandonment and no skipping).
-  const uint4* src = reinterpret_cast<const uint4*>(static_cast<const LutT*>(a.lut) + static_cast<size_t>(q) * MT * kKsub);
-  bool bad = false;
-  for (int v = threadIdx.x; v < kVecQ; v += kThreads) {
-    const uint4 x = src[v];
-    reinterpret_cast<uint4*>(s_lut)[v] = x;
-    const LutT* xe = reinterpret_cast<const LutT*>(&x);
-#pragma unroll
-    for (int e = 0; e < kVec; ++e) bad = bad || !(widen(xe[e]) >= 0.0f);
-  }
-  const bool wave_bad = __ballot(bad) != 0;
-  if (lane == 0) s_bad[wave] = wave_bad ? 1u : 0u;
-  if (threadIdx.x == 0) *s_thr = kNoKey;
   if constexpr (kCount) {
     if (threadIdx.x < 65) s_hist[threadIdx.x] = 0;
   }
-  __syncthreads();
+  int cur_q = -1;
   bool monotone = true;
-#pragma unroll
-  for (int w = 0; w < kScanWaves; ++w) monotone = monotone && s_bad[w] == 0;
-
   uint64_t* pool = pools + static_cast<size_t>(wave) * a.pool_stride;
-  int cnt = 0;
-  uint64_t thr = kNoKey, published = kNoKey, gview = kNoKey, gnext = kNoKey, bound = kNoKey;
-  float cut = __builtin_nanf("");
-  // bound = min(own k-th key, workgroup's, query's); cut its distance (NaN
-  // while there is none, or when the table is not monotone).
-  auto refresh = [&]() {
-    const uint64_t blk = __hip_atomic_load(s_thr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    uint64_t b = thr < blk ? thr : blk;
-    b = b < gview ? b : gview;
-    bound = b;
-    cut = monotone ? from_ordered_bits(static_cast<uint32_t>(bound >> 32)) : __builtin_nanf("");
-  };
-  auto pruned = [&](float lb) -> bool {
-    return lb > 0.0f && __fsub_rn(__fmul_rn(__fmul_rn(lb, lb), a.keep), a.abs_m) > cut;
-  };
+  const int total_jobs = *a.job_total;
 
-  // Tile generator over the query's items.
-  // G is a power of two (splits is), so positions reduce with a mask.
-  const int G = kScanWaves * a.splits, g = split * kScanWaves + wave;
-  const int gmask = G - 1;
-  const size_t ib = static_cast<size_t>(q) * a.C;
-  int batch = -64;
-  int stop_at = n_items;   // items from here on are prunable
-  uint64_t pend = 0;
-  int v_r0 = 0, v_r1 = 0, v_t = 0;
-  float v_lb = 0.0f;
-  bool in_item = false;
-  int i_r0 = 0, i_r1 = 0, i_t = 0, i_nt = 0, p = 0;
-  float i_lb = 0.0f;
-  auto next_tile = [&](int& t, uint64_t& mask) -> bool {
-    for (;;) {
-      if (in_item) {
-        if (pruned(i_lb)) {
-          // this item and every later one
-          stop_at = 0;
-          pend = 0;
-          in_item = false;
-          return false;
-        }
-        if (p < i_t + i_nt) {
-          t = (i_r0 >> 6) + (p - i_t);
-          p += G;
-          const int row0 = t * 64;
-          mask = bit_range(max(i_r0 - row0, 0), min(i_r1 - row0, 64));
-          return true;
-        }
-        in_item = false;
-      }
-      if (pend == 0) {
-        batch += 64;
-        if (batch >= stop_at) return false;
-        // Every lane loads (lanes past the end reload the batch's first
-        // item) and every loaded value is used before the ballot, so the
-        // loads complete here and not at a later wait that would also hold
-        // the tile loads issued meanwhile.
-        const int it = batch + lane;
-        const int itc = it < stop_at ? it : batch;
-        v_r0 = a.it_r0[ib + itc];
-        v_r1 = a.it_r1[ib + itc];
-        v_t = a.it_t[ib + itc];
-        v_lb = a.it_lb[ib + itc];
-        const int nt = ((v_r1 - 1) >> 6) - (v_r0 >> 6) + 1;
-        const int off = (g - v_t) & gmask;   // first position of the item this wavefront takes
-        const bool gone = it < stop_at && pruned(v_lb);
-        bool ok = it < stop_at && off < nt && !gone;
-        const uint64_t gm = __ballot(gone);
-        if (gm != 0) {
-          // the first prunable item ends the query's list for this wavefront
-          const int j0 = __builtin_ctzll(gm);
-          stop_at = batch + j0;
-          ok = ok && lane < j0;
-        }
-        pend = __ballot(ok);
-        continue;
-      }
-      const int j = __builtin_ctzll(pend);
-      pend &= pend - 1;
-      i_r0 = __builtin_amdgcn_readlane(v_r0, j);
-      i_r1 = __builtin_amdgcn_readlane(v_r1, j);
-      i_t = __builtin_amdgcn_readlane(v_t, j);
-      i_lb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v_lb), j));
-      i_nt = ((i_r1 - 1) >> 6) - (i_r0 >> 6) + 1;
-      p = i_t + ((g - i_t) & gmask);
-      in_item = true;
-    }
-  };
-  auto load = [&](int t, uint32_t (&w)[kMW]) {
-    const uint32_t* __restrict__ tile = a.codes_t + static_cast<size_t>(t) * (kMW * 64);
-#pragma unroll
-    for (int j = 0; j < kMW; ++j) w[j] = tile[j * 64 + lane];
-  };
-  const bool union_bound = a.union_bound != 0 && k <= n_slots;
-  unsigned long long* pairs = reinterpret_cast<unsigned long long*>(a.slots + static_cast<size_t>(q) * kListSlots);
-  uint32_t best1 = ~0u, best2 = ~0u;   // this wavefront's two smallest full distances
-  auto publish = [&](uint64_t key) {
-    if (key < published) {
-      published = key;
-      if (lane == 0) {
-        atomicMin(s_thr, static_cast<unsigned long long>(key));
-        __hip_atomic_fetch_min(a.gthr + q, key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-    }
-  };
-  auto consider = [&](bool act, float d, int t) {
-    uint64_t key = kNoKey;
-    bool cand = false;
-    if (act) {
-      const uint32_t db = ordered_bits(d);
-      if (db <= static_cast<uint32_t>(bound >> 32)) {
-        key = row_key(db, static_cast<uint32_t>(t * 64 + lane));
-        cand = true;
-      }
-    }
-    if (union_bound) {
-      // The step's two smallest distances (pairs merged across lanes), then
-      // the wavefront's two smallest so far.
-      uint32_t x1 = act ? ordered_bits(d) : ~0u, x2 = ~0u;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t y1 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(x1), o, 64));
-        const uint32_t y2 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(x2), o, 64));
-        const uint32_t hi = x1 > y1 ? x1 : y1;
-        const uint32_t lo2 = x2 < y2 ? x2 : y2;
-        x1 = x1 < y1 ? x1 : y1;
-        x2 = hi < lo2 ? hi : lo2;
-      }
-      const uint32_t hi = best1 > x1 ? best1 : x1;
-      const uint32_t lo2 = best2 < x2 ? best2 : x2;
-      const uint32_t n1 = best1 < x1 ? best1 : x1;
-      const uint32_t n2 = hi < lo2 ? hi : lo2;
-      if (n1 < best1 || n2 < best2) {
-        // The k-th smallest slot only falls when a slot drops from at or
-        // above the published value to below it.
-        const uint32_t kth = static_cast<uint32_t>(published >> 32);
-        const bool crossed = (n1 < kth && best1 >= kth) || (n2 < kth && best2 >= kth);
-        best1 = n1;
-        best2 = n2;
-        if (lane == 0)
-          __hip_atomic_store(&pairs[g], (static_cast<unsigned long long>(n2) << 32) | n1, __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
-        if (crossed) {
-          // all kListSlots / 2 words are loaded (the unused ones hold all
-          // ones), together, with one wait; each lane reads its own words
-          constexpr int kW = kListSlots / 128;
-          unsigned long long pw[kW];
-#pragma unroll
-          for (int u = 0; u < kW; ++u)
-            pw[u] = __hip_atomic_load(&pairs[lane * kW + u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          uint64_t v[2 * kW];
-#pragma unroll
-          for (int u = 0; u < kW; ++u) {
-            const bool used = lane * kW + u < n_slots / 2;
-            v[2 * u] = (static_cast<uint64_t>(used ? static_cast<uint32_t>(pw[u]) : ~0u) << 32) | 0xFFFFFFFFull;
-            v[2 * u + 1] = (static_cast<uint64_t>(used ? static_cast<uint32_t>(pw[u] >> 32) : ~0u) << 32) |
-                           0xFFFFFFFFull;
-          }
-          wave_bitonic_sort<2 * kW>(v);
-          const int e = k - 1;
-          uint64_t mine = v[0];
-#pragma unroll
-          for (int u = 1; u < 2 * kW; ++u)
-            if (u == e % (2 * kW)) mine = v[u];
-          const uint64_t ub = shfl_u64(mine, e / (2 * kW));
-          if ((ub >> 32) != 0xFFFFFFFFull) publish(ub);
-        }
-      }
-    }
-    pool_push(pool, cnt, thr, key, cand, k, a.kpl, a.ids);
-    publish(thr);
-  };
-  auto sum_tile = [&](int t, uint64_t mask, const uint32_t (&w)[kMW]) {
-    if constexpr (kCount) {
-      if (lane == 0) atomicAdd(&s_hist[0], 1u);
-    }
-    bool live = __builtin_amdgcn_inverse_ballot_w64(mask);
-    float d = 0.0f;
-    // (most tiles lose every row to the bound or to the first groups: the
-    // loop ends as soon as no lane is live)
-#pragma unroll
-    for (int gr = 0; gr < MT / kGroup; ++gr) {
-      if (__ballot(live) == 0) break;
-      int addr[kGroup];
-#pragma unroll
-      for (int u = 0; u < kGroup; ++u) {
-        const int m = gr * kGroup + u;
-        addr[u] = m * kKsub + static_cast<int>((w[m >> 2] >> (8 * (m & 3))) & 0xFFu);
-      }
-      if constexpr (kCount) {
-        const uint64_t lanes = __ballot(live);
-        if (lanes != 0 && lane == 0) atomicAdd(&s_hist[__popcll(lanes)], static_cast<uint32_t>(kGroup));
-      }
-      if (live) {
-        LutT v[kGroup];
-#pragma unroll
-        for (int u = 0; u < kGroup; ++u) v[u] = s_lut[addr[u]];
-#pragma unroll
-        for (int u = 0; u < kGroup; ++u) d = __fadd_rn(d, widen(v[u]));
-      }
-      live = live && !(d > cut);
-    }
-    if (__ballot(live) != 0) consider(live, d, t);
-  };
-
-  // Register sets in a ring: step i refills the set summed in the step
-  // before with the next tile, then sums set i.  Tiles come in generation
-  // order, so the first set without one ends the scan.  The loads are issued
-  // on every path (tile 0 stands in when there is no next tile, in bounds
-  // and unused), so the compiler's wait counts never make a sum wait for the
-  // tile loaded after it.
-  // The bound is refreshed once per round of kDepth tiles (a bound a few
-  // tiles old is looser, never wrong).
-  uint32_t ws[kDepth][kMW];
-  int ts[kDepth];
-  uint64_t ms[kDepth];
-  bool hs[kDepth];
-#pragma unroll
-  for (int i = 0; i < kDepth; ++i) {
-    ts[i] = 0;
-    ms[i] = 0;
-    hs[i] = false;
-  }
-#pragma unroll
-  for (int i = 0; i < kDepth - 1; ++i) {
-    hs[i] = next_tile(ts[i], ms[i]);
-    load(hs[i] ? ts[i] : 0, ws[i]);
-  }
   for (;;) {
-    gview = gnext;
-    gnext = __hip_atomic_load(a.gthr + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();   // every wavefront is done with the previous job's table and job record
+    if (threadIdx.x == 0) {
+      const int j = atomicAdd(a.job_next, 1);
+      s_job = j < total_jobs ? a.jobs[j] : make_int4(-1, 0, 0, 0);
+    }
+    __syncthreads();
+    const int4 job = s_job;
+    const int pos = __builtin_amdgcn_readfirstlane(job.x);
+    if (pos < 0) break;
+    const int c = __builtin_amdgcn_readfirstlane(job.y);
+    const int p_begin = __builtin_amdgcn_readfirstlane(job.z);
+    const int p_end = __builtin_amdgcn_readfirstlane(job.w);
+    const int q = __builtin_amdgcn_readfirstlane(a.qorder[pos]);
+    if (q != cur_q) {
+      // The query's table into LDS, noting negative or NaN entries (then
+      // partial sums bound nothing: no abandonment and no skipping).
+      const uint4* src =
+          reinterpret_cast<const uint4*>(static_cast<const LutT*>(a.lut) + static_cast<size_t>(q) * MT * kKsub);
+      bool bad = false;
+      for (int v = threadIdx.x; v < kVecQ; v += kThreads) {
+        const uint4 x = src[v];
+        reinterpret_cast<uint4*>(s_lut)[v] = x;
+        const LutT* xe = reinterpret_cast<const LutT*>(&x);
+#pragma unroll
+        for (int e = 0; e < kVec; ++e) bad = bad || !(widen(xe[e]) >= 0.0f);
+      }
+      const bool wave_bad = __ballot(bad) != 0;
+      if (lane == 0) s_bad[wave] = wave_bad ? 1u : 0u;
+      if (threadIdx.x == 0) *s_thr = kNoKey;
+      __syncthreads();
+      monotone = true;
+#pragma unroll
+      for (int w = 0; w < kScanWaves; ++w) monotone = monotone && s_bad[w] == 0;
+      cur_q = q;
+    }
+    const float* hdr = a.hdr + 4 * static_cast<size_t>(q);
+    const int n_items = __float_as_int(hdr[0]);
+
+    int cnt = 0;
+    uint64_t thr = kNoKey, published = kNoKey, bound = kNoKey;
+    uint64_t gview = __hip_atomic_load(a.gthr + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), gnext = gview;
+    float cut = __builtin_nanf("");
+    // bound = min(own k-th key, workgroup's, query's); cut its distance (NaN
+    // while there is none, or when the table is not monotone).
+    auto refresh = [&]() {
+      const uint64_t blk = __hip_atomic_load(s_thr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      uint64_t b = thr < blk ? thr : blk;
+      b = b < gview ? b : gview;
+      bound = b;
+      cut = monotone ? from_ordered_bits(static_cast<uint32_t>(bound >> 32)) : __builtin_nanf("");
+    };
+    auto pruned = [&](float lb) -> bool {
+      return lb > 0.0f && __fsub_rn(__fmul_rn(__fmul_rn(lb, lb), a.keep), a.abs_m) > cut;
+    };
     refresh();
+
+    // The item holding position p_begin: the last with tile offset <= p_begin
+    // (offsets increase), by 64-way search.
+    const size_t ib = static_cast<size_t>(q) * a.C;
+    int item0 = 0;
+    if (n_items > 0) {
+      int lo = 0, hi = n_items;
+      while (hi - lo > 64) {
+        const int step = (hi - lo + 63) / 64;
+        const int idx = min(lo + lane * step, hi - 1);
+        const bool le = lo + lane * step < hi && a.it_t[ib + idx] <= p_begin;
+        const uint64_t m = __ballot(le);
+        const int l = 63 - __builtin_clzll(m | 1ull);
+        lo = lo + l * step;
+        hi = min(hi, lo + step);
+      }
+      const int idx = min(lo + lane, hi - 1);
+      const bool le = lo + lane < hi && a.it_t[ib + idx] <= p_begin;
+      item0 = lo + (63 - __builtin_clzll(__ballot(le) | 1ull));
+    }
+
+    // Tile generator over the job's items.
+    int batch = item0 - 64;
+    int stop_at = n_items;   // items from here on are prunable or past the job
+    uint64_t pend = 0;
+    int v_r0 = 0, v_r1 = 0, v_t = 0;
+    float v_lb = 0.0f;
+    bool in_item = false;
+    int i_r0 = 0, i_r1 = 0, i_end = 0, i_t = 0, p = 0;
+    float i_lb = 0.0f;
+    auto next_tile = [&](int& t, uint64_t& mask) -> bool {
+      for (;;) {
+        if (in_item) {
+          if (pruned(i_lb)) {
+            // this item and every later one
+            stop_at = 0;
+            pend = 0;
+            in_item = false;
+            return false;
+          }
+          if (p < i_end) {
+            t = (i_r0 >> 6) + (p - i_t);
+            p += kScanWaves;
+            const int row0 = t * 64;
+            mask = bit_range(max(i_r0 - row0, 0), min(i_r1 - row0, 64));
+            return true;
+          }
+          in_item = false;
+        }
+        if (pend == 0) {
+          batch += 64;
+          if (batch >= stop_at) return false;
+          // Every lane loads (lanes past the end reload the batch's first
+          // item) and every loaded value is used before the ballot, so the
+          // loads complete here and not at a later wait that would also hold
+          // the tile loads issued meanwhile.
+          const int it = batch + lane;
+          const int itc = it < stop_at ? it : batch;
+          v_r0 = a.it_r0[ib + itc];
+          v_r1 = a.it_r1[ib + itc];
+          v_t = a.it_t[ib + itc];
+          v_lb = a.it_lb[ib + itc];
+          const int nt = ((v_r1 - 1) >> 6) - (v_r0 >> 6) + 1;
+          const int from = max(v_t, p_begin);
+          const int first = from + ((wave - from) & (kScanWaves - 1));   // this wavefront's first position
+          const bool gone = it < stop_at && (pruned(v_lb) || v_t >= p_end);
+          bool ok = it < stop_at && first < min(v_t + nt, p_end) && !gone;
+          const uint64_t gm = __ballot(gone);
+          if (gm != 0) {
+            // the first prunable item, or the first past the job, ends it
+            const int j0 = __builtin_ctzll(gm);
+            stop_at = batch + j0;
+            ok = ok && lane < j0;
+          }
+          pend = __ballot(ok);
+          continue;
+        }
+        const int j = __builtin_ctzll(pend);
+        pend &= pend - 1;
+        i_r0 = __builtin_amdgcn_readlane(v_r0, j);
+        i_r1 = __builtin_amdgcn_readlane(v_r1, j);
+        i_t = __builtin_amdgcn_readlane(v_t, j);
+        i_lb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v_lb), j));
+        const int i_nt = ((i_r1 - 1) >> 6) - (i_r0 >> 6) + 1;
+        const int from = max(i_t, p_begin);
+        p = from + ((wave - from) & (kScanWaves - 1));
+        i_end = min(i_t + i_nt, p_end);
+        in_item = true;
+      }
+    };
+    auto load = [&](int t, uint32_t (&w)[kMW]) {
+      const uint32_t* __restrict__ tile = a.codes_t + static_cast<size_t>(t) * (kMW * 64);
+#pragma unroll
+      for (int j = 0; j < kMW; ++j) w[j] = tile[j * 64 + lane];
+    };
+    const bool union_bound = a.union_bound != 0 && k <= kListSlots;
+    unsigned long long* pairs = reinterpret_cast<unsigned long long*>(a.slots + static_cast<size_t>(q) * kListSlots);
+    const int my_pair = c * kScanWaves + wave;
+    uint32_t best1 = ~0u, best2 = ~0u;   // this wavefront's two smallest full distances in this job
+    auto publish = [&](uint64_t key) {
+      if (key < published) {
+        published = key;
+        if (lane == 0) {
+          atomicMin(s_thr, static_cast<unsigned long long>(key));
+          __hip_atomic_fetch_min(a.gthr + q, key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+    };
+    auto consider = [&](bool act, float d, int t) {
+      uint64_t key = kNoKey;
+      bool cand = false;
+      if (act) {
+        const uint32_t db = ordered_bits(d);
+        if (db <= static_cast<uint32_t>(bound >> 32)) {
+          key = row_key(db, static_cast<uint32_t>(t * 64 + lane));
+          cand = true;
+        }
+      }
+      if (union_bound) {
+        // The step's two smallest distances (pairs merged across lanes), then
+        // the wavefront's two smallest so far.
+        uint32_t x1 = act ? ordered_bits(d) : ~0u, x2 = ~0u;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const uint32_t y1 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(x1), o, 64));
+          const uint32_t y2 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(x2), o, 64));
+          const uint32_t hi = x1 > y1 ? x1 : y1;
+          const uint32_t lo2 = x2 < y2 ? x2 : y2;
+          x1 = x1 < y1 ? x1 : y1;
+          x2 = hi < lo2 ? hi : lo2;
+        }
+        const uint32_t hi = best1 > x1 ? best1 : x1;
+        const uint32_t lo2 = best2 < x2 ? best2 : x2;
+        const uint32_t n1 = best1 < x1 ? best1 : x1;
+        const uint32_t n2 = hi < lo2 ? hi : lo2;
+        if (n1 < best1 || n2 < best2) {
+          // The k-th smallest slot only falls when a slot drops from at or
+          // above the published value to below it.
+          const uint32_t kth = static_cast<uint32_t>(published >> 32);
+          const bool crossed = (n1 < kth && best1 >= kth) || (n2 < kth && best2 >= kth);
+          best1 = n1;
+          best2 = n2;
+          if (lane == 0)
+            __hip_atomic_store(&pairs[my_pair], (static_cast<unsigned long long>(n2) << 32) | n1, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+          if (crossed) {
+            // all kListSlots / 2 words are loaded (the unused ones hold all
+            // ones), together, with one wait; each lane reads its own words
+            constexpr int kW = kListSlots / 128;
+            unsigned long long pw[kW];
+#pragma unroll
+            for (int u = 0; u < kW; ++u)
+              pw[u] = __hip_atomic_load(&pairs[lane * kW + u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            uint64_t v[2 * kW];
+#pragma unroll
+            for (int u = 0; u < kW; ++u) {
+              v[2 * u] = (static_cast<uint64_t>(static_cast<uint32_t>(pw[u])) << 32) | 0xFFFFFFFFull;
+              v[2 * u + 1] = (static_cast<uint64_t>(static_cast<uint32_t>(pw[u] >> 32)) << 32) | 0xFFFFFFFFull;
+            }
+            wave_bitonic_sort<2 * kW>(v);
+            const int e = k - 1;
+            uint64_t mine = v[0];
+#pragma unroll
+            for (int u = 1; u < 2 * kW; ++u)
+              if (u == e % (2 * kW)) mine = v[u];
+            const uint64_t ub = shfl_u64(mine, e / (2 * kW));
+            if ((ub >> 32) != 0xFFFFFFFFull) publish(ub);
+          }
+        }
+      }
+      pool_push(pool, cnt, thr, key, cand, k, a.kpl, a.ids);
+      publish(thr);
+    };
+    auto sum_tile = [&](int t, uint64_t mask, const uint32_t (&w)[kMW]) {
+      if constexpr (kCount) {
+        if (lane == 0) atomicAdd(&s_hist[0], 1u);
+      }
+      bool live = __builtin_amdgcn_inverse_ballot_w64(mask);
+      float d = 0.0f;
+      // (most tiles lose every row to the first groups: the loop ends as soon
+      // as no lane is live)
+#pragma unroll
+      for (int gr = 0; gr < MT / kGroup; ++gr) {
+        if (__ballot(live) == 0) break;
+        int addr[kGroup];
+#pragma unroll
+        for (int u = 0; u < kGroup; ++u) {
+          const int m = gr * kGroup + u;
+          addr[u] = m * kKsub + static_cast<int>((w[m >> 2] >> (8 * (m & 3))) & 0xFFu);
+        }
+        if constexpr (kCount) {
+          const uint64_t lanes = __ballot(live);
+          if (lanes != 0 && lane == 0) atomicAdd(&s_hist[__popcll(lanes)], static_cast<uint32_t>(kGroup));
+        }
+        if (live) {
+          LutT v[kGroup];
+#pragma unroll
+          for (int u = 0; u < kGroup; ++u) v[u] = s_lut[addr[u]];
+#pragma unroll
+          for (int u = 0; u < kGroup; ++u) d = __fadd_rn(d, widen(v[u]));
+        }
+        live = live && !(d > cut);
+      }
+      if (__ballot(live) != 0) consider(live, d, t);
+    };
+
+    // Register sets in a ring: step i refills the set summed in the step
+    // before with the next tile, then sums set i.  Tiles come in generation
+    // order, so the first set without one ends the job.  The loads are
+    // issued on every path (tile 0 stands in when there is no next tile, in
+    // bounds and unused), so the compiler's wait counts never make a sum wait
+    // for the tile loaded after it.  The bound is refreshed once per round
+    // of kDepth tiles (a bound a few tiles old is looser, never wrong).
+    uint32_t ws[kDepth][kMW];
+    int ts[kDepth];
+    uint64_t ms[kDepth];
+    bool hs[kDepth];
 #pragma unroll
     for (int i = 0; i < kDepth; ++i) {
-      const int j = (i + kDepth - 1) % kDepth;
-      hs[j] = next_tile(ts[j], ms[j]);
-      load(hs[j] ? ts[j] : 0, ws[j]);
-      if (!hs[i]) goto scanned;
-      sum_tile(ts[i], ms[i], ws[i]);
+      ts[i] = 0;
+      ms[i] = 0;
+      hs[i] = false;
     }
+#pragma unroll
+    for (int i = 0; i < kDepth - 1; ++i) {
+      hs[i] = next_tile(ts[i], ms[i]);
+      load(hs[i] ? ts[i] : 0, ws[i]);
+    }
+    for (;;) {
+      gview = gnext;
+      gnext = __hip_atomic_load(a.gthr + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      refresh();
+#pragma unroll
+      for (int i = 0; i < kDepth; ++i) {
+        const int j = (i + kDepth - 1) % kDepth;
+        hs[j] = next_tile(ts[j], ms[j]);
+        load(hs[j] ? ts[j] : 0, ws[j]);
+        if (!hs[i]) goto scanned;
+        sum_tile(ts[i], ms[i], ws[i]);
+      }
+    }
+  scanned:
+    pool_compact(pool, cnt, thr, k, a.kpl, a.ids);
+    uint64_t* dst = a.partials + ((static_cast<size_t>(pos) * a.max_jobs + c) * kScanWaves + wave) * k;
+    for (int e = lane; e < k; e += 64) dst[e] = pool[e];
   }
-scanned:
-
-  pool_compact(pool, cnt, thr, k, a.kpl, a.ids);
-  uint64_t* dst = a.partials + ((static_cast<size_t>(pos) * a.splits + split) * kScanWaves + wave) * k;
-  for (int e = lane; e < k; e += 64) dst[e] = pool[e];
   if constexpr (kCount) {
     __syncthreads();
     if (threadIdx.x < 65 && s_hist[threadIdx.x] != 0)
       atomicAdd(&a.lookup_hist[threadIdx.x], static_cast<unsigned long long>(s_hist[threadIdx.x]));
+  }
+}
+
+// The job table (one workgroup): per query position, jobs = min(kListJobs,
+// ceil(W / kJobTiles)) chunks of about equal size (multiples of kScanWaves
+// positions) of its W tiles (the tiles before the first item the plan's
+// seed bound prunes), the heaviest queries first; the keys each position's
+// jobs write are counted for the merge; the job counter is reset.
+__global__ __launch_bounds__(1024) void list_jobs_kernel(const ListJobArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  uint64_t* s_key = reinterpret_cast<uint64_t*>(smem);   // [np2]
+  int32_t* s_base = reinterpret_cast<int32_t*>(s_key + a.np2);   // [np2 + 1]
+  const int tid = threadIdx.x;
+  for (int i = tid; i < a.np2; i += 1024) {
+    uint64_t key = ~0ull;
+    if (i < a.nq) {
+      const int q = a.qorder[i];
+      const int w = __float_as_int(a.hdr[4 * static_cast<size_t>(q) + 1]);
+      key = (static_cast<uint64_t>(0x7FFFFFFF - w) << 32) | static_cast<uint32_t>(i);
+    }
+    s_key[i] = key;
+  }
+  __syncthreads();
+  for (int size = 2; size <= a.np2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int p = tid; p < a.np2 / 2; p += 1024) {
+        const int i = ((p & ~(stride - 1)) << 1) | (p & (stride - 1));
+        const int j = i | stride;
+        const uint64_t x = s_key[i], y = s_key[j];
+        const bool up = (i & size) == 0;
+        if (up ? (x > y) : (x < y)) {
+          s_key[i] = y;
+          s_key[j] = x;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // jobs per position in sorted order, then their exclusive prefix (serial
+  // per thread block of positions, then across blocks)
+  auto jobs_of = [&](int i) -> int {
+    if (i >= a.nq) return 0;
+    const int w = 0x7FFFFFFF - static_cast<int>(s_key[i] >> 32);
+    return w <= 0 ? 0 : min(a.max_jobs, (w + kJobTiles - 1) / kJobTiles);
+  };
+  const int per = (a.np2 + 1023) / 1024;
+  int mine = 0;
+  for (int u = 0; u < per; ++u) mine += jobs_of(tid * per + u);
+  s_base[tid] = mine;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int v = tid >= off ? s_base[tid - off] : 0;
+    __syncthreads();
+    s_base[tid] += v;
+    __syncthreads();
+  }
+  int base = tid == 0 ? 0 : s_base[tid - 1];
+  for (int u = 0; u < per; ++u) {
+    const int i = tid * per + u;
+    if (i >= a.nq) break;
+    const int pos = static_cast<int>(s_key[i] & 0xFFFFFFFFu);
+    const int w = 0x7FFFFFFF - static_cast<int>(s_key[i] >> 32);
+    const int nj = jobs_of(i);
+    const int chunk = nj > 0 ? ((w + nj - 1) / nj + kScanWaves - 1) / kScanWaves * kScanWaves : 0;
+    for (int c = 0; c < nj; ++c)
+      a.jobs[base + c] = make_int4(pos, c, c * chunk, min(w, (c + 1) * chunk));
+    base += nj;
+    a.n_keys[pos] = nj * kScanWaves * a.k;   // the merge reads the written chunks only
+  }
+  if (tid == 1023) {
+    *a.job_total = s_base[1023];
+    *a.job_next = 0;
   }
 }
 
@@ -395,17 +518,47 @@ size_t list_scan_lds_bytes(int m, int lut_dtype, int pool_stride) {
   return static_cast<size_t>(m) * kKsub * (lut_dtype == 1 ? 2 : 4) + list_dyn_bytes(pool_stride);
 }
 
+hipError_t launch_list_jobs(const ListJobArgs& a, hipStream_t s) {
+  if (a.nq <= 0) return hipSuccess;
+  const size_t lds = static_cast<size_t>(a.np2) * 8 + 1025 * 4;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&list_jobs_kernel),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+  if (e != hipSuccess) return e;
+  ListJobArgs args = a;
+  void* kargs[] = {&args};
+  return hipLaunchKernel(reinterpret_cast<const void*>(&list_jobs_kernel), dim3(1), dim3(1024), kargs, lds, s);
+}
+
 hipError_t launch_list_scan(const ListScanArgs& a, int lut_dtype, hipStream_t s) {
   const void* fn = pick_list(a.m, lut_dtype, a.lookup_hist != nullptr);
-  if (!fn || a.splits < 1 || (a.splits & (a.splits - 1)) != 0) return hipErrorInvalidValue;
+  if (!fn) return hipErrorInvalidValue;
   if (a.nq <= 0) return hipSuccess;
   const size_t dyn = list_dyn_bytes(a.pool_stride);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(dyn));
   if (e != hipSuccess) return e;
+  // Persistent: the workgroups the chip holds at once (looked up once per
+  // device, kernel and LDS size).
+  int device = 0;
+  if ((e = hipGetDevice(&device)) != hipSuccess) return e;
+  int grid = 0;
+  {
+    static std::mutex mu;
+    static std::map<std::tuple<int, const void*, size_t>, int> cache;
+    std::lock_guard<std::mutex> lock(mu);
+    const auto key = std::make_tuple(device, fn, dyn);
+    auto it = cache.find(key);
+    if (it == cache.end()) {
+      int cus = 0, per_cu = 0;
+      if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device)) != hipSuccess) return e;
+      if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kScanWaves * 64, dyn)) != hipSuccess)
+        return e;
+      it = cache.emplace(key, std::max(1, cus * std::max(1, per_cu))).first;
+    }
+    grid = it->second;
+  }
   ListScanArgs args = a;
   void* kargs[] = {&args};
-  return hipLaunchKernel(fn, dim3(static_cast<unsigned>(a.nq) * static_cast<unsigned>(a.splits)),
-                         dim3(kScanWaves * 64), kargs, dyn, s);
+  return hipLaunchKernel(fn, dim3(static_cast<unsigned>(grid)), dim3(kScanWaves * 64), kargs, dyn, s);
 }
 
 }  // namespace ifvs

@@ -9,7 +9,7 @@
 // key is rejected by one compare.
 // When the scan's chunks are absolute cells of a grid, only the slots of the
 // cells the query's row interval touches are read (the scan leaves the others
-// unwritten).
+// unwritten); with per-position key counts, only the first that many.
 #include "ifvs_internal.h"
 #include "topk_device.h"
 
@@ -24,6 +24,7 @@ __global__ __launch_bounds__(64) void topk_merge_kernel(const uint64_t* __restri
                                                         const int64_t* __restrict__ iv,
                                                         int64_t cell_tiles, int64_t slot_keys,
                                                         const int32_t* __restrict__ qorder,
+                                                        const int32_t* __restrict__ n_keys,
                                                         int32_t* __restrict__ ids_out,
                                                         float* __restrict__ dist_out) {
   extern __shared__ uint64_t pool[];
@@ -33,7 +34,7 @@ __global__ __launch_bounds__(64) void topk_merge_kernel(const uint64_t* __restri
   int cnt = 0;
   uint64_t thr = kNoKey;
   const uint64_t* src = partials + static_cast<size_t>(pos) * per_query;
-  int64_t first = 0, end = per_query;
+  int64_t first = 0, end = n_keys ? min(per_query, static_cast<int64_t>(n_keys[pos])) : per_query;
   if (cell_tiles > 0) {
     const int64_t r0 = iv[2 * q], r1 = iv[2 * q + 1];
     first = end = 0;
@@ -75,11 +76,11 @@ __global__ __launch_bounds__(64) void topk_merge_kernel(const uint64_t* __restri
 hipError_t launch_topk_merge(const uint64_t* partials, int nq, int64_t per_query, int k,
                              const int64_t* iv, int64_t cell_tiles, int64_t slot_keys,
                              const int32_t* qorder, int32_t* ids_out, float* dist_out,
-                             hipStream_t s) {
+                             hipStream_t s, const int32_t* n_keys) {
   const int kpl = pool_kpl(k);
   const size_t lds = static_cast<size_t>(64 * kpl) * sizeof(uint64_t);
   topk_merge_kernel<<<dim3(nq), dim3(64), lds, s>>>(partials, per_query, k, kpl, iv, cell_tiles,
-                                                    slot_keys, qorder, ids_out, dist_out);
+                                                    slot_keys, qorder, n_keys, ids_out, dist_out);
   return hipGetLastError();
 }
 
