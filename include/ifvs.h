@@ -267,7 +267,7 @@ ifvs_status ifvs_filtered_search_noalloc(ifvs_index* idx, int32_t nq, const ifvs
  * codes.  Synchronous; replaces any earlier coarse quantizer.  Costs about
  * n * (4 ceil(m/4) + 13) bytes of device memory (codes, ids, row words,
  * bands and list positions), a rank table of at most 64 MiB, and max_batch *
- * n_centroids * 96 + max_batch * 1040 bytes of list-plan workspace.
+ * n_centroids * 64 + max_batch * 1300 bytes of list-plan workspace.
  * Errors: IFVS_E_INVALID (n_centroids outside 1..4096 or above n, iters
  * outside 0..1000), IFVS_E_UNSUPPORTED (dim > 128), IFVS_E_STATE,
  * IFVS_E_NOMEM, IFVS_E_HIP. */
@@ -302,10 +302,11 @@ ifvs_status ifvs_lut_bounds(ifvs_index* idx, int32_t nq, const float* alpha, con
  * tested row by row), M is 16, 48 or 120, and its workspace holds the batch
  * (IFVS_OPT_COARSE: automatic for batches whose widest interval spans 8192
  * or more 64-row tiles); otherwise the call is ifvs_filtered_search.  The
- * list scan adds the bound kernels and one planning kernel per call (one
- * workgroup per query sorts the query's groups by their bound).
- * IFVS_OPT_SPLITS sets its workgroups per query (rounded down to a power of
- * two, at most 16; default about 2048 workgroups in all).
+ * list scan adds the bound kernels, one planning kernel per call (one
+ * workgroup per query orders the query's groups by their bound) and a job
+ * table kernel; the scan's workgroups take chunks of the queries' work from
+ * the table, the queries with the most work first.  IFVS_OPT_SPLITS caps a
+ * query's chunks (at most 16, the default).
  * Errors: as ifvs_filtered_search, plus IFVS_E_INVALID for alpha given on an
  * index without a memory bank. */
 ifvs_status ifvs_filtered_search_bounded(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,

@@ -134,8 +134,6 @@ struct CoarseLists {
   uint32_t* codes_t = nullptr;   // [n_tiles][mw][64] list order
   int32_t* ids = nullptr;        // [n_tiles * 64] list position -> original id
   int32_t* lrow = nullptr;       // [n] list position -> layout row
-  int32_t* tmp_r0 = nullptr;     // [max_batch][C * kBands] list plan workspace
-  int32_t* tmp_r1 = nullptr;
   int32_t* it_r0 = nullptr;      // [max_batch][C * kBands] list plan items
   int32_t* it_r1 = nullptr;
   int32_t* it_t = nullptr;
@@ -151,7 +149,7 @@ struct CoarseLists {
                     static_cast<void*>(sub_off), static_cast<void*>(rmax), static_cast<void*>(cnt_f),
                     static_cast<void*>(codes_t), static_cast<void*>(ids),
                     static_cast<void*>(lrow),
-                    static_cast<void*>(tmp_r0), static_cast<void*>(tmp_r1), static_cast<void*>(it_r0),
+                    static_cast<void*>(it_r0),
                     static_cast<void*>(it_r1), static_cast<void*>(it_t),
                     static_cast<void*>(it_lb), static_cast<void*>(hdr), static_cast<void*>(slots),
                     static_cast<void*>(jobs), static_cast<void*>(n_keys), static_cast<void*>(job_ctr)})
@@ -1256,7 +1254,6 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     pa.mw = idx->mw;
     pa.C = cl.C;
     pa.n_sub = cl.C * kBands;
-    pa.Sp = list_plan_width(cl.C);
     pa.bounds = idx->bounds_ws;
     pa.iv = ws.iv;
     pa.cnt_f = cl.cnt_f;
@@ -1269,8 +1266,6 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     pa.codes_t = cl.codes_t;
     pa.k = k;
     pa.gthr = ws.gthr;
-    pa.tmp_r0 = cl.tmp_r0;
-    pa.tmp_r1 = cl.tmp_r1;
     pa.keep = coarse_keep(idx->m, idx->dsub, lut_dtype);
     pa.abs_m = coarse_abs(idx->m, lut_dtype);
     pa.it_r0 = cl.it_r0;
@@ -2076,7 +2071,7 @@ ifvs_status ifvs_build_coarse(ifvs_index* idx, int32_t n_centroids, int32_t iter
   if (ifvs_status st = alloc(&nl.ids, static_cast<size_t>(n_pad), "list-order ids"); st != IFVS_OK)
     return cleanup(st);
   if (ifvs_status st = alloc(&nl.lrow, hrow.size(), "list rows"); st != IFVS_OK) return cleanup(st);
-  for (int32_t** a : {&nl.it_r0, &nl.it_r1, &nl.it_t, &nl.tmp_r0, &nl.tmp_r1})
+  for (int32_t** a : {&nl.it_r0, &nl.it_r1, &nl.it_t})
     if (ifvs_status st = alloc(a, items, "list plan"); st != IFVS_OK) return cleanup(st);
   if (ifvs_status st = alloc(&nl.it_lb, items, "list plan"); st != IFVS_OK) return cleanup(st);
   if (ifvs_status st = alloc(&nl.hdr, static_cast<size_t>(idx->max_batch) * 4, "list plan"); st != IFVS_OK)

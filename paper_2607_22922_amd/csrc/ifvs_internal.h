@@ -21,7 +21,10 @@ constexpr int kCoarseMaxDim = 128;         // largest D with a coarse quantizer 
 constexpr int kCoarseMax = 4096;           // most coarse centroids
 constexpr int kBands = 4;                  // radius bands per coarse list (sub-lists)
 constexpr int kMaxItems = kCoarseMax * kBands;   // sub-lists a list plan sorts in one workgroup
-constexpr int kItemMask = kMaxItems - 1;         // sub-list index bits of a plan's sort key
+constexpr int kItemBits = 14;                    // sub-list index bits of a plan's sort entry
+constexpr int kItemMask = (1 << kItemBits) - 1;
+static_assert(kMaxItems <= (1 << kItemBits), "sub-list index must fit the plan's entry");
+constexpr int kPlanBuckets = 4096;               // list plan: bucket 0 (no bound) and 4095 bound buckets
 constexpr int kSeedRows = 4096;                  // rows of the nearest list a plan scores for its seed
 
 // A predicate as the device sees it.  The raw fields are the caller's clauses
@@ -268,7 +271,7 @@ struct ListPlanArgs {
   const void* lut;          // [nq][m][256] tables (fp32 or binary16)
   int m, nq;
   const uint32_t* cc_t;     // [mw][C] centroid code words
-  int mw, C, n_sub, Sp;     // n_sub = C * kBands sub-lists, Sp = list_plan_width(C)
+  int mw, C, n_sub;         // n_sub = C * kBands sub-lists
   const float* bounds;      // [nq][2]: sqrt(max w), delta (ifvs_lut_bounds)
   const int64_t* iv;        // [nq][2] layout row interval of each query
   const int32_t* cnt_f;     // [(n >> f_shift) + 1][n_sub]: rows of sub-list s among layout rows [0, b << f_shift)
@@ -282,8 +285,6 @@ struct ListPlanArgs {
   int k;
   uint64_t* gthr;           // [nq] the queries' shared thresholds (the seed lowers them)
   float keep, abs_m;
-  int32_t* tmp_r0;          // [nq][n_sub] workspace
-  int32_t* tmp_r1;          // [nq][n_sub] workspace
   // Outputs by original query: items [nq][n_sub] in increasing bound order,
   // and a header [nq][4] = {items (int bits), tiles (int bits), sqrt(max w),
   // delta}.
@@ -294,7 +295,6 @@ struct ListPlanArgs {
   float* hdr;
   uint32_t* slots;          // [nq][kListSlots] the list scan's union-bound slots, reset here
 };
-int list_plan_width(int C);   // power of two >= C * kBands
 size_t list_plan_lds_bytes(int m, int lut_dtype, int C);
 hipError_t launch_list_plan(const ListPlanArgs& a, int lut_dtype, hipStream_t s);
 

@@ -228,7 +228,6 @@ __global__ __launch_bounds__(256) void bound_parts_kernel(const float* __restric
   const int m = blockIdx.x;
   const int c = threadIdx.x;
   const int lane = c & 63, wave = c >> 6;
-  __shared__ float s_red[4];
   float creg[kFixed ? DSUB : 1];
   float wreg[kFixed ? R : 1][kFixed ? DSUB : 1];
   if constexpr (kFixed) {
@@ -243,9 +242,15 @@ __global__ __launch_bounds__(256) void bound_parts_kernel(const float* __restric
   }
   const int q_begin = blockIdx.y * kBoundQueries;
   const int q_end = min(nq, q_begin + kBoundQueries);
-  for (int q = q_begin; q < q_end; ++q) {
-    float n2 = 0.0f;
-    if (alpha) {
+  __shared__ float s_red[kBoundQueries][4];
+  // every query's shift first (independent loads together), then one
+  // reduction round
+  float n2[kBoundQueries];
+#pragma unroll
+  for (int qi = 0; qi < kBoundQueries; ++qi) {
+    const int q = q_begin + qi;
+    n2[qi] = 0.0f;
+    if (alpha && q < q_end) {
       const float* aq = alpha + (static_cast<size_t>(q) * M + m) * r;
       for (int j = 0; j < dsub; ++j) {
         float delta = 0.0f;
@@ -260,27 +265,31 @@ __global__ __launch_bounds__(256) void bound_parts_kernel(const float* __restric
           base = cpq[(static_cast<size_t>(m) * kKsub + c) * dsub + j];
         }
         const float e = __fsub_rn(__fadd_rn(base, delta), base);
-        n2 = __fadd_rn(n2, __fmul_rn(e, e));
+        n2[qi] = __fadd_rn(n2[qi], __fmul_rn(e, e));
       }
     }
+  }
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) n2 = nan_max(n2, __shfl_xor(n2, o, 64));
-    if (lane == 0) s_red[wave] = n2;
-    __syncthreads();
-    if (c == 0) {
-      float mx = nan_max(nan_max(s_red[0], s_red[1]), nan_max(s_red[2], s_red[3]));
-      float wm = 1.0f;
-      if (wf) {
-        wm = 0.0f;
-        for (int j = 0; j < dsub; ++j) {
-          const float v = wf[static_cast<size_t>(q) * M * dsub + m * dsub + j];
-          wm = (v >= 0.0f && v <= FLT_MAX && wm == wm) ? fmaxf(wm, v) : __builtin_nanf("");
-        }
+  for (int qi = 0; qi < kBoundQueries; ++qi) {
+    float v = n2[qi];
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) v = nan_max(v, __shfl_xor(v, o, 64));
+    if (lane == 0) s_red[qi][wave] = v;
+  }
+  __syncthreads();
+  const int q = q_begin + c;
+  if (c < kBoundQueries && q < q_end) {
+    const float mx = nan_max(nan_max(s_red[c][0], s_red[c][1]), nan_max(s_red[c][2], s_red[c][3]));
+    float wm = 1.0f;
+    if (wf) {
+      wm = 0.0f;
+      for (int j = 0; j < dsub; ++j) {
+        const float v = wf[static_cast<size_t>(q) * M * dsub + m * dsub + j];
+        wm = (v >= 0.0f && v <= FLT_MAX && wm == wm) ? fmaxf(wm, v) : __builtin_nanf("");
       }
-      parts[(static_cast<size_t>(q) * 2) * M + m] = mx;
-      parts[(static_cast<size_t>(q) * 2 + 1) * M + m] = wm;
     }
-    __syncthreads();
+    parts[(static_cast<size_t>(q) * 2) * M + m] = mx;
+    parts[(static_cast<size_t>(q) * 2 + 1) * M + m] = wm;
   }
 }
 
@@ -291,9 +300,21 @@ __global__ __launch_bounds__(256) void bound_final_kernel(const float* __restric
   const float* pd = parts + static_cast<size_t>(q) * 2 * M;
   const float* pw = pd + M;
   float d2 = 0.0f, wm = 0.0f;
-  for (int m = 0; m < M; ++m) {
-    d2 = __fadd_rn(d2, __fmul_rn(4.0f, pd[m]));
-    wm = nan_max(wm, pw[m]);
+  for (int m0 = 0; m0 < M; m0 += 16) {
+    // sixteen subspaces' loads at a time, summed in subspace order
+    float vd[16], vw[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      vd[u] = m0 + u < M ? pd[m0 + u] : 0.0f;
+      vw[u] = m0 + u < M ? pw[m0 + u] : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      if (m0 + u < M) {
+        d2 = __fadd_rn(d2, __fmul_rn(4.0f, vd[u]));
+        wm = nan_max(wm, vw[u]);
+      }
+    }
   }
   bounds[2 * q] = __fmul_rn(sqrtf(wm), 1.0f + 0x1p-19f);
   bounds[2 * q + 1] = __fmul_rn(sqrtf(d2), grow);
@@ -333,51 +354,113 @@ __global__ __launch_bounds__(256) void gather_list_rows_kernel(const int32_t* __
   ids[p] = id;
 }
 
+// Wavefront minimum / maximum (one LDS atomic per wavefront then, not one
+// per lane on a single address).
+__device__ __forceinline__ unsigned long long wave_min_u64(unsigned long long v) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const unsigned long long y = __shfl_xor(v, o, 64);
+    v = y < v ? y : v;
+  }
+  return v;
+}
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), o, 64));
+    v = y < v ? y : v;
+  }
+  return v;
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), o, 64));
+    v = y > v ? y : v;
+  }
+  return v;
+}
+
+// Exclusive prefix sum of one value per thread over a 1024-thread
+// workgroup; the total goes to every thread.  s_w: 16 ints of LDS.
+__device__ int block_exclusive_sum(int v, int* s_w, int& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) s_w[wave] = x;
+  __syncthreads();
+  int off = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < 16; ++w) {
+    const int t = s_w[w];
+    off += w < wave ? t : 0;
+    tot += t;
+  }
+  __syncthreads();
+  total = tot;
+  return off + x - v;
+}
+
 // Per query q (original index): the sub-lists holding rows of its
-// interval, in increasing order of their lower bound.  Sub-list s = (list c,
-// band b) holds the rows of centroid c whose radius falls in band b of the
-// list (radius quantiles), in layout order, so the rows of the query's layout
-// interval [x0, x1) are positions [off[s] + rank_s(x0), off[s] + rank_s(x1)),
-// rank_s(x) = rows of s among layout rows [0, x): the table entry at the last
-// multiple of 2^f_shift below x plus a count over the rest.  Per sub-list
-// with selected rows:
+// interval, in increasing order of a lower bound of their rows' distances.
+// Sub-list s = (list c, band b) holds the rows of centroid c whose radius
+// falls in band b of the list (radius quantiles), in layout order, so the
+// rows of the query's layout interval [x0, x1) are positions
+// [off[s] + rank_s(x0), off[s] + rank_s(x1)), rank_s(x) = rows of s among
+// layout rows [0, x): the table entry at the last multiple of 2^f_shift
+// below x plus a count over the rest.  Per sub-list with selected rows:
 //   sdc = a lower bound of ||q - c^||_w: sqrt((sum_m LUT[m][cc_m] - abs) keep)
 //         widened down by 2^-20 (0 when not a positive finite number),
 //   lb  = sdc - (rmax_s + delta) sqrt(max w), rmax_s the sub-list's largest
-//         radius: a lower bound of the distance of each of its rows,
-// sorted ascending by lb rounded down to 18 bits of its order-preserving
-// code (the item index fills the other 14); the items carry that rounded
-// lb, so a scan may stop at the first item it can prune: every later item
-// has a bound at least as large.  Before them come, with no bound (NaN), the
-// sub-lists of the query's nearest centroid that has selected rows (its
-// rows hold the query's nearest rows as a rule, so the scan's k-th distance
-// is tight from its first tiles) and any sub-list whose bound is NaN.
-// Header: the item count; T, the 64-row tiles of the items before the first
-// one the seed's k-th distance prunes (of all items when there is no seed or
-// a table entry is negative or NaN); sqrt(max w); delta.
+//         radius: a lower bound of the distance of each of its rows.
+// Order: a counting sort into kPlanBuckets buckets: bucket 0 for the
+// sub-lists of the query's nearest centroid that has selected rows (its rows
+// hold the query's nearest rows as a rule, so the scan's k-th distance is
+// tight from its first tiles) and those whose lb is NaN, bucket 1 for lb <= 0
+// (never pruned), then buckets of 2^shift consecutive order-preserving codes
+// of positive lb (a monotone function of lb, so every lb of a bucket is at
+// most every lb of the next; shift the least that fits the query's range).
+// Each item carries its bucket's smallest lb (NaN in bucket 0): the carried
+// bounds never decrease along the order, so a scan may stop at the first
+// item it can prune, and the items from the first bucket that the seed's
+// k-th distance prunes on are left out.  The order inside a bucket is the
+// order the threads reach it.  Header: the items kept; T, their 64-row
+// tiles; sqrt(max w); delta.
 //
 // Seed: the distances (summed exactly as the scan sums them) of the
 // selected rows among the first kSeedRows positions of the list of the
 // centroid with the smallest sdc; when there are k of them, the k-th
-// smallest bounds the query's k-th distance (k distinct selected rows lie
-// at or below it) and goes to the query's shared threshold, with the
-// largest id so rows at that distance stay eligible.
-template <typename LutT>
+// smallest (a radix select, 8 bits a pass) bounds the query's k-th distance
+// (k distinct selected rows lie at or below it) and goes to the query's
+// shared threshold, with the largest id so rows at that distance stay
+// eligible.
+template <int MT, typename LutT>
 __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
+  constexpr int kMW = (MT + 3) / 4;
+  constexpr int kSPer = kMaxItems / 1024;   // sub-lists a thread holds (in registers)
+  static_assert(kSeedRows % 1024 == 0 && kPlanBuckets % 1024 == 0 && kMaxItems % 1024 == 0,
+                "a 1024-thread plan takes whole shares");
   extern __shared__ __align__(16) unsigned char smem[];
-  const int C = a.C, S = a.n_sub, Sp = a.Sp;
+  const int C = a.C, S = a.n_sub;
   float* s_sdc = reinterpret_cast<float*>(smem);                          // [C]
   unsigned char* scratch = smem + ((static_cast<size_t>(C) * 4 + 15) & ~size_t{15});
   LutT* s_lut = reinterpret_cast<LutT*>(scratch);                         // phase 1
-  uint32_t* s_seed = reinterpret_cast<uint32_t*>(scratch + static_cast<size_t>(a.m) * kKsub * sizeof(LutT));
   int32_t* s_cnt = reinterpret_cast<int32_t*>(scratch);                   // phase 2: [S]
-  uint32_t* s_key = reinterpret_cast<uint32_t*>(s_cnt + S);               // phase 2: [Sp]
+  int32_t* s_hist = s_cnt + S;                                            // phase 2: [kPlanBuckets]
+  uint32_t* s_bmin = reinterpret_cast<uint32_t*>(s_hist + kPlanBuckets);  // phase 2: [kPlanBuckets]
   __shared__ int s_count;
   __shared__ unsigned long long s_near;   // (sdc bits, centroid) of the nearest selected centroid
   __shared__ unsigned long long s_first;  // (sdc bits, centroid) of the nearest centroid
   __shared__ int s_lut_bad;               // a table entry is negative or NaN: no pruning
-  __shared__ int s_stop;                  // the first item the seed's bound prunes
-  __shared__ uint32_t s_seed_kth;         // the seed's k-th distance (order-preserving bits)
+  __shared__ int s_stop;                  // the first bucket the seed's bound prunes
+  __shared__ uint32_t s_lo, s_hi;         // smallest and largest positive bounded lb (order-preserving bits)
+  __shared__ int s_rh[256];               // radix select histogram
+  __shared__ int s_pick[2];
+  __shared__ int s_w[16];
   const int q = blockIdx.x;
   const int tid = threadIdx.x;
   const int64_t x0 = a.iv[2 * q], x1 = a.iv[2 * q + 1];
@@ -393,202 +476,307 @@ __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
     }
     return;
   }
+  // A row's distance from its code words, summed as the scan sums it.
+  auto code_distance = [&](const uint32_t (&wd)[kMW]) -> float {
+    float d = 0.0f;
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+      d = __fadd_rn(d, widen(s_lut[m * kKsub + static_cast<int>((wd[m >> 2] >> (8 * (m & 3))) & 0xFFu)]));
+    return d;
+  };
   // Phase 1: the table, then each centroid's bound.
-  const LutT* lut = static_cast<const LutT*>(a.lut) + static_cast<size_t>(q) * a.m * kKsub;
-  const int lut_vecs = a.m * kKsub * static_cast<int>(sizeof(LutT)) / 16;
+  const LutT* lut = static_cast<const LutT*>(a.lut) + static_cast<size_t>(q) * MT * kKsub;
+  constexpr int kLutVecs = MT * kKsub * static_cast<int>(sizeof(LutT)) / 16;
   if (tid == 0) {
     s_count = 0;
     s_near = ~0ull;
     s_first = ~0ull;
     s_lut_bad = 0;
     s_stop = 0x7FFFFFFF;
+    s_lo = ~0u;
+    s_hi = 0u;
   }
   __syncthreads();
   {
     bool bad = false;
-    for (int v = tid; v < lut_vecs; v += 1024) {
+    for (int v = tid; v < kLutVecs; v += 1024) {
       const uint4 x = reinterpret_cast<const uint4*>(lut)[v];
       reinterpret_cast<uint4*>(s_lut)[v] = x;
       const LutT* xe = reinterpret_cast<const LutT*>(&x);
+#pragma unroll
       for (int e = 0; e < 16 / static_cast<int>(sizeof(LutT)); ++e) bad = bad || !(widen(xe[e]) >= 0.0f);
     }
     if (bad) s_lut_bad = 1;
   }
   __syncthreads();
-  for (int c = tid; c < C; c += 1024) {
-    float d = 0.0f;
-    for (int w = 0; w < a.mw; ++w) {
-      const uint32_t word = a.cc_t[static_cast<size_t>(w) * C + c];
-      for (int b = 0; b < 4; ++b) {
-        const int m = 4 * w + b;
-        if (m < a.m) d = __fadd_rn(d, widen(s_lut[m * kKsub + static_cast<int>((word >> (8 * b)) & 0xFFu)]));
-      }
+  {
+    unsigned long long first = ~0ull;
+    for (int c = tid; c < C; c += 1024) {
+      uint32_t wd[kMW];
+#pragma unroll
+      for (int w = 0; w < kMW; ++w) wd[w] = a.cc_t[static_cast<size_t>(w) * C + c];
+      const float lo = __fmul_rn(__fsub_rn(code_distance(wd), a.abs_m), a.keep);
+      const float sdc = lo > 0.0f && lo <= FLT_MAX ? __fmul_rn(sqrtf(lo), 1.0f - 0x1p-20f) : 0.0f;
+      s_sdc[c] = sdc;
+      const unsigned long long key = (static_cast<unsigned long long>(ordered_bits(sdc)) << 32) | static_cast<uint32_t>(c);
+      first = key < first ? key : first;
     }
-    const float lo = __fmul_rn(__fsub_rn(d, a.abs_m), a.keep);
-    s_sdc[c] = lo > 0.0f && lo <= FLT_MAX ? __fmul_rn(sqrtf(lo), 1.0f - 0x1p-20f) : 0.0f;
-    atomicMin(&s_first, (static_cast<unsigned long long>(ordered_bits(s_sdc[c])) << 32) | static_cast<uint32_t>(c));
+    first = wave_min_u64(first);
+    if ((tid & 63) == 0 && first != ~0ull) atomicMin(&s_first, first);
   }
   __syncthreads();
-  {
+  uint32_t seed_kth = ~0u;   // the seed's k-th distance (order-preserving bits; all ones: none)
+  if (a.k <= kSeedRows) {
     // The seed (see above), from the nearest centroid's list.
+    constexpr int kPer = kSeedRows / 1024;
     const int c0 = static_cast<int>(s_first & 0xFFFFFFFFu);
     const int32_t p0 = a.sub_off[c0 * kBands], p1 = min(a.sub_off[c0 * kBands + kBands], p0 + kSeedRows);
-    for (int i = tid; i < kSeedRows; i += 1024) {
-      uint32_t key = ~0u;
-      const int32_t p = p0 + i;
-      if (p < p1) {
-        const int64_t r = a.lrow[p];
-        if (r >= x0 && r < x1) {
-          const uint32_t* tile = a.codes_t + static_cast<size_t>(p >> 6) * a.mw * 64 + (p & 63);
-          float d = 0.0f;
-          for (int w = 0; w < a.mw; ++w) {
-            const uint32_t word = tile[w * 64];
-            for (int b = 0; b < 4; ++b) {
-              const int m = 4 * w + b;
-              if (m < a.m) d = __fadd_rn(d, widen(s_lut[m * kKsub + static_cast<int>((word >> (8 * b)) & 0xFFu)]));
-            }
-          }
-          key = ordered_bits(d);
-        }
-      }
-      s_seed[i] = key;
+    int64_t row[kPer];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int32_t p = p0 + tid + u * 1024;
+      row[u] = p < p1 ? a.lrow[p] : -1;
     }
-    __syncthreads();
-    for (int size = 2; size <= kSeedRows; size <<= 1) {
-      for (int stride = size >> 1; stride > 0; stride >>= 1) {
-        for (int p = tid; p < kSeedRows / 2; p += 1024) {
-          const int i = ((p & ~(stride - 1)) << 1) | (p & (stride - 1));
-          const int j = i | stride;
-          const uint32_t x = s_seed[i], y = s_seed[j];
-          const bool up = (i & size) == 0;
-          if (up ? (x > y) : (x < y)) {
-            s_seed[i] = y;
-            s_seed[j] = x;
-          }
-        }
-        __syncthreads();
+    uint32_t key[kPer];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      key[u] = ~0u;
+      if (row[u] >= x0 && row[u] < x1) {
+        const int32_t p = p0 + tid + u * 1024;
+        const uint32_t* tile = a.codes_t + static_cast<size_t>(p >> 6) * kMW * 64 + (p & 63);
+        uint32_t wd[kMW];
+#pragma unroll
+        for (int w = 0; w < kMW; ++w) wd[w] = tile[w * 64];
+        key[u] = ordered_bits(code_distance(wd));
       }
     }
-    if (tid == 0) s_seed_kth = a.k <= kSeedRows ? s_seed[a.k - 1] : ~0u;
-    if (tid == 0 && a.k <= kSeedRows && s_seed[a.k - 1] != ~0u)
-      atomicMin(reinterpret_cast<unsigned long long*>(a.gthr + q),
-                (static_cast<unsigned long long>(s_seed[a.k - 1]) << 32) | 0xFFFFFFFFull);
-  }
-  __syncthreads();
-  // Phase 2: ranks at x0 (kept in tmp_r0), then at x1 with the items'
-  // rows, bounds and sort keys.
-  const size_t base = static_cast<size_t>(q) * S;
-  const int64_t b0 = x0 >> a.f_shift, b1 = x1 >> a.f_shift;
-  for (int pass = 0; pass < 2; ++pass) {
-    const int64_t x = pass == 0 ? x0 : x1, bx = pass == 0 ? b0 : b1;
-    for (int s = tid; s < S; s += 1024) s_cnt[s] = a.cnt_f[bx * S + s];
-    __syncthreads();
-    for (int64_t r = (bx << a.f_shift) + tid; r < x; r += 1024)
-      atomicAdd(&s_cnt[static_cast<int>(a.words[r] & 0xFFFFu) * kBands + a.band[r]], 1);
-    __syncthreads();
-    if (pass == 0) {
-      for (int s = tid; s < S; s += 1024) a.tmp_r0[base + s] = a.sub_off[s] + s_cnt[s];
-    } else {
-      for (int s = tid; s < S; s += 1024) {
-        const int32_t r0 = a.tmp_r0[base + s];
-        const int32_t r1 = a.sub_off[s] + s_cnt[s];
-        a.tmp_r1[base + s] = r1;
-        if (r1 > r0) {
-          const int c = s / kBands;
-          atomicMin(&s_near, (static_cast<unsigned long long>(ordered_bits(s_sdc[c])) << 32) |
-                                 static_cast<uint32_t>(c));
+    // k-th smallest of the kSeedRows keys (all ones for rows not selected):
+    // per pass the digit whose bin holds it among the keys with the digits
+    // found so far.
+    uint32_t prefix = 0, pmask = 0;
+    int kk = a.k;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      if (tid < 256) s_rh[tid] = 0;
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < kPer; ++u)
+        if ((key[u] & pmask) == prefix) atomicAdd(&s_rh[(key[u] >> shift) & 0xFFu], 1);
+      __syncthreads();
+      if (tid < 64) {
+        int c[4], sum = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          c[j] = s_rh[4 * tid + j];
+          sum += c[j];
         }
-      }
-    }
-    __syncthreads();
-  }
-  {
-    const int near = s_near == ~0ull ? -1 : static_cast<int>(s_near & 0xFFFFFFFFu);
-    int mine = 0;
-    for (int s = tid; s < Sp; s += 1024) {
-      uint32_t key = ~0u;
-      if (s < S) {
-        const int32_t r0 = a.tmp_r0[base + s];
-        const int32_t r1 = a.tmp_r1[base + s];
-        if (r1 > r0) {
-          const float lb = __fsub_rn(s_sdc[s / kBands], __fmul_rn(__fadd_rn(a.rmax[s], delta), sw));
-          // the nearest centroid's sub-lists and NaN bounds sort first with
-          // the top bits 0, carried as NaN (never pruned)
-          const uint32_t ob = lb == lb && s / kBands != near ? ordered_bits(lb) : 0u;
-          key = (ob & ~uint32_t{kItemMask}) | static_cast<uint32_t>(s);
-          ++mine;
+        int x = sum;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(x, o, 64);
+          if (tid >= o) x += y;
         }
-      }
-      s_key[s] = key;
-    }
-    atomicAdd(&s_count, mine);
-  }
-  __syncthreads();
-  // ascending bitonic sort of the Sp keys
-  for (int size = 2; size <= Sp; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int p = tid; p < Sp / 2; p += 1024) {
-        const int i = ((p & ~(stride - 1)) << 1) | (p & (stride - 1));
-        const int j = i | stride;
-        const uint32_t x = s_key[i], y = s_key[j];
-        const bool up = (i & size) == 0;
-        if (up ? (x > y) : (x < y)) {
-          s_key[i] = y;
-          s_key[j] = x;
+        int acc = x - sum;
+        if (acc < kk && kk <= x) {
+          int j = 0;
+          while (acc + c[j] < kk) acc += c[j++];
+          s_pick[0] = 4 * tid + j;
+          s_pick[1] = kk - acc;
         }
       }
       __syncthreads();
+      prefix |= static_cast<uint32_t>(s_pick[0]) << shift;
+      pmask |= 0xFFu << shift;
+      kk = s_pick[1];
     }
-  }
-  const int n_items = s_count;
-  int32_t* s_nt = s_cnt;   // the counts are no longer needed: tile counts in sorted order
-  for (int i = tid; i < n_items; i += 1024) {
-    const uint32_t key = s_key[i];
-    const int s = static_cast<int>(key & kItemMask);
-    const int32_t r0 = a.tmp_r0[base + s], r1 = a.tmp_r1[base + s];
-    s_nt[i] = ((r1 - 1) >> 6) - (r0 >> 6) + 1;
-    a.it_r0[base + i] = r0;
-    a.it_r1[base + i] = r1;
-    const uint32_t ob = key & ~uint32_t{kItemMask};
-    a.it_lb[base + i] = ob == 0u ? __builtin_nanf("") : from_ordered_bits(ob);
+    seed_kth = prefix;
+    if (tid == 0 && seed_kth != ~0u)
+      atomicMin(reinterpret_cast<unsigned long long*>(a.gthr + q),
+                (static_cast<unsigned long long>(seed_kth) << 32) | 0xFFFFFFFFull);
   }
   __syncthreads();
-  // inclusive scan of the tile counts (Hillis-Steele), then exclusive
-  for (int off = 1; off < n_items; off <<= 1) {
-    int v[kMaxItems / 1024] = {};
+  // Phase 2: each sub-list's positions of rows x0 and x1 (ranks), held by
+  // the thread of sub-list s = tid + 1024 j in slot j.
+  int32_t r0[kSPer], r1[kSPer];
+  for (int pass = 0; pass < 2; ++pass) {
+    const int64_t x = pass == 0 ? x0 : x1, bx = x >> a.f_shift;
 #pragma unroll
-    for (int u = 0; u < kMaxItems / 1024; ++u) {
-      const int i = tid + u * 1024;
-      if (i < n_items && i >= off) v[u] = s_nt[i - off];
+    for (int j = 0; j < kSPer; ++j) {
+      const int s = tid + j * 1024;
+      if (s < S) s_cnt[s] = a.cnt_f[bx * S + s];
+    }
+    __syncthreads();
+    for (int64_t r = (bx << a.f_shift) + tid; r < x; r += 4 * 1024) {
+      uint32_t wv[4];
+      int bv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int64_t rr = r + u * 1024;
+        wv[u] = rr < x ? a.words[rr] : 0u;
+        bv[u] = rr < x ? a.band[rr] : 0;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (r + u * 1024 < x) atomicAdd(&s_cnt[static_cast<int>(wv[u] & 0xFFFFu) * kBands + bv[u]], 1);
     }
     __syncthreads();
 #pragma unroll
-    for (int u = 0; u < kMaxItems / 1024; ++u) {
-      const int i = tid + u * 1024;
-      if (i < n_items) s_nt[i] += v[u];
+    for (int j = 0; j < kSPer; ++j) {
+      const int s = tid + j * 1024;
+      const int32_t v = s < S ? a.sub_off[s] + s_cnt[s] : 0;
+      if (pass == 0) r0[j] = v; else r1[j] = v;
     }
     __syncthreads();
   }
-  for (int i = tid; i < n_items; i += 1024) a.it_t[base + i] = i == 0 ? 0 : s_nt[i - 1];
-  // T: the items' bounds rise in order, so the first item the seed's k-th
-  // distance prunes (the test the scan makes, whose bound is never looser)
-  // ends what any scan of the query visits.
-  if (s_lut_bad == 0 && s_seed_kth != ~0u) {
-    const float cut = from_ordered_bits(s_seed_kth);
-    for (int i = tid; i < n_items; i += 1024) {
-      const uint32_t ob = s_key[i] & ~uint32_t{kItemMask};
-      const float lb = ob == 0u ? __builtin_nanf("") : from_ordered_bits(ob);
-      if (lb > 0.0f && __fsub_rn(__fmul_rn(__fmul_rn(lb, lb), a.keep), a.abs_m) > cut) atomicMin(&s_stop, i);
+  // Items: the nearest selected centroid, the bounds' range, then the
+  // buckets' counts and smallest bounds.
+  {
+    unsigned long long nearest = ~0ull;
+#pragma unroll
+    for (int j = 0; j < kSPer; ++j) {
+      const int s = tid + j * 1024;
+      if (s < S && r1[j] > r0[j]) {
+        const int c = s / kBands;
+        const unsigned long long key = (static_cast<unsigned long long>(ordered_bits(s_sdc[c])) << 32) |
+                                       static_cast<uint32_t>(c);
+        nearest = key < nearest ? key : nearest;
+      }
+    }
+    nearest = wave_min_u64(nearest);
+    if ((tid & 63) == 0 && nearest != ~0ull) atomicMin(&s_near, nearest);
+    for (int b = tid; b < kPlanBuckets; b += 1024) {
+      s_hist[b] = 0;
+      s_bmin[b] = ~0u;
     }
   }
   __syncthreads();
-  if (tid == 0) {
-    const int stop = min(s_stop, n_items);
-    hdr[0] = __int_as_float(n_items);
-    hdr[1] = __int_as_float(stop > 0 ? s_nt[stop - 1] : 0);
-    hdr[2] = sw;
-    hdr[3] = delta;
+  const int near = s_near == ~0ull ? -1 : static_cast<int>(s_near & 0xFFFFFFFFu);
+  float lb[kSPer];
+  {
+    int mine = 0;
+    uint32_t lo_b = ~0u, hi_b = 0u;
+#pragma unroll
+    for (int j = 0; j < kSPer; ++j) {
+      const int s = tid + j * 1024;
+      lb[j] = 0.0f;
+      if (s < S && r1[j] > r0[j]) {
+        ++mine;
+        lb[j] = __fsub_rn(s_sdc[s / kBands], __fmul_rn(__fadd_rn(a.rmax[s], delta), sw));
+        if (lb[j] > 0.0f && s / kBands != near) {
+          lo_b = min(lo_b, ordered_bits(lb[j]));
+          hi_b = max(hi_b, ordered_bits(lb[j]));
+        }
+      }
+    }
+    lo_b = wave_min_u32(lo_b);
+    hi_b = wave_max_u32(hi_b);
+    if ((tid & 63) == 0 && lo_b != ~0u) {
+      atomicMin(&s_lo, lo_b);
+      atomicMax(&s_hi, hi_b);
+    }
+    if (mine) atomicAdd(&s_count, mine);
   }
+  __syncthreads();
+  // positive bounds: buckets of 2^shift order-preserving codes from the
+  // smallest, shift the least that fits the range in the buckets
+  const uint32_t lo_bits = s_lo, span = s_lo == ~0u ? 0u : s_hi - s_lo;
+  int shift = 0;
+  while ((span >> shift) > static_cast<uint32_t>(kPlanBuckets - 3)) ++shift;
+  auto bucket = [&](int s, float v) -> int {
+    if (!(v == v) || s / kBands == near) return 0;
+    if (!(v > 0.0f)) return 1;
+    return 2 + static_cast<int>((ordered_bits(v) - lo_bits) >> shift);
+  };
+#pragma unroll
+  for (int j = 0; j < kSPer; ++j) {
+    const int s = tid + j * 1024;
+    if (s < S && r1[j] > r0[j]) {
+      const int b = bucket(s, lb[j]);
+      atomicAdd(&s_hist[b], 1);
+      if (b != 0) atomicMin(&s_bmin[b], ordered_bits(lb[j]));
+    }
+  }
+  __syncthreads();
+  {
+    // bucket offsets: exclusive prefix of the counts, kPlanBuckets / 1024 a thread
+    constexpr int kPer = kPlanBuckets / 1024;
+    int c[kPer], sum = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      c[j] = s_hist[kPer * tid + j];
+      sum += c[j];
+    }
+    int total = 0;
+    int off = block_exclusive_sum(sum, s_w, total);
+    // The first bucket whose smallest bound the seed's k-th distance prunes
+    // (the scan's test, whose bound is never looser): the carried bounds
+    // never decrease, so it and every later bucket are never visited and
+    // are left out.
+    const bool can_prune = s_lut_bad == 0 && seed_kth != ~0u;
+    const float cut = can_prune ? from_ordered_bits(seed_kth) : 0.0f;
+    uint32_t stop = kPlanBuckets;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int b = kPer * tid + j;
+      s_hist[b] = off;
+      off += c[j];
+      if (can_prune && c[j] > 0 && b >= 2) {
+        const float blb = from_ordered_bits(s_bmin[b]);
+        if (__fsub_rn(__fmul_rn(__fmul_rn(blb, blb), a.keep), a.abs_m) > cut) stop = min(stop, static_cast<uint32_t>(b));
+      }
+    }
+    stop = wave_min_u32(stop);
+    if ((tid & 63) == 0 && stop != static_cast<uint32_t>(kPlanBuckets)) atomicMin(&s_stop, static_cast<int>(stop));
+  }
+  __syncthreads();
+  // Each item before the first pruned bucket to its place: rows, carried
+  // bound, tile count (LDS).
+  int32_t* s_nt = s_cnt;   // the counts are no longer needed
+  const int stop_b = min(s_stop, kPlanBuckets);
+  const int n_items = stop_b < kPlanBuckets ? s_hist[stop_b] : s_count;
+  const size_t base = static_cast<size_t>(q) * S;
+  __syncthreads();   // s_hist[stop_b] read before the cursors move
+#pragma unroll
+  for (int j = 0; j < kSPer; ++j) {
+    const int s = tid + j * 1024;
+    if (s < S && r1[j] > r0[j]) {
+      const int b = bucket(s, lb[j]);
+      if (b < stop_b) {
+        const int i = atomicAdd(&s_hist[b], 1);
+        a.it_r0[base + i] = r0[j];
+        a.it_r1[base + i] = r1[j];
+        a.it_lb[base + i] = b == 0 ? __builtin_nanf("") : from_ordered_bits(s_bmin[b]);
+        s_nt[i] = ((r1[j] - 1) >> 6) - (r0[j] >> 6) + 1;
+      }
+    }
+  }
+  __syncthreads();
+  {
+    // tile offsets: exclusive prefix, a contiguous run of items a thread
+    const int per = (n_items + 1023) / 1024;
+    int sum = 0;
+    for (int u = 0; u < per; ++u) {
+      const int i = tid * per + u;
+      if (i < n_items) sum += s_nt[i];
+    }
+    int total = 0;
+    int off = block_exclusive_sum(sum, s_w, total);
+    for (int u = 0; u < per; ++u) {
+      const int i = tid * per + u;
+      if (i < n_items) {
+        const int nt = s_nt[i];
+        a.it_t[base + i] = off;
+        s_nt[i] = off;
+        off += nt;
+      }
+    }
+    if (tid == 0) {
+      hdr[0] = __int_as_float(n_items);
+      hdr[1] = __int_as_float(total);
+      hdr[2] = sw;
+      hdr[3] = delta;
+    }
+  }
+ 
 }
 
 }  // namespace
@@ -658,23 +846,26 @@ hipError_t launch_lut_bounds(const float* alpha, const float* wf, const float* c
 }
 
 size_t list_plan_lds_bytes(int m, int lut_dtype, int C) {
-  const size_t lut = static_cast<size_t>(m) * kKsub * (lut_dtype == 1 ? 2 : 4) + kSeedRows * 4;
-  const size_t items = static_cast<size_t>(C) * kBands * 4 + static_cast<size_t>(list_plan_width(C)) * 4;
+  const size_t lut = static_cast<size_t>(m) * kKsub * (lut_dtype == 1 ? 2 : 4);
+  const size_t items = static_cast<size_t>(C) * kBands * 4 + static_cast<size_t>(kPlanBuckets) * 8;
   return ((static_cast<size_t>(C) * 4 + 15) & ~size_t{15}) + std::max(lut, items);
-}
-
-int list_plan_width(int C) {
-  int p = 2;
-  while (p < C * kBands) p <<= 1;
-  return p;
 }
 
 hipError_t launch_list_plan(const ListPlanArgs& a, int lut_dtype, hipStream_t s) {
   if (a.nq <= 0) return hipSuccess;
-  const void* fn = lut_dtype == 1 ? reinterpret_cast<const void*>(&list_plan_kernel<__half>)
-                                  : reinterpret_cast<const void*>(&list_plan_kernel<float>);
+  const bool h = lut_dtype == 1;
+  const void* fn = nullptr;
+  switch (a.m) {
+    case 16: fn = h ? reinterpret_cast<const void*>(&list_plan_kernel<16, __half>)
+                    : reinterpret_cast<const void*>(&list_plan_kernel<16, float>); break;
+    case 48: fn = h ? reinterpret_cast<const void*>(&list_plan_kernel<48, __half>)
+                    : reinterpret_cast<const void*>(&list_plan_kernel<48, float>); break;
+    case 120: fn = h ? reinterpret_cast<const void*>(&list_plan_kernel<120, __half>)
+                     : reinterpret_cast<const void*>(&list_plan_kernel<120, float>); break;
+    default: return hipErrorInvalidValue;
+  }
   const size_t lds = list_plan_lds_bytes(a.m, lut_dtype, a.C);
-  if (a.n_sub != a.C * kBands || a.Sp != list_plan_width(a.C) || a.Sp > kMaxItems) return hipErrorInvalidValue;
+  if (a.n_sub != a.C * kBands || a.n_sub > kMaxItems) return hipErrorInvalidValue;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
   if (e != hipSuccess) return e;
   ListPlanArgs args = a;
