@@ -78,11 +78,21 @@ constexpr int list_waves_per_eu() {
 // [p0, p1) of its items' concatenated tiles; wavefront w takes the positions
 // congruent to w mod kScanWaves.  Each (job, wavefront) has its own partial
 // list ([pos][c][wave][k]) and union-bound word ([q][c * kScanWaves + wave]).
-template <int MT, typename LutT, bool kCount = false, int kDepth = 2>
+//
+// A tile's code words are fetched in two parts: the words of the first
+// kPreGroups groups of subspaces ahead of time (the ring below), the rest
+// only when a row is still live after those groups (on 10M x 48-byte codes
+// at 10% and 50% selectivity, 86% of the tiles lose every row within the
+// first two groups of eight subspaces, and fetching their other 32 bytes a
+// row was most of the kernel's fabric traffic).
+template <int MT, typename LutT, bool kCount = false, int kDepth = 2, int kPreGroups = 2>
 __global__ __launch_bounds__(kScanWaves * 64) __attribute__((amdgpu_waves_per_eu(list_waves_per_eu<MT, LutT>())))
 void list_scan_kernel(const ListScanArgs a) {
   constexpr int kMW = (MT + 3) / 4;
   constexpr int kGroup = MT % 8 == 0 && MT > 16 ? 8 : (MT % 4 == 0 ? 4 : MT);
+  constexpr int kPre = (kPreGroups * kGroup + 3) / 4 < kMW ? (kPreGroups * kGroup + 3) / 4 : kMW;   // words fetched ahead
+  constexpr int kRest = kMW - kPre;
+  static_assert(kRest == 0 || (kPre * 4) % kGroup == 0, "the words fetched ahead end on a group");
   constexpr int kThreads = kScanWaves * 64;
   constexpr int kVec = 16 / sizeof(LutT);
   constexpr int kVecQ = MT * kKsub / kVec;
@@ -136,9 +146,10 @@ void list_scan_kernel(const ListScanArgs a) {
       if (lane == 0) s_bad[wave] = wave_bad ? 1u : 0u;
       if (threadIdx.x == 0) *s_thr = kNoKey;
       __syncthreads();
-      monotone = true;
+      bool mono = true;
 #pragma unroll
-      for (int w = 0; w < kScanWaves; ++w) monotone = monotone && s_bad[w] == 0;
+      for (int w = 0; w < kScanWaves; ++w) mono = mono && s_bad[w] == 0;
+      monotone = __builtin_amdgcn_readfirstlane(mono ? 1 : 0) != 0;
       cur_q = q;
     }
     const float* hdr = a.hdr + 4 * static_cast<size_t>(q);
@@ -150,11 +161,15 @@ void list_scan_kernel(const ListScanArgs a) {
     float cut = __builtin_nanf("");
     // bound = min(own k-th key, workgroup's, query's); cut its distance (NaN
     // while there is none, or when the table is not monotone).
+    // (every lane holds the same three values; taking lane 0's tells the
+    // compiler so, which keeps the tile walk's state and branches scalar)
     auto refresh = [&]() {
       const uint64_t blk = __hip_atomic_load(s_thr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
       uint64_t b = thr < blk ? thr : blk;
       b = b < gview ? b : gview;
-      bound = b;
+      bound = (static_cast<uint64_t>(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b >> 32))))
+               << 32) |
+              static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b)));
       cut = monotone ? from_ordered_bits(static_cast<uint32_t>(bound >> 32)) : __builtin_nanf("");
     };
     auto pruned = [&](float lb) -> bool {
@@ -190,11 +205,11 @@ void list_scan_kernel(const ListScanArgs a) {
     float v_lb = 0.0f;
     bool in_item = false;
     int i_r0 = 0, i_r1 = 0, i_end = 0, i_t = 0, p = 0;
-    float i_lb = 0.0f;
+    float i_lbv = 0.0f;   // the item's lb^2 * keep - abs (-inf when lb is not positive)
     auto next_tile = [&](int& t, uint64_t& mask) -> bool {
       for (;;) {
         if (in_item) {
-          if (pruned(i_lb)) {
+          if (i_lbv > cut) {
             // this item and every later one
             stop_at = 0;
             pend = 0;
@@ -243,7 +258,8 @@ void list_scan_kernel(const ListScanArgs a) {
         i_r0 = __builtin_amdgcn_readlane(v_r0, j);
         i_r1 = __builtin_amdgcn_readlane(v_r1, j);
         i_t = __builtin_amdgcn_readlane(v_t, j);
-        i_lb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v_lb), j));
+        const float i_lb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v_lb), j));
+        i_lbv = i_lb > 0.0f ? __fsub_rn(__fmul_rn(__fmul_rn(i_lb, i_lb), a.keep), a.abs_m) : -__builtin_inff();
         const int i_nt = ((i_r1 - 1) >> 6) - (i_r0 >> 6) + 1;
         const int from = max(i_t, p_begin);
         p = from + ((wave - from) & (kScanWaves - 1));
@@ -251,10 +267,10 @@ void list_scan_kernel(const ListScanArgs a) {
         in_item = true;
       }
     };
-    auto load = [&](int t, uint32_t (&w)[kMW]) {
+    auto load = [&](int t, uint32_t (&w)[kPre]) {
       const uint32_t* __restrict__ tile = a.codes_t + static_cast<size_t>(t) * (kMW * 64);
 #pragma unroll
-      for (int j = 0; j < kMW; ++j) w[j] = tile[j * 64 + lane];
+      for (int j = 0; j < kPre; ++j) w[j] = tile[j * 64 + lane];
     };
     const bool union_bound = a.union_bound != 0 && k <= kListSlots;
     unsigned long long* pairs = reinterpret_cast<unsigned long long*>(a.slots + static_cast<size_t>(q) * kListSlots);
@@ -334,37 +350,46 @@ void list_scan_kernel(const ListScanArgs a) {
       pool_push(pool, cnt, thr, key, cand, k, a.kpl, a.ids);
       publish(thr);
     };
-    auto sum_tile = [&](int t, uint64_t mask, const uint32_t (&w)[kMW]) {
+    auto sum_tile = [&](int t, uint64_t mask, const uint32_t (&w)[kPre]) {
       if constexpr (kCount) {
         if (lane == 0) atomicAdd(&s_hist[0], 1u);
       }
-      bool live = __builtin_amdgcn_inverse_ballot_w64(mask);
+      uint64_t live = mask;   // live lanes, as a wavefront-wide mask
       float d = 0.0f;
+      uint32_t rest[kRest > 0 ? kRest : 1];
       // (most tiles lose every row to the first groups: the loop ends as soon
       // as no lane is live)
 #pragma unroll
       for (int gr = 0; gr < MT / kGroup; ++gr) {
-        if (__ballot(live) == 0) break;
+        if (live == 0) break;
+        if constexpr (kRest > 0) {
+          if (gr * kGroup == kPre * 4) {
+            // a row is live past the words fetched ahead: the rest of the tile
+            const uint32_t* __restrict__ tile = a.codes_t + static_cast<size_t>(t) * (kMW * 64);
+#pragma unroll
+            for (int j = 0; j < kRest; ++j) rest[j] = tile[(kPre + j) * 64 + lane];
+          }
+        }
         int addr[kGroup];
 #pragma unroll
         for (int u = 0; u < kGroup; ++u) {
           const int m = gr * kGroup + u;
-          addr[u] = m * kKsub + static_cast<int>((w[m >> 2] >> (8 * (m & 3))) & 0xFFu);
+          const uint32_t word = (m >> 2) < kPre ? w[m >> 2] : rest[(m >> 2) - kPre];
+          addr[u] = m * kKsub + static_cast<int>((word >> (8 * (m & 3))) & 0xFFu);
         }
         if constexpr (kCount) {
-          const uint64_t lanes = __ballot(live);
-          if (lanes != 0 && lane == 0) atomicAdd(&s_hist[__popcll(lanes)], static_cast<uint32_t>(kGroup));
+          if (lane == 0) atomicAdd(&s_hist[__popcll(live)], static_cast<uint32_t>(kGroup));
         }
-        if (live) {
+        if (__builtin_amdgcn_inverse_ballot_w64(live)) {
           LutT v[kGroup];
 #pragma unroll
           for (int u = 0; u < kGroup; ++u) v[u] = s_lut[addr[u]];
 #pragma unroll
           for (int u = 0; u < kGroup; ++u) d = __fadd_rn(d, widen(v[u]));
         }
-        live = live && !(d > cut);
+        live &= __ballot(!(d > cut));
       }
-      if (__ballot(live) != 0) consider(live, d, t);
+      if (live != 0) consider(__builtin_amdgcn_inverse_ballot_w64(live), d, t);
     };
 
     // Register sets in a ring: step i refills the set summed in the step
@@ -374,7 +399,7 @@ void list_scan_kernel(const ListScanArgs a) {
     // bounds and unused), so the compiler's wait counts never make a sum wait
     // for the tile loaded after it.  The bound is refreshed once per round
     // of kDepth tiles (a bound a few tiles old is looser, never wrong).
-    uint32_t ws[kDepth][kMW];
+    uint32_t ws[kDepth][kPre];
     int ts[kDepth];
     uint64_t ms[kDepth];
     bool hs[kDepth];
