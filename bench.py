@@ -544,12 +544,17 @@ def main():
         is_list = bool(plans[s].get("list_scan"))
         kind[s] = "list_scan_kernel" if is_list else "scan_kernel"
         if is_list and s in read_hist:
-            # the list scan reads the code tiles it sums (counted by its
-            # counting build; a tile two queries sum is counted twice) and
-            # the tables, and writes partial lists (at most its job cap per
-            # query)
+            # the list scan reads the first two groups' code words of each
+            # tile it sums and the other words of the tiles with a row live
+            # after them (both counted by its counting build; a tile two
+            # queries sum is counted twice), and the tables, and writes
+            # partial lists (at most its job cap per query)
             tiles = read_hist[s][0] / max(1, b_n)
-            b_union = (tiles * ((w.M + 3) // 4 * 256) + batch * w.M * 256 * lut_entry
+            whole = read_hist[s][65] / max(1, b_n)
+            mw = (w.M + 3) // 4
+            group = 8 if (w.M % 8 == 0 and w.M > 16) else (4 if w.M % 4 == 0 else w.M)
+            pre = min(mw, (2 * group + 3) // 4)
+            b_union = (tiles * pre * 256 + whole * (mw - pre) * 256 + batch * w.M * 256 * lut_entry
                        + batch * plans[s]["splits"] * 8 * k * 8)
             b_bytes = b_union
         bin_bytes[s] = (b_union, b_bytes, b_n, b_ms)
@@ -570,8 +575,8 @@ def main():
                             "achieved_GBps": round(4 * lk / b_sec / 1e9, 1),
                             "peak_GBps": round(4 * lk / lsec / 1e9, 1) if lsec > 0 else None,
                             "frac": round(lsec / b_sec, 4),
-                            "reads_per_launch": sum(read_hist[s]) / max(1, b_n),
-                            "lanes_per_read": round(lk / max(1.0, sum(read_hist[s]) / max(1, b_n)), 2)}
+                            "reads_per_launch": sum(read_hist[s][1:65]) / max(1, b_n),
+                            "lanes_per_read": round(lk / max(1.0, sum(read_hist[s][1:65]) / max(1, b_n)), 2)}
         bound = max(roofs, key=lambda r: roofs[r]["frac"])
         roofs["bound"] = bound
         roofs["frac"] = roofs[bound]["frac"]
@@ -937,10 +942,11 @@ def main():
                      "scan_ms_by_kernel": {kk: round(v / args.steps, 4) for kk, v in k_time.items()},
                      "hbm": {"achieved": hbm_achieved, "peak": HBM_PEAK_GBPS, "frac": hbm_achieved / HBM_PEAK_GBPS,
                              "bytes_per_launch": union_per_launch,
-                             "bytes_definition": ("the code tiles the list scan sums (its counting build counts "
-                                                  "them; a tile several queries sum counts once per query, the "
-                                                  "repeats mostly served by L2 and Infinity Cache), + tables "
-                                                  "+ partial lists written"
+                             "bytes_definition": ("the code words the list scan reads: the first two groups' "
+                                                  "words of each tile it sums, the rest of the tiles with a row "
+                                                  "live after them (its counting build counts both; a tile several "
+                                                  "queries sum counts once per query, the repeats mostly served by "
+                                                  "L2 and Infinity Cache), + tables + partial lists written"
                                                   if dom == "list_scan_kernel" else
                                                   "code tiles some query of the batch selects, read once, + tables "
                                                   "+ partial lists written (the least a launch moves to and from "

@@ -553,12 +553,14 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value);
 #define IFVS_N_STAGES 7
 ifvs_status ifvs_read_profile(ifvs_index* idx, double* ms_out, int64_t* launches_out);
 
-/* ifvs_read_scan_reads -- with IFVS_OPT_COUNT_READS on: hist_out[n] (65
+/* ifvs_read_scan_reads -- with IFVS_OPT_COUNT_READS on: hist_out[n] (66
  * entries) = table reads the scans issued with n of a wavefront's 64 lanes
  * active (a read is one LDS instruction of a wavefront; it fetches n table
- * entries), for n = 1..64, and hist_out[0] = the 64-row code tiles the
- * scans summed, both summed over the scans since the last call, which it
- * then clears.
+ * entries), for n = 1..64, hist_out[0] = the 64-row code tiles the scans
+ * summed and hist_out[65] = the tiles the list scan read past their first
+ * two groups of subspaces (it fetches those code words only for tiles with
+ * a row still live), all summed over the scans since the last call, which
+ * it then clears.
  * Waits for `stream`.  The LDS cost of the Rank stage's distance-table
  * lookups (Section 2, stage 2) follows from it and ifvs_probe_lds_gather.
  * All zero when counting was never on.

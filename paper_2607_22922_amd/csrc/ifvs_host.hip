@@ -1065,8 +1065,10 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
       if (value > 1) return fail(IFVS_E_INVALID, "IFVS_OPT_COUNT_READS takes 0 or 1");
       if (value == 1 && !idx->read_hist) {
         IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
-        if (ifvs_status st = dev_alloc(&idx->read_hist, 65, "read histogram"); st != IFVS_OK) return st;
-        IFVS_HIP(hipMemset(idx->read_hist, 0, 65 * sizeof(unsigned long long)), "clearing the read histogram");
+        if (ifvs_status st = dev_alloc(&idx->read_hist, kReadHistEntries, "read histogram"); st != IFVS_OK)
+          return st;
+        IFVS_HIP(hipMemset(idx->read_hist, 0, kReadHistEntries * sizeof(unsigned long long)),
+                 "clearing the read histogram");
       }
       idx->opt_count_reads = static_cast<int>(value);
       return IFVS_OK;
@@ -1779,16 +1781,16 @@ ifvs_status ifvs_encode_predicates(ifvs_index* idx, int32_t nq, const ifvs_predi
 ifvs_status ifvs_read_scan_reads(ifvs_index* idx, int64_t* hist_out, void* stream) {
   if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
   if (!hist_out) return fail(IFVS_E_INVALID, "hist_out is NULL");
-  for (int i = 0; i < 65; ++i) hist_out[i] = 0;
+  for (int i = 0; i < kReadHistEntries; ++i) hist_out[i] = 0;
   if (!idx->read_hist) return IFVS_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
   IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
-  unsigned long long h[65];
+  unsigned long long h[kReadHistEntries];
   IFVS_HIP(hipMemcpyAsync(h, idx->read_hist, sizeof(h), hipMemcpyDeviceToHost, s), "reading the read histogram");
   IFVS_HIP(hipStreamSynchronize(s), "reading the read histogram");
   IFVS_HIP(hipMemsetAsync(idx->read_hist, 0, sizeof(h), s), "clearing the read histogram");
   IFVS_HIP(hipStreamSynchronize(s), "clearing the read histogram");
-  for (int i = 0; i < 65; ++i) hist_out[i] = static_cast<int64_t>(h[i]);
+  for (int i = 0; i < kReadHistEntries; ++i) hist_out[i] = static_cast<int64_t>(h[i]);
   return IFVS_OK;
 }
 

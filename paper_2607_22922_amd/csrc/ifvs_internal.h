@@ -16,7 +16,8 @@ constexpr int kScanWaves = 8;              // wavefronts per scan workgroup
 constexpr int kScanPub = 2;                // best keys per (wavefront, query) published for the workgroup bound
 constexpr int kScanSeed = 8;               // seed candidates per wavefront (kScanWaves * kScanSeed = 64 >= k)
 constexpr int kFilterQueries = 16;         // predicates evaluated per attribute read
-constexpr int kLookupHistBytes = 272;      // LDS of the scan's read-counting build: 65 counters, padded
+constexpr int kReadHistEntries = 66;       // read-counting builds: tiles, reads by 1..64 lanes, tiles fetched whole
+constexpr int kLookupHistBytes = 272;      // LDS of the scan's read-counting build: 66 counters, padded
 constexpr int kCoarseMaxDim = 128;         // largest D with a coarse quantizer (a row held in registers)
 constexpr int kCoarseMax = 4096;           // most coarse centroids
 constexpr int kBands = 4;                  // radius bands per coarse list (sub-lists)
@@ -335,7 +336,8 @@ struct ListScanArgs {
   uint64_t* partials;       // [positions][max_jobs][kScanWaves][k]
   uint64_t* gthr;           // [nq] shared thresholds, all ones before the scan
   uint32_t* slots;          // [nq][kListSlots] union-bound slots, all ones before the scan (list plan)
-  unsigned long long* lookup_hist;  // [65] non-null: the counting build (table reads by lanes, [0] tiles)
+  unsigned long long* lookup_hist;  // [kReadHistEntries] non-null: the counting build (table reads by lanes,
+                                    // [0] tiles, [65] tiles whose later code words were fetched)
   int union_bound;          // 1: the query-wide union bound of the wavefronts' best distances
 };
 constexpr int kListSlots = 2 * kScanWaves * kListJobs;   // two per wavefront of each job of a query

@@ -102,13 +102,13 @@ void list_scan_kernel(const ListScanArgs a) {
   uint64_t* pools = reinterpret_cast<uint64_t*>(smem);
   unsigned long long* s_thr = reinterpret_cast<unsigned long long*>(pools + kScanWaves * a.pool_stride);
   uint32_t* s_bad = reinterpret_cast<uint32_t*>(s_thr + 1);
-  uint32_t* s_hist = s_bad + kScanWaves;   // [65], counting build only
+  uint32_t* s_hist = s_bad + kScanWaves;   // [kReadHistEntries], counting build only
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int k = a.k;
   if constexpr (kCount) {
-    if (threadIdx.x < 65) s_hist[threadIdx.x] = 0;
+    if (threadIdx.x < kReadHistEntries) s_hist[threadIdx.x] = 0;
   }
   int cur_q = -1;
   bool monotone = true;
@@ -365,6 +365,9 @@ void list_scan_kernel(const ListScanArgs a) {
         if constexpr (kRest > 0) {
           if (gr * kGroup == kPre * 4) {
             // a row is live past the words fetched ahead: the rest of the tile
+            if constexpr (kCount) {
+              if (lane == 0) atomicAdd(&s_hist[65], 1u);
+            }
             const uint32_t* __restrict__ tile = a.codes_t + static_cast<size_t>(t) * (kMW * 64);
 #pragma unroll
             for (int j = 0; j < kRest; ++j) rest[j] = tile[(kPre + j) * 64 + lane];
@@ -434,7 +437,7 @@ void list_scan_kernel(const ListScanArgs a) {
   }
   if constexpr (kCount) {
     __syncthreads();
-    if (threadIdx.x < 65 && s_hist[threadIdx.x] != 0)
+    if (threadIdx.x < kReadHistEntries && s_hist[threadIdx.x] != 0)
       atomicAdd(&a.lookup_hist[threadIdx.x], static_cast<unsigned long long>(s_hist[threadIdx.x]));
   }
 }

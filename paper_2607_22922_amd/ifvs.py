@@ -344,9 +344,10 @@ class Index:
         return wz
 
     def read_scan_reads(self, stream=None) -> list:
-        """With OPT_COUNT_READS on: [65] table reads issued with n active
-        lanes (index n) since the last read."""
-        out = (ctypes.c_int64 * 65)()
+        """With OPT_COUNT_READS on: [66] table reads issued with n active
+        lanes (index n), tiles summed ([0]) and tiles the list scan read
+        whole ([65]) since the last read."""
+        out = (ctypes.c_int64 * 66)()
         _check(_lib.ifvs_read_scan_reads(self.handle, out, _stream(stream)))
         return list(out)
 

@@ -307,3 +307,34 @@ def test_m16_index(B):
             res = O.filtered_search(ox, _np(q[i]), preds[i], 10, w_z=_np(w.w_z[s][i]))
             check_search_row(ids[i], dist[i], res["ids"], res["dist"], f"m16 s={s} q{i}")
     idx.close()
+
+
+def test_counting_build_of_the_list_scan(B, c4s):
+    """The list scan's read-counting build: same answers as the timed build;
+    it sums at least one tile, reads every tile's first groups and the rest
+    of at most every tile, and its table reads come in groups of eight
+    subspaces (M = 48)."""
+    w, idx, ox = c4s
+    nq = 24
+    s = 0.5
+    preds = w.preds[s][:nq]
+    q = w.queries[:nq]
+    alpha, wf = idx.select_codebook(q, preds, w.w_z[s][:nq])
+    lut = idx.build_lut(q, alpha, wf)
+    idx.set_option(B.OPT_COARSE, 2)
+    try:
+        ids0, d0 = idx.search_bounded(preds, lut, alpha, wf, 10)
+        idx.set_option(B.OPT_COUNT_READS, 1)
+        idx.read_scan_reads()
+        ids1, d1 = idx.search_bounded(preds, lut, alpha, wf, 10)
+        torch.cuda.synchronize()
+        assert idx.last_coarse()
+        hist = idx.read_scan_reads()
+    finally:
+        idx.set_option(B.OPT_COUNT_READS, 0)
+        idx.set_option(B.OPT_COARSE, 0)
+    assert torch.equal(ids1, ids0) and torch.equal(d1.view(torch.int32), d0.view(torch.int32))
+    assert len(hist) == 66
+    assert hist[0] > 0 and 0 <= hist[65] <= hist[0]
+    assert sum(hist[1:65]) % 8 == 0
+    assert sum(hist[1:65]) >= 8 * hist[0]   # every tile reads its first group

@@ -68,7 +68,7 @@ def test_counting_scan_same_results_and_every_read_counted(B):
     assert torch.equal(ids0, ids1) and torch.equal(d0.view(torch.int32), d1.view(torch.int32))
     assert hist[0] == _interval_tiles(ix, preds)    # entry 0: every tile of each interval, once
     assert sum(n * hist[n] for n in range(1, 65)) == M * n_sel
-    assert sum(hist[1:]) % 8 == 0      # reads come in groups of 8 subspaces at M = 48
+    assert sum(hist[1:65]) % 8 == 0    # reads come in groups of 8 subspaces at M = 48
 
 
 def test_counting_scan_with_early_abandonment(B):
