@@ -190,7 +190,6 @@ struct ifvs_index {
   int64_t* iv_dev = nullptr;     // [max_batch][2]
   uint64_t* gthr_dev = nullptr;  // [max_batch] shared scan thresholds
   float* bound_parts = nullptr;  // [max_batch][2][m] coarse-bound partial maxima
-  float* bounds_ws = nullptr;    // [max_batch][2] coarse-bound factors of a bounded search
   int32_t* slot_order_dev = nullptr;  // [slot_order_cap] chunk-grid scan dispatch order
   int64_t slot_order_cap = 0;
   DevPred* staging[kStagingSlots] = {};   // pinned: [max_batch] DevPred + [max_batch] int32
@@ -308,7 +307,7 @@ struct ifvs_index {
                     static_cast<void*>(perm), static_cast<void*>(bank), static_cast<void*>(W),
                     static_cast<void*>(preds_dev), static_cast<void*>(qorder_dev),
                     static_cast<void*>(iv_dev), static_cast<void*>(gthr_dev), static_cast<void*>(bitmap),
-                    static_cast<void*>(bound_parts), static_cast<void*>(bounds_ws),
+                    static_cast<void*>(bound_parts),
                     static_cast<void*>(slot_order_dev),
                     static_cast<void*>(counts), static_cast<void*>(count_parts), static_cast<void*>(vstart),
                     static_cast<void*>(partials), static_cast<void*>(codes_rm),
@@ -981,8 +980,6 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
     return bail(st);
   if ((st = dev_alloc(&idx->bound_parts, static_cast<size_t>(d.max_batch) * 2 * d.m, "bound workspace")) != IFVS_OK)
     return bail(st);
-  if ((st = dev_alloc(&idx->bounds_ws, static_cast<size_t>(d.max_batch) * 2, "bound workspace")) != IFVS_OK)
-    return bail(st);
   if ((st = dev_alloc(&idx->gthr_dev, static_cast<size_t>(d.max_batch), "scan thresholds")) != IFVS_OK)
     return bail(st);
   // Room for the dispatch order of a chunk-grid scan: 8 XCD runs of query
@@ -1219,6 +1216,7 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
       list_scan_supported(idx->m, lut_dtype) &&
       list_plan_lds_bytes(idx->m, lut_dtype, cl.C) <= size_t{kLdsBudget} &&
       list_scan_lds_bytes(idx->m, lut_dtype, pool_stride_for(k)) <= size_t{kLdsBudget} &&
+      list_jobs_lds_bytes(nq) <= size_t{kLdsBudget} &&
       static_cast<size_t>(nq) * list_splits * kScanWaves * k <= ws.partial_keys &&
       (idx->opt_coarse == 2 || span >= kCoarseAutoTiles);
   if (idx->opt_count_reads && !list_mode &&
@@ -1245,9 +1243,8 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
                                ws.slot_order, ordered ? n_order : 0, s));
   if (ifvs_status st = release_slot(idx, slot, s); st != IFVS_OK) return st;
   if (list_mode) {
-    IFVS_LAUNCH(idx, kStCoarse, s, "launching table bound kernels",
-                launch_lut_bounds(alpha, wf, idx->cpq, idx->W, nq, idx->m, idx->r, idx->dsub, idx->bound_parts,
-                                  idx->bounds_ws, s));
+    IFVS_LAUNCH(idx, kStCoarse, s, "launching table bound kernel",
+                launch_bound_parts(alpha, wf, idx->cpq, idx->W, nq, idx->m, idx->r, idx->dsub, idx->bound_parts, s));
     ListPlanArgs pa{};
     pa.lut = lut;
     pa.m = idx->m;
@@ -1256,7 +1253,8 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     pa.mw = idx->mw;
     pa.C = cl.C;
     pa.n_sub = cl.C * kBands;
-    pa.bounds = idx->bounds_ws;
+    pa.parts = idx->bound_parts;
+    pa.grow = bound_grow(idx->m, idx->dsub);
     pa.iv = ws.iv;
     pa.cnt_f = cl.cnt_f;
     pa.f_shift = cl.f_shift;
@@ -1276,7 +1274,6 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     pa.it_lb = cl.it_lb;
     pa.hdr = cl.hdr;
     pa.slots = cl.slots;
-    IFVS_LAUNCH(idx, kStCoarse, s, "launching list plan kernel", launch_list_plan(pa, lut_dtype, s));
     ListJobArgs ja{};
     ja.hdr = cl.hdr;
     ja.qorder = ws.qorder;
@@ -1289,6 +1286,7 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
     ja.n_keys = cl.n_keys;
     ja.job_next = cl.job_ctr;
     ja.job_total = cl.job_ctr + 1;
+    IFVS_LAUNCH(idx, kStCoarse, s, "launching list plan kernel", launch_list_plan(pa, lut_dtype, s));
     IFVS_LAUNCH(idx, kStCoarse, s, "launching list job table kernel", launch_list_jobs(ja, s));
     ListScanArgs sa{};
     sa.codes_t = cl.codes_t;

@@ -260,6 +260,10 @@ hipError_t launch_coarse_rows(const uint32_t* codes_t, int64_t n, int64_t n_pad,
 // [nq][2][m] workspace.
 hipError_t launch_lut_bounds(const float* alpha, const float* wf, const float* cpq, const float* W, int nq, int m,
                              int r, int dsub, float* parts, float* bounds, hipStream_t s);
+// The first of those two kernels alone (the list plan finishes the bounds).
+hipError_t launch_bound_parts(const float* alpha, const float* wf, const float* cpq, const float* W, int nq, int m,
+                              int r, int dsub, float* parts, hipStream_t s);
+float bound_grow(int m, int dsub);   // delta's rounding allowance
 // List order: rows grouped by sub-list s = (centroid c, radius band b),
 // s = c * kBands + b, positions [sub_off[s], sub_off[s+1]), each sub-list in
 // layout order.  Code tiles and original ids gathered through src_rows[p] =
@@ -267,13 +271,30 @@ hipError_t launch_lut_bounds(const float* alpha, const float* wf, const float* c
 hipError_t launch_gather_list(const uint32_t* src_t, int mw, const int32_t* perm, const int32_t* src_rows, int64_t n,
                               int64_t n_tiles, uint32_t* dst_t, int32_t* ids, hipStream_t s);
 
+// List scan (k_listscan.hip): the Rank and Select stages over the items of
+// each query in bound order, persistent workgroups taking jobs (chunks of a
+// query's tiles) from a table built after the plan.
+constexpr int kListJobs = 16;     // most jobs (and partial-list slots) per query
+constexpr int kJobTiles = 1024;   // tiles per job before a query is split further
+constexpr int kListPreGroups = 3; // subspace groups whose code words the list scan fetches ahead
+struct ListJobArgs {
+  const float* hdr;         // [nq][4] list plan headers ([1]: tiles to scan, int bits)
+  const int32_t* qorder;
+  int nq, np2;              // np2: power of two >= nq
+  int k, max_jobs;          // max_jobs <= kListJobs
+  int4* jobs;               // [nq * kListJobs] (position, chunk, first tile position, end)
+  int32_t* n_keys;          // [positions] partial keys written per position
+  int* job_next;
+  int* job_total;
+};
 // Per-query list plan (one workgroup per original query index).
 struct ListPlanArgs {
   const void* lut;          // [nq][m][256] tables (fp32 or binary16)
   int m, nq;
   const uint32_t* cc_t;     // [mw][C] centroid code words
   int mw, C, n_sub;         // n_sub = C * kBands sub-lists
-  const float* bounds;      // [nq][2]: sqrt(max w), delta (ifvs_lut_bounds)
+  const float* parts;       // [nq][2][m] bound_parts output; the plan reduces it to sqrt(max w), delta
+  float grow;               // delta's rounding allowance (launch_lut_bounds)
   const int64_t* iv;        // [nq][2] layout row interval of each query
   const int32_t* cnt_f;     // [(n >> f_shift) + 1][n_sub]: rows of sub-list s among layout rows [0, b << f_shift)
   int f_shift;
@@ -298,23 +319,10 @@ struct ListPlanArgs {
 };
 size_t list_plan_lds_bytes(int m, int lut_dtype, int C);
 hipError_t launch_list_plan(const ListPlanArgs& a, int lut_dtype, hipStream_t s);
-
-// List scan (k_listscan.hip): the Rank and Select stages over the items of
-// each query in bound order, persistent workgroups taking jobs (chunks of a
-// query's tiles) from a table built after the plan.
-constexpr int kListJobs = 16;     // most jobs (and partial-list slots) per query
-constexpr int kJobTiles = 512;    // tiles per job before a query is split further
-struct ListJobArgs {
-  const float* hdr;         // [nq][4] list plan headers ([1]: tiles to scan, int bits)
-  const int32_t* qorder;
-  int nq, np2;              // np2: power of two >= nq
-  int k, max_jobs;          // max_jobs <= kListJobs
-  int4* jobs;               // [nq * kListJobs] (position, chunk, first tile position, end)
-  int32_t* n_keys;          // [positions] partial keys written per position
-  int* job_next;
-  int* job_total;
-};
+// The job table from the plan's headers (one workgroup).
 hipError_t launch_list_jobs(const ListJobArgs& a, hipStream_t s);
+
+size_t list_jobs_lds_bytes(int nq);   // the job table's LDS (one workgroup sorts the batch)
 struct ListScanArgs {
   const uint32_t* codes_t;  // [n_tiles][mw][64] list-order code words
   const int32_t* ids;       // list position -> original id

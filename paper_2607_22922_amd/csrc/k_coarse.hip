@@ -293,11 +293,9 @@ __global__ __launch_bounds__(256) void bound_parts_kernel(const float* __restric
   }
 }
 
-__global__ __launch_bounds__(256) void bound_final_kernel(const float* __restrict__ parts, int M, int nq, float grow,
-                                                          float* __restrict__ bounds) {
-  const int q = blockIdx.x * blockDim.x + threadIdx.x;
-  if (q >= nq) return;
-  const float* pd = parts + static_cast<size_t>(q) * 2 * M;
+// sqrt(max_m parts[1][m]) widened by 2^-19 and sqrt(sum_m 4 parts[0][m]) *
+// grow, from one query's parts (pd = parts[q]).
+__device__ void reduce_bound_parts(const float* __restrict__ pd, int M, float grow, float& sw, float& delta) {
   const float* pw = pd + M;
   float d2 = 0.0f, wm = 0.0f;
   for (int m0 = 0; m0 < M; m0 += 16) {
@@ -316,8 +314,15 @@ __global__ __launch_bounds__(256) void bound_final_kernel(const float* __restric
       }
     }
   }
-  bounds[2 * q] = __fmul_rn(sqrtf(wm), 1.0f + 0x1p-19f);
-  bounds[2 * q + 1] = __fmul_rn(sqrtf(d2), grow);
+  sw = __fmul_rn(sqrtf(wm), 1.0f + 0x1p-19f);
+  delta = __fmul_rn(sqrtf(d2), grow);
+}
+
+__global__ __launch_bounds__(256) void bound_final_kernel(const float* __restrict__ parts, int M, int nq, float grow,
+                                                          float* __restrict__ bounds) {
+  const int q = blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= nq) return;
+  reduce_bound_parts(parts + static_cast<size_t>(q) * 2 * M, M, grow, bounds[2 * q], bounds[2 * q + 1]);
 }
 
 // List order (rows grouped by coarse centroid, each list in layout order):
@@ -352,6 +357,78 @@ __global__ __launch_bounds__(256) void gather_list_rows_kernel(const int32_t* __
     id = perm ? perm[r] : static_cast<int32_t>(r);
   }
   ids[p] = id;
+}
+
+// The job table (one 1024-thread workgroup): per query position, jobs =
+// min(max_jobs, ceil(T / kJobTiles)) chunks of about equal size (multiples of
+// kScanWaves positions) of its T tiles (the tiles of the items the plan
+// kept), the queries with the most tiles first; the keys each position's
+// jobs write are counted for the merge; the job counter is reset.  LDS:
+// list_jobs_lds_bytes(nq) at smem.
+__device__ void build_job_table(const ListJobArgs& a, unsigned char* smem) {
+  uint64_t* s_key = reinterpret_cast<uint64_t*>(smem);   // [np2]
+  int32_t* s_base = reinterpret_cast<int32_t*>(s_key + a.np2);   // [np2 + 1]
+  const int tid = threadIdx.x;
+  for (int i = tid; i < a.np2; i += 1024) {
+    uint64_t key = ~0ull;
+    if (i < a.nq) {
+      const int q = a.qorder[i];
+      const int w = __float_as_int(a.hdr[4 * static_cast<size_t>(q) + 1]);
+      key = (static_cast<uint64_t>(0x7FFFFFFF - w) << 32) | static_cast<uint32_t>(i);
+    }
+    s_key[i] = key;
+  }
+  __syncthreads();
+  for (int size = 2; size <= a.np2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int p = tid; p < a.np2 / 2; p += 1024) {
+        const int i = ((p & ~(stride - 1)) << 1) | (p & (stride - 1));
+        const int j = i | stride;
+        const uint64_t x = s_key[i], y = s_key[j];
+        const bool up = (i & size) == 0;
+        if (up ? (x > y) : (x < y)) {
+          s_key[i] = y;
+          s_key[j] = x;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // jobs per position in sorted order, then their exclusive prefix (serial
+  // per thread block of positions, then across blocks)
+  auto jobs_of = [&](int i) -> int {
+    if (i >= a.nq) return 0;
+    const int w = 0x7FFFFFFF - static_cast<int>(s_key[i] >> 32);
+    return w <= 0 ? 0 : min(a.max_jobs, (w + kJobTiles - 1) / kJobTiles);
+  };
+  const int per = (a.np2 + 1023) / 1024;
+  int mine = 0;
+  for (int u = 0; u < per; ++u) mine += jobs_of(tid * per + u);
+  s_base[tid] = mine;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int v = tid >= off ? s_base[tid - off] : 0;
+    __syncthreads();
+    s_base[tid] += v;
+    __syncthreads();
+  }
+  int base = tid == 0 ? 0 : s_base[tid - 1];
+  for (int u = 0; u < per; ++u) {
+    const int i = tid * per + u;
+    if (i >= a.nq) break;
+    const int pos = static_cast<int>(s_key[i] & 0xFFFFFFFFu);
+    const int w = 0x7FFFFFFF - static_cast<int>(s_key[i] >> 32);
+    const int nj = jobs_of(i);
+    const int chunk = nj > 0 ? ((w + nj - 1) / nj + kScanWaves - 1) / kScanWaves * kScanWaves : 0;
+    for (int c = 0; c < nj; ++c)
+      a.jobs[base + c] = make_int4(pos, c, c * chunk, min(w, (c + 1) * chunk));
+    base += nj;
+    a.n_keys[pos] = nj * kScanWaves * a.k;   // the merge reads the written chunks only
+  }
+  if (tid == 1023) {
+    *a.job_total = s_base[1023];
+    *a.job_next = 0;
+  }
 }
 
 // Wavefront minimum / maximum (one LDS atomic per wavefront then, not one
@@ -439,7 +516,7 @@ __device__ int block_exclusive_sum(int v, int* s_w, int& total) {
 // shared threshold, with the largest id so rows at that distance stay
 // eligible.
 template <int MT, typename LutT>
-__global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
+__device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const float sw, const float delta) {
   constexpr int kMW = (MT + 3) / 4;
   constexpr int kSPer = kMaxItems / 1024;   // sub-lists a thread holds (in registers)
   static_assert(kSeedRows % 1024 == 0 && kPlanBuckets % 1024 == 0 && kMaxItems % 1024 == 0,
@@ -464,7 +541,6 @@ __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
   const int q = blockIdx.x;
   const int tid = threadIdx.x;
   const int64_t x0 = a.iv[2 * q], x1 = a.iv[2 * q + 1];
-  const float sw = a.bounds[2 * q], delta = a.bounds[2 * q + 1];
   float* hdr = a.hdr + 4 * static_cast<size_t>(q);
   for (int i = tid; i < kListSlots; i += 1024) a.slots[static_cast<size_t>(q) * kListSlots + i] = ~0u;
   if (x1 <= x0) {
@@ -779,6 +855,28 @@ __global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
  
 }
 
+// The plan of query blockIdx.x, its bound factors reduced from the parts
+// first.  (Building the job table in the workgroup that finishes last, behind
+// a device-wide counter, cost more than its own launch: every workgroup's
+// release fence writes back its L2.)
+template <int MT, typename LutT>
+__global__ __launch_bounds__(1024) void list_plan_kernel(const ListPlanArgs a) {
+  __shared__ float s_bounds[2];
+  if (threadIdx.x == 0) {
+    float sw, delta;
+    reduce_bound_parts(a.parts + static_cast<size_t>(blockIdx.x) * 2 * a.m, a.m, a.grow, sw, delta);
+    s_bounds[0] = sw;
+    s_bounds[1] = delta;
+  }
+  __syncthreads();
+  plan_one_query<MT, LutT>(a, s_bounds[0], s_bounds[1]);
+}
+
+__global__ __launch_bounds__(1024) void list_jobs_kernel(const ListJobArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  build_job_table(a, smem);
+}
+
 }  // namespace
 
 int64_t coarse_samples(int64_t n, int C) {
@@ -828,8 +926,10 @@ hipError_t launch_coarse_rows(const uint32_t* codes_t, int64_t n, int64_t n_pad,
   return hipGetLastError();
 }
 
-hipError_t launch_lut_bounds(const float* alpha, const float* wf, const float* cpq, const float* W, int nq, int m,
-                             int r, int dsub, float* parts, float* bounds, hipStream_t s) {
+float bound_grow(int m, int dsub) { return 1.0f + 2.0f * static_cast<float>(dsub + m + 8) * 0x1p-24f + 0x1p-20f; }
+
+hipError_t launch_bound_parts(const float* alpha, const float* wf, const float* cpq, const float* W, int nq, int m,
+                              int r, int dsub, float* parts, hipStream_t s) {
   if (nq <= 0) return hipSuccess;
   const dim3 g(static_cast<unsigned>(m), static_cast<unsigned>((nq + kBoundQueries - 1) / kBoundQueries));
   if (dsub == 2 && r == 8)
@@ -838,10 +938,16 @@ hipError_t launch_lut_bounds(const float* alpha, const float* wf, const float* c
     bound_parts_kernel<8, 8><<<g, 256, 0, s>>>(alpha, wf, cpq, W, m, dsub, r, nq, parts);
   else
     bound_parts_kernel<0, 0><<<g, 256, 0, s>>>(alpha, wf, cpq, W, m, dsub, r, nq, parts);
-  const hipError_t e = hipGetLastError();
+  return hipGetLastError();
+}
+
+hipError_t launch_lut_bounds(const float* alpha, const float* wf, const float* cpq, const float* W, int nq, int m,
+                             int r, int dsub, float* parts, float* bounds, hipStream_t s) {
+  if (nq <= 0) return hipSuccess;
+  const hipError_t e = launch_bound_parts(alpha, wf, cpq, W, nq, m, r, dsub, parts, s);
   if (e != hipSuccess) return e;
-  const float grow = 1.0f + 2.0f * static_cast<float>(dsub + m + 8) * 0x1p-24f + 0x1p-20f;
-  bound_final_kernel<<<static_cast<unsigned>((nq + 255) / 256), 256, 0, s>>>(parts, m, nq, grow, bounds);
+  bound_final_kernel<<<static_cast<unsigned>((nq + 255) / 256), 256, 0, s>>>(parts, m, nq, bound_grow(m, dsub),
+                                                                             bounds);
   return hipGetLastError();
 }
 
@@ -849,6 +955,12 @@ size_t list_plan_lds_bytes(int m, int lut_dtype, int C) {
   const size_t lut = static_cast<size_t>(m) * kKsub * (lut_dtype == 1 ? 2 : 4);
   const size_t items = static_cast<size_t>(C) * kBands * 4 + static_cast<size_t>(kPlanBuckets) * 8;
   return ((static_cast<size_t>(C) * 4 + 15) & ~size_t{15}) + std::max(lut, items);
+}
+
+size_t list_jobs_lds_bytes(int nq) {
+  size_t np2 = 1;
+  while (np2 < static_cast<size_t>(nq)) np2 *= 2;
+  return np2 * 8 + 1025 * 4;
 }
 
 hipError_t launch_list_plan(const ListPlanArgs& a, int lut_dtype, hipStream_t s) {
@@ -871,6 +983,17 @@ hipError_t launch_list_plan(const ListPlanArgs& a, int lut_dtype, hipStream_t s)
   ListPlanArgs args = a;
   void* kargs[] = {&args};
   return hipLaunchKernel(fn, dim3(static_cast<unsigned>(a.nq)), dim3(1024), kargs, lds, s);
+}
+
+hipError_t launch_list_jobs(const ListJobArgs& a, hipStream_t s) {
+  if (a.nq <= 0) return hipSuccess;
+  const size_t lds = list_jobs_lds_bytes(a.nq);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&list_jobs_kernel),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+  if (e != hipSuccess) return e;
+  ListJobArgs args = a;
+  void* kargs[] = {&args};
+  return hipLaunchKernel(reinterpret_cast<const void*>(&list_jobs_kernel), dim3(1), dim3(1024), kargs, lds, s);
 }
 
 hipError_t launch_gather_list(const uint32_t* src_t, int mw, const int32_t* perm, const int32_t* src_rows, int64_t n,

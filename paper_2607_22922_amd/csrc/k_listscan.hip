@@ -83,9 +83,9 @@ constexpr int list_waves_per_eu() {
 // kPreGroups groups of subspaces ahead of time (the ring below), the rest
 // only when a row is still live after those groups (on 10M x 48-byte codes
 // at 10% and 50% selectivity, 86% of the tiles lose every row within the
-// first two groups of eight subspaces, and fetching their other 32 bytes a
-// row was most of the kernel's fabric traffic).
-template <int MT, typename LutT, bool kCount = false, int kDepth = 2, int kPreGroups = 2>
+// first two groups of eight subspaces and 97% within three, and fetching
+// every tile's 48 bytes a row was most of the kernel's fabric traffic).
+template <int MT, typename LutT, bool kCount = false, int kDepth = 2, int kPreGroups = kListPreGroups>
 __global__ __launch_bounds__(kScanWaves * 64) __attribute__((amdgpu_waves_per_eu(list_waves_per_eu<MT, LutT>())))
 void list_scan_kernel(const ListScanArgs a) {
   constexpr int kMW = (MT + 3) / 4;
@@ -442,77 +442,6 @@ void list_scan_kernel(const ListScanArgs a) {
   }
 }
 
-// The job table (one workgroup): per query position, jobs = min(kListJobs,
-// ceil(W / kJobTiles)) chunks of about equal size (multiples of kScanWaves
-// positions) of its W tiles (the tiles before the first item the plan's
-// seed bound prunes), the heaviest queries first; the keys each position's
-// jobs write are counted for the merge; the job counter is reset.
-__global__ __launch_bounds__(1024) void list_jobs_kernel(const ListJobArgs a) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  uint64_t* s_key = reinterpret_cast<uint64_t*>(smem);   // [np2]
-  int32_t* s_base = reinterpret_cast<int32_t*>(s_key + a.np2);   // [np2 + 1]
-  const int tid = threadIdx.x;
-  for (int i = tid; i < a.np2; i += 1024) {
-    uint64_t key = ~0ull;
-    if (i < a.nq) {
-      const int q = a.qorder[i];
-      const int w = __float_as_int(a.hdr[4 * static_cast<size_t>(q) + 1]);
-      key = (static_cast<uint64_t>(0x7FFFFFFF - w) << 32) | static_cast<uint32_t>(i);
-    }
-    s_key[i] = key;
-  }
-  __syncthreads();
-  for (int size = 2; size <= a.np2; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int p = tid; p < a.np2 / 2; p += 1024) {
-        const int i = ((p & ~(stride - 1)) << 1) | (p & (stride - 1));
-        const int j = i | stride;
-        const uint64_t x = s_key[i], y = s_key[j];
-        const bool up = (i & size) == 0;
-        if (up ? (x > y) : (x < y)) {
-          s_key[i] = y;
-          s_key[j] = x;
-        }
-      }
-      __syncthreads();
-    }
-  }
-  // jobs per position in sorted order, then their exclusive prefix (serial
-  // per thread block of positions, then across blocks)
-  auto jobs_of = [&](int i) -> int {
-    if (i >= a.nq) return 0;
-    const int w = 0x7FFFFFFF - static_cast<int>(s_key[i] >> 32);
-    return w <= 0 ? 0 : min(a.max_jobs, (w + kJobTiles - 1) / kJobTiles);
-  };
-  const int per = (a.np2 + 1023) / 1024;
-  int mine = 0;
-  for (int u = 0; u < per; ++u) mine += jobs_of(tid * per + u);
-  s_base[tid] = mine;
-  __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
-    const int v = tid >= off ? s_base[tid - off] : 0;
-    __syncthreads();
-    s_base[tid] += v;
-    __syncthreads();
-  }
-  int base = tid == 0 ? 0 : s_base[tid - 1];
-  for (int u = 0; u < per; ++u) {
-    const int i = tid * per + u;
-    if (i >= a.nq) break;
-    const int pos = static_cast<int>(s_key[i] & 0xFFFFFFFFu);
-    const int w = 0x7FFFFFFF - static_cast<int>(s_key[i] >> 32);
-    const int nj = jobs_of(i);
-    const int chunk = nj > 0 ? ((w + nj - 1) / nj + kScanWaves - 1) / kScanWaves * kScanWaves : 0;
-    for (int c = 0; c < nj; ++c)
-      a.jobs[base + c] = make_int4(pos, c, c * chunk, min(w, (c + 1) * chunk));
-    base += nj;
-    a.n_keys[pos] = nj * kScanWaves * a.k;   // the merge reads the written chunks only
-  }
-  if (tid == 1023) {
-    *a.job_total = s_base[1023];
-    *a.job_next = 0;
-  }
-}
 
 template <int MT>
 const void* pick_list_t(int lut_dtype, bool count) {
@@ -544,17 +473,6 @@ bool list_scan_supported(int m, int lut_dtype) { return pick_list(m, lut_dtype, 
 
 size_t list_scan_lds_bytes(int m, int lut_dtype, int pool_stride) {
   return static_cast<size_t>(m) * kKsub * (lut_dtype == 1 ? 2 : 4) + list_dyn_bytes(pool_stride);
-}
-
-hipError_t launch_list_jobs(const ListJobArgs& a, hipStream_t s) {
-  if (a.nq <= 0) return hipSuccess;
-  const size_t lds = static_cast<size_t>(a.np2) * 8 + 1025 * 4;
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&list_jobs_kernel),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
-  if (e != hipSuccess) return e;
-  ListJobArgs args = a;
-  void* kargs[] = {&args};
-  return hipLaunchKernel(reinterpret_cast<const void*>(&list_jobs_kernel), dim3(1), dim3(1024), kargs, lds, s);
 }
 
 hipError_t launch_list_scan(const ListScanArgs& a, int lut_dtype, hipStream_t s) {
