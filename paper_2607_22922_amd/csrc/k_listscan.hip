@@ -99,7 +99,9 @@ void list_scan_kernel(const ListScanArgs a) {
   __shared__ __align__(16) LutT s_lut[MT * kKsub];
   __shared__ int4 s_job;
   extern __shared__ __align__(16) unsigned char smem[];
-  uint64_t* pools = reinterpret_cast<uint64_t*>(smem);
+  int4* s_item = reinterpret_cast<int4*>(smem);                       // [kScanWaves][64] (r0, r1, first, end)
+  int2* s_item2 = reinterpret_cast<int2*>(s_item + kScanWaves * 64);  // [kScanWaves][64] (tile base, bound test)
+  uint64_t* pools = reinterpret_cast<uint64_t*>(s_item2 + kScanWaves * 64);
   unsigned long long* s_thr = reinterpret_cast<unsigned long long*>(pools + kScanWaves * a.pool_stride);
   uint32_t* s_bad = reinterpret_cast<uint32_t*>(s_thr + 1);
   uint32_t* s_hist = s_bad + kScanWaves;   // [kReadHistEntries], counting build only
@@ -157,7 +159,7 @@ void list_scan_kernel(const ListScanArgs a) {
 
     int cnt = 0;
     uint64_t thr = kNoKey, published = kNoKey, bound = kNoKey;
-    uint64_t gview = __hip_atomic_load(a.gthr + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), gnext = gview;
+    uint64_t gview = __hip_atomic_load(a.gthr + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     float cut = __builtin_nanf("");
     // bound = min(own k-th key, workgroup's, query's); cut its distance (NaN
     // while there is none, or when the table is not monotone).
@@ -171,9 +173,6 @@ void list_scan_kernel(const ListScanArgs a) {
                << 32) |
               static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b)));
       cut = monotone ? from_ordered_bits(static_cast<uint32_t>(bound >> 32)) : __builtin_nanf("");
-    };
-    auto pruned = [&](float lb) -> bool {
-      return lb > 0.0f && __fsub_rn(__fmul_rn(__fmul_rn(lb, lb), a.keep), a.abs_m) > cut;
     };
     refresh();
 
@@ -197,15 +196,18 @@ void list_scan_kernel(const ListScanArgs a) {
       item0 = lo + (63 - __builtin_clzll(__ballot(le) | 1ull));
     }
 
-    // Tile generator over the job's items.
+    // Tile generator over the job's items.  A batch of 64 items is read one
+    // item a lane; what a wavefront needs of each item is kept in its LDS
+    // rows (an item's start reads them back), so no per-lane register is
+    // carried along the tile loop.
     int batch = item0 - 64;
     int stop_at = n_items;   // items from here on are prunable or past the job
     uint64_t pend = 0;
-    int v_r0 = 0, v_r1 = 0, v_t = 0;
-    float v_lb = 0.0f;
     bool in_item = false;
-    int i_r0 = 0, i_r1 = 0, i_end = 0, i_t = 0, p = 0;
+    int i_r0 = 0, i_r1 = 0, i_end = 0, i_tb = 0, p = 0;
     float i_lbv = 0.0f;   // the item's lb^2 * keep - abs (-inf when lb is not positive)
+    int4* my_items = s_item + wave * 64;
+    int2* my_items2 = s_item2 + wave * 64;
     auto next_tile = [&](int& t, uint64_t& mask) -> bool {
       for (;;) {
         if (in_item) {
@@ -217,7 +219,7 @@ void list_scan_kernel(const ListScanArgs a) {
             return false;
           }
           if (p < i_end) {
-            t = (i_r0 >> 6) + (p - i_t);
+            t = i_tb + p;
             p += kScanWaves;
             const int row0 = t * 64;
             mask = bit_range(max(i_r0 - row0, 0), min(i_r1 - row0, 64));
@@ -229,20 +231,23 @@ void list_scan_kernel(const ListScanArgs a) {
           batch += 64;
           if (batch >= stop_at) return false;
           // Every lane loads (lanes past the end reload the batch's first
-          // item) and every loaded value is used before the ballot, so the
-          // loads complete here and not at a later wait that would also hold
-          // the tile loads issued meanwhile.
+          // item) and uses what it loaded before the ballot.
           const int it = batch + lane;
           const int itc = it < stop_at ? it : batch;
-          v_r0 = a.it_r0[ib + itc];
-          v_r1 = a.it_r1[ib + itc];
-          v_t = a.it_t[ib + itc];
-          v_lb = a.it_lb[ib + itc];
+          const int v_r0 = a.it_r0[ib + itc];
+          const int v_r1 = a.it_r1[ib + itc];
+          const int v_t = a.it_t[ib + itc];
+          const float v_lb = a.it_lb[ib + itc];
           const int nt = ((v_r1 - 1) >> 6) - (v_r0 >> 6) + 1;
           const int from = max(v_t, p_begin);
           const int first = from + ((wave - from) & (kScanWaves - 1));   // this wavefront's first position
-          const bool gone = it < stop_at && (pruned(v_lb) || v_t >= p_end);
-          bool ok = it < stop_at && first < min(v_t + nt, p_end) && !gone;
+          const int end = min(v_t + nt, p_end);
+          const float lbv = v_lb > 0.0f ? __fsub_rn(__fmul_rn(__fmul_rn(v_lb, v_lb), a.keep), a.abs_m)
+                                        : -__builtin_inff();
+          const bool gone = it < stop_at && (lbv > cut || v_t >= p_end);
+          bool ok = it < stop_at && first < end && !gone;
+          my_items[lane] = make_int4(v_r0, v_r1, first, end);
+          my_items2[lane] = make_int2((v_r0 >> 6) - v_t, __float_as_int(lbv));
           const uint64_t gm = __ballot(gone);
           if (gm != 0) {
             // the first prunable item, or the first past the job, ends it
@@ -255,15 +260,14 @@ void list_scan_kernel(const ListScanArgs a) {
         }
         const int j = __builtin_ctzll(pend);
         pend &= pend - 1;
-        i_r0 = __builtin_amdgcn_readlane(v_r0, j);
-        i_r1 = __builtin_amdgcn_readlane(v_r1, j);
-        i_t = __builtin_amdgcn_readlane(v_t, j);
-        const float i_lb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v_lb), j));
-        i_lbv = i_lb > 0.0f ? __fsub_rn(__fmul_rn(__fmul_rn(i_lb, i_lb), a.keep), a.abs_m) : -__builtin_inff();
-        const int i_nt = ((i_r1 - 1) >> 6) - (i_r0 >> 6) + 1;
-        const int from = max(i_t, p_begin);
-        p = from + ((wave - from) & (kScanWaves - 1));
-        i_end = min(i_t + i_nt, p_end);
+        const int4 x = my_items[j];
+        const int2 y = my_items2[j];
+        i_r0 = __builtin_amdgcn_readfirstlane(x.x);
+        i_r1 = __builtin_amdgcn_readfirstlane(x.y);
+        p = __builtin_amdgcn_readfirstlane(x.z);
+        i_end = __builtin_amdgcn_readfirstlane(x.w);
+        i_tb = __builtin_amdgcn_readfirstlane(y.x);
+        i_lbv = __int_as_float(__builtin_amdgcn_readfirstlane(y.y));
         in_item = true;
       }
     };
@@ -418,9 +422,11 @@ void list_scan_kernel(const ListScanArgs a) {
       load(hs[i] ? ts[i] : 0, ws[i]);
     }
     for (;;) {
-      gview = gnext;
-      gnext = __hip_atomic_load(a.gthr + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      refresh();
+      // The query's shared threshold is loaded at the top of a round and
+      // read at its end, when the tile loads issued after it have been waited
+      // for anyway (read at the next round's top, its wait also held back
+      // the round's first tile loads).
+      const uint64_t gload = __hip_atomic_load(a.gthr + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
       for (int i = 0; i < kDepth; ++i) {
         const int j = (i + kDepth - 1) % kDepth;
@@ -429,6 +435,8 @@ void list_scan_kernel(const ListScanArgs a) {
         if (!hs[i]) goto scanned;
         sum_tile(ts[i], ms[i], ws[i]);
       }
+      gview = gload;
+      refresh();
     }
   scanned:
     pool_compact(pool, cnt, thr, k, a.kpl, a.ids);
@@ -462,9 +470,10 @@ const void* pick_list(int m, int lut_dtype, bool count) {
 }
 
 size_t list_dyn_bytes(int pool_stride) {
-  // pools, the workgroup threshold, monotonicity flags, the counting build's
-  // histogram
-  return static_cast<size_t>(kScanWaves) * pool_stride * sizeof(uint64_t) + 8 + 4 * kScanWaves + kLookupHistBytes;
+  // item rows, pools, the workgroup threshold, monotonicity flags, the
+  // counting build's histogram
+  return static_cast<size_t>(kScanWaves) * 64 * (sizeof(int4) + sizeof(int2)) +
+         static_cast<size_t>(kScanWaves) * pool_stride * sizeof(uint64_t) + 8 + 4 * kScanWaves + kLookupHistBytes;
 }
 
 }  // namespace
