@@ -299,9 +299,11 @@ ifvs_status ifvs_lut_bounds(ifvs_index* idx, int32_t nq, const float* alpha, con
  * bit, whenever alpha and wf are the tables' operands; others can drop true
  * neighbours.  The list scan runs once ifvs_build_coarse has run, when every
  * query's selection is a run of rows of the index's layout (no clause
- * tested row by row), M is 16, 48 or 120, and its workspace holds the batch
+ * tested row by row), M is 16, 48 or 120, nq is at most 16384 and its
+ * workspace holds the batch
  * (IFVS_OPT_COARSE: automatic for batches whose widest interval spans 8192
- * or more 64-row tiles); otherwise the call is ifvs_filtered_search.  The
+ * or more 64-row tiles, on indexes of 32 or more subspaces); otherwise the
+ * call is ifvs_filtered_search.  The
  * list scan adds the bound kernels, one planning kernel per call (one
  * workgroup per query orders the query's groups by their bound) and a job
  * table kernel; the scan's workgroups take chunks of the queries' work from
@@ -531,7 +533,7 @@ ifvs_status ifvs_encode_predicates(ifvs_index* idx, int32_t nq, const ifvs_predi
                                      exactly, 2 always screen first                           */
 #define IFVS_OPT_COARSE 13       /* ifvs_filtered_search_bounded: 0 automatic (the list scan for
                                      batches whose widest interval spans 8192 or more 64-row
-                                     tiles), 1 never, 2 whenever the batch allows it          */
+                                     tiles, M >= 32), 1 never, 2 whenever the batch allows it  */
 #define IFVS_OPT_COUNT_READS 12  /* measurement only: 1 = scans run a build of the scan kernel
                                      that also counts its table reads (one per subspace and
                                      wavefront instruction, and one per coarse-bound lookup)
@@ -558,7 +560,7 @@ ifvs_status ifvs_read_profile(ifvs_index* idx, double* ms_out, int64_t* launches
  * active (a read is one LDS instruction of a wavefront; it fetches n table
  * entries), for n = 1..64, hist_out[0] = the 64-row code tiles the scans
  * summed and hist_out[65] = the tiles the list scan read past their first
- * two groups of subspaces (it fetches those code words only for tiles with
+ * three groups of subspaces (it fetches those code words only for tiles with
  * a row still live), all summed over the scans since the last call, which
  * it then clears.
  * Waits for `stream`.  The LDS cost of the Rank stage's distance-table

@@ -58,8 +58,13 @@ constexpr int kStagingSlots = 8;
 // Automatic list scan: batches whose widest interval spans at least this
 // many 64-row tiles (measured on 10M x 48-byte codes, 256 queries: at 10%
 // selectivity, 15.6K tiles, the list scan and its plan take 0.74 ms against
-// the interval scan's 1.16; at 1%, 1.6K tiles, 1.2 ms against 0.25).
+// the interval scan's 1.16; at 1%, 1.6K tiles, 1.2 ms against 0.25), on
+// indexes of at least kCoarseAutoM subspaces (on 100M x 16-byte codes, whose
+// bounds prune little and whose one-kilobyte tiles leave the list scan's
+// per-tile work in front, it ran 1.6x the interval scan's time at 1% and
+// 1.26x at 10%).
 constexpr int64_t kCoarseAutoTiles = 8192;
+constexpr int kCoarseAutoM = 32;
 // Radius quantiles that split each coarse list into its kBands bands.
 constexpr float kBandQuantiles[kBands - 1] = {0.5f, 0.85f, 0.97f};
 
@@ -1218,7 +1223,7 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
       list_scan_lds_bytes(idx->m, lut_dtype, pool_stride_for(k)) <= size_t{kLdsBudget} &&
       list_jobs_lds_bytes(nq) <= size_t{kLdsBudget} &&
       static_cast<size_t>(nq) * list_splits * kScanWaves * k <= ws.partial_keys &&
-      (idx->opt_coarse == 2 || span >= kCoarseAutoTiles);
+      (idx->opt_coarse == 2 || (span >= kCoarseAutoTiles && idx->m >= kCoarseAutoM));
   if (idx->opt_count_reads && !list_mode &&
       (!scan_can_count(idx->m, plan.qtile, lut_dtype) || plan.lds_bytes + kLookupHistBytes > size_t{kLdsBudget}))
     return fail(IFVS_E_UNSUPPORTED, "IFVS_OPT_COUNT_READS: no read-counting scan for this plan (it needs one query "
