@@ -7,8 +7,9 @@ whole query sets one by one, in a pool of host processes, for an
 element-by-element comparison of ids and distance bits:
 
 * 10M x 96 (c4), in the launch configuration the benchmark times (clustered
-  rows, conditioned mode, batches of 256, k = 10, fp32 tables): all 256
-  queries of a batch in each of the four bins;
+  rows, conditioned mode, batches of 256, k = 10, fp32 tables, coarse
+  quantizer of 2048 centroids: the list scan in the 10% and 50% bins): all
+  256 queries of a batch in each of the four bins;
 * 1M x 128 with a range and a category clause (c2): 64 queries per bin;
 * 1M x 960 with k = 100 (c3): 32 queries per bin, and 8 more in the fp16
   table mode;
@@ -66,10 +67,12 @@ def _workers():
     return max(1, min(15, host_cores() - 1))
 
 
-def _run_config(B, w, idx, plain, bins, nq, k, per_bin, conditioned=True, lut_dtype="f32"):
+def _run_config(B, w, idx, plain, bins, nq, k, per_bin, conditioned=True, lut_dtype="f32", list_bins=()):
     """Searches the first nq queries of every bin on the GPU, checks the
     properties of every row, and compares the first per_bin[s] queries of
-    bin s with the oracle."""
+    bin s with the oracle.  With a coarse build on idx, the bounded search
+    runs too (it must take the list scan in list_bins) and must return the
+    same ids and distance bits."""
     dt = B.LUT_F16 if lut_dtype == "f16" else B.LUT_F32
     tasks, got = [], {}
     for s in bins:
@@ -82,6 +85,11 @@ def _run_config(B, w, idx, plain, bins, nq, k, per_bin, conditioned=True, lut_dt
         _, counts = idx.filter(preds)
         torch.cuda.synchronize()
         _properties(w, preds, ids, dist, counts, k)
+        if list_bins:
+            ib, db = idx.search_bounded(preds, lut, a if conditioned else None, f, k, dt)
+            torch.cuda.synchronize()
+            assert idx.last_coarse() == (s in list_bins), (s, idx.last_coarse())
+            assert torch.equal(ids, ib) and torch.equal(dist.view(torch.int32), db.view(torch.int32)), s
         if plain is not None:
             i2, d2 = plain.search(preds, lut, k, dt)
             torch.cuda.synchronize()
@@ -114,7 +122,11 @@ def test_c4_10m_bench_configuration(B):
     w = make_workload("c4", device="cuda", n_queries=256, keep_x=False)
     clus = B.Index.from_workload(w, max_batch=256, max_k=10, cluster_cols=(0,))
     plain = B.Index.from_workload(w, max_batch=256, max_k=10)
-    n = _run_config(B, w, clus, plain, w.bins, 256, 10, {s: 256 for s in w.bins})
+    say("[full] c4: coarse quantizer, 2048 centroids")
+    clus.build_coarse(2048, 20)
+    # the bench's path: the list scan with the coarse bound in the 10% and 50%
+    # bins, equal to the interval scan's answers and so to the oracle's
+    n = _run_config(B, w, clus, plain, w.bins, 256, 10, {s: 256 for s in w.bins}, list_bins=(0.1, 0.5))
     assert n == 4 * 256
 
 
