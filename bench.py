@@ -12,10 +12,11 @@ the GPU (the paper's SIFT10M-style workload is not available here).
 100M x 128, and the 10K-vector toy); rows are clustered by the range
 attribute, or by (category, range attribute) where queries carry both.
 
-One step = one batch of queries from each selectivity bin, each batch going
-through encode_predicates -> select_codebook -> build_lut ->
-filtered_search_bounded (the list scan with the coarse bound where the
-planner takes it: the 10% and 50% bins on c4; the interval scan elsewhere).  `value` is queries
+One step = one batch of queries from each selectivity bin, each batch one
+ifvs_query_batch call: encoder -> condition -> distance tables -> bounded
+search (the list scan with the coarse bound where the planner takes it: the
+10% and 50% bins on c4; the interval scan elsewhere).  `--separate-calls`
+runs the four stages as four calls instead.  `value` is queries
 per second over the timed steps, inputs resident in HBM.  In the timed
 region only the scan kernel (the roofline kernel) and each bin's run of
 batches are bracketed by HIP events; the per-stage breakdown and the
@@ -358,6 +359,9 @@ def main():
                     help="batches per bin timed with queries and weights uploaded from pinned host memory "
                          "and results downloaded inside each batch (the PCIe-inclusive rate; 0 = skip)")
     ap.add_argument("--lut", choices=["f32", "f16"], default="f32")
+    ap.add_argument("--separate-calls", action="store_true",
+                    help="run each batch as four calls (encoder, condition, tables, search) instead of "
+                         "ifvs_query_batch; same results, each call stages the predicates again")
     ap.add_argument("--coarse", type=int, default=None,
                     help="coarse centroids of the list scan (ifvs_build_coarse; 0 = plain interval scan only; "
                          "default 2048 when D <= 128)")
@@ -449,6 +453,11 @@ def main():
     def run_batch(idx, s, b):
         sl = slice(b * batch, (b + 1) * batch)
         q = w.queries[sl]
+        if not args.separate_calls:
+            # one call: encoder, condition, tables and the search (the list
+            # scan with the coarse bound where the planner picks it)
+            idx.query_batch_into(q, packed[s][b], None, wz, alpha, wf, lut_dt, lut, k, ids[s], dist[s])
+            return
         idx.encode_predicates_into(batch, packed[s][b], wz)
         idx.select_codebook_into(q, packed[s][b], wz, alpha, wf)
         idx.build_lut_into(q, alpha, wf, lut_dt, lut)
@@ -643,7 +652,9 @@ def main():
         roof_bound, achieved, peak = "lds", lds_achieved, lds_peak
     else:
         roof_bound, achieved, peak = "hbm", hbm_achieved, HBM_PEAK_GBPS
-    bytes_word = ("code tiles each query sums, counted per query" if dom == "list_scan_kernel"
+    bytes_word = ("code tiles each query sums, counted per query"
+                  if dom == "list_scan_kernel" and all(s in read_hist for s in dom_bins)
+                  else "the queries' interval tiles, from HBM at least" if dom == "list_scan_kernel"
                   else "from HBM at least")
     log(f"[bench] {dom} (bins {dom_bins}): {scan_launches} launches, avg {scan_avg_ms:.3f} ms, "
         f"{union_per_launch / 1e6:.1f} MB/launch ({bytes_word}) -> {hbm_achieved:.0f} GB/s; "
@@ -951,6 +962,8 @@ def main():
         "config": {"workload": f"{name}: {DESCRIPTIONS[name]}", "batch": batch, "k": k,
                    "coarse_centroids": args.coarse, "coarse_build_s": coarse_build_s,
                    "bins": bins, "mode": "conditioned (predicate encoder -> w_z, memory bank, W)",
+                   "calls_per_batch": ("4 (encode_predicates, select_codebook, build_lut, filtered_search_bounded)"
+                                       if args.separate_calls else "1 (ifvs_query_batch)"),
                    "layout": ("rows clustered by the range attribute" if cols == (0,)
                               else "rows clustered by (category, range attribute)"),
                    "queries_per_step": len(bins) * batch,

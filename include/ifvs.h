@@ -316,6 +316,30 @@ ifvs_status ifvs_filtered_search_bounded(ifvs_index* idx, int32_t nq, const ifvs
                                          int32_t k, int32_t* ids_out, float* dist_out, uint32_t* bitmap_out,
                                          void* stream);
 
+/* ifvs_query_batch -- the whole path of Section 2 for a batch in one call:
+ * the predicate encoder (f -> w_z, when w_z is NULL), the condition (alpha,
+ * w_f), the distance tables, then ifvs_filtered_search_bounded with those
+ * tables and their operands.  Same outputs, bit for bit, as
+ * ifvs_encode_predicates + ifvs_select_codebook + ifvs_build_lut +
+ * ifvs_filtered_search_bounded on the same arguments; the predicates are
+ * validated and staged once for all four (each separate call stages them
+ * and marks its staging with an event, a few microseconds of the stream's
+ * time each).
+ *  q: device [nq][dim];  preds: HOST [nq]
+ *  w_z: device [nq][dim], or NULL to encode the predicates with the attached
+ *       encoder into wz_out (device [nq][dim], caller-owned; unused when w_z
+ *       is given)
+ *  alpha_out: device [nq][m*r] (may be NULL on an index without a bank);
+ *  wf_out: device [nq][dim];  lut_out: device [nq][m][256] of lut_dtype,
+ *  16-byte aligned;  ids_out, dist_out: device [nq][k] -- all caller-owned,
+ *  written in stream order.
+ * Errors: IFVS_E_INVALID (nq, k, NULL arrays, predicate errors, unknown
+ * dtype), IFVS_E_STATE (NULL handle; w_z NULL with no encoder attached),
+ * IFVS_E_UNSUPPORTED, IFVS_E_HIP. */
+ifvs_status ifvs_query_batch(ifvs_index* idx, int32_t nq, const float* q, const ifvs_predicate* preds,
+                             const float* w_z, float* wz_out, float* alpha_out, float* wf_out, int32_t lut_dtype,
+                             void* lut_out, int32_t k, int32_t* ids_out, float* dist_out, void* stream);
+
 /* ifvs_read_coarse -- the coarse quantizer, for inspection and tests
  * (synchronous; every output may be NULL): *n_centroids_out; assign_out
  * HOST [n] centroid of each vector id; radius_out HOST [n] its stored

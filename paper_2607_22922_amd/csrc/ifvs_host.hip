@@ -1169,7 +1169,7 @@ namespace {
 ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds, const void* lut,
                         int32_t lut_dtype, bool bounded, const float* alpha, const float* wf, int32_t k,
                         int32_t* ids_out, float* dist_out, uint32_t* bitmap_out, void* stream,
-                        bool static_scratch) {
+                        bool static_scratch, int pre_slot = -1, DevPred* pre_host = nullptr) {
   if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
   if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
   if (lut_dtype != IFVS_LUT_F32 && lut_dtype != IFVS_LUT_F16) return fail(IFVS_E_INVALID, "unknown lut_dtype");
@@ -1185,8 +1185,14 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
   DevPred* host = nullptr;
   int slot = 0;
-  // Predicates are validated before anything is enqueued.
-  if (ifvs_status st = stage_predicates(idx, nq, preds, true, false, s, &slot, &host); st != IFVS_OK) return st;
+  // Predicates are validated before anything is enqueued (or were, with the
+  // scan order, by a caller that staged them for earlier kernels too).
+  if (pre_slot >= 0) {
+    slot = pre_slot;
+    host = pre_host;
+  } else if (ifvs_status st = stage_predicates(idx, nq, preds, true, false, s, &slot, &host); st != IFVS_OK) {
+    return st;
+  }
   bool need_bitmap = false, interval_batch = true;
   int64_t span = 0;
   for (int i = 0; i < nq; ++i) {
@@ -1438,6 +1444,68 @@ ifvs_status ifvs_filtered_search_bounded(ifvs_index* idx, int32_t nq, const ifvs
                                          void* stream) {
   return search_impl(idx, nq, preds, lut, lut_dtype, true, alpha, wf, k, ids_out, dist_out, bitmap_out, stream,
                      false);
+}
+
+ifvs_status ifvs_query_batch(ifvs_index* idx, int32_t nq, const float* q, const ifvs_predicate* preds,
+                             const float* w_z, float* wz_out, float* alpha_out, float* wf_out, int32_t lut_dtype,
+                             void* lut_out, int32_t k, int32_t* ids_out, float* dist_out, void* stream) {
+  if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
+  if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
+  if (lut_dtype != IFVS_LUT_F32 && lut_dtype != IFVS_LUT_F16) return fail(IFVS_E_INVALID, "unknown lut_dtype");
+  if (k < 1 || k > idx->max_k)
+    return fail(IFVS_E_INVALID, "k = " + std::to_string(k) + " outside 1.." + std::to_string(idx->max_k) + " (max_k)");
+  if (nq == 0) return IFVS_OK;
+  if (!q || !wf_out || !lut_out || !ids_out || !dist_out)
+    return fail(IFVS_E_INVALID, "q, wf_out, lut_out, ids_out or dist_out is NULL");
+  if (idx->bank_rows > 0 && !alpha_out) return fail(IFVS_E_INVALID, "alpha_out is NULL but the index has a memory bank");
+  if (!w_z && !idx->enc_params)
+    return fail(IFVS_E_STATE, "w_z is NULL and no encoder is attached (ifvs_load_encoder)");
+  if (!w_z && !wz_out) return fail(IFVS_E_INVALID, "w_z and wz_out are both NULL");
+  if (reinterpret_cast<uintptr_t>(lut_out) % 16 != 0) return fail(IFVS_E_INVALID, "lut must be 16-byte aligned");
+  ScanPlan probe{};
+  if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, false, 0, size_t{1} << 40, &probe); st != IFVS_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
+  // One staging of the predicates (validated, with the scan order) for the
+  // encoder, the condition and the search kernels.
+  DevPred* host = nullptr;
+  int slot = 0;
+  if (ifvs_status st = stage_predicates(idx, nq, preds, true, false, s, &slot, &host); st != IFVS_OK) return st;
+  // (a failed launch still releases the slot: kernels enqueued before it
+  // may read it)
+  auto launch = [&](int stage, const char* what, auto&& fn) -> ifvs_status {
+    const ifvs_status st = timed(idx, stage, s, what, fn);
+    if (st != IFVS_OK) (void)release_slot(idx, slot, s);
+    return st;
+  };
+  const float* wz = w_z;
+  if (!w_z) {
+    if (ifvs_status st = launch(kStEncode, "launching encoder kernel", [&]() -> hipError_t {
+          return launch_encoder(idx->enc_params, idx->enc_off, idx->enc_scale, idx->enc_H, idx->enc_heads,
+                                idx->enc_layers, idx->enc_F, idx->dim, idx->n_attr, idx->staging_dev[slot], nq, wz_out,
+                                s);
+        });
+        st != IFVS_OK)
+      return st;
+    wz = wz_out;
+  }
+  float* alpha = idx->bank_rows > 0 ? alpha_out : nullptr;
+  if (ifvs_status st = launch(kStCondition, "launching condition kernel", [&]() -> hipError_t {
+        return launch_condition(q, idx->dim, idx->staging_dev[slot], nq, idx->bank, idx->bank_rows, idx->m * idx->r,
+                                idx->h, idx->hash_seed, wz, alpha, wf_out, s);
+      });
+      st != IFVS_OK)
+    return st;
+  if (ifvs_status st = launch(kStLut, "launching LUT kernel", [&]() -> hipError_t {
+        return launch_build_lut(q, idx->dim, idx->m, idx->dsub, idx->r, idx->cpq, idx->W, alpha, wf_out, nq,
+                                lut_dtype, lut_out, s);
+      });
+      st != IFVS_OK)
+    return st;
+  const ifvs_status st = search_impl(idx, nq, preds, lut_out, lut_dtype, true, alpha, wf_out, k, ids_out, dist_out,
+                                     nullptr, stream, false, slot, host);
+  if (st != IFVS_OK && !idx->slot_busy[slot]) (void)release_slot(idx, slot, s);   // the earlier kernels read it
+  return st;
 }
 
 ifvs_status ifvs_filtered_search_noalloc(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds,

@@ -39,7 +39,7 @@ EXPORTED = ("ifvs_load_index", "ifvs_free_index", "ifvs_select_codebook", "ifvs_
             "ifvs_filtered_search_noalloc", "ifvs_read_scan_reads", "ifvs_probe_lds_gather",
             "ifvs_encoder_params", "ifvs_load_encoder", "ifvs_encode_predicates",
             "ifvs_build_coarse", "ifvs_lut_bounds", "ifvs_filtered_search_bounded", "ifvs_read_coarse",
-            "ifvs_last_coarse")
+            "ifvs_last_coarse", "ifvs_query_batch")
 
 
 class IfvsError(RuntimeError):
@@ -130,6 +130,7 @@ def _load_library() -> ctypes.CDLL:
         "ifvs_build_coarse": ([vp, i32, i32], i32),
         "ifvs_lut_bounds": ([vp, i32, vp, vp, vp, vp], i32),
         "ifvs_filtered_search_bounded": ([vp, i32, vp, vp, i32, vp, vp, i32, vp, vp, vp, vp], i32),
+        "ifvs_query_batch": ([vp, i32, vp, vp, vp, vp, vp, vp, i32, vp, i32, vp, vp, vp], i32),
         "ifvs_read_coarse": ([vp, ctypes.POINTER(i32), vp, vp, vp], i32),
         "ifvs_last_coarse": ([vp, ctypes.POINTER(i32)], i32),
     }
@@ -302,6 +303,14 @@ class Index:
         self.search_bounded_into(nq, pack_predicates(preds), lut, lut_dtype, alpha, wf, k, ids, dist)
         return ids, dist
 
+    def query_batch_into(self, q, preds_c, w_z, wz_out, alpha_out, wf_out, lut_dtype, lut_out, k, ids_out,
+                         dist_out, stream=None):
+        """ifvs_query_batch: encoder (when w_z is None), condition, tables
+        and the bounded search in one call."""
+        _check(_lib.ifvs_query_batch(self.handle, q.shape[0], q.data_ptr(), preds_c, _ptr(w_z), _ptr(wz_out),
+                                     _ptr(alpha_out), wf_out.data_ptr(), lut_dtype, lut_out.data_ptr(), k,
+                                     ids_out.data_ptr(), dist_out.data_ptr(), _stream(stream)))
+
     def read_profile(self) -> dict:
         """Per-stage (total kernel ms, launches) since the last read."""
         ms = (ctypes.c_double * len(STAGES))()
@@ -432,6 +441,23 @@ class Index:
         wf = torch.empty(nq, self.dim, device=self.device)
         self.select_codebook_into(q, pack_predicates(preds), w_z, alpha, wf)
         return alpha, wf
+
+    def query_batch(self, q, preds, k, w_z=None, lut_dtype=LUT_F32):
+        """Returns (ids, dist, w_z, alpha, w_f, lut); w_z is the encoder's
+        output when none is given, else the argument."""
+        nq = q.shape[0]
+        q = _dev_f32(q, self.device)
+        wz = torch.empty(nq, self.dim, device=self.device) if w_z is None else _dev_f32(w_z, self.device)
+        alpha = (torch.empty(nq, self.m * self.r, device=self.device)
+                 if self.bank_rows > 0 else None)
+        wf = torch.empty(nq, self.dim, device=self.device)
+        dt = torch.float16 if lut_dtype == LUT_F16 else torch.float32
+        lut = torch.empty(nq, self.m, KSUB, device=self.device, dtype=dt)
+        ids = torch.empty(nq, k, device=self.device, dtype=torch.int32)
+        dist = torch.empty(nq, k, device=self.device, dtype=torch.float32)
+        self.query_batch_into(q, pack_predicates(preds), None if w_z is None else wz,
+                              wz if w_z is None else None, alpha, wf, lut_dtype, lut, k, ids, dist)
+        return ids, dist, wz, alpha, wf, lut
 
     def build_lut(self, q, alpha=None, wf=None, lut_dtype=LUT_F32):
         nq = q.shape[0]

@@ -141,6 +141,8 @@ int main() {
   expect("filtered_search_bounded",
          ifvs_filtered_search_bounded(nullptr, 1, &pred, f, 0, nullptr, nullptr, 1, i32, f, nullptr, nullptr),
          IFVS_E_STATE);
+  expect("query_batch",
+         ifvs_query_batch(nullptr, 1, f, &pred, f, nullptr, f, f, 0, f, 1, i32, f, nullptr), IFVS_E_STATE);
   expect("read_coarse", ifvs_read_coarse(nullptr, i32, nullptr, nullptr, u8), IFVS_E_STATE);
   expect("last_coarse", ifvs_last_coarse(nullptr, i32), IFVS_E_STATE);
   expect("load_vectors", ifvs_load_vectors(nullptr, f, IFVS_MEM_HOST), IFVS_E_STATE);

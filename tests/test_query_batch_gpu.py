@@ -1,0 +1,127 @@
+"""ifvs_query_batch, the whole path of Section 2 in one call (encoder,
+condition, tables, bounded search), against the same stages called one by
+one: every output (w_z, alpha, w_f, the tables, ids, distance bits) equal
+bit for bit, with and without a given w_z, fp32 and binary16 tables, list
+scan forced on; then a sample of rows against the oracle, and the error
+paths (each leaves the index usable)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from workload import random_encoder, random_index
+from tests._gpu_util import check_search_row, oracle_index, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_2607_22922_amd import ifvs
+    return ifvs
+
+
+@pytest.fixture(scope="module")
+def case(B):
+    """40K rows, M = 48 subspaces of 2 dims, a bank of 97 rows, clustered by
+    the first of two attributes, a 64-centroid coarse build and an encoder."""
+    say("[query_batch] index N=40000 M=48")
+    M, dsub = 48, 2
+    ix = random_index(40_000, M, dsub, 2, 1000, seed=17, device="cuda", bank_rows=97)
+    idx = B.Index(ix["codes"], ix["C_pq"], ix["attrs"], ix["bank"], ix["W"], ix["r"], ix["h"], ix["hash_seed"],
+                  max_batch=64, max_k=32, cluster_cols=(0,))
+    idx.load_encoder(random_encoder(2, M * dsub, [1000, 1000], seed=4))
+    idx.build_coarse(64, 5)
+    g = torch.Generator(device="cpu").manual_seed(8)
+    nq = 40
+    q = torch.randn(nq, M * dsub, generator=g).cuda()
+    preds = []
+    for i in range(nq):
+        lo = int(torch.randint(0, 900, (1,), generator=g))
+        w = [0, 1, 30, 100, 500, 1000][i % 6]
+        preds.append([(0, lo, lo + w)] + ([(1, 100, 700)] if i % 7 == 3 else []))
+    return ix, idx, q, preds
+
+
+def _bits(t):
+    return t.contiguous().view(torch.int32) if t.dtype == torch.float32 else t.contiguous().view(torch.int16)
+
+
+def _stagewise(idx, q, preds, k, w_z, lut_dtype):
+    wz = idx.encode_predicates(preds) if w_z is None else w_z
+    alpha, wf = idx.select_codebook(q, preds, wz)
+    lut = idx.build_lut(q, alpha, wf, lut_dtype)
+    ids, dist = idx.search_bounded(preds, lut, alpha, wf, k, lut_dtype)
+    return ids, dist, wz, alpha, wf, lut
+
+
+@pytest.mark.parametrize("given_wz", [False, True])
+@pytest.mark.parametrize("lut_dtype", [0, 1])
+@pytest.mark.parametrize("mode", [0, 2])
+def test_same_bits_as_the_separate_calls(B, case, given_wz, lut_dtype, mode):
+    ix, idx, q, preds = case
+    say(f"[query_batch] given_wz={given_wz} lut_dtype={lut_dtype} coarse_mode={mode}")
+    k = 20
+    w_z = None
+    if given_wz:
+        w_z = torch.rand(q.shape[0], q.shape[1], device="cuda", generator=torch.Generator(device="cuda")
+                         .manual_seed(3)) * 0.5 + 0.25
+    # residual clauses take the batch off the list scan: drop them in forced mode
+    p = [c[:1] for c in preds] if mode == 2 else preds
+    idx.set_option(B.OPT_COARSE, mode)
+    try:
+        ref = _stagewise(idx, q, p, k, w_z, lut_dtype)
+        used_ref = idx.last_coarse()
+        got = idx.query_batch(q, p, k, w_z=w_z, lut_dtype=lut_dtype)
+        used = idx.last_coarse()
+    finally:
+        idx.set_option(B.OPT_COARSE, 0)
+    torch.cuda.synchronize()
+    assert used == used_ref and used == (mode == 2)
+    for name, a, b in zip(("ids", "dist", "w_z", "alpha", "w_f", "lut"), got, ref):
+        assert a.shape == b.shape, name
+        assert torch.equal(_bits(a) if a.is_floating_point() else a, _bits(b) if b.is_floating_point() else b), name
+
+
+def test_rows_against_the_oracle(B, case):
+    ix, idx, q, preds = case
+    say("[query_batch] oracle rows")
+    k = 10
+    p = [c[:1] for c in preds]
+    idx.set_option(B.OPT_COARSE, 2)
+    try:
+        ids, dist, wz, *_ = idx.query_batch(q, p, k)
+        assert idx.last_coarse()
+    finally:
+        idx.set_option(B.OPT_COARSE, 0)
+    torch.cuda.synchronize()
+    ox = oracle_index(ix["codes"], ix["C_pq"], ix["attrs"], ix["bank"], ix["W"], ix["r"], ix["h"], ix["hash_seed"])
+    ids, dist, wz_h, q_h = ids.cpu().numpy(), dist.cpu().numpy(), wz.cpu().numpy(), q.cpu().numpy()
+    for i in range(0, len(p), 5):
+        res = O.filtered_search(ox, q_h[i], p[i], k, w_z=wz_h[i])
+        check_search_row(ids[i], dist[i], res["ids"], res["dist"], f"q{i} {p[i]}")
+
+
+def test_errors_leave_the_index_usable(B, case):
+    ix, idx, q, preds = case
+    say("[query_batch] errors")
+    with pytest.raises(B.IfvsError):
+        idx.query_batch(q, preds, 33)                          # beyond max_k
+    with pytest.raises(B.IfvsError):
+        idx.query_batch(q, preds[:-1] + [[(5, 0, 1)]], 10)     # unknown attribute column
+    q2 = torch.randn(65, q.shape[1], device="cuda")
+    with pytest.raises(B.IfvsError):
+        idx.query_batch(q2, [[]] * 65, 10)                     # beyond max_batch
+    bare = B.Index(ix["codes"], ix["C_pq"], ix["attrs"], ix["bank"], ix["W"], ix["r"], ix["h"], ix["hash_seed"],
+                   max_batch=8, max_k=10)
+    with pytest.raises(B.IfvsError) as e:
+        bare.query_batch(q[:2], preds[:2], 5)                  # no encoder, no w_z
+    assert e.value.status == B.E_STATE
+    empty = bare.query_batch(q[:0], [], 5)
+    assert empty[0].shape == (0, 5)
+    # the slots the failed calls staged were released
+    for _ in range(6):
+        ids, dist, *_ = idx.query_batch(q, preds, 10)
+    ref = _stagewise(idx, q, preds, 10, None, 0)
+    torch.cuda.synchronize()
+    assert torch.equal(ids, ref[0]) and torch.equal(_bits(dist), _bits(ref[1]))
