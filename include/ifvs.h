@@ -321,10 +321,13 @@ ifvs_status ifvs_filtered_search_bounded(ifvs_index* idx, int32_t nq, const ifvs
  * w_f), the distance tables, then ifvs_filtered_search_bounded with those
  * tables and their operands.  Same outputs, bit for bit, as
  * ifvs_encode_predicates + ifvs_select_codebook + ifvs_build_lut +
- * ifvs_filtered_search_bounded on the same arguments; the predicates are
- * validated and staged once for all four (each separate call stages them
- * and marks its staging with an event, a few microseconds of the stream's
- * time each).
+ * ifvs_filtered_search_bounded on the same arguments, in fewer launches:
+ * the predicates are validated and staged once for all four (each separate
+ * call stages them and marks its staging with an event, a few microseconds
+ * of the stream's time each); when the encoder runs, its launch also
+ * conditions the queries (indexes without a bank, or h of at most 4); and
+ * when the list scan is expected, the table kernel also writes the coarse
+ * bound's factors.
  *  q: device [nq][dim];  preds: HOST [nq]
  *  w_z: device [nq][dim], or NULL to encode the predicates with the attached
  *       encoder into wz_out (device [nq][dim], caller-owned; unused when w_z

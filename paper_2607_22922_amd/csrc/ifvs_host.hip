@@ -1160,6 +1160,37 @@ ifvs_status ifvs_filter(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
 
 namespace {
 
+// Selection shape of a staged batch: a clause tested row by row somewhere,
+// every selection a run of rows of the layout, the widest run in 64-row
+// tiles.
+struct BatchShape {
+  bool need_bitmap = false;
+  bool interval_batch = true;
+  int64_t span = 0;
+};
+
+BatchShape batch_shape(const ifvs_index* idx, int32_t nq, const DevPred* host) {
+  BatchShape b;
+  for (int i = 0; i < nq; ++i) {
+    b.need_bitmap = b.need_bitmap || host[i].residual_mask != 0;
+    // A predicate no row can satisfy has the empty interval on a clustered
+    // index, so it does not take the batch off the interval plan.
+    b.interval_batch = b.interval_batch && (host[i].iv_mode != 0 || (idx->n_cluster > 0 && host[i].n_eff < 0));
+    if (idx->n_cluster > 0) b.span = std::max(b.span, estimate_interval_tiles(idx, host[i]));
+  }
+  return b;
+}
+
+// The list scan's conditions that depend on the index, the tables' type and
+// the batch's selections (the search adds its workspace's): a coarse build,
+// no clause tested row by row, a supported M, and IFVS_OPT_COARSE (forced,
+// or automatic for batches whose widest interval spans kCoarseAutoTiles or
+// more tiles on indexes of kCoarseAutoM or more subspaces).
+bool list_scan_wanted(const ifvs_index* idx, int32_t lut_dtype, const BatchShape& b) {
+  return idx->coarse.words && idx->opt_coarse != 1 && !b.need_bitmap && list_scan_supported(idx->m, lut_dtype) &&
+         (idx->opt_coarse == 2 || (b.span >= kCoarseAutoTiles && idx->m >= kCoarseAutoM));
+}
+
 // Filter, Rank and Select for one batch.  With static_scratch the device
 // workspace is carved from the static array of the index's device instead of
 // the index's own workspace (no gather scan then: every query takes the tiled
@@ -1169,7 +1200,8 @@ namespace {
 ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds, const void* lut,
                         int32_t lut_dtype, bool bounded, const float* alpha, const float* wf, int32_t k,
                         int32_t* ids_out, float* dist_out, uint32_t* bitmap_out, void* stream,
-                        bool static_scratch, int pre_slot = -1, DevPred* pre_host = nullptr) {
+                        bool static_scratch, int pre_slot = -1, DevPred* pre_host = nullptr,
+                        bool parts_ready = false) {
   if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
   if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
   if (lut_dtype != IFVS_LUT_F32 && lut_dtype != IFVS_LUT_F16) return fail(IFVS_E_INVALID, "unknown lut_dtype");
@@ -1193,15 +1225,9 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   } else if (ifvs_status st = stage_predicates(idx, nq, preds, true, false, s, &slot, &host); st != IFVS_OK) {
     return st;
   }
-  bool need_bitmap = false, interval_batch = true;
-  int64_t span = 0;
-  for (int i = 0; i < nq; ++i) {
-    need_bitmap = need_bitmap || host[i].residual_mask != 0;
-    // A predicate no row can satisfy has the empty interval on a clustered
-    // index, so it does not take the batch off the interval plan.
-    interval_batch = interval_batch && (host[i].iv_mode != 0 || (idx->n_cluster > 0 && host[i].n_eff < 0));
-    if (idx->n_cluster > 0) span = std::max(span, estimate_interval_tiles(idx, host[i]));
-  }
+  const BatchShape shape = batch_shape(idx, nq, host);
+  const bool need_bitmap = shape.need_bitmap, interval_batch = shape.interval_batch;
+  const int64_t span = shape.span;
   SearchWs ws;
   if (!static_scratch) {
     ws = index_ws(idx);
@@ -1223,13 +1249,11 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   while (list_jobs > 1 && static_cast<size_t>(nq) * list_jobs * kScanWaves * k > ws.partial_keys) --list_jobs;
   const int list_splits = list_jobs;
   const bool list_mode =
-      bounded && cl.words && idx->opt_coarse != 1 && !static_scratch && !need_bitmap &&
-      list_scan_supported(idx->m, lut_dtype) &&
+      bounded && !static_scratch && list_scan_wanted(idx, lut_dtype, shape) &&
       list_plan_lds_bytes(idx->m, lut_dtype, cl.C) <= size_t{kLdsBudget} &&
       list_scan_lds_bytes(idx->m, lut_dtype, pool_stride_for(k)) <= size_t{kLdsBudget} &&
       list_jobs_lds_bytes(nq) <= size_t{kLdsBudget} &&
-      static_cast<size_t>(nq) * list_splits * kScanWaves * k <= ws.partial_keys &&
-      (idx->opt_coarse == 2 || (span >= kCoarseAutoTiles && idx->m >= kCoarseAutoM));
+      static_cast<size_t>(nq) * list_splits * kScanWaves * k <= ws.partial_keys;
   if (idx->opt_count_reads && !list_mode &&
       (!scan_can_count(idx->m, plan.qtile, lut_dtype) || plan.lds_bytes + kLookupHistBytes > size_t{kLdsBudget}))
     return fail(IFVS_E_UNSUPPORTED, "IFVS_OPT_COUNT_READS: no read-counting scan for this plan (it needs one query "
@@ -1254,8 +1278,11 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
                                ws.slot_order, ordered ? n_order : 0, s));
   if (ifvs_status st = release_slot(idx, slot, s); st != IFVS_OK) return st;
   if (list_mode) {
-    IFVS_LAUNCH(idx, kStCoarse, s, "launching table bound kernel",
-                launch_bound_parts(alpha, wf, idx->cpq, idx->W, nq, idx->m, idx->r, idx->dsub, idx->bound_parts, s));
+    // (the table kernel wrote the bound's factors when the caller says so)
+    if (!parts_ready)
+      IFVS_LAUNCH(idx, kStCoarse, s, "launching table bound kernel",
+                  launch_bound_parts(alpha, wf, idx->cpq, idx->W, nq, idx->m, idx->r, idx->dsub, idx->bound_parts,
+                                     s));
     ListPlanArgs pa{};
     pa.lut = lut;
     pa.m = idx->m;
@@ -1478,32 +1505,54 @@ ifvs_status ifvs_query_batch(ifvs_index* idx, int32_t nq, const float* q, const 
     if (st != IFVS_OK) (void)release_slot(idx, slot, s);
     return st;
   };
+  float* alpha = idx->bank_rows > 0 ? alpha_out : nullptr;
+  // The encoder conditions the queries it encodes in the same launch (alpha
+  // and w_f, the condition kernel's bits) where it can.
+  const bool fused_condition = !w_z && encoder_conditions(idx->h, alpha != nullptr);
   const float* wz = w_z;
   if (!w_z) {
+    EncCondition cond;
+    cond.q = q;
+    cond.bank = idx->bank;
+    cond.bank_rows = idx->bank_rows;
+    cond.mr = idx->m * idx->r;
+    cond.h = idx->h;
+    cond.seed = idx->hash_seed;
+    cond.alpha = alpha;
+    cond.wf = wf_out;
     if (ifvs_status st = launch(kStEncode, "launching encoder kernel", [&]() -> hipError_t {
           return launch_encoder(idx->enc_params, idx->enc_off, idx->enc_scale, idx->enc_H, idx->enc_heads,
                                 idx->enc_layers, idx->enc_F, idx->dim, idx->n_attr, idx->staging_dev[slot], nq, wz_out,
-                                s);
+                                s, fused_condition ? &cond : nullptr);
         });
         st != IFVS_OK)
       return st;
     wz = wz_out;
   }
-  float* alpha = idx->bank_rows > 0 ? alpha_out : nullptr;
-  if (ifvs_status st = launch(kStCondition, "launching condition kernel", [&]() -> hipError_t {
-        return launch_condition(q, idx->dim, idx->staging_dev[slot], nq, idx->bank, idx->bank_rows, idx->m * idx->r,
-                                idx->h, idx->hash_seed, wz, alpha, wf_out, s);
-      });
-      st != IFVS_OK)
-    return st;
+  // When the list scan is likely to run, the table kernel writes the coarse
+  // bound's factors as it forms the conditioned codewords (the search then
+  // skips its own bound kernel; a batch that takes the interval scan after
+  // all just leaves them unread).
+  float* parts = list_scan_wanted(idx, lut_dtype, batch_shape(idx, nq, host)) &&
+                         lut_emits_bound_parts(idx->dsub, idx->r, alpha != nullptr)
+                     ? idx->bound_parts
+                     : nullptr;
+  if (!fused_condition) {
+    if (ifvs_status st = launch(kStCondition, "launching condition kernel", [&]() -> hipError_t {
+          return launch_condition(q, idx->dim, idx->staging_dev[slot], nq, idx->bank, idx->bank_rows,
+                                  idx->m * idx->r, idx->h, idx->hash_seed, wz, alpha, wf_out, s);
+        });
+        st != IFVS_OK)
+      return st;
+  }
   if (ifvs_status st = launch(kStLut, "launching LUT kernel", [&]() -> hipError_t {
         return launch_build_lut(q, idx->dim, idx->m, idx->dsub, idx->r, idx->cpq, idx->W, alpha, wf_out, nq,
-                                lut_dtype, lut_out, s);
+                                lut_dtype, lut_out, s, parts);
       });
       st != IFVS_OK)
     return st;
   const ifvs_status st = search_impl(idx, nq, preds, lut_out, lut_dtype, true, alpha, wf_out, k, ids_out, dist_out,
-                                     nullptr, stream, false, slot, host);
+                                     nullptr, stream, false, slot, host, parts != nullptr);
   if (st != IFVS_OK && !idx->slot_busy[slot]) (void)release_slot(idx, slot, s);   // the earlier kernels read it
   return st;
 }

@@ -148,10 +148,14 @@ hipError_t launch_train_update_bank(float* bank, int mr, const int32_t* rows, in
 // inv[perm[r]] = r.
 hipError_t launch_invert_perm(const int32_t* perm, int64_t n, int32_t* inv, hipStream_t s);
 
+// parts: optional [nq][2][m] coarse-bound factors (launch_bound_parts's
+// output, the same bits), written by the table kernel itself when
+// lut_emits_bound_parts holds for the shape (hipErrorInvalidValue otherwise).
 hipError_t launch_build_lut(const float* q, int dim, int m, int dsub, int r,
                             const float* cpq, const float* W, const float* alpha,
                             const float* wf, int nq, int lut_dtype, void* lut_out,
-                            hipStream_t s);
+                            hipStream_t s, float* parts = nullptr);
+bool lut_emits_bound_parts(int dsub, int r, bool has_alpha);
 
 struct ScanPlan {
   int qtile;        // queries sharing one LDS residency and one pass over the codes
@@ -234,9 +238,24 @@ hipError_t launch_scan(const ScanBatch& b, const ScanPlan& plan, hipStream_t s);
 // Predicate encoder (k_encoder.hip): w_z [nq][D] of the predicates in
 // `preds` (device-readable DevPred records) through the packed parameters
 // (layout in ifvs.h), H <= 128 a multiple of 16, F <= 256 a multiple of 16.
+// With cond, the launch also writes what launch_condition would for the
+// same queries and w_z (bit for bit): w_f = softplus(w_z), and alpha when
+// cond->alpha is set (h hash functions over the bank).
+struct EncCondition {
+  const float* q = nullptr;      // [nq][D] queries (for the fingerprint)
+  const float* bank = nullptr;   // [bank_rows][mr]
+  int bank_rows = 0, mr = 0, h = 0;
+  uint64_t seed = 0;
+  float* alpha = nullptr;        // [nq][mr], or null: w_f only
+  float* wf = nullptr;           // [nq][D]
+};
 size_t encoder_lds_bytes(int H, int F);
+// Whether the encoder can condition in-launch: any index without a bank,
+// else h of at most 4.
+bool encoder_conditions(int h, bool has_bank);
 hipError_t launch_encoder(const float* params, const double* off, const double* scale, int H, int heads, int layers,
-                          int F, int D, int n_attr, const DevPred* preds, int nq, float* wz, hipStream_t s);
+                          int F, int D, int n_attr, const DevPred* preds, int nq, float* wz, hipStream_t s,
+                          const EncCondition* cond = nullptr);
 
 // Whether a read-counting build of the scan exists for this plan (one query
 // per tile, M of 16, 48 or 120).

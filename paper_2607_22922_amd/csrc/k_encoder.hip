@@ -19,8 +19,16 @@
 // loads in flight, so a projection waits for memory once or twice rather
 // than once per 16-deep step; layer norms, the per-head softmax and the
 // final H x D map run on the vector ALU.
+//
+// Optionally the launch also conditions the queries it encodes (the
+// condition kernel's work, the same bits): w_f = softplus(w_z) as w_z is
+// written, and alpha from extra workgroups after the encoder's, a wavefront
+// per query (fingerprint, bank-row hashes, sum).  The fingerprint is a
+// sequential chain of several microseconds per query; on CUs of their own
+// these workgroups run beside the encoder's instead of lengthening them.
 #include <cmath>
 
+#include "condition_device.h"
 #include "ifvs_internal.h"
 
 namespace ifvs {
@@ -36,6 +44,7 @@ constexpr int kPad = 4;                        // LDS row padding (floats): spre
 constexpr int kWbuf = 9216;                    // floats of the weight staging buffer: 8192 + padding (36 KB)
 constexpr int kEncMaxHeads = 16;
 constexpr int kEncVec = 9 * 128 + 256;          // a layer's gains and biases at the largest H and F
+constexpr int kEncCondMaxH = 4;                // hash functions the in-launch condition handles
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
@@ -47,7 +56,28 @@ struct EncArgs {
   const DevPred* preds;    // [nq] (pinned staging slot)
   int nq;
   float* wz;               // [nq][D]
+  EncCondition cond;       // the in-launch condition (cond.wf null: none)
+  int enc_blocks;          // workgroups of the encoder; those after them compute alpha
 };
+
+// alpha of query qi (one wavefront), as the condition kernel computes it.
+__device__ void condition_alpha(const EncArgs& a, int qi, int lane) {
+  const EncCondition& cd = a.cond;
+  constexpr int kPredWords = static_cast<int>(sizeof(DevPred) / 4);
+  const uint32_t pw = lane < kPredWords ? reinterpret_cast<const uint32_t*>(a.preds + qi)[lane] : 0u;
+  uint32_t lo, hi;
+  fingerprint_query(cd.q + static_cast<size_t>(qi) * a.D, a.D, lo, hi);
+  const uint64_t key = fingerprint_key(lo, hi, pw);
+  const uint32_t row = hashed_bank_row(key, cd.seed, lane, cd.h, cd.bank_rows);
+  float* arow = cd.alpha + static_cast<size_t>(qi) * cd.mr;
+  switch (cd.h) {
+    case 1: gather_alpha<1>(cd.bank, row, cd.mr, lane, arow); break;
+    case 2: gather_alpha<2>(cd.bank, row, cd.mr, lane, arow); break;
+    case 3: gather_alpha<3>(cd.bank, row, cd.mr, lane, arow); break;
+    case 4: gather_alpha<4>(cd.bank, row, cd.mr, lane, arow); break;
+    default: break;
+  }
+}
 
 // Weight chunks.  A matrix W [K][N] (row-major, rows 16-byte aligned) goes
 // through the LDS buffer in chunks of chunk_cols(K, N) columns, at most 8192
@@ -262,6 +292,12 @@ __global__ __launch_bounds__(kEncThreads) void encoder_kernel(const EncArgs a) {
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
+  if (static_cast<int>(blockIdx.x) >= a.enc_blocks) {
+    // a condition workgroup: no barrier below, the whole group leaves here
+    const int qi = (static_cast<int>(blockIdx.x) - a.enc_blocks) * kEncWaves + __builtin_amdgcn_readfirstlane(wave);
+    if (qi < a.nq) condition_alpha(a, qi, lane);
+    return;
+  }
   const int q0 = blockIdx.x * kEncQ;
   const float* col_embed = a.p;
   const float* feat_w = col_embed + static_cast<size_t>(a.n_attr) * H;
@@ -425,7 +461,11 @@ __global__ __launch_bounds__(kEncThreads) void encoder_kernel(const EncArgs a) {
 #pragma unroll
       for (int qi = 0; qi < kEncQ; ++qi) acc[qi] += Z[qi * ldh + h] * w;
     }
-    for (int qi = 0; qi < nv; ++qi) a.wz[static_cast<size_t>(q0 + qi) * a.D + d] = acc[qi] + out_b[d];
+    for (int qi = 0; qi < nv; ++qi) {
+      const float wz = acc[qi] + out_b[d];
+      a.wz[static_cast<size_t>(q0 + qi) * a.D + d] = wz;
+      if (a.cond.wf) a.cond.wf[static_cast<size_t>(q0 + qi) * a.D + d] = softplus_weight(wz);
+    }
   }
 }
 
@@ -438,9 +478,15 @@ size_t encoder_lds_bytes(int H, int F) {
          (2 * kEncRows + kEncQ) * sizeof(int);
 }
 
+bool encoder_conditions(int h, bool has_bank) { return !has_bank || (h >= 1 && h <= kEncCondMaxH); }
+
 hipError_t launch_encoder(const float* params, const double* off, const double* scale, int H, int heads, int layers,
-                          int F, int D, int n_attr, const DevPred* preds, int nq, float* wz, hipStream_t s) {
+                          int F, int D, int n_attr, const DevPred* preds, int nq, float* wz, hipStream_t s,
+                          const EncCondition* cond) {
   if (nq <= 0) return hipSuccess;
+  if (cond && (!cond->wf || !encoder_conditions(cond->h, cond->alpha != nullptr) ||
+               (cond->alpha && (!cond->q || !cond->bank || cond->bank_rows <= 0))))
+    return hipErrorInvalidValue;
   EncArgs a{};
   a.p = params;
   a.off = off;
@@ -454,11 +500,14 @@ hipError_t launch_encoder(const float* params, const double* off, const double* 
   a.preds = preds;
   a.nq = nq;
   a.wz = wz;
+  if (cond) a.cond = *cond;
+  a.enc_blocks = (nq + kEncQ - 1) / kEncQ;
+  const int cond_blocks = cond && cond->alpha ? (nq + kEncWaves - 1) / kEncWaves : 0;
   const size_t lds = encoder_lds_bytes(H, F);
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&encoder_kernel),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(encoder_kernel, dim3((nq + kEncQ - 1) / kEncQ), dim3(kEncThreads), lds, s, a);
+  hipLaunchKernelGGL(encoder_kernel, dim3(a.enc_blocks + cond_blocks), dim3(kEncThreads), lds, s, a);
   return hipGetLastError();
 }
 

@@ -2,7 +2,9 @@
 condition, tables, bounded search), against the same stages called one by
 one: every output (w_z, alpha, w_f, the tables, ids, distance bits) equal
 bit for bit, with and without a given w_z, fp32 and binary16 tables, list
-scan forced on; then a sample of rows against the oracle, and the error
+scan forced on (the table kernel then also writes the bound's factors), the
+condition inside the encoder's launch (h of 1 to 4, no bank) or in its own
+kernel (h = 5); then a sample of rows against the oracle, and the error
 paths (each leaves the index usable)."""
 import numpy as np
 import pytest
@@ -80,6 +82,31 @@ def test_same_bits_as_the_separate_calls(B, case, given_wz, lut_dtype, mode):
     assert used == used_ref and used == (mode == 2)
     for name, a, b in zip(("ids", "dist", "w_z", "alpha", "w_f", "lut"), got, ref):
         assert a.shape == b.shape, name
+        assert torch.equal(_bits(a) if a.is_floating_point() else a, _bits(b) if b.is_floating_point() else b), name
+
+
+@pytest.mark.parametrize("h,bank_rows", [(1, 45), (3, 97), (4, 1000), (5, 33), (0, 0)])
+def test_condition_in_the_encoder_launch(B, h, bank_rows):
+    """The encoder launch conditions the queries itself for h <= 4 (and
+    without a bank); h = 5 takes the condition kernel.  Either way alpha,
+    w_f, the tables and the results are the separate calls' bits."""
+    say(f"[query_batch] h={h} bank_rows={bank_rows}")
+    M, dsub = 16, 4
+    ix = random_index(9_000, M, dsub, 2, 300, seed=h + 40, device="cuda", bank_rows=max(bank_rows, 1))
+    bank, W = (ix["bank"], ix["W"]) if bank_rows else (None, None)
+    idx = B.Index(ix["codes"], ix["C_pq"], ix["attrs"], bank, W, ix["r"] if bank_rows else 0, h,
+                  ix["hash_seed"], max_batch=32, max_k=10, cluster_cols=(0,))
+    idx.load_encoder(random_encoder(2, M * dsub, [300, 300], seed=h, layers=1))
+    g = torch.Generator(device="cpu").manual_seed(h)
+    q = torch.randn(29, M * dsub, generator=g).cuda()
+    preds = [[(0, 7 * i, 7 * i + 40)] + ([(1, 0, 150)] if i % 3 == 0 else []) for i in range(29)]
+    got = idx.query_batch(q, preds, 10)
+    ref = _stagewise(idx, q, preds, 10, None, 0)
+    torch.cuda.synchronize()
+    for name, a, b in zip(("ids", "dist", "w_z", "alpha", "w_f", "lut"), got, ref):
+        if a is None or b is None:
+            assert a is None and b is None and name == "alpha"
+            continue
         assert torch.equal(_bits(a) if a.is_floating_point() else a, _bits(b) if b.is_floating_point() else b), name
 
 
