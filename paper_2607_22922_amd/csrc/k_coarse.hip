@@ -526,7 +526,7 @@ __device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const floa
   float* s_sdc = reinterpret_cast<float*>(smem);                          // [C]
   unsigned char* scratch = smem + ((static_cast<size_t>(C) * 4 + 15) & ~size_t{15});
   LutT* s_lut = reinterpret_cast<LutT*>(scratch);                         // phase 1
-  int32_t* s_cnt = reinterpret_cast<int32_t*>(scratch);                   // phase 2: [S]
+  int32_t* s_cnt = reinterpret_cast<int32_t*>(scratch);                   // phase 2: [S] ranks, then items
   int32_t* s_hist = s_cnt + S;                                            // phase 2: [kPlanBuckets]
   uint32_t* s_bmin = reinterpret_cast<uint32_t*>(s_hist + kPlanBuckets);  // phase 2: [kPlanBuckets]
   __shared__ int s_count;
@@ -671,17 +671,13 @@ __device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const floa
   }
   __syncthreads();
   // Phase 2: each sub-list's positions of rows x0 and x1 (ranks), held by
-  // the thread of sub-list s = tid + 1024 j in slot j.
-  int32_t r0[kSPer], r1[kSPer];
-  for (int pass = 0; pass < 2; ++pass) {
-    const int64_t x = pass == 0 ? x0 : x1, bx = x >> a.f_shift;
-#pragma unroll
-    for (int j = 0; j < kSPer; ++j) {
-      const int s = tid + j * 1024;
-      if (s < S) s_cnt[s] = a.cnt_f[bx * S + s];
-    }
-    __syncthreads();
-    for (int64_t r = (bx << a.f_shift) + tid; r < x; r += 4 * 1024) {
+  // the thread of sub-list s = tid + 1024 j in slot j: the rank table's rows
+  // at x0 and x1 plus counts over the rows after them (fewer than
+  // 2^f_shift).  The table rows and the first 4096 rows after each table
+  // entry (four a thread) go out in one round; longer stretches (f_shift
+  // above 12) take more rounds.
+  auto count_rest = [&](int64_t from, int64_t x) {
+    for (int64_t r = from + tid; r < x; r += 4 * 1024) {
       uint32_t wv[4];
       int bv[4];
 #pragma unroll
@@ -694,14 +690,67 @@ __device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const floa
       for (int u = 0; u < 4; ++u)
         if (r + u * 1024 < x) atomicAdd(&s_cnt[static_cast<int>(wv[u] & 0xFFFFu) * kBands + bv[u]], 1);
     }
+  };
+  int32_t r0[kSPer], r1[kSPer];
+  {
+    const int64_t bx0 = x0 >> a.f_shift, bx1 = x1 >> a.f_shift;
+    int32_t c0[kSPer], c1[kSPer], so[kSPer];
+#pragma unroll
+    for (int j = 0; j < kSPer; ++j) {
+      const int s = tid + j * 1024;
+      c0[j] = s < S ? a.cnt_f[bx0 * S + s] : 0;
+      c1[j] = s < S ? a.cnt_f[bx1 * S + s] : 0;
+    }
+    uint32_t w0[4], w1[4];
+    int b0[4], b1[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t ra = (bx0 << a.f_shift) + tid + u * 1024, rb = (bx1 << a.f_shift) + tid + u * 1024;
+      w0[u] = ra < x0 ? a.words[ra] : 0u;
+      b0[u] = ra < x0 ? a.band[ra] : 0;
+      w1[u] = rb < x1 ? a.words[rb] : 0u;
+      b1[u] = rb < x1 ? a.band[rb] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < kSPer; ++j) {
+      const int s = tid + j * 1024;
+      if (s < S) s_cnt[s] = c0[j];
+    }
+    __syncthreads();
+    // (the offsets in c0's registers, on their way during the counting)
+#pragma unroll
+    for (int j = 0; j < kSPer; ++j) {
+      const int s = tid + j * 1024;
+      so[j] = s < S ? a.sub_off[s] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t ra = (bx0 << a.f_shift) + tid + u * 1024;
+      if (ra < x0) atomicAdd(&s_cnt[static_cast<int>(w0[u] & 0xFFFFu) * kBands + b0[u]], 1);
+    }
+    count_rest((bx0 << a.f_shift) + 4 * 1024, x0);
+    __syncthreads();
+    // (entry s is this thread's until the next barrier: x0's rank out, x1's
+    // table row in)
+#pragma unroll
+    for (int j = 0; j < kSPer; ++j) {
+      const int s = tid + j * 1024;
+      r0[j] = s < S ? so[j] + s_cnt[s] : 0;
+      if (s < S) s_cnt[s] = c1[j];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t rb = (bx1 << a.f_shift) + tid + u * 1024;
+      if (rb < x1) atomicAdd(&s_cnt[static_cast<int>(w1[u] & 0xFFFFu) * kBands + b1[u]], 1);
+    }
+    count_rest((bx1 << a.f_shift) + 4 * 1024, x1);
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < kSPer; ++j) {
       const int s = tid + j * 1024;
-      const int32_t v = s < S ? a.sub_off[s] + s_cnt[s] : 0;
-      if (pass == 0) r0[j] = v; else r1[j] = v;
+      r1[j] = s < S ? so[j] + s_cnt[s] : 0;
     }
-    __syncthreads();
   }
   // Items: the nearest selected centroid, the bounds' range, then the
   // buckets' counts and smallest bounds.
@@ -804,28 +853,46 @@ __device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const floa
     if ((tid & 63) == 0 && stop != static_cast<uint32_t>(kPlanBuckets)) atomicMin(&s_stop, static_cast<int>(stop));
   }
   __syncthreads();
-  // Each item before the first pruned bucket to its place: rows, carried
-  // bound, tile count (LDS).
-  int32_t* s_nt = s_cnt;   // the counts are no longer needed
+  // Each item before the first pruned bucket gets its place; then its
+  // fields go out field by field through LDS (s_cnt, free now), so that the
+  // stores are coalesced: rows, carried bound, and the tile counts, which
+  // stay in s_nt for the offsets.
+  int32_t* s_nt = s_cnt;
   const int stop_b = min(s_stop, kPlanBuckets);
   const int n_items = stop_b < kPlanBuckets ? s_hist[stop_b] : s_count;
   const size_t base = static_cast<size_t>(q) * S;
   __syncthreads();   // s_hist[stop_b] read before the cursors move
+  static_assert(kMaxItems <= (1 << kItemBits) && kPlanBuckets <= (1 << (31 - kItemBits)),
+                "a place and a bucket in one non-negative word");
+  int32_t place[kSPer];   // (bucket << kItemBits) | position, or -1
 #pragma unroll
   for (int j = 0; j < kSPer; ++j) {
     const int s = tid + j * 1024;
+    place[j] = -1;
     if (s < S && r1[j] > r0[j]) {
       const int b = bucket(s, lb[j]);
-      if (b < stop_b) {
-        const int i = atomicAdd(&s_hist[b], 1);
-        a.it_r0[base + i] = r0[j];
-        a.it_r1[base + i] = r1[j];
-        a.it_lb[base + i] = b == 0 ? __builtin_nanf("") : from_ordered_bits(s_bmin[b]);
-        s_nt[i] = ((r1[j] - 1) >> 6) - (r0[j] >> 6) + 1;
-      }
+      if (b < stop_b) place[j] = (b << kItemBits) | atomicAdd(&s_hist[b], 1);
     }
   }
-  __syncthreads();
+  int32_t* const outs[3] = {a.it_r0, a.it_r1, reinterpret_cast<int32_t*>(a.it_lb)};
+#pragma unroll
+  for (int field = 0; field < 4; ++field) {
+    __syncthreads();   // the previous field is out (the ranks are read, for the first)
+#pragma unroll
+    for (int j = 0; j < kSPer; ++j) {
+      if (place[j] < 0) continue;
+      const int b = place[j] >> kItemBits;
+      int32_t v;
+      if (field == 0) v = r0[j];
+      else if (field == 1) v = r1[j];
+      else if (field == 2) v = __float_as_int(b == 0 ? __builtin_nanf("") : from_ordered_bits(s_bmin[b]));
+      else v = ((r1[j] - 1) >> 6) - (r0[j] >> 6) + 1;
+      s_cnt[place[j] & kItemMask] = v;
+    }
+    __syncthreads();
+    if (field < 3)
+      for (int i = tid; i < n_items; i += 1024) outs[field][base + i] = s_cnt[i];
+  }
   {
     // tile offsets: exclusive prefix, a contiguous run of items a thread
     const int per = (n_items + 1023) / 1024;
@@ -840,7 +907,6 @@ __device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const floa
       const int i = tid * per + u;
       if (i < n_items) {
         const int nt = s_nt[i];
-        a.it_t[base + i] = off;
         s_nt[i] = off;
         off += nt;
       }
@@ -852,7 +918,8 @@ __device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const floa
       hdr[3] = delta;
     }
   }
- 
+  __syncthreads();
+  for (int i = tid; i < n_items; i += 1024) a.it_t[base + i] = s_nt[i];
 }
 
 // The plan of query blockIdx.x, its bound factors reduced from the parts
