@@ -1191,32 +1191,47 @@ bool list_scan_wanted(const ifvs_index* idx, int32_t lut_dtype, const BatchShape
          (idx->opt_coarse == 2 || (b.span >= kCoarseAutoTiles && idx->m >= kCoarseAutoM));
 }
 
-// Filter, Rank and Select for one batch.  With static_scratch the device
-// workspace is carved from the static array of the index's device instead of
-// the index's own workspace (no gather scan then: every query takes the tiled
-// scan, with the same results).
-// bounded: the caller gave the alpha and w_f its tables were built with
-// (either may be null), so the list scan may run with the coarse bound.
-ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds, const void* lut,
-                        int32_t lut_dtype, bool bounded, const float* alpha, const float* wf, int32_t k,
-                        int32_t* ids_out, float* dist_out, uint32_t* bitmap_out, void* stream,
-                        bool static_scratch, int pre_slot = -1, DevPred* pre_host = nullptr,
-                        bool parts_ready = false) {
+// The host side of a search, before anything is enqueued: validation, the
+// staged predicates (or the caller's staging, pre_slot >= 0), the batch's
+// shape, the workspace, the scan plan, whether the list scan runs, the
+// scan's dispatch order.  With static_scratch the device workspace is carved
+// from the static array of the index's device instead of the index's own
+// workspace (no gather scan then: every query takes the tiled scan, with the
+// same results).  bounded: the caller gave the alpha and w_f its tables were
+// built with (either may be null), so the list scan may run with the coarse
+// bound.
+struct SearchPrep {
+  bool empty = false;   // nq == 0: nothing to do
+  int slot = 0;
+  DevPred* host = nullptr;
+  BatchShape shape;
+  SearchWs ws;
+  ScanPlan plan{};
+  int list_jobs = 1;
+  bool list_mode = false;
+  bool ordered = false;
+  int64_t n_order = 0;
+};
+
+ifvs_status prepare_search(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds, const void* lut,
+                           int32_t lut_dtype, bool bounded, const float* alpha, int32_t k, int32_t* ids_out,
+                           float* dist_out, uint32_t* bitmap_out, hipStream_t s, bool static_scratch, int pre_slot,
+                           DevPred* pre_host, SearchPrep& p) {
   if (ifvs_status st = check_index(idx); st != IFVS_OK) return st;
   if (ifvs_status st = check_nq(idx, nq); st != IFVS_OK) return st;
   if (lut_dtype != IFVS_LUT_F32 && lut_dtype != IFVS_LUT_F16) return fail(IFVS_E_INVALID, "unknown lut_dtype");
   if (k < 1 || k > idx->max_k)
     return fail(IFVS_E_INVALID, "k = " + std::to_string(k) + " outside 1.." + std::to_string(idx->max_k) + " (max_k)");
-  if (nq == 0) return IFVS_OK;
+  p.empty = nq == 0;
+  if (p.empty) return IFVS_OK;
   if (!lut || !ids_out || !dist_out) return fail(IFVS_E_INVALID, "lut, ids_out or dist_out is NULL");
   if (alpha && idx->bank_rows == 0) return fail(IFVS_E_INVALID, "alpha given but the index has no memory bank");
   if (reinterpret_cast<uintptr_t>(lut) % 16 != 0) return fail(IFVS_E_INVALID, "lut must be 16-byte aligned");
   ScanPlan probe{};
   if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, false, 0, size_t{1} << 40, &probe); st != IFVS_OK) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
   IFVS_HIP(hipSetDevice(idx->device), "hipSetDevice");
-  DevPred* host = nullptr;
-  int slot = 0;
+  DevPred*& host = p.host;
+  int& slot = p.slot;
   // Predicates are validated before anything is enqueued (or were, with the
   // scan order, by a caller that staged them for earlier kernels too).
   if (pre_slot >= 0) {
@@ -1225,17 +1240,18 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   } else if (ifvs_status st = stage_predicates(idx, nq, preds, true, false, s, &slot, &host); st != IFVS_OK) {
     return st;
   }
-  const BatchShape shape = batch_shape(idx, nq, host);
+  p.shape = batch_shape(idx, nq, host);
+  const BatchShape& shape = p.shape;
   const bool need_bitmap = shape.need_bitmap, interval_batch = shape.interval_batch;
   const int64_t span = shape.span;
-  SearchWs ws;
+  SearchWs& ws = p.ws;
   if (!static_scratch) {
     ws = index_ws(idx);
   } else if (ifvs_status st = carve_static_ws(idx, nq, k, need_bitmap || bitmap_out != nullptr, &ws);
              st != IFVS_OK) {
     return st;
   }
-  ScanPlan plan{};
+  ScanPlan& plan = p.plan;
   if (ifvs_status st = plan_scan(idx, nq, k, lut_dtype, interval_batch, span, ws.partial_keys, &plan); st != IFVS_OK)
     return st;
   // List scan (coarse bound): when the caller passed the tables' operands, a
@@ -1245,16 +1261,17 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   const CoarseLists& cl = idx->coarse;
   // Jobs per query: at most kListJobs (IFVS_OPT_SPLITS lowers the cap), as
   // the partial lists have room.
-  int list_jobs = std::min(kListJobs, idx->opt_splits > 0 ? idx->opt_splits : kListJobs);
+  int& list_jobs = p.list_jobs;
+  list_jobs = std::min(kListJobs, idx->opt_splits > 0 ? idx->opt_splits : kListJobs);
   while (list_jobs > 1 && static_cast<size_t>(nq) * list_jobs * kScanWaves * k > ws.partial_keys) --list_jobs;
   const int list_splits = list_jobs;
-  const bool list_mode =
+  p.list_mode =
       bounded && !static_scratch && list_scan_wanted(idx, lut_dtype, shape) &&
       list_plan_lds_bytes(idx->m, lut_dtype, cl.C) <= size_t{kLdsBudget} &&
       list_scan_lds_bytes(idx->m, lut_dtype, pool_stride_for(k)) <= size_t{kLdsBudget} &&
       list_jobs_lds_bytes(nq) <= size_t{kLdsBudget} &&
       static_cast<size_t>(nq) * list_splits * kScanWaves * k <= ws.partial_keys;
-  if (idx->opt_count_reads && !list_mode &&
+  if (idx->opt_count_reads && !p.list_mode &&
       (!scan_can_count(idx->m, plan.qtile, lut_dtype) || plan.lds_bytes + kLookupHistBytes > size_t{kLdsBudget}))
     return fail(IFVS_E_UNSUPPORTED, "IFVS_OPT_COUNT_READS: no read-counting scan for this plan (it needs one query "
                                     "per tile, M of 16, 48 or 120, and 272 bytes of LDS to spare)");
@@ -1262,22 +1279,55 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   // the interval kernel copies it to the device.
   const int32_t* qorder_host = reinterpret_cast<const int32_t*>(host + idx->max_batch);
   int32_t* order_host = reinterpret_cast<int32_t*>(host + idx->max_batch) + idx->max_batch;
-  const int64_t n_order = plan.abs_cells && idx->opt_slot_order == 0
-                              ? static_cast<int64_t>(8) * ((((nq + plan.qtile - 1) / plan.qtile) + 7) / 8) * plan.splits
-                              : 0;
-  const bool ordered = n_order > 0 && n_order <= ws.slot_order_cap;
-  if (ordered) order_scan_slots(idx, host, qorder_host, nq, plan, order_host);
-  IFVS_LAUNCH(idx, kStFilter, s, "launching interval kernel",
-              launch_intervals(idx->attrs_phys, idx->n, idx->c0, idx->c1, idx->vstart, idx->vmin, idx->vcount,
-                               idx->staging_dev[slot],
-                               reinterpret_cast<const int32_t*>(idx->staging_dev[slot] + idx->max_batch), nq,
-                               ws.preds, ws.qorder, ws.iv, ws.gthr,
-                               ordered ? reinterpret_cast<const int32_t*>(idx->staging_dev[slot] + idx->max_batch) +
-                                             idx->max_batch
-                                       : nullptr,
-                               ws.slot_order, ordered ? n_order : 0, s));
-  if (ifvs_status st = release_slot(idx, slot, s); st != IFVS_OK) return st;
-  if (list_mode) {
+  p.n_order = plan.abs_cells && idx->opt_slot_order == 0
+                  ? static_cast<int64_t>(8) * ((((nq + plan.qtile - 1) / plan.qtile) + 7) / 8) * plan.splits
+                  : 0;
+  p.ordered = p.n_order > 0 && p.n_order <= ws.slot_order_cap;
+  if (p.ordered) order_scan_slots(idx, host, qorder_host, nq, plan, order_host);
+  return IFVS_OK;
+}
+
+// The interval kernel's work for a prepared search: the batch's predicates,
+// scan order and dispatch order from its staging slot.
+IntervalArgs search_intervals(const ifvs_index* idx, int32_t nq, const SearchPrep& p) {
+  IntervalArgs a;
+  a.attrs_phys = idx->attrs_phys;
+  a.n = idx->n;
+  a.c0 = idx->c0;
+  a.c1 = idx->c1;
+  a.vstart = idx->vstart;
+  a.vmin = idx->vmin;
+  a.vcount = idx->vcount;
+  a.staged_preds = idx->staging_dev[p.slot];
+  a.staged_order = reinterpret_cast<const int32_t*>(idx->staging_dev[p.slot] + idx->max_batch);
+  a.nq = nq;
+  a.preds_out = p.ws.preds;
+  a.order_out = p.ws.qorder;
+  a.iv = p.ws.iv;
+  a.gthr = p.ws.gthr;
+  a.slots_src = p.ordered ? a.staged_order + idx->max_batch : nullptr;
+  a.slots_dst = p.ws.slot_order;
+  a.n_slots = p.ordered ? p.n_order : 0;
+  return a;
+}
+
+// The device side of a prepared search (intervals_done: the caller already
+// enqueued search_intervals' work; parts_ready: the table kernel wrote the
+// coarse bound's factors).
+ifvs_status run_search(ifvs_index* idx, int32_t nq, const void* lut, int32_t lut_dtype, const float* alpha,
+                       const float* wf, int32_t k, int32_t* ids_out, float* dist_out, uint32_t* bitmap_out,
+                       hipStream_t s, const SearchPrep& p, bool intervals_done, bool parts_ready) {
+  if (p.empty) return IFVS_OK;
+  const SearchWs& ws = p.ws;
+  const ScanPlan& plan = p.plan;
+  const bool need_bitmap = p.shape.need_bitmap, interval_batch = p.shape.interval_batch;
+  const int list_jobs = p.list_jobs, list_splits = p.list_jobs;
+  const bool ordered = p.ordered;
+  const CoarseLists& cl = idx->coarse;
+  if (!intervals_done)
+    IFVS_LAUNCH(idx, kStFilter, s, "launching interval kernel", launch_intervals(search_intervals(idx, nq, p), s));
+  if (ifvs_status st = release_slot(idx, p.slot, s); st != IFVS_OK) return st;
+  if (p.list_mode) {
     // (the table kernel wrote the bound's factors when the caller says so)
     if (!parts_ready)
       IFVS_LAUNCH(idx, kStCoarse, s, "launching table bound kernel",
@@ -1454,6 +1504,20 @@ ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds
   return IFVS_OK;
 }
 
+// Filter, Rank and Select for one batch: prepare_search, then run_search.
+ifvs_status search_impl(ifvs_index* idx, int32_t nq, const ifvs_predicate* preds, const void* lut,
+                        int32_t lut_dtype, bool bounded, const float* alpha, const float* wf, int32_t k,
+                        int32_t* ids_out, float* dist_out, uint32_t* bitmap_out, void* stream,
+                        bool static_scratch) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  SearchPrep p;
+  if (ifvs_status st = prepare_search(idx, nq, preds, lut, lut_dtype, bounded, alpha, k, ids_out, dist_out,
+                                      bitmap_out, s, static_scratch, -1, nullptr, p);
+      st != IFVS_OK)
+    return st;
+  return run_search(idx, nq, lut, lut_dtype, alpha, wf, k, ids_out, dist_out, bitmap_out, s, p, false, false);
+}
+
 }  // namespace
 
 extern "C" {
@@ -1509,6 +1573,16 @@ ifvs_status ifvs_query_batch(ifvs_index* idx, int32_t nq, const float* q, const 
   // The encoder conditions the queries it encodes in the same launch (alpha
   // and w_f, the condition kernel's bits) where it can.
   const bool fused_condition = !w_z && encoder_conditions(idx->h, alpha != nullptr);
+  // The search's host side now (its intervals can then go into the encoder's
+  // launch too).
+  SearchPrep prep;
+  if (ifvs_status st = prepare_search(idx, nq, preds, lut_out, lut_dtype, true, alpha, k, ids_out, dist_out, nullptr,
+                                      s, false, slot, host, prep);
+      st != IFVS_OK) {
+    (void)release_slot(idx, slot, s);
+    return st;
+  }
+  const IntervalArgs iva = search_intervals(idx, nq, prep);
   const float* wz = w_z;
   if (!w_z) {
     EncCondition cond;
@@ -1523,20 +1597,17 @@ ifvs_status ifvs_query_batch(ifvs_index* idx, int32_t nq, const float* q, const 
     if (ifvs_status st = launch(kStEncode, "launching encoder kernel", [&]() -> hipError_t {
           return launch_encoder(idx->enc_params, idx->enc_off, idx->enc_scale, idx->enc_H, idx->enc_heads,
                                 idx->enc_layers, idx->enc_F, idx->dim, idx->n_attr, idx->staging_dev[slot], nq, wz_out,
-                                s, fused_condition ? &cond : nullptr);
+                                s, fused_condition ? &cond : nullptr, &iva);
         });
         st != IFVS_OK)
       return st;
     wz = wz_out;
   }
-  // When the list scan is likely to run, the table kernel writes the coarse
-  // bound's factors as it forms the conditioned codewords (the search then
-  // skips its own bound kernel; a batch that takes the interval scan after
-  // all just leaves them unread).
-  float* parts = list_scan_wanted(idx, lut_dtype, batch_shape(idx, nq, host)) &&
-                         lut_emits_bound_parts(idx->dsub, idx->r, alpha != nullptr)
-                     ? idx->bound_parts
-                     : nullptr;
+  // When the list scan runs, the table kernel writes the coarse bound's
+  // factors as it forms the conditioned codewords (the search then skips its
+  // own bound kernel).
+  float* parts =
+      prep.list_mode && lut_emits_bound_parts(idx->dsub, idx->r, alpha != nullptr) ? idx->bound_parts : nullptr;
   if (!fused_condition) {
     if (ifvs_status st = launch(kStCondition, "launching condition kernel", [&]() -> hipError_t {
           return launch_condition(q, idx->dim, idx->staging_dev[slot], nq, idx->bank, idx->bank_rows,
@@ -1551,8 +1622,9 @@ ifvs_status ifvs_query_batch(ifvs_index* idx, int32_t nq, const float* q, const 
       });
       st != IFVS_OK)
     return st;
-  const ifvs_status st = search_impl(idx, nq, preds, lut_out, lut_dtype, true, alpha, wf_out, k, ids_out, dist_out,
-                                     nullptr, stream, false, slot, host, parts != nullptr);
+  // (the encoder's launch computed the intervals when it ran)
+  const ifvs_status st = run_search(idx, nq, lut_out, lut_dtype, alpha, wf_out, k, ids_out, dist_out, nullptr, s,
+                                    prep, !w_z, parts != nullptr);
   if (st != IFVS_OK && !idx->slot_busy[slot]) (void)release_slot(idx, slot, s);   // the earlier kernels read it
   return st;
 }
@@ -1618,6 +1690,32 @@ ifvs_status attach_vectors(ifvs_index* idx, const float* src, const int32_t* src
   if (e != hipSuccess) return bail(hip_fail(e, "staging vectors"));
   if (bad) return bail(fail(IFVS_E_INVALID, std::to_string(bad) + " vector values are NaN or infinite"));
   return IFVS_OK;
+}
+
+}  // namespace
+
+namespace {
+
+// The interval kernel's work for the exact search (the index's own device
+// copies; no dispatch order).
+IntervalArgs exact_intervals(const ifvs_index* idx, int slot, int32_t nq) {
+  IntervalArgs a;
+  a.attrs_phys = idx->attrs_phys;
+  a.n = idx->n;
+  a.c0 = idx->c0;
+  a.c1 = idx->c1;
+  a.vstart = idx->vstart;
+  a.vmin = idx->vmin;
+  a.vcount = idx->vcount;
+  a.staged_preds = idx->staging_dev[slot];
+  a.staged_order = reinterpret_cast<const int32_t*>(idx->staging_dev[slot] + idx->max_batch);
+  a.nq = nq;
+  a.preds_out = idx->preds_dev;
+  a.order_out = idx->qorder_dev;
+  a.iv = idx->iv_dev;
+  a.gthr = idx->gthr_dev;
+  a.slots_dst = idx->slot_order_dev;
+  return a;
 }
 
 }  // namespace
@@ -1706,11 +1804,7 @@ ifvs_status ifvs_exact_search(ifvs_index* idx, int32_t nq, const float* q, const
   }
   const bool screened = idx->opt_exact_plan == 2 || (idx->opt_exact_plan == 0 && sum_hull < sum_iv);
   IFVS_LAUNCH(idx, kStFilter, s, "launching interval kernel",
-              launch_intervals(idx->attrs_phys, idx->n, idx->c0, idx->c1, idx->vstart, idx->vmin, idx->vcount,
-                               idx->staging_dev[slot],
-                               reinterpret_cast<const int32_t*>(idx->staging_dev[slot] + idx->max_batch), nq,
-                               idx->preds_dev, idx->qorder_dev, idx->iv_dev, idx->gthr_dev, nullptr,
-                               idx->slot_order_dev, 0, s));
+              launch_intervals(exact_intervals(idx, slot, nq), s));
   if (ifvs_status st = release_slot(idx, slot, s); st != IFVS_OK) return st;
   if (need_bitmap)
     if (ifvs_status st = filter_into_workspace(idx, index_ws(idx), nq, true, false, s); st != IFVS_OK) return st;

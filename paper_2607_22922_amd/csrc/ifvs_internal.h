@@ -76,22 +76,33 @@ hipError_t cluster_permutation(const int32_t* attrs, int64_t n, int n_cluster, i
                                int32_t* perm, hipStream_t s);
 hipError_t launch_gather_attrs(const int32_t* attrs, int64_t n, int n_attr, const int32_t* perm,
                                int32_t* attrs_phys, hipStream_t s);
-// Row interval [iv[2q], iv[2q+1]) of each query's cluster-key clauses.
-// Also resets each query's shared scan threshold gthr[q] to all ones.
-// Row interval of every query on the clustered layout (whole index for
-// predicates without a cluster-key interval).  Reads the predicates and the
-// scan order from the staging slot (pinned host memory) and leaves device
-// copies in preds_out / order_out for the kernels that follow; resets the
-// per-query global thresholds.
-// vstart (may be null): vstart[t] = first physical row whose leading cluster
-// key is >= vmin + t, for t < vcount (the last entry is n).
-// It also copies n_slots words of the scan's dispatch order from the
-// staging slot (slots_src) to slots_dst.
-hipError_t launch_intervals(const int32_t* attrs_phys, int64_t n, int c0, int c1, const int32_t* vstart,
-                            int64_t vmin, int64_t vcount, const DevPred* staged_preds,
-                            const int32_t* staged_order, int nq, DevPred* preds_out, int32_t* order_out,
-                            int64_t* iv, uint64_t* gthr, const int32_t* slots_src, int32_t* slots_dst,
-                            int64_t n_slots, hipStream_t s);
+// Row interval [iv[2q], iv[2q+1]) of every query on the clustered layout
+// (whole index for predicates without a cluster-key interval).  Reads the
+// predicates and the scan order from the staging slot (pinned host memory)
+// and leaves device copies in preds_out / order_out for the kernels that
+// follow; resets each query's shared scan threshold gthr[q] to all ones;
+// copies n_slots words of the scan's dispatch order from the staging slot
+// (slots_src) to slots_dst.  vstart (may be null): vstart[t] = first
+// physical row whose leading cluster key is >= vmin + t, for t < vcount (the
+// last entry is n).
+struct IntervalArgs {
+  const int32_t* attrs_phys = nullptr;
+  int64_t n = 0;
+  int c0 = 0, c1 = 0;
+  const int32_t* vstart = nullptr;
+  int64_t vmin = 0, vcount = 0;
+  const DevPred* staged_preds = nullptr;
+  const int32_t* staged_order = nullptr;
+  int nq = 0;
+  DevPred* preds_out = nullptr;
+  int32_t* order_out = nullptr;
+  int64_t* iv = nullptr;
+  uint64_t* gthr = nullptr;
+  const int32_t* slots_src = nullptr;
+  int32_t* slots_dst = nullptr;
+  int64_t n_slots = 0;
+};
+hipError_t launch_intervals(const IntervalArgs& a, hipStream_t s);
 
 // codes (row-major [n][m]) -> 64-row tiles, physical row r taken from
 // original row perm[r] (perm may be null: identity).
@@ -253,9 +264,11 @@ size_t encoder_lds_bytes(int H, int F);
 // Whether the encoder can condition in-launch: any index without a bank,
 // else h of at most 4.
 bool encoder_conditions(int h, bool has_bank);
+// With iv, the launch also does launch_intervals' work for the batch (in
+// workgroups of its own beside the encoder's).
 hipError_t launch_encoder(const float* params, const double* off, const double* scale, int H, int heads, int layers,
                           int F, int D, int n_attr, const DevPred* preds, int nq, float* wz, hipStream_t s,
-                          const EncCondition* cond = nullptr);
+                          const EncCondition* cond = nullptr, const IntervalArgs* iv = nullptr);
 
 // Whether a read-counting build of the scan exists for this plan (one query
 // per tile, M of 16, 48 or 120).

@@ -11,6 +11,7 @@
 #include <hipcub/hipcub.hpp>
 
 #include "ifvs_internal.h"
+#include "intervals_device.h"
 
 namespace ifvs {
 
@@ -39,104 +40,12 @@ __global__ void gather_attrs_kernel(const int32_t* __restrict__ attrs, int64_t n
   }
 }
 
-// (c0, c1) key of row r is below (x0, x1)?  (x1 ignored when a1 is null.)
-__device__ __forceinline__ bool key_below(const int32_t* __restrict__ a0, const int32_t* __restrict__ a1,
-                                          int64_t r, int64_t x0, int64_t x1) {
-  const int64_t v0 = a0[r];
-  if (a1 && v0 == x0) return static_cast<int64_t>(a1[r]) < x1;
-  return v0 < x0;
-}
-
-// First row of [lo, hi) whose key is >= (x0, x1) (hi when there is none),
-// given that the rows before lo are below it: a 64-ary search by one
-// wavefront.  Each step every lane probes one of 64 evenly spaced rows of the
-// current range; the ballot of "probe below x" narrows the range to the gap
-// after the last such probe, so 10^7 rows take four dependent loads.
-__device__ int64_t wave_lower_bound(const int32_t* __restrict__ a0, const int32_t* __restrict__ a1,
-                                    int64_t lo, int64_t hi, int64_t x0, int64_t x1) {
-  const int lane = threadIdx.x & 63;
-  while (hi - lo > 64) {
-    const int64_t step = (hi - lo + 63) / 64;
-    const int64_t r = lo + lane * step; // probes lo, lo+step, ... (< hi or past it)
-    const bool below = r < hi && key_below(a0, a1, r, x0, x1);
-    const uint64_t mask = __ballot(below);
-    if (mask == 0) {
-      hi = lo;                           // key(lo) >= x
-    } else {
-      const int last = 63 - __clzll(mask);
-      const int64_t r_last = lo + last * step;
-      lo = r_last + 1;
-      hi = min(hi, r_last + step);
-    }
-  }
-  // Final <= 64 rows: one probe per lane.
-  const int64_t r = lo + lane;
-  const bool below = r < hi && key_below(a0, a1, r, x0, x1);
-  return lo + __popcll(__ballot(below));
-}
-
-// First row whose leading key is >= x, from the value table (vstart[t] =
-// first row with leading key >= vmin + t, t < vcount; the last entry is n).
-__device__ __forceinline__ int64_t table_lower_bound(const int32_t* __restrict__ vstart, int64_t vmin,
-                                                     int64_t vcount, int64_t n, int64_t x) {
-  if (x <= vmin) return 0;
-  if (x >= vmin + (vcount - 1)) return n;
-  return vstart[x - vmin];
-}
-
-__global__ __launch_bounds__(64) void intervals_kernel(const int32_t* __restrict__ attrs_phys, int64_t n,
-                                                       int c0, int c1, const int32_t* __restrict__ vstart,
-                                                       int64_t vmin, int64_t vcount,
-                                                       const DevPred* __restrict__ staged_preds,
-                                                       const int32_t* __restrict__ staged_order, int nq,
-                                                       DevPred* __restrict__ preds_out,
-                                                       int32_t* __restrict__ order_out,
-                                                       int64_t* __restrict__ iv,
-                                                       uint64_t* __restrict__ gthr,
-                                                       const int32_t* __restrict__ slots_src,
-                                                       int32_t* __restrict__ slots_dst, int64_t n_slots) {
-  const int q = blockIdx.x >> 1;        // two wavefronts per query: lower and upper bound
-  const bool upper = blockIdx.x & 1;
-  // The scan's dispatch order, spread over all workgroups of this launch.
-  for (int64_t i = blockIdx.x * 64 + threadIdx.x; i < n_slots; i += static_cast<int64_t>(gridDim.x) * 64)
-    slots_dst[i] = slots_src[i];
-  if (q >= nq) return;
-  __shared__ DevPred sp;
-  copy_pred(staged_preds + q, &sp, threadIdx.x);
-  __syncthreads();
-  if (!upper) {
-    copy_pred(&sp, preds_out + q, threadIdx.x);
-    if (threadIdx.x == 0) order_out[q] = staged_order[q];
-  }
-  const DevPred& p = sp;
-  int64_t r = upper ? n : 0;
-  if (p.n_eff < 0) {
-    r = 0;
-  } else if (p.iv_mode == 1) {
-    const int64_t x = upper ? p.iv_hi0 : p.iv_lo0;
-    if (vstart) {
-      r = table_lower_bound(vstart, vmin, vcount, n, x);
-    } else {
-      const int32_t* a0 = attrs_phys + static_cast<int64_t>(c0) * n;
-      r = wave_lower_bound(a0, nullptr, 0, n, x, 0);
-    }
-  } else if (p.iv_mode == 2) {
-    // Leading key equal to iv_lo0, second key in [iv_lo1, iv_hi1): the value
-    // table (when present) gives the rows of that leading key, the search
-    // runs inside them.
-    const int32_t* a0 = attrs_phys + static_cast<int64_t>(c0) * n;
-    const int32_t* a1 = attrs_phys + static_cast<int64_t>(c1) * n;
-    int64_t lo = 0, hi = n;
-    if (vstart) {
-      lo = table_lower_bound(vstart, vmin, vcount, n, p.iv_lo0);
-      hi = table_lower_bound(vstart, vmin, vcount, n, p.iv_lo0 + 1);
-    }
-    r = wave_lower_bound(a0, a1, lo, hi, p.iv_lo0, upper ? p.iv_hi1 : p.iv_lo1);
-  }
-  if (threadIdx.x == 0) {
-    iv[2 * q + (upper ? 1 : 0)] = r;
-    if (!upper) gthr[q] = ~0ull;
-  }
+// Two wavefronts per query (lower and upper bound), one per workgroup; the
+// dispatch-order copy is spread over all of them.
+__global__ __launch_bounds__(64) void intervals_kernel(const IntervalArgs a) {
+  copy_slot_order(a, blockIdx.x, gridDim.x, threadIdx.x);
+  const int q = blockIdx.x >> 1;
+  if (q < a.nq) interval_bound(a, q, blockIdx.x & 1, threadIdx.x);
 }
 
 unsigned grid_for(int64_t work) { return static_cast<unsigned>(std::min<int64_t>((work + 255) / 256, 65536)); }
@@ -181,14 +90,9 @@ hipError_t launch_gather_attrs(const int32_t* attrs, int64_t n, int n_attr, cons
   return hipGetLastError();
 }
 
-hipError_t launch_intervals(const int32_t* attrs_phys, int64_t n, int c0, int c1, const int32_t* vstart,
-                            int64_t vmin, int64_t vcount, const DevPred* staged_preds,
-                            const int32_t* staged_order, int nq, DevPred* preds_out, int32_t* order_out,
-                            int64_t* iv, uint64_t* gthr, const int32_t* slots_src, int32_t* slots_dst,
-                            int64_t n_slots, hipStream_t s) {
-  intervals_kernel<<<dim3(2 * nq), dim3(64), 0, s>>>(attrs_phys, n, c0, c1, vstart, vmin, vcount, staged_preds,
-                                                     staged_order, nq, preds_out, order_out, iv, gthr, slots_src,
-                                                     slots_dst, n_slots);
+hipError_t launch_intervals(const IntervalArgs& a, hipStream_t s) {
+  if (a.nq <= 0 && a.n_slots <= 0) return hipSuccess;
+  intervals_kernel<<<dim3(2 * a.nq > 0 ? 2 * a.nq : 1), dim3(64), 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -22,14 +22,17 @@
 //
 // Optionally the launch also conditions the queries it encodes (the
 // condition kernel's work, the same bits): w_f = softplus(w_z) as w_z is
-// written, and alpha from extra workgroups after the encoder's, a wavefront
+// written, and alpha from side workgroups after the encoder's, a wavefront
 // per query (fingerprint, bank-row hashes, sum).  The fingerprint is a
 // sequential chain of several microseconds per query; on CUs of their own
 // these workgroups run beside the encoder's instead of lengthening them.
+// The same side workgroups can also find the batch's row intervals (the
+// interval kernel's work, a wavefront per bound).
 #include <cmath>
 
 #include "condition_device.h"
 #include "ifvs_internal.h"
+#include "intervals_device.h"
 
 namespace ifvs {
 
@@ -57,7 +60,10 @@ struct EncArgs {
   int nq;
   float* wz;               // [nq][D]
   EncCondition cond;       // the in-launch condition (cond.wf null: none)
-  int enc_blocks;          // workgroups of the encoder; those after them compute alpha
+  IntervalArgs iv;         // the in-launch intervals (iv.nq 0: none)
+  int enc_blocks;          // workgroups of the encoder; the side workgroups follow
+  int n_cond;              // side items: n_cond queries' alpha, then 2 iv.nq interval bounds
+  int n_side_waves;        // wavefronts of the side workgroups
 };
 
 // alpha of query qi (one wavefront), as the condition kernel computes it.
@@ -293,9 +299,15 @@ __global__ __launch_bounds__(kEncThreads) void encoder_kernel(const EncArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   if (static_cast<int>(blockIdx.x) >= a.enc_blocks) {
-    // a condition workgroup: no barrier below, the whole group leaves here
-    const int qi = (static_cast<int>(blockIdx.x) - a.enc_blocks) * kEncWaves + __builtin_amdgcn_readfirstlane(wave);
-    if (qi < a.nq) condition_alpha(a, qi, lane);
+    // a side workgroup: no barrier below, the whole group leaves here
+    const int item = (static_cast<int>(blockIdx.x) - a.enc_blocks) * kEncWaves + __builtin_amdgcn_readfirstlane(wave);
+    copy_slot_order(a.iv, item, a.n_side_waves, lane);
+    if (item < a.n_cond) {
+      condition_alpha(a, item, lane);
+    } else if (item - a.n_cond < 2 * a.iv.nq) {
+      const int j = item - a.n_cond;
+      interval_bound(a.iv, j >> 1, j & 1, lane);
+    }
     return;
   }
   const int q0 = blockIdx.x * kEncQ;
@@ -482,8 +494,9 @@ bool encoder_conditions(int h, bool has_bank) { return !has_bank || (h >= 1 && h
 
 hipError_t launch_encoder(const float* params, const double* off, const double* scale, int H, int heads, int layers,
                           int F, int D, int n_attr, const DevPred* preds, int nq, float* wz, hipStream_t s,
-                          const EncCondition* cond) {
+                          const EncCondition* cond, const IntervalArgs* iv) {
   if (nq <= 0) return hipSuccess;
+  if (iv && iv->nq != nq) return hipErrorInvalidValue;
   if (cond && (!cond->wf || !encoder_conditions(cond->h, cond->alpha != nullptr) ||
                (cond->alpha && (!cond->q || !cond->bank || cond->bank_rows <= 0))))
     return hipErrorInvalidValue;
@@ -501,13 +514,17 @@ hipError_t launch_encoder(const float* params, const double* off, const double* 
   a.nq = nq;
   a.wz = wz;
   if (cond) a.cond = *cond;
+  if (iv) a.iv = *iv;
   a.enc_blocks = (nq + kEncQ - 1) / kEncQ;
-  const int cond_blocks = cond && cond->alpha ? (nq + kEncWaves - 1) / kEncWaves : 0;
+  a.n_cond = cond && cond->alpha ? nq : 0;
+  const int side_items = a.n_cond + 2 * a.iv.nq;
+  const int side_blocks = (side_items + kEncWaves - 1) / kEncWaves;
+  a.n_side_waves = side_blocks * kEncWaves;
   const size_t lds = encoder_lds_bytes(H, F);
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&encoder_kernel),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(encoder_kernel, dim3(a.enc_blocks + cond_blocks), dim3(kEncThreads), lds, s, a);
+  hipLaunchKernelGGL(encoder_kernel, dim3(a.enc_blocks + side_blocks), dim3(kEncThreads), lds, s, a);
   return hipGetLastError();
 }
 
