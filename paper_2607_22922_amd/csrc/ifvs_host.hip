@@ -1006,7 +1006,11 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
     if (hipError_t e = hipHostGetDevicePointer(reinterpret_cast<void**>(&idx->staging_dev[i]), idx->staging[i], 0);
         e != hipSuccess)
       return bail(hip_fail(e, "mapping the staging slot"));
-    if (hipError_t e = hipEventCreateWithFlags(&idx->staged[i], hipEventDisableTiming); e != hipSuccess)
+    // (the event only tells the host that the kernels reading the slot have
+    // run: no timing, and no system-scope fence, which would write back and
+    // invalidate the caches at each record)
+    if (hipError_t e = hipEventCreateWithFlags(&idx->staged[i], hipEventDisableTiming | hipEventDisableSystemFence);
+        e != hipSuccess)
       return bail(hip_fail(e, "creating staging event"));
   }
   idx->stride64 = idx->n_tiles;
@@ -1078,8 +1082,8 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
       if (value != 0 && !idx->timers) {
         idx->timers = new StageTimer[kStages];
         for (int st = 0; st < kStages; ++st)
-          for (hipEvent_t& e : idx->timers[st].ev)
-            IFVS_HIP(hipEventCreate(&e), "creating profile events");
+          for (hipEvent_t& e : idx->timers[st].ev)   // timing only: no system-scope fence
+            IFVS_HIP(hipEventCreateWithFlags(&e, hipEventDisableSystemFence), "creating profile events");
       }
       if (value > 2) return fail(IFVS_E_INVALID, "IFVS_OPT_PROFILE takes 0, 1 or 2");
       idx->profile_mask = value == 0 ? 0 : (value == 1 ? (1 << kStages) - 1 : 1 << kStScan);
