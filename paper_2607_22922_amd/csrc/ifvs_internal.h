@@ -260,7 +260,7 @@ struct EncCondition {
   float* alpha = nullptr;        // [nq][mr], or null: w_f only
   float* wf = nullptr;           // [nq][D]
 };
-size_t encoder_lds_bytes(int H, int F);
+size_t encoder_lds_bytes(int H, int F, int layers);
 // Whether the encoder can condition in-launch: any index without a bank,
 // else h of at most 4.
 bool encoder_conditions(int h, bool has_bank);

@@ -45,8 +45,9 @@ constexpr int kEncThreads = 256;
 constexpr int kEncWaves = kEncThreads / 64;
 constexpr int kPad = 4;                        // LDS row padding (floats): spreads a 16 x 4 operand over the banks
 constexpr int kWbuf = 9216;                    // floats of the weight staging buffer: 8192 + padding (36 KB)
-constexpr int kEncMaxHeads = 16;
-constexpr int kEncVec = 9 * 128 + 256;          // a layer's gains and biases at the largest H and F
+
+// Floats of every layer's gains and biases and the final layer norm's.
+__host__ __device__ constexpr int vec_floats(int H, int F, int layers) { return layers * (9 * H + F) + 2 * H; }
 constexpr int kEncCondMaxH = 4;                // hash functions the in-launch condition handles
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
@@ -287,9 +288,8 @@ __global__ __launch_bounds__(kEncThreads) void encoder_kernel(const EncArgs a) {
   float* QKV = Z + kEncRows * ldh;                    // [16][ldq]
   float* Hd = QKV + kEncRows * ldq;                   // [16][ldf] feed-forward hidden
   float* Wb = Hd + kEncRows * ldf;                    // [kWbuf + 4] weight staging (+ a 16-byte sink)
-  float* Sc = Wb + kWbuf + 4;                         // [kEncQ][heads][8][8] attention scores
-  float* sv = Sc + kEncQ * kEncMaxHeads * kEncSlots * kEncSlots;   // [kEncVec] the layer's gains and biases
-  DevPred* sp = reinterpret_cast<DevPred*>(sv + kEncVec);   // [kEncQ]
+  float* sv = Wb + kWbuf + 4;                         // [layers * (9H + F) + 2H] gains and biases
+  DevPred* sp = reinterpret_cast<DevPred*>(sv + vec_floats(H, F, a.layers));   // [kEncQ]
   float* fa = reinterpret_cast<float*>(sp + kEncQ);   // [16] normalized lower bound of the row's clause
   float* fb = fa + kEncRows;                          // [16] normalized upper bound
   int* kind = reinterpret_cast<int*>(fb + kEncRows);  // [16] 0 padding, 1 summary, 2 clause
@@ -318,11 +318,38 @@ __global__ __launch_bounds__(kEncThreads) void encoder_kernel(const EncArgs a) {
   const float* layer0 = cls + H;
   const size_t layer_floats = static_cast<size_t>(2 * H) + 3 * H * H + 3 * H + H * H + H + 2 * H + H * F + F +
                               F * H + H;
-  // The first projection's weights are on their way while the predicates
-  // come from host memory.
+  // The first projection's weights are on their way, and every layer's gains
+  // and biases go to LDS, while the predicates come from host memory.  sv
+  // holds per layer ln1_g, ln1_b | bqkv | bo, ln2_g, ln2_b | b1 | b2, then
+  // lnf_g, lnf_b.
   Prefetch pf;
   prefetch(first_chunk(layer_ptrs(layer0, H, F).Wqkv, H, 3 * H), pf);
   if (wave < kEncQ && q0 + wave < a.nq) copy_pred(a.preds + q0 + wave, sp + wave, lane);
+  {
+    const int vs = 9 * H + F, n = vec_floats(H, F, a.layers);
+    const float* lnf = layer0 + a.layers * layer_floats;
+    for (int i0 = 0; i0 < n; i0 += 8 * kEncThreads) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int i = i0 + static_cast<int>(threadIdx.x) + u * kEncThreads;
+        const int l = i / vs, e = i - l * vs;
+        const LayerPtrs w = layer_ptrs(layer0 + l * layer_floats, H, F);
+        const float* src = l >= a.layers ? lnf + e
+                           : e < 2 * H   ? w.ln1_g + e
+                           : e < 5 * H   ? w.bqkv + (e - 2 * H)
+                           : e < 8 * H   ? w.bo + (e - 5 * H)
+                           : e < 8 * H + F ? w.b1 + (e - 8 * H)
+                                           : w.b2 + (e - 8 * H - F);
+        v[u] = i < n ? *src : 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int i = i0 + static_cast<int>(threadIdx.x) + u * kEncThreads;
+        if (i < n) sv[i] = v[u];
+      }
+    }
+  }
   __syncthreads();
 
   // Tokens: the summary token, then one per clause (bounds normalized in
@@ -375,71 +402,52 @@ __global__ __launch_bounds__(kEncThreads) void encoder_kernel(const EncArgs a) {
         layer + 1 < a.layers ? first_chunk(layer_ptrs(layer0 + (layer + 1) * layer_floats, H, F).Wqkv, H, 3 * H)
                              : none;
 
-    // The layer's gains and biases into LDS, one round of loads: sv holds
-    // ln1_g, ln1_b | bqkv | bo, ln2_g, ln2_b | b1 | b2.
-    {
-      const int n = 9 * H + F;
-      float v[6];
-#pragma unroll
-      for (int u = 0; u < 6; ++u) {
-        const int i = static_cast<int>(threadIdx.x) + u * kEncThreads;
-        const float* src = i < 2 * H ? w.ln1_g + i
-                           : i < 5 * H ? w.bqkv + (i - 2 * H)
-                           : i < 8 * H ? w.bo + (i - 5 * H)
-                           : i < 8 * H + F ? w.b1 + (i - 8 * H)
-                                           : w.b2 + (i - 8 * H - F);
-        v[u] = i < n ? *src : 0.0f;
-      }
-#pragma unroll
-      for (int u = 0; u < 6; ++u) {
-        const int i = static_cast<int>(threadIdx.x) + u * kEncThreads;
-        if (i < n) sv[i] = v[u];
-      }
-      __syncthreads();
-    }
-    const float* s_ln1_g = sv;
-    const float* s_ln1_b = sv + H;
-    const float* s_bqkv = sv + 2 * H;
-    const float* s_bo = sv + 5 * H;
-    const float* s_ln2_g = sv + 6 * H;
-    const float* s_ln2_b = sv + 7 * H;
-    const float* s_b1 = sv + 8 * H;
-    const float* s_b2 = sv + 8 * H + F;
+    const float* lv = sv + layer * (9 * H + F);
+    const float* s_ln1_g = lv;
+    const float* s_ln1_b = lv + H;
+    const float* s_bqkv = lv + 2 * H;
+    const float* s_bo = lv + 5 * H;
+    const float* s_ln2_g = lv + 6 * H;
+    const float* s_ln2_b = lv + 7 * H;
+    const float* s_b1 = lv + 8 * H;
+    const float* s_b2 = lv + 8 * H + F;
     layer_norm_rows(X, ldh, Z, ldh, s_ln1_g, s_ln1_b, H, kEncRows);
     gemm_rows(Z, ldh, first_chunk(w.Wqkv, H, 3 * H), s_bqkv, QKV, ldq, false, false, Wb, pf,
               first_chunk(w.Wo, H, H));
-    // Attention, in two passes over all threads.  Scores: one item per
-    // (predicate, head, query token i, key token j) of the predicate's
-    // tokens, into Sc.  Outputs: one item per (predicate, head, token i,
-    // dimension d) -- the softmax over the keys of row i, then the weighted
-    // sum of V -- into Z (head slices side by side); padding rows get zeros.
-    for (int t = threadIdx.x; t < kEncQ * a.heads * kEncSlots * kEncSlots; t += kEncThreads) {
-      const int j = t % kEncSlots, i = (t / kEncSlots) % kEncSlots;
-      const int hd = (t / (kEncSlots * kEncSlots)) % a.heads, qi = t / (kEncSlots * kEncSlots * a.heads);
-      const int S = seq[qi];
-      if (i >= S || j >= S) continue;
-      const float* qv = QKV + (qi * kEncSlots + i) * ldq + hd * dh;
-      const float* kv = QKV + (qi * kEncSlots + j) * ldq + H + hd * dh;
-      float acc = 0.0f;
-#pragma unroll 4
-      for (int d = 0; d < dh; ++d) acc += qv[d] * kv[d];
-      Sc[t] = acc * inv_sqrt_dh;
-    }
-    __syncthreads();
+    // Attention, one item per (predicate, head, token i, dimension d): the
+    // scores of row i against the predicate's tokens (the dh threads of a
+    // (row, head) compute them alike; their reads are broadcasts), the
+    // softmax over them, then the weighted sum of V, into Z (head slices side
+    // by side); padding rows get zeros.
     for (int t = threadIdx.x; t < kEncRows * H; t += kEncThreads) {
       const int d = t % dh, hd = (t / dh) % a.heads, r = t / H;   // r = qi * kEncSlots + i
       const int qi = r / kEncSlots, i = r % kEncSlots;
       const int S = seq[qi];
       float out = 0.0f;
       if (i < S) {
-        const float* sc = Sc + ((qi * a.heads + hd) * kEncSlots + i) * kEncSlots;
+        const float* qv = QKV + r * ldq + hd * dh;
+        float sc[kEncSlots];
         float mx = -INFINITY;
-        for (int j = 0; j < S; ++j) mx = fmaxf(mx, sc[j]);
+#pragma unroll
+        for (int j = 0; j < kEncSlots; ++j) {
+          sc[j] = -INFINITY;
+          if (j < S) {
+            const float* kv = QKV + (qi * kEncSlots + j) * ldq + H + hd * dh;
+            float acc = 0.0f;
+#pragma unroll 4
+            for (int e = 0; e < dh; ++e) acc += qv[e] * kv[e];
+            sc[j] = acc * inv_sqrt_dh;
+            mx = fmaxf(mx, sc[j]);
+          }
+        }
         float sum = 0.0f, acc = 0.0f;
-        for (int j = 0; j < S; ++j) {
-          const float e = expf(sc[j] - mx);
-          sum += e;
-          acc += e * QKV[(qi * kEncSlots + j) * ldq + 2 * H + hd * dh + d];
+#pragma unroll
+        for (int j = 0; j < kEncSlots; ++j) {
+          if (j < S) {
+            const float e = expf(sc[j] - mx);
+            sum += e;
+            acc += e * QKV[(qi * kEncSlots + j) * ldq + 2 * H + hd * dh + d];
+          }
         }
         out = acc / sum;
       }
@@ -460,9 +468,8 @@ __global__ __launch_bounds__(kEncThreads) void encoder_kernel(const EncArgs a) {
   const float* out_b = out_w + static_cast<size_t>(H) * a.D;
   // (row r of the normalization is predicate r's summary token: input row
   // stride kEncSlots rows)
-  for (int i = threadIdx.x; i < 2 * H; i += kEncThreads) sv[i] = lnf_g[i];   // lnf_g, lnf_b are adjacent
-  __syncthreads();
-  layer_norm_rows(X, kEncSlots * ldh, Z, ldh, sv, sv + H, H, kEncQ);
+  const float* s_lnf = sv + a.layers * (9 * H + F);
+  layer_norm_rows(X, kEncSlots * ldh, Z, ldh, s_lnf, s_lnf + H, H, kEncQ);
   __syncthreads();
   const int nv = min(kEncQ, a.nq - q0);
   for (int d = threadIdx.x; d < a.D; d += kEncThreads) {
@@ -483,9 +490,9 @@ __global__ __launch_bounds__(kEncThreads) void encoder_kernel(const EncArgs a) {
 
 }  // namespace
 
-size_t encoder_lds_bytes(int H, int F) {
+size_t encoder_lds_bytes(int H, int F, int layers) {
   const size_t floats = static_cast<size_t>(kEncRows) * (2 * (H + kPad) + (3 * H + kPad) + (F + kPad)) + kWbuf + 4 +
-                        kEncQ * kEncMaxHeads * kEncSlots * kEncSlots + kEncVec;
+                        vec_floats(H, F, layers);
   return floats * sizeof(float) + kEncQ * sizeof(DevPred) + kEncRows * 2 * sizeof(float) +
          (2 * kEncRows + kEncQ) * sizeof(int);
 }
@@ -520,7 +527,7 @@ hipError_t launch_encoder(const float* params, const double* off, const double* 
   const int side_items = a.n_cond + 2 * a.iv.nq;
   const int side_blocks = (side_items + kEncWaves - 1) / kEncWaves;
   a.n_side_waves = side_blocks * kEncWaves;
-  const size_t lds = encoder_lds_bytes(H, F);
+  const size_t lds = encoder_lds_bytes(H, F, layers);
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&encoder_kernel),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
   if (e != hipSuccess) return e;
