@@ -1283,7 +1283,8 @@ ifvs_status prepare_search(ifvs_index* idx, int32_t nq, const ifvs_predicate* pr
   // the interval kernel copies it to the device.
   const int32_t* qorder_host = reinterpret_cast<const int32_t*>(host + idx->max_batch);
   int32_t* order_host = reinterpret_cast<int32_t*>(host + idx->max_batch) + idx->max_batch;
-  p.n_order = plan.abs_cells && idx->opt_slot_order == 0
+  // (the list scan takes its work from its job table: no dispatch order)
+  p.n_order = plan.abs_cells && idx->opt_slot_order == 0 && !p.list_mode
                   ? static_cast<int64_t>(8) * ((((nq + plan.qtile - 1) / plan.qtile) + 7) / 8) * plan.splits
                   : 0;
   p.ordered = p.n_order > 0 && p.n_order <= ws.slot_order_cap;
