@@ -449,6 +449,11 @@ __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
   }
   return v;
 }
+__device__ __forceinline__ int wave_sum_i32(int v) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
@@ -524,7 +529,8 @@ __device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const floa
   extern __shared__ __align__(16) unsigned char smem[];
   const int C = a.C, S = a.n_sub;
   float* s_sdc = reinterpret_cast<float*>(smem);                          // [C]
-  unsigned char* scratch = smem + ((static_cast<size_t>(C) * 4 + 15) & ~size_t{15});
+  int32_t* s_off = reinterpret_cast<int32_t*>(s_sdc + C);                 // [C + 1] first list position of centroid c
+  unsigned char* scratch = smem + ((static_cast<size_t>(2 * C + 1) * 4 + 15) & ~size_t{15});
   LutT* s_lut = reinterpret_cast<LutT*>(scratch);                         // phase 1
   int32_t* s_cnt = reinterpret_cast<int32_t*>(scratch);                   // phase 2: [S] ranks, then items
   int32_t* s_hist = s_cnt + S;                                            // phase 2: [kPlanBuckets]
@@ -587,7 +593,10 @@ __device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const floa
   __syncthreads();
   {
     unsigned long long first = ~0ull;
-    for (int c = tid; c < C; c += 1024) {
+    for (int c = tid; c <= C; c += 1024) {
+      // (its list's first position too, for the seed: sub_off[C * kBands] ends the last list)
+      s_off[c] = a.sub_off[c * kBands];
+      if (c == C) break;
       uint32_t wd[kMW];
 #pragma unroll
       for (int w = 0; w < kMW; ++w) wd[w] = a.cc_t[static_cast<size_t>(w) * C + c];
@@ -606,7 +615,7 @@ __device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const floa
     // The seed (see above), from the nearest centroid's list.
     constexpr int kPer = kSeedRows / 1024;
     const int c0 = static_cast<int>(s_first & 0xFFFFFFFFu);
-    const int32_t p0 = a.sub_off[c0 * kBands], p1 = min(a.sub_off[c0 * kBands + kBands], p0 + kSeedRows);
+    const int32_t p0 = s_off[c0], p1 = min(s_off[c0 + 1], p0 + kSeedRows);
     int64_t row[kPer];
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
@@ -628,10 +637,12 @@ __device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const floa
     }
     // k-th smallest of the kSeedRows keys (all ones for rows not selected):
     // per pass the digit whose bin holds it among the keys with the digits
-    // found so far.
+    // found so far.  Three passes fix its top 24 bits; the seed is the top of
+    // that bin (at most 255 ulps above the k-th value, and still a bound:
+    // k selected rows lie at or below it; all ones stays all ones).
     uint32_t prefix = 0, pmask = 0;
     int kk = a.k;
-    for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int shift = 24; shift >= 8; shift -= 8) {
       if (tid < 256) s_rh[tid] = 0;
       __syncthreads();
 #pragma unroll
@@ -664,7 +675,7 @@ __device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const floa
       pmask |= 0xFFu << shift;
       kk = s_pick[1];
     }
-    seed_kth = prefix;
+    seed_kth = prefix | 0xFFu;
     if (tid == 0 && seed_kth != ~0u)
       atomicMin(reinterpret_cast<unsigned long long*>(a.gthr + q),
                 (static_cast<unsigned long long>(seed_kth) << 32) | 0xFFFFFFFFull);
@@ -692,6 +703,7 @@ __device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const floa
     }
   };
   int32_t r0[kSPer], r1[kSPer];
+  float rm[kSPer];   // each selected sub-list's largest radius
   {
     const int64_t bx0 = x0 >> a.f_shift, bx1 = x1 >> a.f_shift;
     int32_t c0[kSPer], c1[kSPer], so[kSPer];
@@ -768,6 +780,11 @@ __device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const floa
     }
     nearest = wave_min_u64(nearest);
     if ((tid & 63) == 0 && nearest != ~0ull) atomicMin(&s_near, nearest);
+#pragma unroll
+    for (int j = 0; j < kSPer; ++j) {   // (on their way across the barrier)
+      const int s = tid + j * 1024;
+      rm[j] = s < S && r1[j] > r0[j] ? a.rmax[s] : 0.0f;
+    }
     for (int b = tid; b < kPlanBuckets; b += 1024) {
       s_hist[b] = 0;
       s_bmin[b] = ~0u;
@@ -785,7 +802,7 @@ __device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const floa
       lb[j] = 0.0f;
       if (s < S && r1[j] > r0[j]) {
         ++mine;
-        lb[j] = __fsub_rn(s_sdc[s / kBands], __fmul_rn(__fadd_rn(a.rmax[s], delta), sw));
+        lb[j] = __fsub_rn(s_sdc[s / kBands], __fmul_rn(__fadd_rn(rm[j], delta), sw));
         if (lb[j] > 0.0f && s / kBands != near) {
           lo_b = min(lo_b, ordered_bits(lb[j]));
           hi_b = max(hi_b, ordered_bits(lb[j]));
@@ -798,7 +815,8 @@ __device__ __forceinline__ void plan_one_query(const ListPlanArgs& a, const floa
       atomicMin(&s_lo, lo_b);
       atomicMax(&s_hi, hi_b);
     }
-    if (mine) atomicAdd(&s_count, mine);
+    mine = wave_sum_i32(mine);
+    if ((tid & 63) == 0 && mine) atomicAdd(&s_count, mine);
   }
   __syncthreads();
   // positive bounds: buckets of 2^shift order-preserving codes from the
@@ -1021,7 +1039,7 @@ hipError_t launch_lut_bounds(const float* alpha, const float* wf, const float* c
 size_t list_plan_lds_bytes(int m, int lut_dtype, int C) {
   const size_t lut = static_cast<size_t>(m) * kKsub * (lut_dtype == 1 ? 2 : 4);
   const size_t items = static_cast<size_t>(C) * kBands * 4 + static_cast<size_t>(kPlanBuckets) * 8;
-  return ((static_cast<size_t>(C) * 4 + 15) & ~size_t{15}) + std::max(lut, items);
+  return ((static_cast<size_t>(2 * C + 1) * 4 + 15) & ~size_t{15}) + std::max(lut, items);
 }
 
 size_t list_jobs_lds_bytes(int nq) {
