@@ -110,6 +110,35 @@ def test_condition_in_the_encoder_launch(B, h, bank_rows):
         assert torch.equal(_bits(a) if a.is_floating_point() else a, _bits(b) if b.is_floating_point() else b), name
 
 
+def test_chunk_grid_dispatch_order_from_the_encoder_launch(B):
+    """An interval-scan batch wide enough for the chunk grid (>= 8192 tiles):
+    the scan's dispatch order is copied to the device by the encoder's side
+    workgroups under ifvs_query_batch, by the interval kernel otherwise; the
+    results are the separate calls' bits either way."""
+    say("[query_batch] chunk grid, N=600000")
+    M, dsub = 16, 2
+    ix = random_index(600_000, M, dsub, 1, 1000, seed=23, device="cuda", bank_rows=45)
+    idx = B.Index(ix["codes"], ix["C_pq"], ix["attrs"], ix["bank"], ix["W"], ix["r"], ix["h"], ix["hash_seed"],
+                  max_batch=16, max_k=10, cluster_cols=(0,))
+    idx.load_encoder(random_encoder(1, M * dsub, [1000], seed=6, layers=1))
+    g = torch.Generator(device="cpu").manual_seed(11)
+    q = torch.randn(12, M * dsub, generator=g).cuda()
+    preds = [[(0, 5 * i, 1000)] for i in range(12)]              # 94-100% of the rows each
+    got = idx.query_batch(q, preds, 10)
+    plan = idx.last_plan()
+    ref = _stagewise(idx, q, preds, 10, None, 0)
+    torch.cuda.synchronize()
+    assert plan["grid_tiles"] > 0, plan                          # the chunk grid ran
+    assert not idx.last_coarse()
+    for name, a, b in zip(("ids", "dist", "w_z", "alpha", "w_f", "lut"), got, ref):
+        assert torch.equal(_bits(a) if a.is_floating_point() else a, _bits(b) if b.is_floating_point() else b), name
+    idx.set_option(B.OPT_SLOT_ORDER, 1)                          # the plain order: no copy at all
+    ids2, dist2, *_ = idx.query_batch(q, preds, 10)
+    idx.set_option(B.OPT_SLOT_ORDER, 0)
+    torch.cuda.synchronize()
+    assert torch.equal(ids2, ref[0]) and torch.equal(_bits(dist2), _bits(ref[1]))
+
+
 def test_rows_against_the_oracle(B, case):
     ix, idx, q, preds = case
     say("[query_batch] oracle rows")
