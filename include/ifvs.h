@@ -526,7 +526,8 @@ ifvs_status ifvs_encode_predicates(ifvs_index* idx, int32_t nq, const ifvs_predi
 #define IFVS_OPT_QTILE  1
 #define IFVS_OPT_SPLITS 2
 #define IFVS_OPT_PROFILE 3        /* 1: time every kernel launch with HIP events (see below);
-                                     2: time only the scan kernel's launches              */
+                                     2: time only the scan kernels' launches;
+                                     3: time only the list scan's launches (coarse bound) */
 #define IFVS_OPT_MIN_CHUNK 4      /* fewest 64-row code tiles per chunk (0 = automatic)      */
 #define IFVS_OPT_GRID_TILES 5     /* chunk grid cell in 64-row tiles (0 = automatic)         */
 #define IFVS_OPT_GRID_RELATIVE 7  /* 1: chunk c of a query tile is cell (its first cell) + c

@@ -70,6 +70,9 @@ constexpr float kBandQuantiles[kBands - 1] = {0.5f, 0.85f, 0.97f};
 
 // Optional per-stage kernel timing with HIP events (IFVS_OPT_PROFILE).
 enum Stage { kStCondition = 0, kStLut, kStFilter, kStScan, kStMerge, kStEncode, kStCoarse, kStages };
+// The list scan's launches: reported under kStScan, selectable on their own
+// (IFVS_OPT_PROFILE 3) by this bit of the profile mask.
+constexpr int kStListScan = kStages;
 constexpr int kProfilePairs = 4096;
 
 struct StageTimer {
@@ -688,7 +691,7 @@ ifvs_status flush_timer(StageTimer& t) {
 // Launch through `fn`, bracketed by events when profiling.
 template <typename Fn>
 ifvs_status timed(ifvs_index* idx, int stage, hipStream_t s, const char* what, Fn&& fn) {
-  StageTimer* t = (idx->profile_mask >> stage) & 1 ? &idx->timers[stage] : nullptr;
+  StageTimer* t = (idx->profile_mask >> stage) & 1 ? &idx->timers[stage == kStListScan ? kStScan : stage] : nullptr;
   if (t) {
     if (t->used + 2 > 2 * kProfilePairs)
       if (ifvs_status st = flush_timer(*t); st != IFVS_OK) return st;
@@ -1085,8 +1088,11 @@ ifvs_status ifvs_set_option(ifvs_index* idx, int32_t option, int64_t value) {
           for (hipEvent_t& e : idx->timers[st].ev)   // timing only: no system-scope fence
             IFVS_HIP(hipEventCreateWithFlags(&e, hipEventDisableSystemFence), "creating profile events");
       }
-      if (value > 2) return fail(IFVS_E_INVALID, "IFVS_OPT_PROFILE takes 0, 1 or 2");
-      idx->profile_mask = value == 0 ? 0 : (value == 1 ? (1 << kStages) - 1 : 1 << kStScan);
+      if (value > 3) return fail(IFVS_E_INVALID, "IFVS_OPT_PROFILE takes 0, 1, 2 or 3");
+      idx->profile_mask = value == 0   ? 0
+                          : value == 1 ? (1 << (kStListScan + 1)) - 1
+                          : value == 2 ? (1 << kStScan) | (1 << kStListScan)
+                                       : 1 << kStListScan;
       return IFVS_OK;
     default: return fail(IFVS_E_INVALID, "unknown option " + std::to_string(option));
   }
@@ -1409,7 +1415,7 @@ ifvs_status run_search(ifvs_index* idx, int32_t nq, const void* lut, int32_t lut
     sa.slots = cl.slots;
     sa.lookup_hist = idx->opt_count_reads ? idx->read_hist : nullptr;
     sa.union_bound = idx->opt_shared_bound == 1 ? 0 : 1;
-    IFVS_LAUNCH(idx, kStScan, s, "launching list scan kernel", launch_list_scan(sa, lut_dtype, s));
+    IFVS_LAUNCH(idx, kStListScan, s, "launching list scan kernel", launch_list_scan(sa, lut_dtype, s));
     IFVS_LAUNCH(idx, kStMerge, s, "launching top-k merge kernel",
                 launch_topk_merge(ws.partials, nq, static_cast<int64_t>(list_jobs) * kScanWaves * k, k, ws.iv, 0,
                                   static_cast<int64_t>(kScanWaves) * k, ws.qorder, ids_out, dist_out, s,

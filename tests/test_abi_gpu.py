@@ -91,7 +91,7 @@ def test_other_calls_validate(B, small):
     assert st == B.E_INVALID
     st, _ = _status(B, lib.ifvs_set_option, idx.handle, B.OPT_QTILE, -1)
     assert st == B.E_INVALID
-    for opt, bad in ((B.OPT_PROFILE, 3), (B.OPT_GATHER, 3), (B.OPT_GRID_TILES, -5), (B.OPT_SLOT_ORDER, 2),
+    for opt, bad in ((B.OPT_PROFILE, 4), (B.OPT_GATHER, 3), (B.OPT_GRID_TILES, -5), (B.OPT_SLOT_ORDER, 2),
                      (B.OPT_GRID_RELATIVE, 2), (B.OPT_SHARED_BOUND, 3)):
         st, msg = _status(B, lib.ifvs_set_option, idx.handle, opt, bad)
         assert st == B.E_INVALID, (opt, bad, msg)
@@ -107,10 +107,11 @@ def test_other_calls_validate(B, small):
 
 
 def test_profile_modes(B, small):
-    """IFVS_OPT_PROFILE 1 times every kernel launch, 2 only the scan's."""
+    """IFVS_OPT_PROFILE 1 times every kernel launch, 2 only the scans', 3
+    only the list scan's (none here: no coarse build)."""
     idx, q, lut = small
     preds = [[(0, 0, 10)]] * 4
-    for mode, timed in ((1, {"condition", "lut", "filter", "scan", "merge"}), (2, {"scan"})):
+    for mode, timed in ((1, {"condition", "lut", "filter", "scan", "merge"}), (2, {"scan"}), (3, set())):
         idx.set_option(B.OPT_PROFILE, mode)
         idx.read_profile()
         a, f = idx.select_codebook(q, preds, None)

@@ -139,6 +139,21 @@ def test_chunk_grid_dispatch_order_from_the_encoder_launch(B):
     assert torch.equal(ids2, ref[0]) and torch.equal(_bits(dist2), _bits(ref[1]))
 
 
+def test_profile_mode_three_times_the_list_scan_only(B, case):
+    ix, idx, q, preds = case
+    p = [c[:1] for c in preds]
+    for coarse, launches in ((2, 1), (1, 0)):           # list scan forced, then off
+        idx.set_option(B.OPT_COARSE, coarse)
+        idx.set_option(B.OPT_PROFILE, 3)
+        idx.read_profile()
+        idx.query_batch(q, p, 10)
+        prof = idx.read_profile()
+        idx.set_option(B.OPT_PROFILE, 0)
+        idx.set_option(B.OPT_COARSE, 0)
+        assert prof["scan"][1] == launches, (coarse, prof)
+        assert all(n == 0 for st, (_, n) in prof.items() if st != "scan"), prof
+
+
 def test_rows_against_the_oracle(B, case):
     ix, idx, q, preds = case
     say("[query_batch] oracle rows")
