@@ -10,6 +10,7 @@
 #include "ifvs_internal.h"
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -17,6 +18,7 @@
 #include <limits>
 #include <mutex>
 #include <numeric>
+#include <thread>
 #include <string>
 #include <vector>
 
@@ -204,6 +206,13 @@ struct ifvs_index {
   DevPred* staging_dev[kStagingSlots] = {};  // the same slots as the device addresses them
   hipEvent_t staged[kStagingSlots] = {};
   bool slot_busy[kStagingSlots] = {};
+  // A slot released through a done word (StageDone) instead of its event:
+  // the slot is free once done_host[slot] == slot_seq[slot].
+  bool slot_by_word[kStagingSlots] = {};
+  uint64_t slot_seq[kStagingSlots] = {};
+  uint64_t* done_host = nullptr;   // pinned [kStagingSlots]
+  uint64_t* done_dev = nullptr;    // the same words as the device addresses them
+  uint64_t release_seq = 0;
   int next_slot = 0;
 
   uint64_t* bitmap = nullptr;    // [max_batch][stride64]
@@ -333,6 +342,7 @@ struct ifvs_index {
       if (staging[i]) hipHostFree(staging[i]);
       if (staged[i]) hipEventDestroy(staged[i]);
     }
+    if (done_host) hipHostFree(done_host);
   }
 };
 
@@ -628,6 +638,25 @@ void order_scan_slots(const ifvs_index* idx, const DevPred* host, const int32_t*
   }
 }
 
+// Wait until the kernel carrying slot's StageDone has started (its word
+// holds the slot's sequence number).  The word is written from the device
+// over the host link; after about a second of polling the device is
+// synchronized once, after which it must hold the number.
+ifvs_status wait_done_word(ifvs_index* idx, int slot) {
+  const uint64_t want = idx->slot_seq[slot];
+  const auto t0 = std::chrono::steady_clock::now();
+  while (__atomic_load_n(&idx->done_host[slot], __ATOMIC_ACQUIRE) != want) {
+    if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(1)) {
+      IFVS_HIP(hipDeviceSynchronize(), "waiting for staging slot");
+      if (__atomic_load_n(&idx->done_host[slot], __ATOMIC_ACQUIRE) != want)
+        return fail(IFVS_E_HIP, "staging slot " + std::to_string(slot) + ": its done word was not written");
+      break;
+    }
+    std::this_thread::yield();
+  }
+  return IFVS_OK;
+}
+
 // Validate and normalize predicates into the next pinned staging slot (and
 // the scan's query order, when asked).  With copy_to_device the slot is
 // copied to the device workspace and released at once; otherwise the
@@ -637,8 +666,13 @@ ifvs_status stage_predicates(ifvs_index* idx, int32_t nq, const ifvs_predicate* 
                              bool with_order, bool copy_to_device, hipStream_t s, int* slot_out,
                              DevPred** host_out = nullptr) {
   const int slot = idx->next_slot;
-  if (idx->slot_busy[slot]) IFVS_HIP(hipEventSynchronize(idx->staged[slot]), "waiting for staging slot");
+  if (idx->slot_busy[slot] && idx->slot_by_word[slot]) {
+    if (ifvs_status st = wait_done_word(idx, slot); st != IFVS_OK) return st;
+  } else if (idx->slot_busy[slot]) {
+    IFVS_HIP(hipEventSynchronize(idx->staged[slot]), "waiting for staging slot");
+  }
   idx->slot_busy[slot] = false;
+  idx->slot_by_word[slot] = false;
   DevPred* host = idx->staging[slot];
   const ifvs_status st = normalize_predicates(idx, nq, preds, host);
   if (st != IFVS_OK) return st;
@@ -665,6 +699,18 @@ ifvs_status stage_predicates(ifvs_index* idx, int32_t nq, const ifvs_predicate* 
   *slot_out = slot;
   if (host_out) *host_out = host;
   return IFVS_OK;
+}
+
+// A slot released through its done word: the word is set by the kernel that
+// carries the StageDone, which starts only after the slot's readers ran.
+StageDone slot_done_word(ifvs_index* idx, int slot) {
+  idx->slot_seq[slot] = ++idx->release_seq;
+  return StageDone{idx->done_dev + slot, idx->slot_seq[slot]};
+}
+
+void release_slot_by_word(ifvs_index* idx, int slot) {
+  idx->slot_busy[slot] = true;
+  idx->slot_by_word[slot] = true;
 }
 
 // The slot's readers are enqueued on s: it may be reused once they ran.
@@ -1016,6 +1062,18 @@ ifvs_status ifvs_load_index(const ifvs_index_desc* desc, ifvs_index** out) {
         e != hipSuccess)
       return bail(hip_fail(e, "creating staging event"));
   }
+  if (forced_alloc_failure() ||
+      // (coherent: the device's store reaches host memory without a cache flush)
+      hipHostMalloc(reinterpret_cast<void**>(&idx->done_host), sizeof(uint64_t) * kStagingSlots,
+                    hipHostMallocCoherent) != hipSuccess) {
+    idx->done_host = nullptr;
+    (void)hipGetLastError();
+    return bail(fail(IFVS_E_NOMEM, "pinned staging allocation failed"));
+  }
+  std::fill(idx->done_host, idx->done_host + kStagingSlots, uint64_t{0});
+  if (hipError_t e = hipHostGetDevicePointer(reinterpret_cast<void**>(&idx->done_dev), idx->done_host, 0);
+      e != hipSuccess)
+    return bail(hip_fail(e, "mapping the staging done words"));
   idx->stride64 = idx->n_tiles;
   if ((st = dev_alloc(&idx->bitmap, static_cast<size_t>(d.max_batch) * idx->stride64, "selection bitmaps")) != IFVS_OK)
     return bail(st);
@@ -1324,10 +1382,12 @@ IntervalArgs search_intervals(const ifvs_index* idx, int32_t nq, const SearchPre
 
 // The device side of a prepared search (intervals_done: the caller already
 // enqueued search_intervals' work; parts_ready: the table kernel wrote the
-// coarse bound's factors).
+// coarse bound's factors; slot_released: the caller released the staging
+// slot, whose readers all ran before this search's kernels).
 ifvs_status run_search(ifvs_index* idx, int32_t nq, const void* lut, int32_t lut_dtype, const float* alpha,
                        const float* wf, int32_t k, int32_t* ids_out, float* dist_out, uint32_t* bitmap_out,
-                       hipStream_t s, const SearchPrep& p, bool intervals_done, bool parts_ready) {
+                       hipStream_t s, const SearchPrep& p, bool intervals_done, bool parts_ready,
+                       bool slot_released = false) {
   if (p.empty) return IFVS_OK;
   const SearchWs& ws = p.ws;
   const ScanPlan& plan = p.plan;
@@ -1337,7 +1397,8 @@ ifvs_status run_search(ifvs_index* idx, int32_t nq, const void* lut, int32_t lut
   const CoarseLists& cl = idx->coarse;
   if (!intervals_done)
     IFVS_LAUNCH(idx, kStFilter, s, "launching interval kernel", launch_intervals(search_intervals(idx, nq, p), s));
-  if (ifvs_status st = release_slot(idx, p.slot, s); st != IFVS_OK) return st;
+  if (!slot_released)
+    if (ifvs_status st = release_slot(idx, p.slot, s); st != IFVS_OK) return st;
   if (p.list_mode) {
     // (the table kernel wrote the bound's factors when the caller says so)
     if (!parts_ready)
@@ -1627,15 +1688,20 @@ ifvs_status ifvs_query_batch(ifvs_index* idx, int32_t nq, const float* q, const 
         st != IFVS_OK)
       return st;
   }
+  // When the encoder ran, every reader of the staging slot (the encoder's
+  // launch with the intervals, the condition kernel) runs before the table
+  // kernel, which then releases the slot through its done word.
+  const StageDone done = !w_z ? slot_done_word(idx, slot) : StageDone{};
   if (ifvs_status st = launch(kStLut, "launching LUT kernel", [&]() -> hipError_t {
         return launch_build_lut(q, idx->dim, idx->m, idx->dsub, idx->r, idx->cpq, idx->W, alpha, wf_out, nq,
-                                lut_dtype, lut_out, s, parts);
+                                lut_dtype, lut_out, s, parts, done);
       });
       st != IFVS_OK)
     return st;
+  if (!w_z) release_slot_by_word(idx, slot);
   // (the encoder's launch computed the intervals when it ran)
   const ifvs_status st = run_search(idx, nq, lut_out, lut_dtype, alpha, wf_out, k, ids_out, dist_out, nullptr, s,
-                                    prep, !w_z, parts != nullptr);
+                                    prep, !w_z, parts != nullptr, !w_z);
   if (st != IFVS_OK && !idx->slot_busy[slot]) (void)release_slot(idx, slot, s);   // the earlier kernels read it
   return st;
 }

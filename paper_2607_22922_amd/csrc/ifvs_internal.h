@@ -159,13 +159,27 @@ hipError_t launch_train_update_bank(float* bank, int mr, const int32_t* rows, in
 // inv[perm[r]] = r.
 hipError_t launch_invert_perm(const int32_t* perm, int64_t n, int32_t* inv, hipStream_t s);
 
+// A word in pinned host memory that a kernel sets to `seq` as it starts: the
+// kernels enqueued before it on the stream have all run (the host waits on
+// the word instead of an event, whose record costs the stream a few
+// microseconds).  flag null: nothing to signal.
+struct StageDone {
+  uint64_t* flag = nullptr;
+  uint64_t seq = 0;
+};
+__device__ __forceinline__ void signal_stage_done(const StageDone& d) {
+  if (d.flag && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
+    __hip_atomic_store(d.flag, d.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 // parts: optional [nq][2][m] coarse-bound factors (launch_bound_parts's
 // output, the same bits), written by the table kernel itself when
 // lut_emits_bound_parts holds for the shape (hipErrorInvalidValue otherwise).
+// done: signalled as the table kernel starts.
 hipError_t launch_build_lut(const float* q, int dim, int m, int dsub, int r,
                             const float* cpq, const float* W, const float* alpha,
                             const float* wf, int nq, int lut_dtype, void* lut_out,
-                            hipStream_t s, float* parts = nullptr);
+                            hipStream_t s, float* parts = nullptr, StageDone done = {});
 bool lut_emits_bound_parts(int dsub, int r, bool has_alpha);
 
 struct ScanPlan {

@@ -48,9 +48,10 @@ template <int DSUB, int R, typename OutT, bool kParts = false>
 __global__ __launch_bounds__(256) void lut_fixed_kernel(
     const float* __restrict__ q, int dim, int M, const float* __restrict__ cpq,
     const float* __restrict__ W, const float* __restrict__ alpha, const float* __restrict__ wf,
-    int nq, OutT* __restrict__ out, float* __restrict__ parts) {
+    int nq, OutT* __restrict__ out, float* __restrict__ parts, StageDone done) {
   const int m = blockIdx.x;
   const int c = threadIdx.x;
+  signal_stage_done(done);
   float creg[DSUB];
 #pragma unroll
   for (int j = 0; j < DSUB; ++j) creg[j] = cpq[(static_cast<int64_t>(m) * kKsub + c) * DSUB + j];
@@ -132,9 +133,10 @@ template <typename OutT>
 __global__ __launch_bounds__(256) void lut_generic_kernel(
     const float* __restrict__ q, int dim, int M, int dsub, int r, const float* __restrict__ cpq,
     const float* __restrict__ W, const float* __restrict__ alpha, const float* __restrict__ wf,
-    int nq, OutT* __restrict__ out) {
+    int nq, OutT* __restrict__ out, StageDone done) {
   const int m = blockIdx.x;
   const int c = threadIdx.x;
+  signal_stage_done(done);
   const int q_begin = blockIdx.y * kQueriesPerBlock;
   const int q_end = min(nq, q_begin + kQueriesPerBlock);
   for (int qi = q_begin; qi < q_end; ++qi) {
@@ -160,23 +162,23 @@ __global__ __launch_bounds__(256) void lut_generic_kernel(
 
 template <int DSUB, int R, typename OutT>
 void launch_fixed(dim3 g, hipStream_t s, const float* q, int dim, int M, const float* cpq, const float* W,
-                  const float* alpha, const float* wf, int nq, OutT* out, float* parts) {
+                  const float* alpha, const float* wf, int nq, OutT* out, float* parts, StageDone done) {
   if (parts)
-    lut_fixed_kernel<DSUB, R, OutT, true><<<g, dim3(256), 0, s>>>(q, dim, M, cpq, W, alpha, wf, nq, out, parts);
+    lut_fixed_kernel<DSUB, R, OutT, true><<<g, dim3(256), 0, s>>>(q, dim, M, cpq, W, alpha, wf, nq, out, parts, done);
   else
-    lut_fixed_kernel<DSUB, R, OutT><<<g, dim3(256), 0, s>>>(q, dim, M, cpq, W, alpha, wf, nq, out, nullptr);
+    lut_fixed_kernel<DSUB, R, OutT><<<g, dim3(256), 0, s>>>(q, dim, M, cpq, W, alpha, wf, nq, out, nullptr, done);
 }
 
 template <int DSUB, typename OutT>
 bool launch_fixed_r(int r, bool has_alpha, dim3 g, hipStream_t s, const float* q, int dim, int M,
                     const float* cpq, const float* W, const float* alpha, const float* wf, int nq,
-                    OutT* out, float* parts) {
+                    OutT* out, float* parts, StageDone done) {
   if (!has_alpha) {
-    launch_fixed<DSUB, 0, OutT>(g, s, q, dim, M, cpq, W, nullptr, wf, nq, out, parts);
+    launch_fixed<DSUB, 0, OutT>(g, s, q, dim, M, cpq, W, nullptr, wf, nq, out, parts, done);
     return true;
   }
   if (r == 8) {
-    launch_fixed<DSUB, 8, OutT>(g, s, q, dim, M, cpq, W, alpha, wf, nq, out, parts);
+    launch_fixed<DSUB, 8, OutT>(g, s, q, dim, M, cpq, W, alpha, wf, nq, out, parts, done);
     return true;
   }
   return false;
@@ -185,18 +187,18 @@ bool launch_fixed_r(int r, bool has_alpha, dim3 g, hipStream_t s, const float* q
 template <typename OutT>
 void launch_typed(const float* q, int dim, int M, int dsub, int r, const float* cpq,
                   const float* W, const float* alpha, const float* wf, int nq, OutT* out,
-                  hipStream_t s, float* parts) {
+                  hipStream_t s, float* parts, StageDone done) {
   const dim3 g(M, (nq + kQueriesPerBlock - 1) / kQueriesPerBlock);
   const bool has_alpha = alpha != nullptr;
-  bool done = false;
+  bool launched = false;
   switch (dsub) {
-    case 2: done = launch_fixed_r<2>(r, has_alpha, g, s, q, dim, M, cpq, W, alpha, wf, nq, out, parts); break;
-    case 4: done = launch_fixed_r<4>(r, has_alpha, g, s, q, dim, M, cpq, W, alpha, wf, nq, out, parts); break;
-    case 8: done = launch_fixed_r<8>(r, has_alpha, g, s, q, dim, M, cpq, W, alpha, wf, nq, out, parts); break;
+    case 2: launched = launch_fixed_r<2>(r, has_alpha, g, s, q, dim, M, cpq, W, alpha, wf, nq, out, parts, done); break;
+    case 4: launched = launch_fixed_r<4>(r, has_alpha, g, s, q, dim, M, cpq, W, alpha, wf, nq, out, parts, done); break;
+    case 8: launched = launch_fixed_r<8>(r, has_alpha, g, s, q, dim, M, cpq, W, alpha, wf, nq, out, parts, done); break;
     default: break;
   }
-  if (!done)
-    lut_generic_kernel<OutT><<<g, dim3(256), 0, s>>>(q, dim, M, dsub, r, cpq, W, alpha, wf, nq, out);
+  if (!launched)
+    lut_generic_kernel<OutT><<<g, dim3(256), 0, s>>>(q, dim, M, dsub, r, cpq, W, alpha, wf, nq, out, done);
 }
 
 }  // namespace
@@ -207,12 +209,12 @@ bool lut_emits_bound_parts(int dsub, int r, bool has_alpha) {
 
 hipError_t launch_build_lut(const float* q, int dim, int m, int dsub, int r, const float* cpq,
                             const float* W, const float* alpha, const float* wf, int nq,
-                            int lut_dtype, void* lut_out, hipStream_t s, float* parts) {
+                            int lut_dtype, void* lut_out, hipStream_t s, float* parts, StageDone done) {
   if (parts && !lut_emits_bound_parts(dsub, r, alpha != nullptr)) return hipErrorInvalidValue;
   if (lut_dtype == 1)
-    launch_typed(q, dim, m, dsub, r, cpq, W, alpha, wf, nq, static_cast<__half*>(lut_out), s, parts);
+    launch_typed(q, dim, m, dsub, r, cpq, W, alpha, wf, nq, static_cast<__half*>(lut_out), s, parts, done);
   else
-    launch_typed(q, dim, m, dsub, r, cpq, W, alpha, wf, nq, static_cast<float*>(lut_out), s, parts);
+    launch_typed(q, dim, m, dsub, r, cpq, W, alpha, wf, nq, static_cast<float*>(lut_out), s, parts, done);
   return hipGetLastError();
 }
 
