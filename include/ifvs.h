@@ -326,8 +326,9 @@ ifvs_status ifvs_filtered_search_bounded(ifvs_index* idx, int32_t nq, const ifvs
  * call stages them and marks its staging with an event, a few microseconds
  * of the stream's time each); when the encoder runs, its launch also
  * conditions the queries (indexes without a bank, or h of at most 4) and
- * finds their row intervals; and when the list scan runs, the table kernel
- * also writes the coarse bound's factors.
+ * finds their row intervals, and the table kernel then releases the
+ * staging slot through a pinned word instead of an event; and when the list
+ * scan runs, the table kernel also writes the coarse bound's factors.
  *  q: device [nq][dim];  preds: HOST [nq]
  *  w_z: device [nq][dim], or NULL to encode the predicates with the attached
  *       encoder into wz_out (device [nq][dim], caller-owned; unused when w_z
